@@ -1,0 +1,237 @@
+"""Test-only float64 PyTorch (CPU) interpreter of a network description.
+
+Used to pin the oracle: a second, independent implementation of the same
+network built from library routines (torch.nn.functional + autograd +
+torch.optim.SGD), and the register/cycle simulator of the paper's pipeline
+(Sec. 3) with ONE weight copy per partition.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+import torch.nn.functional as F
+
+from paper_1912_12675_amd.synth import BN, CONV, F_BIAS, F_RELU, FC, GAVG, MAXPOOL
+
+torch.set_default_dtype(torch.float64)
+
+
+def op_param_slices(ops, stage_end):
+    """Per op: (stage, [(name, offset, shape)]) in the flat per-stage layout."""
+    stage_of = np.zeros(len(ops), dtype=int)
+    prev = 0
+    for s, e in enumerate(stage_end):
+        stage_of[prev:e] = s
+        prev = e
+    off = [0] * len(stage_end)
+    out = []
+    for i, o in enumerate(ops):
+        kind, _, _, cin, cout, k, _, _, flags = (int(v) for v in o)
+        s = int(stage_of[i])
+        items = []
+        if kind == CONV:
+            items.append(("weight", (cout, cin, k, k)))
+            if flags & F_BIAS:
+                items.append(("bias", (cout,)))
+        elif kind == BN:
+            items += [("gamma", (cin,)), ("beta", (cin,))]
+        elif kind == FC:
+            items.append(("weight", (cout, cin)))
+            if flags & F_BIAS:
+                items.append(("bias", (cout,)))
+        lst = []
+        for name, shape in items:
+            lst.append((name, off[s], shape))
+            off[s] += int(np.prod(shape))
+        out.append((s, lst))
+    return out, off
+
+
+def _shortcut(res, c_out, h_out):
+    c_in, h_in = res.shape[1], res.shape[2]
+    if c_in == c_out and h_in == h_out:
+        return res
+    step = h_in // h_out
+    lo = (c_out - c_in) // 2
+    return F.pad(res[:, :, ::step, ::step], (0, 0, 0, 0, lo, c_out - c_in - lo))
+
+
+def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5, bn_mom=0.1):
+    """Apply ops[lo:hi].  inputs: dict tensor_id -> tensor (must hold every
+    tensor that ops[lo:hi] read from outside the range).  stage_params: list
+    of flat per-stage torch tensors.  Returns the dict extended with the
+    tensors written."""
+    t = dict(inputs)
+    for i in range(lo, hi):
+        kind, in0, in1, cin, cout, k, stride, pad, flags = (int(v) for v in ops[i])
+        s, lst = slices[i]
+        P = {name: stage_params[s][off:off + int(np.prod(shape))].view(shape) for name, off, shape in lst}
+        a = t[in0]
+        if kind == CONV:
+            y = F.conv2d(a, P["weight"], P.get("bias"), stride=stride, padding=pad)
+            if flags & F_RELU:
+                y = F.relu(y)
+        elif kind == BN:
+            rm = rv = None
+            if running is not None:
+                rm, rv = running[i]
+            y = F.batch_norm(a, rm, rv, P["gamma"], P["beta"], training=True, momentum=bn_mom, eps=bn_eps)
+            if in1 >= 0:
+                y = y + _shortcut(t[in1], y.shape[1], y.shape[2])
+            if flags & F_RELU:
+                y = F.relu(y)
+        elif kind == MAXPOOL:
+            y = F.max_pool2d(a, k, stride)
+        elif kind == GAVG:
+            y = a.mean(dim=(2, 3), keepdim=True)
+        elif kind == FC:
+            y = F.linear(a.reshape(a.shape[0], -1), P["weight"], P.get("bias"))
+            if flags & F_RELU:
+                y = F.relu(y)
+            y = y.reshape(y.shape[0], -1, 1, 1)
+        else:
+            raise ValueError(kind)
+        t[i + 1] = y
+    return t
+
+
+def running_stats(ops):
+    return {i: (torch.zeros(int(o[3])), torch.ones(int(o[3]))) for i, o in enumerate(ops) if int(o[0]) == BN}
+
+
+def split_flat(flat, counts):
+    out, off = [], 0
+    for c in counts:
+        out.append(flat[off:off + c])
+        off += c
+    return out
+
+
+def train_nonpipelined(ops, stage_end, params0, xs, labels, lr, mom=0.9, wd=0.0, nesterov=False):
+    """Plain mini-batch SGD (every staleness 0) with autograd and
+    torch.optim.SGD.  Returns (final flat params, losses, running stats)."""
+    slices, counts = op_param_slices(ops, stage_end)
+    flat = [torch.tensor(p, requires_grad=True) for p in split_flat(np.asarray(params0, np.float64), counts)]
+    lrs = np.broadcast_to(np.asarray(lr, dtype=np.float64), (len(counts),))
+    opt = torch.optim.SGD([{"params": [p], "lr": float(lrs[s])} for s, p in enumerate(flat)],
+                          lr=float(lrs[0]), momentum=mom, weight_decay=wd, nesterov=nesterov)
+    running = running_stats(ops)
+    losses = []
+    n = len(ops)
+    for t in range(len(xs)):
+        opt.zero_grad()
+        outs = run_ops(ops, 0, n, {0: torch.tensor(xs[t], dtype=torch.float64)}, flat, slices, running)
+        loss = F.cross_entropy(outs[n].reshape(outs[n].shape[0], -1), torch.tensor(labels[t], dtype=torch.long))
+        loss.backward()
+        opt.step()
+        losses.append(float(loss))
+    return torch.cat([p.detach() for p in flat]).numpy(), np.array(losses), running
+
+
+def boundary_tensor_ok(ops, stage_end):
+    """True when exactly one tensor crosses each stage boundary: the last
+    tensor of the previous stage (required by the partition simulator)."""
+    begin = 0
+    for e in stage_end:
+        for i in range(begin, e):
+            for src in (int(ops[i][1]), int(ops[i][2])):
+                if src >= 0 and src < begin and src != begin:
+                    return False
+        begin = e
+    return True
+
+
+def simulate_register_pipeline(ops, stage_end, params0, xs, labels, lr, mom=0.9, variant="paper", stash=False):
+    """Register/cycle simulator of pipelined backpropagation (Sec. 3).
+
+    K = S-1 register pairs split the network into partitions 1..K+1.  ONE
+    weight tensor per partition is updated in place after each of its
+    backward stages (no weight stashing).  Mini-batch t runs forward stage
+    FS_i at cycle t+i-1.  Backward stages:
+
+    variant "paper": BKS_j (partition K-j+2) at cycle t+K+j-1, i.e. FS_{K+1}
+        and BKS_1 share a cycle (they share an accelerator);
+    variant "same_cycle": every backward stage of mini-batch t runs in cycle
+        t+K, last partition first.
+
+    Inside a cycle every forward task runs before every backward task
+    (a forward reads the weights present at the start of the cycle).
+    Autograd saves each partition's weight tensor by reference, and updates
+    go through .data, so a backward pass computes data gradients with the
+    weights present when it runs and weight gradients from the activations
+    saved by its forward pass.
+
+    stash=True is the negative control (weight stashing as in PipeDream):
+    the forward pass runs on a private copy of the weights, so its backward
+    pass also sees the forward's version.
+
+    Returns (final flat params, losses by mini-batch, versions [T, S] = the
+    number of updates each partition had received when its forward ran,
+    last cycle used).
+    """
+    assert boundary_tensor_ok(ops, stage_end)
+    slices, counts = op_param_slices(ops, stage_end)
+    S = len(stage_end)
+    K = S - 1
+    T = len(xs)
+    W = [torch.tensor(p, requires_grad=True) for p in split_flat(np.asarray(params0, np.float64), counts)]
+    V = [torch.zeros_like(w) for w in W]
+    n_updates = [0] * S
+    begins = [0] + list(stage_end[:-1])
+    lrs = np.broadcast_to(np.asarray(lr, dtype=np.float64), (S,))
+    tasks = []  # (cycle, phase, order, t, partition, kind)
+    for t in range(T):
+        for i in range(S):
+            tasks.append((t + i, 0, i, t, i, "F"))
+        for i in range(S):  # partition i (0-based) = paper partition i+1
+            if variant == "paper":
+                j = K - i + 1          # BKS_j handles partition K-j+2 (1-based) = i+1
+                cyc = t + K + j - 1
+                order = 0
+            else:
+                cyc = t + K
+                order = S - 1 - i      # last partition first
+            tasks.append((cyc, 1, order, t, i, "B"))
+    tasks.sort(key=lambda z: (z[0], z[1], z[2], z[3]))
+    fwd = {}      # (t, i) -> (input leaf, output tensor)
+    stashed = {}  # (t, i) -> private weight copy (stash=True only)
+    grad_in = {}  # (t, i) -> gradient w.r.t. the output of partition i
+    losses = np.zeros(T)
+    versions = np.zeros((T, S), dtype=np.int32)
+    for cyc, phase, _, t, i, kind in tasks:
+        lo, hi = begins[i], stage_end[i]
+        if kind == "F":
+            if i == 0:
+                inp = torch.tensor(xs[t], dtype=torch.float64)
+            else:
+                inp = fwd[(t, i - 1)][1].detach().requires_grad_(True)
+            versions[t, i] = n_updates[i]
+            Wf = W
+            if stash:
+                Wf = list(W)
+                Wf[i] = W[i].detach().clone().requires_grad_(True)
+                stashed[(t, i)] = Wf[i]
+            outs = run_ops(ops, lo, hi, {lo: inp} if i > 0 else {0: inp}, Wf, slices)
+            out = outs[hi]
+            if i == S - 1:
+                out = F.cross_entropy(out.reshape(out.shape[0], -1), torch.tensor(labels[t], dtype=torch.long))
+                losses[t] = float(out)
+            fwd[(t, i)] = (inp, out)
+        else:
+            inp, out = fwd.pop((t, i))
+            if W[i].grad is not None:
+                W[i].grad = None
+            if i == S - 1:
+                out.backward()
+            else:
+                out.backward(grad_in.pop((t, i)))
+            if i > 0:
+                grad_in[(t, i - 1)] = inp.grad.detach().clone()
+            src = stashed.pop((t, i)) if stash else W[i]
+            g = src.grad if src.grad is not None else torch.zeros_like(W[i])
+            with torch.no_grad():
+                V[i].mul_(mom).add_(g)
+                W[i].data.sub_(float(lrs[i]) * V[i])
+            n_updates[i] += 1
+    last_cycle = max(z[0] for z in tasks)
+    return torch.cat([w.detach() for w in W]).numpy(), losses, versions, last_cycle
