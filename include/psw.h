@@ -1,0 +1,298 @@
+/*
+ * psw.h -- C ABI of libpsw: pipelined CNN training with stale weights on
+ * AMD Instinct MI355X (gfx950).
+ *
+ * Method: Zhang & Abdelrahman, "Pipelined Training with Stale Weights of
+ * Deep Convolutional Neural Networks" (arXiv 1912.12675).  Sec. 2 states
+ * layered backpropagation (x^(l) from x^(l-1) and W^(l); delta^(l-1) from
+ * delta^(l); dE/dW^(l) from x^(l-1) and delta^(l); update after all
+ * gradients).  Sec. 3 inserts pipeline register pairs after layers p_1..p_K
+ * (the Pipeline Placement Vector) so that forward stage FS_i computes with
+ * weights that are several updates old ("degree of staleness").  Sec. 4
+ * switches from pipelined to non-pipelined training after n_p iterations.
+ * App. A/B fix SGD with momentum 0.9 and a per-stage learning rate (Table 7).
+ *
+ * Conventions shared by every entry point
+ *  - Every pointer argument is a DEVICE pointer unless its comment says
+ *    "host".  The caller owns all device memory; the library never
+ *    allocates device memory.
+ *  - Activations are float32 NCHW (layout code PSW_NCHW); conv weights are
+ *    KCRS [K_out][C_in][R][S]; FC weights are [out][in]; all contiguous.
+ *  - `stream` is a hipStream_t passed as void* (NULL = default stream).
+ *    Every call only enqueues work on that stream; nothing synchronises the
+ *    host.  Faults inside kernels surface at the caller's next sync.
+ *  - `prec`: PSW_FP32, or PSW_BF16 = both operands of every conv/FC product
+ *    rounded to bfloat16 (round to nearest even) with fp32 accumulation;
+ *    all other arithmetic and all storage stay fp32.
+ *  - Return value: PSW_OK (0) or a negative PSW_ERR_* code.  Nothing is
+ *    enqueued when argument validation fails.  psw_last_error() returns a
+ *    thread-local description of the last failure on the calling thread.
+ *  - Workspaces: entry points that need scratch device memory take
+ *    (ws, ws_bytes) and report the size they need through a *_ws_bytes
+ *    query; a too-small workspace is PSW_ERR_WORKSPACE.
+ */
+#ifndef PSW_H
+#define PSW_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    PSW_OK = 0,
+    PSW_ERR_NULL = -1,        /* a required pointer is NULL */
+    PSW_ERR_SHAPE = -2,       /* inconsistent or out-of-range sizes */
+    PSW_ERR_UNSUPPORTED = -3, /* valid request this build does not implement */
+    PSW_ERR_STALENESS = -4,   /* staleness < 0 or >= ring depth */
+    PSW_ERR_STEP_ORDER = -5,  /* stage_step t is not the expected next step */
+    PSW_ERR_WORKSPACE = -6,   /* workspace / arena too small */
+    PSW_ERR_HIP = -7,         /* the HIP runtime reported an error */
+    PSW_ERR_STATE = -8        /* object not ready (e.g. net not bound) */
+};
+
+enum { PSW_NCHW = 0, PSW_NHWC = 1 };
+enum { PSW_FP32 = 0, PSW_BF16 = 1 };
+
+/* Thread-local message of the last failing call on this thread ("" if none). */
+const char *psw_last_error(void);
+/* Library version string. */
+const char *psw_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* Per-layer operations (Sec. 2, layered backpropagation).                  */
+/* ------------------------------------------------------------------------ */
+
+/* Convolution forward (Sec. 2: x^(l) from x^(l-1) and W^(l)):
+ *   y[n,k,p,q] = bias[k] + sum_{c,r,s} w[k,c,r,s] x[n,c,p*stride+r-pad,q*stride+s-pad]
+ *   followed by max(0,.) when relu != 0.  Zero padding.
+ * x: [n,c,h,w]; w: [k,c,r,s]; bias: [k] or NULL; y: [n,k,p,q] with
+ * p = (h+2pad-r)/stride+1, q likewise.  y must not overlap x. */
+int psw_conv_fwd(int n, int c, int h, int w, int k, int r, int s, int stride, int pad,
+                 const float *x, const float *wt, const float *bias, int relu, float *y, int prec,
+                 void *stream);
+
+/* Convolution backward-data (Sec. 2: delta^(l-1) from delta^(l) and W):
+ * the adjoint of the forward map (without bias/ReLU; mask dy first with
+ * psw_relu_mask when the forward applied ReLU).
+ *   dx[n,c,ih,iw] (+)= sum over (k,r,s,p,q) with ih=p*stride+r-pad, iw=q*stride+s-pad
+ *                      of dy[n,k,p,q] w[k,c,r,s]
+ * Overwrites dx when accumulate == 0, adds into it otherwise. */
+int psw_conv_bwd_data(int n, int c, int h, int w, int k, int r, int s, int stride, int pad,
+                      const float *wt, const float *dy, float *dx, int accumulate, int prec,
+                      void *stream);
+
+/* Workspace bytes psw_conv_bwd_weight needs for this shape and precision. */
+size_t psw_conv_bwd_weight_ws_bytes(int n, int c, int h, int w, int k, int r, int s, int stride,
+                                    int pad, int prec);
+
+/* Convolution backward-weight (Sec. 2: dE/dW^(l) from x^(l-1) and delta^(l)):
+ *   dw[k,c,r,s] = sum_{n,p,q} dy[n,k,p,q] x[n,c,p*stride+r-pad,q*stride+s-pad]
+ *   dbias[k]    = sum_{n,p,q} dy[n,k,p,q]        (skipped when dbias == NULL)
+ * Overwrites dw / dbias.  The reduction over n*p*q is split across
+ * workgroups and the partial sums are added in a fixed order, so the result
+ * is bit-reproducible. */
+int psw_conv_bwd_weight(int n, int c, int h, int w, int k, int r, int s, int stride, int pad,
+                        const float *x, const float *dy, float *dw, float *dbias, int prec, void *ws,
+                        size_t ws_bytes, void *stream);
+
+/* Workspace bytes of the batch-norm entry points for [n,c,h,w]. */
+size_t psw_bn_ws_bytes(int n, int c, int h, int w);
+
+/* Batch norm in training mode, optional residual add, optional ReLU (the
+ * normalisation the paper's VGG and ResNet training uses, App. A/B):
+ *   mean_c, var_c over n*h*w (biased);  xhat = (y-mean)/sqrt(var+eps)
+ *   z = gamma*xhat + beta [+ sc(res)];  z = max(z,0) if relu
+ * sc(res): identity when res is [n,c,h,w]; otherwise the CIFAR-ResNet
+ * "option A" shortcut: res [n,rc,rh,rw] with rh = h*k, rw = w*k, rc <= c,
+ * subsampled at even positions and zero-padded by (c-rc)/2 channels on each
+ * side.  res may be NULL (rc, rh, rw ignored).
+ * save_mean / save_invstd [c] receive the batch statistics for the
+ * backward pass.  run_mean / run_var [c] (both NULL or both set) are
+ * updated as r = (1-momentum) r + momentum * stat, unbiased variance. */
+int psw_bn_relu_fwd(int n, int c, int h, int w, const float *y, const float *gamma,
+                    const float *beta, const float *res, int rc, int rh, int rw, int relu, float eps,
+                    float momentum, float *z, float *save_mean, float *save_invstd, float *run_mean,
+                    float *run_var, void *ws, size_t ws_bytes, void *stream);
+
+/* Backward of psw_bn_relu_fwd.  g = dz * [z > 0] (relu) or dz;
+ *   dbeta = sum g;  dgamma = sum g*xhat;
+ *   dy = gamma*invstd*(g - dbeta/M - xhat*dgamma/M)   (overwrites dy)
+ *   dres (+)= sc^T(g)  (when dres != NULL; accumulate per res_accumulate)
+ * gamma is whichever version the caller passes: the stale-weight schedule
+ * passes the current weights (the backward stage reads the single, already
+ * updated copy, Sec. 3).  y is the BN input saved by the forward pass. */
+int psw_bn_relu_bwd(int n, int c, int h, int w, const float *dz, const float *z, const float *y,
+                    const float *gamma, const float *save_mean, const float *save_invstd, int relu,
+                    float *dy, float *dgamma, float *dbeta, float *dres, int rc, int rh, int rw,
+                    int res_accumulate, void *ws, size_t ws_bytes, void *stream);
+
+enum { PSW_POOL_MAX = 0, PSW_POOL_GAVG = 1 };
+
+/* Pooling forward.  PSW_POOL_MAX: k x k window, step `stride`, no padding,
+ * floor mode; argmax [n,c,p,q] receives the flat in-plane index (ih*w+iw)
+ * of the first maximum in row-major window order.  Only non-overlapping
+ * windows (k == stride) are supported.  PSW_POOL_GAVG: global average,
+ * y [n,c] (k, stride, argmax ignored). */
+int psw_pool_fwd(int kind, int n, int c, int h, int w, int k, int stride, const float *x, float *y,
+                 int32_t *argmax, void *stream);
+
+/* Pooling backward: MAX routes dy to the saved argmax; GAVG spreads dy/(h*w)
+ * over the plane.  dx [n,c,h,w] overwritten (accumulate == 0) or added to. */
+int psw_pool_bwd(int kind, int n, int c, int h, int w, int k, int stride, const float *dy,
+                 const int32_t *argmax, float *dx, int accumulate, void *stream);
+
+/* Fully connected forward: y[n,o] = b[o] + sum_i x[n,i] w[o,i], then
+ * max(0,.) if relu.  x [n,in], w [out,in], b [out] or NULL, y [n,out]. */
+int psw_fc_fwd(int n, int in, int out, const float *x, const float *wt, const float *b, int relu,
+               float *y, int prec, void *stream);
+
+size_t psw_fc_bwd_ws_bytes(int n, int in, int out);
+
+/* Fully connected backward (dy already masked for a ReLU output):
+ *   dx[n,i] (+)= sum_o dy[n,o] w[o,i]   (dx may be NULL)
+ *   dw[o,i]  = sum_n dy[n,o] x[n,i];  db[o] = sum_n dy[n,o] (db may be NULL) */
+int psw_fc_bwd(int n, int in, int out, const float *x, const float *wt, const float *dy, float *dx,
+               int dx_accumulate, float *dw, float *db, int prec, void *ws, size_t ws_bytes,
+               void *stream);
+
+/* ReLU backward in place: g[i] = 0 where z[i] <= 0 (z = the ReLU output). */
+int psw_relu_mask(int64_t count, const float *z, float *g, void *stream);
+
+/* Softmax cross-entropy, mean over the mini-batch (the training error e of
+ * Sec. 2):  loss = (1/n) sum_i [logsumexp(logits_i) - logits_i[label_i]],
+ * dlogits = (softmax - onehot)/n.  loss: one device float.  labels [n] in
+ * [0, classes) (not checked on the device). */
+int psw_softmax_xent(int n, int classes, const float *logits, const int32_t *labels, float *loss,
+                     float *dlogits, void *stream);
+
+/* SGD with momentum (App. A/B):  d = g + wd*w_in;  v = mom*v + d;
+ *   w_out = w_in - lr*(nesterov ? d + mom*v : v).
+ * w_out may equal w_in (in-place); otherwise the ranges must not overlap. */
+int psw_sgd_momentum_step(int64_t count, const float *w_in, float *w_out, float *v, const float *g,
+                          float lr, float mom, float wd, int nesterov, void *stream);
+
+/* ------------------------------------------------------------------------ */
+/* Networks and the stale-weight stage scheduler (Sec. 3, Sec. 4).          */
+/* ------------------------------------------------------------------------ */
+
+/* One operation of a network; tensor 0 is the mini-batch, operation i
+ * writes tensor i+1.  kind: PSW_OP_*.  in0: input tensor id; in1: residual
+ * tensor id of a batch norm (-1 none).  cin/cout: channels (features for
+ * FC); k, stride, pad: conv / max-pool geometry.  flags: PSW_F_BIAS,
+ * PSW_F_RELU.  Parameters of a stage are packed, in operation order, as
+ * conv (weight, bias), bn (gamma, beta), fc (weight, bias). */
+typedef struct {
+    int32_t kind, in0, in1, cin, cout, k, stride, pad, flags;
+} psw_layer;
+
+enum { PSW_OP_CONV = 1, PSW_OP_BN = 2, PSW_OP_MAXPOOL = 3, PSW_OP_GAVG = 4, PSW_OP_FC = 5 };
+enum { PSW_F_BIAS = 1, PSW_F_RELU = 2 };
+
+typedef struct psw_net psw_net;
+
+/* Build a network plan (host only; no device work, no HIP call).
+ * layers[n_layers]; the input batch is [batch, c0, h0, w0]; the last
+ * operation produces the logits.  stage_end[n_stages]: one past the last
+ * operation of each stage (the PPV of Sec. 3 expressed in operations;
+ * stage_end[n_stages-1] == n_layers).  ring_depth[s] >= 1: number of weight
+ * versions stage s keeps resident (max staleness it will be asked for + 1).
+ * *out receives the new object (free with psw_net_destroy). */
+int psw_net_create(const psw_layer *layers, int n_layers, int batch, int c0, int h0, int w0,
+                   const int32_t *stage_end, int n_stages, const int32_t *ring_depth, int prec,
+                   psw_net **out);
+
+void psw_net_destroy(psw_net *net);
+
+/* Sizes the caller must allocate before psw_net_bind (host outputs):
+ * stage_params[s] = parameters of stage s; ring_floats = sum_s
+ * ring_depth[s]*stage_params[s]; n_params = sum_s stage_params[s];
+ * bn_channels = running-statistic entries (sum of BN channels);
+ * arena_bytes = activations, gradients and workspaces of one step. */
+int psw_net_sizes(const psw_net *net, int64_t *stage_params, int64_t *ring_floats,
+                  int64_t *n_params, int64_t *bn_channels, int64_t *arena_bytes);
+
+/* Attach device memory.  ring [ring_floats]: stage-major, then version slot,
+ * then that stage's packed parameters; the caller writes W^(0) into slot 0
+ * of every stage (see psw_net_slot) before step 0.  momentum, grad
+ * [n_params] (stage-major; momentum must start at zero).  run_mean,
+ * run_var [bn_channels] (may be NULL).  arena [arena_bytes] (>= 256-byte
+ * aligned). */
+int psw_net_bind(psw_net *net, float *ring, float *momentum, float *grad, float *run_mean,
+                 float *run_var, void *arena, size_t arena_bytes);
+
+/* One training step of mini-batch t under the stale-weight schedule.
+ * For every stage s, with d_s = staleness[s] (host array, 0 <= d_s <
+ * ring_depth[s]):
+ *   the forward pass reads weight version r_s = max(0, t - d_s) (Sec. 3:
+ *     FS_i computes with weights several updates old; pipeline fill clamps
+ *     at version 0),
+ *   the backward pass computes weight gradients from the activations that
+ *     forward pass saved and data gradients with the current version t
+ *     (one weight copy per partition, no stashing),
+ *   the update writes version t+1 = SGD(version t, grad) with rate lr[s]
+ *     (host array; per-stage rates as in Table 7).
+ * All stages d_s = 0 is plain mini-batch SGD (Sec. 2); switching every
+ * d_s to 0 at t = n_p is the hybrid schedule of Sec. 4.
+ * t must equal the previous call's t + 1 (0 for the first call, or the value
+ * set by psw_net_set_step), else PSW_ERR_STEP_ORDER.
+ * x [batch,c0,h0,w0] and labels [batch] are device buffers; loss_out is one
+ * device float; versions_out (host, [n_stages], may be NULL) receives r_s. */
+int psw_stage_step(psw_net *net, int64_t t, const int32_t *staleness, const float *lr, float mom,
+                   float wd, int nesterov, const float *x, const int32_t *labels, float *loss_out,
+                   int32_t *versions_out, void *stream);
+
+/* Set the next expected step (resume from a checkpoint whose ring holds
+ * versions t-ring_depth+1 .. t in their slots v mod ring_depth). */
+int psw_net_set_step(psw_net *net, int64_t t);
+
+/* Device pointer (through *params) of stage `stage`'s weight version
+ * `version`, which must be resident: next_t - ring_depth < version <= next_t
+ * (any version <= next_t while next_t < ring_depth).  Slot = version mod
+ * ring_depth. */
+int psw_net_slot(const psw_net *net, int stage, int64_t version, float **params);
+
+/* Offset (in floats, inside the packed parameters of the op's stage) and
+ * count of operation `op`'s parameters (host outputs). */
+int psw_net_param_offset(const psw_net *net, int op, int *stage, int64_t *offset, int64_t *count);
+
+/* Dry run of psw_stage_step (host only, no device work): the kernel-level
+ * plan of step t.  Each record is (op, what, stage, version) where `what`
+ * is a PSW_PLAN_* code, `version` the weight version it reads (-1 if
+ * none).  Writes up to cap records; *n_out receives the total count.
+ * Validates exactly as psw_stage_step does (step order excepted). */
+typedef struct {
+    int32_t op, what, stage;
+    int64_t version;
+} psw_launch;
+
+enum {
+    PSW_PLAN_CONV_FWD = 1, PSW_PLAN_BN_FWD, PSW_PLAN_POOL_FWD, PSW_PLAN_FC_FWD, PSW_PLAN_LOSS,
+    PSW_PLAN_RELU_MASK, PSW_PLAN_CONV_BWD_WEIGHT, PSW_PLAN_CONV_BWD_DATA, PSW_PLAN_BN_BWD,
+    PSW_PLAN_POOL_BWD, PSW_PLAN_FC_BWD, PSW_PLAN_SGD
+};
+
+int psw_net_plan(const psw_net *net, int64_t t, const int32_t *staleness, psw_launch *out, int cap,
+                 int *n_out);
+
+/* Per-launch timing of psw_stage_step with HIP events recorded on the
+ * step's stream around every launcher (for measurement; off by default).
+ * psw_net_profile(net, 1) enables it and clears previous records;
+ * psw_net_profile_read waits for the recorded events, writes the summed
+ * milliseconds and launcher counts per PSW_PROF_* kind into the host arrays
+ * ms[n_kinds] and launches[n_kinds], and clears the records.  Events are
+ * created on first use and kept until psw_net_destroy. */
+enum {
+    PSW_PROF_CONV_FWD = 0, PSW_PROF_CONV_BWD_DATA = 1, PSW_PROF_CONV_BWD_WEIGHT = 2, PSW_PROF_BN_FWD = 3,
+    PSW_PROF_BN_BWD = 4, PSW_PROF_POOL = 5, PSW_PROF_FC = 6, PSW_PROF_LOSS = 7, PSW_PROF_SGD = 8,
+    PSW_PROF_OTHER = 9, PSW_PROF_KINDS = 10
+};
+int psw_net_profile(psw_net *net, int enable);
+int psw_net_profile_read(psw_net *net, int n_kinds, double *ms, int64_t *launches);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* PSW_H */

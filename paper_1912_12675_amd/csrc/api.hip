@@ -1,0 +1,825 @@
+// C ABI of libpsw (declared in include/psw.h): argument validation, error
+// reporting, and the stale-weight stage scheduler with its per-stage
+// weight-version ring.
+//
+// Schedule (Sec. 3 of the paper, one weight copy per partition, no stashing,
+// read as: mini-batch t's forward stage i sees the updates of mini-batches
+// < t - d_i, its backward stage sees every update of mini-batches < t):
+//   forward of stage s at step t   : version r_s = max(0, t - d_s)
+//   backward of stage s at step t  : weight gradients from the activations
+//                                    saved by that forward, data gradients
+//                                    with version t
+//   update of stage s at step t    : version t+1 = SGD(version t)
+// The ring of stage s keeps D_s = ring_depth[s] consecutive versions, version
+// v in slot v mod D_s.  After step t-1 the resident versions are t-D_s+1..t,
+// so any d_s <= D_s-1 is readable; the update of step t writes slot
+// (t+1) mod D_s, which holds version t+1-D_s <= t-d_s: only the version the
+// forward pass of this same step may read, and that pass has already run on
+// the stream.  D_s = 1 updates in place.
+#include <hip/hip_runtime.h>
+
+#include <stdarg.h>
+#include <stdio.h>
+#include <string.h>
+
+#include <string>
+#include <vector>
+
+#include "../../include/psw.h"
+#include "internal.h"
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_err = buf;
+    return code;
+}
+
+int hip_check(hipError_t e, const char* what)
+{
+    if (e == hipSuccess) return PSW_OK;
+    return fail(PSW_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+inline hipStream_t S(void* s) { return (hipStream_t)s; }
+
+bool bad_dims(std::initializer_list<int> v)
+{
+    for (int x : v)
+        if (x <= 0) return true;
+    return false;
+}
+
+int check_conv(int n, int c, int h, int w, int k, int r, int s, int stride, int pad, int prec, psw::ConvShape* cs)
+{
+    if (bad_dims({n, c, h, w, k, r, s, stride}) || pad < 0)
+        return fail(PSW_ERR_SHAPE, "conv: sizes must be positive (pad >= 0)");
+    if (prec != PSW_FP32 && prec != PSW_BF16) return fail(PSW_ERR_UNSUPPORTED, "conv: unknown precision %d", prec);
+    const int p = psw::conv_out_dim(h, r, stride, pad), q = psw::conv_out_dim(w, s, stride, pad);
+    if (h + 2 * pad < r || w + 2 * pad < s || p <= 0 || q <= 0)
+        return fail(PSW_ERR_SHAPE, "conv: kernel larger than padded input");
+    if ((int64_t)n * c * h * w > INT32_MAX || (int64_t)n * k * p * q > INT32_MAX ||
+        (int64_t)k * c * r * s > INT32_MAX)
+        return fail(PSW_ERR_SHAPE, "conv: tensor too large for 32-bit GEMM indexing");
+    *cs = psw::ConvShape{n, c, h, w, k, r, s, stride, pad, p, q};
+    return PSW_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* psw_last_error(void) { return g_err.c_str(); }
+const char* psw_version(void) { return "psw 0.1 gfx950"; }
+
+int psw_conv_fwd(int n, int c, int h, int w, int k, int r, int s, int stride, int pad, const float* x,
+                 const float* wt, const float* bias, int relu, float* y, int prec, void* stream)
+{
+    psw::ConvShape cs;
+    int rc = check_conv(n, c, h, w, k, r, s, stride, pad, prec, &cs);
+    if (rc) return rc;
+    if (!x || !wt || !y) return fail(PSW_ERR_NULL, "conv_fwd: x, w and y are required");
+    return hip_check(psw::conv_fwd(cs, x, wt, bias, relu, y, prec == PSW_BF16, S(stream)), "conv_fwd");
+}
+
+int psw_conv_bwd_data(int n, int c, int h, int w, int k, int r, int s, int stride, int pad, const float* wt,
+                      const float* dy, float* dx, int accumulate, int prec, void* stream)
+{
+    psw::ConvShape cs;
+    int rc = check_conv(n, c, h, w, k, r, s, stride, pad, prec, &cs);
+    if (rc) return rc;
+    if (!wt || !dy || !dx) return fail(PSW_ERR_NULL, "conv_bwd_data: w, dy and dx are required");
+    return hip_check(psw::conv_bwd_data(cs, wt, dy, dx, accumulate, prec == PSW_BF16, S(stream)), "conv_bwd_data");
+}
+
+size_t psw_conv_bwd_weight_ws_bytes(int n, int c, int h, int w, int k, int r, int s, int stride, int pad, int prec)
+{
+    psw::ConvShape cs;
+    if (check_conv(n, c, h, w, k, r, s, stride, pad, prec, &cs)) return 0;
+    return psw::conv_bwd_weight_ws_bytes(cs, prec == PSW_BF16);
+}
+
+int psw_conv_bwd_weight(int n, int c, int h, int w, int k, int r, int s, int stride, int pad, const float* x,
+                        const float* dy, float* dw, float* dbias, int prec, void* ws, size_t ws_bytes, void* stream)
+{
+    psw::ConvShape cs;
+    int rc = check_conv(n, c, h, w, k, r, s, stride, pad, prec, &cs);
+    if (rc) return rc;
+    if (!x || !dy || !dw || !ws) return fail(PSW_ERR_NULL, "conv_bwd_weight: x, dy, dw and ws are required");
+    const size_t need = psw::conv_bwd_weight_ws_bytes(cs, prec == PSW_BF16);
+    if (ws_bytes < need) return fail(PSW_ERR_WORKSPACE, "conv_bwd_weight: workspace %zu < %zu bytes", ws_bytes, need);
+    return hip_check(psw::conv_bwd_weight(cs, x, dy, dw, dbias, prec == PSW_BF16, ws, ws_bytes, S(stream)),
+                     "conv_bwd_weight");
+}
+
+size_t psw_bn_ws_bytes(int n, int c, int h, int w)
+{
+    if (bad_dims({n, c, h, w})) return 0;
+    return psw::bn_ws_bytes(n, c, h, w);
+}
+
+static int check_residual(int c, int h, int w, const float* res, int rc, int rh, int rw)
+{
+    if (!res) return PSW_OK;
+    if (rc == c && rh == h && rw == w) return PSW_OK;
+    if (rc <= 0 || rc > c || (c - rc) % 2 != 0 || rh <= 0 || rw <= 0 || rh % h != 0 || rw % w != 0 ||
+        rh / h != rw / w)
+        return fail(PSW_ERR_SHAPE, "bn: residual [%d,%d,%d] does not fit output [%d,%d,%d]", rc, rh, rw, c, h, w);
+    return PSW_OK;
+}
+
+int psw_bn_relu_fwd(int n, int c, int h, int w, const float* y, const float* gamma, const float* beta, const float* res,
+                    int rc, int rh, int rw, int relu, float eps, float momentum, float* z, float* save_mean,
+                    float* save_invstd, float* run_mean, float* run_var, void* ws, size_t ws_bytes, void* stream)
+{
+    if (bad_dims({n, c, h, w})) return fail(PSW_ERR_SHAPE, "bn_fwd: sizes must be positive");
+    if (!y || !gamma || !beta || !z || !save_mean || !save_invstd || !ws)
+        return fail(PSW_ERR_NULL, "bn_fwd: required pointer is NULL");
+    if ((run_mean == nullptr) != (run_var == nullptr))
+        return fail(PSW_ERR_NULL, "bn_fwd: run_mean and run_var must both be set or both NULL");
+    int e = check_residual(c, h, w, res, rc, rh, rw);
+    if (e) return e;
+    const size_t need = psw::bn_ws_bytes(n, c, h, w);
+    if (ws_bytes < need) return fail(PSW_ERR_WORKSPACE, "bn_fwd: workspace %zu < %zu bytes", ws_bytes, need);
+    return hip_check(psw::bn_fwd(n, c, h, w, y, gamma, beta, res, rc, rh, rw, relu, eps, momentum, z, save_mean,
+                                 save_invstd, run_mean, run_var, ws, ws_bytes, S(stream)),
+                     "bn_fwd");
+}
+
+int psw_bn_relu_bwd(int n, int c, int h, int w, const float* dz, const float* z, const float* y, const float* gamma,
+                    const float* save_mean, const float* save_invstd, int relu, float* dy, float* dgamma,
+                    float* dbeta, float* dres, int rc, int rh, int rw, int res_accumulate, void* ws, size_t ws_bytes,
+                    void* stream)
+{
+    if (bad_dims({n, c, h, w})) return fail(PSW_ERR_SHAPE, "bn_bwd: sizes must be positive");
+    if (!dz || !z || !y || !gamma || !save_mean || !save_invstd || !dy || !dgamma || !dbeta || !ws)
+        return fail(PSW_ERR_NULL, "bn_bwd: required pointer is NULL");
+    int e = check_residual(c, h, w, dres, rc, rh, rw);
+    if (e) return e;
+    const size_t need = psw::bn_ws_bytes(n, c, h, w);
+    if (ws_bytes < need) return fail(PSW_ERR_WORKSPACE, "bn_bwd: workspace %zu < %zu bytes", ws_bytes, need);
+    return hip_check(psw::bn_bwd(n, c, h, w, dz, z, y, gamma, save_mean, save_invstd, relu, dy, dgamma, dbeta, dres,
+                                 rc, rh, rw, res_accumulate, ws, ws_bytes, S(stream)),
+                     "bn_bwd");
+}
+
+int psw_pool_fwd(int kind, int n, int c, int h, int w, int k, int stride, const float* x, float* y, int32_t* argmax,
+                 void* stream)
+{
+    if (bad_dims({n, c, h, w})) return fail(PSW_ERR_SHAPE, "pool_fwd: sizes must be positive");
+    if (!x || !y) return fail(PSW_ERR_NULL, "pool_fwd: x and y are required");
+    if (kind == PSW_POOL_GAVG) return hip_check(psw::gavgpool_fwd(n, c, h, w, x, y, S(stream)), "pool_fwd");
+    if (kind != PSW_POOL_MAX) return fail(PSW_ERR_UNSUPPORTED, "pool_fwd: unknown kind %d", kind);
+    if (!argmax) return fail(PSW_ERR_NULL, "pool_fwd: max pooling needs argmax");
+    if (k <= 0 || stride <= 0 || k > h || k > w) return fail(PSW_ERR_SHAPE, "pool_fwd: bad window");
+    if (k != stride) return fail(PSW_ERR_UNSUPPORTED, "pool_fwd: only non-overlapping windows (k == stride)");
+    return hip_check(psw::maxpool_fwd(n, c, h, w, k, stride, x, y, argmax, S(stream)), "pool_fwd");
+}
+
+int psw_pool_bwd(int kind, int n, int c, int h, int w, int k, int stride, const float* dy, const int32_t* argmax,
+                 float* dx, int accumulate, void* stream)
+{
+    if (bad_dims({n, c, h, w})) return fail(PSW_ERR_SHAPE, "pool_bwd: sizes must be positive");
+    if (!dy || !dx) return fail(PSW_ERR_NULL, "pool_bwd: dy and dx are required");
+    if (kind == PSW_POOL_GAVG)
+        return hip_check(psw::gavgpool_bwd(n, c, h, w, dy, dx, accumulate, S(stream)), "pool_bwd");
+    if (kind != PSW_POOL_MAX) return fail(PSW_ERR_UNSUPPORTED, "pool_bwd: unknown kind %d", kind);
+    if (!argmax) return fail(PSW_ERR_NULL, "pool_bwd: max pooling needs argmax");
+    if (k <= 0 || stride <= 0 || k > h || k > w) return fail(PSW_ERR_SHAPE, "pool_bwd: bad window");
+    if (k != stride) return fail(PSW_ERR_UNSUPPORTED, "pool_bwd: only non-overlapping windows (k == stride)");
+    return hip_check(psw::maxpool_bwd(n, c, h, w, k, stride, dy, argmax, dx, accumulate, S(stream)), "pool_bwd");
+}
+
+int psw_fc_fwd(int n, int in, int out, const float* x, const float* wt, const float* b, int relu, float* y, int prec,
+               void* stream)
+{
+    if (bad_dims({n, in, out})) return fail(PSW_ERR_SHAPE, "fc_fwd: sizes must be positive");
+    if (!x || !wt || !y) return fail(PSW_ERR_NULL, "fc_fwd: x, w and y are required");
+    if (prec != PSW_FP32 && prec != PSW_BF16) return fail(PSW_ERR_UNSUPPORTED, "fc_fwd: unknown precision");
+    return hip_check(psw::fc_fwd(n, in, out, x, wt, b, relu, y, prec == PSW_BF16, S(stream)), "fc_fwd");
+}
+
+size_t psw_fc_bwd_ws_bytes(int n, int in, int out)
+{
+    if (bad_dims({n, in, out})) return 0;
+    return psw::fc_bwd_ws_bytes(n, in, out);
+}
+
+int psw_fc_bwd(int n, int in, int out, const float* x, const float* wt, const float* dy, float* dx, int dx_accumulate,
+               float* dw, float* db, int prec, void* ws, size_t ws_bytes, void* stream)
+{
+    if (bad_dims({n, in, out})) return fail(PSW_ERR_SHAPE, "fc_bwd: sizes must be positive");
+    if (!x || !wt || !dy || !dw || !ws) return fail(PSW_ERR_NULL, "fc_bwd: x, w, dy, dw and ws are required");
+    if (prec != PSW_FP32 && prec != PSW_BF16) return fail(PSW_ERR_UNSUPPORTED, "fc_bwd: unknown precision");
+    const size_t need = psw::fc_bwd_ws_bytes(n, in, out);
+    if (ws_bytes < need) return fail(PSW_ERR_WORKSPACE, "fc_bwd: workspace %zu < %zu bytes", ws_bytes, need);
+    return hip_check(psw::fc_bwd(n, in, out, x, wt, dy, dx, dx_accumulate, dw, db, prec == PSW_BF16, ws, ws_bytes,
+                                 S(stream)),
+                     "fc_bwd");
+}
+
+int psw_relu_mask(int64_t count, const float* z, float* g, void* stream)
+{
+    if (count < 0) return fail(PSW_ERR_SHAPE, "relu_mask: negative count");
+    if (count == 0) return PSW_OK;
+    if (!z || !g) return fail(PSW_ERR_NULL, "relu_mask: z and g are required");
+    return hip_check(psw::relu_mask(count, z, g, S(stream)), "relu_mask");
+}
+
+int psw_softmax_xent(int n, int classes, const float* logits, const int32_t* labels, float* loss, float* dlogits,
+                     void* stream)
+{
+    if (bad_dims({n, classes})) return fail(PSW_ERR_SHAPE, "softmax_xent: sizes must be positive");
+    if (!logits || !labels || !loss || !dlogits) return fail(PSW_ERR_NULL, "softmax_xent: required pointer is NULL");
+    return hip_check(psw::softmax_xent(n, classes, logits, labels, loss, dlogits, S(stream)), "softmax_xent");
+}
+
+int psw_sgd_momentum_step(int64_t count, const float* w_in, float* w_out, float* v, const float* g, float lr,
+                          float mom, float wd, int nesterov, void* stream)
+{
+    if (count < 0) return fail(PSW_ERR_SHAPE, "sgd: negative count");
+    if (count == 0) return PSW_OK;
+    if (!w_in || !w_out || !v || !g) return fail(PSW_ERR_NULL, "sgd: required pointer is NULL");
+    if (w_out != w_in && w_out < w_in + count && w_in < w_out + count)
+        return fail(PSW_ERR_SHAPE, "sgd: w_out partially overlaps w_in");
+    return hip_check(psw::sgd_momentum(count, w_in, w_out, v, g, lr, mom, wd, nesterov, S(stream)), "sgd");
+}
+
+}  // extern "C"
+
+// ============================================================================
+// Network plan and stage scheduler
+// ============================================================================
+struct Tensor {
+    int n, c, h, w;
+    int64_t numel() const { return (int64_t)n * c * h * w; }
+};
+
+struct psw_net {
+    std::vector<psw_layer> ops;
+    int batch = 0, prec = 0, S = 0;
+    std::vector<Tensor> t;              // n_ops + 1
+    std::vector<int> stage_begin, stage_end, ring_depth, stage_of;
+    std::vector<int64_t> stage_np;      // params per stage
+    std::vector<int64_t> ring_off;      // float offset of each stage's ring
+    std::vector<int64_t> flat_off;      // float offset of each stage in momentum/grad
+    std::vector<int64_t> poff, pcount;  // per op, inside its stage
+    std::vector<int64_t> bn_off;        // per op (BN): offset into running stats, else -1
+    int64_t bn_channels = 0;
+    // arena layout (bytes)
+    std::vector<size_t> act_off, grad_off;  // per tensor (index 0 unused)
+    std::vector<size_t> save_off;           // per op: BN mean/invstd or max-pool argmax
+    std::vector<char> grad_accum;           // per op input slot: 0 overwrite, 1 accumulate (in0, in1)
+    size_t ws_off = 0, ws_bytes = 0, arena_bytes = 0;
+    // bound memory
+    float *ring = nullptr, *momentum = nullptr, *grad = nullptr, *run_mean = nullptr, *run_var = nullptr;
+    char* arena = nullptr;
+    bool bound = false;
+    int64_t next_t = 0;
+    // optional per-launch timing with HIP events (psw_net_profile)
+    struct ProfRec {
+        int kind;
+        hipEvent_t a, b;
+    };
+    bool profiling = false;
+    std::vector<hipEvent_t> ev_pool;
+    size_t ev_used = 0;
+    std::vector<ProfRec> prof;
+    ~psw_net()
+    {
+        for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
+    }
+    hipEvent_t next_event()
+    {
+        if (ev_used == ev_pool.size()) {
+            hipEvent_t e;
+            if (hipEventCreate(&e) != hipSuccess) return nullptr;
+            ev_pool.push_back(e);
+        }
+        return ev_pool[ev_used++];
+    }
+};
+
+namespace {
+
+size_t align256(size_t x) { return (x + 255) / 256 * 256; }
+
+int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, int c0, int h0, int w0,
+              const int32_t* stage_end, int n_stages, const int32_t* ring_depth, int prec)
+{
+    if (!layers || !stage_end || !ring_depth) return fail(PSW_ERR_NULL, "net_create: required pointer is NULL");
+    if (n_layers <= 0 || n_stages <= 0 || n_stages > n_layers || bad_dims({batch, c0, h0, w0}))
+        return fail(PSW_ERR_SHAPE, "net_create: bad sizes");
+    if (prec != PSW_FP32 && prec != PSW_BF16) return fail(PSW_ERR_UNSUPPORTED, "net_create: unknown precision");
+    net->ops.assign(layers, layers + n_layers);
+    net->batch = batch;
+    net->prec = prec;
+    net->S = n_stages;
+    net->t.assign(n_layers + 1, Tensor{0, 0, 0, 0});
+    net->t[0] = Tensor{batch, c0, h0, w0};
+    net->stage_of.assign(n_layers, 0);
+    int prev = 0;
+    for (int s = 0; s < n_stages; ++s) {
+        if (stage_end[s] <= prev || stage_end[s] > n_layers)
+            return fail(PSW_ERR_SHAPE, "net_create: stage_end[%d] = %d is not increasing within (0, %d]", s,
+                        stage_end[s], n_layers);
+        if (ring_depth[s] < 1) return fail(PSW_ERR_SHAPE, "net_create: ring_depth[%d] < 1", s);
+        net->stage_begin.push_back(prev);
+        net->stage_end.push_back(stage_end[s]);
+        net->ring_depth.push_back(ring_depth[s]);
+        for (int i = prev; i < stage_end[s]; ++i) net->stage_of[i] = s;
+        prev = stage_end[s];
+    }
+    if (prev != n_layers) return fail(PSW_ERR_SHAPE, "net_create: last stage_end must equal n_layers");
+    net->stage_np.assign(n_stages, 0);
+    net->poff.assign(n_layers, 0);
+    net->pcount.assign(n_layers, 0);
+    net->bn_off.assign(n_layers, -1);
+    std::vector<int> consumers(n_layers + 1, 0);
+    for (int i = 0; i < n_layers; ++i) {
+        const psw_layer& o = net->ops[i];
+        if (o.in0 < 0 || o.in0 > i) return fail(PSW_ERR_SHAPE, "op %d: in0 %d is not an earlier tensor", i, o.in0);
+        if (o.in1 > i || (o.in1 >= 0 && o.kind != PSW_OP_BN))
+            return fail(PSW_ERR_SHAPE, "op %d: in1 only allowed on BN and must be earlier", i);
+        const Tensor a = net->t[o.in0];
+        Tensor out = a;
+        int64_t np = 0;
+        consumers[o.in0]++;
+        if (o.in1 >= 0) consumers[o.in1]++;
+        switch (o.kind) {
+        case PSW_OP_CONV: {
+            if (a.c != o.cin || o.cout <= 0 || o.k <= 0 || o.stride <= 0 || o.pad < 0)
+                return fail(PSW_ERR_SHAPE, "op %d: conv channels/geometry do not match its input", i);
+            psw::ConvShape cs;
+            if (check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, prec, &cs)) return PSW_ERR_SHAPE;
+            out = Tensor{a.n, o.cout, cs.p, cs.q};
+            np = (int64_t)o.cout * o.cin * o.k * o.k + ((o.flags & PSW_F_BIAS) ? o.cout : 0);
+            break;
+        }
+        case PSW_OP_BN:
+            if (a.c != o.cin || o.cout != o.cin) return fail(PSW_ERR_SHAPE, "op %d: bn channels", i);
+            if (o.in1 >= 0) {
+                const Tensor r = net->t[o.in1];
+                if (r.n != a.n || check_residual(a.c, a.h, a.w, (const float*)1, r.c, r.h, r.w))
+                    return fail(PSW_ERR_SHAPE, "op %d: residual shape does not fit", i);
+            }
+            np = 2 * (int64_t)o.cin;
+            net->bn_off[i] = net->bn_channels;
+            net->bn_channels += o.cin;
+            break;
+        case PSW_OP_MAXPOOL:
+            if (o.k <= 0 || o.stride != o.k || o.k > a.h || o.k > a.w)
+                return fail(PSW_ERR_UNSUPPORTED, "op %d: max-pool needs k == stride <= input", i);
+            out.h = (a.h - o.k) / o.stride + 1;
+            out.w = (a.w - o.k) / o.stride + 1;
+            break;
+        case PSW_OP_GAVG:
+            out.h = out.w = 1;
+            break;
+        case PSW_OP_FC:
+            if ((int64_t)a.c * a.h * a.w != o.cin || o.cout <= 0)
+                return fail(PSW_ERR_SHAPE, "op %d: fc input features %lld != cin %d", i, (long long)a.c * a.h * a.w,
+                            o.cin);
+            out = Tensor{a.n, o.cout, 1, 1};
+            np = (int64_t)o.cout * o.cin + ((o.flags & PSW_F_BIAS) ? o.cout : 0);
+            break;
+        default:
+            return fail(PSW_ERR_UNSUPPORTED, "op %d: unknown kind %d", i, o.kind);
+        }
+        const int s = net->stage_of[i];
+        net->poff[i] = net->stage_np[s];
+        net->pcount[i] = np;
+        net->stage_np[s] += np;
+        net->t[i + 1] = out;
+    }
+    for (int i = 1; i < n_layers; ++i)
+        if (consumers[i] == 0) return fail(PSW_ERR_SHAPE, "tensor %d is never used", i);
+    const Tensor lg = net->t[n_layers];
+    if (lg.h != 1 || lg.w != 1) return fail(PSW_ERR_SHAPE, "the last operation must produce [batch, classes] logits");
+    // gradient write modes in reverse order: the first writer overwrites
+    std::vector<char> written(n_layers + 1, 0);
+    net->grad_accum.assign(2 * n_layers, 0);
+    for (int i = n_layers - 1; i >= 0; --i) {
+        const psw_layer& o = net->ops[i];
+        if (o.kind == PSW_OP_BN && o.in1 >= 0 && o.in1 > 0) {
+            net->grad_accum[2 * i + 1] = written[o.in1];
+            written[o.in1] = 1;
+        }
+        if (o.in0 > 0) {
+            net->grad_accum[2 * i] = written[o.in0];
+            if (o.kind == PSW_OP_BN && written[o.in0])
+                return fail(PSW_ERR_UNSUPPORTED, "op %d: a BN input must have no other consumer", i);
+            written[o.in0] = 1;
+        }
+    }
+    // parameter and ring offsets
+    int64_t fo = 0, ro = 0;
+    for (int s = 0; s < n_stages; ++s) {
+        net->flat_off.push_back(fo);
+        net->ring_off.push_back(ro);
+        fo += net->stage_np[s];
+        ro += net->stage_np[s] * net->ring_depth[s];
+    }
+    // arena: activations, gradients, saved BN stats / argmax, workspace
+    size_t off = 0;
+    net->act_off.assign(n_layers + 1, 0);
+    net->grad_off.assign(n_layers + 1, 0);
+    net->save_off.assign(n_layers, 0);
+    for (int i = 1; i <= n_layers; ++i) {
+        net->act_off[i] = off;
+        off = align256(off + (size_t)net->t[i].numel() * sizeof(float));
+    }
+    for (int i = 1; i <= n_layers; ++i) {
+        net->grad_off[i] = off;
+        off = align256(off + (size_t)net->t[i].numel() * sizeof(float));
+    }
+    size_t ws = 0;
+    for (int i = 0; i < n_layers; ++i) {
+        const psw_layer& o = net->ops[i];
+        const Tensor a = net->t[o.in0];
+        if (o.kind == PSW_OP_BN) {
+            net->save_off[i] = off;
+            off = align256(off + 2 * (size_t)o.cin * sizeof(float));
+            ws = std::max(ws, psw::bn_ws_bytes(a.n, a.c, a.h, a.w));
+        } else if (o.kind == PSW_OP_MAXPOOL) {
+            net->save_off[i] = off;
+            off = align256(off + (size_t)net->t[i + 1].numel() * sizeof(int32_t));
+        } else if (o.kind == PSW_OP_CONV) {
+            psw::ConvShape cs;
+            check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, prec, &cs);
+            ws = std::max(ws, psw::conv_bwd_weight_ws_bytes(cs, prec == PSW_BF16));
+        } else if (o.kind == PSW_OP_FC) {
+            ws = std::max(ws, psw::fc_bwd_ws_bytes(a.n, o.cin, o.cout));
+        }
+    }
+    net->ws_off = off;
+    net->ws_bytes = align256(ws);
+    off += net->ws_bytes;
+    net->arena_bytes = off;
+    g_err.clear();
+    return PSW_OK;
+}
+
+int check_staleness(const psw_net* net, int64_t t, const int32_t* staleness)
+{
+    if (!staleness) return fail(PSW_ERR_NULL, "staleness array is required");
+    if (t < 0) return fail(PSW_ERR_STEP_ORDER, "t must be >= 0");
+    for (int s = 0; s < net->S; ++s)
+        if (staleness[s] < 0 || staleness[s] >= net->ring_depth[s])
+            return fail(PSW_ERR_STALENESS, "stage %d: staleness %d outside [0, ring_depth-1 = %d]", s, staleness[s],
+                        net->ring_depth[s] - 1);
+    return PSW_OK;
+}
+
+inline int64_t fwd_version(int64_t t, int d) { return t - d > 0 ? t - d : 0; }
+
+float* slot_ptr(const psw_net* net, int s, int64_t version)
+{
+    const int64_t slot = version % net->ring_depth[s];
+    return net->ring + net->ring_off[s] + slot * net->stage_np[s];
+}
+
+}  // namespace
+
+extern "C" {
+
+int psw_net_create(const psw_layer* layers, int n_layers, int batch, int c0, int h0, int w0, const int32_t* stage_end,
+                   int n_stages, const int32_t* ring_depth, int prec, psw_net** out)
+{
+    if (!out) return fail(PSW_ERR_NULL, "net_create: out is NULL");
+    *out = nullptr;
+    psw_net* net = new psw_net();
+    int rc = build_net(net, layers, n_layers, batch, c0, h0, w0, stage_end, n_stages, ring_depth, prec);
+    if (rc) {
+        delete net;
+        return rc;
+    }
+    *out = net;
+    return PSW_OK;
+}
+
+void psw_net_destroy(psw_net* net) { delete net; }
+
+int psw_net_sizes(const psw_net* net, int64_t* stage_params, int64_t* ring_floats, int64_t* n_params,
+                  int64_t* bn_channels, int64_t* arena_bytes)
+{
+    if (!net) return fail(PSW_ERR_NULL, "net_sizes: net is NULL");
+    int64_t rf = 0, np = 0;
+    for (int s = 0; s < net->S; ++s) {
+        if (stage_params) stage_params[s] = net->stage_np[s];
+        rf += net->stage_np[s] * net->ring_depth[s];
+        np += net->stage_np[s];
+    }
+    if (ring_floats) *ring_floats = rf;
+    if (n_params) *n_params = np;
+    if (bn_channels) *bn_channels = net->bn_channels;
+    if (arena_bytes) *arena_bytes = (int64_t)net->arena_bytes;
+    return PSW_OK;
+}
+
+int psw_net_bind(psw_net* net, float* ring, float* momentum, float* grad, float* run_mean, float* run_var, void* arena,
+                 size_t arena_bytes)
+{
+    if (!net || !ring || !momentum || !grad || !arena) return fail(PSW_ERR_NULL, "net_bind: required pointer is NULL");
+    if ((run_mean == nullptr) != (run_var == nullptr))
+        return fail(PSW_ERR_NULL, "net_bind: run_mean and run_var must both be set or both NULL");
+    if (arena_bytes < net->arena_bytes)
+        return fail(PSW_ERR_WORKSPACE, "net_bind: arena %zu < %zu bytes", arena_bytes, net->arena_bytes);
+    if (((uintptr_t)arena) % 256 != 0) return fail(PSW_ERR_SHAPE, "net_bind: arena must be 256-byte aligned");
+    net->ring = ring;
+    net->momentum = momentum;
+    net->grad = grad;
+    net->run_mean = run_mean;
+    net->run_var = run_var;
+    net->arena = (char*)arena;
+    net->bound = true;
+    return PSW_OK;
+}
+
+int psw_net_set_step(psw_net* net, int64_t t)
+{
+    if (!net) return fail(PSW_ERR_NULL, "net_set_step: net is NULL");
+    if (t < 0) return fail(PSW_ERR_STEP_ORDER, "net_set_step: t < 0");
+    net->next_t = t;
+    return PSW_OK;
+}
+
+int psw_net_slot(const psw_net* net, int stage, int64_t version, float** params)
+{
+    if (!net || !params) return fail(PSW_ERR_NULL, "net_slot: required pointer is NULL");
+    if (stage < 0 || stage >= net->S) return fail(PSW_ERR_SHAPE, "net_slot: stage %d out of range", stage);
+    if (!net->bound) return fail(PSW_ERR_STATE, "net_slot: net is not bound");
+    const int64_t newest = net->next_t;
+    if (version < 0 || version > newest || version <= newest - net->ring_depth[stage])
+        return fail(PSW_ERR_STALENESS, "net_slot: version %lld of stage %d is not resident (newest %lld, depth %d)",
+                    (long long)version, stage, (long long)newest, net->ring_depth[stage]);
+    *params = slot_ptr(net, stage, version);
+    return PSW_OK;
+}
+
+int psw_net_param_offset(const psw_net* net, int op, int* stage, int64_t* offset, int64_t* count)
+{
+    if (!net) return fail(PSW_ERR_NULL, "net_param_offset: net is NULL");
+    if (op < 0 || op >= (int)net->ops.size()) return fail(PSW_ERR_SHAPE, "net_param_offset: op out of range");
+    if (stage) *stage = net->stage_of[op];
+    if (offset) *offset = net->poff[op];
+    if (count) *count = net->pcount[op];
+    return PSW_OK;
+}
+
+int psw_net_plan(const psw_net* net, int64_t t, const int32_t* staleness, psw_launch* out, int cap, int* n_out)
+{
+    if (!net || !n_out) return fail(PSW_ERR_NULL, "net_plan: required pointer is NULL");
+    int rc = check_staleness(net, t, staleness);
+    if (rc) return rc;
+    int n = 0;
+    auto rec = [&](int op, int what, int s, int64_t v) {
+        if (out && n < cap) out[n] = psw_launch{op, what, s, v};
+        ++n;
+    };
+    const int L = (int)net->ops.size();
+    for (int i = 0; i < L; ++i) {
+        const psw_layer& o = net->ops[i];
+        const int s = net->stage_of[i];
+        const int64_t r = fwd_version(t, staleness[s]);
+        switch (o.kind) {
+        case PSW_OP_CONV: rec(i, PSW_PLAN_CONV_FWD, s, r); break;
+        case PSW_OP_BN: rec(i, PSW_PLAN_BN_FWD, s, r); break;
+        case PSW_OP_MAXPOOL:
+        case PSW_OP_GAVG: rec(i, PSW_PLAN_POOL_FWD, s, -1); break;
+        case PSW_OP_FC: rec(i, PSW_PLAN_FC_FWD, s, r); break;
+        }
+    }
+    rec(L - 1, PSW_PLAN_LOSS, net->stage_of[L - 1], -1);
+    for (int i = L - 1; i >= 0; --i) {
+        const psw_layer& o = net->ops[i];
+        const int s = net->stage_of[i];
+        switch (o.kind) {
+        case PSW_OP_CONV:
+            if (o.flags & PSW_F_RELU) rec(i, PSW_PLAN_RELU_MASK, s, -1);
+            rec(i, PSW_PLAN_CONV_BWD_WEIGHT, s, -1);
+            if (o.in0 > 0) rec(i, PSW_PLAN_CONV_BWD_DATA, s, t);
+            break;
+        case PSW_OP_BN: rec(i, PSW_PLAN_BN_BWD, s, t); break;
+        case PSW_OP_MAXPOOL:
+        case PSW_OP_GAVG:
+            if (o.in0 > 0) rec(i, PSW_PLAN_POOL_BWD, s, -1);
+            break;
+        case PSW_OP_FC:
+            if (o.flags & PSW_F_RELU) rec(i, PSW_PLAN_RELU_MASK, s, -1);
+            rec(i, PSW_PLAN_FC_BWD, s, t);
+            break;
+        }
+    }
+    for (int s = 0; s < net->S; ++s) rec(-1, PSW_PLAN_SGD, s, t);
+    *n_out = n;
+    return PSW_OK;
+}
+
+int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const float* lr, float mom, float wd,
+                   int nesterov, const float* x, const int32_t* labels, float* loss_out, int32_t* versions_out,
+                   void* stream)
+{
+    if (!net) return fail(PSW_ERR_NULL, "stage_step: net is NULL");
+    if (!net->bound) return fail(PSW_ERR_STATE, "stage_step: net is not bound");
+    if (!lr || !x || !labels || !loss_out) return fail(PSW_ERR_NULL, "stage_step: required pointer is NULL");
+    int rc = check_staleness(net, t, staleness);
+    if (rc) return rc;
+    if (t != net->next_t)
+        return fail(PSW_ERR_STEP_ORDER, "stage_step: expected t = %lld, got %lld", (long long)net->next_t, (long long)t);
+    hipStream_t st = S(stream);
+    const int L = (int)net->ops.size();
+    const int bf16 = net->prec == PSW_BF16;
+    char* A = net->arena;
+    auto act = [&](int id) -> float* { return id == 0 ? (float*)x : (float*)(A + net->act_off[id]); };
+    auto grd = [&](int id) -> float* { return (float*)(A + net->grad_off[id]); };
+    void* ws = A + net->ws_off;
+    const size_t wsb = net->ws_bytes;
+    std::vector<int64_t> rv(net->S);
+    for (int s = 0; s < net->S; ++s) rv[s] = fwd_version(t, staleness[s]);
+    auto wfwd = [&](int i) { return slot_ptr(net, net->stage_of[i], rv[net->stage_of[i]]) + net->poff[i]; };
+    auto wcur = [&](int i) { return slot_ptr(net, net->stage_of[i], t) + net->poff[i]; };
+    auto gptr = [&](int i) { return net->grad + net->flat_off[net->stage_of[i]] + net->poff[i]; };
+    hipError_t e = hipSuccess;
+    // kind of the launcher being issued, for psw_net_profile
+    int kind = PSW_PROF_OTHER;
+#define PSW_TRY(expr, what)                                                   \
+    do {                                                                      \
+        hipEvent_t ea = nullptr, eb = nullptr;                                \
+        if (net->profiling) {                                                 \
+            ea = net->next_event();                                           \
+            eb = net->next_event();                                           \
+            if (ea && eb) (void)hipEventRecord(ea, st);                       \
+        }                                                                     \
+        e = (expr);                                                           \
+        if (e != hipSuccess) return hip_check(e, what);                       \
+        if (ea && eb) {                                                       \
+            (void)hipEventRecord(eb, st);                                     \
+            net->prof.push_back(psw_net::ProfRec{kind, ea, eb});              \
+        }                                                                     \
+    } while (0)
+
+    // ---- forward: every stage with its (possibly stale) version r_s ----
+    for (int i = 0; i < L; ++i) {
+        const psw_layer& o = net->ops[i];
+        const Tensor a = net->t[o.in0];
+        const float* W = wfwd(i);
+        switch (o.kind) {
+        case PSW_OP_CONV: {
+            psw::ConvShape cs;
+            check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, net->prec, &cs);
+            const float* b = (o.flags & PSW_F_BIAS) ? W + (int64_t)o.cout * o.cin * o.k * o.k : nullptr;
+            kind = PSW_PROF_CONV_FWD;
+            PSW_TRY(psw::conv_fwd(cs, act(o.in0), W, b, (o.flags & PSW_F_RELU) != 0, act(i + 1), bf16, st), "conv_fwd");
+            break;
+        }
+        case PSW_OP_BN: {
+            const Tensor r = o.in1 >= 0 ? net->t[o.in1] : Tensor{0, 0, 0, 0};
+            float* save = (float*)(A + net->save_off[i]);
+            float* rm = net->run_mean ? net->run_mean + net->bn_off[i] : nullptr;
+            float* rvv = net->run_var ? net->run_var + net->bn_off[i] : nullptr;
+            kind = PSW_PROF_BN_FWD;
+            PSW_TRY(psw::bn_fwd(a.n, a.c, a.h, a.w, act(o.in0), W, W + o.cin, o.in1 >= 0 ? act(o.in1) : nullptr, r.c,
+                                r.h, r.w, (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, act(i + 1), save, save + o.cin, rm,
+                                rvv, ws, wsb, st),
+                    "bn_fwd");
+            break;
+        }
+        case PSW_OP_MAXPOOL:
+            kind = PSW_PROF_POOL;
+            PSW_TRY(psw::maxpool_fwd(a.n, a.c, a.h, a.w, o.k, o.stride, act(o.in0), act(i + 1),
+                                     (int32_t*)(A + net->save_off[i]), st),
+                    "maxpool_fwd");
+            break;
+        case PSW_OP_GAVG:
+            kind = PSW_PROF_POOL;
+            PSW_TRY(psw::gavgpool_fwd(a.n, a.c, a.h, a.w, act(o.in0), act(i + 1), st), "gavgpool_fwd");
+            break;
+        case PSW_OP_FC: {
+            const float* b = (o.flags & PSW_F_BIAS) ? W + (int64_t)o.cout * o.cin : nullptr;
+            kind = PSW_PROF_FC;
+            PSW_TRY(psw::fc_fwd(a.n, o.cin, o.cout, act(o.in0), W, b, (o.flags & PSW_F_RELU) != 0, act(i + 1), bf16, st),
+                    "fc_fwd");
+            break;
+        }
+        }
+    }
+    // ---- loss ----
+    const Tensor lg = net->t[L];
+    kind = PSW_PROF_LOSS;
+    PSW_TRY(psw::softmax_xent(lg.n, lg.c, act(L), labels, loss_out, grd(L), st), "softmax_xent");
+    // ---- backward: weight grads from saved activations, data grads with version t ----
+    for (int i = L - 1; i >= 0; --i) {
+        const psw_layer& o = net->ops[i];
+        const Tensor a = net->t[o.in0];
+        const Tensor y = net->t[i + 1];
+        float* g = grd(i + 1);
+        float* din = o.in0 > 0 ? grd(o.in0) : nullptr;
+        const int acc0 = net->grad_accum[2 * i];
+        switch (o.kind) {
+        case PSW_OP_CONV: {
+            psw::ConvShape cs;
+            check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, net->prec, &cs);
+            kind = PSW_PROF_OTHER;
+            if (o.flags & PSW_F_RELU) PSW_TRY(psw::relu_mask(y.numel(), act(i + 1), g, st), "relu_mask");
+            float* dw = gptr(i);
+            float* db = (o.flags & PSW_F_BIAS) ? dw + (int64_t)o.cout * o.cin * o.k * o.k : nullptr;
+            kind = PSW_PROF_CONV_BWD_WEIGHT;
+            PSW_TRY(psw::conv_bwd_weight(cs, act(o.in0), g, dw, db, bf16, ws, wsb, st), "conv_bwd_weight");
+            kind = PSW_PROF_CONV_BWD_DATA;
+            if (din) PSW_TRY(psw::conv_bwd_data(cs, wcur(i), g, din, acc0, bf16, st), "conv_bwd_data");
+            break;
+        }
+        case PSW_OP_BN: {
+            const float* save = (const float*)(A + net->save_off[i]);
+            const Tensor r = o.in1 >= 0 ? net->t[o.in1] : Tensor{0, 0, 0, 0};
+            float* dres = o.in1 > 0 ? grd(o.in1) : nullptr;
+            float* dg = gptr(i);
+            if (!din) return fail(PSW_ERR_UNSUPPORTED, "op %d: BN directly on the input batch", i);
+            kind = PSW_PROF_BN_BWD;
+            PSW_TRY(psw::bn_bwd(a.n, a.c, a.h, a.w, g, act(i + 1), act(o.in0), wcur(i), save, save + o.cin,
+                                (o.flags & PSW_F_RELU) != 0, din, dg, dg + o.cin, dres, r.c, r.h, r.w,
+                                net->grad_accum[2 * i + 1], ws, wsb, st),
+                    "bn_bwd");
+            break;
+        }
+        case PSW_OP_MAXPOOL:
+            if (din)
+                kind = PSW_PROF_POOL;
+                PSW_TRY(psw::maxpool_bwd(a.n, a.c, a.h, a.w, o.k, o.stride, g, (const int32_t*)(A + net->save_off[i]),
+                                         din, acc0, st),
+                        "maxpool_bwd");
+            break;
+        case PSW_OP_GAVG:
+            kind = PSW_PROF_POOL;
+            if (din) PSW_TRY(psw::gavgpool_bwd(a.n, a.c, a.h, a.w, g, din, acc0, st), "gavgpool_bwd");
+            break;
+        case PSW_OP_FC: {
+            kind = PSW_PROF_OTHER;
+            if (o.flags & PSW_F_RELU) PSW_TRY(psw::relu_mask(y.numel(), act(i + 1), g, st), "relu_mask");
+            float* dw = gptr(i);
+            float* db = (o.flags & PSW_F_BIAS) ? dw + (int64_t)o.cout * o.cin : nullptr;
+            kind = PSW_PROF_FC;
+            PSW_TRY(psw::fc_bwd(a.n, o.cin, o.cout, act(o.in0), wcur(i), g, din, acc0, dw, db, bf16, ws, wsb, st),
+                    "fc_bwd");
+            break;
+        }
+        }
+    }
+    // ---- update: version t+1 of every stage ----
+    for (int s = 0; s < net->S; ++s) {
+        const float* win = slot_ptr(net, s, t);
+        float* wout = slot_ptr(net, s, t + 1);
+        kind = PSW_PROF_SGD;
+        PSW_TRY(psw::sgd_momentum(net->stage_np[s], win, wout, net->momentum + net->flat_off[s],
+                                  net->grad + net->flat_off[s], lr[s], mom, wd, nesterov, st),
+                "sgd");
+    }
+#undef PSW_TRY
+    if (versions_out)
+        for (int s = 0; s < net->S; ++s) versions_out[s] = (int32_t)rv[s];
+    net->next_t = t + 1;
+    return PSW_OK;
+}
+
+int psw_net_profile(psw_net* net, int enable)
+{
+    if (!net) return fail(PSW_ERR_NULL, "net_profile: net is NULL");
+    net->profiling = enable != 0;
+    net->prof.clear();
+    net->ev_used = 0;
+    return PSW_OK;
+}
+
+int psw_net_profile_read(psw_net* net, int n_kinds, double* ms, int64_t* launches)
+{
+    if (!net || !ms || !launches) return fail(PSW_ERR_NULL, "net_profile_read: required pointer is NULL");
+    for (int k = 0; k < n_kinds; ++k) {
+        ms[k] = 0.0;
+        launches[k] = 0;
+    }
+    for (const auto& r : net->prof) {
+        hipError_t e = hipEventSynchronize(r.b);
+        if (e != hipSuccess) return hip_check(e, "net_profile_read");
+        float t = 0.f;
+        e = hipEventElapsedTime(&t, r.a, r.b);
+        if (e != hipSuccess) return hip_check(e, "net_profile_read");
+        if (r.kind >= 0 && r.kind < n_kinds) {
+            ms[r.kind] += t;
+            launches[r.kind] += 1;
+        }
+    }
+    net->prof.clear();
+    net->ev_used = 0;
+    return PSW_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,327 @@
+// Convolution forward / backward-data / backward-weight as implicit GEMMs on
+// CDNA4 matrix cores (gfx950).
+//
+// The three passes of a conv layer (Sec. 2 of the paper: x^(l) from x^(l-1)
+// and W^(l); delta^(l-1) from delta^(l) and W^(l); dE/dW^(l) from x^(l-1) and
+// delta^(l)) are each one GEMM  C[M][N] = sum_k A(m,k) B(k,n)  whose operands
+// are gathered on the fly from the NCHW tensors:
+//
+//   forward      M = K_out   N = n*P*Q (output pixels)  Kd = C*R*S
+//                A = W[m][(c,r,s)],  B = x[img][c][p*st+r-pad][q*st+s-pad]
+//   backward-data M = C      N = n*H*W (input pixels)   Kd = K_out*R*S
+//                A = W[k][m][r][s],  B = dy[img][k][(h+pad-r)/st][(w+pad-s)/st]
+//                (zero where the division is inexact or out of range)
+//   backward-weight M = K_out N = C*R*S                 Kd = n*P*Q (split over
+//                grid.z, partial sums reduced in a fixed order)
+//                A = dy[img][m][p][q],  B = x[img][c][p*st+r-pad][q*st+s-pad]
+//
+// Output rows (M) are channels and columns (N) pixels, so the 16 lanes that
+// share an MFMA output row write 16 consecutive pixels of one NCHW channel.
+// Tiles are staged through LDS; fp32 uses v_mfma_f32_16x16x4_f32, the bf16
+// mode rounds both operands to bfloat16 (nearest even) when staging and uses
+// v_mfma_f32_16x16x32_bf16 with fp32 accumulation.
+#include "internal.h"
+
+namespace psw {
+namespace {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef unsigned short v8us __attribute__((ext_vector_type(8)));
+
+enum { FWD = 0, BWD_DATA = 1, BWD_WEIGHT = 2 };
+
+struct IgArgs {
+    const float* A;
+    const float* B;
+    float* C;
+    const float* bias;
+    int n, c, h, w, k, r, s, stride, pad, p, q;
+    int M, N, Kd;
+    int kchunk;  // reduction length handled by one grid.z slice (multiple of BK)
+    int relu, accumulate;
+};
+
+__device__ __forceinline__ float round_bf16(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) != 0x7f800000u) u += 0x7fffu + ((u >> 16) & 1u);
+    return __uint_as_float(u & 0xffff0000u);
+}
+
+template <int PASS>
+__device__ __forceinline__ float fetch_a(const IgArgs& a, int m, int k)
+{
+    const int RS = a.r * a.s;
+    if (PASS == FWD) return a.A[(size_t)m * a.Kd + k];
+    if (PASS == BWD_DATA) {
+        const int ko = k / RS, rs = k - ko * RS;
+        return a.A[((size_t)ko * a.c + m) * RS + rs];
+    }
+    const int PQ = a.p * a.q;
+    const int img = k / PQ, pq = k - img * PQ;
+    return a.A[((size_t)img * a.k + m) * PQ + pq];
+}
+
+template <int PASS>
+__device__ __forceinline__ float fetch_b(const IgArgs& a, int k, int n)
+{
+    const int RS = a.r * a.s;
+    if (PASS == FWD || PASS == BWD_WEIGHT) {
+        int c, rs, img, pq;
+        const int PQ = a.p * a.q;
+        if (PASS == FWD) {
+            c = k / RS; rs = k - c * RS;
+            img = n / PQ; pq = n - img * PQ;
+        } else {
+            img = k / PQ; pq = k - img * PQ;
+            c = n / RS; rs = n - c * RS;
+        }
+        const int r = rs / a.s, s = rs - r * a.s;
+        const int p = pq / a.q, q = pq - p * a.q;
+        const int ih = p * a.stride + r - a.pad, iw = q * a.stride + s - a.pad;
+        if (ih < 0 || ih >= a.h || iw < 0 || iw >= a.w) return 0.f;
+        return a.B[(((size_t)img * a.c + c) * a.h + ih) * a.w + iw];
+    }
+    // backward data: gather dy
+    const int ko = k / RS, rs = k - ko * RS;
+    const int r = rs / a.s, s = rs - r * a.s;
+    const int HW = a.h * a.w;
+    const int img = n / HW, hw = n - img * HW;
+    const int hh = hw / a.w, ww = hw - hh * a.w;
+    const int ih = hh + a.pad - r, iw = ww + a.pad - s;
+    if (ih < 0 || iw < 0) return 0.f;
+    const int p = ih / a.stride, q = iw / a.stride;
+    if (p * a.stride != ih || q * a.stride != iw || p >= a.p || q >= a.q) return 0.f;
+    return a.B[(((size_t)img * a.k + ko) * a.p + p) * a.q + q];
+}
+
+// BM x BN block tile, BK reduction slice, WM x WN waves (256 threads total).
+template <int PASS, int BM, int BN, int WM, int WN, bool BF16>
+__global__ __launch_bounds__(256) void igemm_kernel(IgArgs a)
+{
+    constexpr int BK = BF16 ? 32 : 16;
+    constexpr int KSTEP = BF16 ? 32 : 4;
+    constexpr int TM = BM / WM / 16, TN = BN / WN / 16;
+    static_assert(WM * WN == 4, "four waves");
+    static_assert(TM >= 1 && TN >= 1, "tile");
+    __shared__ float As[BK][BM + 4];
+    __shared__ float Bs[BK][BN + 4];
+
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+    const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+    const int kbeg = blockIdx.z * a.kchunk;
+    const int kend = min(a.Kd, kbeg + a.kchunk);
+
+    v4f acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    for (int k0 = kbeg; k0 < kend; k0 += BK) {
+        // stage A: consecutive threads along k
+#pragma unroll
+        for (int e = 0; e < (BM * BK + 255) / 256; ++e) {
+            const int idx = e * 256 + tid;
+            if (idx < BM * BK) {
+                const int kk = idx % BK, mm = idx / BK;
+                const int m = m0 + mm, k = k0 + kk;
+                float v = (m < a.M && k < kend) ? fetch_a<PASS>(a, m, k) : 0.f;
+                As[kk][mm] = BF16 ? round_bf16(v) : v;
+            }
+        }
+        // stage B: along the memory-contiguous index (pixels)
+#pragma unroll
+        for (int e = 0; e < (BN * BK + 255) / 256; ++e) {
+            const int idx = e * 256 + tid;
+            if (idx < BN * BK) {
+                int kk, nn;
+                if (PASS == BWD_WEIGHT) { kk = idx % BK; nn = idx / BK; }
+                else { nn = idx % BN; kk = idx / BN; }
+                const int n = n0 + nn, k = k0 + kk;
+                float v = (n < a.N && k < kend) ? fetch_b<PASS>(a, k, n) : 0.f;
+                Bs[kk][nn] = BF16 ? round_bf16(v) : v;
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int ks = 0; ks < BK; ks += KSTEP) {
+            if constexpr (!BF16) {
+                float af[TM], bfr[TN];
+#pragma unroll
+                for (int i = 0; i < TM; ++i) af[i] = As[ks + (lane >> 4)][wm * (BM / WM) + i * 16 + (lane & 15)];
+#pragma unroll
+                for (int j = 0; j < TN; ++j) bfr[j] = Bs[ks + (lane >> 4)][wn * (BN / WN) + j * 16 + (lane & 15)];
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i], bfr[j], acc[i][j], 0, 0, 0);
+            } else {
+                v8bf af[TM], bfr[TN];
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+                    v8us u;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        u[e] = (unsigned short)(__float_as_uint(
+                                   As[ks + 8 * (lane >> 4) + e][wm * (BM / WM) + i * 16 + (lane & 15)]) >> 16);
+                    af[i] = __builtin_bit_cast(v8bf, u);
+                }
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    v8us u;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        u[e] = (unsigned short)(__float_as_uint(
+                                   Bs[ks + 8 * (lane >> 4) + e][wn * (BN / WN) + j * 16 + (lane & 15)]) >> 16);
+                    bfr[j] = __builtin_bit_cast(v8bf, u);
+                }
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+            }
+        }
+        __syncthreads();
+    }
+
+    // epilogue: lane holds rows 4*(lane/16)+v, column lane%16 of each 16x16 tile
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int n = n0 + wn * (BN / WN) + j * 16 + (lane & 15);
+            if (n >= a.N) continue;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int m = m0 + wm * (BM / WM) + i * 16 + 4 * (lane >> 4) + v;
+                if (m >= a.M) continue;
+                float val = acc[i][j][v];
+                if (PASS == FWD) {
+                    const int PQ = a.p * a.q;
+                    const int img = n / PQ, pq = n - img * PQ;
+                    if (a.bias) val += a.bias[m];
+                    if (a.relu) val = fmaxf(val, 0.f);
+                    a.C[((size_t)img * a.M + m) * PQ + pq] = val;
+                } else if (PASS == BWD_DATA) {
+                    const int HW = a.h * a.w;
+                    const int img = n / HW, hw = n - img * HW;
+                    float* dst = a.C + ((size_t)img * a.M + m) * HW + hw;
+                    *dst = a.accumulate ? *dst + val : val;
+                } else {
+                    a.C[((size_t)blockIdx.z * a.M + m) * a.N + n] = val;
+                }
+            }
+        }
+}
+
+// dw[i] = sum_z part[z][i], z in increasing order (deterministic)
+__global__ void reduce_splits(const float* part, int splits, int64_t count, float* out)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= count) return;
+    float acc = 0.f;
+    for (int z = 0; z < splits; ++z) acc += part[(int64_t)z * count + i];
+    out[i] = acc;
+}
+
+template <int PASS, bool BF16>
+hipError_t launch(const IgArgs& a, int splits, hipStream_t st)
+{
+    const int M = a.M;
+    dim3 block(256);
+    if (M <= 16) {
+        dim3 grid((a.N + 127) / 128, (M + 15) / 16, splits);
+        hipLaunchKernelGGL((igemm_kernel<PASS, 16, 128, 1, 4, BF16>), grid, block, 0, st, a);
+    } else if (M <= 32) {
+        dim3 grid((a.N + 127) / 128, (M + 31) / 32, splits);
+        hipLaunchKernelGGL((igemm_kernel<PASS, 32, 128, 1, 4, BF16>), grid, block, 0, st, a);
+    } else {
+        dim3 grid((a.N + 127) / 128, (M + 63) / 64, splits);
+        hipLaunchKernelGGL((igemm_kernel<PASS, 64, 128, 2, 2, BF16>), grid, block, 0, st, a);
+    }
+    return hipGetLastError();
+}
+
+IgArgs make_args(const ConvShape& cs)
+{
+    IgArgs a{};
+    a.n = cs.n; a.c = cs.c; a.h = cs.h; a.w = cs.w;
+    a.k = cs.k; a.r = cs.r; a.s = cs.s;
+    a.stride = cs.stride; a.pad = cs.pad; a.p = cs.p; a.q = cs.q;
+    return a;
+}
+
+int wgrad_splits(const ConvShape& cs, int bf16)
+{
+    const int BK = bf16 ? 32 : 16;
+    const int M = cs.k, N = cs.c * cs.r * cs.s;
+    const int tiles = ((N + 127) / 128) * ((M + (M <= 16 ? 15 : M <= 32 ? 31 : 63)) / (M <= 16 ? 16 : M <= 32 ? 32 : 64));
+    const int64_t Kd = (int64_t)cs.n * cs.p * cs.q;
+    int z = 1024 / (tiles > 0 ? tiles : 1);
+    if (z < 1) z = 1;
+    const int64_t max_z = (Kd + 4 * BK - 1) / (4 * BK);  // at least 4 BK slices per split
+    if (z > max_z) z = (int)max_z;
+    if (z < 1) z = 1;
+    return z;
+}
+
+}  // namespace
+
+hipError_t conv_fwd(const ConvShape& cs, const float* x, const float* w, const float* bias, int relu, float* y,
+                    int bf16, hipStream_t st)
+{
+    IgArgs a = make_args(cs);
+    a.A = w; a.B = x; a.C = y; a.bias = bias; a.relu = relu;
+    a.M = cs.k; a.N = cs.n * cs.p * cs.q; a.Kd = cs.c * cs.r * cs.s;
+    a.kchunk = ((a.Kd + 31) / 32) * 32;
+    return bf16 ? launch<FWD, true>(a, 1, st) : launch<FWD, false>(a, 1, st);
+}
+
+hipError_t conv_bwd_data(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate, int bf16,
+                         hipStream_t st)
+{
+    IgArgs a = make_args(cs);
+    a.A = w; a.B = dy; a.C = dx; a.accumulate = accumulate;
+    a.M = cs.c; a.N = cs.n * cs.h * cs.w; a.Kd = cs.k * cs.r * cs.s;
+    a.kchunk = ((a.Kd + 31) / 32) * 32;
+    return bf16 ? launch<BWD_DATA, true>(a, 1, st) : launch<BWD_DATA, false>(a, 1, st);
+}
+
+size_t conv_bwd_weight_ws_bytes(const ConvShape& cs, int bf16)
+{
+    const int z = wgrad_splits(cs, bf16);
+    const size_t mn = (size_t)cs.k * cs.c * cs.r * cs.s;
+    size_t bytes = (size_t)z * mn * sizeof(float);
+    bytes += channel_sum_ws_bytes(cs.n, cs.k, cs.p * cs.q);
+    return bytes;
+}
+
+hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy, float* dw, float* db, int bf16,
+                           void* ws, size_t ws_bytes, hipStream_t st)
+{
+    const int z = wgrad_splits(cs, bf16);
+    const int BK = bf16 ? 32 : 16;
+    IgArgs a = make_args(cs);
+    a.A = dy; a.B = x; a.C = (float*)ws;
+    a.M = cs.k; a.N = cs.c * cs.r * cs.s; a.Kd = cs.n * cs.p * cs.q;
+    const int64_t per = ((int64_t)a.Kd + z - 1) / z;
+    a.kchunk = (int)(((per + BK - 1) / BK) * BK);
+    const int zz = (int)(((int64_t)a.Kd + a.kchunk - 1) / a.kchunk);
+    const size_t mn = (size_t)a.M * a.N;
+    if (ws_bytes < conv_bwd_weight_ws_bytes(cs, bf16)) return hipErrorInvalidValue;
+    hipError_t e = bf16 ? launch<BWD_WEIGHT, true>(a, zz, st) : launch<BWD_WEIGHT, false>(a, zz, st);
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(reduce_splits, dim3((unsigned)((mn + 255) / 256)), dim3(256), 0, st, (const float*)ws, zz,
+                       (int64_t)mn, dw);
+    e = hipGetLastError();
+    if (e != hipSuccess || !db) return e;
+    char* rest = (char*)ws + (size_t)z * mn * sizeof(float);
+    return channel_sum(cs.n, cs.k, cs.p * cs.q, dy, db, rest, channel_sum_ws_bytes(cs.n, cs.k, cs.p * cs.q), st);
+}
+
+}  // namespace psw

@@ -1,0 +1,66 @@
+// Internal launchers of libpsw (not part of the public C ABI).
+// All tensors are NCHW float32 in device memory; conv weights are KCRS.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace psw {
+
+struct ConvShape {
+    int n, c, h, w;        // input
+    int k, r, s;           // output channels, kernel
+    int stride, pad;
+    int p, q;              // output spatial size
+};
+
+inline int conv_out_dim(int in, int k, int stride, int pad) { return (in + 2 * pad - k) / stride + 1; }
+
+// ---- convolution (implicit GEMM on MFMA) ----
+hipError_t conv_fwd(const ConvShape& cs, const float* x, const float* w, const float* bias, int relu,
+                    float* y, int bf16, hipStream_t st);
+hipError_t conv_bwd_data(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate,
+                         int bf16, hipStream_t st);
+size_t conv_bwd_weight_ws_bytes(const ConvShape& cs, int bf16);
+hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy, float* dw, float* db,
+                           int bf16, void* ws, size_t ws_bytes, hipStream_t st);
+
+// ---- batch norm (+ residual) (+ ReLU) ----
+size_t bn_ws_bytes(int n, int c, int h, int w);
+hipError_t bn_fwd(int n, int c, int h, int w, const float* y, const float* gamma, const float* beta,
+                  const float* res, int rc, int rh, int rw, int relu, float eps, float momentum, float* z,
+                  float* save_mean, float* save_invstd, float* run_mean, float* run_var, void* ws,
+                  size_t ws_bytes, hipStream_t st);
+hipError_t bn_bwd(int n, int c, int h, int w, const float* dz, const float* z, const float* y,
+                  const float* gamma, const float* save_mean, const float* save_invstd, int relu, float* dy,
+                  float* dgamma, float* dbeta, float* dres, int rc, int rh, int rw, int res_accumulate,
+                  void* ws, size_t ws_bytes, hipStream_t st);
+
+// ---- pooling ----
+hipError_t maxpool_fwd(int n, int c, int h, int w, int k, int stride, const float* x, float* y,
+                       int32_t* argmax, hipStream_t st);
+hipError_t maxpool_bwd(int n, int c, int h, int w, int k, int stride, const float* dy,
+                       const int32_t* argmax, float* dx, int accumulate, hipStream_t st);
+hipError_t gavgpool_fwd(int n, int c, int h, int w, const float* x, float* y, hipStream_t st);
+hipError_t gavgpool_bwd(int n, int c, int h, int w, const float* dy, float* dx, int accumulate,
+                        hipStream_t st);
+
+// ---- fully connected (GEMM on MFMA) ----
+hipError_t fc_fwd(int n, int in, int out, const float* x, const float* w, const float* b, int relu, float* y,
+                  int bf16, hipStream_t st);
+size_t fc_bwd_ws_bytes(int n, int in, int out);
+hipError_t fc_bwd(int n, int in, int out, const float* x, const float* w, const float* dy, float* dx,
+                  int dx_accumulate, float* dw, float* db, int bf16, void* ws, size_t ws_bytes,
+                  hipStream_t st);
+
+// ---- misc ----
+hipError_t relu_mask(int64_t count, const float* z, float* g, hipStream_t st);
+hipError_t softmax_xent(int n, int classes, const float* logits, const int32_t* labels, float* loss,
+                        float* dlogits, hipStream_t st);
+hipError_t sgd_momentum(int64_t count, const float* w_in, float* w_out, float* v, const float* g, float lr,
+                        float mom, float wd, int nesterov, hipStream_t st);
+hipError_t channel_sum(int n, int c, int hw, const float* x, float* out, void* ws, size_t ws_bytes,
+                       hipStream_t st);
+size_t channel_sum_ws_bytes(int n, int c, int hw);
+
+}  // namespace psw

@@ -1,0 +1,674 @@
+// Batch norm (+residual, +ReLU), pooling, fully-connected GEMMs, softmax
+// cross-entropy and the SGD-momentum update for gfx950.
+//
+// Reductions (BN statistics, BN backward sums, bias gradients, the loss) are
+// deterministic: every partial sum has a fixed owner and partials are
+// combined in a fixed order; BN sums are accumulated in double so the
+// E[y^2]-E[y]^2 form loses nothing at these sizes.
+#include "internal.h"
+
+namespace psw {
+namespace {
+
+typedef float v4f __attribute__((ext_vector_type(4)));
+typedef __bf16 v8bf __attribute__((ext_vector_type(8)));
+typedef unsigned short v8us __attribute__((ext_vector_type(8)));
+
+constexpr int kBlock = 256;
+
+__device__ __forceinline__ double wave_sum(double v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_down(v, off, 64);
+    return v;
+}
+
+__device__ __forceinline__ float wave_sum_f(float v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_down(v, off, 64);
+    return v;
+}
+
+// Sum over the block in a fixed order; result valid in thread 0.
+__device__ __forceinline__ double block_sum(double v, double* sh)
+{
+    v = wave_sum(v);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    if (lane == 0) sh[wave] = v;
+    __syncthreads();
+    double t = 0.0;
+    if (threadIdx.x == 0)
+        for (int i = 0; i < (int)(blockDim.x >> 6); ++i) t += sh[i];
+    __syncthreads();
+    return t;
+}
+
+int channel_splits(int n, int c)
+{
+    int sp = (1024 + c - 1) / c;
+    if (sp > n) sp = n;
+    if (sp < 1) sp = 1;
+    return sp;
+}
+
+// ---------------------------------------------------------------- BN -------
+// mode 0: sum y, sum y^2              (forward statistics)
+// mode 1: sum g, sum g*xhat with g = dz*[z>0 if relu]   (backward sums)
+// mode 2: sum x                       (bias gradient; second slot unused)
+__global__ __launch_bounds__(kBlock) void chan_partials(int mode, int n, int c, int hw, int split, const float* x,
+                                                         const float* z, const float* y, const float* mean,
+                                                         const float* invstd, int relu, double* part)
+{
+    __shared__ double sh[kBlock / 64];
+    const int ch = blockIdx.x, sp = blockIdx.y;
+    const int i0 = (int)((int64_t)n * sp / split), i1 = (int)((int64_t)n * (sp + 1) / split);
+    const int64_t total = (int64_t)(i1 - i0) * hw;
+    double s1 = 0.0, s2 = 0.0;
+    const double mu = mode == 1 ? (double)mean[ch] : 0.0;
+    const double is = mode == 1 ? (double)invstd[ch] : 0.0;
+    for (int64_t idx = threadIdx.x; idx < total; idx += kBlock) {
+        const int img = i0 + (int)(idx / hw);
+        const int off = (int)(idx - (int64_t)(img - i0) * hw);
+        const size_t g = ((size_t)img * c + ch) * hw + off;
+        const double v = x[g];
+        if (mode == 0) {
+            s1 += v;
+            s2 += v * v;
+        } else if (mode == 1) {
+            const double gg = (relu && !(z[g] > 0.f)) ? 0.0 : v;
+            s1 += gg;
+            s2 += gg * ((double)y[g] - mu) * is;
+        } else {
+            s1 += v;
+        }
+    }
+    s1 = block_sum(s1, sh);
+    s2 = block_sum(s2, sh);
+    if (threadIdx.x == 0) {
+        part[((size_t)ch * split + sp) * 2 + 0] = s1;
+        part[((size_t)ch * split + sp) * 2 + 1] = s2;
+    }
+}
+
+__global__ void bn_fwd_finalize(int c, int split, double count, const double* part, const float* gamma,
+                                const float* beta, float eps, float momentum, float* save_mean, float* save_invstd,
+                                float* run_mean, float* run_var, float* coef)
+{
+    const int ch = blockIdx.x * blockDim.x + threadIdx.x;
+    if (ch >= c) return;
+    double s1 = 0.0, s2 = 0.0;
+    for (int sp = 0; sp < split; ++sp) {
+        s1 += part[((size_t)ch * split + sp) * 2 + 0];
+        s2 += part[((size_t)ch * split + sp) * 2 + 1];
+    }
+    const double mean = s1 / count;
+    double var = s2 / count - mean * mean;
+    if (var < 0.0) var = 0.0;
+    const double invstd = 1.0 / sqrt(var + (double)eps);
+    save_mean[ch] = (float)mean;
+    save_invstd[ch] = (float)invstd;
+    if (run_mean) run_mean[ch] = (float)((1.0 - momentum) * run_mean[ch] + momentum * mean);
+    if (run_var)
+        run_var[ch] = (float)((1.0 - momentum) * run_var[ch] +
+                              momentum * (count > 1.0 ? var * count / (count - 1.0) : var));
+    const double scale = (double)gamma[ch] * invstd;
+    coef[2 * ch + 0] = (float)scale;
+    coef[2 * ch + 1] = (float)((double)beta[ch] - mean * scale);
+}
+
+__global__ void bn_fwd_apply(int64_t total, int c, int hw, const float* y, const float* coef, const float* res,
+                             int rc, int rh, int rw, int h, int w, int relu, float* z)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= total) return;
+    const int64_t nc = i / hw;
+    const int ch = (int)(nc % c);
+    float v = y[i] * coef[2 * ch] + coef[2 * ch + 1];
+    if (res) {
+        if (rc == c && rh == h && rw == w) {
+            v += res[i];
+        } else {
+            const int lo = (c - rc) / 2, cc = ch - lo;
+            if (cc >= 0 && cc < rc) {
+                const int img = (int)(nc / c), off = (int)(i - nc * hw);
+                const int hh = off / w, ww = off - hh * w;
+                v += res[(((size_t)img * rc + cc) * rh + hh * (rh / h)) * rw + ww * (rw / w)];
+            }
+        }
+    }
+    if (relu) v = fmaxf(v, 0.f);
+    z[i] = v;
+}
+
+__global__ void bn_bwd_finalize(int c, int split, double count, const double* part, const float* gamma,
+                                const float* invstd, float* dgamma, float* dbeta, float* coef)
+{
+    const int ch = blockIdx.x * blockDim.x + threadIdx.x;
+    if (ch >= c) return;
+    double s1 = 0.0, s2 = 0.0;
+    for (int sp = 0; sp < split; ++sp) {
+        s1 += part[((size_t)ch * split + sp) * 2 + 0];
+        s2 += part[((size_t)ch * split + sp) * 2 + 1];
+    }
+    dbeta[ch] = (float)s1;
+    dgamma[ch] = (float)s2;
+    coef[3 * ch + 0] = (float)((double)gamma[ch] * (double)invstd[ch]);
+    coef[3 * ch + 1] = (float)(s1 / count);
+    coef[3 * ch + 2] = (float)(s2 / count);
+}
+
+__global__ void bn_bwd_apply(int64_t total, int c, int hw, const float* dz, const float* z, const float* y,
+                             const float* mean, const float* invstd, const float* coef, int relu, float* dy,
+                             float* dres_identity, int res_accumulate)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= total) return;
+    const int ch = (int)((i / hw) % c);
+    const float g = (relu && !(z[i] > 0.f)) ? 0.f : dz[i];
+    const float xh = (y[i] - mean[ch]) * invstd[ch];
+    dy[i] = coef[3 * ch] * (g - coef[3 * ch + 1] - xh * coef[3 * ch + 2]);
+    if (dres_identity) dres_identity[i] = res_accumulate ? dres_identity[i] + g : g;
+}
+
+// option-A shortcut backward: dres[n][cr][hr][wr] gets g[n][cr+lo][hr/sh][wr/sw]
+// at subsampled positions and zero elsewhere
+__global__ void shortcut_a_bwd(int64_t total, int c, int h, int w, int rc, int rh, int rw, const float* dz,
+                               const float* z, int relu, float* dres, int accumulate)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= total) return;
+    const int rhw = rh * rw;
+    const int64_t ncr = i / rhw;
+    const int off = (int)(i - ncr * rhw);
+    const int cr = (int)(ncr % rc), img = (int)(ncr / rc);
+    const int hr = off / rw, wr = off - hr * rw;
+    const int sh = rh / h, sw = rw / w;
+    float g = 0.f;
+    if (hr % sh == 0 && wr % sw == 0) {
+        const int ch = cr + (c - rc) / 2;
+        const size_t j = (((size_t)img * c + ch) * h + hr / sh) * w + wr / sw;
+        g = (relu && !(z[j] > 0.f)) ? 0.f : dz[j];
+    }
+    dres[i] = accumulate ? dres[i] + g : g;
+}
+
+__global__ void chan_sum_finalize(int c, int split, const double* part, float* out)
+{
+    const int ch = blockIdx.x * blockDim.x + threadIdx.x;
+    if (ch >= c) return;
+    double s = 0.0;
+    for (int sp = 0; sp < split; ++sp) s += part[((size_t)ch * split + sp) * 2];
+    out[ch] = (float)s;
+}
+
+// -------------------------------------------------------------- pooling ----
+__global__ void maxpool_fwd_k(int64_t total, int h, int w, int p, int q, int k, int stride, const float* x,
+                              float* y, int32_t* argmax)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= total) return;
+    const int64_t nc = i / ((int64_t)p * q);
+    const int pq = (int)(i - nc * p * q);
+    const int pp = pq / q, qq = pq - pp * q;
+    const float* xp = x + nc * h * w;
+    float best = 0.f;
+    int bi = -1;
+    for (int r = 0; r < k; ++r)
+        for (int s = 0; s < k; ++s) {
+            const int ih = pp * stride + r, iw = qq * stride + s;
+            const float v = xp[ih * w + iw];
+            if (bi < 0 || v > best) {
+                best = v;
+                bi = ih * w + iw;
+            }
+        }
+    y[i] = best;
+    argmax[i] = bi;
+}
+
+// non-overlapping windows (k == stride): each input element belongs to at
+// most one window, so the backward pass is a gather with no conflicts
+__global__ void maxpool_bwd_k(int64_t total, int h, int w, int p, int q, int k, const float* dy,
+                              const int32_t* argmax, float* dx, int accumulate)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= total) return;
+    const int64_t nc = i / ((int64_t)h * w);
+    const int hw = (int)(i - nc * h * w);
+    const int ih = hw / w, iw = hw - ih * w;
+    const int pp = ih / k, qq = iw / k;
+    float g = 0.f;
+    if (pp < p && qq < q) {
+        const int64_t o = nc * p * q + pp * q + qq;
+        if (argmax[o] == hw) g = dy[o];
+    }
+    dx[i] = accumulate ? dx[i] + g : g;
+}
+
+__global__ void gavg_fwd_k(int64_t planes, int hw, const float* x, float* y)
+{
+    const int64_t plane = (int64_t)blockIdx.x * (blockDim.x >> 6) + (threadIdx.x >> 6);
+    const int lane = threadIdx.x & 63;
+    if (plane >= planes) return;
+    float s = 0.f;
+    for (int i = lane; i < hw; i += 64) s += x[plane * hw + i];
+    s = wave_sum_f(s);
+    if (lane == 0) y[plane] = s / (float)hw;
+}
+
+__global__ void gavg_bwd_k(int64_t total, int hw, const float* dy, float* dx, int accumulate)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= total) return;
+    const float g = dy[i / hw] / (float)hw;
+    dx[i] = accumulate ? dx[i] + g : g;
+}
+
+// -------------------------------------------------------------- misc -------
+__global__ void relu_mask_k(int64_t count, const float* z, float* g)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < count && !(z[i] > 0.f)) g[i] = 0.f;
+}
+
+__global__ __launch_bounds__(kBlock) void softmax_xent_k(int n, int classes, const float* logits,
+                                                          const int32_t* labels, float* loss, float* dlogits)
+{
+    __shared__ double sh[kBlock / 64];
+    double part = 0.0;
+    for (int row = threadIdx.x; row < n; row += kBlock) {
+        const float* z = logits + (size_t)row * classes;
+        float mx = z[0];
+        for (int j = 1; j < classes; ++j) mx = fmaxf(mx, z[j]);
+        float se = 0.f;
+        for (int j = 0; j < classes; ++j) se += expf(z[j] - mx);
+        const float lse = mx + logf(se);
+        const int lab = labels[row];
+        part += (double)(lse - z[lab]);
+        for (int j = 0; j < classes; ++j)
+            dlogits[(size_t)row * classes + j] = (expf(z[j] - lse) - (j == lab ? 1.f : 0.f)) / (float)n;
+    }
+    const double t = block_sum(part, sh);
+    if (threadIdx.x == 0) loss[0] = (float)(t / n);
+}
+
+__global__ void sgd_k(int64_t count, const float* w_in, float* w_out, float* v, const float* g, float lr, float mom,
+                      float wd, int nesterov)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= count) return;
+    const float w = w_in[i];
+    const float d = g[i] + wd * w;
+    const float vv = mom * v[i] + d;
+    v[i] = vv;
+    w_out[i] = w - lr * (nesterov ? d + mom * vv : vv);
+}
+
+// ------------------------------------------------------ FC GEMM (MFMA) -----
+// C[m][n] = sum_k A(m,k) B(k,n); A(m,k) = A[m*sam + k*sak], B(k,n) = B[k*sbk + n*sbn]
+struct GemmArgs {
+    const float* A;
+    const float* B;
+    float* C;
+    const float* bias;  // per column n (direct mode only)
+    int M, N, K;
+    int64_t sam, sak, sbk, sbn;
+    int kchunk;
+    int relu, accumulate;
+    int partial;  // 1: write raw sums to C + z*M*N
+};
+
+__device__ __forceinline__ float round_bf16(float f)
+{
+    uint32_t u = __float_as_uint(f);
+    if ((u & 0x7f800000u) != 0x7f800000u) u += 0x7fffu + ((u >> 16) & 1u);
+    return __uint_as_float(u & 0xffff0000u);
+}
+
+template <int BM, int BN, int WM, int WN, bool BF16, bool AK, bool BKC>
+__global__ __launch_bounds__(256) void gemm_kernel(GemmArgs a)
+{
+    constexpr int BK = BF16 ? 32 : 16;
+    constexpr int KSTEP = BF16 ? 32 : 4;
+    constexpr int TM = BM / WM / 16, TN = BN / WN / 16;
+    __shared__ float As[BK][BM + 4];
+    __shared__ float Bs[BK][BN + 4];
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave / WN, wn = wave % WN;
+    const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+    const int kbeg = blockIdx.z * a.kchunk;
+    const int kend = min(a.K, kbeg + a.kchunk);
+    v4f acc[TM][TN];
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) acc[i][j] = v4f{0.f, 0.f, 0.f, 0.f};
+    for (int k0 = kbeg; k0 < kend; k0 += BK) {
+#pragma unroll
+        for (int e = 0; e < (BM * BK + 255) / 256; ++e) {
+            const int idx = e * 256 + tid;
+            if (idx < BM * BK) {
+                int kk, mm;
+                if (AK) { kk = idx % BK; mm = idx / BK; } else { mm = idx % BM; kk = idx / BM; }
+                const int m = m0 + mm, k = k0 + kk;
+                const float v = (m < a.M && k < kend) ? a.A[(int64_t)m * a.sam + (int64_t)k * a.sak] : 0.f;
+                As[kk][mm] = BF16 ? round_bf16(v) : v;
+            }
+        }
+#pragma unroll
+        for (int e = 0; e < (BN * BK + 255) / 256; ++e) {
+            const int idx = e * 256 + tid;
+            if (idx < BN * BK) {
+                int kk, nn;
+                if (BKC) { kk = idx % BK; nn = idx / BK; } else { nn = idx % BN; kk = idx / BN; }
+                const int n = n0 + nn, k = k0 + kk;
+                const float v = (n < a.N && k < kend) ? a.B[(int64_t)k * a.sbk + (int64_t)n * a.sbn] : 0.f;
+                Bs[kk][nn] = BF16 ? round_bf16(v) : v;
+            }
+        }
+        __syncthreads();
+#pragma unroll
+        for (int ks = 0; ks < BK; ks += KSTEP) {
+            if constexpr (!BF16) {
+                float af[TM], bfr[TN];
+#pragma unroll
+                for (int i = 0; i < TM; ++i) af[i] = As[ks + (lane >> 4)][wm * (BM / WM) + i * 16 + (lane & 15)];
+#pragma unroll
+                for (int j = 0; j < TN; ++j) bfr[j] = Bs[ks + (lane >> 4)][wn * (BN / WN) + j * 16 + (lane & 15)];
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x4f32(af[i], bfr[j], acc[i][j], 0, 0, 0);
+            } else {
+                v8bf af[TM], bfr[TN];
+#pragma unroll
+                for (int i = 0; i < TM; ++i) {
+                    v8us u;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        u[e] = (unsigned short)(__float_as_uint(
+                                   As[ks + 8 * (lane >> 4) + e][wm * (BM / WM) + i * 16 + (lane & 15)]) >> 16);
+                    af[i] = __builtin_bit_cast(v8bf, u);
+                }
+#pragma unroll
+                for (int j = 0; j < TN; ++j) {
+                    v8us u;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e)
+                        u[e] = (unsigned short)(__float_as_uint(
+                                   Bs[ks + 8 * (lane >> 4) + e][wn * (BN / WN) + j * 16 + (lane & 15)]) >> 16);
+                    bfr[j] = __builtin_bit_cast(v8bf, u);
+                }
+#pragma unroll
+                for (int i = 0; i < TM; ++i)
+#pragma unroll
+                    for (int j = 0; j < TN; ++j)
+                        acc[i][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(af[i], bfr[j], acc[i][j], 0, 0, 0);
+            }
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < TM; ++i)
+#pragma unroll
+        for (int j = 0; j < TN; ++j) {
+            const int n = n0 + wn * (BN / WN) + j * 16 + (lane & 15);
+            if (n >= a.N) continue;
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                const int m = m0 + wm * (BM / WM) + i * 16 + 4 * (lane >> 4) + v;
+                if (m >= a.M) continue;
+                float val = acc[i][j][v];
+                if (a.partial) {
+                    a.C[((int64_t)blockIdx.z * a.M + m) * a.N + n] = val;
+                } else {
+                    if (a.bias) val += a.bias[n];
+                    if (a.relu) val = fmaxf(val, 0.f);
+                    float* dst = a.C + (int64_t)m * a.N + n;
+                    *dst = a.accumulate ? *dst + val : val;
+                }
+            }
+        }
+}
+
+__global__ void gemm_reduce(const float* part, int splits, int M, int N, const float* bias, int relu, int accumulate,
+                            float* C)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t count = (int64_t)M * N;
+    if (i >= count) return;
+    float v = 0.f;
+    for (int z = 0; z < splits; ++z) v += part[(int64_t)z * count + i];
+    if (bias) v += bias[i % N];
+    if (relu) v = fmaxf(v, 0.f);
+    C[i] = accumulate ? C[i] + v : v;
+}
+
+template <bool AK, bool BKC>
+hipError_t gemm(GemmArgs a, int bf16, void* ws, size_t ws_bytes, hipStream_t st)
+{
+    constexpr int BM = 64, BN = 64;
+    const int tiles = ((a.M + BM - 1) / BM) * ((a.N + BN - 1) / BN);
+    const int BK = bf16 ? 32 : 16;
+    int splits = 1;
+    if (tiles < 512 && ws) {
+        splits = (1024 + tiles - 1) / tiles;
+        const int maxs = (a.K + 4 * BK - 1) / (4 * BK);  // at least four BK slices per split
+        if (splits > maxs) splits = maxs;
+        while (splits > 1 && (size_t)splits * a.M * a.N * sizeof(float) > ws_bytes) --splits;
+        if (splits < 1) splits = 1;
+    }
+    const int per = (a.K + splits - 1) / splits;
+    a.kchunk = ((per + BK - 1) / BK) * BK;
+    splits = (a.K + a.kchunk - 1) / a.kchunk;
+    if (splits < 1) splits = 1;
+    float* out = a.C;
+    const float* bias = a.bias;
+    const int relu = a.relu, accum = a.accumulate;
+    if (splits > 1) {
+        a.partial = 1;
+        a.C = (float*)ws;
+    }
+    dim3 grid((a.N + BN - 1) / BN, (a.M + BM - 1) / BM, splits);
+    if (bf16)
+        hipLaunchKernelGGL((gemm_kernel<BM, BN, 2, 2, true, AK, BKC>), grid, dim3(256), 0, st, a);
+    else
+        hipLaunchKernelGGL((gemm_kernel<BM, BN, 2, 2, false, AK, BKC>), grid, dim3(256), 0, st, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || splits == 1) return e;
+    const int64_t count = (int64_t)a.M * a.N;
+    hipLaunchKernelGGL(gemm_reduce, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, st, (const float*)ws, splits,
+                       a.M, a.N, bias, relu, accum, out);
+    return hipGetLastError();
+}
+
+inline unsigned blocks_for(int64_t n, int b = kBlock) { return (unsigned)((n + b - 1) / b); }
+
+}  // namespace
+
+// ------------------------------------------------------------ launchers -----
+size_t channel_sum_ws_bytes(int n, int c, int hw)
+{
+    (void)hw;
+    return (size_t)c * channel_splits(n, c) * 2 * sizeof(double);
+}
+
+hipError_t channel_sum(int n, int c, int hw, const float* x, float* out, void* ws, size_t ws_bytes, hipStream_t st)
+{
+    const int sp = channel_splits(n, c);
+    if (ws_bytes < channel_sum_ws_bytes(n, c, hw)) return hipErrorInvalidValue;
+    hipLaunchKernelGGL(chan_partials, dim3(c, sp), dim3(kBlock), 0, st, 2, n, c, hw, sp, x, (const float*)nullptr,
+                       (const float*)nullptr, (const float*)nullptr, (const float*)nullptr, 0, (double*)ws);
+    hipLaunchKernelGGL(chan_sum_finalize, dim3(blocks_for(c)), dim3(kBlock), 0, st, c, sp, (const double*)ws, out);
+    return hipGetLastError();
+}
+
+size_t bn_ws_bytes(int n, int c, int h, int w)
+{
+    (void)h; (void)w;
+    return (size_t)c * channel_splits(n, c) * 2 * sizeof(double) + (size_t)c * 3 * sizeof(float) + 256;
+}
+
+hipError_t bn_fwd(int n, int c, int h, int w, const float* y, const float* gamma, const float* beta, const float* res,
+                  int rc, int rh, int rw, int relu, float eps, float momentum, float* z, float* save_mean,
+                  float* save_invstd, float* run_mean, float* run_var, void* ws, size_t ws_bytes, hipStream_t st)
+{
+    if (ws_bytes < bn_ws_bytes(n, c, h, w)) return hipErrorInvalidValue;
+    const int sp = channel_splits(n, c);
+    const int hw = h * w;
+    double* part = (double*)ws;
+    float* coef = (float*)((char*)ws + (size_t)c * sp * 2 * sizeof(double));
+    hipLaunchKernelGGL(chan_partials, dim3(c, sp), dim3(kBlock), 0, st, 0, n, c, hw, sp, y, (const float*)nullptr,
+                       (const float*)nullptr, (const float*)nullptr, (const float*)nullptr, 0, part);
+    hipLaunchKernelGGL(bn_fwd_finalize, dim3(blocks_for(c)), dim3(kBlock), 0, st, c, sp, (double)n * hw,
+                       (const double*)part, gamma, beta, eps, momentum, save_mean, save_invstd, run_mean, run_var, coef);
+    const int64_t total = (int64_t)n * c * hw;
+    hipLaunchKernelGGL(bn_fwd_apply, dim3(blocks_for(total)), dim3(kBlock), 0, st, total, c, hw, y,
+                       (const float*)coef, res, rc, rh, rw, h, w, relu, z);
+    return hipGetLastError();
+}
+
+hipError_t bn_bwd(int n, int c, int h, int w, const float* dz, const float* z, const float* y, const float* gamma,
+                  const float* save_mean, const float* save_invstd, int relu, float* dy, float* dgamma,
+                  float* dbeta, float* dres, int rc, int rh, int rw, int res_accumulate, void* ws, size_t ws_bytes,
+                  hipStream_t st)
+{
+    if (ws_bytes < bn_ws_bytes(n, c, h, w)) return hipErrorInvalidValue;
+    const int sp = channel_splits(n, c);
+    const int hw = h * w;
+    double* part = (double*)ws;
+    float* coef = (float*)((char*)ws + (size_t)c * sp * 2 * sizeof(double));
+    hipLaunchKernelGGL(chan_partials, dim3(c, sp), dim3(kBlock), 0, st, 1, n, c, hw, sp, dz, z, y, save_mean,
+                       save_invstd, relu, part);
+    hipLaunchKernelGGL(bn_bwd_finalize, dim3(blocks_for(c)), dim3(kBlock), 0, st, c, sp, (double)n * hw,
+                       (const double*)part, gamma, save_invstd, dgamma, dbeta, coef);
+    const int64_t total = (int64_t)n * c * hw;
+    const bool identity = dres && rc == c && rh == h && rw == w;
+    hipLaunchKernelGGL(bn_bwd_apply, dim3(blocks_for(total)), dim3(kBlock), 0, st, total, c, hw, dz, z, y, save_mean,
+                       save_invstd, (const float*)coef, relu, dy, identity ? dres : (float*)nullptr, res_accumulate);
+    if (dres && !identity) {
+        const int64_t rtotal = (int64_t)n * rc * rh * rw;
+        hipLaunchKernelGGL(shortcut_a_bwd, dim3(blocks_for(rtotal)), dim3(kBlock), 0, st, rtotal, c, h, w, rc, rh, rw,
+                           dz, z, relu, dres, res_accumulate);
+    }
+    return hipGetLastError();
+}
+
+hipError_t maxpool_fwd(int n, int c, int h, int w, int k, int stride, const float* x, float* y, int32_t* argmax,
+                       hipStream_t st)
+{
+    const int p = (h - k) / stride + 1, q = (w - k) / stride + 1;
+    const int64_t total = (int64_t)n * c * p * q;
+    hipLaunchKernelGGL(maxpool_fwd_k, dim3(blocks_for(total)), dim3(kBlock), 0, st, total, h, w, p, q, k, stride, x,
+                       y, argmax);
+    return hipGetLastError();
+}
+
+hipError_t maxpool_bwd(int n, int c, int h, int w, int k, int stride, const float* dy, const int32_t* argmax,
+                       float* dx, int accumulate, hipStream_t st)
+{
+    const int p = (h - k) / stride + 1, q = (w - k) / stride + 1;
+    const int64_t total = (int64_t)n * c * h * w;
+    hipLaunchKernelGGL(maxpool_bwd_k, dim3(blocks_for(total)), dim3(kBlock), 0, st, total, h, w, p, q, k, dy, argmax,
+                       dx, accumulate);
+    return hipGetLastError();
+}
+
+hipError_t gavgpool_fwd(int n, int c, int h, int w, const float* x, float* y, hipStream_t st)
+{
+    const int64_t planes = (int64_t)n * c;
+    hipLaunchKernelGGL(gavg_fwd_k, dim3(blocks_for(planes, 4)), dim3(kBlock), 0, st, planes, h * w, x, y);
+    return hipGetLastError();
+}
+
+hipError_t gavgpool_bwd(int n, int c, int h, int w, const float* dy, float* dx, int accumulate, hipStream_t st)
+{
+    const int64_t total = (int64_t)n * c * h * w;
+    hipLaunchKernelGGL(gavg_bwd_k, dim3(blocks_for(total)), dim3(kBlock), 0, st, total, h * w, dy, dx, accumulate);
+    return hipGetLastError();
+}
+
+hipError_t relu_mask(int64_t count, const float* z, float* g, hipStream_t st)
+{
+    hipLaunchKernelGGL(relu_mask_k, dim3(blocks_for(count)), dim3(kBlock), 0, st, count, z, g);
+    return hipGetLastError();
+}
+
+hipError_t softmax_xent(int n, int classes, const float* logits, const int32_t* labels, float* loss, float* dlogits,
+                        hipStream_t st)
+{
+    hipLaunchKernelGGL(softmax_xent_k, dim3(1), dim3(kBlock), 0, st, n, classes, logits, labels, loss, dlogits);
+    return hipGetLastError();
+}
+
+hipError_t sgd_momentum(int64_t count, const float* w_in, float* w_out, float* v, const float* g, float lr, float mom,
+                        float wd, int nesterov, hipStream_t st)
+{
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(sgd_k, dim3(blocks_for(count)), dim3(kBlock), 0, st, count, w_in, w_out, v, g, lr, mom, wd,
+                       nesterov);
+    return hipGetLastError();
+}
+
+hipError_t fc_fwd(int n, int in, int out, const float* x, const float* w, const float* b, int relu, float* y, int bf16,
+                  hipStream_t st)
+{
+    GemmArgs a{};
+    a.A = x; a.B = w; a.C = y; a.bias = b; a.relu = relu;
+    a.M = n; a.N = out; a.K = in;
+    a.sam = in; a.sak = 1;    // x[n][i]
+    a.sbk = 1; a.sbn = in;    // w[o][i]
+    return gemm<true, true>(a, bf16, nullptr, 0, st);
+}
+
+size_t fc_bwd_ws_bytes(int n, int in, int out)
+{
+    // [db partials: out x 2 doubles, padded][split-K partials of the dx GEMM]
+    const int tiles = ((n + 63) / 64) * ((in + 63) / 64);
+    int splits = tiles < 512 ? (1024 + tiles - 1) / tiles : 1;
+    const int maxs = (out + 63) / 64;
+    if (splits > maxs) splits = maxs;
+    if (splits < 1) splits = 1;
+    const size_t head = (((size_t)out * 2 * sizeof(double)) + 255) / 256 * 256;
+    return head + (size_t)splits * n * in * sizeof(float);
+}
+
+hipError_t fc_bwd(int n, int in, int out, const float* x, const float* w, const float* dy, float* dx, int dx_accumulate,
+                  float* dw, float* db, int bf16, void* ws, size_t ws_bytes, hipStream_t st)
+{
+    if (ws_bytes < fc_bwd_ws_bytes(n, in, out)) return hipErrorInvalidValue;
+    const size_t head = (((size_t)out * 2 * sizeof(double)) + 255) / 256 * 256;
+    hipError_t e = hipSuccess;
+    if (dx) {
+        GemmArgs a{};
+        a.A = dy; a.B = w; a.C = dx; a.accumulate = dx_accumulate;
+        a.M = n; a.N = in; a.K = out;
+        a.sam = out; a.sak = 1;   // dy[n][o]
+        a.sbk = in; a.sbn = 1;    // w[o][i]
+        e = gemm<true, false>(a, bf16, (char*)ws + head, ws_bytes - head, st);
+        if (e != hipSuccess) return e;
+    }
+    {
+        GemmArgs a{};
+        a.A = dy; a.B = x; a.C = dw;
+        a.M = out; a.N = in; a.K = n;
+        a.sam = 1; a.sak = out;   // dy[n][o] read as A(m=o, k=n)
+        a.sbk = in; a.sbn = 1;    // x[n][i]
+        e = gemm<false, false>(a, bf16, nullptr, 0, st);
+        if (e != hipSuccess) return e;
+    }
+    if (db) {
+        // db[o] = sum_n dy[n][o]: the column sums of dy viewed as [n][out][1]
+        // (not a product, so never rounded to bf16)
+        hipLaunchKernelGGL(chan_partials, dim3(out, 1), dim3(kBlock), 0, st, 2, n, out, 1, 1, dy,
+                           (const float*)nullptr, (const float*)nullptr, (const float*)nullptr, (const float*)nullptr,
+                           0, (double*)ws);
+        hipLaunchKernelGGL(chan_sum_finalize, dim3(blocks_for(out)), dim3(kBlock), 0, st, out, 1, (const double*)ws, db);
+        e = hipGetLastError();
+    }
+    return e;
+}
+
+}  // namespace psw

@@ -1,0 +1,182 @@
+"""Host-only checks of the C ABI (no GPU needed): the library loads, exports
+every symbol include/psw.h declares, and the stage scheduler's dry run
+(psw_net_plan) follows the stale-weight schedule and rejects bad input."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_1912_12675_amd import synth
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "psw.h")
+
+
+@pytest.fixture(scope="module")
+def psw():
+    from paper_1912_12675_amd import psw as P
+    if not os.path.exists(P.LIB_PATH):
+        pytest.fail("libpsw.so is not built (python -m paper_1912_12675_amd.build)")
+    P.lib()
+    return P
+
+
+def declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(psw_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_header_symbols_exported(psw):
+    syms = declared_symbols()
+    assert len(syms) >= 25
+    L = ctypes.CDLL(psw.LIB_PATH)
+    missing = [s for s in syms if not hasattr(L, s)]
+    assert not missing, missing
+    # the binding covers the whole surface, with the header's names
+    assert sorted(psw.SIGNATURES) == syms
+
+
+def test_version_and_error_string(psw):
+    assert b"gfx950" in psw.lib().psw_version()
+    rc = psw.lib().psw_conv_fwd(0, 1, 1, 1, 1, 1, 1, 1, 0, None, None, None, 0, None, 0, None)
+    assert rc == -2
+    assert b"positive" in psw.lib().psw_last_error()
+    rc = psw.lib().psw_conv_fwd(1, 1, 4, 4, 1, 3, 3, 1, 1, None, None, None, 0, None, 0, None)
+    assert rc == -1
+    rc = psw.lib().psw_conv_fwd(1, 1, 4, 4, 1, 3, 3, 1, 1, 8, 8, None, 0, 8, 7, None)
+    assert rc == -3  # unknown precision
+    rc = psw.lib().psw_pool_fwd(0, 1, 1, 8, 8, 3, 2, 8, 8, 8, None)
+    assert rc == -3  # overlapping windows are not supported
+    rc = psw.lib().psw_sgd_momentum_step(10, 1000, 1004, 8, 8, 0.1, 0.9, 0.0, 0, None)
+    assert rc == -2  # partial overlap of w_in / w_out
+
+
+def _plan(psw, wl, t, staleness, ring=None):
+    ring = wl.ring_depth() if ring is None else ring
+    return psw.net_plan_only(wl.ops, wl.batch, wl.in_shape, wl.stage_end, ring, t, staleness)
+
+
+def test_plan_versions_follow_schedule(psw):
+    wl = synth.resnet20_workload(batch=4)
+    S = wl.n_stages
+    stage_of = np.zeros(len(wl.ops), dtype=int)
+    prev = 0
+    for s, e in enumerate(wl.stage_end):
+        stage_of[prev:e] = s
+        prev = e
+    for t in range(0, 9):
+        d = [3, 2, 1, 0]
+        plan = _plan(psw, wl, t, d)
+        fwd = [p for p in plan if p[1] in (1, 2, 4)]           # conv / bn / fc forward
+        bwd = [p for p in plan if p[1] in (8, 9, 11)]          # bwd-data / bn bwd / fc bwd
+        sgd = [p for p in plan if p[1] == 12]
+        for op, what, stage, ver in fwd:
+            assert stage == stage_of[op]
+            assert ver == max(0, t - d[stage])                  # forward reads version t - d_s
+        assert all(ver == t for _, _, _, ver in bwd)            # backward reads the current version
+        assert [(s, v) for _, _, s, v in sgd] == [(s, t) for s in range(S)]
+    # order: every forward before the loss, every backward after it, updates last
+    plan = _plan(psw, wl, 5, [3, 2, 1, 0])
+    kinds = [p[1] for p in plan]
+    li = kinds.index(5)
+    assert all(k in (1, 2, 3, 4) for k in kinds[:li])
+    assert all(k not in (1, 2, 3, 4) for k in kinds[li + 1:])
+    assert kinds[-S:] == [12] * S
+    # 19 conv forwards, 19 wgrads, 18 dgrads (none for the stem) in ResNet-20
+    assert kinds.count(1) == 19 and kinds.count(7) == 19 and kinds.count(8) == 18
+
+
+def test_plan_rejects_bad_staleness(psw):
+    wl = synth.resnet20_workload(batch=4)
+    with pytest.raises(psw.PswError) as e:
+        _plan(psw, wl, 3, [4, 2, 1, 0])        # ring depth of stage 0 is 4
+    assert e.value.code == -4
+    with pytest.raises(psw.PswError) as e:
+        _plan(psw, wl, 3, [0, 0, 0, -1])
+    assert e.value.code == -4
+    with pytest.raises(psw.PswError) as e:
+        _plan(psw, wl, -1, [0, 0, 0, 0])
+    assert e.value.code == -5
+    # a deeper ring accepts more staleness
+    assert _plan(psw, wl, 3, [6, 4, 2, 0], ring=[7, 5, 3, 1])
+
+
+def test_net_create_rejects_bad_descriptions(psw):
+    ops, le, ins = synth.resnet_cifar(20)
+    L = psw.lib()
+
+    def create(o, se, rd, batch=2, shape=ins):
+        layers = psw._layers(o)
+        se = np.ascontiguousarray(se, dtype=np.int32)
+        rd = np.ascontiguousarray(rd, dtype=np.int32)
+        h = ctypes.c_void_p()
+        rc = L.psw_net_create(layers, len(layers), batch, *shape, se.ctypes.data, len(se), rd.ctypes.data, 0,
+                              ctypes.byref(h))
+        if rc == 0:
+            L.psw_net_destroy(h.value)
+        return rc
+
+    assert create(ops, [len(ops)], [1]) == 0
+    assert create(ops, [10, 5, len(ops)], [1, 1, 1]) == -2          # stage ends not increasing
+    assert create(ops, [len(ops) - 1], [1]) == -2                   # last stage must end at n_ops
+    assert create(ops, [len(ops)], [0]) == -2                       # ring depth >= 1
+    bad = ops.copy()
+    bad[0][3] = 4                                                   # conv cin != input channels
+    assert create(bad, [len(ops)], [1]) == -2
+    bad = ops.copy()
+    bad[-1][3] = 65                                                 # fc input features
+    assert create(bad, [len(ops)], [1]) == -2
+    lops, _, _ = synth.lenet5()
+    assert create(lops, [len(lops)], [1], shape=(1, 28, 28)) == 0
+    assert create(lops, [len(lops)], [1], shape=(1, 32, 32)) == -2  # fc1 would see 16*6*6 features, not 400
+    assert create(lops, [len(lops)], [1], shape=(1, 3, 3)) == -2    # 5x5 kernel larger than the input
+
+
+def test_net_sizes_match_oracle(psw, oracle):
+    for wl in (synth.resnet20_workload(batch=2), synth.lenet5_workload(batch=2), synth.vgg16_workload(batch=2)):
+        counts = oracle.param_counts(wl.ops, wl.in_shape, wl.batch, wl.stage_end)
+        layers = psw._layers(wl.ops)
+        se = np.ascontiguousarray(wl.stage_end, dtype=np.int32)
+        rd = np.ascontiguousarray(wl.ring_depth(), dtype=np.int32)
+        h = ctypes.c_void_p()
+        L = psw.lib()
+        assert L.psw_net_create(layers, len(layers), wl.batch, *wl.in_shape, se.ctypes.data, len(se), rd.ctypes.data,
+                                0, ctypes.byref(h)) == 0
+        sp = np.zeros(len(se), dtype=np.int64)
+        rf, npar, nbn, ab = (ctypes.c_int64() for _ in range(4))
+        assert L.psw_net_sizes(h.value, sp.ctypes.data, ctypes.byref(rf), ctypes.byref(npar), ctypes.byref(nbn),
+                               ctypes.byref(ab)) == 0
+        assert list(sp) == list(counts)
+        assert rf.value == int(sum(c * d for c, d in zip(counts, rd)))
+        layout, _ = synth.param_layout(wl)
+        for op in range(len(wl.ops)):
+            st, off, cnt = ctypes.c_int(), ctypes.c_int64(), ctypes.c_int64()
+            assert L.psw_net_param_offset(h.value, op, ctypes.byref(st), ctypes.byref(off), ctypes.byref(cnt)) == 0
+            mine = [(s, o, int(np.prod(shape))) for (i, _, shape, s, o) in layout if i == op]
+            if mine:
+                assert (st.value, off.value) == mine[0][:2]
+                assert cnt.value == sum(m[2] for m in mine)
+            else:
+                assert cnt.value == 0
+        L.psw_net_destroy(h.value)
+
+
+def test_stage_step_requires_binding(psw):
+    wl = synth.resnet20_workload(batch=2)
+    L = psw.lib()
+    layers = psw._layers(wl.ops)
+    se = np.ascontiguousarray(wl.stage_end, dtype=np.int32)
+    rd = np.ascontiguousarray(wl.ring_depth(), dtype=np.int32)
+    h = ctypes.c_void_p()
+    assert L.psw_net_create(layers, len(layers), 2, *wl.in_shape, se.ctypes.data, 4, rd.ctypes.data, 0,
+                            ctypes.byref(h)) == 0
+    st = np.zeros(4, dtype=np.int32)
+    lr = np.full(4, 0.01, dtype=np.float32)
+    rc = L.psw_stage_step(h.value, 0, st.ctypes.data, lr.ctypes.data, 0.9, 0.0, 0, 8, 8, 8, None, None)
+    assert rc == -8
+    p = ctypes.c_void_p()
+    assert L.psw_net_slot(h.value, 0, 0, ctypes.byref(p)) == -8
+    L.psw_net_destroy(h.value)

@@ -1,0 +1,169 @@
+"""End-to-end GPU parity of the stale-weight training path (psw_stage_step)
+against the oracle: parameters after N steps, per-step losses, and the
+weight-version table.
+
+Bar: ||gpu - oracle||_2 / ||oracle||_2 <= 1e-4 (fp32) or 2e-2 (bf16 mode)
+over the whole parameter vector and for every tensor with a non-zero
+initial value (see compare_params); versions equal as integers.  The small cases
+run the oracle live at sizes it finishes in seconds; the full-size ResNet-20
+case (batch 128, 50 steps, the configuration bench.py times) compares with
+the oracle's stored result (tests/golden/make_golden.py)."""
+import os
+
+import numpy as np
+import pytest
+import torch
+
+from paper_1912_12675_amd import synth
+
+pytestmark = pytest.mark.gpu
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+
+@pytest.fixture(scope="module")
+def P():
+    from paper_1912_12675_amd import psw
+    psw.lib()
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    return psw
+
+
+def gpu_train(P, wl, T, batch=None, net=None, t0=0):
+    N = wl.batch if batch is None else batch
+    st = wl.staleness(T)
+    if net is None:
+        net = P.Net(wl.ops, N, wl.in_shape, wl.stage_end, wl.ring_depth(T), bf16=wl.bf16)
+        net.load_params(synth.init_params(wl))
+    losses, versions = [], []
+    for t in range(t0, T):
+        x, y = synth.batch(wl, t, N)
+        ver = net.step(t, st[t], wl.lr, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), wl.momentum,
+                       wl.weight_decay, wl.nesterov)
+        losses.append(float(net.loss.item()))
+        versions.append(ver)
+    torch.cuda.synchronize()
+    return net, np.array(losses), np.array(versions)
+
+
+def oracle_train(oracle, wl, T, batch=None):
+    N = wl.batch if batch is None else batch
+    xs, ys = synth.batches(wl, T, N)
+    return oracle.train(wl.ops, wl.in_shape, wl.stage_end, synth.init_params(wl), xs, ys, wl.staleness(T), wl.lr,
+                        wl.momentum, wl.weight_decay, wl.nesterov, bf16=wl.bf16)
+
+
+def compare_params(wl, gpu_flat, ref_flat, p0, tol):
+    """Spec bar: ||W_gpu - W_ref|| / ||W_ref|| <= tol over the whole
+    parameter vector.  Every tensor with a non-zero initial value (conv/FC
+    weights, BN gamma) must also meet it on its own.  Zero-initialised
+    tensors (BN beta, biases) consist only of their updates, which carry the
+    rounding noise of ReLU-sign and max-pool decisions taken near zero: an
+    independent float32 implementation (torch, CPU) of the same 10-step
+    ResNet-20 run sits 1e-3 away from the float64 oracle on those tensors,
+    so they are held by the whole-vector bar.  In fp32 the whole update
+    W^(T) - W^(0) must also agree to 1e-2 (float32 torch: 4.8e-4)."""
+    layout, counts = synth.param_layout(wl)
+    base = np.concatenate([[0], np.cumsum(counts)])
+    glob = np.linalg.norm(gpu_flat - ref_flat) / np.linalg.norm(ref_flat)
+    upd = np.linalg.norm((gpu_flat - p0) - (ref_flat - p0)) / max(np.linalg.norm(ref_flat - p0), 1e-30)
+    worst = (0.0, None)
+    for op, name, shape, s, off in layout:
+        n = int(np.prod(shape))
+        i0 = int(base[s]) + off
+        if np.linalg.norm(p0[i0:i0 + n]) == 0.0:
+            continue
+        a, b = gpu_flat[i0:i0 + n], ref_flat[i0:i0 + n]
+        rel = np.linalg.norm(a - b) / np.linalg.norm(b)
+        if rel > worst[0]:
+            worst = (rel, f"op {op} {name}{shape}")
+    print(f"{wl.name}: params rel-L2 {glob:.3e}, update rel-L2 {upd:.3e}, worst tensor {worst[0]:.3e} ({worst[1]})",
+          flush=True)
+    assert glob <= tol, f"whole-vector rel-L2 {glob:.3e} > {tol}"
+    assert worst[0] <= tol, f"{worst[1]}: rel-L2 {worst[0]:.3e} > {tol}"
+    if not wl.bf16:
+        assert upd <= 1e-2, f"update rel-L2 {upd:.3e} > 1e-2"
+    return glob, upd
+
+
+CASES = [
+    # (workload factory, batch, steps)
+    ("lenet5", lambda: synth.lenet5_workload(), 16, 1),
+    ("resnet20_b8", lambda: synth.resnet20_workload(batch=8), 8, 10),
+    ("resnet20_bf16_b8", lambda: synth.resnet20_workload(batch=8, bf16=True), 8, 6),
+    ("alexnet_b4", lambda: synth.alexnet_workload(batch=4), 4, 4),
+    ("vgg16_hybrid_b16", lambda: synth.vgg16_workload(batch=16, n_pipelined=3), 16, 5),
+    ("resnet110_bf16_b8", lambda: synth.resnet110_workload(batch=8), 8, 3),
+]
+
+
+@pytest.mark.parametrize("name,factory,batch,T", CASES, ids=[c[0] for c in CASES])
+def test_train_parity(P, oracle, name, factory, batch, T):
+    print(f"train parity {name}: batch {batch}, {T} steps", flush=True)
+    wl = factory()
+    net, losses, versions = gpu_train(P, wl, T, batch)
+    ref = oracle_train(oracle, wl, T, batch)
+    np.testing.assert_array_equal(versions, ref["versions"])
+    np.testing.assert_array_equal(versions, np.maximum(0, np.arange(T)[:, None] - wl.staleness(T)))
+    tol = 2e-2 if wl.bf16 else 1e-4
+    np.testing.assert_allclose(losses, ref["losses"], rtol=tol)
+    p0 = synth.init_params(wl).astype(np.float64)
+    compare_params(wl, net.params(T).double().numpy(), ref["params"], p0, tol)
+    # the stale schedule changes the result (it is not plain SGD in disguise)
+    if T > 1 and wl.staleness(T).max() > 0:
+        assert np.abs(ref["params"] - p0).max() > 0
+
+
+@pytest.mark.parametrize("mode", ["fp32", "bf16"])
+def test_resnet20_full_size_50_steps(P, mode):
+    """ResNet-20, batch 128, PPV (7,13,19), staleness [3,2,1,0], 50 steps:
+    the configuration the benchmark times, against the stored oracle run."""
+    path = os.path.join(GOLDEN, f"resnet20_b128_50steps_{mode}.npz")
+    assert os.path.exists(path), f"missing {path} (python tests/golden/make_golden.py)"
+    g = np.load(path)
+    wl = synth.resnet20_workload(bf16=(mode == "bf16"))
+    print(f"resnet20 b128 50 steps {mode}", flush=True)
+    net, losses, versions = gpu_train(P, wl, wl.steps)
+    p0 = synth.init_params(wl).astype(np.float64)
+    np.testing.assert_array_equal(versions, g["versions"])
+    tol = 2e-2 if wl.bf16 else 1e-4
+    np.testing.assert_allclose(losses, g["losses"], rtol=tol)
+    compare_params(wl, net.params(wl.steps).double().numpy(), p0 + g["delta"].astype(np.float64), p0, tol)
+
+
+def test_runs_are_bit_identical(P):
+    wl = synth.resnet20_workload(batch=16)
+    a, la, _ = gpu_train(P, wl, 4, 16)
+    b, lb, _ = gpu_train(P, wl, 4, 16)
+    assert torch.equal(a.params(4), b.params(4))
+    np.testing.assert_array_equal(la, lb)
+
+
+def test_resume_is_bit_identical(P):
+    """Checkpoint after 3 steps (ring, momentum, running statistics), resume
+    in a new net with psw_net_set_step, continue: same result as an
+    uninterrupted run."""
+    wl = synth.resnet20_workload(batch=8)
+    full, lf, _ = gpu_train(P, wl, 6, 8)
+    part, _, _ = gpu_train(P, wl, 3, 8)
+    ck = {k: getattr(part, k).clone() for k in ("ring", "momentum", "run_mean", "run_var")}
+    net = P.Net(wl.ops, 8, wl.in_shape, wl.stage_end, wl.ring_depth(6), bf16=False)
+    for k, v in ck.items():
+        getattr(net, k).copy_(v)
+    net.set_step(3)
+    net, lr_, _ = gpu_train(P, wl, 6, 8, net=net, t0=3)
+    assert torch.equal(net.params(6), full.params(6))
+    np.testing.assert_array_equal(lr_, lf[3:])
+    assert torch.equal(net.run_mean, full.run_mean)
+
+
+def test_step_order_enforced(P):
+    wl = synth.resnet20_workload(batch=2)
+    net = P.Net(wl.ops, 2, wl.in_shape, wl.stage_end, wl.ring_depth(), bf16=False)
+    x, y = synth.batch(wl, 0, 2)
+    with pytest.raises(P.PswError) as e:
+        net.step(1, [0, 0, 0, 0], wl.lr, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda())
+    assert e.value.code == -5
+    with pytest.raises(P.PswError) as e:
+        net.step(0, [4, 0, 0, 0], wl.lr, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda())
+    assert e.value.code == -4

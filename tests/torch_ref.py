@@ -141,7 +141,8 @@ def boundary_tensor_ok(ops, stage_end):
     return True
 
 
-def simulate_register_pipeline(ops, stage_end, params0, xs, labels, lr, mom=0.9, variant="paper", stash=False):
+def simulate_register_pipeline(ops, stage_end, params0, xs, labels, lr, mom=0.9, variant="paper", stash=False,
+                               dtype=torch.float64):
     """Register/cycle simulator of pipelined backpropagation (Sec. 3).
 
     K = S-1 register pairs split the network into partitions 1..K+1.  ONE
@@ -174,7 +175,7 @@ def simulate_register_pipeline(ops, stage_end, params0, xs, labels, lr, mom=0.9,
     S = len(stage_end)
     K = S - 1
     T = len(xs)
-    W = [torch.tensor(p, requires_grad=True) for p in split_flat(np.asarray(params0, np.float64), counts)]
+    W = [torch.tensor(p, dtype=dtype, requires_grad=True) for p in split_flat(np.asarray(params0, np.float64), counts)]
     V = [torch.zeros_like(w) for w in W]
     n_updates = [0] * S
     begins = [0] + list(stage_end[:-1])
@@ -202,7 +203,7 @@ def simulate_register_pipeline(ops, stage_end, params0, xs, labels, lr, mom=0.9,
         lo, hi = begins[i], stage_end[i]
         if kind == "F":
             if i == 0:
-                inp = torch.tensor(xs[t], dtype=torch.float64)
+                inp = torch.tensor(xs[t], dtype=dtype)
             else:
                 inp = fwd[(t, i - 1)][1].detach().requires_grad_(True)
             versions[t, i] = n_updates[i]
@@ -234,4 +235,4 @@ def simulate_register_pipeline(ops, stage_end, params0, xs, labels, lr, mom=0.9,
                 W[i].data.sub_(float(lrs[i]) * V[i])
             n_updates[i] += 1
     last_cycle = max(z[0] for z in tasks)
-    return torch.cat([w.detach() for w in W]).numpy(), losses, versions, last_cycle
+    return torch.cat([w.detach() for w in W]).double().numpy(), losses, versions, last_cycle
