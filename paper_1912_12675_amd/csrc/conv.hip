@@ -20,6 +20,8 @@
 // Tiles are staged through LDS; fp32 uses v_mfma_f32_16x16x4_f32, the bf16
 // mode rounds both operands to bfloat16 (nearest even) when staging and uses
 // v_mfma_f32_16x16x32_bf16 with fp32 accumulation.
+#include <algorithm>
+
 #include "internal.h"
 
 namespace psw {
@@ -219,14 +221,20 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a)
         }
 }
 
-// dw[i] = sum_z part[z][i], z in increasing order (deterministic)
-__global__ void reduce_splits(const float* part, int splits, int64_t count, float* out)
+// dw[i] = sum_z part[z][i] in a fixed order (deterministic): each block owns
+// 64 consecutive outputs; its four waves sum the splits z = zl (mod 4) in
+// increasing z, then wave 0 adds the four partial sums in order zl = 0..3.
+__global__ __launch_bounds__(256) void reduce_splits(const float* part, int splits, int64_t count, float* out)
 {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= count) return;
+    __shared__ float sh[4][64];
+    const int o = threadIdx.x & 63, zl = threadIdx.x >> 6;
+    const int64_t i = (int64_t)blockIdx.x * 64 + o;
     float acc = 0.f;
-    for (int z = 0; z < splits; ++z) acc += part[(int64_t)z * count + i];
-    out[i] = acc;
+    if (i < count)
+        for (int z = zl; z < splits; z += 4) acc += part[(int64_t)z * count + i];
+    sh[zl][o] = acc;
+    __syncthreads();
+    if (zl == 0 && i < count) out[i] = ((sh[0][o] + sh[1][o]) + sh[2][o]) + sh[3][o];
 }
 
 template <int PASS, bool BF16>
@@ -263,6 +271,7 @@ int wgrad_splits(const ConvShape& cs, int bf16)
     const int tiles = ((N + 127) / 128) * ((M + (M <= 16 ? 15 : M <= 32 ? 31 : 63)) / (M <= 16 ? 16 : M <= 32 ? 32 : 64));
     const int64_t Kd = (int64_t)cs.n * cs.p * cs.q;
     int z = 1024 / (tiles > 0 ? tiles : 1);
+    if (z > 256) z = 256;  // bounds the partial-sum traffic (z * M * N floats)
     if (z < 1) z = 1;
     const int64_t max_z = (Kd + 4 * BK - 1) / (4 * BK);  // at least 4 BK slices per split
     if (z > max_z) z = (int)max_z;
@@ -275,6 +284,10 @@ int wgrad_splits(const ConvShape& cs, int bf16)
 hipError_t conv_fwd(const ConvShape& cs, const float* x, const float* w, const float* bias, int relu, float* y,
                     int bf16, hipStream_t st)
 {
+    if (!bf16 && !bias && !relu && cs.r == 3 && cs.s == 3 && cs.pad == 1) {
+        hipError_t e = conv3x3_direct(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, w, y, 0, false, st);
+        if (e != hipErrorNotSupported) return e;
+    }
     IgArgs a = make_args(cs);
     a.A = w; a.B = x; a.C = y; a.bias = bias; a.relu = relu;
     a.M = cs.k; a.N = cs.n * cs.p * cs.q; a.Kd = cs.c * cs.r * cs.s;
@@ -285,6 +298,11 @@ hipError_t conv_fwd(const ConvShape& cs, const float* x, const float* w, const f
 hipError_t conv_bwd_data(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate, int bf16,
                          hipStream_t st)
 {
+    if (!bf16 && cs.r == 3 && cs.s == 3 && cs.pad == 1 && cs.stride == 1) {
+        // stride-1 backward data = stride-1 conv of dy with transposed, flipped weights
+        hipError_t e = conv3x3_direct(cs.n, cs.k, cs.h, cs.w, cs.c, 1, dy, w, dx, accumulate, true, st);
+        if (e != hipErrorNotSupported) return e;
+    }
     IgArgs a = make_args(cs);
     a.A = w; a.B = dy; a.C = dx; a.accumulate = accumulate;
     a.M = cs.c; a.N = cs.n * cs.h * cs.w; a.Kd = cs.k * cs.r * cs.s;
@@ -292,9 +310,16 @@ hipError_t conv_bwd_data(const ConvShape& cs, const float* w, const float* dy, f
     return bf16 ? launch<BWD_DATA, true>(a, 1, st) : launch<BWD_DATA, false>(a, 1, st);
 }
 
+static bool use_direct_wgrad(const ConvShape& cs, int bf16)
+{
+    return !bf16 && cs.r == 3 && cs.s == 3 && cs.pad == 1 &&
+           conv3x3_wgrad_splits(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride) > 0;
+}
+
 size_t conv_bwd_weight_ws_bytes(const ConvShape& cs, int bf16)
 {
-    const int z = wgrad_splits(cs, bf16);
+    int z = wgrad_splits(cs, bf16);
+    if (use_direct_wgrad(cs, bf16)) z = std::max(z, conv3x3_wgrad_splits(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride));
     const size_t mn = (size_t)cs.k * cs.c * cs.r * cs.s;
     size_t bytes = (size_t)z * mn * sizeof(float);
     bytes += channel_sum_ws_bytes(cs.n, cs.k, cs.p * cs.q);
@@ -304,6 +329,20 @@ size_t conv_bwd_weight_ws_bytes(const ConvShape& cs, int bf16)
 hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy, float* dw, float* db, int bf16,
                            void* ws, size_t ws_bytes, hipStream_t st)
 {
+    if (ws_bytes < conv_bwd_weight_ws_bytes(cs, bf16)) return hipErrorInvalidValue;
+    const size_t mn = (size_t)cs.k * cs.c * cs.r * cs.s;
+    if (use_direct_wgrad(cs, bf16)) {
+        const int zd = conv3x3_wgrad_splits(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride);
+        hipError_t e = conv3x3_wgrad(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, (float*)ws, st);
+        if (e != hipSuccess) return e;
+        hipLaunchKernelGGL(reduce_splits, dim3((unsigned)((mn + 63) / 64)), dim3(256), 0, st, (const float*)ws, zd,
+                           (int64_t)mn, dw);
+        e = hipGetLastError();
+        if (e != hipSuccess || !db) return e;
+        const size_t zmax = conv_bwd_weight_ws_bytes(cs, bf16) - channel_sum_ws_bytes(cs.n, cs.k, cs.p * cs.q);
+        char* rest = (char*)ws + zmax;
+        return channel_sum(cs.n, cs.k, cs.p * cs.q, dy, db, rest, channel_sum_ws_bytes(cs.n, cs.k, cs.p * cs.q), st);
+    }
     const int z = wgrad_splits(cs, bf16);
     const int BK = bf16 ? 32 : 16;
     IgArgs a = make_args(cs);
@@ -312,15 +351,14 @@ hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy,
     const int64_t per = ((int64_t)a.Kd + z - 1) / z;
     a.kchunk = (int)(((per + BK - 1) / BK) * BK);
     const int zz = (int)(((int64_t)a.Kd + a.kchunk - 1) / a.kchunk);
-    const size_t mn = (size_t)a.M * a.N;
-    if (ws_bytes < conv_bwd_weight_ws_bytes(cs, bf16)) return hipErrorInvalidValue;
     hipError_t e = bf16 ? launch<BWD_WEIGHT, true>(a, zz, st) : launch<BWD_WEIGHT, false>(a, zz, st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(reduce_splits, dim3((unsigned)((mn + 255) / 256)), dim3(256), 0, st, (const float*)ws, zz,
+    hipLaunchKernelGGL(reduce_splits, dim3((unsigned)((mn + 63) / 64)), dim3(256), 0, st, (const float*)ws, zz,
                        (int64_t)mn, dw);
     e = hipGetLastError();
     if (e != hipSuccess || !db) return e;
-    char* rest = (char*)ws + (size_t)z * mn * sizeof(float);
+    const size_t zmax = conv_bwd_weight_ws_bytes(cs, bf16) - channel_sum_ws_bytes(cs.n, cs.k, cs.p * cs.q);
+    char* rest = (char*)ws + zmax;
     return channel_sum(cs.n, cs.k, cs.p * cs.q, dy, db, rest, channel_sum_ws_bytes(cs.n, cs.k, cs.p * cs.q), st);
 }
 

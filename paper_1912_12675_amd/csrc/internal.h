@@ -17,6 +17,15 @@ struct ConvShape {
 inline int conv_out_dim(int in, int k, int stride, int pad) { return (in + 2 * pad - k) / stride + 1; }
 
 // ---- convolution (implicit GEMM on MFMA) ----
+// Direct 3x3 / pad 1 kernel (forward, or backward-data of a stride-1 layer
+// when transpose is set); hipErrorNotSupported when no tile config fits.
+hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const float* x, const float* w, float* y,
+                          int accumulate, bool transpose, hipStream_t st);
+// Backward-weight partial sums of a 3x3 / pad 1 conv (dW-shaped, one per
+// workgroup); conv3x3_wgrad_splits is 0 when no configuration covers it.
+int conv3x3_wgrad_splits(int n, int C, int H, int W, int K, int stride);
+hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const float* x, const float* dy, float* part,
+                         hipStream_t st);
 hipError_t conv_fwd(const ConvShape& cs, const float* x, const float* w, const float* bias, int relu,
                     float* y, int bf16, hipStream_t st);
 hipError_t conv_bwd_data(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate,

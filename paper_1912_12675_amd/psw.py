@@ -114,6 +114,8 @@ def _ptr(t):
             raise ValueError("libpsw takes device tensors")
         if not t.is_contiguous():
             raise ValueError("libpsw takes contiguous tensors")
+        if t.dtype not in (torch.float32, torch.int32, torch.uint8):
+            raise TypeError(f"libpsw takes float32 / int32 buffers (workspaces uint8), got {t.dtype}")
         return t.data_ptr()
     raise TypeError(type(t))
 

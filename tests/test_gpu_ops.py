@@ -57,6 +57,14 @@ CONV = [
     (1, 33, 7, 9, 70, 3, 1, 1),
     (5, 3, 6, 6, 4, 1, 1, 0),
     (1, 64, 4, 4, 130, 3, 1, 1),
+    # shapes of the direct 3x3 kernel: ResNet groups 1-3, the stride-2
+    # transitions, VGG layers with several input-channel chunks and
+    # several output-channel blocks
+    (3, 32, 16, 16, 32, 3, 1, 1),
+    (2, 64, 32, 32, 64, 3, 1, 1),
+    (2, 128, 16, 16, 128, 3, 1, 1),
+    (2, 256, 8, 8, 256, 3, 1, 1),
+    (3, 16, 16, 16, 64, 3, 2, 1),
 ]
 
 

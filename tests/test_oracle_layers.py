@@ -9,7 +9,6 @@ import pytest
 import torch
 import torch.nn.functional as F
 
-torch.set_default_dtype(torch.float64)
 
 CONV_CASES = [
     # N, C, H, W, K, R, stride, pad
@@ -108,7 +107,7 @@ def test_bn_vs_torch(oracle, residual, relu):
     elif residual == "optionA":
         res = rng.standard_normal((N, C // 2, 2 * H, 2 * W))
     yt, gt, bt = _t(y, True), _t(g, True), _t(be, True)
-    rm_t, rv_t = torch.zeros(C), torch.ones(C)
+    rm_t, rv_t = torch.zeros(C, dtype=torch.float64), torch.ones(C, dtype=torch.float64)
     zt = F.batch_norm(yt, rm_t, rv_t, gt, bt, training=True, momentum=0.1, eps=1e-5)
     rt = None
     if res is not None:

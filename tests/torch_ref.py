@@ -13,8 +13,6 @@ import torch.nn.functional as F
 
 from paper_1912_12675_amd.synth import BN, CONV, F_BIAS, F_RELU, FC, GAVG, MAXPOOL
 
-torch.set_default_dtype(torch.float64)
-
 
 def op_param_slices(ops, stage_end):
     """Per op: (stage, [(name, offset, shape)]) in the flat per-stage layout."""
@@ -95,8 +93,9 @@ def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5
     return t
 
 
-def running_stats(ops):
-    return {i: (torch.zeros(int(o[3])), torch.ones(int(o[3]))) for i, o in enumerate(ops) if int(o[0]) == BN}
+def running_stats(ops, dtype=torch.float64):
+    return {i: (torch.zeros(int(o[3]), dtype=dtype), torch.ones(int(o[3]), dtype=dtype))
+            for i, o in enumerate(ops) if int(o[0]) == BN}
 
 
 def split_flat(flat, counts):
@@ -111,7 +110,8 @@ def train_nonpipelined(ops, stage_end, params0, xs, labels, lr, mom=0.9, wd=0.0,
     """Plain mini-batch SGD (every staleness 0) with autograd and
     torch.optim.SGD.  Returns (final flat params, losses, running stats)."""
     slices, counts = op_param_slices(ops, stage_end)
-    flat = [torch.tensor(p, requires_grad=True) for p in split_flat(np.asarray(params0, np.float64), counts)]
+    flat = [torch.tensor(p, dtype=torch.float64, requires_grad=True)
+            for p in split_flat(np.asarray(params0, np.float64), counts)]
     lrs = np.broadcast_to(np.asarray(lr, dtype=np.float64), (len(counts),))
     opt = torch.optim.SGD([{"params": [p], "lr": float(lrs[s])} for s, p in enumerate(flat)],
                           lr=float(lrs[0]), momentum=mom, weight_decay=wd, nesterov=nesterov)
@@ -236,3 +236,45 @@ def simulate_register_pipeline(ops, stage_end, params0, xs, labels, lr, mom=0.9,
             n_updates[i] += 1
     last_cycle = max(z[0] for z in tasks)
     return torch.cat([w.detach() for w in W]).double().numpy(), losses, versions, last_cycle
+
+
+def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=0.0, dtype=torch.float64):
+    """The stale-weight schedule written with autograd, for any staleness
+    table (hybrid included): keep every stage's version history; for step t
+    load version max(0, t - d_s) into the stage's weight tensor and run the
+    forward pass; then overwrite that tensor IN PLACE with version t and run
+    backward (autograd holds the tensor by reference, so data gradients see
+    version t while weight gradients use the saved activations); append
+    version t+1 = SGD(version t).  Returns (final flat params, losses,
+    versions)."""
+    slices, counts = op_param_slices(ops, stage_end)
+    S = len(counts)
+    hist = [[torch.tensor(p, dtype=dtype)] for p in split_flat(np.asarray(params0, np.float64), counts)]
+    Wp = [torch.zeros(c, dtype=dtype, requires_grad=True) for c in counts]
+    V = [torch.zeros(c, dtype=dtype) for c in counts]
+    lrs = np.broadcast_to(np.asarray(lr, dtype=np.float64), (S,))
+    T = len(xs)
+    st = np.asarray(staleness).reshape(T, S)
+    n = len(ops)
+    losses = np.zeros(T)
+    versions = np.zeros((T, S), dtype=np.int32)
+    for t in range(T):
+        for s in range(S):
+            r = max(0, t - int(st[t, s]))
+            versions[t, s] = r
+            with torch.no_grad():
+                Wp[s].copy_(hist[s][r])
+            Wp[s].grad = None
+        outs = run_ops(ops, 0, n, {0: torch.tensor(xs[t], dtype=dtype)}, Wp, slices)
+        loss = F.cross_entropy(outs[n].reshape(outs[n].shape[0], -1), torch.tensor(labels[t], dtype=torch.long))
+        losses[t] = float(loss.detach())
+        with torch.no_grad():
+            for s in range(S):
+                Wp[s].data.copy_(hist[s][t])
+        loss.backward()
+        with torch.no_grad():
+            for s in range(S):
+                g = Wp[s].grad if Wp[s].grad is not None else torch.zeros_like(V[s])
+                V[s].mul_(mom).add_(g + wd * hist[s][t])
+                hist[s].append(hist[s][t] - float(lrs[s]) * V[s])
+    return torch.cat([h[-1] for h in hist]).double().numpy(), losses, versions
