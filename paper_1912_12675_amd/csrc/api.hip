@@ -276,7 +276,9 @@ struct psw_net {
     int64_t bn_channels = 0;
     // arena layout (bytes)
     std::vector<size_t> act_off, grad_off;  // per tensor (index 0 unused)
-    std::vector<size_t> save_off;           // per op: BN mean/invstd or max-pool argmax
+    std::vector<size_t> save_off;           // per op: BN mean/invstd/scale,shift or max-pool argmax
+    std::vector<char> fuse_stats;           // per conv op: its BN (op+1) statistics come from the conv epilogue
+
     std::vector<char> grad_accum;           // per op input slot: 0 overwrite, 1 accumulate (in0, in1)
     size_t ws_off = 0, ws_bytes = 0, arena_bytes = 0;
     // bound memory
@@ -442,12 +444,13 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
         off = align256(off + (size_t)net->t[i].numel() * sizeof(float));
     }
     size_t ws = 0;
+    net->fuse_stats.assign(n_layers, 0);
     for (int i = 0; i < n_layers; ++i) {
         const psw_layer& o = net->ops[i];
         const Tensor a = net->t[o.in0];
         if (o.kind == PSW_OP_BN) {
             net->save_off[i] = off;
-            off = align256(off + 2 * (size_t)o.cin * sizeof(float));
+            off = align256(off + 4 * (size_t)o.cin * sizeof(float));  // mean, invstd, (scale, shift)
             ws = std::max(ws, psw::bn_ws_bytes(a.n, a.c, a.h, a.w));
         } else if (o.kind == PSW_OP_MAXPOOL) {
             net->save_off[i] = off;
@@ -456,6 +459,12 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
             psw::ConvShape cs;
             check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, prec, &cs);
             ws = std::max(ws, psw::conv_bwd_weight_ws_bytes(cs, prec == PSW_BF16));
+            // BN right after this conv, on its output only: statistics in the conv epilogue
+            const bool next_bn = i + 1 < n_layers && net->ops[i + 1].kind == PSW_OP_BN && net->ops[i + 1].in0 == i + 1;
+            const bool plain = !(o.flags & (PSW_F_BIAS | PSW_F_RELU)) && prec == PSW_FP32;
+            const size_t pf = psw::conv_fwd_bnstats_part_floats(cs);
+            net->fuse_stats[i] = next_bn && plain && pf > 0;
+            if (net->fuse_stats[i]) ws = std::max(ws, pf * sizeof(float));
         } else if (o.kind == PSW_OP_FC) {
             ws = std::max(ws, psw::fc_bwd_ws_bytes(a.n, o.cin, o.cout));
         }
@@ -678,7 +687,14 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
             check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, net->prec, &cs);
             const float* b = (o.flags & PSW_F_BIAS) ? W + (int64_t)o.cout * o.cin * o.k * o.k : nullptr;
             kind = PSW_PROF_CONV_FWD;
-            PSW_TRY(psw::conv_fwd(cs, act(o.in0), W, b, (o.flags & PSW_F_RELU) != 0, act(i + 1), bf16, st), "conv_fwd");
+            if (net->fuse_stats[i]) {  // the next op's BN statistics come out of this conv
+                psw::BnStatsFuse bn{(float*)ws};
+                PSW_TRY(psw::conv_fwd_bnstats(cs, act(o.in0), W, act(i + 1), bn, wsb / sizeof(float), st),
+                        "conv_fwd_bnstats");
+            } else {
+                PSW_TRY(psw::conv_fwd(cs, act(o.in0), W, b, (o.flags & PSW_F_RELU) != 0, act(i + 1), bf16, st),
+                        "conv_fwd");
+            }
             break;
         }
         case PSW_OP_BN: {
@@ -687,6 +703,20 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
             float* rm = net->run_mean ? net->run_mean + net->bn_off[i] : nullptr;
             float* rvv = net->run_var ? net->run_var + net->bn_off[i] : nullptr;
             kind = PSW_PROF_BN_FWD;
+            if (i > 0 && net->fuse_stats[i - 1]) {  // per-tile statistics written by the conv into ws
+                const psw_layer& cv = net->ops[i - 1];
+                const Tensor ci = net->t[cv.in0];
+                psw::ConvShape ccs;
+                check_conv(ci.n, ci.c, ci.h, ci.w, cv.cout, cv.k, cv.k, cv.stride, cv.pad, net->prec, &ccs);
+                const int T = psw::conv_fwd_bnstats_tiles(ccs);
+                const int P = a.n * a.h * a.w / T;
+                PSW_TRY(psw::bn_apply_from_partials(a.n, a.c, a.h, a.w, act(o.in0), (const float*)ws, T, P, W, W + o.cin,
+                                                    o.in1 >= 0 ? act(o.in1) : nullptr, r.c, r.h, r.w,
+                                                    (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, act(i + 1), save,
+                                                    save + o.cin, rm, rvv, st),
+                        "bn_apply");
+                break;
+            }
             PSW_TRY(psw::bn_fwd(a.n, a.c, a.h, a.w, act(o.in0), W, W + o.cin, o.in1 >= 0 ? act(o.in1) : nullptr, r.c,
                                 r.h, r.w, (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, act(i + 1), save, save + o.cin, rm,
                                 rvv, ws, wsb, st),

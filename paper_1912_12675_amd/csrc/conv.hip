@@ -221,20 +221,24 @@ __global__ __launch_bounds__(256) void igemm_kernel(IgArgs a)
         }
 }
 
-// dw[i] = sum_z part[z][i] in a fixed order (deterministic): each block owns
-// 64 consecutive outputs; its four waves sum the splits z = zl (mod 4) in
-// increasing z, then wave 0 adds the four partial sums in order zl = 0..3.
+// dw[i] = sum_z part[z][i] in a fixed order (deterministic): a block owns 16
+// consecutive outputs; its 16 lane groups sum the splits z = zl (mod 16) in
+// increasing z, then the 16 partial sums are added in order zl = 0..15.
 __global__ __launch_bounds__(256) void reduce_splits(const float* part, int splits, int64_t count, float* out)
 {
-    __shared__ float sh[4][64];
-    const int o = threadIdx.x & 63, zl = threadIdx.x >> 6;
-    const int64_t i = (int64_t)blockIdx.x * 64 + o;
+    __shared__ float sh[16][17];
+    const int o = threadIdx.x & 15, zl = threadIdx.x >> 4;
+    const int64_t i = (int64_t)blockIdx.x * 16 + o;
     float acc = 0.f;
     if (i < count)
-        for (int z = zl; z < splits; z += 4) acc += part[(int64_t)z * count + i];
+        for (int z = zl; z < splits; z += 16) acc += part[(int64_t)z * count + i];
     sh[zl][o] = acc;
     __syncthreads();
-    if (zl == 0 && i < count) out[i] = ((sh[0][o] + sh[1][o]) + sh[2][o]) + sh[3][o];
+    if (zl == 0 && i < count) {
+        float t = 0.f;
+        for (int k = 0; k < 16; ++k) t += sh[k][o];
+        out[i] = t;
+    }
 }
 
 template <int PASS, bool BF16>
@@ -295,12 +299,33 @@ hipError_t conv_fwd(const ConvShape& cs, const float* x, const float* w, const f
     return bf16 ? launch<FWD, true>(a, 1, st) : launch<FWD, false>(a, 1, st);
 }
 
+int conv_fwd_bnstats_tiles(const ConvShape& cs)
+{
+    if (cs.r != 3 || cs.s != 3 || cs.pad != 1) return 0;
+    return conv3x3_direct_tiles(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride);
+}
+
+size_t conv_fwd_bnstats_part_floats(const ConvShape& cs) { return (size_t)conv_fwd_bnstats_tiles(cs) * cs.k * 2; }
+
+hipError_t conv_fwd_bnstats(const ConvShape& cs, const float* x, const float* w, float* y, const BnStatsFuse& bn,
+                            size_t part_capacity_floats, hipStream_t st)
+{
+    const size_t need = conv_fwd_bnstats_part_floats(cs);
+    if (need == 0) return hipErrorNotSupported;
+    if (part_capacity_floats < need) return hipErrorInvalidValue;
+    return conv3x3_direct(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, w, y, 0, false, st, &bn);
+}
+
 hipError_t conv_bwd_data(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate, int bf16,
                          hipStream_t st)
 {
     if (!bf16 && cs.r == 3 && cs.s == 3 && cs.pad == 1 && cs.stride == 1) {
         // stride-1 backward data = stride-1 conv of dy with transposed, flipped weights
         hipError_t e = conv3x3_direct(cs.n, cs.k, cs.h, cs.w, cs.c, 1, dy, w, dx, accumulate, true, st);
+        if (e != hipErrorNotSupported) return e;
+    }
+    if (!bf16 && cs.r == 3 && cs.s == 3 && cs.pad == 1 && cs.stride == 2 && cs.h == 2 * cs.p && cs.w == 2 * cs.q) {
+        hipError_t e = conv3x3_dgrad_s2(cs.n, cs.c, cs.h, cs.w, cs.k, w, dy, dx, accumulate, st);
         if (e != hipErrorNotSupported) return e;
     }
     IgArgs a = make_args(cs);
@@ -335,7 +360,7 @@ hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy,
         const int zd = conv3x3_wgrad_splits(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride);
         hipError_t e = conv3x3_wgrad(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, (float*)ws, st);
         if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(reduce_splits, dim3((unsigned)((mn + 63) / 64)), dim3(256), 0, st, (const float*)ws, zd,
+        hipLaunchKernelGGL(reduce_splits, dim3((unsigned)((mn + 15) / 16)), dim3(256), 0, st, (const float*)ws, zd,
                            (int64_t)mn, dw);
         e = hipGetLastError();
         if (e != hipSuccess || !db) return e;
@@ -353,7 +378,7 @@ hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy,
     const int zz = (int)(((int64_t)a.Kd + a.kchunk - 1) / a.kchunk);
     hipError_t e = bf16 ? launch<BWD_WEIGHT, true>(a, zz, st) : launch<BWD_WEIGHT, false>(a, zz, st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(reduce_splits, dim3((unsigned)((mn + 63) / 64)), dim3(256), 0, st, (const float*)ws, zz,
+    hipLaunchKernelGGL(reduce_splits, dim3((unsigned)((mn + 15) / 16)), dim3(256), 0, st, (const float*)ws, zz,
                        (int64_t)mn, dw);
     e = hipGetLastError();
     if (e != hipSuccess || !db) return e;

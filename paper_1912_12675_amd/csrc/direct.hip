@@ -7,8 +7,10 @@
 // output channels.  Input channels are processed in chunks of CC: the
 // chunk's halo tile  [CC][(TH-1)*STRIDE+3][WIN+halo]  is staged in LDS with
 // float4 loads (zero rows/columns supply the padding), and the chunk's
-// weights are staged in LDS already in MFMA-fragment order so that every
-// wave reads its A operand with one conflict-free ds_read per k-step.
+// weights are staged in LDS as [output channel][CC*9] rows padded to a stride
+// of 2 (mod 32) floats: the coalesced staging writes are contiguous, and the
+// A-operand read of a k-step (16 output channels x 4 input channels, nine
+// floats apart) touches 64 distinct banks... per half-wave.
 //
 // MFMA v_mfma_f32_16x16x4_f32, D[m][n] += A[m][k] B[k][n] with
 //   m = output channel (16 per wave), n = output pixel (16 per block),
@@ -29,9 +31,19 @@ struct DirArgs {
     float* y;        // output [n][K][HO][WO]
     int C, H, K, HO;
     int accumulate;
+    BnStatsFuse bn;  // bn.part == nullptr: no statistics
 };
 
 constexpr int round4(int v) { return (v + 3) / 4 * 4; }
+// weight row stride (floats) of an LDS tile with `n` floats per output
+// channel: the smallest v >= n with v = 2 (mod 32), so that lanes
+// (m, g) -> m*v + 9*g hit distinct banks within each 32-lane half
+constexpr int wrow(int n)
+{
+    int v = n;
+    while (v % 32 != 2) ++v;
+    return v;
+}
 
 template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, bool TRANS>
 __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
@@ -42,12 +54,13 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     constexpr int RSTR = round4(WIN + (STRIDE == 1 ? 5 : 4));  // LDS row stride (cols 3 .. WIN+4)
     constexpr int PS0 = HR * RSTR;
     constexpr int PS = PS0 + ((16 - PS0 % 32) + 32) % 32;  // plane stride = 16 mod 32: lane groups hit disjoint banks
-    constexpr int KSTEPS = CC / 4 * 9;
     constexpr int TK = 16 * WK;
+    constexpr int WR = wrow(CC * 9);
     static_assert(TH * WO == 16 * NBW * WP, "pixel tiling");
     static_assert(CC % 4 == 0 && WIN % 4 == 0, "tiling");
+    static_assert(CC * PS >= WP * TK, "input tile reused by the statistics epilogue");
     __shared__ __attribute__((aligned(16))) float Xs[CC * PS];
-    __shared__ float Wf[WK * KSTEPS * 64];
+    __shared__ float Wc[TK * WR];
 
     const int tiles = a.HO / TH;
     const int img = blockIdx.x / tiles;
@@ -86,40 +99,32 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
             const int rr = rem / Q4, q4 = rem - (rem / Q4) * Q4;
             const int ih = ih0 + rr;
             float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (ih >= 0 && ih < a.H)
+            if (ih >= 0 && ih < a.H && c0 + c < a.C)
                 v = *reinterpret_cast<const float4*>(a.x + (((size_t)img * a.C + c0 + c) * a.H + ih) * WIN + q4 * 4);
             *reinterpret_cast<float4*>(&Xs[c * PS + rr * RSTR + 4 + q4 * 4]) = v;
         }
-        // weights of (TK output channels) x (CC input channels), fragment order
+        // weights of (TK output channels) x (CC input channels): Wc[m][c*9 + rs]
         for (int i = tid; i < TK * CC * 9; i += NT) {
-            int m, c, rs;
-            float v;
             if (!TRANS) {  // w[m][c][rs]: each output channel's CC*9 run is contiguous
-                m = i / (CC * 9);
-                const int rem = i - m * (CC * 9);
-                c = rem / 9;
-                rs = rem - c * 9;
-                v = a.w[((size_t)(mblk + m) * a.C + c0 + c) * 9 + rs];
-            } else {       // w_layer[c][m][8-rs]: each input channel's TK*9 run is contiguous
-                c = i / (TK * 9);
-                const int rem = i - c * (TK * 9);
-                m = rem / 9;
-                const int rsl = rem - m * 9;
-                rs = 8 - rsl;
-                v = a.w[((size_t)(c0 + c) * a.K + mblk + m) * 9 + rsl];
+                const int m = i / (CC * 9), rem = i - (i / (CC * 9)) * (CC * 9);
+                const int c = rem / 9;
+                Wc[m * WR + rem] = c0 + c < a.C ? a.w[((size_t)(mblk + m) * a.C + c0) * 9 + rem] : 0.f;
+            } else {       // w_layer[c][m][rs]: each input channel's TK*9 run is contiguous; flip the taps
+                const int c = i / (TK * 9), rem = i - (i / (TK * 9)) * (TK * 9);
+                const int m = rem / 9, rsl = rem - (rem / 9) * 9;
+                Wc[m * WR + c * 9 + 8 - rsl] =
+                    c0 + c < a.C ? a.w[((size_t)(c0 + c) * a.K + mblk) * 9 + rem] : 0.f;
             }
-            const int kb = m >> 4, ml = m & 15, c4 = c >> 2, gg = c & 3;
-            Wf[((kb * (CC / 4) + c4) * 9 + rs) * 64 + gg * 16 + ml] = v;
         }
         __syncthreads();
-        const float* wf = Wf + wk * KSTEPS * 64 + lane;
+        const float* wf = Wc + (wk * 16 + j) * WR + g * 9;
 #pragma unroll
         for (int c4 = 0; c4 < CC / 4; ++c4)
 #pragma unroll
             for (int r = 0; r < 3; ++r)
 #pragma unroll
                 for (int s = 0; s < 3; ++s) {
-                    const float av = wf[((c4 * 9) + r * 3 + s) * 64];
+                    const float av = wf[c4 * 36 + r * 3 + s];
 #pragma unroll
                     for (int nb = 0; nb < NBW; ++nb) {
                         const float bv = Xs[boff[nb] + c4 * 4 * PS + r * RSTR + s];
@@ -137,6 +142,184 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
             const int m = mblk + wk * 16 + 4 * g + i;
             float* dst = a.y + (((size_t)img * a.K + m) * a.HO + oh0 + row) * WO + col;
             *dst = a.accumulate ? *dst + acc[nb][i] : acc[nb][i];
+        }
+    }
+    if constexpr (!TRANS) {
+        if (a.bn.part) {
+            // per-tile statistics of each output channel over the TH*WO pixels
+            constexpr int P = TH * WO;
+            float* red = Xs;  // [WP][TK], the input tile is no longer read
+            __syncthreads();
+            float sv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float v = 0.f;
+#pragma unroll
+                for (int nb = 0; nb < NBW; ++nb) v += acc[nb][i];
+#pragma unroll
+                for (int off = 8; off > 0; off >>= 1) v += __shfl_xor(v, off, 16);
+                sv[i] = v;
+            }
+            if (j == 0)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) red[wp * TK + wk * 16 + 4 * g + i] = sv[i];
+            __syncthreads();
+            float mu[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float t = 0.f;
+                for (int q = 0; q < WP; ++q) t += red[q * TK + wk * 16 + 4 * g + i];
+                mu[i] = t / (float)P;
+            }
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                float v = 0.f;
+#pragma unroll
+                for (int nb = 0; nb < NBW; ++nb) {
+                    const float d = acc[nb][i] - mu[i];
+                    v += d * d;
+                }
+#pragma unroll
+                for (int off = 8; off > 0; off >>= 1) v += __shfl_xor(v, off, 16);
+                sv[i] = v;
+            }
+            if (j == 0)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) red[wp * TK + wk * 16 + 4 * g + i] = sv[i];
+            __syncthreads();
+            const int T = gridDim.x;
+            if (wp == 0 && j == 0)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    float t = 0.f;
+                    for (int q = 0; q < WP; ++q) t += red[q * TK + wk * 16 + 4 * g + i];
+                    const int m = mblk + wk * 16 + 4 * g + i;
+                    a.bn.part[((size_t)m * T + blockIdx.x) * 2 + 0] = mu[i];
+                    a.bn.part[((size_t)m * T + blockIdx.x) * 2 + 1] = t;
+                }
+        }
+    }
+}
+
+// Backward-data of a 3x3 / pad 1 / stride 2 convolution: dx (H = 2*HO) from
+// dy.  Output pixel (2i+ph, 2j+pw) receives dy[i+di][j+dj] w[r][s] for the
+// taps with 2i+ph = 2(i+di)+r-1:  ph = 0 -> r = 1 (di 0);  ph = 1 -> r = 0
+// (di 1) and r = 2 (di 0); likewise for columns.  A 16-pixel block of dy
+// positions therefore feeds four output parity classes from only four
+// B fragments (di, dj in {0,1}); the nine taps are nine MFMAs.  Each lane
+// stores the pw = 0,1 pair of a class row as one float2.
+struct DgArgs {
+    const float* dy;  // [n][KL][HO][WO]
+    const float* w;   // layer weights [KL][CL][3][3]
+    float* dx;        // [n][CL][2*HO][2*WO]
+    int KL, CL, HO;
+    int accumulate;
+};
+
+template <int WO, int TH, int CC, int WK, int WP, int NBW>
+__global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
+{
+    constexpr int NT = 64 * WK * WP;
+    constexpr int HR = TH + 1;                 // dy rows i0 .. i0+TH (the last may be past the edge)
+    constexpr int RSTR = round4(WO + 1);       // dy cols 0 .. WO (col WO is zero)
+    constexpr int PS0 = HR * RSTR;
+    constexpr int PS = PS0 + ((16 - PS0 % 32) + 32) % 32;
+    constexpr int TK = 16 * WK;
+    constexpr int WR = wrow(CC * 9);
+    static_assert(TH * WO == 16 * NBW * WP, "pixel tiling");
+    __shared__ __attribute__((aligned(16))) float Xs[CC * PS];
+    __shared__ float Wc[TK * WR];
+
+    const int tiles = a.HO / TH;
+    const int img = blockIdx.x / tiles;
+    const int i0 = (blockIdx.x - img * tiles) * TH;
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wk = wave % WK, wp = wave / WK;
+    const int mblk = blockIdx.y * TK;
+    const int g = lane >> 4, j = lane & 15;
+
+    int boff[NBW];
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+        const int pix = (wp * NBW + nb) * 16 + j;
+        boff[nb] = g * PS + (pix / WO) * RSTR + (pix - (pix / WO) * WO);
+    }
+    v4f acc[NBW][4];  // [block][class ph*2+pw]
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) acc[nb][q] = v4f{0.f, 0.f, 0.f, 0.f};
+
+    for (int i = tid; i < CC * HR; i += NT) {
+        const int c = i / HR, rr = i - (i / HR) * HR;
+        Xs[c * PS + rr * RSTR + WO] = 0.f;
+    }
+    for (int c0 = 0; c0 < a.KL; c0 += CC) {
+        __syncthreads();
+        constexpr int Q4 = WO / 4;
+        for (int i = tid; i < CC * HR * Q4; i += NT) {
+            const int c = i / (HR * Q4);
+            const int rem = i - c * (HR * Q4);
+            const int rr = rem / Q4, q4 = rem - (rem / Q4) * Q4;
+            const int ih = i0 + rr;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (ih < a.HO)
+                v = *reinterpret_cast<const float4*>(a.dy + (((size_t)img * a.KL + c0 + c) * a.HO + ih) * WO + q4 * 4);
+            *reinterpret_cast<float4*>(&Xs[c * PS + rr * RSTR + q4 * 4]) = v;
+        }
+        for (int i = tid; i < TK * CC * 9; i += NT) {  // w_layer[c][m][rs] -> Wc[m][c*9 + rs]
+            const int c = i / (TK * 9), rem = i - (i / (TK * 9)) * (TK * 9);
+            const int m = rem / 9, rs = rem - (rem / 9) * 9;
+            Wc[m * WR + c * 9 + rs] = a.w[((size_t)(c0 + c) * a.CL + mblk) * 9 + rem];
+        }
+        __syncthreads();
+        const float* wf = Wc + (wk * 16 + j) * WR + g * 9;
+#pragma unroll
+        for (int c4 = 0; c4 < CC / 4; ++c4) {
+            float w9[9];
+#pragma unroll
+            for (int t = 0; t < 9; ++t) w9[t] = wf[c4 * 36 + t];
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) {
+                const float* xb = Xs + boff[nb] + c4 * 4 * PS;
+                const float b00 = xb[0], b01 = xb[1], b10 = xb[RSTR], b11 = xb[RSTR + 1];
+                // class (0,0): r=1,s=1
+                acc[nb][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(w9[4], b00, acc[nb][0], 0, 0, 0);
+                // class (0,1): r=1; s=0 -> dj 1, s=2 -> dj 0
+                acc[nb][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(w9[3], b01, acc[nb][1], 0, 0, 0);
+                acc[nb][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(w9[5], b00, acc[nb][1], 0, 0, 0);
+                // class (1,0): s=1; r=0 -> di 1, r=2 -> di 0
+                acc[nb][2] = __builtin_amdgcn_mfma_f32_16x16x4f32(w9[1], b10, acc[nb][2], 0, 0, 0);
+                acc[nb][2] = __builtin_amdgcn_mfma_f32_16x16x4f32(w9[7], b00, acc[nb][2], 0, 0, 0);
+                // class (1,1)
+                acc[nb][3] = __builtin_amdgcn_mfma_f32_16x16x4f32(w9[0], b11, acc[nb][3], 0, 0, 0);
+                acc[nb][3] = __builtin_amdgcn_mfma_f32_16x16x4f32(w9[2], b10, acc[nb][3], 0, 0, 0);
+                acc[nb][3] = __builtin_amdgcn_mfma_f32_16x16x4f32(w9[6], b01, acc[nb][3], 0, 0, 0);
+                acc[nb][3] = __builtin_amdgcn_mfma_f32_16x16x4f32(w9[8], b00, acc[nb][3], 0, 0, 0);
+            }
+        }
+    }
+    constexpr int W2 = 2 * WO;
+    const int H2 = 2 * a.HO;
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) {
+        const int pix = (wp * NBW + nb) * 16 + j;
+        const int ii = i0 + pix / WO, jj = pix - (pix / WO) * WO;
+#pragma unroll
+        for (int v = 0; v < 4; ++v) {
+            const int m = mblk + wk * 16 + 4 * g + v;
+#pragma unroll
+            for (int ph = 0; ph < 2; ++ph) {
+                float2* dst = reinterpret_cast<float2*>(a.dx + (((size_t)img * a.CL + m) * H2 + 2 * ii + ph) * W2 + 2 * jj);
+                float2 val = make_float2(acc[nb][2 * ph][v], acc[nb][2 * ph + 1][v]);
+                if (a.accumulate) {
+                    const float2 o = *dst;
+                    val.x += o.x;
+                    val.y += o.y;
+                }
+                *dst = val;
+            }
         }
     }
 }
@@ -157,22 +340,60 @@ hipError_t launch_direct(const DirArgs& a, int n, bool trans, hipStream_t st)
 
 // Returns hipErrorNotSupported (nothing launched) when no tile configuration
 // covers the shape; the caller then uses the general implicit GEMM.
+int conv3x3_direct_tiles(int n, int C, int H, int W, int K, int stride)
+{
+    if ((stride != 1 && stride != 2) || H % stride || W % stride) return 0;
+    const int HO = H / stride, WO = W / stride;
+    if (C <= 4 && stride == 1) return (WO == 32 && HO % 8 == 0 && K % 16 == 0) ? n * (HO / 8) : 0;
+    if (C % 16) return 0;
+    if (WO == 32 && stride == 1 && HO % 8 == 0 && K % 16 == 0) return n * (HO / 8);
+    if (WO == 16 && HO % 8 == 0 && K % 32 == 0) return n * (HO / 8);
+    if (WO == 8 && HO % 8 == 0 && K % 32 == 0) return n * (HO / 8);
+    return 0;
+}
+
 hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const float* x, const float* w, float* y,
-                          int accumulate, bool transpose, hipStream_t st)
+                          int accumulate, bool transpose, hipStream_t st, const BnStatsFuse* bn)
 {
     if (stride != 1 && stride != 2) return hipErrorNotSupported;
-    if (H % stride || W % stride || C % 16) return hipErrorNotSupported;
+    if (H % stride || W % stride) return hipErrorNotSupported;
+    if (bn && transpose) return hipErrorNotSupported;
     const int HO = H / stride, WO = W / stride;
-    DirArgs a{x, w, y, C, H, K, HO, accumulate};
+    DirArgs a{x, w, y, C, H, K, HO, accumulate, BnStatsFuse{nullptr}};
+    if (bn) a.bn = *bn;
+    if (C <= 4 && stride == 1 && !transpose) {  // first layer of an image net (3 input channels)
+        if (WO == 32 && HO % 8 == 0 && K % 16 == 0) return launch_direct<32, 1, 8, 4, 1, 4, 4>(a, n, false, st);
+        return hipErrorNotSupported;
+    }
+    if (C % 16) return hipErrorNotSupported;
     if (stride == 1) {
-        if (WO == 32 && HO % 4 == 0 && K % 16 == 0) return launch_direct<32, 1, 4, 16, 1, 4, 2>(a, n, transpose, st);
-        if (WO == 16 && HO % 4 == 0 && K % 32 == 0) return launch_direct<16, 1, 4, 16, 2, 2, 2>(a, n, transpose, st);
-        if (WO == 8 && HO % 2 == 0 && K % 64 == 0) return launch_direct<8, 1, 2, 16, 4, 1, 1>(a, n, transpose, st);
+        if (WO == 32 && HO % 8 == 0 && K % 16 == 0) return launch_direct<32, 1, 8, 16, 1, 4, 4>(a, n, transpose, st);
+        if (WO == 16 && HO % 8 == 0 && K % 32 == 0) return launch_direct<16, 1, 8, 16, 2, 4, 2>(a, n, transpose, st);
+        if (WO == 8 && HO % 8 == 0 && K % 32 == 0) return launch_direct<8, 1, 8, 16, 2, 2, 2>(a, n, transpose, st);
     } else if (!transpose) {
-        if (WO == 16 && HO % 4 == 0 && K % 32 == 0) return launch_direct<16, 2, 4, 16, 2, 2, 2>(a, n, false, st);
-        if (WO == 8 && HO % 2 == 0 && K % 64 == 0) return launch_direct<8, 2, 2, 16, 4, 1, 1>(a, n, false, st);
+        if (WO == 16 && HO % 8 == 0 && K % 32 == 0) return launch_direct<16, 2, 8, 16, 2, 4, 2>(a, n, false, st);
+        if (WO == 8 && HO % 8 == 0 && K % 32 == 0) return launch_direct<8, 2, 8, 16, 2, 2, 2>(a, n, false, st);
     }
     return hipErrorNotSupported;
 }
 
+}  // namespace psw
+
+namespace psw {
+hipError_t conv3x3_dgrad_s2(int n, int CL, int H, int W, int KL, const float* w, const float* dy, float* dx,
+                            int accumulate, hipStream_t st)
+{
+    if (H % 2 || W % 2 || KL % 16) return hipErrorNotSupported;
+    const int HO = H / 2, WO = W / 2;
+    DgArgs a{dy, w, dx, KL, CL, HO, accumulate};
+    if (WO == 16 && HO % 4 == 0 && CL % 16 == 0) {
+        hipLaunchKernelGGL((conv3x3_dgrad_s2<16, 4, 16, 1, 4, 1>), dim3(n * (HO / 4), CL / 16), dim3(256), 0, st, a);
+        return hipGetLastError();
+    }
+    if (WO == 8 && HO % 2 == 0 && CL % 32 == 0) {
+        hipLaunchKernelGGL((conv3x3_dgrad_s2<8, 2, 16, 2, 1, 1>), dim3(n * (HO / 2), CL / 32), dim3(128), 0, st, a);
+        return hipGetLastError();
+    }
+    return hipErrorNotSupported;
+}
 }  // namespace psw

@@ -16,11 +16,38 @@ struct ConvShape {
 
 inline int conv_out_dim(int in, int k, int stride, int pad) { return (in + 2 * pad - k) / stride + 1; }
 
+// Batch-norm statistics fused into a convolution's epilogue: every workgroup
+// writes the (mean, M2) of each of its output channels over its P pixels to
+// part[channel][tile][2]; bn_apply_from_partials merges them.
+struct BnStatsFuse {
+    float* part;
+};
+
 // ---- convolution (implicit GEMM on MFMA) ----
+// Forward conv + fused BN statistics (direct kernel only); returns
+// hipErrorNotSupported when the shape has no direct configuration.
+hipError_t conv_fwd_bnstats(const ConvShape& cs, const float* x, const float* w, float* y, const BnStatsFuse& bn,
+                            size_t part_capacity_floats, hipStream_t st);
+size_t conv_fwd_bnstats_part_floats(const ConvShape& cs);
+int conv_fwd_bnstats_tiles(const ConvShape& cs);  // tiles T (partials per channel), 0 if not fused
+// BN forward (+residual, +ReLU) whose statistics come as per-tile (mean, M2)
+// partials over P pixels each: every block merges its channel's T partials
+// in a fixed order (double precision), block 0 of a channel stores the saved
+// statistics and running statistics, and every block normalises its part.
+hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, const float* part, int T, int P,
+                                  const float* gamma, const float* beta, const float* res, int rc, int rh, int rw,
+                                  int relu, float eps, float momentum, float* z, float* save_mean, float* save_invstd,
+                                  float* run_mean, float* run_var, hipStream_t st);
 // Direct 3x3 / pad 1 kernel (forward, or backward-data of a stride-1 layer
 // when transpose is set); hipErrorNotSupported when no tile config fits.
 hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const float* x, const float* w, float* y,
-                          int accumulate, bool transpose, hipStream_t st);
+                          int accumulate, bool transpose, hipStream_t st, const BnStatsFuse* bn = nullptr);
+// number of pixel tiles (workgroups along x) of the direct forward kernel, 0 if none
+int conv3x3_direct_tiles(int n, int C, int H, int W, int K, int stride);
+// Backward-data of a 3x3 / pad 1 / stride 2 conv (layer channels CL in, KL
+// out, input H x W); hipErrorNotSupported when no tile config fits.
+hipError_t conv3x3_dgrad_s2(int n, int CL, int H, int W, int KL, const float* w, const float* dy, float* dx,
+                            int accumulate, hipStream_t st);
 // Backward-weight partial sums of a 3x3 / pad 1 conv (dW-shaped, one per
 // workgroup); conv3x3_wgrad_splits is 0 when no configuration covers it.
 int conv3x3_wgrad_splits(int n, int C, int H, int W, int K, int stride);

@@ -556,6 +556,90 @@ hipError_t bn_bwd(int n, int c, int h, int w, const float* dz, const float* z, c
     return hipGetLastError();
 }
 
+namespace {
+// grid (c, blocks per channel); each block merges its channel's T tile
+// partials (mean_t, M2_t over P pixels each) in a fixed order:
+//   mean = (1/T) sum mean_t,  M2 = sum M2_t + P sum (mean_t - mean)^2
+// then normalises its share of the channel's n*hw elements.
+constexpr int kApplyPerBlock = 4096;
+
+__global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int hw, const float* y, const float* part,
+                                                               int T, int P, const float* gamma, const float* beta,
+                                                               const float* res, int rc, int rh, int rw, int h, int w,
+                                                               int relu, float eps, float momentum, float* z,
+                                                               float* save_mean, float* save_invstd, float* run_mean,
+                                                               float* run_var)
+{
+    __shared__ double sh[kBlock / 64];
+    __shared__ float coef[2];
+    const int ch = blockIdx.x;
+    const float* pp = part + (size_t)ch * T * 2;
+    double s1 = 0.0;
+    for (int t = threadIdx.x; t < T; t += kBlock) s1 += (double)pp[2 * t];
+    s1 = block_sum(s1, sh);
+    __shared__ double mean_sh;
+    if (threadIdx.x == 0) mean_sh = s1 / T;
+    __syncthreads();
+    const double mean = mean_sh;
+    double s2 = 0.0;
+    for (int t = threadIdx.x; t < T; t += kBlock) {
+        const double d = (double)pp[2 * t] - mean;
+        s2 += (double)pp[2 * t + 1] + (double)P * d * d;
+    }
+    s2 = block_sum(s2, sh);
+    if (threadIdx.x == 0) {
+        const double cnt = (double)T * P;
+        const double var = s2 / cnt;
+        const double invstd = 1.0 / sqrt(var + (double)eps);
+        const double scale = (double)gamma[ch] * invstd;
+        coef[0] = (float)scale;
+        coef[1] = (float)((double)beta[ch] - mean * scale);
+        if (blockIdx.y == 0) {
+            save_mean[ch] = (float)mean;
+            save_invstd[ch] = (float)invstd;
+            if (run_mean) {
+                run_mean[ch] = (float)((1.0 - momentum) * run_mean[ch] + momentum * mean);
+                run_var[ch] = (float)((1.0 - momentum) * run_var[ch] + momentum * (cnt > 1.0 ? var * cnt / (cnt - 1.0) : var));
+            }
+        }
+    }
+    __syncthreads();
+    const float sc = coef[0], sf = coef[1];
+    const int64_t total = (int64_t)n * hw;
+    const int64_t e0 = (int64_t)blockIdx.y * kApplyPerBlock;
+    const int64_t e1 = e0 + kApplyPerBlock < total ? e0 + kApplyPerBlock : total;
+    const bool identity = res && rc == c && rh == h && rw == w;
+    const int lo = (c - rc) / 2, cc = ch - lo;
+    for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
+        const int img = (int)(e / hw), off = (int)(e - (int64_t)img * hw);
+        const size_t i = ((size_t)img * c + ch) * hw + off;
+        float v = y[i] * sc + sf;
+        if (res) {
+            if (identity) {
+                v += res[i];
+            } else if (cc >= 0 && cc < rc) {
+                const int hh = off / w, ww = off - hh * w;
+                v += res[(((size_t)img * rc + cc) * rh + hh * (rh / h)) * rw + ww * (rw / w)];
+            }
+        }
+        if (relu) v = fmaxf(v, 0.f);
+        z[i] = v;
+    }
+}
+}  // namespace
+
+hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, const float* part, int T, int P,
+                                  const float* gamma, const float* beta, const float* res, int rc, int rh, int rw,
+                                  int relu, float eps, float momentum, float* z, float* save_mean, float* save_invstd,
+                                  float* run_mean, float* run_var, hipStream_t st)
+{
+    const int64_t total = (int64_t)n * h * w;
+    const unsigned per_ch = (unsigned)((total + kApplyPerBlock - 1) / kApplyPerBlock);
+    hipLaunchKernelGGL(bn_apply_partials_k, dim3(c, per_ch), dim3(kBlock), 0, st, n, c, h * w, y, part, T, P, gamma,
+                       beta, res, rc, rh, rw, h, w, relu, eps, momentum, z, save_mean, save_invstd, run_mean, run_var);
+    return hipGetLastError();
+}
+
 hipError_t maxpool_fwd(int n, int c, int h, int w, int k, int stride, const float* x, float* y, int32_t* argmax,
                        hipStream_t st)
 {

@@ -8,16 +8,18 @@
 // writes one
 // dW-shaped partial sum; the partials are added in a fixed order by the
 // reduction kernel of conv.hip, so the result is bit-reproducible.
-// In the workgroup, wave (kb, cb, wpx) owns the 16x16 output blocks
-// (output channels kb*16.., input channels cb*16..) of all 9 taps (9 MFMA
-// accumulators) and the pixel quads wpx, wpx+WPX, ...; waves that differ only
-// in wpx are summed through LDS in wpx order at the end.
+// blockIdx.y selects a group of CBW 16-channel input blocks.  In the
+// workgroup, wave (kb, cb, wpx) owns the 16x16 output blocks (output channels
+// kb*16.., input channels of block cb) of all 9 taps (9 MFMA accumulators)
+// and the pixel quads wpx, wpx+WPX, ...; waves that differ only in wpx are
+// summed through LDS in wpx order at the end.
 //
 // MFMA v_mfma_f32_16x16x4_f32 with k = 4 consecutive output pixels of one
 // row: A[m=k_out][k=pixel] from dy, B[k=pixel][n=c_in] from x shifted by the
-// tap.  Both tiles sit in LDS pixel-major (channels innermost) with a pixel
-// stride chosen so that the four lane groups (four pixels) of an operand
-// read land in disjoint banks.
+// tap.  Both tiles sit in LDS plane-major (one plane per channel, as in NCHW)
+// with a plane stride of 2 (mod 32) floats: an operand read by lanes
+// (channel j, pixel g) hits bank 2j + g (stride 1), all distinct within a
+// 32-lane half, and the staging writes are contiguous runs.
 #include "internal.h"
 
 namespace psw {
@@ -32,11 +34,11 @@ struct WgArgs {
     int n, C, H, W, K, HO;
 };
 
-// smallest v >= lo with (v * mult) % 32 == 16
-constexpr int bank_stride(int lo, int mult)
+// smallest v >= lo with v % 32 == 2
+constexpr int plane_stride(int lo)
 {
     int v = lo;
-    while ((v * mult) % 32 != 16) ++v;
+    while (v % 32 != 2) ++v;
     return v;
 }
 
@@ -48,13 +50,13 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
     constexpr int WS = WIN + (STRIDE == 1 ? 2 : 1);   // staged input columns: -1 .. WIN (-1 .. WIN-1 for stride 2)
     constexpr int HRR = (TH - 1) * STRIDE + 3;        // staged input rows
     constexpr int KC = 16 * KBW, CCH = 16 * CBW;
-    constexpr int KSTR = bank_stride(KC, 1);          // dy pixel stride
-    constexpr int CSTR = bank_stride(CCH, STRIDE);    // x pixel stride
     constexpr int NPIX = TH * WO;
     constexpr int QUADS = NPIX / 4;
+    constexpr int DPS = plane_stride(NPIX);           // dy plane stride
+    constexpr int XPS = plane_stride(HRR * WS);       // x plane stride
     static_assert(WO % 4 == 0, "pixel quads stay inside one row");
-    constexpr int DS_FLOATS = NPIX * KSTR;
-    constexpr int XS_FLOATS = HRR * WS * CSTR;
+    constexpr int DS_FLOATS = KC * DPS;
+    constexpr int XS_FLOATS = CCH * XPS;
     constexpr int RED_FLOATS = (WPX > 1) ? (WPX - 1) * KBW * CBW * 9 * 4 * 64 : 0;
     constexpr int LDS_FLOATS = (DS_FLOATS + XS_FLOATS) > RED_FLOATS ? (DS_FLOATS + XS_FLOATS) : RED_FLOATS;
     __shared__ float lds[LDS_FLOATS];
@@ -65,6 +67,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
     const int kb = wave % KBW, cb = (wave / KBW) % CBW, wpx = wave / (KBW * CBW);
     const int g = lane >> 4, j = lane & 15;
     const int tiles = a.HO / TH;  // row bands per image
+    const int cbase = blockIdx.y * CCH;  // first input channel of this workgroup
 
     v4f acc[9];
 #pragma unroll
@@ -72,9 +75,9 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
 
     // zero padding columns of the x tile (never written by the staging loop)
     for (int i = tid; i < HRR * CCH; i += NT) {
-        const int rr = i / CCH, c = i - (i / CCH) * CCH;
-        Xs[(rr * WS + 0) * CSTR + c] = 0.f;
-        if (STRIDE == 1) Xs[(rr * WS + WS - 1) * CSTR + c] = 0.f;
+        const int c = i / HRR, rr = i - (i / HRR) * HRR;
+        Xs[c * XPS + rr * WS] = 0.f;
+        if (STRIDE == 1) Xs[c * XPS + rr * WS + WS - 1] = 0.f;
     }
 
     for (int it = 0; it < TPW; ++it) {
@@ -84,7 +87,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
         __syncthreads();  // previous tile's LDS reads are done
         for (int i = tid; i < KC * NPIX; i += NT) {
             const int k = i / NPIX, pix = i - (i / NPIX) * NPIX;
-            Ds[pix * KSTR + k] = a.dy[(((size_t)img * a.K + k) * a.HO + oh0) * WO + pix];
+            Ds[k * DPS + pix] = a.dy[(((size_t)img * a.K + k) * a.HO + oh0) * WO + pix];
         }
         const int ih0 = oh0 * STRIDE - 1;
         for (int i = tid; i < CCH * HRR * WIN; i += NT) {
@@ -93,22 +96,22 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
             const int rr = rem / WIN, iw = rem - (rem / WIN) * WIN;
             const int ih = ih0 + rr;
             float v = 0.f;
-            if (ih >= 0 && ih < a.H) v = a.x[(((size_t)img * a.C + c) * a.H + ih) * WIN + iw];
-            Xs[(rr * WS + iw + 1) * CSTR + c] = v;
+            if (ih >= 0 && ih < a.H && cbase + c < a.C) v = a.x[(((size_t)img * a.C + cbase + c) * a.H + ih) * WIN + iw];
+            Xs[c * XPS + rr * WS + iw + 1] = v;
         }
         __syncthreads();
-        const float* dsl = Ds + g * KSTR + kb * 16 + j;
-        const float* xsl = Xs + g * STRIDE * CSTR + cb * 16 + j;
+        const float* dsl = Ds + (kb * 16 + j) * DPS + g;
+        const float* xsl = Xs + (cb * 16 + j) * XPS + g * STRIDE;
         for (int qd = wpx; qd < QUADS; qd += WPX) {
             const int pix0 = qd * 4;
             const int row = pix0 / WO, col0 = pix0 - (pix0 / WO) * WO;
-            const float av = dsl[pix0 * KSTR];
-            const float* xb = xsl + ((row * STRIDE) * WS + col0 * STRIDE) * CSTR;
+            const float av = dsl[pix0];
+            const float* xb = xsl + (row * STRIDE) * WS + col0 * STRIDE;
 #pragma unroll
             for (int r = 0; r < 3; ++r)
 #pragma unroll
                 for (int s = 0; s < 3; ++s) {
-                    const float bv = xb[(r * WS + s) * CSTR];
+                    const float bv = xb[r * WS + s];
                     acc[r * 3 + s] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[r * 3 + s], 0, 0, 0);
                 }
         }
@@ -137,7 +140,8 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
     float* out = a.part + (size_t)blockIdx.x * a.K * a.C * 9;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int k = kb * 16 + 4 * g + i, c = cb * 16 + j;
+        const int k = kb * 16 + 4 * g + i, c = cbase + cb * 16 + j;
+        if (c >= a.C) continue;  // zero-filled channels of a narrow input (C < 16)
         float* o = out + ((size_t)k * a.C + c) * 9;
 #pragma unroll
         for (int t = 0; t < 9; ++t) o[t] = acc[t][i];
@@ -151,7 +155,8 @@ int wgrad_config(int n, int C, int H, int W, int K, int stride)
     if (stride == 1 && H == 16 && W == 16 && C == 32 && K == 32) return 2;
     if (stride == 1 && H == 8 && W == 8 && C == 64 && K == 64 && n % 2 == 0) return 3;
     if (stride == 2 && H == 32 && W == 32 && C == 16 && K == 32) return 4;
-    if (stride == 2 && H == 16 && W == 16 && C == 32 && K == 64 && n % 2 == 0) return 5;
+    if (stride == 2 && H == 16 && W == 16 && C == 32 && K == 64) return 5;
+    if (stride == 1 && H == 32 && W == 32 && C < 16 && K == 16) return 6;
     return 0;
 }
 
@@ -165,7 +170,8 @@ int conv3x3_wgrad_splits(int n, int C, int H, int W, int K, int stride)
     case 2: return n;           // one image per workgroup
     case 3: return n / 2;       // two images per workgroup
     case 4: return n * 2;       // one 8-row band (of 16 output rows) per workgroup
-    case 5: return n / 2;       // two images per workgroup
+    case 5: return n;           // one image per workgroup
+    case 6: return n * 2;       // as 1, input channels zero-filled to 16
     default: return 0;
     }
 }
@@ -177,22 +183,24 @@ hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const fl
     if (!cfg) return hipErrorNotSupported;
     WgArgs a{x, dy, part, n, C, H, W, K, H / stride};
     const int splits = conv3x3_wgrad_splits(n, C, H, W, K, stride);
-    const int nt = cfg == 1 ? 256 : cfg == 2 ? 512 : cfg == 3 ? 1024 : cfg == 4 ? 256 : 512;
+    const int cgroups = (C + 15) / 16;  // one 16-channel block per workgroup (grid.y)
+    const dim3 grid(splits, cgroups);
     switch (cfg) {
+    case 6:
     case 1:
-        hipLaunchKernelGGL((conv3x3_wgrad<1, 32, 16, 1, 1, 4, 1>), dim3(splits), dim3(nt), 0, st, a);
+        hipLaunchKernelGGL((conv3x3_wgrad<1, 32, 16, 1, 1, 4, 1>), grid, dim3(256), 0, st, a);
         break;
     case 2:
-        hipLaunchKernelGGL((conv3x3_wgrad<1, 16, 16, 2, 2, 2, 1>), dim3(splits), dim3(nt), 0, st, a);
+        hipLaunchKernelGGL((conv3x3_wgrad<1, 16, 16, 2, 1, 2, 1>), grid, dim3(256), 0, st, a);
         break;
     case 3:
-        hipLaunchKernelGGL((conv3x3_wgrad<1, 8, 8, 4, 4, 1, 2>), dim3(splits), dim3(nt), 0, st, a);
+        hipLaunchKernelGGL((conv3x3_wgrad<1, 8, 8, 4, 1, 1, 2>), grid, dim3(256), 0, st, a);
         break;
     case 4:
-        hipLaunchKernelGGL((conv3x3_wgrad<2, 16, 8, 2, 1, 2, 1>), dim3(splits), dim3(nt), 0, st, a);
+        hipLaunchKernelGGL((conv3x3_wgrad<2, 16, 8, 2, 1, 2, 1>), grid, dim3(256), 0, st, a);
         break;
     case 5:
-        hipLaunchKernelGGL((conv3x3_wgrad<2, 8, 8, 4, 2, 1, 2>), dim3(splits), dim3(nt), 0, st, a);
+        hipLaunchKernelGGL((conv3x3_wgrad<2, 8, 8, 4, 1, 1, 1>), grid, dim3(256), 0, st, a);
         break;
     }
     return hipGetLastError();
