@@ -278,6 +278,7 @@ struct psw_net {
     std::vector<size_t> act_off, grad_off;  // per tensor (index 0 unused)
     std::vector<size_t> save_off;           // per op: BN mean/invstd/scale,shift or max-pool argmax
     std::vector<char> fuse_stats;           // per conv op: its BN (op+1) statistics come from the conv epilogue
+    std::vector<char> fused_now;            // per conv op: the fused kernel ran in the current step
 
     std::vector<char> grad_accum;           // per op input slot: 0 overwrite, 1 accumulate (in0, in1)
     size_t ws_off = 0, ws_bytes = 0, arena_bytes = 0;
@@ -445,6 +446,7 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
     }
     size_t ws = 0;
     net->fuse_stats.assign(n_layers, 0);
+    net->fused_now.assign(n_layers, 0);
     for (int i = 0; i < n_layers; ++i) {
         const psw_layer& o = net->ops[i];
         const Tensor a = net->t[o.in0];
@@ -687,11 +689,29 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
             check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, net->prec, &cs);
             const float* b = (o.flags & PSW_F_BIAS) ? W + (int64_t)o.cout * o.cin * o.k * o.k : nullptr;
             kind = PSW_PROF_CONV_FWD;
+            net->fused_now[i] = 0;
             if (net->fuse_stats[i]) {  // the next op's BN statistics come out of this conv
                 psw::BnStatsFuse bn{(float*)ws};
-                PSW_TRY(psw::conv_fwd_bnstats(cs, act(o.in0), W, act(i + 1), bn, wsb / sizeof(float), st),
-                        "conv_fwd_bnstats");
-            } else {
+                hipEvent_t ea = nullptr, eb = nullptr;
+                if (net->profiling) {
+                    ea = net->next_event();
+                    eb = net->next_event();
+                    if (ea && eb) (void)hipEventRecord(ea, st);
+                }
+                e = psw::conv_fwd_bnstats(cs, act(o.in0), W, act(i + 1), bn, wsb / sizeof(float), st);
+                if (e == hipSuccess) {
+                    net->fused_now[i] = 1;
+                    if (ea && eb) {
+                        (void)hipEventRecord(eb, st);
+                        net->prof.push_back(psw_net::ProfRec{kind, ea, eb});
+                    }
+                } else if (e != hipErrorNotSupported) {
+                    return hip_check(e, "conv_fwd_bnstats");
+                } else if (ea && eb) {
+                    net->ev_used -= 2;  // nothing was launched between the two events
+                }
+            }
+            if (!net->fused_now[i]) {
                 PSW_TRY(psw::conv_fwd(cs, act(o.in0), W, b, (o.flags & PSW_F_RELU) != 0, act(i + 1), bf16, st),
                         "conv_fwd");
             }
@@ -703,7 +723,7 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
             float* rm = net->run_mean ? net->run_mean + net->bn_off[i] : nullptr;
             float* rvv = net->run_var ? net->run_var + net->bn_off[i] : nullptr;
             kind = PSW_PROF_BN_FWD;
-            if (i > 0 && net->fuse_stats[i - 1]) {  // per-tile statistics written by the conv into ws
+            if (i > 0 && net->fused_now[i - 1]) {  // per-tile statistics written by the conv into ws
                 const psw_layer& cv = net->ops[i - 1];
                 const Tensor ci = net->t[cv.in0];
                 psw::ConvShape ccs;

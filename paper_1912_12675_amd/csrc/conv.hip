@@ -359,14 +359,17 @@ hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy,
     if (use_direct_wgrad(cs, bf16)) {
         const int zd = conv3x3_wgrad_splits(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride);
         hipError_t e = conv3x3_wgrad(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, (float*)ws, st);
-        if (e != hipSuccess) return e;
-        hipLaunchKernelGGL(reduce_splits, dim3((unsigned)((mn + 15) / 16)), dim3(256), 0, st, (const float*)ws, zd,
-                           (int64_t)mn, dw);
-        e = hipGetLastError();
-        if (e != hipSuccess || !db) return e;
-        const size_t zmax = conv_bwd_weight_ws_bytes(cs, bf16) - channel_sum_ws_bytes(cs.n, cs.k, cs.p * cs.q);
-        char* rest = (char*)ws + zmax;
-        return channel_sum(cs.n, cs.k, cs.p * cs.q, dy, db, rest, channel_sum_ws_bytes(cs.n, cs.k, cs.p * cs.q), st);
+        if (e != hipErrorNotSupported) {  // otherwise (misaligned operands) fall through to the implicit GEMM
+            if (e != hipSuccess) return e;
+            hipLaunchKernelGGL(reduce_splits, dim3((unsigned)((mn + 15) / 16)), dim3(256), 0, st, (const float*)ws,
+                               zd, (int64_t)mn, dw);
+            e = hipGetLastError();
+            if (e != hipSuccess || !db) return e;
+            const size_t zmax = conv_bwd_weight_ws_bytes(cs, bf16) - channel_sum_ws_bytes(cs.n, cs.k, cs.p * cs.q);
+            char* rest = (char*)ws + zmax;
+            return channel_sum(cs.n, cs.k, cs.p * cs.q, dy, db, rest, channel_sum_ws_bytes(cs.n, cs.k, cs.p * cs.q),
+                               st);
+        }
     }
     const int z = wgrad_splits(cs, bf16);
     const int BK = bf16 ? 32 : 16;

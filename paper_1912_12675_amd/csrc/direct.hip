@@ -35,6 +35,39 @@ struct DirArgs {
 };
 
 constexpr int round4(int v) { return (v + 3) / 4 * 4; }
+
+// B-operand LDS offset of pixel j (0..15) of a block relative to pixel 0
+constexpr int pix_off(int j, int wo, int stride, int rstr) { return (j / wo) * stride * rstr + (j % wo) * stride; }
+
+// Number of LDS bank collisions (32 banks of 4 bytes) of one B-operand read
+// for a plane stride ps: lanes (j, g) read g*ps + pix_off(j); the hardware
+// serves each 32-lane half (g = 0,1 and g = 2,3) separately.
+constexpr int b_conflicts(int ps, int wo, int stride, int rstr)
+{
+    int worst = 0;
+    for (int half = 0; half < 2; ++half) {
+        int cnt[32] = {};
+        for (int g = 2 * half; g < 2 * half + 2; ++g)
+            for (int j = 0; j < 16; ++j) cnt[(g * ps + pix_off(j, wo, stride, rstr)) % 32]++;
+        for (int b = 0; b < 32; ++b) worst = cnt[b] > worst ? cnt[b] : worst;
+    }
+    return worst;
+}
+
+// smallest plane stride >= lo, multiple of 4 (float4 staging), with the
+// fewest B-operand bank collisions
+constexpr int plane_stride_b(int lo, int wo, int stride, int rstr)
+{
+    int best = round4(lo), bestc = b_conflicts(round4(lo), wo, stride, rstr);
+    for (int v = round4(lo); v < round4(lo) + 32; v += 4) {
+        const int c = b_conflicts(v, wo, stride, rstr);
+        if (c < bestc) {
+            bestc = c;
+            best = v;
+        }
+    }
+    return best;
+}
 // weight row stride (floats) of an LDS tile with `n` floats per output
 // channel: the smallest v >= n with v = 2 (mod 32), so that lanes
 // (m, g) -> m*v + 9*g hit distinct banks within each 32-lane half
@@ -52,8 +85,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     constexpr int WIN = WO * STRIDE;                       // input width
     constexpr int HR = (TH - 1) * STRIDE + 3;              // staged input rows
     constexpr int RSTR = round4(WIN + (STRIDE == 1 ? 5 : 4));  // LDS row stride (cols 3 .. WIN+4)
-    constexpr int PS0 = HR * RSTR;
-    constexpr int PS = PS0 + ((16 - PS0 % 32) + 32) % 32;  // plane stride = 16 mod 32: lane groups hit disjoint banks
+    constexpr int PS = plane_stride_b(HR * RSTR, WO, STRIDE, RSTR);  // lane groups hit disjoint banks where possible
     constexpr int TK = 16 * WK;
     constexpr int WR = wrow(CC * 9);
     static_assert(TH * WO == 16 * NBW * WP, "pixel tiling");
@@ -89,34 +121,103 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
         if (STRIDE == 1) Xs[c * PS + rr * RSTR + WIN + 4] = 0.f;
     }
 
-    for (int c0 = 0; c0 < a.C; c0 += CC) {
-        __syncthreads();  // the previous chunk's LDS reads are complete
-        // input halo tile, float4 per thread (rows outside the image are zero)
-        constexpr int Q4 = WIN / 4;
-        for (int i = tid; i < CC * HR * Q4; i += NT) {
-            const int c = i / (HR * Q4);
-            const int rem = i - c * (HR * Q4);
-            const int rr = rem / Q4, q4 = rem - (rem / Q4) * Q4;
-            const int ih = ih0 + rr;
+    // software pipeline over input-channel chunks: the next chunk's tile and
+    // weights are loaded into registers while the current chunk computes
+    constexpr int Q4 = WIN / 4;
+    constexpr int XN = CC * HR * Q4;
+    // weights: TK runs of CC*9 floats (forward) or CC runs of TK*9 floats
+    // (transposed), both multiples of 4: loaded as float4, stored as scalars
+    constexpr int WN4 = TK * CC * 9 / 4;
+    static_assert((CC * 9) % 4 == 0 && (TK * 9) % 4 == 0, "float4 weight runs");
+    constexpr int XV = (XN + NT - 1) / NT, WV = (WN4 + NT - 1) / NT;
+    const bool wvec = (a.C % 4 == 0) && (TRANS ? (a.K % 4 == 0) : true) && ((uintptr_t)a.w % 16 == 0);
+    float4 xr[XV];
+    float4 wr[WV];
+    auto load_chunk = [&](int c0) {
+#pragma unroll
+        for (int k = 0; k < XV; ++k) {
+            const int i = tid + k * NT;
             float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (ih >= 0 && ih < a.H && c0 + c < a.C)
-                v = *reinterpret_cast<const float4*>(a.x + (((size_t)img * a.C + c0 + c) * a.H + ih) * WIN + q4 * 4);
-            *reinterpret_cast<float4*>(&Xs[c * PS + rr * RSTR + 4 + q4 * 4]) = v;
+            if (i < XN) {
+                const int c = i / (HR * Q4);
+                const int rem = i - c * (HR * Q4);
+                const int rr = rem / Q4, q4 = rem - (rem / Q4) * Q4;
+                const int ih = ih0 + rr;
+                if (ih >= 0 && ih < a.H && c0 + c < a.C)
+                    v = *reinterpret_cast<const float4*>(a.x + (((size_t)img * a.C + c0 + c) * a.H + ih) * WIN + q4 * 4);
+            }
+            xr[k] = v;
         }
-        // weights of (TK output channels) x (CC input channels): Wc[m][c*9 + rs]
-        for (int i = tid; i < TK * CC * 9; i += NT) {
-            if (!TRANS) {  // w[m][c][rs]: each output channel's CC*9 run is contiguous
-                const int m = i / (CC * 9), rem = i - (i / (CC * 9)) * (CC * 9);
-                const int c = rem / 9;
-                Wc[m * WR + rem] = c0 + c < a.C ? a.w[((size_t)(mblk + m) * a.C + c0) * 9 + rem] : 0.f;
-            } else {       // w_layer[c][m][rs]: each input channel's TK*9 run is contiguous; flip the taps
-                const int c = i / (TK * 9), rem = i - (i / (TK * 9)) * (TK * 9);
-                const int m = rem / 9, rsl = rem - (rem / 9) * 9;
-                Wc[m * WR + c * 9 + 8 - rsl] =
-                    c0 + c < a.C ? a.w[((size_t)(c0 + c) * a.K + mblk) * 9 + rem] : 0.f;
+#pragma unroll
+        for (int k = 0; k < WV; ++k) {
+            const int i4 = tid + k * NT;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (i4 < WN4) {
+                const int i = i4 * 4;
+                if (!TRANS) {  // w[m][c][rs]: each output channel's CC*9 run is contiguous
+                    const int m = i / (CC * 9), rem = i - (i / (CC * 9)) * (CC * 9);
+                    const float* src = a.w + ((size_t)(mblk + m) * a.C + c0) * 9 + rem;
+                    if (wvec && c0 + CC <= a.C) {
+                        v = *reinterpret_cast<const float4*>(src);
+                    } else {  // narrow input (C < CC) or misaligned: element-wise with bounds
+                        float t[4];
+                        for (int e = 0; e < 4; ++e) t[e] = (c0 + (rem + e) / 9 < a.C) ? src[e] : 0.f;
+                        v = make_float4(t[0], t[1], t[2], t[3]);
+                    }
+                } else {       // w_layer[c][m][rs]: each input channel's TK*9 run is contiguous
+                    const int c = i / (TK * 9), rem = i - (i / (TK * 9)) * (TK * 9);
+                    const float* src = a.w + ((size_t)(c0 + c) * a.K + mblk) * 9 + rem;
+                    if (c0 + c < a.C) {
+                        if (wvec) {
+                            v = *reinterpret_cast<const float4*>(src);
+                        } else {
+                            v = make_float4(src[0], src[1], src[2], src[3]);
+                        }
+                    }
+                }
+            }
+            wr[k] = v;
+        }
+    };
+    auto store_chunk = [&]() {
+#pragma unroll
+        for (int k = 0; k < XV; ++k) {
+            const int i = tid + k * NT;
+            if (i < XN) {
+                const int c = i / (HR * Q4);
+                const int rem = i - c * (HR * Q4);
+                const int rr = rem / Q4, q4 = rem - (rem / Q4) * Q4;
+                *reinterpret_cast<float4*>(&Xs[c * PS + rr * RSTR + 4 + q4 * 4]) = xr[k];
             }
         }
+#pragma unroll
+        for (int k = 0; k < WV; ++k) {
+            const int i4 = tid + k * NT;
+            if (i4 < WN4) {
+                const int i = i4 * 4;
+                const float vv[4] = {wr[k].x, wr[k].y, wr[k].z, wr[k].w};
+                if (!TRANS) {
+                    const int m = i / (CC * 9), rem = i - (i / (CC * 9)) * (CC * 9);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) Wc[m * WR + rem + e] = vv[e];  // a run never crosses m (CC*9 % 4 == 0)
+                } else {  // flip the taps
+                    const int c = i / (TK * 9), rem = i - (i / (TK * 9)) * (TK * 9);
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const int m = (rem + e) / 9, rsl = (rem + e) - ((rem + e) / 9) * 9;
+                        Wc[m * WR + c * 9 + 8 - rsl] = vv[e];
+                    }
+                }
+            }
+        }
+    };
+
+    load_chunk(0);
+    for (int c0 = 0; c0 < a.C; c0 += CC) {
+        __syncthreads();  // the previous chunk's LDS reads are complete
+        store_chunk();
         __syncthreads();
+        if (c0 + CC < a.C) load_chunk(c0 + CC);
         const float* wf = Wc + (wk * 16 + j) * WR + g * 9;
 #pragma unroll
         for (int c4 = 0; c4 < CC / 4; ++c4)
@@ -223,8 +324,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
     constexpr int NT = 64 * WK * WP;
     constexpr int HR = TH + 1;                 // dy rows i0 .. i0+TH (the last may be past the edge)
     constexpr int RSTR = round4(WO + 1);       // dy cols 0 .. WO (col WO is zero)
-    constexpr int PS0 = HR * RSTR;
-    constexpr int PS = PS0 + ((16 - PS0 % 32) + 32) % 32;
+    constexpr int PS = plane_stride_b(HR * RSTR, WO, 1, RSTR);
     constexpr int TK = 16 * WK;
     constexpr int WR = wrow(CC * 9);
     static_assert(TH * WO == 16 * NBW * WP, "pixel tiling");
@@ -358,6 +458,7 @@ hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const f
     if (stride != 1 && stride != 2) return hipErrorNotSupported;
     if (H % stride || W % stride) return hipErrorNotSupported;
     if (bn && transpose) return hipErrorNotSupported;
+    if ((uintptr_t)x % 16) return hipErrorNotSupported;  // float4 tile staging
     const int HO = H / stride, WO = W / stride;
     DirArgs a{x, w, y, C, H, K, HO, accumulate, BnStatsFuse{nullptr}};
     if (bn) a.bn = *bn;
@@ -384,6 +485,7 @@ hipError_t conv3x3_dgrad_s2(int n, int CL, int H, int W, int KL, const float* w,
                             int accumulate, hipStream_t st)
 {
     if (H % 2 || W % 2 || KL % 16) return hipErrorNotSupported;
+    if ((uintptr_t)dy % 16 || (uintptr_t)dx % 8) return hipErrorNotSupported;  // float4 staging, float2 stores
     const int HO = H / 2, WO = W / 2;
     DgArgs a{dy, w, dx, KL, CL, HO, accumulate};
     if (WO == 16 && HO % 4 == 0 && CL % 16 == 0) {

@@ -85,19 +85,27 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
         const int img = tl / tiles;
         const int oh0 = (tl - img * tiles) * TH;
         __syncthreads();  // previous tile's LDS reads are done
-        for (int i = tid; i < KC * NPIX; i += NT) {
+        // dy tile and x tile, float4 global loads (rows are multiples of 4
+        // floats), scalar LDS stores into the plane-major layout
+        for (int i4 = tid; i4 < KC * NPIX / 4; i4 += NT) {
+            const int i = i4 * 4;
             const int k = i / NPIX, pix = i - (i / NPIX) * NPIX;
-            Ds[k * DPS + pix] = a.dy[(((size_t)img * a.K + k) * a.HO + oh0) * WO + pix];
+            const float4 v = *reinterpret_cast<const float4*>(a.dy + (((size_t)img * a.K + k) * a.HO + oh0) * WO + pix);
+            float* d = Ds + k * DPS + pix;
+            d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
         }
         const int ih0 = oh0 * STRIDE - 1;
-        for (int i = tid; i < CCH * HRR * WIN; i += NT) {
+        for (int i4 = tid; i4 < CCH * HRR * WIN / 4; i4 += NT) {
+            const int i = i4 * 4;
             const int c = i / (HRR * WIN);
             const int rem = i - c * (HRR * WIN);
             const int rr = rem / WIN, iw = rem - (rem / WIN) * WIN;
             const int ih = ih0 + rr;
-            float v = 0.f;
-            if (ih >= 0 && ih < a.H && cbase + c < a.C) v = a.x[(((size_t)img * a.C + cbase + c) * a.H + ih) * WIN + iw];
-            Xs[c * XPS + rr * WS + iw + 1] = v;
+            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (ih >= 0 && ih < a.H && cbase + c < a.C)
+                v = *reinterpret_cast<const float4*>(a.x + (((size_t)img * a.C + cbase + c) * a.H + ih) * WIN + iw);
+            float* d = Xs + c * XPS + rr * WS + iw + 1;
+            d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
         }
         __syncthreads();
         const float* dsl = Ds + (kb * 16 + j) * DPS + g;
@@ -181,6 +189,7 @@ hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const fl
 {
     const int cfg = wgrad_config(n, C, H, W, K, stride);
     if (!cfg) return hipErrorNotSupported;
+    if ((uintptr_t)x % 16 || (uintptr_t)dy % 16) return hipErrorNotSupported;  // float4 staging
     WgArgs a{x, dy, part, n, C, H, W, K, H / stride};
     const int splits = conv3x3_wgrad_splits(n, C, H, W, K, stride);
     const int cgroups = (C + 15) / 16;  // one 16-channel block per workgroup (grid.y)
