@@ -279,6 +279,8 @@ struct psw_net {
     std::vector<size_t> save_off;           // per op: BN mean/invstd/scale,shift or max-pool argmax
     std::vector<char> fuse_stats;           // per conv op: its BN (op+1) statistics come from the conv epilogue
     std::vector<char> fused_now;            // per conv op: the fused kernel ran in the current step
+    std::vector<char> fuse_bwd;             // per conv op: its input's BN (op-1) backward sums come from its dgrad
+    std::vector<char> fused_bwd_now;        // per conv op: the fused dgrad ran in the current step
 
     std::vector<char> grad_accum;           // per op input slot: 0 overwrite, 1 accumulate (in0, in1)
     size_t ws_off = 0, ws_bytes = 0, arena_bytes = 0;
@@ -447,6 +449,8 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
     size_t ws = 0;
     net->fuse_stats.assign(n_layers, 0);
     net->fused_now.assign(n_layers, 0);
+    net->fuse_bwd.assign(n_layers, 0);
+    net->fused_bwd_now.assign(n_layers, 0);
     for (int i = 0; i < n_layers; ++i) {
         const psw_layer& o = net->ops[i];
         const Tensor a = net->t[o.in0];
@@ -467,6 +471,13 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
             const size_t pf = psw::conv_fwd_bnstats_part_floats(cs);
             net->fuse_stats[i] = next_bn && plain && pf > 0;
             if (net->fuse_stats[i]) ws = std::max(ws, pf * sizeof(float));
+            // input produced by the BN right before this conv: the conv is that
+            // tensor's lowest-index consumer, so its dgrad is the last writer of
+            // the BN output's gradient and can also form the BN backward sums
+            const bool prev_bn = i > 0 && net->ops[i - 1].kind == PSW_OP_BN && o.in0 == i && net->ops[i - 1].in0 > 0;
+            const int tb = psw::conv_bwd_data_bnsums_tiles(cs);
+            net->fuse_bwd[i] = prev_bn && prec == PSW_FP32 && tb > 0;
+            if (net->fuse_bwd[i]) ws = std::max(ws, (size_t)tb * cs.c * 2 * sizeof(float));
         } else if (o.kind == PSW_OP_FC) {
             ws = std::max(ws, psw::fc_bwd_ws_bytes(a.n, o.cin, o.cout));
         }
@@ -730,12 +741,25 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
                 check_conv(ci.n, ci.c, ci.h, ci.w, cv.cout, cv.k, cv.k, cv.stride, cv.pad, net->prec, &ccs);
                 const int T = psw::conv_fwd_bnstats_tiles(ccs);
                 const int P = a.n * a.h * a.w / T;
-                PSW_TRY(psw::bn_apply_from_partials(a.n, a.c, a.h, a.w, act(o.in0), (const float*)ws, T, P, W, W + o.cin,
-                                                    o.in1 >= 0 ? act(o.in1) : nullptr, r.c, r.h, r.w,
-                                                    (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, act(i + 1), save,
-                                                    save + o.cin, rm, rvv, st),
-                        "bn_apply");
-                break;
+                hipEvent_t ea = nullptr, eb = nullptr;
+                if (net->profiling) {
+                    ea = net->next_event();
+                    eb = net->next_event();
+                    if (ea && eb) (void)hipEventRecord(ea, st);
+                }
+                e = psw::bn_apply_from_partials(a.n, a.c, a.h, a.w, act(o.in0), (const float*)ws, T, P, W, W + o.cin,
+                                                o.in1 >= 0 ? act(o.in1) : nullptr, r.c, r.h, r.w,
+                                                (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, act(i + 1), save,
+                                                save + o.cin, rm, rvv, st);
+                if (e == hipSuccess) {
+                    if (ea && eb) {
+                        (void)hipEventRecord(eb, st);
+                        net->prof.push_back(psw_net::ProfRec{kind, ea, eb});
+                    }
+                    break;
+                }
+                if (e != hipErrorNotSupported) return hip_check(e, "bn_apply");
+                if (ea && eb) net->ev_used -= 2;  // nothing launched: statistics are recomputed below
             }
             PSW_TRY(psw::bn_fwd(a.n, a.c, a.h, a.w, act(o.in0), W, W + o.cin, o.in1 >= 0 ? act(o.in1) : nullptr, r.c,
                                 r.h, r.w, (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, act(i + 1), save, save + o.cin, rm,
@@ -785,6 +809,30 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
             kind = PSW_PROF_CONV_BWD_WEIGHT;
             PSW_TRY(psw::conv_bwd_weight(cs, act(o.in0), g, dw, db, bf16, ws, wsb, st), "conv_bwd_weight");
             kind = PSW_PROF_CONV_BWD_DATA;
+            net->fused_bwd_now[i] = 0;
+            if (din && net->fuse_bwd[i]) {  // BN op i-1's backward sums out of this dgrad
+                const psw_layer& bo = net->ops[i - 1];
+                const float* bsave = (const float*)(A + net->save_off[i - 1]);
+                const psw::BnBwdFuse bnb{(float*)ws, act(i), act(bo.in0), bsave, bsave + bo.cin,
+                                         (bo.flags & PSW_F_RELU) != 0};
+                hipEvent_t ea = nullptr, eb = nullptr;
+                if (net->profiling) {
+                    ea = net->next_event();
+                    eb = net->next_event();
+                    if (ea && eb) (void)hipEventRecord(ea, st);
+                }
+                e = psw::conv_bwd_data_bnsums(cs, wcur(i), g, din, acc0, bnb, st);
+                if (e == hipSuccess) {
+                    net->fused_bwd_now[i] = 1;
+                    if (ea && eb) {
+                        (void)hipEventRecord(eb, st);
+                        net->prof.push_back(psw_net::ProfRec{kind, ea, eb});
+                    }
+                    break;
+                }
+                if (e != hipErrorNotSupported) return hip_check(e, "conv_bwd_data_bnsums");
+                if (ea && eb) net->ev_used -= 2;  // nothing was launched between the two events
+            }
             if (din) PSW_TRY(psw::conv_bwd_data(cs, wcur(i), g, din, acc0, bf16, st), "conv_bwd_data");
             break;
         }
@@ -795,6 +843,35 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
             float* dg = gptr(i);
             if (!din) return fail(PSW_ERR_UNSUPPORTED, "op %d: BN directly on the input batch", i);
             kind = PSW_PROF_BN_BWD;
+            if (i + 1 < L && net->fused_bwd_now[i + 1]) {  // sums written by the next conv's dgrad into ws
+                const psw_layer& cv = net->ops[i + 1];
+                psw::ConvShape ccs;
+                check_conv(y.n, y.c, y.h, y.w, cv.cout, cv.k, cv.k, cv.stride, cv.pad, net->prec, &ccs);
+                const int T = psw::conv_bwd_data_bnsums_tiles(ccs);
+                const bool identity = dres && r.c == a.c && r.h == a.h && r.w == a.w;
+                const int racc = net->grad_accum[2 * i + 1];
+                hipEvent_t ea = nullptr, eb = nullptr;
+                if (net->profiling) {
+                    ea = net->next_event();
+                    eb = net->next_event();
+                    if (ea && eb) (void)hipEventRecord(ea, st);
+                }
+                e = psw::bn_bwd_from_partials(a.n, a.c, a.h, a.w, g, act(i + 1), act(o.in0), wcur(i), save,
+                                              save + o.cin, (const float*)ws, T, (o.flags & PSW_F_RELU) != 0, din, dg,
+                                              dg + o.cin, identity ? dres : nullptr, racc, st);
+                if (e == hipSuccess && dres && !identity)
+                    e = psw::shortcut_a_backward(a.n, a.c, a.h, a.w, r.c, r.h, r.w, g, act(i + 1),
+                                                 (o.flags & PSW_F_RELU) != 0, dres, racc, st);
+                if (e == hipSuccess) {
+                    if (ea && eb) {
+                        (void)hipEventRecord(eb, st);
+                        net->prof.push_back(psw_net::ProfRec{kind, ea, eb});
+                    }
+                    break;
+                }
+                if (e != hipErrorNotSupported) return hip_check(e, "bn_bwd_from_partials");
+                if (ea && eb) net->ev_used -= 2;  // nothing launched: sums are recomputed below
+            }
             PSW_TRY(psw::bn_bwd(a.n, a.c, a.h, a.w, g, act(i + 1), act(o.in0), wcur(i), save, save + o.cin,
                                 (o.flags & PSW_F_RELU) != 0, din, dg, dg + o.cin, dres, r.c, r.h, r.w,
                                 net->grad_accum[2 * i + 1], ws, wsb, st),
@@ -802,8 +879,8 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
             break;
         }
         case PSW_OP_MAXPOOL:
+            kind = PSW_PROF_POOL;
             if (din)
-                kind = PSW_PROF_POOL;
                 PSW_TRY(psw::maxpool_bwd(a.n, a.c, a.h, a.w, o.k, o.stride, g, (const int32_t*)(A + net->save_off[i]),
                                          din, acc0, st),
                         "maxpool_bwd");

@@ -341,6 +341,22 @@ static bool use_direct_wgrad(const ConvShape& cs, int bf16)
            conv3x3_wgrad_splits(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride) > 0;
 }
 
+int conv_bwd_data_bnsums_tiles(const ConvShape& cs)
+{
+    if (cs.r != 3 || cs.s != 3 || cs.pad != 1) return 0;
+    if (cs.stride == 2 && (cs.h != 2 * cs.p || cs.w != 2 * cs.q)) return 0;
+    return dgrad_bnsums_tiles(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride);
+}
+
+hipError_t conv_bwd_data_bnsums(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate,
+                                const BnBwdFuse& bnb, hipStream_t st)
+{
+    if (conv_bwd_data_bnsums_tiles(cs) == 0) return hipErrorNotSupported;
+    if ((uintptr_t)bnb.z % 8 || (uintptr_t)bnb.y % 8) return hipErrorNotSupported;
+    if (cs.stride == 1) return conv3x3_direct(cs.n, cs.k, cs.h, cs.w, cs.c, 1, dy, w, dx, accumulate, true, st, nullptr, &bnb);
+    return conv3x3_dgrad_s2(cs.n, cs.c, cs.h, cs.w, cs.k, w, dy, dx, accumulate, st, &bnb);
+}
+
 size_t conv_bwd_weight_ws_bytes(const ConvShape& cs, int bf16)
 {
     int z = wgrad_splits(cs, bf16);

@@ -32,6 +32,7 @@ struct DirArgs {
     int C, H, K, HO;
     int accumulate;
     BnStatsFuse bn;  // bn.part == nullptr: no statistics
+    BnBwdFuse bnb;   // bnb.part == nullptr: no backward sums (transposed kernel only)
 };
 
 constexpr int round4(int v) { return (v + 3) / 4 * 4; }
@@ -90,7 +91,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     constexpr int WR = wrow(CC * 9);
     static_assert(TH * WO == 16 * NBW * WP, "pixel tiling");
     static_assert(CC % 4 == 0 && WIN % 4 == 0, "tiling");
-    static_assert(CC * PS >= WP * TK, "input tile reused by the statistics epilogue");
+    static_assert(CC * PS >= 2 * WP * TK, "input tile reused by the statistics epilogue");
     __shared__ __attribute__((aligned(16))) float Xs[CC * PS];
     __shared__ float Wc[TK * WR];
 
@@ -234,6 +235,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
                 }
     }
 
+    float gs1[4] = {0.f, 0.f, 0.f, 0.f}, gs2[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
         const int pix = (wp * NBW + nb) * 16 + j;
@@ -241,8 +243,47 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
             const int m = mblk + wk * 16 + 4 * g + i;
-            float* dst = a.y + (((size_t)img * a.K + m) * a.HO + oh0 + row) * WO + col;
-            *dst = a.accumulate ? *dst + acc[nb][i] : acc[nb][i];
+            const size_t idx = (((size_t)img * a.K + m) * a.HO + oh0 + row) * WO + col;
+            float* dst = a.y + idx;
+            const float v = a.accumulate ? *dst + acc[nb][i] : acc[nb][i];
+            *dst = v;
+            if (TRANS && a.bnb.part) {  // v is the final gradient of the preceding BN's output
+                const float gg = (a.bnb.relu && !(a.bnb.z[idx] > 0.f)) ? 0.f : v;
+                gs1[i] += gg;
+                gs2[i] += gg * ((a.bnb.y[idx] - a.bnb.mean[m]) * a.bnb.invstd[m]);
+            }
+        }
+    }
+    if constexpr (TRANS) {
+        if (a.bnb.part) {  // per-tile backward sums of each channel
+            float* red = Xs;  // [2][WP][TK]
+            __syncthreads();
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int off = 8; off > 0; off >>= 1) {
+                    gs1[i] += __shfl_xor(gs1[i], off, 16);
+                    gs2[i] += __shfl_xor(gs2[i], off, 16);
+                }
+            if (j == 0)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    red[wp * TK + wk * 16 + 4 * g + i] = gs1[i];
+                    red[(WP + wp) * TK + wk * 16 + 4 * g + i] = gs2[i];
+                }
+            __syncthreads();
+            if (wp == 0 && j == 0)
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    float t1 = 0.f, t2 = 0.f;
+                    for (int q = 0; q < WP; ++q) {
+                        t1 += red[q * TK + wk * 16 + 4 * g + i];
+                        t2 += red[(WP + q) * TK + wk * 16 + 4 * g + i];
+                    }
+                    const int m = mblk + wk * 16 + 4 * g + i;
+                    a.bnb.part[((size_t)m * gridDim.x + blockIdx.x) * 2 + 0] = t1;
+                    a.bnb.part[((size_t)m * gridDim.x + blockIdx.x) * 2 + 1] = t2;
+                }
         }
     }
     if constexpr (!TRANS) {
@@ -316,6 +357,7 @@ struct DgArgs {
     float* dx;        // [n][CL][2*HO][2*WO]
     int KL, CL, HO;
     int accumulate;
+    BnBwdFuse bnb;    // bnb.part == nullptr: no backward sums
 };
 
 template <int WO, int TH, int CC, int WK, int WP, int NBW>
@@ -328,6 +370,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
     constexpr int TK = 16 * WK;
     constexpr int WR = wrow(CC * 9);
     static_assert(TH * WO == 16 * NBW * WP, "pixel tiling");
+    static_assert(CC * PS >= 2 * WP * TK, "input tile reused by the backward-sums epilogue");
     __shared__ __attribute__((aligned(16))) float Xs[CC * PS];
     __shared__ float Wc[TK * WR];
 
@@ -402,6 +445,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
     }
     constexpr int W2 = 2 * WO;
     const int H2 = 2 * a.HO;
+    float gs1[4] = {0.f, 0.f, 0.f, 0.f}, gs2[4] = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
         const int pix = (wp * NBW + nb) * 16 + j;
@@ -411,7 +455,8 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
             const int m = mblk + wk * 16 + 4 * g + v;
 #pragma unroll
             for (int ph = 0; ph < 2; ++ph) {
-                float2* dst = reinterpret_cast<float2*>(a.dx + (((size_t)img * a.CL + m) * H2 + 2 * ii + ph) * W2 + 2 * jj);
+                const size_t idx = (((size_t)img * a.CL + m) * H2 + 2 * ii + ph) * W2 + 2 * jj;
+                float2* dst = reinterpret_cast<float2*>(a.dx + idx);
                 float2 val = make_float2(acc[nb][2 * ph][v], acc[nb][2 * ph + 1][v]);
                 if (a.accumulate) {
                     const float2 o = *dst;
@@ -419,8 +464,47 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
                     val.y += o.y;
                 }
                 *dst = val;
+                if (a.bnb.part) {
+                    const float2 zz = *reinterpret_cast<const float2*>(a.bnb.z + idx);
+                    const float2 yy = *reinterpret_cast<const float2*>(a.bnb.y + idx);
+                    const float g0 = (a.bnb.relu && !(zz.x > 0.f)) ? 0.f : val.x;
+                    const float g1 = (a.bnb.relu && !(zz.y > 0.f)) ? 0.f : val.y;
+                    const float mu = a.bnb.mean[m], is = a.bnb.invstd[m];
+                    gs1[v] += g0 + g1;
+                    gs2[v] += g0 * ((yy.x - mu) * is) + g1 * ((yy.y - mu) * is);
+                }
             }
         }
+    }
+    if (a.bnb.part) {
+        float* red = Xs;  // [2][WP][TK]
+        __syncthreads();
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+#pragma unroll
+            for (int off = 8; off > 0; off >>= 1) {
+                gs1[v] += __shfl_xor(gs1[v], off, 16);
+                gs2[v] += __shfl_xor(gs2[v], off, 16);
+            }
+        if (j == 0)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                red[wp * TK + wk * 16 + 4 * g + v] = gs1[v];
+                red[(WP + wp) * TK + wk * 16 + 4 * g + v] = gs2[v];
+            }
+        __syncthreads();
+        if (wp == 0 && j == 0)
+#pragma unroll
+            for (int v = 0; v < 4; ++v) {
+                float t1 = 0.f, t2 = 0.f;
+                for (int q = 0; q < WP; ++q) {
+                    t1 += red[q * TK + wk * 16 + 4 * g + v];
+                    t2 += red[(WP + q) * TK + wk * 16 + 4 * g + v];
+                }
+                const int m = mblk + wk * 16 + 4 * g + v;
+                a.bnb.part[((size_t)m * gridDim.x + blockIdx.x) * 2 + 0] = t1;
+                a.bnb.part[((size_t)m * gridDim.x + blockIdx.x) * 2 + 1] = t2;
+            }
     }
 }
 
@@ -453,15 +537,17 @@ int conv3x3_direct_tiles(int n, int C, int H, int W, int K, int stride)
 }
 
 hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const float* x, const float* w, float* y,
-                          int accumulate, bool transpose, hipStream_t st, const BnStatsFuse* bn)
+                          int accumulate, bool transpose, hipStream_t st, const BnStatsFuse* bn, const BnBwdFuse* bnb)
 {
+    if (bnb && (!transpose || stride != 1)) return hipErrorNotSupported;
     if (stride != 1 && stride != 2) return hipErrorNotSupported;
     if (H % stride || W % stride) return hipErrorNotSupported;
     if (bn && transpose) return hipErrorNotSupported;
     if ((uintptr_t)x % 16) return hipErrorNotSupported;  // float4 tile staging
     const int HO = H / stride, WO = W / stride;
-    DirArgs a{x, w, y, C, H, K, HO, accumulate, BnStatsFuse{nullptr}};
+    DirArgs a{x, w, y, C, H, K, HO, accumulate, BnStatsFuse{nullptr}, BnBwdFuse{}};
     if (bn) a.bn = *bn;
+    if (bnb) a.bnb = *bnb;
     if (C <= 4 && stride == 1 && !transpose) {  // first layer of an image net (3 input channels)
         if (WO == 32 && HO % 8 == 0 && K % 16 == 0) return launch_direct<32, 1, 8, 4, 1, 4, 4>(a, n, false, st);
         return hipErrorNotSupported;
@@ -482,20 +568,43 @@ hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const f
 
 namespace psw {
 hipError_t conv3x3_dgrad_s2(int n, int CL, int H, int W, int KL, const float* w, const float* dy, float* dx,
-                            int accumulate, hipStream_t st)
+                            int accumulate, hipStream_t st, const BnBwdFuse* bnb)
 {
     if (H % 2 || W % 2 || KL % 16) return hipErrorNotSupported;
     if ((uintptr_t)dy % 16 || (uintptr_t)dx % 8) return hipErrorNotSupported;  // float4 staging, float2 stores
     const int HO = H / 2, WO = W / 2;
-    DgArgs a{dy, w, dx, KL, CL, HO, accumulate};
+    DgArgs a{dy, w, dx, KL, CL, HO, accumulate, BnBwdFuse{}};
+    if (bnb) a.bnb = *bnb;
     if (WO == 16 && HO % 4 == 0 && CL % 16 == 0) {
         hipLaunchKernelGGL((conv3x3_dgrad_s2<16, 4, 16, 1, 4, 1>), dim3(n * (HO / 4), CL / 16), dim3(256), 0, st, a);
         return hipGetLastError();
     }
-    if (WO == 8 && HO % 2 == 0 && CL % 32 == 0) {
-        hipLaunchKernelGGL((conv3x3_dgrad_s2<8, 2, 16, 2, 1, 1>), dim3(n * (HO / 2), CL / 32), dim3(128), 0, st, a);
+    if (WO == 8 && HO % 8 == 0 && CL % 16 == 0) {
+        hipLaunchKernelGGL((conv3x3_dgrad_s2<8, 8, 16, 1, 4, 1>), dim3(n * (HO / 8), CL / 16), dim3(256), 0, st, a);
         return hipGetLastError();
     }
     return hipErrorNotSupported;
+}
+}  // namespace psw
+
+namespace psw {
+// tiles (workgroups along x) of the backward-data kernels that can carry the
+// BN backward sums; 0 when neither kernel covers the shape
+int dgrad_bnsums_tiles(int n, int CL, int H, int W, int KL, int stride)
+{
+    if (stride == 1) {
+        if (KL % 16) return 0;
+        if (W == 32 && H % 8 == 0 && CL % 16 == 0) return n * (H / 8);
+        if (W == 16 && H % 8 == 0 && CL % 32 == 0) return n * (H / 8);
+        if (W == 8 && H % 8 == 0 && CL % 32 == 0) return n * (H / 8);
+        return 0;
+    }
+    if (stride == 2) {
+        if (H % 2 || W % 2 || KL % 16) return 0;
+        const int HO = H / 2, WO = W / 2;
+        if (WO == 16 && HO % 4 == 0 && CL % 16 == 0) return n * (HO / 4);
+        if (WO == 8 && HO % 8 == 0 && CL % 16 == 0) return n * (HO / 8);
+    }
+    return 0;
 }
 }  // namespace psw

@@ -23,6 +23,20 @@ struct BnStatsFuse {
     float* part;
 };
 
+// Batch-norm backward sums fused into the epilogue of the backward-data
+// kernel that produces dz (the gradient of the BN output): with
+// g = dz * [z > 0] (relu) or dz and xhat = (y - mean) * invstd, every
+// workgroup writes (sum g, sum g*xhat) of each channel over its pixels to
+// part[channel][tile][2]; bn_bwd_from_partials merges them.
+struct BnBwdFuse {
+    float* part;
+    const float* z;       // BN output (its ReLU mask)
+    const float* y;       // BN input
+    const float* mean;
+    const float* invstd;
+    int relu;
+};
+
 // ---- convolution (implicit GEMM on MFMA) ----
 // Forward conv + fused BN statistics (direct kernel only); returns
 // hipErrorNotSupported when the shape has no direct configuration.
@@ -41,13 +55,29 @@ hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, co
 // Direct 3x3 / pad 1 kernel (forward, or backward-data of a stride-1 layer
 // when transpose is set); hipErrorNotSupported when no tile config fits.
 hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const float* x, const float* w, float* y,
-                          int accumulate, bool transpose, hipStream_t st, const BnStatsFuse* bn = nullptr);
+                          int accumulate, bool transpose, hipStream_t st, const BnStatsFuse* bn = nullptr,
+                          const BnBwdFuse* bnb = nullptr);
 // number of pixel tiles (workgroups along x) of the direct forward kernel, 0 if none
 int conv3x3_direct_tiles(int n, int C, int H, int W, int K, int stride);
 // Backward-data of a 3x3 / pad 1 / stride 2 conv (layer channels CL in, KL
 // out, input H x W); hipErrorNotSupported when no tile config fits.
 hipError_t conv3x3_dgrad_s2(int n, int CL, int H, int W, int KL, const float* w, const float* dy, float* dx,
-                            int accumulate, hipStream_t st);
+                            int accumulate, hipStream_t st, const BnBwdFuse* bnb = nullptr);
+int dgrad_bnsums_tiles(int n, int CL, int H, int W, int KL, int stride);
+// Backward data with the preceding BN's backward sums fused (direct kernel
+// or stride-2 kernel only); tiles = partials per channel, 0 if not fused.
+int conv_bwd_data_bnsums_tiles(const ConvShape& cs);
+hipError_t conv_bwd_data_bnsums(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate,
+                                const BnBwdFuse& bnb, hipStream_t st);
+// BN backward (+ identity residual) from per-tile (sum g, sum g*xhat)
+// partials over P pixels: merges them in a fixed order, writes dgamma,
+// dbeta (block 0 of a channel) and dy, and dres for an identity residual.
+hipError_t bn_bwd_from_partials(int n, int c, int h, int w, const float* dz, const float* z, const float* y,
+                                const float* gamma, const float* mean, const float* invstd, const float* part, int T,
+                                int relu, float* dy, float* dgamma, float* dbeta, float* dres_identity,
+                                int res_accumulate, hipStream_t st);
+hipError_t shortcut_a_backward(int n, int c, int h, int w, int rc, int rh, int rw, const float* dz, const float* z,
+                               int relu, float* dres, int accumulate, hipStream_t st);
 // Backward-weight partial sums of a 3x3 / pad 1 conv (dW-shaped, one per
 // workgroup); conv3x3_wgrad_splits is 0 when no configuration covers it.
 int conv3x3_wgrad_splits(int n, int C, int H, int W, int K, int stride);

@@ -557,12 +557,15 @@ hipError_t bn_bwd(int n, int c, int h, int w, const float* dz, const float* z, c
 }
 
 namespace {
-// grid (c, blocks per channel); each block merges its channel's T tile
-// partials (mean_t, M2_t over P pixels each) in a fixed order:
-//   mean = (1/T) sum mean_t,  M2 = sum M2_t + P sum (mean_t - mean)^2
-// then normalises its share of the channel's n*hw elements.
-constexpr int kApplyPerBlock = 4096;
+// Both kernels run on grid (c, blocks per channel): every block first merges
+// its channel's T per-tile partials in a fixed order (so all blocks of a
+// channel see bit-identical coefficients), then transforms its share of the
+// channel's n*hw elements.  Element loops walk float4 units of one channel
+// (unit u: image u / hw4, offset 4*(u % hw4)) with 32-bit index arithmetic.
+constexpr int kApplyUnits = 1024;  // float4 units per block
 
+// forward: tile partials (mean_t, M2_t over P pixels each)
+//   mean = (1/T) sum mean_t,  M2 = sum M2_t + P sum (mean_t - mean)^2
 __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int hw, const float* y, const float* part,
                                                                int T, int P, const float* gamma, const float* beta,
                                                                const float* res, int rc, int rh, int rw, int h, int w,
@@ -572,12 +575,12 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
 {
     __shared__ double sh[kBlock / 64];
     __shared__ float coef[2];
+    __shared__ double mean_sh;
     const int ch = blockIdx.x;
     const float* pp = part + (size_t)ch * T * 2;
     double s1 = 0.0;
     for (int t = threadIdx.x; t < T; t += kBlock) s1 += (double)pp[2 * t];
     s1 = block_sum(s1, sh);
-    __shared__ double mean_sh;
     if (threadIdx.x == 0) mean_sh = s1 / T;
     __syncthreads();
     const double mean = mean_sh;
@@ -605,27 +608,101 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
     }
     __syncthreads();
     const float sc = coef[0], sf = coef[1];
-    const int64_t total = (int64_t)n * hw;
-    const int64_t e0 = (int64_t)blockIdx.y * kApplyPerBlock;
-    const int64_t e1 = e0 + kApplyPerBlock < total ? e0 + kApplyPerBlock : total;
+    const int hw4 = hw >> 2;
+    const int units = n * hw4;
+    const int u0 = blockIdx.y * kApplyUnits;
+    const int u1 = min(u0 + kApplyUnits, units);
     const bool identity = res && rc == c && rh == h && rw == w;
     const int lo = (c - rc) / 2, cc = ch - lo;
-    for (int64_t e = e0 + threadIdx.x; e < e1; e += kBlock) {
-        const int img = (int)(e / hw), off = (int)(e - (int64_t)img * hw);
+    for (int u = u0 + threadIdx.x; u < u1; u += kBlock) {
+        const int img = u / hw4, off = (u - img * hw4) * 4;
         const size_t i = ((size_t)img * c + ch) * hw + off;
-        float v = y[i] * sc + sf;
-        if (res) {
-            if (identity) {
-                v += res[i];
-            } else if (cc >= 0 && cc < rc) {
-                const int hh = off / w, ww = off - hh * w;
-                v += res[(((size_t)img * rc + cc) * rh + hh * (rh / h)) * rw + ww * (rw / w)];
-            }
+        const float4 yv = *reinterpret_cast<const float4*>(y + i);
+        float v[4] = {yv.x * sc + sf, yv.y * sc + sf, yv.z * sc + sf, yv.w * sc + sf};
+        if (identity) {
+            const float4 r = *reinterpret_cast<const float4*>(res + i);
+            v[0] += r.x; v[1] += r.y; v[2] += r.z; v[3] += r.w;
+        } else if (res && cc >= 0 && cc < rc) {  // option-A shortcut: subsampled, channel-padded residual
+            const int hh = off / w, ww = off - hh * w;  // w % 4 == 0: the four elements share a row
+            const float* rp = res + (((size_t)img * rc + cc) * rh + hh * (rh / h)) * rw + ww * (rw / w);
+            const int sw = rw / w;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v[q] += rp[q * sw];
         }
-        if (relu) v = fmaxf(v, 0.f);
-        z[i] = v;
+        if (relu) {
+#pragma unroll
+            for (int q = 0; q < 4; ++q) v[q] = fmaxf(v[q], 0.f);
+        }
+        *reinterpret_cast<float4*>(z + i) = make_float4(v[0], v[1], v[2], v[3]);
     }
 }
+
+// backward: tile partials (sum g, sum g*xhat) with g = dz*[z > 0] (relu);
+//   dbeta = sum g, dgamma = sum g*xhat,
+//   dy = gamma*invstd*(g - dbeta/M - xhat*dgamma/M),  dres (+)= g (identity)
+__global__ __launch_bounds__(kBlock) void bn_bwd_partials_k(int n, int c, int hw, const float* dz, const float* z,
+                                                             const float* y, const float* gamma, const float* mean,
+                                                             const float* invstd, const float* part, int T, int relu,
+                                                             float* dy, float* dgamma, float* dbeta, float* dres,
+                                                             int res_accumulate)
+{
+    __shared__ double sh[kBlock / 64];
+    __shared__ float coef[3];
+    const int ch = blockIdx.x;
+    const float* pp = part + (size_t)ch * T * 2;
+    double s1 = 0.0, s2 = 0.0;
+    for (int t = threadIdx.x; t < T; t += kBlock) {
+        s1 += (double)pp[2 * t];
+        s2 += (double)pp[2 * t + 1];
+    }
+    s1 = block_sum(s1, sh);
+    s2 = block_sum(s2, sh);
+    const float mu = mean[ch], is = invstd[ch];
+    if (threadIdx.x == 0) {
+        const double cnt = (double)n * hw;
+        coef[0] = (float)((double)gamma[ch] * (double)is);
+        coef[1] = (float)(s1 / cnt);
+        coef[2] = (float)(s2 / cnt);
+        if (blockIdx.y == 0) {
+            dbeta[ch] = (float)s1;
+            dgamma[ch] = (float)s2;
+        }
+    }
+    __syncthreads();
+    const float a = coef[0], b = coef[1], d = coef[2];
+    const int hw4 = hw >> 2;
+    const int units = n * hw4;
+    const int u0 = blockIdx.y * kApplyUnits;
+    const int u1 = min(u0 + kApplyUnits, units);
+    for (int u = u0 + threadIdx.x; u < u1; u += kBlock) {
+        const int img = u / hw4, off = (u - img * hw4) * 4;
+        const size_t i = ((size_t)img * c + ch) * hw + off;
+        const float4 gv = *reinterpret_cast<const float4*>(dz + i);
+        const float4 zv = *reinterpret_cast<const float4*>(z + i);
+        const float4 yv = *reinterpret_cast<const float4*>(y + i);
+        float g[4] = {gv.x, gv.y, gv.z, gv.w};
+        const float zz[4] = {zv.x, zv.y, zv.z, zv.w};
+        const float yy[4] = {yv.x, yv.y, yv.z, yv.w};
+        float o[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            if (relu && !(zz[q] > 0.f)) g[q] = 0.f;
+            const float xh = (yy[q] - mu) * is;
+            o[q] = a * (g[q] - b - xh * d);
+        }
+        *reinterpret_cast<float4*>(dy + i) = make_float4(o[0], o[1], o[2], o[3]);
+        if (dres) {
+            float4 r = make_float4(g[0], g[1], g[2], g[3]);
+            if (res_accumulate) {
+                const float4 old = *reinterpret_cast<const float4*>(dres + i);
+                r.x += old.x; r.y += old.y; r.z += old.z; r.w += old.w;
+            }
+            *reinterpret_cast<float4*>(dres + i) = r;
+        }
+    }
+}
+
+bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 }  // namespace
 
 hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, const float* part, int T, int P,
@@ -633,10 +710,40 @@ hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, co
                                   int relu, float eps, float momentum, float* z, float* save_mean, float* save_invstd,
                                   float* run_mean, float* run_var, hipStream_t st)
 {
-    const int64_t total = (int64_t)n * h * w;
-    const unsigned per_ch = (unsigned)((total + kApplyPerBlock - 1) / kApplyPerBlock);
+    const bool identity = res && rc == c && rh == h && rw == w;
+    if (w % 4 || !aligned16(y) || !aligned16(z) || (identity && !aligned16(res))) return hipErrorNotSupported;
+    const int64_t units = (int64_t)n * h * w / 4;
+    if (units > INT32_MAX) return hipErrorNotSupported;
+    const unsigned per_ch = (unsigned)((units + kApplyUnits - 1) / kApplyUnits);
     hipLaunchKernelGGL(bn_apply_partials_k, dim3(c, per_ch), dim3(kBlock), 0, st, n, c, h * w, y, part, T, P, gamma,
                        beta, res, rc, rh, rw, h, w, relu, eps, momentum, z, save_mean, save_invstd, run_mean, run_var);
+    return hipGetLastError();
+}
+
+hipError_t bn_bwd_from_partials(int n, int c, int h, int w, const float* dz, const float* z, const float* y,
+                                const float* gamma, const float* mean, const float* invstd, const float* part, int T,
+                                int relu, float* dy, float* dgamma, float* dbeta, float* dres_identity,
+                                int res_accumulate, hipStream_t st)
+{
+    if (w % 4 || !aligned16(dz) || !aligned16(z) || !aligned16(y) || !aligned16(dy) ||
+        (dres_identity && !aligned16(dres_identity)))
+        return hipErrorNotSupported;
+    const int64_t units = (int64_t)n * h * w / 4;
+    if (units > INT32_MAX) return hipErrorNotSupported;
+    const unsigned per_ch = (unsigned)((units + kApplyUnits - 1) / kApplyUnits);
+    hipLaunchKernelGGL(bn_bwd_partials_k, dim3(c, per_ch), dim3(kBlock), 0, st, n, c, h * w, dz, z, y, gamma, mean,
+                       invstd, part, T, relu, dy, dgamma, dbeta, dres_identity, res_accumulate);
+    return hipGetLastError();
+}
+
+// option-A shortcut backward alone (the identity case is folded into the BN
+// backward kernels)
+hipError_t shortcut_a_backward(int n, int c, int h, int w, int rc, int rh, int rw, const float* dz, const float* z,
+                               int relu, float* dres, int accumulate, hipStream_t st)
+{
+    const int64_t rtotal = (int64_t)n * rc * rh * rw;
+    hipLaunchKernelGGL(shortcut_a_bwd, dim3(blocks_for(rtotal)), dim3(kBlock), 0, st, rtotal, c, h, w, rc, rh, rw, dz,
+                       z, relu, dres, accumulate);
     return hipGetLastError();
 }
 
