@@ -9,11 +9,24 @@ Inputs are synthetic N(0,1) [128,3,32,32] batches with uniform labels, all
 resident in HBM before timing starts.
 
 Prints one JSON line.  `value` is images/s over the K timed steps.
-`roofline` reports the convolution kernels (forward, backward-data,
-backward-weight: the matrix-core work of the path) against the fp32 MFMA
-peak, timed with HIP events recorded on the step's stream around every conv
-launcher during a second run of K steps.  `cpu_baseline` times the CPU oracle
-on a bounded sample (2 steps of the same workload).
+
+Measurement, in order: W warm-up steps; the K timed steps (wall clock, no
+events); then a profiling pass of min(K, 100) steps of the same workload in
+which every kernel is launched with a start / stop HIP event pair that the
+runtime stamps from the kernel's own dispatch (so the durations agree with a
+rocprofv3 kernel trace).  That pass gives the per-kernel table, the conv
+matrix-core figure the metric names, and the dominant kernel (largest summed
+time): `roofline.achieved` = its algorithmic work per launch / its mean
+launch duration.  `roofline.traffic` is
+the HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE counters
+(calibrated on a plain device copy) stored in profiles/traffic.json, used
+only when the kernel sources still hash to what was profiled, else null.
+`cpu_baseline` times the CPU oracle on a bounded sample (2 steps of the same
+workload).
+
+`python bench.py --copy-calibration` instead runs a plain streaming kernel
+five times: y = -x over 256 MiB (reads and writes 256 MiB each; the
+reference kernel for the counter scale).
 """
 from __future__ import annotations
 
@@ -29,44 +42,63 @@ sys.path.insert(0, ROOT)
 METRIC = "training images/sec at 1 GPU (ResNet-20, batch 128) + conv MFMA % of peak"
 PEAK_FP32_MFMA = 157.3   # TFLOP/s, MI355X dense fp32 matrix
 PEAK_BF16_MFMA = 2500.0  # TFLOP/s, MI355X dense bf16 matrix
+PEAK_HBM = 8000.0        # GB/s, MI355X HBM3E
+PROFILE_STEPS = 100
+COPY_BYTES = 256 << 20
 
 
-def shapes(ops, batch, in_shape):
-    """Output shape of every tensor (tensor 0 = the batch)."""
-    t = [(batch,) + tuple(in_shape)]
-    for o in ops:
-        kind, in0, _, cin, cout, k, st, pad, _ = (int(v) for v in o)
-        n, c, h, w = t[in0]
-        if kind == 1:
-            t.append((n, cout, (h + 2 * pad - k) // st + 1, (w + 2 * pad - k) // st + 1))
-        elif kind == 2:
-            t.append((n, c, h, w))
-        elif kind == 3:
-            t.append((n, c, (h - k) // st + 1, (w - k) // st + 1))
-        elif kind == 4:
-            t.append((n, c, 1, 1))
-        else:
-            t.append((n, cout, 1, 1))
-    return t
+def source_hash():
+    """sha256 over the library's kernel sources (csrc/*.hip, *.h, sorted)."""
+    import hashlib
+
+    d = os.path.join(ROOT, "paper_1912_12675_amd", "csrc")
+    h = hashlib.sha256()
+    for f in sorted(os.listdir(d)):
+        if f.endswith((".hip", ".h")):
+            h.update(f.encode())
+            with open(os.path.join(d, f), "rb") as fh:
+                h.update(fh.read())
+    return h.hexdigest()
 
 
-def conv_flops(ops, batch, in_shape):
-    """Algorithmic FLOPs of the conv passes of one step: 2*N*K*P*Q*C*R*S for
-    the forward, the backward-weight, and the backward-data pass (none for a
-    conv that reads the input batch)."""
-    t = shapes(ops, batch, in_shape)
-    fwd = bwd_w = bwd_d = 0
-    for i, o in enumerate(ops):
-        kind, in0, _, cin, cout, k, _, _, _ = (int(v) for v in o)
-        if kind != 1:
-            continue
-        n, kk, p, q = t[i + 1]
-        f = 2 * n * kk * p * q * cin * k * k
-        fwd += f
-        bwd_w += f
-        if in0 > 0:
-            bwd_d += f
-    return fwd, bwd_d, bwd_w
+def measured_traffic(kernel):
+    """HBM bytes per launch of `kernel` from profiles/traffic.json, or None
+    when absent, taken for another kernel, or taken on other sources."""
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    try:
+        with open(path) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernel") != kernel or t.get("source_sha256") != source_hash():
+        return None
+    return t.get("bytes_per_launch")
+
+
+def roofline_of(k, peak_flops):
+    """Roofline entry of one kernel's profile record (summed over launches)."""
+    t_s = k["ms"] * 1e-3
+    # the binding roof: the one the algorithmic work needs longer at
+    mfma = k["flops"] / (peak_flops * 1e12) >= k["bytes"] / (PEAK_HBM * 1e9)
+    if mfma:
+        ach = k["flops"] / t_s / 1e12
+        return {"bound": "mfma", "achieved": round(ach, 3), "peak": peak_flops, "unit": "TFLOP/s",
+                "frac": round(ach / peak_flops, 4)}
+    ach = k["bytes"] / t_s / 1e9
+    return {"bound": "hbm", "achieved": round(ach, 1), "peak": PEAK_HBM, "unit": "GB/s",
+            "frac": round(ach / PEAK_HBM, 4)}
+
+
+def copy_calibration():
+    import torch
+
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(5):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 5}), flush=True)
 
 
 def cpu_baseline(wl, steps=2):
@@ -93,7 +125,10 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--bf16", action="store_true", help="bf16-in / fp32-accumulate conv and FC products")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-profile", action="store_true", help="skip the event-timed second pass")
+    ap.add_argument("--no-profile", action="store_true",
+                    help="no events at all: skip the profiling pass and the dominant-kernel timing")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run a plain 256 MiB streaming kernel 5 times (counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for {args.gpus}): this build has no multi-GPU path; "
@@ -107,9 +142,13 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        copy_calibration()
+        return
     wl = synth.resnet20_workload(bf16=args.bf16)
     K, W = args.steps, args.warmup
-    T = K * (1 if args.no_profile else 2) + W
+    KP = 0 if args.no_profile else min(K, PROFILE_STEPS)
+    T = W + KP + K
     net = psw.Net(wl.ops, wl.batch, wl.in_shape, wl.stage_end, wl.ring_depth(T), bf16=wl.bf16)
     net.load_params(synth.init_params(wl))
     stal = wl.staleness(T)
@@ -133,6 +172,7 @@ def main():
 
     run(W)
     torch.cuda.synchronize()
+    # timed region: no events
     t0 = time.perf_counter()
     run(K)
     torch.cuda.synchronize()
@@ -142,26 +182,40 @@ def main():
     ms_per_step = 1000.0 * elapsed / K
     img_s = wl.batch * K / elapsed
 
-    fwd, bwd_d, bwd_w = conv_flops(wl.ops, wl.batch, wl.in_shape)
-    conv_flop = fwd + bwd_d + bwd_w
-    roof = None
-    breakdown = None
-    if not args.no_profile:
+    # profiling pass over the same workload: every kernel launched with
+    # start / stop events stamped from its own dispatch
+    peak = PEAK_BF16_MFMA if wl.bf16 else PEAK_FP32_MFMA
+    kernels, breakdown, conv, roof = [], None, None, None
+    if KP:
         net.profile(True)
-        run(K)
+        run(KP)
         torch.cuda.synchronize()
         prof = net.profile_read()
+        kernels = net.profile_kernels()
         net.profile(False)
-        breakdown = {k: round(v[0] / K, 4) for k, v in prof.items() if v[1]}
-        conv_ms = sum(prof[k][0] for k in ("conv_fwd", "conv_bwd_data", "conv_bwd_weight")) / K
-        launches = sum(prof[k][1] for k in ("conv_fwd", "conv_bwd_data", "conv_bwd_weight")) / K
-        achieved = conv_flop / (conv_ms * 1e-3) / 1e12
-        peak = PEAK_BF16_MFMA if wl.bf16 else PEAK_FP32_MFMA
-        roof = {"bound": "mfma", "achieved": round(achieved, 3), "peak": peak, "unit": "TFLOP/s",
-                "frac": round(achieved / peak, 4), "traffic": None,
-                "kernel": "conv implicit-GEMM launchers (forward, backward-data, backward-weight), all layers",
-                "flop_per_step": conv_flop, "conv_ms_per_step": round(conv_ms, 4),
-                "conv_launches_per_step": launches}
+        breakdown = {k: round(v[0] / KP, 4) for k, v in prof.items() if v[1]}
+        ck = [k for k in kernels if k["kind"] in ("conv_fwd", "conv_bwd_data", "conv_bwd_weight")]
+        conv_ms = sum(k["ms"] for k in ck) / KP
+        conv_flop = sum(k["flops"] for k in ck) / KP
+        ach = conv_flop / (conv_ms * 1e-3) / 1e12
+        conv = {"achieved": round(ach, 3), "peak": peak, "unit": "TFLOP/s", "frac": round(ach / peak, 4),
+                "flop_per_step": conv_flop, "conv_kernel_ms_per_step": round(conv_ms, 4),
+                "conv_kernel_launches_per_step": sum(k["launches"] for k in ck) / KP,
+                "what": "all convolution kernels (forward, backward-data with fused BN sums, backward-weight and "
+                        "its split reduction): algorithmic conv FLOPs / summed kernel time"}
+        d = kernels[0]  # the dominant kernel: largest summed time
+        roof = roofline_of(d, peak)
+        roof["traffic"] = measured_traffic(d["name"])
+        roof.update({"kernel": d["name"], "launches": d["launches"], "avg_launch_us": round(1e3 * d["ms"] / d["launches"], 3),
+                     "flop_per_launch": d["flops"] / d["launches"], "bytes_per_launch": d["bytes"] / d["launches"],
+                     "timed_over": f"{KP} steps of the same workload after the timed region, every kernel launched "
+                                   "with start/stop events stamped from its own dispatch"})
+    top = []
+    for k in kernels[:10]:
+        r = roofline_of(k, peak)
+        top.append({"kernel": k["name"], "kind": k["kind"], "launches_per_step": k["launches"] / KP,
+                    "us_per_step": round(1e3 * k["ms"] / KP, 2), "avg_launch_us": round(1e3 * k["ms"] / k["launches"], 3),
+                    "bound": r["bound"], "achieved": r["achieved"], "unit": r["unit"], "frac": r["frac"]})
 
     out = {
         "metric": METRIC,
@@ -180,7 +234,9 @@ def main():
                                "SGD momentum 0.9, lr 0.01",
                    "global_batch": wl.batch, "input": "3x32x32 N(0,1)", "parallelism": "single GPU, all stages"},
         "roofline": roof,
+        "conv_mfma": conv,
         "kernel_ms_per_step": breakdown,
+        "top_kernels": top,
         "final_loss": round(loss, 5),
     }
     if not args.no_cpu_baseline:

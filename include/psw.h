@@ -277,20 +277,45 @@ enum {
 int psw_net_plan(const psw_net *net, int64_t t, const int32_t *staleness, psw_launch *out, int cap,
                  int *n_out);
 
-/* Per-launch timing of psw_stage_step with HIP events recorded on the
- * step's stream around every launcher (for measurement; off by default).
- * psw_net_profile(net, 1) enables it and clears previous records;
- * psw_net_profile_read waits for the recorded events, writes the summed
- * milliseconds and launcher counts per PSW_PROF_* kind into the host arrays
- * ms[n_kinds] and launches[n_kinds], and clears the records.  Events are
- * created on first use and kept until psw_net_destroy. */
+/* Per-kernel timing of psw_stage_step (for measurement; off by default).
+ * With profiling on, every kernel the library launches inside
+ * psw_stage_step is bracketed by two HIP events recorded on the step's
+ * stream, and tagged with the kind of launcher that issued it, the kernel's
+ * name (template arguments as the compiler spells them, so the name matches
+ * a kernel trace) and its algorithmic work.
+ * psw_net_profile(net, enable) switches profiling and clears the records;
+ * the records are kept until the next psw_net_profile call.
+ * psw_net_profile_only does the same but records only the launches of the
+ * kernel with exactly the given name (NULL or "" = every kernel), so that
+ * one kernel can be timed inside a throughput run at the cost of two events
+ * per launch of it.  Events are created on first use and kept until
+ * psw_net_destroy.
+ * psw_net_profile_read waits for the recorded events and writes the summed
+ * milliseconds and kernel launch counts per PSW_PROF_* kind into the host
+ * arrays ms[n_kinds] and launches[n_kinds].
+ * psw_net_profile_kernels writes one psw_kernel_stat per distinct kernel
+ * name (at most cap of them, in decreasing total time) and the number of
+ * distinct names to *n_out.  flops and bytes are the summed algorithmic work
+ * of the launches: floating-point operations of what the kernel computes
+ * (a convolution pass counts 2*N*P*Q*K*C*R*S) and the minimal HBM bytes
+ * (each operand read once, each result written once). */
 enum {
     PSW_PROF_CONV_FWD = 0, PSW_PROF_CONV_BWD_DATA = 1, PSW_PROF_CONV_BWD_WEIGHT = 2, PSW_PROF_BN_FWD = 3,
     PSW_PROF_BN_BWD = 4, PSW_PROF_POOL = 5, PSW_PROF_FC = 6, PSW_PROF_LOSS = 7, PSW_PROF_SGD = 8,
     PSW_PROF_OTHER = 9, PSW_PROF_KINDS = 10
 };
+typedef struct psw_kernel_stat {
+    char name[192];
+    int32_t kind;     /* PSW_PROF_* kind of its first launch */
+    int64_t launches;
+    double ms;        /* summed event time */
+    double flops;     /* summed algorithmic floating-point operations */
+    double bytes;     /* summed algorithmic HBM bytes */
+} psw_kernel_stat;
 int psw_net_profile(psw_net *net, int enable);
+int psw_net_profile_only(psw_net *net, int enable, const char *kernel);
 int psw_net_profile_read(psw_net *net, int n_kinds, double *ms, int64_t *launches);
+int psw_net_profile_kernels(psw_net *net, int cap, psw_kernel_stat *out, int *n_out);
 
 #ifdef __cplusplus
 }

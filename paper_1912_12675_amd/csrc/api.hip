@@ -22,6 +22,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <string>
 #include <vector>
 
@@ -284,23 +285,59 @@ struct psw_net {
 
     std::vector<char> grad_accum;           // per op input slot: 0 overwrite, 1 accumulate (in0, in1)
     size_t ws_off = 0, ws_bytes = 0, arena_bytes = 0;
+    size_t wsw_off = 0, wsw_bytes = 0;      // workspace of the backward-weight kernels (side stream)
+    // backward-weight kernels run on a second stream of the library, forked
+    // from the caller's stream when a conv's output gradient is final and
+    // joined before the update (created at bind, default priority)
+    hipStream_t side = nullptr;
+    std::vector<hipEvent_t> fork_ev;        // per op
+    hipEvent_t join_ev = nullptr;
     // bound memory
     float *ring = nullptr, *momentum = nullptr, *grad = nullptr, *run_mean = nullptr, *run_var = nullptr;
     char* arena = nullptr;
     bool bound = false;
     int64_t next_t = 0;
-    // optional per-launch timing with HIP events (psw_net_profile)
-    struct ProfRec {
+    // optional per-kernel timing with HIP events (psw_net_profile): while
+    // psw_stage_step runs with profiling on, rec is this thread's kernel
+    // recorder and every library kernel launch adds one KRec
+    struct KRec {
         int kind;
+        std::string name;
+        psw::Work work;
         hipEvent_t a, b;
     };
+    struct Recorder final : psw::KernelRecorder {
+        psw_net* net = nullptr;
+        int kind = PSW_PROF_OTHER;  // the launcher being issued
+        std::string only;           // non-empty: time launches of this kernel only
+        bool begin(const std::string& name, hipEvent_t* start, hipEvent_t* stop) override
+        {
+            if (!only.empty() && name != only) return false;
+            *start = net->next_event();
+            *stop = *start ? net->next_event() : nullptr;
+            return *start && *stop;
+        }
+        void end(std::string&& name, const psw::Work& w, hipEvent_t start, hipEvent_t stop) override
+        {
+            net->krecs.push_back(KRec{kind, std::move(name), w, start, stop});
+        }
+    };
     bool profiling = false;
+    Recorder rec;
     std::vector<hipEvent_t> ev_pool;
     size_t ev_used = 0;
-    std::vector<ProfRec> prof;
+    std::vector<KRec> krecs;
+    psw_net() { rec.net = this; }
+    psw_net(const psw_net&) = delete;
+    psw_net& operator=(const psw_net&) = delete;
     ~psw_net()
     {
         for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
+        if (side) (void)hipStreamSynchronize(side);
+        for (hipEvent_t e : fork_ev)
+            if (e) (void)hipEventDestroy(e);
+        if (join_ev) (void)hipEventDestroy(join_ev);
+        if (side) (void)hipStreamDestroy(side);
     }
     hipEvent_t next_event()
     {
@@ -312,6 +349,14 @@ struct psw_net {
         return ev_pool[ev_used++];
     }
 };
+
+namespace psw {
+KernelRecorder*& kernel_recorder()
+{
+    static thread_local KernelRecorder* r = nullptr;
+    return r;
+}
+}  // namespace psw
 
 namespace {
 
@@ -446,6 +491,7 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
         net->grad_off[i] = off;
         off = align256(off + (size_t)net->t[i].numel() * sizeof(float));
     }
+    size_t wsw = 0;
     size_t ws = 0;
     net->fuse_stats.assign(n_layers, 0);
     net->fused_now.assign(n_layers, 0);
@@ -464,7 +510,7 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
         } else if (o.kind == PSW_OP_CONV) {
             psw::ConvShape cs;
             check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, prec, &cs);
-            ws = std::max(ws, psw::conv_bwd_weight_ws_bytes(cs, prec == PSW_BF16));
+            wsw = std::max(wsw, psw::conv_bwd_weight_ws_bytes(cs, prec == PSW_BF16));
             // BN right after this conv, on its output only: statistics in the conv epilogue
             const bool next_bn = i + 1 < n_layers && net->ops[i + 1].kind == PSW_OP_BN && net->ops[i + 1].in0 == i + 1;
             const bool plain = !(o.flags & (PSW_F_BIAS | PSW_F_RELU)) && prec == PSW_FP32;
@@ -485,6 +531,9 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
     net->ws_off = off;
     net->ws_bytes = align256(ws);
     off += net->ws_bytes;
+    net->wsw_off = off;
+    net->wsw_bytes = align256(wsw);
+    off += net->wsw_bytes;
     net->arena_bytes = off;
     g_err.clear();
     return PSW_OK;
@@ -562,6 +611,20 @@ int psw_net_bind(psw_net* net, float* ring, float* momentum, float* grad, float*
     net->run_mean = run_mean;
     net->run_var = run_var;
     net->arena = (char*)arena;
+    if (!net->side) {
+        hipError_t e = hipStreamCreateWithFlags(&net->side, hipStreamNonBlocking);
+        if (e != hipSuccess) {
+            net->side = nullptr;
+            return hip_check(e, "net_bind: side stream");
+        }
+        net->fork_ev.assign(net->ops.size(), nullptr);
+        for (auto& ev : net->fork_ev) {
+            e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+            if (e != hipSuccess) return hip_check(e, "net_bind: events");
+        }
+        e = hipEventCreateWithFlags(&net->join_ev, hipEventDisableTiming);
+        if (e != hipSuccess) return hip_check(e, "net_bind: events");
+    }
     net->bound = true;
     return PSW_OK;
 }
@@ -665,28 +728,43 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
     auto grd = [&](int id) -> float* { return (float*)(A + net->grad_off[id]); };
     void* ws = A + net->ws_off;
     const size_t wsb = net->ws_bytes;
+    void* wsw = A + net->wsw_off;
+    const size_t wswb = net->wsw_bytes;
+    // side-stream work is always joined back into the caller's stream, also
+    // when a launcher fails part way (the error is reported all the same)
+    struct Join {
+        hipStream_t main, side;
+        hipEvent_t ev;
+        bool forked = false;
+        hipError_t join()
+        {
+            if (!forked) return hipSuccess;
+            forked = false;
+            hipError_t e = hipEventRecord(ev, side);
+            if (e == hipSuccess) e = hipStreamWaitEvent(main, ev, 0);
+            return e;
+        }
+        ~Join() { (void)join(); }
+    } joiner{st, net->side, net->join_ev};
+    bool& forked = joiner.forked;
     std::vector<int64_t> rv(net->S);
     for (int s = 0; s < net->S; ++s) rv[s] = fwd_version(t, staleness[s]);
     auto wfwd = [&](int i) { return slot_ptr(net, net->stage_of[i], rv[net->stage_of[i]]) + net->poff[i]; };
     auto wcur = [&](int i) { return slot_ptr(net, net->stage_of[i], t) + net->poff[i]; };
     auto gptr = [&](int i) { return net->grad + net->flat_off[net->stage_of[i]] + net->poff[i]; };
     hipError_t e = hipSuccess;
-    // kind of the launcher being issued, for psw_net_profile
-    int kind = PSW_PROF_OTHER;
+    // kind of the launcher being issued, for psw_net_profile; with profiling
+    // on, every kernel launched below is timed by net->rec
+    int& kind = net->rec.kind;
+    kind = PSW_PROF_OTHER;
+    struct RecorderScope {
+        explicit RecorderScope(psw::KernelRecorder* r) { psw::kernel_recorder() = r; }
+        ~RecorderScope() { psw::kernel_recorder() = nullptr; }
+    } rec_scope(net->profiling ? &net->rec : nullptr);
 #define PSW_TRY(expr, what)                                                   \
     do {                                                                      \
-        hipEvent_t ea = nullptr, eb = nullptr;                                \
-        if (net->profiling) {                                                 \
-            ea = net->next_event();                                           \
-            eb = net->next_event();                                           \
-            if (ea && eb) (void)hipEventRecord(ea, st);                       \
-        }                                                                     \
         e = (expr);                                                           \
         if (e != hipSuccess) return hip_check(e, what);                       \
-        if (ea && eb) {                                                       \
-            (void)hipEventRecord(eb, st);                                     \
-            net->prof.push_back(psw_net::ProfRec{kind, ea, eb});              \
-        }                                                                     \
     } while (0)
 
     // ---- forward: every stage with its (possibly stale) version r_s ----
@@ -703,24 +781,11 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
             net->fused_now[i] = 0;
             if (net->fuse_stats[i]) {  // the next op's BN statistics come out of this conv
                 psw::BnStatsFuse bn{(float*)ws};
-                hipEvent_t ea = nullptr, eb = nullptr;
-                if (net->profiling) {
-                    ea = net->next_event();
-                    eb = net->next_event();
-                    if (ea && eb) (void)hipEventRecord(ea, st);
-                }
                 e = psw::conv_fwd_bnstats(cs, act(o.in0), W, act(i + 1), bn, wsb / sizeof(float), st);
-                if (e == hipSuccess) {
+                if (e == hipSuccess)
                     net->fused_now[i] = 1;
-                    if (ea && eb) {
-                        (void)hipEventRecord(eb, st);
-                        net->prof.push_back(psw_net::ProfRec{kind, ea, eb});
-                    }
-                } else if (e != hipErrorNotSupported) {
+                else if (e != hipErrorNotSupported)  // not supported: nothing launched, unfused path below
                     return hip_check(e, "conv_fwd_bnstats");
-                } else if (ea && eb) {
-                    net->ev_used -= 2;  // nothing was launched between the two events
-                }
             }
             if (!net->fused_now[i]) {
                 PSW_TRY(psw::conv_fwd(cs, act(o.in0), W, b, (o.flags & PSW_F_RELU) != 0, act(i + 1), bf16, st),
@@ -741,25 +806,13 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
                 check_conv(ci.n, ci.c, ci.h, ci.w, cv.cout, cv.k, cv.k, cv.stride, cv.pad, net->prec, &ccs);
                 const int T = psw::conv_fwd_bnstats_tiles(ccs);
                 const int P = a.n * a.h * a.w / T;
-                hipEvent_t ea = nullptr, eb = nullptr;
-                if (net->profiling) {
-                    ea = net->next_event();
-                    eb = net->next_event();
-                    if (ea && eb) (void)hipEventRecord(ea, st);
-                }
                 e = psw::bn_apply_from_partials(a.n, a.c, a.h, a.w, act(o.in0), (const float*)ws, T, P, W, W + o.cin,
                                                 o.in1 >= 0 ? act(o.in1) : nullptr, r.c, r.h, r.w,
                                                 (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, act(i + 1), save,
                                                 save + o.cin, rm, rvv, st);
-                if (e == hipSuccess) {
-                    if (ea && eb) {
-                        (void)hipEventRecord(eb, st);
-                        net->prof.push_back(psw_net::ProfRec{kind, ea, eb});
-                    }
-                    break;
-                }
+                if (e == hipSuccess) break;
                 if (e != hipErrorNotSupported) return hip_check(e, "bn_apply");
-                if (ea && eb) net->ev_used -= 2;  // nothing launched: statistics are recomputed below
+                // not supported: nothing launched, the statistics are recomputed below
             }
             PSW_TRY(psw::bn_fwd(a.n, a.c, a.h, a.w, act(o.in0), W, W + o.cin, o.in1 >= 0 ? act(o.in1) : nullptr, r.c,
                                 r.h, r.w, (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, act(i + 1), save, save + o.cin, rm,
@@ -807,7 +860,11 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
             float* dw = gptr(i);
             float* db = (o.flags & PSW_F_BIAS) ? dw + (int64_t)o.cout * o.cin * o.k * o.k : nullptr;
             kind = PSW_PROF_CONV_BWD_WEIGHT;
-            PSW_TRY(psw::conv_bwd_weight(cs, act(o.in0), g, dw, db, bf16, ws, wsb, st), "conv_bwd_weight");
+            // fork: the weight gradient runs beside the data-gradient chain
+            PSW_TRY(hipEventRecord(net->fork_ev[i], st), "fork");
+            PSW_TRY(hipStreamWaitEvent(net->side, net->fork_ev[i], 0), "fork");
+            forked = true;
+            PSW_TRY(psw::conv_bwd_weight(cs, act(o.in0), g, dw, db, bf16, wsw, wswb, net->side), "conv_bwd_weight");
             kind = PSW_PROF_CONV_BWD_DATA;
             net->fused_bwd_now[i] = 0;
             if (din && net->fuse_bwd[i]) {  // BN op i-1's backward sums out of this dgrad
@@ -815,23 +872,13 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
                 const float* bsave = (const float*)(A + net->save_off[i - 1]);
                 const psw::BnBwdFuse bnb{(float*)ws, act(i), act(bo.in0), bsave, bsave + bo.cin,
                                          (bo.flags & PSW_F_RELU) != 0};
-                hipEvent_t ea = nullptr, eb = nullptr;
-                if (net->profiling) {
-                    ea = net->next_event();
-                    eb = net->next_event();
-                    if (ea && eb) (void)hipEventRecord(ea, st);
-                }
                 e = psw::conv_bwd_data_bnsums(cs, wcur(i), g, din, acc0, bnb, st);
                 if (e == hipSuccess) {
                     net->fused_bwd_now[i] = 1;
-                    if (ea && eb) {
-                        (void)hipEventRecord(eb, st);
-                        net->prof.push_back(psw_net::ProfRec{kind, ea, eb});
-                    }
                     break;
                 }
                 if (e != hipErrorNotSupported) return hip_check(e, "conv_bwd_data_bnsums");
-                if (ea && eb) net->ev_used -= 2;  // nothing was launched between the two events
+                // not supported: nothing launched, unfused path below
             }
             if (din) PSW_TRY(psw::conv_bwd_data(cs, wcur(i), g, din, acc0, bf16, st), "conv_bwd_data");
             break;
@@ -850,27 +897,15 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
                 const int T = psw::conv_bwd_data_bnsums_tiles(ccs);
                 const bool identity = dres && r.c == a.c && r.h == a.h && r.w == a.w;
                 const int racc = net->grad_accum[2 * i + 1];
-                hipEvent_t ea = nullptr, eb = nullptr;
-                if (net->profiling) {
-                    ea = net->next_event();
-                    eb = net->next_event();
-                    if (ea && eb) (void)hipEventRecord(ea, st);
-                }
                 e = psw::bn_bwd_from_partials(a.n, a.c, a.h, a.w, g, act(i + 1), act(o.in0), wcur(i), save,
                                               save + o.cin, (const float*)ws, T, (o.flags & PSW_F_RELU) != 0, din, dg,
                                               dg + o.cin, identity ? dres : nullptr, racc, st);
                 if (e == hipSuccess && dres && !identity)
                     e = psw::shortcut_a_backward(a.n, a.c, a.h, a.w, r.c, r.h, r.w, g, act(i + 1),
                                                  (o.flags & PSW_F_RELU) != 0, dres, racc, st);
-                if (e == hipSuccess) {
-                    if (ea && eb) {
-                        (void)hipEventRecord(eb, st);
-                        net->prof.push_back(psw_net::ProfRec{kind, ea, eb});
-                    }
-                    break;
-                }
+                if (e == hipSuccess) break;
                 if (e != hipErrorNotSupported) return hip_check(e, "bn_bwd_from_partials");
-                if (ea && eb) net->ev_used -= 2;  // nothing launched: sums are recomputed below
+                // not supported: nothing launched, the sums are recomputed below
             }
             PSW_TRY(psw::bn_bwd(a.n, a.c, a.h, a.w, g, act(i + 1), act(o.in0), wcur(i), save, save + o.cin,
                                 (o.flags & PSW_F_RELU) != 0, din, dg, dg + o.cin, dres, r.c, r.h, r.w,
@@ -901,6 +936,8 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
         }
         }
     }
+    // ---- join: every weight gradient is complete before the update ----
+    PSW_TRY(joiner.join(), "join");
     // ---- update: version t+1 of every stage ----
     for (int s = 0; s < net->S; ++s) {
         const float* win = slot_ptr(net, s, t);
@@ -919,12 +956,30 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
 
 int psw_net_profile(psw_net* net, int enable)
 {
+    return psw_net_profile_only(net, enable, nullptr);
+}
+
+int psw_net_profile_only(psw_net* net, int enable, const char* kernel)
+{
     if (!net) return fail(PSW_ERR_NULL, "net_profile: net is NULL");
     net->profiling = enable != 0;
-    net->prof.clear();
+    net->rec.only = kernel ? kernel : "";
+    net->krecs.clear();
     net->ev_used = 0;
     return PSW_OK;
 }
+
+namespace {
+hipError_t krec_ms(const psw_net::KRec& r, double* ms)
+{
+    hipError_t e = hipEventSynchronize(r.b);
+    if (e != hipSuccess) return e;
+    float t = 0.f;
+    e = hipEventElapsedTime(&t, r.a, r.b);
+    *ms = t;
+    return e;
+}
+}  // namespace
 
 int psw_net_profile_read(psw_net* net, int n_kinds, double* ms, int64_t* launches)
 {
@@ -933,19 +988,44 @@ int psw_net_profile_read(psw_net* net, int n_kinds, double* ms, int64_t* launche
         ms[k] = 0.0;
         launches[k] = 0;
     }
-    for (const auto& r : net->prof) {
-        hipError_t e = hipEventSynchronize(r.b);
-        if (e != hipSuccess) return hip_check(e, "net_profile_read");
-        float t = 0.f;
-        e = hipEventElapsedTime(&t, r.a, r.b);
+    for (const auto& r : net->krecs) {
+        double t = 0.0;
+        hipError_t e = krec_ms(r, &t);
         if (e != hipSuccess) return hip_check(e, "net_profile_read");
         if (r.kind >= 0 && r.kind < n_kinds) {
             ms[r.kind] += t;
             launches[r.kind] += 1;
         }
     }
-    net->prof.clear();
-    net->ev_used = 0;
+    return PSW_OK;
+}
+
+int psw_net_profile_kernels(psw_net* net, int cap, psw_kernel_stat* out, int* n_out)
+{
+    if (!net || !n_out || (cap > 0 && !out)) return fail(PSW_ERR_NULL, "net_profile_kernels: required pointer is NULL");
+    std::vector<psw_kernel_stat> st;
+    std::vector<std::string> names;
+    for (const auto& r : net->krecs) {
+        double t = 0.0;
+        hipError_t e = krec_ms(r, &t);
+        if (e != hipSuccess) return hip_check(e, "net_profile_kernels");
+        size_t j = 0;
+        while (j < names.size() && names[j] != r.name) ++j;
+        if (j == names.size()) {
+            names.push_back(r.name);
+            psw_kernel_stat k{};
+            snprintf(k.name, sizeof(k.name), "%s", r.name.c_str());
+            k.kind = r.kind;
+            st.push_back(k);
+        }
+        st[j].launches += 1;
+        st[j].ms += t;
+        st[j].flops += r.work.flops;
+        st[j].bytes += r.work.bytes;
+    }
+    std::stable_sort(st.begin(), st.end(), [](const psw_kernel_stat& x, const psw_kernel_stat& y) { return x.ms > y.ms; });
+    *n_out = (int)st.size();
+    for (int i = 0; i < cap && i < (int)st.size(); ++i) out[i] = st[i];
     return PSW_OK;
 }
 

@@ -246,15 +246,19 @@ hipError_t launch(const IgArgs& a, int splits, hipStream_t st)
 {
     const int M = a.M;
     dim3 block(256);
+    const Work wk = conv_work(a.n, a.c, a.h, a.w, a.k, a.r, a.s, a.p, a.q);
     if (M <= 16) {
         dim3 grid((a.N + 127) / 128, (M + 15) / 16, splits);
-        hipLaunchKernelGGL((igemm_kernel<PASS, 16, 128, 1, 4, BF16>), grid, block, 0, st, a);
+        PSW_LAUNCH(kname("igemm_kernel", PASS, 16, 128, 1, 4, BF16), wk, (igemm_kernel<PASS, 16, 128, 1, 4, BF16>),
+                   grid, block, 0, st, a);
     } else if (M <= 32) {
         dim3 grid((a.N + 127) / 128, (M + 31) / 32, splits);
-        hipLaunchKernelGGL((igemm_kernel<PASS, 32, 128, 1, 4, BF16>), grid, block, 0, st, a);
+        PSW_LAUNCH(kname("igemm_kernel", PASS, 32, 128, 1, 4, BF16), wk, (igemm_kernel<PASS, 32, 128, 1, 4, BF16>),
+                   grid, block, 0, st, a);
     } else {
         dim3 grid((a.N + 127) / 128, (M + 63) / 64, splits);
-        hipLaunchKernelGGL((igemm_kernel<PASS, 64, 128, 2, 2, BF16>), grid, block, 0, st, a);
+        PSW_LAUNCH(kname("igemm_kernel", PASS, 64, 128, 2, 2, BF16), wk, (igemm_kernel<PASS, 64, 128, 2, 2, BF16>),
+                   grid, block, 0, st, a);
     }
     return hipGetLastError();
 }
@@ -377,8 +381,8 @@ hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy,
         hipError_t e = conv3x3_wgrad(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, (float*)ws, st);
         if (e != hipErrorNotSupported) {  // otherwise (misaligned operands) fall through to the implicit GEMM
             if (e != hipSuccess) return e;
-            hipLaunchKernelGGL(reduce_splits, dim3((unsigned)((mn + 15) / 16)), dim3(256), 0, st, (const float*)ws,
-                               zd, (int64_t)mn, dw);
+            PSW_LAUNCH(kname("reduce_splits"), (Work{(double)zd * mn, kF * (zd + 1.0) * mn}), reduce_splits,
+                       dim3((unsigned)((mn + 15) / 16)), dim3(256), 0, st, (const float*)ws, zd, (int64_t)mn, dw);
             e = hipGetLastError();
             if (e != hipSuccess || !db) return e;
             const size_t zmax = conv_bwd_weight_ws_bytes(cs, bf16) - channel_sum_ws_bytes(cs.n, cs.k, cs.p * cs.q);
@@ -397,8 +401,8 @@ hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy,
     const int zz = (int)(((int64_t)a.Kd + a.kchunk - 1) / a.kchunk);
     hipError_t e = bf16 ? launch<BWD_WEIGHT, true>(a, zz, st) : launch<BWD_WEIGHT, false>(a, zz, st);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(reduce_splits, dim3((unsigned)((mn + 15) / 16)), dim3(256), 0, st, (const float*)ws, zz,
-                       (int64_t)mn, dw);
+    PSW_LAUNCH(kname("reduce_splits"), (Work{(double)zz * mn, kF * (zz + 1.0) * mn}), reduce_splits,
+               dim3((unsigned)((mn + 15) / 16)), dim3(256), 0, st, (const float*)ws, zz, (int64_t)mn, dw);
     e = hipGetLastError();
     if (e != hipSuccess || !db) return e;
     const size_t zmax = conv_bwd_weight_ws_bytes(cs, bf16) - channel_sum_ws_bytes(cs.n, cs.k, cs.p * cs.q);

@@ -235,25 +235,56 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
                 }
     }
 
-    float gs1[4] = {0.f, 0.f, 0.f, 0.f}, gs2[4] = {0.f, 0.f, 0.f, 0.f};
+    // epilogue: every global load is issued before the first store (the
+    // output may alias nothing, but the compiler cannot know that, and a
+    // load after a store would wait for it)
+    size_t oidx[NBW];  // index of (channel mblk+wk*16+4g, pixel) of block nb
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
         const int pix = (wp * NBW + nb) * 16 + j;
         const int row = pix / WO, col = pix - (pix / WO) * WO;
+        oidx[nb] = (((size_t)img * a.K + mblk + wk * 16 + 4 * g) * a.HO + oh0 + row) * WO + col;
+    }
+    const size_t cstr = (size_t)a.HO * WO;  // channel stride
+    if (a.accumulate) {
+        float old[NBW][4];
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) old[nb][i] = a.y[oidx[nb] + i * cstr];
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) acc[nb][i] += old[nb][i];
+    }
+    float gs1[4] = {0.f, 0.f, 0.f, 0.f}, gs2[4] = {0.f, 0.f, 0.f, 0.f};
+    if (TRANS && a.bnb.part) {  // acc is the final gradient of the preceding BN's output
+        float zz[NBW][4], yy[NBW][4], mu[4], is[4];
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                zz[nb][i] = a.bnb.z[oidx[nb] + i * cstr];
+                yy[nb][i] = a.bnb.y[oidx[nb] + i * cstr];
+            }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            const int m = mblk + wk * 16 + 4 * g + i;
-            const size_t idx = (((size_t)img * a.K + m) * a.HO + oh0 + row) * WO + col;
-            float* dst = a.y + idx;
-            const float v = a.accumulate ? *dst + acc[nb][i] : acc[nb][i];
-            *dst = v;
-            if (TRANS && a.bnb.part) {  // v is the final gradient of the preceding BN's output
-                const float gg = (a.bnb.relu && !(a.bnb.z[idx] > 0.f)) ? 0.f : v;
-                gs1[i] += gg;
-                gs2[i] += gg * ((a.bnb.y[idx] - a.bnb.mean[m]) * a.bnb.invstd[m]);
-            }
+            mu[i] = a.bnb.mean[mblk + wk * 16 + 4 * g + i];
+            is[i] = a.bnb.invstd[mblk + wk * 16 + 4 * g + i];
         }
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                const float gg = (a.bnb.relu && !(zz[nb][i] > 0.f)) ? 0.f : acc[nb][i];
+                gs1[i] += gg;
+                gs2[i] += gg * ((yy[nb][i] - mu[i]) * is[i]);
+            }
     }
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) a.y[oidx[nb] + i * cstr] = acc[nb][i];
     if constexpr (TRANS) {
         if (a.bnb.part) {  // per-tile backward sums of each channel
             float* red = Xs;  // [2][WP][TK]
@@ -445,37 +476,80 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
     }
     constexpr int W2 = 2 * WO;
     const int H2 = 2 * a.HO;
-    float gs1[4] = {0.f, 0.f, 0.f, 0.f}, gs2[4] = {0.f, 0.f, 0.f, 0.f};
+    // all loads before the first store (see the direct kernel's epilogue)
+    size_t oidx[NBW];  // dx index of (channel mblk+wk*16+4g, row 2ii, col 2jj) of block nb
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
         const int pix = (wp * NBW + nb) * 16 + j;
         const int ii = i0 + pix / WO, jj = pix - (pix / WO) * WO;
+        oidx[nb] = (((size_t)img * a.CL + mblk + wk * 16 + 4 * g) * H2 + 2 * ii) * W2 + 2 * jj;
+    }
+    const size_t cstr = (size_t)H2 * W2;
+    // element (nb, v, ph): dx[oidx[nb] + v*cstr + ph*W2 + {0,1}] = classes (ph,0), (ph,1)
+    float2 val[NBW][4][2];
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+#pragma unroll
+            for (int ph = 0; ph < 2; ++ph) val[nb][v][ph] = make_float2(acc[nb][2 * ph][v], acc[nb][2 * ph + 1][v]);
+    if (a.accumulate) {
+        float2 old[NBW][4][2];
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+#pragma unroll
+                for (int ph = 0; ph < 2; ++ph)
+                    old[nb][v][ph] = *reinterpret_cast<const float2*>(a.dx + oidx[nb] + v * cstr + ph * W2);
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+#pragma unroll
+                for (int ph = 0; ph < 2; ++ph) {
+                    val[nb][v][ph].x += old[nb][v][ph].x;
+                    val[nb][v][ph].y += old[nb][v][ph].y;
+                }
+    }
+    float gs1[4] = {0.f, 0.f, 0.f, 0.f}, gs2[4] = {0.f, 0.f, 0.f, 0.f};
+    if (a.bnb.part) {
+        float2 zz[NBW][4][2], yy[NBW][4][2];
+        float mu[4], is[4];
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+#pragma unroll
+                for (int ph = 0; ph < 2; ++ph) {
+                    zz[nb][v][ph] = *reinterpret_cast<const float2*>(a.bnb.z + oidx[nb] + v * cstr + ph * W2);
+                    yy[nb][v][ph] = *reinterpret_cast<const float2*>(a.bnb.y + oidx[nb] + v * cstr + ph * W2);
+                }
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            const int m = mblk + wk * 16 + 4 * g + v;
-#pragma unroll
-            for (int ph = 0; ph < 2; ++ph) {
-                const size_t idx = (((size_t)img * a.CL + m) * H2 + 2 * ii + ph) * W2 + 2 * jj;
-                float2* dst = reinterpret_cast<float2*>(a.dx + idx);
-                float2 val = make_float2(acc[nb][2 * ph][v], acc[nb][2 * ph + 1][v]);
-                if (a.accumulate) {
-                    const float2 o = *dst;
-                    val.x += o.x;
-                    val.y += o.y;
-                }
-                *dst = val;
-                if (a.bnb.part) {
-                    const float2 zz = *reinterpret_cast<const float2*>(a.bnb.z + idx);
-                    const float2 yy = *reinterpret_cast<const float2*>(a.bnb.y + idx);
-                    const float g0 = (a.bnb.relu && !(zz.x > 0.f)) ? 0.f : val.x;
-                    const float g1 = (a.bnb.relu && !(zz.y > 0.f)) ? 0.f : val.y;
-                    const float mu = a.bnb.mean[m], is = a.bnb.invstd[m];
-                    gs1[v] += g0 + g1;
-                    gs2[v] += g0 * ((yy.x - mu) * is) + g1 * ((yy.y - mu) * is);
-                }
-            }
+            mu[v] = a.bnb.mean[mblk + wk * 16 + 4 * g + v];
+            is[v] = a.bnb.invstd[mblk + wk * 16 + 4 * g + v];
         }
+#pragma unroll
+        for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+            for (int v = 0; v < 4; ++v)
+#pragma unroll
+                for (int ph = 0; ph < 2; ++ph) {
+                    const float2 gv = val[nb][v][ph], zv = zz[nb][v][ph], yv = yy[nb][v][ph];
+                    const float g0 = (a.bnb.relu && !(zv.x > 0.f)) ? 0.f : gv.x;
+                    const float g1 = (a.bnb.relu && !(zv.y > 0.f)) ? 0.f : gv.y;
+                    gs1[v] += g0 + g1;
+                    gs2[v] += g0 * ((yv.x - mu[v]) * is[v]) + g1 * ((yv.y - mu[v]) * is[v]);
+                }
     }
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb)
+#pragma unroll
+        for (int v = 0; v < 4; ++v)
+#pragma unroll
+            for (int ph = 0; ph < 2; ++ph)
+                *reinterpret_cast<float2*>(a.dx + oidx[nb] + v * cstr + ph * W2) = val[nb][v][ph];
     if (a.bnb.part) {
         float* red = Xs;  // [2][WP][TK]
         __syncthreads();
@@ -513,10 +587,17 @@ hipError_t launch_direct(const DirArgs& a, int n, bool trans, hipStream_t st)
 {
     dim3 grid(n * (a.HO / TH), a.K / (16 * WK));
     dim3 block(64 * WK * WP);
+    // as a convolution: input a.C x a.H x WO*STRIDE, output a.K x a.HO x WO
+    Work wk = conv_work(n, a.C, a.H, WO * STRIDE, a.K, 3, 3, a.HO, WO);
+    const double out_bytes = kF * n * (double)a.K * a.HO * WO;
+    if (a.accumulate) wk.bytes += out_bytes;        // the existing output is read
+    if (a.bnb.part) wk.bytes += 2.0 * out_bytes;    // BN output and input for the backward sums
     if (trans)
-        hipLaunchKernelGGL((conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true>), grid, block, 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true), wk,
+                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true>), grid, block, 0, st, a);
     else
-        hipLaunchKernelGGL((conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, false>), grid, block, 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, false), wk,
+                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, false>), grid, block, 0, st, a);
     return hipGetLastError();
 }
 
@@ -575,12 +656,19 @@ hipError_t conv3x3_dgrad_s2(int n, int CL, int H, int W, int KL, const float* w,
     const int HO = H / 2, WO = W / 2;
     DgArgs a{dy, w, dx, KL, CL, HO, accumulate, BnBwdFuse{}};
     if (bnb) a.bnb = *bnb;
+    // the layer: CL x H x W -> KL x HO x WO, stride 2
+    Work wk = conv_work(n, CL, H, W, KL, 3, 3, HO, WO);
+    const double dx_bytes = kF * n * (double)CL * H * W;
+    if (accumulate) wk.bytes += dx_bytes;
+    if (bnb) wk.bytes += 2.0 * dx_bytes;
     if (WO == 16 && HO % 4 == 0 && CL % 16 == 0) {
-        hipLaunchKernelGGL((conv3x3_dgrad_s2<16, 4, 16, 1, 4, 1>), dim3(n * (HO / 4), CL / 16), dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_dgrad_s2", 16, 4, 16, 1, 4, 1), wk, (conv3x3_dgrad_s2<16, 4, 16, 1, 4, 1>),
+                   dim3(n * (HO / 4), CL / 16), dim3(256), 0, st, a);
         return hipGetLastError();
     }
     if (WO == 8 && HO % 8 == 0 && CL % 16 == 0) {
-        hipLaunchKernelGGL((conv3x3_dgrad_s2<8, 8, 16, 1, 4, 1>), dim3(n * (HO / 8), CL / 16), dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_dgrad_s2", 8, 8, 16, 1, 4, 1), wk, (conv3x3_dgrad_s2<8, 8, 16, 1, 4, 1>),
+                   dim3(n * (HO / 8), CL / 16), dim3(256), 0, st, a);
         return hipGetLastError();
     }
     return hipErrorNotSupported;

@@ -1,11 +1,73 @@
 // Internal launchers of libpsw (not part of the public C ABI).
 // All tensors are NCHW float32 in device memory; conv weights are KCRS.
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stddef.h>
 #include <stdint.h>
 
+#include <string>
+
 namespace psw {
+
+// ---- kernel timing hook -------------------------------------------------
+// While a recorder is installed on the calling thread (the scheduler does so
+// in its profiling mode), every kernel the library launches is launched with
+// hipExtLaunchKernelGGL and a start / stop event pair, which the runtime
+// stamps from the kernel's own dispatch (no extra packets in the stream), and
+// is reported with its name (template arguments spelled as the compiler
+// prints them) and its algorithmic work: the floating-point operations and
+// the minimal HBM bytes (each input read once, each output written once) of
+// what the kernel computes.
+struct Work {
+    double flops;
+    double bytes;
+};
+
+class KernelRecorder {
+public:
+    // false: do not time this launch; else *start / *stop are the events
+    virtual bool begin(const std::string& name, hipEvent_t* start, hipEvent_t* stop) = 0;
+    virtual void end(std::string&& name, const Work& w, hipEvent_t start, hipEvent_t stop) = 0;
+
+protected:
+    ~KernelRecorder() = default;
+};
+
+KernelRecorder*& kernel_recorder();  // this thread's recorder, nullptr when off
+
+inline void kname_arg(std::string& s, int v) { s += std::to_string(v); }
+inline void kname_arg(std::string& s, bool v) { s += v ? "true" : "false"; }
+template <typename... T>
+std::string kname(const char* base, T... v)
+{
+    std::string s = base;
+    if constexpr (sizeof...(v) > 0) {
+        s += '<';
+        bool first = true;
+        ((s += first ? "" : ", ", first = false, kname_arg(s, v)), ...);
+        s += '>';
+    }
+    return s;
+}
+
+#define PSW_LAUNCH(NAME, WORK, KERNEL, GRID, BLOCK, SHMEM, STREAM, ...)                              \
+    do {                                                                                          \
+        ::psw::KernelRecorder* psw_rec_ = ::psw::kernel_recorder();                               \
+        hipEvent_t psw_e0_ = nullptr, psw_e1_ = nullptr;                                          \
+        std::string psw_name_;                                                                    \
+        if (psw_rec_) {                                                                           \
+            psw_name_ = NAME;                                                                     \
+            if (!psw_rec_->begin(psw_name_, &psw_e0_, &psw_e1_)) psw_rec_ = nullptr;              \
+        }                                                                                         \
+        if (psw_rec_)                                                                             \
+            hipExtLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, psw_e0_, psw_e1_, 0, __VA_ARGS__); \
+        else                                                                                      \
+            hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, __VA_ARGS__);                  \
+        if (psw_rec_) psw_rec_->end(std::move(psw_name_), WORK, psw_e0_, psw_e1_);                \
+    } while (0)
+
+constexpr double kF = 4.0;  // bytes per float
 
 struct ConvShape {
     int n, c, h, w;        // input
@@ -15,6 +77,14 @@ struct ConvShape {
 };
 
 inline int conv_out_dim(int in, int k, int stride, int pad) { return (in + 2 * pad - k) / stride + 1; }
+
+// algorithmic work of one pass of a convolution (the three passes have the
+// same multiply-add count); bytes: x, w and y once each
+inline Work conv_work(int n, int c, int h, int w, int k, int r, int s, int p, int q)
+{
+    return Work{2.0 * n * p * q * (double)k * c * r * s, kF * ((double)n * c * h * w + (double)k * c * r * s + (double)n * k * p * q)};
+}
+inline Work conv_work(const ConvShape& cs) { return conv_work(cs.n, cs.c, cs.h, cs.w, cs.k, cs.r, cs.s, cs.p, cs.q); }
 
 // Batch-norm statistics fused into a convolution's epilogue: every workgroup
 // writes the (mean, M2) of each of its output channels over its P pixels to

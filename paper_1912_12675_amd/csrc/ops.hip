@@ -5,6 +5,8 @@
 // deterministic: every partial sum has a fixed owner and partials are
 // combined in a fixed order; BN sums are accumulated in double so the
 // E[y^2]-E[y]^2 form loses nothing at these sizes.
+#include <algorithm>
+
 #include "internal.h"
 
 namespace psw {
@@ -472,14 +474,18 @@ hipError_t gemm(GemmArgs a, int bf16, void* ws, size_t ws_bytes, hipStream_t st)
         a.C = (float*)ws;
     }
     dim3 grid((a.N + BN - 1) / BN, (a.M + BM - 1) / BM, splits);
+    const Work gw{2.0 * a.M * a.N * (double)a.K, kF * ((double)a.M * a.K + (double)a.K * a.N + (double)a.M * a.N)};
     if (bf16)
-        hipLaunchKernelGGL((gemm_kernel<BM, BN, 2, 2, true, AK, BKC>), grid, dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("gemm_kernel", BM, BN, 2, 2, true, AK, BKC), gw, (gemm_kernel<BM, BN, 2, 2, true, AK, BKC>),
+                   grid, dim3(256), 0, st, a);
     else
-        hipLaunchKernelGGL((gemm_kernel<BM, BN, 2, 2, false, AK, BKC>), grid, dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("gemm_kernel", BM, BN, 2, 2, false, AK, BKC), gw, (gemm_kernel<BM, BN, 2, 2, false, AK, BKC>),
+                   grid, dim3(256), 0, st, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || splits == 1) return e;
     const int64_t count = (int64_t)a.M * a.N;
-    hipLaunchKernelGGL(gemm_reduce, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, st, (const float*)ws, splits,
+    PSW_LAUNCH(kname("gemm_reduce"), (Work{(double)splits * count, kF * (splits + 1.0 + accum) * count}), gemm_reduce,
+               dim3((unsigned)((count + 255) / 256)), dim3(256), 0, st, (const float*)ws, splits,
                        a.M, a.N, bias, relu, accum, out);
     return hipGetLastError();
 }
@@ -499,9 +505,12 @@ hipError_t channel_sum(int n, int c, int hw, const float* x, float* out, void* w
 {
     const int sp = channel_splits(n, c);
     if (ws_bytes < channel_sum_ws_bytes(n, c, hw)) return hipErrorInvalidValue;
-    hipLaunchKernelGGL(chan_partials, dim3(c, sp), dim3(kBlock), 0, st, 2, n, c, hw, sp, x, (const float*)nullptr,
-                       (const float*)nullptr, (const float*)nullptr, (const float*)nullptr, 0, (double*)ws);
-    hipLaunchKernelGGL(chan_sum_finalize, dim3(blocks_for(c)), dim3(kBlock), 0, st, c, sp, (const double*)ws, out);
+    const double elems = (double)n * c * hw;
+    PSW_LAUNCH(kname("chan_partials"), (Work{elems, kF * elems}), chan_partials, dim3(c, sp), dim3(kBlock), 0, st, 2,
+               n, c, hw, sp, x, (const float*)nullptr, (const float*)nullptr, (const float*)nullptr,
+               (const float*)nullptr, 0, (double*)ws);
+    PSW_LAUNCH(kname("chan_sum_finalize"), (Work{(double)c * sp, 16.0 * c * sp + kF * c}), chan_sum_finalize,
+               dim3(blocks_for(c)), dim3(kBlock), 0, st, c, sp, (const double*)ws, out);
     return hipGetLastError();
 }
 
@@ -520,13 +529,17 @@ hipError_t bn_fwd(int n, int c, int h, int w, const float* y, const float* gamma
     const int hw = h * w;
     double* part = (double*)ws;
     float* coef = (float*)((char*)ws + (size_t)c * sp * 2 * sizeof(double));
-    hipLaunchKernelGGL(chan_partials, dim3(c, sp), dim3(kBlock), 0, st, 0, n, c, hw, sp, y, (const float*)nullptr,
-                       (const float*)nullptr, (const float*)nullptr, (const float*)nullptr, 0, part);
-    hipLaunchKernelGGL(bn_fwd_finalize, dim3(blocks_for(c)), dim3(kBlock), 0, st, c, sp, (double)n * hw,
-                       (const double*)part, gamma, beta, eps, momentum, save_mean, save_invstd, run_mean, run_var, coef);
     const int64_t total = (int64_t)n * c * hw;
-    hipLaunchKernelGGL(bn_fwd_apply, dim3(blocks_for(total)), dim3(kBlock), 0, st, total, c, hw, y,
-                       (const float*)coef, res, rc, rh, rw, h, w, relu, z);
+    PSW_LAUNCH(kname("chan_partials"), (Work{3.0 * total, kF * total}), chan_partials, dim3(c, sp), dim3(kBlock), 0, st,
+               0, n, c, hw, sp, y, (const float*)nullptr, (const float*)nullptr, (const float*)nullptr,
+               (const float*)nullptr, 0, part);
+    PSW_LAUNCH(kname("bn_fwd_finalize"), (Work{2.0 * c * sp, 16.0 * c * sp + 6 * kF * c}), bn_fwd_finalize,
+               dim3(blocks_for(c)), dim3(kBlock), 0, st, c, sp, (double)n * hw, (const double*)part, gamma, beta, eps,
+               momentum, save_mean, save_invstd, run_mean, run_var, coef);
+    const double rbytes = res ? kF * (double)n * std::min(c, rc) * hw : 0.0;
+    PSW_LAUNCH(kname("bn_fwd_apply"), (Work{3.0 * total, kF * 2.0 * total + rbytes}), bn_fwd_apply,
+               dim3(blocks_for(total)), dim3(kBlock), 0, st, total, c, hw, y, (const float*)coef, res, rc, rh, rw, h, w,
+               relu, z);
     return hipGetLastError();
 }
 
@@ -540,18 +553,22 @@ hipError_t bn_bwd(int n, int c, int h, int w, const float* dz, const float* z, c
     const int hw = h * w;
     double* part = (double*)ws;
     float* coef = (float*)((char*)ws + (size_t)c * sp * 2 * sizeof(double));
-    hipLaunchKernelGGL(chan_partials, dim3(c, sp), dim3(kBlock), 0, st, 1, n, c, hw, sp, dz, z, y, save_mean,
-                       save_invstd, relu, part);
-    hipLaunchKernelGGL(bn_bwd_finalize, dim3(blocks_for(c)), dim3(kBlock), 0, st, c, sp, (double)n * hw,
-                       (const double*)part, gamma, save_invstd, dgamma, dbeta, coef);
     const int64_t total = (int64_t)n * c * hw;
+    PSW_LAUNCH(kname("chan_partials"), (Work{5.0 * total, 3 * kF * total}), chan_partials, dim3(c, sp), dim3(kBlock), 0,
+               st, 1, n, c, hw, sp, dz, z, y, save_mean, save_invstd, relu, part);
+    PSW_LAUNCH(kname("bn_bwd_finalize"), (Work{2.0 * c * sp, 16.0 * c * sp + 7 * kF * c}), bn_bwd_finalize,
+               dim3(blocks_for(c)), dim3(kBlock), 0, st, c, sp, (double)n * hw, (const double*)part, gamma, save_invstd,
+               dgamma, dbeta, coef);
     const bool identity = dres && rc == c && rh == h && rw == w;
-    hipLaunchKernelGGL(bn_bwd_apply, dim3(blocks_for(total)), dim3(kBlock), 0, st, total, c, hw, dz, z, y, save_mean,
-                       save_invstd, (const float*)coef, relu, dy, identity ? dres : (float*)nullptr, res_accumulate);
+    PSW_LAUNCH(kname("bn_bwd_apply"),
+               (Work{6.0 * total, kF * (4.0 + (identity ? 1.0 + res_accumulate : 0.0)) * total}), bn_bwd_apply,
+               dim3(blocks_for(total)), dim3(kBlock), 0, st, total, c, hw, dz, z, y, save_mean, save_invstd,
+               (const float*)coef, relu, dy, identity ? dres : (float*)nullptr, res_accumulate);
     if (dres && !identity) {
         const int64_t rtotal = (int64_t)n * rc * rh * rw;
-        hipLaunchKernelGGL(shortcut_a_bwd, dim3(blocks_for(rtotal)), dim3(kBlock), 0, st, rtotal, c, h, w, rc, rh, rw,
-                           dz, z, relu, dres, res_accumulate);
+        PSW_LAUNCH(kname("shortcut_a_bwd"), (Work{0.0, kF * ((1.0 + res_accumulate) * rtotal + 2.0 * n * rc * hw)}),
+                   shortcut_a_bwd, dim3(blocks_for(rtotal)), dim3(kBlock), 0, st, rtotal, c, h, w, rc, rh, rw, dz, z,
+                   relu, dres, res_accumulate);
     }
     return hipGetLastError();
 }
@@ -562,10 +579,14 @@ namespace {
 // channel see bit-identical coefficients), then transforms its share of the
 // channel's n*hw elements.  Element loops walk float4 units of one channel
 // (unit u: image u / hw4, offset 4*(u % hw4)) with 32-bit index arithmetic.
-constexpr int kApplyUnits = 1024;  // float4 units per block
+constexpr int kApplyUnits = 1024;  // float4 units per block (a multiple of kBlock)
 
 // forward: tile partials (mean_t, M2_t over P pixels each)
 //   mean = (1/T) sum mean_t,  M2 = sum M2_t + P sum (mean_t - mean)^2
+// The element loads are issued before the partial merge so that the two
+// memory latencies overlap, and every load precedes every store.
+constexpr int kUnitsPerThread = kApplyUnits / kBlock;
+
 __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int hw, const float* y, const float* part,
                                                                int T, int P, const float* gamma, const float* beta,
                                                                const float* res, int rc, int rh, int rw, int h, int w,
@@ -577,6 +598,35 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
     __shared__ float coef[2];
     __shared__ double mean_sh;
     const int ch = blockIdx.x;
+    const int hw4 = hw >> 2;
+    const int units = n * hw4;
+    const int u0 = blockIdx.y * kApplyUnits;
+    const int u1 = min(u0 + kApplyUnits, units);
+    const bool identity = res && rc == c && rh == h && rw == w;
+    const int lo = (c - rc) / 2, cc = ch - lo;
+    const bool shortcut_a = res && !identity && cc >= 0 && cc < rc;
+    constexpr int U = kUnitsPerThread;
+    size_t idx[U];
+    float4 yv[U], rv[U];
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+        const int u = u0 + threadIdx.x + q * kBlock;
+        yv[q] = rv[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+        idx[q] = 0;
+        if (u < u1) {
+            const int img = u / hw4, off = (u - img * hw4) * 4;
+            idx[q] = ((size_t)img * c + ch) * hw + off;
+            yv[q] = *reinterpret_cast<const float4*>(y + idx[q]);
+            if (identity) {
+                rv[q] = *reinterpret_cast<const float4*>(res + idx[q]);
+            } else if (shortcut_a) {  // option-A shortcut: subsampled, channel-padded residual
+                const int hh = off / w, ww = off - hh * w;  // w % 4 == 0: the four elements share a row
+                const int sw = rw / w;
+                const float* rp = res + (((size_t)img * rc + cc) * rh + hh * (rh / h)) * rw + ww * sw;
+                rv[q] = make_float4(rp[0], rp[sw], rp[2 * sw], rp[3 * sw]);
+            }
+        }
+    }
     const float* pp = part + (size_t)ch * T * 2;
     double s1 = 0.0;
     for (int t = threadIdx.x; t < T; t += kBlock) s1 += (double)pp[2 * t];
@@ -608,32 +658,18 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
     }
     __syncthreads();
     const float sc = coef[0], sf = coef[1];
-    const int hw4 = hw >> 2;
-    const int units = n * hw4;
-    const int u0 = blockIdx.y * kApplyUnits;
-    const int u1 = min(u0 + kApplyUnits, units);
-    const bool identity = res && rc == c && rh == h && rw == w;
-    const int lo = (c - rc) / 2, cc = ch - lo;
-    for (int u = u0 + threadIdx.x; u < u1; u += kBlock) {
-        const int img = u / hw4, off = (u - img * hw4) * 4;
-        const size_t i = ((size_t)img * c + ch) * hw + off;
-        const float4 yv = *reinterpret_cast<const float4*>(y + i);
-        float v[4] = {yv.x * sc + sf, yv.y * sc + sf, yv.z * sc + sf, yv.w * sc + sf};
-        if (identity) {
-            const float4 r = *reinterpret_cast<const float4*>(res + i);
-            v[0] += r.x; v[1] += r.y; v[2] += r.z; v[3] += r.w;
-        } else if (res && cc >= 0 && cc < rc) {  // option-A shortcut: subsampled, channel-padded residual
-            const int hh = off / w, ww = off - hh * w;  // w % 4 == 0: the four elements share a row
-            const float* rp = res + (((size_t)img * rc + cc) * rh + hh * (rh / h)) * rw + ww * (rw / w);
-            const int sw = rw / w;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) v[q] += rp[q * sw];
+    for (int q = 0; q < U; ++q) {
+        if (u0 + (int)threadIdx.x + q * kBlock >= u1) continue;
+        float v[4] = {yv[q].x * sc + sf, yv[q].y * sc + sf, yv[q].z * sc + sf, yv[q].w * sc + sf};
+        if (res) {
+            v[0] += rv[q].x; v[1] += rv[q].y; v[2] += rv[q].z; v[3] += rv[q].w;
         }
         if (relu) {
 #pragma unroll
-            for (int q = 0; q < 4; ++q) v[q] = fmaxf(v[q], 0.f);
+            for (int e = 0; e < 4; ++e) v[e] = fmaxf(v[e], 0.f);
         }
-        *reinterpret_cast<float4*>(z + i) = make_float4(v[0], v[1], v[2], v[3]);
+        *reinterpret_cast<float4*>(z + idx[q]) = make_float4(v[0], v[1], v[2], v[3]);
     }
 }
 
@@ -649,6 +685,27 @@ __global__ __launch_bounds__(kBlock) void bn_bwd_partials_k(int n, int c, int hw
     __shared__ double sh[kBlock / 64];
     __shared__ float coef[3];
     const int ch = blockIdx.x;
+    const int hw4 = hw >> 2;
+    const int units = n * hw4;
+    const int u0 = blockIdx.y * kApplyUnits;
+    const int u1 = min(u0 + kApplyUnits, units);
+    constexpr int U = kUnitsPerThread;
+    size_t idx[U];
+    float4 gv[U], zv[U], yv[U], ov[U];
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+        const int u = u0 + threadIdx.x + q * kBlock;
+        gv[q] = zv[q] = yv[q] = ov[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+        idx[q] = 0;
+        if (u < u1) {
+            const int img = u / hw4, off = (u - img * hw4) * 4;
+            idx[q] = ((size_t)img * c + ch) * hw + off;
+            gv[q] = *reinterpret_cast<const float4*>(dz + idx[q]);
+            zv[q] = *reinterpret_cast<const float4*>(z + idx[q]);
+            yv[q] = *reinterpret_cast<const float4*>(y + idx[q]);
+            if (dres && res_accumulate) ov[q] = *reinterpret_cast<const float4*>(dres + idx[q]);
+        }
+    }
     const float* pp = part + (size_t)ch * T * 2;
     double s1 = 0.0, s2 = 0.0;
     for (int t = threadIdx.x; t < T; t += kBlock) {
@@ -670,35 +727,23 @@ __global__ __launch_bounds__(kBlock) void bn_bwd_partials_k(int n, int c, int hw
     }
     __syncthreads();
     const float a = coef[0], b = coef[1], d = coef[2];
-    const int hw4 = hw >> 2;
-    const int units = n * hw4;
-    const int u0 = blockIdx.y * kApplyUnits;
-    const int u1 = min(u0 + kApplyUnits, units);
-    for (int u = u0 + threadIdx.x; u < u1; u += kBlock) {
-        const int img = u / hw4, off = (u - img * hw4) * 4;
-        const size_t i = ((size_t)img * c + ch) * hw + off;
-        const float4 gv = *reinterpret_cast<const float4*>(dz + i);
-        const float4 zv = *reinterpret_cast<const float4*>(z + i);
-        const float4 yv = *reinterpret_cast<const float4*>(y + i);
-        float g[4] = {gv.x, gv.y, gv.z, gv.w};
-        const float zz[4] = {zv.x, zv.y, zv.z, zv.w};
-        const float yy[4] = {yv.x, yv.y, yv.z, yv.w};
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+        if (u0 + (int)threadIdx.x + q * kBlock >= u1) continue;
+        float g[4] = {gv[q].x, gv[q].y, gv[q].z, gv[q].w};
+        const float zz[4] = {zv[q].x, zv[q].y, zv[q].z, zv[q].w};
+        const float yy[4] = {yv[q].x, yv[q].y, yv[q].z, yv[q].w};
         float o[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            if (relu && !(zz[q] > 0.f)) g[q] = 0.f;
-            const float xh = (yy[q] - mu) * is;
-            o[q] = a * (g[q] - b - xh * d);
+        for (int e = 0; e < 4; ++e) {
+            if (relu && !(zz[e] > 0.f)) g[e] = 0.f;
+            const float xh = (yy[e] - mu) * is;
+            o[e] = a * (g[e] - b - xh * d);
         }
-        *reinterpret_cast<float4*>(dy + i) = make_float4(o[0], o[1], o[2], o[3]);
-        if (dres) {
-            float4 r = make_float4(g[0], g[1], g[2], g[3]);
-            if (res_accumulate) {
-                const float4 old = *reinterpret_cast<const float4*>(dres + i);
-                r.x += old.x; r.y += old.y; r.z += old.z; r.w += old.w;
-            }
-            *reinterpret_cast<float4*>(dres + i) = r;
-        }
+        *reinterpret_cast<float4*>(dy + idx[q]) = make_float4(o[0], o[1], o[2], o[3]);
+        if (dres)
+            *reinterpret_cast<float4*>(dres + idx[q]) =
+                make_float4(g[0] + ov[q].x, g[1] + ov[q].y, g[2] + ov[q].z, g[3] + ov[q].w);
     }
 }
 
@@ -715,8 +760,11 @@ hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, co
     const int64_t units = (int64_t)n * h * w / 4;
     if (units > INT32_MAX) return hipErrorNotSupported;
     const unsigned per_ch = (unsigned)((units + kApplyUnits - 1) / kApplyUnits);
-    hipLaunchKernelGGL(bn_apply_partials_k, dim3(c, per_ch), dim3(kBlock), 0, st, n, c, h * w, y, part, T, P, gamma,
-                       beta, res, rc, rh, rw, h, w, relu, eps, momentum, z, save_mean, save_invstd, run_mean, run_var);
+    const double total = (double)n * c * h * w;
+    const double rbytes = res ? kF * (double)n * std::min(c, rc) * h * w : 0.0;
+    PSW_LAUNCH(kname("bn_apply_partials_k"), (Work{3.0 * total, 2 * kF * total + rbytes + 2 * kF * T * c}),
+               bn_apply_partials_k, dim3(c, per_ch), dim3(kBlock), 0, st, n, c, h * w, y, part, T, P, gamma, beta, res,
+               rc, rh, rw, h, w, relu, eps, momentum, z, save_mean, save_invstd, run_mean, run_var);
     return hipGetLastError();
 }
 
@@ -731,8 +779,11 @@ hipError_t bn_bwd_from_partials(int n, int c, int h, int w, const float* dz, con
     const int64_t units = (int64_t)n * h * w / 4;
     if (units > INT32_MAX) return hipErrorNotSupported;
     const unsigned per_ch = (unsigned)((units + kApplyUnits - 1) / kApplyUnits);
-    hipLaunchKernelGGL(bn_bwd_partials_k, dim3(c, per_ch), dim3(kBlock), 0, st, n, c, h * w, dz, z, y, gamma, mean,
-                       invstd, part, T, relu, dy, dgamma, dbeta, dres_identity, res_accumulate);
+    const double total = (double)n * c * h * w;
+    const double dres_rw = dres_identity ? 1.0 + res_accumulate : 0.0;
+    PSW_LAUNCH(kname("bn_bwd_partials_k"), (Work{6.0 * total, kF * (4.0 + dres_rw) * total + 2 * kF * T * c}),
+               bn_bwd_partials_k, dim3(c, per_ch), dim3(kBlock), 0, st, n, c, h * w, dz, z, y, gamma, mean, invstd,
+               part, T, relu, dy, dgamma, dbeta, dres_identity, res_accumulate);
     return hipGetLastError();
 }
 
@@ -742,8 +793,9 @@ hipError_t shortcut_a_backward(int n, int c, int h, int w, int rc, int rh, int r
                                int relu, float* dres, int accumulate, hipStream_t st)
 {
     const int64_t rtotal = (int64_t)n * rc * rh * rw;
-    hipLaunchKernelGGL(shortcut_a_bwd, dim3(blocks_for(rtotal)), dim3(kBlock), 0, st, rtotal, c, h, w, rc, rh, rw, dz,
-                       z, relu, dres, accumulate);
+    PSW_LAUNCH(kname("shortcut_a_bwd"), (Work{0.0, kF * ((1.0 + accumulate) * rtotal + 2.0 * n * rc * h * w)}),
+               shortcut_a_bwd, dim3(blocks_for(rtotal)), dim3(kBlock), 0, st, rtotal, c, h, w, rc, rh, rw, dz, z, relu,
+               dres, accumulate);
     return hipGetLastError();
 }
 
@@ -752,8 +804,8 @@ hipError_t maxpool_fwd(int n, int c, int h, int w, int k, int stride, const floa
 {
     const int p = (h - k) / stride + 1, q = (w - k) / stride + 1;
     const int64_t total = (int64_t)n * c * p * q;
-    hipLaunchKernelGGL(maxpool_fwd_k, dim3(blocks_for(total)), dim3(kBlock), 0, st, total, h, w, p, q, k, stride, x,
-                       y, argmax);
+    PSW_LAUNCH(kname("maxpool_fwd_k"), (Work{(double)total * k * k, kF * ((double)n * c * h * w + 2.0 * total)}),
+               maxpool_fwd_k, dim3(blocks_for(total)), dim3(kBlock), 0, st, total, h, w, p, q, k, stride, x, y, argmax);
     return hipGetLastError();
 }
 
@@ -762,35 +814,40 @@ hipError_t maxpool_bwd(int n, int c, int h, int w, int k, int stride, const floa
 {
     const int p = (h - k) / stride + 1, q = (w - k) / stride + 1;
     const int64_t total = (int64_t)n * c * h * w;
-    hipLaunchKernelGGL(maxpool_bwd_k, dim3(blocks_for(total)), dim3(kBlock), 0, st, total, h, w, p, q, k, dy, argmax,
-                       dx, accumulate);
+    PSW_LAUNCH(kname("maxpool_bwd_k"), (Work{0.0, kF * (2.0 * n * c * p * q + (1.0 + accumulate) * total)}),
+               maxpool_bwd_k, dim3(blocks_for(total)), dim3(kBlock), 0, st, total, h, w, p, q, k, dy, argmax, dx,
+               accumulate);
     return hipGetLastError();
 }
 
 hipError_t gavgpool_fwd(int n, int c, int h, int w, const float* x, float* y, hipStream_t st)
 {
     const int64_t planes = (int64_t)n * c;
-    hipLaunchKernelGGL(gavg_fwd_k, dim3(blocks_for(planes, 4)), dim3(kBlock), 0, st, planes, h * w, x, y);
+    PSW_LAUNCH(kname("gavg_fwd_k"), (Work{(double)planes * h * w, kF * planes * (h * w + 1.0)}), gavg_fwd_k,
+               dim3(blocks_for(planes, 4)), dim3(kBlock), 0, st, planes, h * w, x, y);
     return hipGetLastError();
 }
 
 hipError_t gavgpool_bwd(int n, int c, int h, int w, const float* dy, float* dx, int accumulate, hipStream_t st)
 {
     const int64_t total = (int64_t)n * c * h * w;
-    hipLaunchKernelGGL(gavg_bwd_k, dim3(blocks_for(total)), dim3(kBlock), 0, st, total, h * w, dy, dx, accumulate);
+    PSW_LAUNCH(kname("gavg_bwd_k"), (Work{(double)total, kF * ((double)n * c + (1.0 + accumulate) * total)}),
+               gavg_bwd_k, dim3(blocks_for(total)), dim3(kBlock), 0, st, total, h * w, dy, dx, accumulate);
     return hipGetLastError();
 }
 
 hipError_t relu_mask(int64_t count, const float* z, float* g, hipStream_t st)
 {
-    hipLaunchKernelGGL(relu_mask_k, dim3(blocks_for(count)), dim3(kBlock), 0, st, count, z, g);
+    PSW_LAUNCH(kname("relu_mask_k"), (Work{(double)count, 3 * kF * count}), relu_mask_k, dim3(blocks_for(count)),
+               dim3(kBlock), 0, st, count, z, g);
     return hipGetLastError();
 }
 
 hipError_t softmax_xent(int n, int classes, const float* logits, const int32_t* labels, float* loss, float* dlogits,
                         hipStream_t st)
 {
-    hipLaunchKernelGGL(softmax_xent_k, dim3(1), dim3(kBlock), 0, st, n, classes, logits, labels, loss, dlogits);
+    PSW_LAUNCH(kname("softmax_xent_k"), (Work{5.0 * n * classes, kF * (2.0 * n * classes + n + 1.0)}), softmax_xent_k,
+               dim3(1), dim3(kBlock), 0, st, n, classes, logits, labels, loss, dlogits);
     return hipGetLastError();
 }
 
@@ -798,8 +855,8 @@ hipError_t sgd_momentum(int64_t count, const float* w_in, float* w_out, float* v
                         float wd, int nesterov, hipStream_t st)
 {
     if (count <= 0) return hipSuccess;
-    hipLaunchKernelGGL(sgd_k, dim3(blocks_for(count)), dim3(kBlock), 0, st, count, w_in, w_out, v, g, lr, mom, wd,
-                       nesterov);
+    PSW_LAUNCH(kname("sgd_k"), (Work{5.0 * count, 5 * kF * count}), sgd_k, dim3(blocks_for(count)), dim3(kBlock), 0, st,
+               count, w_in, w_out, v, g, lr, mom, wd, nesterov);
     return hipGetLastError();
 }
 
@@ -853,10 +910,11 @@ hipError_t fc_bwd(int n, int in, int out, const float* x, const float* w, const 
     if (db) {
         // db[o] = sum_n dy[n][o]: the column sums of dy viewed as [n][out][1]
         // (not a product, so never rounded to bf16)
-        hipLaunchKernelGGL(chan_partials, dim3(out, 1), dim3(kBlock), 0, st, 2, n, out, 1, 1, dy,
-                           (const float*)nullptr, (const float*)nullptr, (const float*)nullptr, (const float*)nullptr,
-                           0, (double*)ws);
-        hipLaunchKernelGGL(chan_sum_finalize, dim3(blocks_for(out)), dim3(kBlock), 0, st, out, 1, (const double*)ws, db);
+        PSW_LAUNCH(kname("chan_partials"), (Work{(double)n * out, kF * n * out}), chan_partials, dim3(out, 1),
+                   dim3(kBlock), 0, st, 2, n, out, 1, 1, dy, (const float*)nullptr, (const float*)nullptr,
+                   (const float*)nullptr, (const float*)nullptr, 0, (double*)ws);
+        PSW_LAUNCH(kname("chan_sum_finalize"), (Work{(double)out, 16.0 * out + kF * out}), chan_sum_finalize,
+                   dim3(blocks_for(out)), dim3(kBlock), 0, st, out, 1, (const double*)ws, db);
         e = hipGetLastError();
     }
     return e;

@@ -194,22 +194,23 @@ hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const fl
     const int splits = conv3x3_wgrad_splits(n, C, H, W, K, stride);
     const int cgroups = (C + 15) / 16;  // one 16-channel block per workgroup (grid.y)
     const dim3 grid(splits, cgroups);
+    const Work wk = conv_work(n, C, H, W, K, 3, 3, H / stride, W / stride);
     switch (cfg) {
     case 6:
     case 1:
-        hipLaunchKernelGGL((conv3x3_wgrad<1, 32, 16, 1, 1, 4, 1>), grid, dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 32, 16, 1, 1, 4, 1), wk, (conv3x3_wgrad<1, 32, 16, 1, 1, 4, 1>), grid, dim3(256), 0, st, a);
         break;
     case 2:
-        hipLaunchKernelGGL((conv3x3_wgrad<1, 16, 16, 2, 1, 2, 1>), grid, dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 16, 16, 2, 1, 2, 1), wk, (conv3x3_wgrad<1, 16, 16, 2, 1, 2, 1>), grid, dim3(256), 0, st, a);
         break;
     case 3:
-        hipLaunchKernelGGL((conv3x3_wgrad<1, 8, 8, 4, 1, 1, 2>), grid, dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 8, 8, 4, 1, 1, 2), wk, (conv3x3_wgrad<1, 8, 8, 4, 1, 1, 2>), grid, dim3(256), 0, st, a);
         break;
     case 4:
-        hipLaunchKernelGGL((conv3x3_wgrad<2, 16, 8, 2, 1, 2, 1>), grid, dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_wgrad", 2, 16, 8, 2, 1, 2, 1), wk, (conv3x3_wgrad<2, 16, 8, 2, 1, 2, 1>), grid, dim3(256), 0, st, a);
         break;
     case 5:
-        hipLaunchKernelGGL((conv3x3_wgrad<2, 8, 8, 4, 1, 1, 1>), grid, dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_wgrad", 2, 8, 8, 4, 1, 1, 1), wk, (conv3x3_wgrad<2, 8, 8, 4, 1, 1, 1>), grid, dim3(256), 0, st, a);
         break;
     }
     return hipGetLastError();

@@ -44,6 +44,11 @@ class psw_launch(ctypes.Structure):
                 ("version", ctypes.c_int64)]
 
 
+class psw_kernel_stat(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 192), ("kind", ctypes.c_int32), ("launches", ctypes.c_int64),
+                ("ms", ctypes.c_double), ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
+
+
 # symbol -> (restype, argtypes); the full public surface of include/psw.h
 SIGNATURES = {
     "psw_last_error": (ctypes.c_char_p, []),
@@ -76,6 +81,8 @@ SIGNATURES = {
     "psw_net_plan": (_I, [_P, _I64, _P, ctypes.POINTER(psw_launch), _I, ctypes.POINTER(ctypes.c_int)]),
     "psw_net_profile": (_I, [_P, _I]),
     "psw_net_profile_read": (_I, [_P, _I, _P, _P]),
+    "psw_net_profile_kernels": (_I, [_P, _I, _P, _P]),
+    "psw_net_profile_only": (_I, [_P, _I, ctypes.c_char_p]),
 }
 
 PROF_KINDS = ["conv_fwd", "conv_bwd_data", "conv_bwd_weight", "bn_fwd", "bn_bwd", "pool", "fc", "loss", "sgd",
@@ -325,16 +332,29 @@ class Net:
                                     _ptr(x), _ptr(labels), _ptr(self.loss), ver.ctypes.data, _stream(stream)))
         return ver
 
-    def profile(self, enable=True):
-        """Enable / disable HIP-event timing of every launcher in step()."""
-        _check(lib().psw_net_profile(self.handle, int(enable)))
+    def profile(self, enable=True, only=None):
+        """Enable / disable HIP-event timing of the kernels launched by step() (all of them, or only the
+        kernel named `only`); clears the records."""
+        if only:
+            _check(lib().psw_net_profile_only(self.handle, int(enable), only.encode()))
+        else:
+            _check(lib().psw_net_profile(self.handle, int(enable)))
 
     def profile_read(self):
-        """{kind: (milliseconds, launches)} summed since the last read."""
+        """{kind: (milliseconds, kernel launches)} summed over the records."""
         ms = np.zeros(len(PROF_KINDS), dtype=np.float64)
         cnt = np.zeros(len(PROF_KINDS), dtype=np.int64)
         _check(lib().psw_net_profile_read(self.handle, len(PROF_KINDS), ms.ctypes.data, cnt.ctypes.data))
         return {k: (float(ms[i]), int(cnt[i])) for i, k in enumerate(PROF_KINDS)}
+
+    def profile_kernels(self, cap=256):
+        """[{name, kind, launches, ms, flops, bytes}] per distinct kernel, in decreasing total time."""
+        buf = (psw_kernel_stat * cap)()
+        n = ctypes.c_int()
+        _check(lib().psw_net_profile_kernels(self.handle, cap, buf, ctypes.byref(n)))
+        return [dict(name=buf[i].name.decode(), kind=PROF_KINDS[buf[i].kind] if 0 <= buf[i].kind < len(PROF_KINDS)
+                     else "other", launches=int(buf[i].launches), ms=float(buf[i].ms), flops=float(buf[i].flops),
+                     bytes=float(buf[i].bytes)) for i in range(min(n.value, cap))]
 
     def plan(self, t, staleness, cap=4096):
         st = np.ascontiguousarray(staleness, dtype=np.int32)
