@@ -230,8 +230,18 @@ __global__ __launch_bounds__(256) void reduce_splits(const float* part, int spli
     const int o = threadIdx.x & 15, zl = threadIdx.x >> 4;
     const int64_t i = (int64_t)blockIdx.x * 16 + o;
     float acc = 0.f;
-    if (i < count)
-        for (int z = zl; z < splits; z += 16) acc += part[(int64_t)z * count + i];
+    if (i < count) {
+        // eight independent loads in flight per batch, added in increasing z
+        int z = zl;
+        for (; z + 7 * 16 < splits; z += 8 * 16) {
+            float v[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) v[u] = part[(int64_t)(z + u * 16) * count + i];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) acc += v[u];
+        }
+        for (; z < splits; z += 16) acc += part[(int64_t)z * count + i];
+    }
     sh[zl][o] = acc;
     __syncthreads();
     if (zl == 0 && i < count) {

@@ -5,21 +5,25 @@
 // delta^(l)).
 //
 // A workgroup reduces over TPW consecutive (image, TH-row band) tiles and
-// writes one
-// dW-shaped partial sum; the partials are added in a fixed order by the
-// reduction kernel of conv.hip, so the result is bit-reproducible.
+// writes one dW-shaped partial sum; the partials are added in a fixed order
+// by the reduction kernel of conv.hip, so the result is bit-reproducible.
 // blockIdx.y selects a group of CBW 16-channel input blocks.  In the
 // workgroup, wave (kb, cb, wpx) owns the 16x16 output blocks (output channels
 // kb*16.., input channels of block cb) of all 9 taps (9 MFMA accumulators)
 // and the pixel quads wpx, wpx+WPX, ...; waves that differ only in wpx are
 // summed through LDS in wpx order at the end.
 //
+// The bands are walked in chunks of RC output rows, software-pipelined: the
+// next chunk's dy rows and input rows (with their halo) are loaded into
+// registers while the matrix cores work on the current chunk in LDS.
+//
 // MFMA v_mfma_f32_16x16x4_f32 with k = 4 consecutive output pixels of one
 // row: A[m=k_out][k=pixel] from dy, B[k=pixel][n=c_in] from x shifted by the
 // tap.  Both tiles sit in LDS plane-major (one plane per channel, as in NCHW)
 // with a plane stride of 2 (mod 32) floats: an operand read by lanes
 // (channel j, pixel g) hits bank 2j + g (stride 1), all distinct within a
-// 32-lane half, and the staging writes are contiguous runs.
+// 32-lane half.  Input rows are stored with the data columns 16-byte aligned
+// (input column -1 at offset 3), so staging writes are 8-byte stores.
 #include "internal.h"
 
 namespace psw {
@@ -42,84 +46,129 @@ constexpr int plane_stride(int lo)
     return v;
 }
 
-template <int STRIDE, int WO, int TH, int KBW, int CBW, int WPX, int TPW>
+constexpr int round4(int v) { return (v + 3) / 4 * 4; }
+
+template <int STRIDE, int WO, int TH, int KBW, int CBW, int WPX, int TPW, int RC>
 __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
 {
     constexpr int NT = 64 * KBW * CBW * WPX;
     constexpr int WIN = WO * STRIDE;
-    constexpr int WS = WIN + (STRIDE == 1 ? 2 : 1);   // staged input columns: -1 .. WIN (-1 .. WIN-1 for stride 2)
-    constexpr int HRR = (TH - 1) * STRIDE + 3;        // staged input rows
+    constexpr int XRS = round4(WIN + (STRIDE == 1 ? 5 : 4));  // input row: cols -1 .. WIN(-1) at offsets 3 ..
+    constexpr int HRC = (RC - 1) * STRIDE + 3;                // staged input rows per chunk
     constexpr int KC = 16 * KBW, CCH = 16 * CBW;
-    constexpr int NPIX = TH * WO;
-    constexpr int QUADS = NPIX / 4;
-    constexpr int DPS = plane_stride(NPIX);           // dy plane stride
-    constexpr int XPS = plane_stride(HRR * WS);       // x plane stride
-    static_assert(WO % 4 == 0, "pixel quads stay inside one row");
+    constexpr int NPC = RC * WO;                              // output pixels per chunk
+    constexpr int QC = NPC / 4;                               // pixel quads per chunk
+    constexpr int DPS = plane_stride(NPC);                    // dy plane stride
+    constexpr int XPS = plane_stride(HRC * XRS);              // x plane stride
+    constexpr int NCH = TPW * (TH / RC);                      // chunks per workgroup
+    static_assert(WO % 4 == 0 && TH % RC == 0 && QC % WPX == 0, "tiling");
     constexpr int DS_FLOATS = KC * DPS;
     constexpr int XS_FLOATS = CCH * XPS;
     constexpr int RED_FLOATS = (WPX > 1) ? (WPX - 1) * KBW * CBW * 9 * 4 * 64 : 0;
     constexpr int LDS_FLOATS = (DS_FLOATS + XS_FLOATS) > RED_FLOATS ? (DS_FLOATS + XS_FLOATS) : RED_FLOATS;
-    __shared__ float lds[LDS_FLOATS];
+    __shared__ __attribute__((aligned(16))) float lds[LDS_FLOATS];
     float* Ds = lds;
     float* Xs = lds + DS_FLOATS;
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int kb = wave % KBW, cb = (wave / KBW) % CBW, wpx = wave / (KBW * CBW);
     const int g = lane >> 4, j = lane & 15;
-    const int tiles = a.HO / TH;  // row bands per image
+    const int bands = a.HO / TH;         // row bands per image
     const int cbase = blockIdx.y * CCH;  // first input channel of this workgroup
 
     v4f acc[9];
 #pragma unroll
     for (int t = 0; t < 9; ++t) acc[t] = v4f{0.f, 0.f, 0.f, 0.f};
 
-    // zero padding columns of the x tile (never written by the staging loop)
-    for (int i = tid; i < HRR * CCH; i += NT) {
-        const int c = i / HRR, rr = i - (i / HRR) * HRR;
-        Xs[c * XPS + rr * WS] = 0.f;
-        if (STRIDE == 1) Xs[c * XPS + rr * WS + WS - 1] = 0.f;
+    // zero halo columns of the x tile (never written by the staging below)
+    for (int i = tid; i < HRC * CCH; i += NT) {
+        const int c = i / HRC, rr = i - (i / HRC) * HRC;
+        Xs[c * XPS + rr * XRS + 3] = 0.f;
+        if (STRIDE == 1) Xs[c * XPS + rr * XRS + WIN + 4] = 0.f;
     }
 
-    for (int it = 0; it < TPW; ++it) {
-        const int tl = blockIdx.x * TPW + it;
-        const int img = tl / tiles;
-        const int oh0 = (tl - img * tiles) * TH;
-        __syncthreads();  // previous tile's LDS reads are done
-        // dy tile and x tile, float4 global loads (rows are multiples of 4
-        // floats), scalar LDS stores into the plane-major layout
-        for (int i4 = tid; i4 < KC * NPIX / 4; i4 += NT) {
-            const int i = i4 * 4;
-            const int k = i / NPIX, pix = i - (i / NPIX) * NPIX;
-            const float4 v = *reinterpret_cast<const float4*>(a.dy + (((size_t)img * a.K + k) * a.HO + oh0) * WO + pix);
-            float* d = Ds + k * DPS + pix;
-            d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
-        }
+    // chunk ch: tile ch / (TH/RC) of this workgroup, rows (ch % (TH/RC))*RC ..
+    constexpr int DN4 = KC * NPC / 4, XN4 = CCH * HRC * WIN / 4;
+    constexpr int DV = (DN4 + NT - 1) / NT, XV = (XN4 + NT - 1) / NT;
+    float4 dr[DV], xr[XV];
+    auto load_chunk = [&](int ch) {
+        const int tl = blockIdx.x * TPW + ch / (TH / RC);
+        const int img = tl / bands;
+        const int oh0 = (tl - img * bands) * TH + (ch % (TH / RC)) * RC;
         const int ih0 = oh0 * STRIDE - 1;
-        for (int i4 = tid; i4 < CCH * HRR * WIN / 4; i4 += NT) {
-            const int i = i4 * 4;
-            const int c = i / (HRR * WIN);
-            const int rem = i - c * (HRR * WIN);
-            const int rr = rem / WIN, iw = rem - (rem / WIN) * WIN;
-            const int ih = ih0 + rr;
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (ih >= 0 && ih < a.H && cbase + c < a.C)
-                v = *reinterpret_cast<const float4*>(a.x + (((size_t)img * a.C + cbase + c) * a.H + ih) * WIN + iw);
-            float* d = Xs + c * XPS + rr * WS + iw + 1;
-            d[0] = v.x; d[1] = v.y; d[2] = v.z; d[3] = v.w;
+#pragma unroll
+        for (int v = 0; v < DV; ++v) {
+            const int i4 = tid + v * NT;
+            float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (i4 < DN4) {
+                const int i = i4 * 4;
+                const int k = i / NPC, pix = i - (i / NPC) * NPC;
+                val = *reinterpret_cast<const float4*>(a.dy + (((size_t)img * a.K + k) * a.HO + oh0) * WO + pix);
+            }
+            dr[v] = val;
         }
+#pragma unroll
+        for (int v = 0; v < XV; ++v) {
+            const int i4 = tid + v * NT;
+            float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
+            if (i4 < XN4) {
+                const int i = i4 * 4;
+                const int c = i / (HRC * WIN);
+                const int rem = i - c * (HRC * WIN);
+                const int rr = rem / WIN, iw = rem - (rem / WIN) * WIN;
+                const int ih = ih0 + rr;
+                if (ih >= 0 && ih < a.H && cbase + c < a.C)
+                    val = *reinterpret_cast<const float4*>(a.x + (((size_t)img * a.C + cbase + c) * a.H + ih) * WIN + iw);
+            }
+            xr[v] = val;
+        }
+    };
+    auto store_chunk = [&]() {
+#pragma unroll
+        for (int v = 0; v < DV; ++v) {
+            const int i4 = tid + v * NT;
+            if (i4 < DN4) {
+                const int i = i4 * 4;
+                const int k = i / NPC, pix = i - (i / NPC) * NPC;
+                float2* d = reinterpret_cast<float2*>(Ds + k * DPS + pix);  // DPS and pix even: 8-byte aligned
+                d[0] = make_float2(dr[v].x, dr[v].y);
+                d[1] = make_float2(dr[v].z, dr[v].w);
+            }
+        }
+#pragma unroll
+        for (int v = 0; v < XV; ++v) {
+            const int i4 = tid + v * NT;
+            if (i4 < XN4) {
+                const int i = i4 * 4;
+                const int c = i / (HRC * WIN);
+                const int rem = i - c * (HRC * WIN);
+                const int rr = rem / WIN, iw = rem - (rem / WIN) * WIN;
+                float2* d = reinterpret_cast<float2*>(Xs + c * XPS + rr * XRS + 4 + iw);  // even offset
+                d[0] = make_float2(xr[v].x, xr[v].y);
+                d[1] = make_float2(xr[v].z, xr[v].w);
+            }
+        }
+    };
+
+    const float* dsl = Ds + (kb * 16 + j) * DPS + g;
+    const float* xsl = Xs + (cb * 16 + j) * XPS + g * STRIDE + 3;
+    load_chunk(0);
+    for (int ch = 0; ch < NCH; ++ch) {
+        __syncthreads();  // the previous chunk's LDS reads are done
+        store_chunk();
         __syncthreads();
-        const float* dsl = Ds + (kb * 16 + j) * DPS + g;
-        const float* xsl = Xs + (cb * 16 + j) * XPS + g * STRIDE;
-        for (int qd = wpx; qd < QUADS; qd += WPX) {
-            const int pix0 = qd * 4;
+        if (ch + 1 < NCH) load_chunk(ch + 1);
+#pragma unroll
+        for (int qi = 0; qi < QC / WPX; ++qi) {
+            const int pix0 = (qi * WPX + wpx) * 4;
             const int row = pix0 / WO, col0 = pix0 - (pix0 / WO) * WO;
             const float av = dsl[pix0];
-            const float* xb = xsl + (row * STRIDE) * WS + col0 * STRIDE;
+            const float* xb = xsl + (row * STRIDE) * XRS + col0 * STRIDE;
 #pragma unroll
             for (int r = 0; r < 3; ++r)
 #pragma unroll
                 for (int s = 0; s < 3; ++s) {
-                    const float bv = xb[r * WS + s];
+                    const float bv = xb[r * XRS + s];
                     acc[r * 3 + s] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[r * 3 + s], 0, 0, 0);
                 }
         }
@@ -198,19 +247,24 @@ hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const fl
     switch (cfg) {
     case 6:
     case 1:
-        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 32, 16, 1, 1, 4, 1), wk, (conv3x3_wgrad<1, 32, 16, 1, 1, 4, 1>), grid, dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 32, 16, 1, 1, 4, 1, 4), wk, (conv3x3_wgrad<1, 32, 16, 1, 1, 4, 1, 4>), grid, dim3(256), 0,
+                   st, a);
         break;
     case 2:
-        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 16, 16, 2, 1, 2, 1), wk, (conv3x3_wgrad<1, 16, 16, 2, 1, 2, 1>), grid, dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 16, 16, 2, 1, 2, 1, 4), wk, (conv3x3_wgrad<1, 16, 16, 2, 1, 2, 1, 4>), grid, dim3(256), 0,
+                   st, a);
         break;
     case 3:
-        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 8, 8, 4, 1, 1, 2), wk, (conv3x3_wgrad<1, 8, 8, 4, 1, 1, 2>), grid, dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 8, 8, 4, 1, 1, 2, 8), wk, (conv3x3_wgrad<1, 8, 8, 4, 1, 1, 2, 8>), grid, dim3(256), 0,
+                   st, a);
         break;
     case 4:
-        PSW_LAUNCH(kname("conv3x3_wgrad", 2, 16, 8, 2, 1, 2, 1), wk, (conv3x3_wgrad<2, 16, 8, 2, 1, 2, 1>), grid, dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_wgrad", 2, 16, 8, 2, 1, 2, 1, 4), wk, (conv3x3_wgrad<2, 16, 8, 2, 1, 2, 1, 4>), grid, dim3(256), 0,
+                   st, a);
         break;
     case 5:
-        PSW_LAUNCH(kname("conv3x3_wgrad", 2, 8, 8, 4, 1, 1, 1), wk, (conv3x3_wgrad<2, 8, 8, 4, 1, 1, 1>), grid, dim3(256), 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_wgrad", 2, 8, 8, 4, 1, 1, 1, 4), wk, (conv3x3_wgrad<2, 8, 8, 4, 1, 1, 1, 4>), grid, dim3(256), 0,
+                   st, a);
         break;
     }
     return hipGetLastError();
