@@ -809,14 +809,14 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
                 e = psw::bn_apply_from_partials(a.n, a.c, a.h, a.w, act(o.in0), (const float*)ws, T, P, W, W + o.cin,
                                                 o.in1 >= 0 ? act(o.in1) : nullptr, r.c, r.h, r.w,
                                                 (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, act(i + 1), save,
-                                                save + o.cin, rm, rvv, st);
+                                                save + o.cin, save + 2 * o.cin, rm, rvv, st);
                 if (e == hipSuccess) break;
                 if (e != hipErrorNotSupported) return hip_check(e, "bn_apply");
                 // not supported: nothing launched, the statistics are recomputed below
             }
             PSW_TRY(psw::bn_fwd(a.n, a.c, a.h, a.w, act(o.in0), W, W + o.cin, o.in1 >= 0 ? act(o.in1) : nullptr, r.c,
                                 r.h, r.w, (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, act(i + 1), save, save + o.cin, rm,
-                                rvv, ws, wsb, st),
+                                rvv, ws, wsb, st, save + 2 * o.cin),
                     "bn_fwd");
             break;
         }
@@ -870,8 +870,12 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
             if (din && net->fuse_bwd[i]) {  // BN op i-1's backward sums out of this dgrad
                 const psw_layer& bo = net->ops[i - 1];
                 const float* bsave = (const float*)(A + net->save_off[i - 1]);
-                const psw::BnBwdFuse bnb{(float*)ws, act(i), act(bo.in0), bsave, bsave + bo.cin,
-                                         (bo.flags & PSW_F_RELU) != 0};
+                psw::BnBwdFuse bnb{(float*)ws, act(i), act(bo.in0), bsave, bsave + bo.cin,
+                                   (bo.flags & PSW_F_RELU) != 0};
+                if (bo.in1 < 0) {  // no residual: the ReLU mask comes from y and the forward's scale / shift
+                    bnb.scale = bsave + 2 * bo.cin;
+                    bnb.shift = bsave + 3 * bo.cin;
+                }
                 e = psw::conv_bwd_data_bnsums(cs, wcur(i), g, din, acc0, bnb, st);
                 if (e == hipSuccess) {
                     net->fused_bwd_now[i] = 1;
@@ -895,14 +899,11 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
                 psw::ConvShape ccs;
                 check_conv(y.n, y.c, y.h, y.w, cv.cout, cv.k, cv.k, cv.stride, cv.pad, net->prec, &ccs);
                 const int T = psw::conv_bwd_data_bnsums_tiles(ccs);
-                const bool identity = dres && r.c == a.c && r.h == a.h && r.w == a.w;
-                const int racc = net->grad_accum[2 * i + 1];
+                // without a residual the ReLU mask comes from y and the forward's scale / shift
+                const float* scale = o.in1 < 0 ? save + 2 * o.cin : nullptr;
                 e = psw::bn_bwd_from_partials(a.n, a.c, a.h, a.w, g, act(i + 1), act(o.in0), wcur(i), save,
-                                              save + o.cin, (const float*)ws, T, (o.flags & PSW_F_RELU) != 0, din, dg,
-                                              dg + o.cin, identity ? dres : nullptr, racc, st);
-                if (e == hipSuccess && dres && !identity)
-                    e = psw::shortcut_a_backward(a.n, a.c, a.h, a.w, r.c, r.h, r.w, g, act(i + 1),
-                                                 (o.flags & PSW_F_RELU) != 0, dres, racc, st);
+                                              save + o.cin, scale, (const float*)ws, T, (o.flags & PSW_F_RELU) != 0,
+                                              din, dg, dg + o.cin, dres, r.c, r.h, r.w, net->grad_accum[2 * i + 1], st);
                 if (e == hipSuccess) break;
                 if (e != hipErrorNotSupported) return hip_check(e, "bn_bwd_from_partials");
                 // not supported: nothing launched, the sums are recomputed below

@@ -367,6 +367,7 @@ hipError_t conv_bwd_data_bnsums(const ConvShape& cs, const float* w, const float
 {
     if (conv_bwd_data_bnsums_tiles(cs) == 0) return hipErrorNotSupported;
     if ((uintptr_t)bnb.z % 8 || (uintptr_t)bnb.y % 8) return hipErrorNotSupported;
+    if (bnb.relu && !bnb.scale && !bnb.z) return hipErrorInvalidValue;
     if (cs.stride == 1) return conv3x3_direct(cs.n, cs.k, cs.h, cs.w, cs.c, 1, dy, w, dx, accumulate, true, st, nullptr, &bnb);
     return conv3x3_dgrad_s2(cs.n, cs.c, cs.h, cs.w, cs.k, w, dy, dx, accumulate, st, &bnb);
 }

@@ -259,24 +259,29 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     }
     float gs1[4] = {0.f, 0.f, 0.f, 0.f}, gs2[4] = {0.f, 0.f, 0.f, 0.f};
     if (TRANS && a.bnb.part) {  // acc is the final gradient of the preceding BN's output
-        float zz[NBW][4], yy[NBW][4], mu[4], is[4];
+        const bool zmask = a.bnb.relu && !a.bnb.scale, ymask = a.bnb.relu && a.bnb.scale;
+        float zz[NBW][4], yy[NBW][4], mu[4], is[4], sc[4], sf[4];
 #pragma unroll
         for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                zz[nb][i] = a.bnb.z[oidx[nb] + i * cstr];
                 yy[nb][i] = a.bnb.y[oidx[nb] + i * cstr];
+                zz[nb][i] = zmask ? a.bnb.z[oidx[nb] + i * cstr] : 1.f;
             }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            mu[i] = a.bnb.mean[mblk + wk * 16 + 4 * g + i];
-            is[i] = a.bnb.invstd[mblk + wk * 16 + 4 * g + i];
+            const int m = mblk + wk * 16 + 4 * g + i;
+            mu[i] = a.bnb.mean[m];
+            is[i] = a.bnb.invstd[m];
+            sc[i] = ymask ? a.bnb.scale[m] : 0.f;
+            sf[i] = ymask ? a.bnb.shift[m] : 0.f;
         }
 #pragma unroll
         for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                const float gg = (a.bnb.relu && !(zz[nb][i] > 0.f)) ? 0.f : acc[nb][i];
+                const bool pass = ymask ? __fmaf_rn(yy[nb][i], sc[i], sf[i]) > 0.f : zz[nb][i] > 0.f;
+                const float gg = (a.bnb.relu && !pass) ? 0.f : acc[nb][i];
                 gs1[i] += gg;
                 gs2[i] += gg * ((yy[nb][i] - mu[i]) * is[i]);
             }
@@ -514,21 +519,26 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
     }
     float gs1[4] = {0.f, 0.f, 0.f, 0.f}, gs2[4] = {0.f, 0.f, 0.f, 0.f};
     if (a.bnb.part) {
+        const bool zmask = a.bnb.relu && !a.bnb.scale, ymask = a.bnb.relu && a.bnb.scale;
         float2 zz[NBW][4][2], yy[NBW][4][2];
-        float mu[4], is[4];
+        float mu[4], is[4], sc[4], sf[4];
 #pragma unroll
         for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
             for (int v = 0; v < 4; ++v)
 #pragma unroll
                 for (int ph = 0; ph < 2; ++ph) {
-                    zz[nb][v][ph] = *reinterpret_cast<const float2*>(a.bnb.z + oidx[nb] + v * cstr + ph * W2);
                     yy[nb][v][ph] = *reinterpret_cast<const float2*>(a.bnb.y + oidx[nb] + v * cstr + ph * W2);
+                    zz[nb][v][ph] = zmask ? *reinterpret_cast<const float2*>(a.bnb.z + oidx[nb] + v * cstr + ph * W2)
+                                          : make_float2(1.f, 1.f);
                 }
 #pragma unroll
         for (int v = 0; v < 4; ++v) {
-            mu[v] = a.bnb.mean[mblk + wk * 16 + 4 * g + v];
-            is[v] = a.bnb.invstd[mblk + wk * 16 + 4 * g + v];
+            const int m = mblk + wk * 16 + 4 * g + v;
+            mu[v] = a.bnb.mean[m];
+            is[v] = a.bnb.invstd[m];
+            sc[v] = ymask ? a.bnb.scale[m] : 0.f;
+            sf[v] = ymask ? a.bnb.shift[m] : 0.f;
         }
 #pragma unroll
         for (int nb = 0; nb < NBW; ++nb)
@@ -537,8 +547,10 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
 #pragma unroll
                 for (int ph = 0; ph < 2; ++ph) {
                     const float2 gv = val[nb][v][ph], zv = zz[nb][v][ph], yv = yy[nb][v][ph];
-                    const float g0 = (a.bnb.relu && !(zv.x > 0.f)) ? 0.f : gv.x;
-                    const float g1 = (a.bnb.relu && !(zv.y > 0.f)) ? 0.f : gv.y;
+                    const bool p0 = ymask ? __fmaf_rn(yv.x, sc[v], sf[v]) > 0.f : zv.x > 0.f;
+                    const bool p1 = ymask ? __fmaf_rn(yv.y, sc[v], sf[v]) > 0.f : zv.y > 0.f;
+                    const float g0 = (a.bnb.relu && !p0) ? 0.f : gv.x;
+                    const float g1 = (a.bnb.relu && !p1) ? 0.f : gv.y;
                     gs1[v] += g0 + g1;
                     gs2[v] += g0 * ((yv.x - mu[v]) * is[v]) + g1 * ((yv.y - mu[v]) * is[v]);
                 }
@@ -591,7 +603,7 @@ hipError_t launch_direct(const DirArgs& a, int n, bool trans, hipStream_t st)
     Work wk = conv_work(n, a.C, a.H, WO * STRIDE, a.K, 3, 3, a.HO, WO);
     const double out_bytes = kF * n * (double)a.K * a.HO * WO;
     if (a.accumulate) wk.bytes += out_bytes;        // the existing output is read
-    if (a.bnb.part) wk.bytes += 2.0 * out_bytes;    // BN output and input for the backward sums
+    if (a.bnb.part) wk.bytes += (a.bnb.scale ? 1.0 : 2.0) * out_bytes;  // BN input (and output) for the sums
     if (trans)
         PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true), wk,
                    (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true>), grid, block, 0, st, a);
@@ -660,7 +672,7 @@ hipError_t conv3x3_dgrad_s2(int n, int CL, int H, int W, int KL, const float* w,
     Work wk = conv_work(n, CL, H, W, KL, 3, 3, HO, WO);
     const double dx_bytes = kF * n * (double)CL * H * W;
     if (accumulate) wk.bytes += dx_bytes;
-    if (bnb) wk.bytes += 2.0 * dx_bytes;
+    if (bnb) wk.bytes += (bnb->scale ? 1.0 : 2.0) * dx_bytes;
     if (WO == 16 && HO % 4 == 0 && CL % 16 == 0) {
         PSW_LAUNCH(kname("conv3x3_dgrad_s2", 16, 4, 16, 1, 4, 1), wk, (conv3x3_dgrad_s2<16, 4, 16, 1, 4, 1>),
                    dim3(n * (HO / 4), CL / 16), dim3(256), 0, st, a);

@@ -98,13 +98,19 @@ struct BnStatsFuse {
 // g = dz * [z > 0] (relu) or dz and xhat = (y - mean) * invstd, every
 // workgroup writes (sum g, sum g*xhat) of each channel over its pixels to
 // part[channel][tile][2]; bn_bwd_from_partials merges them.
+// For a BN without residual the ReLU mask is recomputed from y instead of
+// read from z: z > 0 exactly when fmaf(y, scale, shift) > 0 with the
+// forward's own per-channel scale and shift (the forward evaluates that
+// same fused multiply-add), so scale != nullptr means z is not read.
 struct BnBwdFuse {
     float* part;
-    const float* z;       // BN output (its ReLU mask)
+    const float* z;       // BN output (its ReLU mask); unused when scale is set
     const float* y;       // BN input
     const float* mean;
     const float* invstd;
     int relu;
+    const float* scale = nullptr;  // forward scale / shift (BN without residual)
+    const float* shift = nullptr;
 };
 
 // ---- convolution (implicit GEMM on MFMA) ----
@@ -121,7 +127,7 @@ int conv_fwd_bnstats_tiles(const ConvShape& cs);  // tiles T (partials per chann
 hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, const float* part, int T, int P,
                                   const float* gamma, const float* beta, const float* res, int rc, int rh, int rw,
                                   int relu, float eps, float momentum, float* z, float* save_mean, float* save_invstd,
-                                  float* run_mean, float* run_var, hipStream_t st);
+                                  float* save_scale, float* run_mean, float* run_var, hipStream_t st);
 // Direct 3x3 / pad 1 kernel (forward, or backward-data of a stride-1 layer
 // when transpose is set); hipErrorNotSupported when no tile config fits.
 hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const float* x, const float* w, float* y,
@@ -139,15 +145,16 @@ int dgrad_bnsums_tiles(int n, int CL, int H, int W, int KL, int stride);
 int conv_bwd_data_bnsums_tiles(const ConvShape& cs);
 hipError_t conv_bwd_data_bnsums(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate,
                                 const BnBwdFuse& bnb, hipStream_t st);
-// BN backward (+ identity residual) from per-tile (sum g, sum g*xhat)
-// partials over P pixels: merges them in a fixed order, writes dgamma,
-// dbeta (block 0 of a channel) and dy, and dres for an identity residual.
+// BN backward (+ residual) from per-tile (sum g, sum g*xhat) partials:
+// merges them in a fixed order, writes dgamma, dbeta (block 0 of a channel)
+// and dy, and dres for an identity or option-A (2x subsampled, zero-padded
+// channels) residual.  scale (scale[c], shift[c] after it) replaces z for
+// the ReLU mask of a BN without residual.  hipErrorNotSupported (nothing
+// launched) for other residual shapes or misaligned operands.
 hipError_t bn_bwd_from_partials(int n, int c, int h, int w, const float* dz, const float* z, const float* y,
-                                const float* gamma, const float* mean, const float* invstd, const float* part, int T,
-                                int relu, float* dy, float* dgamma, float* dbeta, float* dres_identity,
-                                int res_accumulate, hipStream_t st);
-hipError_t shortcut_a_backward(int n, int c, int h, int w, int rc, int rh, int rw, const float* dz, const float* z,
-                               int relu, float* dres, int accumulate, hipStream_t st);
+                                const float* gamma, const float* mean, const float* invstd, const float* scale,
+                                const float* part, int T, int relu, float* dy, float* dgamma, float* dbeta,
+                                float* dres, int rc, int rh, int rw, int res_accumulate, hipStream_t st);
 // Backward-weight partial sums of a 3x3 / pad 1 conv (dW-shaped, one per
 // workgroup); conv3x3_wgrad_splits is 0 when no configuration covers it.
 int conv3x3_wgrad_splits(int n, int C, int H, int W, int K, int stride);
@@ -166,7 +173,7 @@ size_t bn_ws_bytes(int n, int c, int h, int w);
 hipError_t bn_fwd(int n, int c, int h, int w, const float* y, const float* gamma, const float* beta,
                   const float* res, int rc, int rh, int rw, int relu, float eps, float momentum, float* z,
                   float* save_mean, float* save_invstd, float* run_mean, float* run_var, void* ws,
-                  size_t ws_bytes, hipStream_t st);
+                  size_t ws_bytes, hipStream_t st, float* save_scale = nullptr);
 hipError_t bn_bwd(int n, int c, int h, int w, const float* dz, const float* z, const float* y,
                   const float* gamma, const float* save_mean, const float* save_invstd, int relu, float* dy,
                   float* dgamma, float* dbeta, float* dres, int rc, int rh, int rw, int res_accumulate,

@@ -46,6 +46,29 @@ __device__ __forceinline__ double block_sum(double v, double* sh)
     return t;
 }
 
+// Two sums over the block at once, fixed order; results valid in thread 0.
+__device__ __forceinline__ void block_sum2(double& a, double& b, double* sh)
+{
+    a = wave_sum(a);
+    b = wave_sum(b);
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = (int)(blockDim.x >> 6);
+    if (lane == 0) {
+        sh[wave] = a;
+        sh[nw + wave] = b;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double ta = 0.0, tb = 0.0;
+        for (int i = 0; i < nw; ++i) {
+            ta += sh[i];
+            tb += sh[nw + i];
+        }
+        a = ta;
+        b = tb;
+    }
+    __syncthreads();
+}
+
 int channel_splits(int n, int c)
 {
     int sp = (1024 + c - 1) / c;
@@ -95,7 +118,7 @@ __global__ __launch_bounds__(kBlock) void chan_partials(int mode, int n, int c, 
 
 __global__ void bn_fwd_finalize(int c, int split, double count, const double* part, const float* gamma,
                                 const float* beta, float eps, float momentum, float* save_mean, float* save_invstd,
-                                float* run_mean, float* run_var, float* coef)
+                                float* run_mean, float* run_var, float* coef, float* save_scale)
 {
     const int ch = blockIdx.x * blockDim.x + threadIdx.x;
     if (ch >= c) return;
@@ -117,6 +140,10 @@ __global__ void bn_fwd_finalize(int c, int split, double count, const double* pa
     const double scale = (double)gamma[ch] * invstd;
     coef[2 * ch + 0] = (float)scale;
     coef[2 * ch + 1] = (float)((double)beta[ch] - mean * scale);
+    if (save_scale) {
+        save_scale[ch] = coef[2 * ch + 0];
+        save_scale[c + ch] = coef[2 * ch + 1];
+    }
 }
 
 __global__ void bn_fwd_apply(int64_t total, int c, int hw, const float* y, const float* coef, const float* res,
@@ -126,7 +153,7 @@ __global__ void bn_fwd_apply(int64_t total, int c, int hw, const float* y, const
     if (i >= total) return;
     const int64_t nc = i / hw;
     const int ch = (int)(nc % c);
-    float v = y[i] * coef[2 * ch] + coef[2 * ch + 1];
+    float v = __fmaf_rn(y[i], coef[2 * ch], coef[2 * ch + 1]);
     if (res) {
         if (rc == c && rh == h && rw == w) {
             v += res[i];
@@ -522,7 +549,8 @@ size_t bn_ws_bytes(int n, int c, int h, int w)
 
 hipError_t bn_fwd(int n, int c, int h, int w, const float* y, const float* gamma, const float* beta, const float* res,
                   int rc, int rh, int rw, int relu, float eps, float momentum, float* z, float* save_mean,
-                  float* save_invstd, float* run_mean, float* run_var, void* ws, size_t ws_bytes, hipStream_t st)
+                  float* save_invstd, float* run_mean, float* run_var, void* ws, size_t ws_bytes, hipStream_t st,
+                  float* save_scale)
 {
     if (ws_bytes < bn_ws_bytes(n, c, h, w)) return hipErrorInvalidValue;
     const int sp = channel_splits(n, c);
@@ -535,7 +563,7 @@ hipError_t bn_fwd(int n, int c, int h, int w, const float* y, const float* gamma
                (const float*)nullptr, 0, part);
     PSW_LAUNCH(kname("bn_fwd_finalize"), (Work{2.0 * c * sp, 16.0 * c * sp + 6 * kF * c}), bn_fwd_finalize,
                dim3(blocks_for(c)), dim3(kBlock), 0, st, c, sp, (double)n * hw, (const double*)part, gamma, beta, eps,
-               momentum, save_mean, save_invstd, run_mean, run_var, coef);
+               momentum, save_mean, save_invstd, run_mean, run_var, coef, save_scale);
     const double rbytes = res ? kF * (double)n * std::min(c, rc) * hw : 0.0;
     PSW_LAUNCH(kname("bn_fwd_apply"), (Work{3.0 * total, kF * 2.0 * total + rbytes}), bn_fwd_apply,
                dim3(blocks_for(total)), dim3(kBlock), 0, st, total, c, hw, y, (const float*)coef, res, rc, rh, rw, h, w,
@@ -581,22 +609,25 @@ namespace {
 // (unit u: image u / hw4, offset 4*(u % hw4)) with 32-bit index arithmetic.
 constexpr int kApplyUnits = 1024;  // float4 units per block (a multiple of kBlock)
 
-// forward: tile partials (mean_t, M2_t over P pixels each)
-//   mean = (1/T) sum mean_t,  M2 = sum M2_t + P sum (mean_t - mean)^2
-// The element loads are issued before the partial merge so that the two
-// memory latencies overlap, and every load precedes every store.
+// forward: tile partials (mean_t, M2_t over P pixels each), merged in one
+// pass in double:
+//   mean = (1/T) sum mean_t,  M2 = sum (M2_t + P mean_t^2) - T P mean^2
+// (exact products of fp32 values; the double sums lose nothing that the
+// fp32 tile statistics did not already round).  The element loads are
+// issued before the merge so that the two memory latencies overlap, and
+// every load precedes every store.  Block y == 0 also stores the channel's
+// scale and shift, which the backward recomputes the ReLU mask from.
 constexpr int kUnitsPerThread = kApplyUnits / kBlock;
 
 __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int hw, const float* y, const float* part,
                                                                int T, int P, const float* gamma, const float* beta,
                                                                const float* res, int rc, int rh, int rw, int h, int w,
                                                                int relu, float eps, float momentum, float* z,
-                                                               float* save_mean, float* save_invstd, float* run_mean,
-                                                               float* run_var)
+                                                               float* save_mean, float* save_invstd, float* save_scale,
+                                                               float* run_mean, float* run_var)
 {
-    __shared__ double sh[kBlock / 64];
+    __shared__ double sh[2 * kBlock / 64];
     __shared__ float coef[2];
-    __shared__ double mean_sh;
     const int ch = blockIdx.x;
     const int hw4 = hw >> 2;
     const int units = n * hw4;
@@ -628,21 +659,18 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
         }
     }
     const float* pp = part + (size_t)ch * T * 2;
-    double s1 = 0.0;
-    for (int t = threadIdx.x; t < T; t += kBlock) s1 += (double)pp[2 * t];
-    s1 = block_sum(s1, sh);
-    if (threadIdx.x == 0) mean_sh = s1 / T;
-    __syncthreads();
-    const double mean = mean_sh;
-    double s2 = 0.0;
+    double s1 = 0.0, s2 = 0.0;
     for (int t = threadIdx.x; t < T; t += kBlock) {
-        const double d = (double)pp[2 * t] - mean;
-        s2 += (double)pp[2 * t + 1] + (double)P * d * d;
+        const double m = (double)pp[2 * t];
+        s1 += m;
+        s2 += (double)pp[2 * t + 1] + (double)P * m * m;
     }
-    s2 = block_sum(s2, sh);
+    block_sum2(s1, s2, sh);
     if (threadIdx.x == 0) {
         const double cnt = (double)T * P;
-        const double var = s2 / cnt;
+        const double mean = s1 / T;
+        double var = (s2 - cnt * mean * mean) / cnt;
+        if (var < 0.0) var = 0.0;
         const double invstd = 1.0 / sqrt(var + (double)eps);
         const double scale = (double)gamma[ch] * invstd;
         coef[0] = (float)scale;
@@ -650,6 +678,10 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
         if (blockIdx.y == 0) {
             save_mean[ch] = (float)mean;
             save_invstd[ch] = (float)invstd;
+            if (save_scale) {
+                save_scale[ch] = coef[0];
+                save_scale[c + ch] = coef[1];
+            }
             if (run_mean) {
                 run_mean[ch] = (float)((1.0 - momentum) * run_mean[ch] + momentum * mean);
                 run_var[ch] = (float)((1.0 - momentum) * run_var[ch] + momentum * (cnt > 1.0 ? var * cnt / (cnt - 1.0) : var));
@@ -661,7 +693,8 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
 #pragma unroll
     for (int q = 0; q < U; ++q) {
         if (u0 + (int)threadIdx.x + q * kBlock >= u1) continue;
-        float v[4] = {yv[q].x * sc + sf, yv[q].y * sc + sf, yv[q].z * sc + sf, yv[q].w * sc + sf};
+        float v[4] = {__fmaf_rn(yv[q].x, sc, sf), __fmaf_rn(yv[q].y, sc, sf), __fmaf_rn(yv[q].z, sc, sf),
+                      __fmaf_rn(yv[q].w, sc, sf)};
         if (res) {
             v[0] += rv[q].x; v[1] += rv[q].y; v[2] += rv[q].z; v[3] += rv[q].w;
         }
@@ -675,35 +708,46 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
 
 // backward: tile partials (sum g, sum g*xhat) with g = dz*[z > 0] (relu);
 //   dbeta = sum g, dgamma = sum g*xhat,
-//   dy = gamma*invstd*(g - dbeta/M - xhat*dgamma/M),  dres (+)= g (identity)
-__global__ __launch_bounds__(kBlock) void bn_bwd_partials_k(int n, int c, int hw, const float* dz, const float* z,
-                                                             const float* y, const float* gamma, const float* mean,
-                                                             const float* invstd, const float* part, int T, int relu,
+//   dy = gamma*invstd*(g - dbeta/M - xhat*dgamma/M),
+// and the residual's gradient: dres (+)= g (identity), or for the option-A
+// shortcut (residual of 2x the resolution, channels padded by lo on each
+// side) g at the even positions of channel ch - lo and zero elsewhere.
+// With scale set (a BN without residual) the mask is fmaf(y, scale, shift)
+// > 0, the forward's own pre-activation, and z is not read.
+__global__ __launch_bounds__(kBlock) void bn_bwd_partials_k(int n, int c, int hw, int w, const float* dz,
+                                                             const float* z, const float* y, const float* gamma,
+                                                             const float* mean, const float* invstd,
+                                                             const float* scale, const float* part, int T, int relu,
                                                              float* dy, float* dgamma, float* dbeta, float* dres,
-                                                             int res_accumulate)
+                                                             int rc, int res_mode, int res_accumulate)
 {
-    __shared__ double sh[kBlock / 64];
+    __shared__ double sh[2 * kBlock / 64];
     __shared__ float coef[3];
     const int ch = blockIdx.x;
     const int hw4 = hw >> 2;
     const int units = n * hw4;
     const int u0 = blockIdx.y * kApplyUnits;
     const int u1 = min(u0 + kApplyUnits, units);
+    const bool ymask = relu && scale, zmask = relu && !scale;
+    const float sc = ymask ? scale[ch] : 0.f, sf = ymask ? scale[c + ch] : 0.f;
+    const int cc = ch - (c - rc) / 2;  // residual channel (option A)
+    const bool identity = res_mode == 1, shortcut_a = res_mode == 2 && cc >= 0 && cc < rc;
     constexpr int U = kUnitsPerThread;
     size_t idx[U];
     float4 gv[U], zv[U], yv[U], ov[U];
 #pragma unroll
     for (int q = 0; q < U; ++q) {
         const int u = u0 + threadIdx.x + q * kBlock;
-        gv[q] = zv[q] = yv[q] = ov[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+        gv[q] = yv[q] = ov[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+        zv[q] = make_float4(1.f, 1.f, 1.f, 1.f);
         idx[q] = 0;
         if (u < u1) {
             const int img = u / hw4, off = (u - img * hw4) * 4;
             idx[q] = ((size_t)img * c + ch) * hw + off;
             gv[q] = *reinterpret_cast<const float4*>(dz + idx[q]);
-            zv[q] = *reinterpret_cast<const float4*>(z + idx[q]);
             yv[q] = *reinterpret_cast<const float4*>(y + idx[q]);
-            if (dres && res_accumulate) ov[q] = *reinterpret_cast<const float4*>(dres + idx[q]);
+            if (zmask) zv[q] = *reinterpret_cast<const float4*>(z + idx[q]);
+            if (identity && res_accumulate) ov[q] = *reinterpret_cast<const float4*>(dres + idx[q]);
         }
     }
     const float* pp = part + (size_t)ch * T * 2;
@@ -712,8 +756,7 @@ __global__ __launch_bounds__(kBlock) void bn_bwd_partials_k(int n, int c, int hw
         s1 += (double)pp[2 * t];
         s2 += (double)pp[2 * t + 1];
     }
-    s1 = block_sum(s1, sh);
-    s2 = block_sum(s2, sh);
+    block_sum2(s1, s2, sh);
     const float mu = mean[ch], is = invstd[ch];
     if (threadIdx.x == 0) {
         const double cnt = (double)n * hw;
@@ -729,21 +772,41 @@ __global__ __launch_bounds__(kBlock) void bn_bwd_partials_k(int n, int c, int hw
     const float a = coef[0], b = coef[1], d = coef[2];
 #pragma unroll
     for (int q = 0; q < U; ++q) {
-        if (u0 + (int)threadIdx.x + q * kBlock >= u1) continue;
+        const int u = u0 + (int)threadIdx.x + q * kBlock;
+        if (u >= u1) continue;
         float g[4] = {gv[q].x, gv[q].y, gv[q].z, gv[q].w};
         const float zz[4] = {zv[q].x, zv[q].y, zv[q].z, zv[q].w};
         const float yy[4] = {yv[q].x, yv[q].y, yv[q].z, yv[q].w};
         float o[4];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-            if (relu && !(zz[e] > 0.f)) g[e] = 0.f;
+            const bool pass = ymask ? __fmaf_rn(yy[e], sc, sf) > 0.f : zz[e] > 0.f;
+            if (relu && !pass) g[e] = 0.f;
             const float xh = (yy[e] - mu) * is;
             o[e] = a * (g[e] - b - xh * d);
         }
         *reinterpret_cast<float4*>(dy + idx[q]) = make_float4(o[0], o[1], o[2], o[3]);
-        if (dres)
+        if (identity) {
             *reinterpret_cast<float4*>(dres + idx[q]) =
                 make_float4(g[0] + ov[q].x, g[1] + ov[q].y, g[2] + ov[q].z, g[3] + ov[q].w);
+        } else if (shortcut_a) {  // residual rows 2hh (g at even columns) and 2hh+1 (zero)
+            const int img = u / hw4, off = (u - img * hw4) * 4;
+            const int hh = off / w, ww = off - hh * w;
+            float4* r0 = reinterpret_cast<float4*>(dres + (((size_t)img * rc + cc) * (2 * (hw / w)) + 2 * hh) * (2 * w) + 2 * ww);
+            float4* r1 = r0 + (2 * w) / 4;
+            float4 e0 = make_float4(g[0], 0.f, g[1], 0.f), e1 = make_float4(g[2], 0.f, g[3], 0.f);
+            if (res_accumulate) {
+                const float4 o0 = r0[0], o1 = r0[1];
+                e0.x += o0.x; e0.y += o0.y; e0.z += o0.z; e0.w += o0.w;
+                e1.x += o1.x; e1.y += o1.y; e1.z += o1.z; e1.w += o1.w;
+            }
+            r0[0] = e0;
+            r0[1] = e1;
+            if (!res_accumulate) {
+                r1[0] = make_float4(0.f, 0.f, 0.f, 0.f);
+                r1[1] = make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+        }
     }
 }
 
@@ -753,7 +816,7 @@ bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, const float* part, int T, int P,
                                   const float* gamma, const float* beta, const float* res, int rc, int rh, int rw,
                                   int relu, float eps, float momentum, float* z, float* save_mean, float* save_invstd,
-                                  float* run_mean, float* run_var, hipStream_t st)
+                                  float* save_scale, float* run_mean, float* run_var, hipStream_t st)
 {
     const bool identity = res && rc == c && rh == h && rw == w;
     if (w % 4 || !aligned16(y) || !aligned16(z) || (identity && !aligned16(res))) return hipErrorNotSupported;
@@ -764,38 +827,35 @@ hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, co
     const double rbytes = res ? kF * (double)n * std::min(c, rc) * h * w : 0.0;
     PSW_LAUNCH(kname("bn_apply_partials_k"), (Work{3.0 * total, 2 * kF * total + rbytes + 2 * kF * T * c}),
                bn_apply_partials_k, dim3(c, per_ch), dim3(kBlock), 0, st, n, c, h * w, y, part, T, P, gamma, beta, res,
-               rc, rh, rw, h, w, relu, eps, momentum, z, save_mean, save_invstd, run_mean, run_var);
+               rc, rh, rw, h, w, relu, eps, momentum, z, save_mean, save_invstd, save_scale, run_mean, run_var);
     return hipGetLastError();
 }
 
 hipError_t bn_bwd_from_partials(int n, int c, int h, int w, const float* dz, const float* z, const float* y,
-                                const float* gamma, const float* mean, const float* invstd, const float* part, int T,
-                                int relu, float* dy, float* dgamma, float* dbeta, float* dres_identity,
-                                int res_accumulate, hipStream_t st)
+                                const float* gamma, const float* mean, const float* invstd, const float* scale,
+                                const float* part, int T, int relu, float* dy, float* dgamma, float* dbeta,
+                                float* dres, int rc, int rh, int rw, int res_accumulate, hipStream_t st)
 {
-    if (w % 4 || !aligned16(dz) || !aligned16(z) || !aligned16(y) || !aligned16(dy) ||
-        (dres_identity && !aligned16(dres_identity)))
+    int res_mode = 0;
+    if (dres) {
+        if (rc == c && rh == h && rw == w) res_mode = 1;
+        else if (rh == 2 * h && rw == 2 * w && rc <= c && (c - rc) % 2 == 0) res_mode = 2;
+        else return hipErrorNotSupported;
+    }
+    if (relu && !scale && !z) return hipErrorInvalidValue;
+    if (w % 4 || !aligned16(dz) || !aligned16(y) || !aligned16(dy) || (z && !aligned16(z)) ||
+        (dres && !aligned16(dres)))
         return hipErrorNotSupported;
     const int64_t units = (int64_t)n * h * w / 4;
     if (units > INT32_MAX) return hipErrorNotSupported;
     const unsigned per_ch = (unsigned)((units + kApplyUnits - 1) / kApplyUnits);
     const double total = (double)n * c * h * w;
-    const double dres_rw = dres_identity ? 1.0 + res_accumulate : 0.0;
-    PSW_LAUNCH(kname("bn_bwd_partials_k"), (Work{6.0 * total, kF * (4.0 + dres_rw) * total + 2 * kF * T * c}),
-               bn_bwd_partials_k, dim3(c, per_ch), dim3(kBlock), 0, st, n, c, h * w, dz, z, y, gamma, mean, invstd,
-               part, T, relu, dy, dgamma, dbeta, dres_identity, res_accumulate);
-    return hipGetLastError();
-}
-
-// option-A shortcut backward alone (the identity case is folded into the BN
-// backward kernels)
-hipError_t shortcut_a_backward(int n, int c, int h, int w, int rc, int rh, int rw, const float* dz, const float* z,
-                               int relu, float* dres, int accumulate, hipStream_t st)
-{
-    const int64_t rtotal = (int64_t)n * rc * rh * rw;
-    PSW_LAUNCH(kname("shortcut_a_bwd"), (Work{0.0, kF * ((1.0 + accumulate) * rtotal + 2.0 * n * rc * h * w)}),
-               shortcut_a_bwd, dim3(blocks_for(rtotal)), dim3(kBlock), 0, st, rtotal, c, h, w, rc, rh, rw, dz, z, relu,
-               dres, accumulate);
+    double bytes = kF * ((relu && !scale ? 4.0 : 3.0) * total) + 2 * kF * T * c;  // dz, y, (z), dy
+    if (res_mode == 1) bytes += kF * (1.0 + res_accumulate) * total;
+    if (res_mode == 2) bytes += kF * (double)n * rc * rh * rw + (res_accumulate ? kF * (double)n * rc * h * w * 2 : 0.0);
+    PSW_LAUNCH(kname("bn_bwd_partials_k"), (Work{6.0 * total, bytes}), bn_bwd_partials_k, dim3(c, per_ch), dim3(kBlock),
+               0, st, n, c, h * w, w, dz, z, y, gamma, mean, invstd, scale, part, T, relu, dy, dgamma, dbeta, dres, rc,
+               res_mode, res_accumulate);
     return hipGetLastError();
 }
 
