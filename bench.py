@@ -1,14 +1,19 @@
 """Benchmark: stale-weight pipelined training of ResNet-20 (CIFAR shape,
 batch 128) on one MI355X through libpsw.
 
-One step = psw_stage_step on one mini-batch: forward of all 4 stages (PPV
-(7,13,19), weights of version t - d_s with d = [3,2,1,0]), softmax
-cross-entropy, backward (weight gradients + data gradients with the current
-weights), and the SGD-momentum update into each stage's weight-version ring.
-Inputs are synthetic N(0,1) [128,3,32,32] batches with uniform labels, all
-resident in HBM before timing starts.
+One step = one mini-batch through all 4 stages: forward (PPV (7,13,19),
+weights of version t - d_s with d = [3,2,1,0]), softmax cross-entropy,
+backward (weight gradients + data gradients with the current weights), and
+the SGD-momentum update into each stage's weight-version ring.  The steps
+run as the paper's pipeline on one GPU (psw_pipeline_run: the forward pass
+of mini-batch t+1 overlaps the backward pass of mini-batch t where the
+stale weights allow it; results identical to one psw_stage_step call per
+step, which --sequential times instead).  Inputs are synthetic N(0,1)
+[128,3,32,32] batches with uniform labels, all resident in HBM before timing
+starts.
 
-Prints one JSON line.  `value` is images/s over the K timed steps.
+Prints one JSON line.  `value` is images/s over the K timed steps; the other
+execution mode is timed over K more steps for context.
 
 Measurement, in order: W warm-up steps; the K timed steps (wall clock, no
 events); then a profiling pass of min(K, 100) steps of the same workload in
@@ -125,6 +130,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--bf16", action="store_true", help="bf16-in / fp32-accumulate conv and FC products")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--sequential", action="store_true",
+                    help="time one psw_stage_step call per step instead of the pipelined run")
     ap.add_argument("--no-profile", action="store_true",
                     help="no events at all: skip the profiling pass and the dominant-kernel timing")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -148,7 +155,7 @@ def main():
     wl = synth.resnet20_workload(bf16=args.bf16)
     K, W = args.steps, args.warmup
     KP = 0 if args.no_profile else min(K, PROFILE_STEPS)
-    T = W + KP + K
+    T = W + KP + 2 * K
     net = psw.Net(wl.ops, wl.batch, wl.in_shape, wl.stage_end, wl.ring_depth(T), bf16=wl.bf16)
     net.load_params(synth.init_params(wl))
     stal = wl.staleness(T)
@@ -162,13 +169,22 @@ def main():
         ys[i].copy_(torch.from_numpy(y))
     torch.cuda.synchronize()
     t = 0
+    losses = torch.zeros(max(K, W, KP, 1), dtype=torch.float32, device="cuda")
 
-    def run(n):
+    def run_sequential(n):
         nonlocal t
         for _ in range(n):
             net.step(t, stal[t], wl.lr, xs[t % n_distinct], ys[t % n_distinct], wl.momentum, wl.weight_decay,
                      wl.nesterov)
             t += 1
+
+    def run_pipelined(n):
+        # one call: step t+i uses batch i mod n_distinct
+        nonlocal t
+        net.pipeline_run(t, stal[t:t + n], wl.lr, xs, ys, losses[:n], wl.momentum, wl.weight_decay, wl.nesterov)
+        t += n
+
+    run = run_sequential if args.sequential else run_pipelined
 
     run(W)
     torch.cuda.synchronize()
@@ -177,10 +193,16 @@ def main():
     run(K)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    loss = float(net.loss.item())
+    loss = float(net.loss.item() if args.sequential else losses[K - 1].item())
     assert np.isfinite(loss), loss
     ms_per_step = 1000.0 * elapsed / K
     img_s = wl.batch * K / elapsed
+    # the other execution mode, for context (same workload, continuing the run)
+    other = run_pipelined if args.sequential else run_sequential
+    t1 = time.perf_counter()
+    other(K)
+    torch.cuda.synchronize()
+    other_img_s = wl.batch * K / (time.perf_counter() - t1)
 
     # profiling pass over the same workload: every kernel launched with
     # start / stop events stamped from its own dispatch
@@ -232,7 +254,10 @@ def main():
         "data": "synthetic",
         "config": {"workload": "ResNet-20 (CIFAR shape), batch 128, 4 stages at PPV (7,13,19), staleness [3,2,1,0], "
                                "SGD momentum 0.9, lr 0.01",
-                   "global_batch": wl.batch, "input": "3x32x32 N(0,1)", "parallelism": "single GPU, all stages"},
+                   "global_batch": wl.batch, "input": "3x32x32 N(0,1)", "parallelism": "single GPU, all stages",
+                   "execution": "per-step psw_stage_step calls" if args.sequential else
+                                "pipelined psw_pipeline_run (forward of t+1 overlaps backward of t)"},
+        ("pipelined_value" if args.sequential else "sequential_value"): round(other_img_s, 2),
         "roofline": roof,
         "conv_mfma": conv,
         "kernel_ms_per_step": breakdown,

@@ -239,10 +239,38 @@ int psw_net_bind(psw_net *net, float *ring, float *momentum, float *grad, float 
  * t must equal the previous call's t + 1 (0 for the first call, or the value
  * set by psw_net_set_step), else PSW_ERR_STEP_ORDER.
  * x [batch,c0,h0,w0] and labels [batch] are device buffers; loss_out is one
- * device float; versions_out (host, [n_stages], may be NULL) receives r_s. */
+ * device float; versions_out (host, [n_stages], may be NULL) receives r_s.
+ * Streams: the forward pass and the data-gradient chain run on `stream`;
+ * the weight gradients and each stage's update (issued as soon as the
+ * backward pass is done with that stage) run on a stream of the library,
+ * joined back into `stream` before the call returns, so all work of the
+ * step is ordered before whatever the caller enqueues next on `stream`. */
 int psw_stage_step(psw_net *net, int64_t t, const int32_t *staleness, const float *lr, float mom,
                    float wd, int nesterov, const float *x, const int32_t *labels, float *loss_out,
                    int32_t *versions_out, void *stream);
+
+/* Pipelined execution of steps t0 .. t0+n_steps-1 (Sec. 3 mapped onto one
+ * GPU): the result is exactly that of n_steps psw_stage_step calls with
+ * the same arguments (same kernels, same order within every dependency),
+ * but the forward pass of mini-batch t+1 runs on a library stream
+ * concurrently with the backward pass of mini-batch t wherever the
+ * stale-weight schedule allows it: stage s's forward pass of step t only
+ * waits for the update that wrote its version t - d_s, so with d_s >= 1 it
+ * overlaps the backward pass of step t-1 (with every d_s = 0 nothing
+ * overlaps, as in plain SGD).  The step sets (activations, saved
+ * statistics) alternate between the net's arena and a second set bound with
+ * psw_net_bind_pipeline (psw_net_pipeline_bytes gives its size).
+ * staleness and lr: host arrays [n_steps][n_stages].  x: device array of
+ * n_batches mini-batches [n_batches][batch,c0,h0,w0]; step t0+i uses batch
+ * i mod n_batches (labels likewise [n_batches][batch]); every batch must
+ * stay unchanged until the call's work on `stream` is complete.  losses:
+ * device [n_steps].  versions_out: host [n_steps][n_stages] or NULL.  All
+ * work is joined into `stream` before the call returns. */
+int psw_net_pipeline_bytes(const psw_net *net, int64_t *bytes);
+int psw_net_bind_pipeline(psw_net *net, void *step_set, size_t bytes);
+int psw_pipeline_run(psw_net *net, int64_t t0, int n_steps, const int32_t *staleness, const float *lr,
+                     float mom, float wd, int nesterov, const float *x, const int32_t *labels,
+                     int n_batches, float *losses, int32_t *versions_out, void *stream);
 
 /* Set the next expected step (resume from a checkpoint whose ring holds
  * versions t-ring_depth+1 .. t in their slots v mod ring_depth). */
@@ -277,12 +305,13 @@ enum {
 int psw_net_plan(const psw_net *net, int64_t t, const int32_t *staleness, psw_launch *out, int cap,
                  int *n_out);
 
-/* Per-kernel timing of psw_stage_step (for measurement; off by default).
- * With profiling on, every kernel the library launches inside
- * psw_stage_step is bracketed by two HIP events recorded on the step's
- * stream, and tagged with the kind of launcher that issued it, the kernel's
- * name (template arguments as the compiler spells them, so the name matches
- * a kernel trace) and its algorithmic work.
+/* Per-kernel timing of psw_stage_step and psw_pipeline_run (for
+ * measurement; off by default).  With profiling on, every kernel the
+ * library launches there is launched with a start / stop event pair that the
+ * runtime stamps from the kernel's own dispatch (hipExtLaunchKernelGGL), and
+ * tagged with the kind of launcher that issued it, the kernel's name
+ * (template arguments as the compiler spells them, so the name matches a
+ * kernel trace) and its algorithmic work.
  * psw_net_profile(net, enable) switches profiling and clears the records;
  * the records are kept until the next psw_net_profile call.
  * psw_net_profile_only does the same but records only the launches of the

@@ -284,14 +284,26 @@ struct psw_net {
     std::vector<char> fused_bwd_now;        // per conv op: the fused dgrad ran in the current step
 
     std::vector<char> grad_accum;           // per op input slot: 0 overwrite, 1 accumulate (in0, in1)
-    size_t ws_off = 0, ws_bytes = 0, arena_bytes = 0;
-    size_t wsw_off = 0, wsw_bytes = 0;      // workspace of the backward-weight kernels (side stream)
+    size_t step_bytes = 0;                  // one step set (activations, saves, logits' gradient, forward ws)
+    size_t wsf_off = 0;                     // forward workspace, in the step set
+    size_t ws_off = 0, ws_bytes = 0, arena_bytes = 0;  // backward workspace, in the shared set
+    size_t wsw_off = 0, wsw_bytes = 0;      // workspace of the backward-weight kernels (shared set)
     // backward-weight kernels run on a second stream of the library, forked
     // from the caller's stream when a conv's output gradient is final and
     // joined before the update (created at bind, default priority)
     hipStream_t side = nullptr;
     std::vector<hipEvent_t> fork_ev;        // per op
+    std::vector<hipEvent_t> stage_ev;       // per stage: the chain is done with the stage
     hipEvent_t join_ev = nullptr;
+    // pipelined runs (psw_pipeline_run): forward stream, second step set,
+    // per-stage update events indexed by version mod upd_q, per step-set
+    // parity "backward done" / "weight stream done" events
+    hipStream_t fwd = nullptr;
+    char* step2 = nullptr;
+    int upd_q = 0;
+    std::vector<hipEvent_t> upd_ev;
+    hipEvent_t par_ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    hipEvent_t fdone_ev = nullptr, start_ev = nullptr;
     // bound memory
     float *ring = nullptr, *momentum = nullptr, *grad = nullptr, *run_mean = nullptr, *run_var = nullptr;
     char* arena = nullptr;
@@ -334,10 +346,19 @@ struct psw_net {
     {
         for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
         if (side) (void)hipStreamSynchronize(side);
+        if (fwd) (void)hipStreamSynchronize(fwd);
         for (hipEvent_t e : fork_ev)
             if (e) (void)hipEventDestroy(e);
-        if (join_ev) (void)hipEventDestroy(join_ev);
+        for (hipEvent_t e : stage_ev)
+            if (e) (void)hipEventDestroy(e);
+        for (hipEvent_t e : upd_ev)
+            if (e) (void)hipEventDestroy(e);
+        for (hipEvent_t e : par_ev)
+            if (e) (void)hipEventDestroy(e);
+        for (hipEvent_t e : {join_ev, fdone_ev, start_ev})
+            if (e) (void)hipEventDestroy(e);
         if (side) (void)hipStreamDestroy(side);
+        if (fwd) (void)hipStreamDestroy(fwd);
     }
     hipEvent_t next_event()
     {
@@ -470,6 +491,9 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
             written[o.in0] = 1;
         }
     }
+    for (int i = 0; i < n_layers; ++i)
+        if (net->ops[i].kind == PSW_OP_BN && net->ops[i].in0 == 0)
+            return fail(PSW_ERR_UNSUPPORTED, "op %d: BN directly on the input batch", i);
     // parameter and ring offsets
     int64_t fo = 0, ro = 0;
     for (int s = 0; s < n_stages; ++s) {
@@ -478,17 +502,19 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
         fo += net->stage_np[s];
         ro += net->stage_np[s] * net->ring_depth[s];
     }
-    // arena: activations, gradients, saved BN stats / argmax, workspace
+    // arena = [step set][shared set].  The step set holds what a step's
+    // forward pass writes and its backward pass reads: activations, saved BN
+    // statistics / max-pool argmax, the logits' gradient (written by the
+    // loss), and the forward workspace; a pipelined run alternates between
+    // two step sets (psw_net_bind_pipeline).  The shared set holds the other
+    // gradients, the backward workspace and the backward-weight workspace.
+    // Offsets of both sets are relative to the start of their set.
     size_t off = 0;
     net->act_off.assign(n_layers + 1, 0);
     net->grad_off.assign(n_layers + 1, 0);
     net->save_off.assign(n_layers, 0);
     for (int i = 1; i <= n_layers; ++i) {
         net->act_off[i] = off;
-        off = align256(off + (size_t)net->t[i].numel() * sizeof(float));
-    }
-    for (int i = 1; i <= n_layers; ++i) {
-        net->grad_off[i] = off;
         off = align256(off + (size_t)net->t[i].numel() * sizeof(float));
     }
     size_t wsw = 0;
@@ -528,13 +554,23 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
             ws = std::max(ws, psw::fc_bwd_ws_bytes(a.n, o.cin, o.cout));
         }
     }
-    net->ws_off = off;
+    net->grad_off[n_layers] = off;  // the logits' gradient: step set
+    off = align256(off + (size_t)net->t[n_layers].numel() * sizeof(float));
     net->ws_bytes = align256(ws);
+    net->wsf_off = off;
+    off += net->ws_bytes;
+    net->step_bytes = off;
+    off = 0;  // shared set
+    for (int i = 1; i < n_layers; ++i) {
+        net->grad_off[i] = off;
+        off = align256(off + (size_t)net->t[i].numel() * sizeof(float));
+    }
+    net->ws_off = off;
     off += net->ws_bytes;
     net->wsw_off = off;
     net->wsw_bytes = align256(wsw);
     off += net->wsw_bytes;
-    net->arena_bytes = off;
+    net->arena_bytes = net->step_bytes + off;
     g_err.clear();
     return PSW_OK;
 }
@@ -622,6 +658,11 @@ int psw_net_bind(psw_net* net, float* ring, float* momentum, float* grad, float*
             e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
             if (e != hipSuccess) return hip_check(e, "net_bind: events");
         }
+        net->stage_ev.assign(net->S, nullptr);
+        for (auto& ev : net->stage_ev) {
+            e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+            if (e != hipSuccess) return hip_check(e, "net_bind: events");
+        }
         e = hipEventCreateWithFlags(&net->join_ev, hipEventDisableTiming);
         if (e != hipSuccess) return hip_check(e, "net_bind: events");
     }
@@ -703,11 +744,296 @@ int psw_net_plan(const psw_net* net, int64_t t, const int32_t* staleness, psw_la
             rec(i, PSW_PLAN_FC_BWD, s, t);
             break;
         }
+        // a stage is updated (version t -> t+1) as soon as the backward pass is done with it
+        if (i == net->stage_begin[s]) rec(-1, PSW_PLAN_SGD, s, t);
     }
-    for (int s = 0; s < net->S; ++s) rec(-1, PSW_PLAN_SGD, s, t);
     *n_out = n;
     return PSW_OK;
 }
+
+}  // extern "C"
+
+namespace {
+
+// One step's inputs and where its step set lives.
+struct StepIO {
+    int64_t t;
+    std::vector<int64_t> rv;  // forward weight version per stage
+    char* P;                  // step set (activations, saves, logits' gradient, forward workspace)
+    const float* x;
+    const int32_t* labels;
+    float* loss_out;
+    const float* lr;          // per stage
+    float mom, wd;
+    int nesterov;
+};
+
+struct Issue {
+    psw_net* net;
+    const StepIO& io;
+    hipError_t e = hipSuccess;
+    const char* what = "";
+    char* A() const { return io.P; }
+    float* act(int id) const { return id == 0 ? (float*)io.x : (float*)(io.P + net->act_off[id]); }
+    float* grd(int id) const
+    {
+        const int L = (int)net->ops.size();
+        return id == L ? (float*)(io.P + net->grad_off[id]) : (float*)(net->arena + net->step_bytes + net->grad_off[id]);
+    }
+    float* save(int i) const { return (float*)(io.P + net->save_off[i]); }
+    void* wsf() const { return io.P + net->wsf_off; }
+    void* wsb() const { return net->arena + net->step_bytes + net->ws_off; }
+    void* wsw() const { return net->arena + net->step_bytes + net->wsw_off; }
+    const float* wfwd(int i) const
+    {
+        const int s = net->stage_of[i];
+        return slot_ptr(net, s, io.rv[s]) + net->poff[i];
+    }
+    const float* wcur(int i) const { return slot_ptr(net, net->stage_of[i], io.t) + net->poff[i]; }
+    float* gptr(int i) const { return net->grad + net->flat_off[net->stage_of[i]] + net->poff[i]; }
+};
+
+#define PSW_TRY(expr, w)          \
+    do {                          \
+        is.e = (expr);            \
+        if (is.e != hipSuccess) { \
+            is.what = (w);        \
+            return is.e;          \
+        }                         \
+    } while (0)
+
+// Forward pass and loss of one step on stream sf.  before_stage(s) runs
+// before the first operation of stage s is issued (the pipelined run makes
+// sf wait there for the update that produced the stage's version).
+template <typename BeforeStage>
+hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
+{
+    psw_net* net = is.net;
+    const int L = (int)net->ops.size();
+    const int bf16 = net->prec == PSW_BF16;
+    int& kind = net->rec.kind;
+    void* ws = is.wsf();
+    const size_t wsb = net->ws_bytes;
+    hipError_t e = hipSuccess;
+    for (int i = 0; i < L; ++i) {
+        if (i == 0 || net->stage_of[i] != net->stage_of[i - 1]) PSW_TRY(before_stage(net->stage_of[i]), "stage wait");
+        const psw_layer& o = net->ops[i];
+        const Tensor a = net->t[o.in0];
+        const float* W = is.wfwd(i);
+        switch (o.kind) {
+        case PSW_OP_CONV: {
+            psw::ConvShape cs;
+            check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, net->prec, &cs);
+            const float* b = (o.flags & PSW_F_BIAS) ? W + (int64_t)o.cout * o.cin * o.k * o.k : nullptr;
+            kind = PSW_PROF_CONV_FWD;
+            net->fused_now[i] = 0;
+            if (net->fuse_stats[i]) {  // the next op's BN statistics come out of this conv
+                psw::BnStatsFuse bn{(float*)ws};
+                e = psw::conv_fwd_bnstats(cs, is.act(o.in0), W, is.act(i + 1), bn, wsb / sizeof(float), sf);
+                if (e == hipSuccess)
+                    net->fused_now[i] = 1;
+                else if (e != hipErrorNotSupported)  // not supported: nothing launched, unfused path below
+                    PSW_TRY(e, "conv_fwd_bnstats");
+            }
+            if (!net->fused_now[i])
+                PSW_TRY(psw::conv_fwd(cs, is.act(o.in0), W, b, (o.flags & PSW_F_RELU) != 0, is.act(i + 1), bf16, sf),
+                        "conv_fwd");
+            break;
+        }
+        case PSW_OP_BN: {
+            const Tensor r = o.in1 >= 0 ? net->t[o.in1] : Tensor{0, 0, 0, 0};
+            float* save = is.save(i);
+            float* rm = net->run_mean ? net->run_mean + net->bn_off[i] : nullptr;
+            float* rvv = net->run_var ? net->run_var + net->bn_off[i] : nullptr;
+            kind = PSW_PROF_BN_FWD;
+            if (i > 0 && net->fused_now[i - 1]) {  // per-tile statistics written by the conv into ws
+                const psw_layer& cv = net->ops[i - 1];
+                const Tensor ci = net->t[cv.in0];
+                psw::ConvShape ccs;
+                check_conv(ci.n, ci.c, ci.h, ci.w, cv.cout, cv.k, cv.k, cv.stride, cv.pad, net->prec, &ccs);
+                const int T = psw::conv_fwd_bnstats_tiles(ccs);
+                const int P = a.n * a.h * a.w / T;
+                e = psw::bn_apply_from_partials(a.n, a.c, a.h, a.w, is.act(o.in0), (const float*)ws, T, P, W,
+                                                W + o.cin, o.in1 >= 0 ? is.act(o.in1) : nullptr, r.c, r.h, r.w,
+                                                (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, is.act(i + 1), save,
+                                                save + o.cin, save + 2 * o.cin, rm, rvv, sf);
+                if (e == hipSuccess) break;
+                if (e != hipErrorNotSupported) PSW_TRY(e, "bn_apply");
+                // not supported: nothing launched, the statistics are recomputed below
+            }
+            PSW_TRY(psw::bn_fwd(a.n, a.c, a.h, a.w, is.act(o.in0), W, W + o.cin, o.in1 >= 0 ? is.act(o.in1) : nullptr,
+                                r.c, r.h, r.w, (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, is.act(i + 1), save,
+                                save + o.cin, rm, rvv, ws, wsb, sf, save + 2 * o.cin),
+                    "bn_fwd");
+            break;
+        }
+        case PSW_OP_MAXPOOL:
+            kind = PSW_PROF_POOL;
+            PSW_TRY(psw::maxpool_fwd(a.n, a.c, a.h, a.w, o.k, o.stride, is.act(o.in0), is.act(i + 1),
+                                     (int32_t*)is.save(i), sf),
+                    "maxpool_fwd");
+            break;
+        case PSW_OP_GAVG:
+            kind = PSW_PROF_POOL;
+            PSW_TRY(psw::gavgpool_fwd(a.n, a.c, a.h, a.w, is.act(o.in0), is.act(i + 1), sf), "gavgpool_fwd");
+            break;
+        case PSW_OP_FC: {
+            const float* b = (o.flags & PSW_F_BIAS) ? W + (int64_t)o.cout * o.cin : nullptr;
+            kind = PSW_PROF_FC;
+            PSW_TRY(psw::fc_fwd(a.n, o.cin, o.cout, is.act(o.in0), W, b, (o.flags & PSW_F_RELU) != 0, is.act(i + 1),
+                                bf16, sf),
+                    "fc_fwd");
+            break;
+        }
+        }
+    }
+    const Tensor lg = net->t[L];
+    kind = PSW_PROF_LOSS;
+    PSW_TRY(psw::softmax_xent(lg.n, lg.c, is.act(L), is.io.labels, is.io.loss_out, is.grd(L), sf), "softmax_xent");
+    return hipSuccess;
+}
+
+// Backward pass and updates of one step: the data-gradient chain on sb; the
+// weight gradient of every conv forked to sw (it shares only the step's
+// activations with the chain); when the chain has finished stage s, sw waits
+// for it and writes version t+1 of stage s (all of the stage's parameter
+// gradients are then complete, and nothing later in the step reads the
+// stage's version t), then after_update(s) runs with sw current.
+template <typename AfterUpdate>
+hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, AfterUpdate after_update)
+{
+    psw_net* net = is.net;
+    const StepIO& io = is.io;
+    const int L = (int)net->ops.size();
+    const int bf16 = net->prec == PSW_BF16;
+    int& kind = net->rec.kind;
+    void* ws = is.wsb();
+    const size_t wsb = net->ws_bytes;
+    void* wsw = is.wsw();
+    const size_t wswb = net->wsw_bytes;
+    hipError_t e = hipSuccess;
+    for (int i = L - 1; i >= 0; --i) {
+        const psw_layer& o = net->ops[i];
+        const Tensor a = net->t[o.in0];
+        const Tensor y = net->t[i + 1];
+        float* g = is.grd(i + 1);
+        float* din = o.in0 > 0 ? is.grd(o.in0) : nullptr;
+        const int acc0 = net->grad_accum[2 * i];
+        switch (o.kind) {
+        case PSW_OP_CONV: {
+            psw::ConvShape cs;
+            check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, net->prec, &cs);
+            kind = PSW_PROF_OTHER;
+            if (o.flags & PSW_F_RELU) PSW_TRY(psw::relu_mask(y.numel(), is.act(i + 1), g, sb), "relu_mask");
+            float* dw = is.gptr(i);
+            float* db = (o.flags & PSW_F_BIAS) ? dw + (int64_t)o.cout * o.cin * o.k * o.k : nullptr;
+            kind = PSW_PROF_CONV_BWD_WEIGHT;
+            // fork: the weight gradient runs beside the data-gradient chain
+            PSW_TRY(hipEventRecord(net->fork_ev[i], sb), "fork");
+            PSW_TRY(hipStreamWaitEvent(sw, net->fork_ev[i], 0), "fork");
+            PSW_TRY(psw::conv_bwd_weight(cs, is.act(o.in0), g, dw, db, bf16, wsw, wswb, sw), "conv_bwd_weight");
+            kind = PSW_PROF_CONV_BWD_DATA;
+            net->fused_bwd_now[i] = 0;
+            if (din && net->fuse_bwd[i]) {  // BN op i-1's backward sums out of this dgrad
+                const psw_layer& bo = net->ops[i - 1];
+                const float* bsave = is.save(i - 1);
+                psw::BnBwdFuse bnb{(float*)ws, is.act(i), is.act(bo.in0), bsave, bsave + bo.cin,
+                                   (bo.flags & PSW_F_RELU) != 0};
+                if (bo.in1 < 0) {  // no residual: the ReLU mask comes from y and the forward's scale / shift
+                    bnb.scale = bsave + 2 * bo.cin;
+                    bnb.shift = bsave + 3 * bo.cin;
+                }
+                e = psw::conv_bwd_data_bnsums(cs, is.wcur(i), g, din, acc0, bnb, sb);
+                if (e == hipSuccess)
+                    net->fused_bwd_now[i] = 1;
+                else if (e != hipErrorNotSupported)  // not supported: nothing launched, unfused path below
+                    PSW_TRY(e, "conv_bwd_data_bnsums");
+            }
+            if (din && !net->fused_bwd_now[i])
+                PSW_TRY(psw::conv_bwd_data(cs, is.wcur(i), g, din, acc0, bf16, sb), "conv_bwd_data");
+            break;
+        }
+        case PSW_OP_BN: {
+            const float* save = is.save(i);
+            const Tensor r = o.in1 >= 0 ? net->t[o.in1] : Tensor{0, 0, 0, 0};
+            float* dres = o.in1 > 0 ? is.grd(o.in1) : nullptr;
+            float* dg = is.gptr(i);
+            if (!din) {  // rejected when the net is created
+                is.what = "BN directly on the input batch";
+                return hipErrorInvalidValue;
+            }
+            kind = PSW_PROF_BN_BWD;
+            bool done = false;
+            if (i + 1 < L && net->fused_bwd_now[i + 1]) {  // sums written by the next conv's dgrad into ws
+                const psw_layer& cv = net->ops[i + 1];
+                psw::ConvShape ccs;
+                check_conv(y.n, y.c, y.h, y.w, cv.cout, cv.k, cv.k, cv.stride, cv.pad, net->prec, &ccs);
+                const int T = psw::conv_bwd_data_bnsums_tiles(ccs);
+                // without a residual the ReLU mask comes from y and the forward's scale / shift
+                const float* scale = o.in1 < 0 ? save + 2 * o.cin : nullptr;
+                e = psw::bn_bwd_from_partials(a.n, a.c, a.h, a.w, g, is.act(i + 1), is.act(o.in0), is.wcur(i), save,
+                                              save + o.cin, scale, (const float*)ws, T, (o.flags & PSW_F_RELU) != 0,
+                                              din, dg, dg + o.cin, dres, r.c, r.h, r.w, net->grad_accum[2 * i + 1], sb);
+                if (e == hipSuccess)
+                    done = true;
+                else if (e != hipErrorNotSupported)  // not supported: nothing launched, sums recomputed below
+                    PSW_TRY(e, "bn_bwd_from_partials");
+            }
+            if (!done)
+                PSW_TRY(psw::bn_bwd(a.n, a.c, a.h, a.w, g, is.act(i + 1), is.act(o.in0), is.wcur(i), save,
+                                    save + o.cin, (o.flags & PSW_F_RELU) != 0, din, dg, dg + o.cin, dres, r.c, r.h,
+                                    r.w, net->grad_accum[2 * i + 1], ws, wsb, sb),
+                        "bn_bwd");
+            break;
+        }
+        case PSW_OP_MAXPOOL:
+            kind = PSW_PROF_POOL;
+            if (din)
+                PSW_TRY(psw::maxpool_bwd(a.n, a.c, a.h, a.w, o.k, o.stride, g, (const int32_t*)is.save(i), din, acc0,
+                                         sb),
+                        "maxpool_bwd");
+            break;
+        case PSW_OP_GAVG:
+            kind = PSW_PROF_POOL;
+            if (din) PSW_TRY(psw::gavgpool_bwd(a.n, a.c, a.h, a.w, g, din, acc0, sb), "gavgpool_bwd");
+            break;
+        case PSW_OP_FC: {
+            kind = PSW_PROF_OTHER;
+            if (o.flags & PSW_F_RELU) PSW_TRY(psw::relu_mask(y.numel(), is.act(i + 1), g, sb), "relu_mask");
+            float* dw = is.gptr(i);
+            float* db = (o.flags & PSW_F_BIAS) ? dw + (int64_t)o.cout * o.cin : nullptr;
+            kind = PSW_PROF_FC;
+            PSW_TRY(psw::fc_bwd(a.n, o.cin, o.cout, is.act(o.in0), is.wcur(i), g, din, acc0, dw, db, bf16, ws, wsb,
+                                sb),
+                    "fc_bwd");
+            break;
+        }
+        }
+        const int s = net->stage_of[i];
+        if (i == net->stage_begin[s]) {  // the chain is done with stage s: update it on sw
+            PSW_TRY(hipEventRecord(net->stage_ev[s], sb), "stage join");
+            PSW_TRY(hipStreamWaitEvent(sw, net->stage_ev[s], 0), "stage join");
+            kind = PSW_PROF_SGD;
+            PSW_TRY(psw::sgd_momentum(net->stage_np[s], slot_ptr(net, s, io.t), slot_ptr(net, s, io.t + 1),
+                                      net->momentum + net->flat_off[s], net->grad + net->flat_off[s], io.lr[s], io.mom,
+                                      io.wd, io.nesterov, sw),
+                    "sgd");
+            PSW_TRY(after_update(s), "update event");
+        }
+    }
+    return hipSuccess;
+}
+
+#undef PSW_TRY
+
+struct RecorderScope {
+    explicit RecorderScope(psw::KernelRecorder* r) { psw::kernel_recorder() = r; }
+    ~RecorderScope() { psw::kernel_recorder() = nullptr; }
+};
+
+}  // namespace
+
+extern "C" {
 
 int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const float* lr, float mom, float wd,
                    int nesterov, const float* x, const int32_t* labels, float* loss_out, int32_t* versions_out,
@@ -721,237 +1047,155 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
     if (t != net->next_t)
         return fail(PSW_ERR_STEP_ORDER, "stage_step: expected t = %lld, got %lld", (long long)net->next_t, (long long)t);
     hipStream_t st = S(stream);
-    const int L = (int)net->ops.size();
-    const int bf16 = net->prec == PSW_BF16;
-    char* A = net->arena;
-    auto act = [&](int id) -> float* { return id == 0 ? (float*)x : (float*)(A + net->act_off[id]); };
-    auto grd = [&](int id) -> float* { return (float*)(A + net->grad_off[id]); };
-    void* ws = A + net->ws_off;
-    const size_t wsb = net->ws_bytes;
-    void* wsw = A + net->wsw_off;
-    const size_t wswb = net->wsw_bytes;
-    // side-stream work is always joined back into the caller's stream, also
-    // when a launcher fails part way (the error is reported all the same)
-    struct Join {
-        hipStream_t main, side;
-        hipEvent_t ev;
-        bool forked = false;
-        hipError_t join()
-        {
-            if (!forked) return hipSuccess;
-            forked = false;
-            hipError_t e = hipEventRecord(ev, side);
-            if (e == hipSuccess) e = hipStreamWaitEvent(main, ev, 0);
-            return e;
-        }
-        ~Join() { (void)join(); }
-    } joiner{st, net->side, net->join_ev};
-    bool& forked = joiner.forked;
-    std::vector<int64_t> rv(net->S);
-    for (int s = 0; s < net->S; ++s) rv[s] = fwd_version(t, staleness[s]);
-    auto wfwd = [&](int i) { return slot_ptr(net, net->stage_of[i], rv[net->stage_of[i]]) + net->poff[i]; };
-    auto wcur = [&](int i) { return slot_ptr(net, net->stage_of[i], t) + net->poff[i]; };
-    auto gptr = [&](int i) { return net->grad + net->flat_off[net->stage_of[i]] + net->poff[i]; };
-    hipError_t e = hipSuccess;
-    // kind of the launcher being issued, for psw_net_profile; with profiling
-    // on, every kernel launched below is timed by net->rec
-    int& kind = net->rec.kind;
-    kind = PSW_PROF_OTHER;
-    struct RecorderScope {
-        explicit RecorderScope(psw::KernelRecorder* r) { psw::kernel_recorder() = r; }
-        ~RecorderScope() { psw::kernel_recorder() = nullptr; }
-    } rec_scope(net->profiling ? &net->rec : nullptr);
-#define PSW_TRY(expr, what)                                                   \
-    do {                                                                      \
-        e = (expr);                                                           \
-        if (e != hipSuccess) return hip_check(e, what);                       \
-    } while (0)
-
-    // ---- forward: every stage with its (possibly stale) version r_s ----
-    for (int i = 0; i < L; ++i) {
-        const psw_layer& o = net->ops[i];
-        const Tensor a = net->t[o.in0];
-        const float* W = wfwd(i);
-        switch (o.kind) {
-        case PSW_OP_CONV: {
-            psw::ConvShape cs;
-            check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, net->prec, &cs);
-            const float* b = (o.flags & PSW_F_BIAS) ? W + (int64_t)o.cout * o.cin * o.k * o.k : nullptr;
-            kind = PSW_PROF_CONV_FWD;
-            net->fused_now[i] = 0;
-            if (net->fuse_stats[i]) {  // the next op's BN statistics come out of this conv
-                psw::BnStatsFuse bn{(float*)ws};
-                e = psw::conv_fwd_bnstats(cs, act(o.in0), W, act(i + 1), bn, wsb / sizeof(float), st);
-                if (e == hipSuccess)
-                    net->fused_now[i] = 1;
-                else if (e != hipErrorNotSupported)  // not supported: nothing launched, unfused path below
-                    return hip_check(e, "conv_fwd_bnstats");
-            }
-            if (!net->fused_now[i]) {
-                PSW_TRY(psw::conv_fwd(cs, act(o.in0), W, b, (o.flags & PSW_F_RELU) != 0, act(i + 1), bf16, st),
-                        "conv_fwd");
-            }
-            break;
-        }
-        case PSW_OP_BN: {
-            const Tensor r = o.in1 >= 0 ? net->t[o.in1] : Tensor{0, 0, 0, 0};
-            float* save = (float*)(A + net->save_off[i]);
-            float* rm = net->run_mean ? net->run_mean + net->bn_off[i] : nullptr;
-            float* rvv = net->run_var ? net->run_var + net->bn_off[i] : nullptr;
-            kind = PSW_PROF_BN_FWD;
-            if (i > 0 && net->fused_now[i - 1]) {  // per-tile statistics written by the conv into ws
-                const psw_layer& cv = net->ops[i - 1];
-                const Tensor ci = net->t[cv.in0];
-                psw::ConvShape ccs;
-                check_conv(ci.n, ci.c, ci.h, ci.w, cv.cout, cv.k, cv.k, cv.stride, cv.pad, net->prec, &ccs);
-                const int T = psw::conv_fwd_bnstats_tiles(ccs);
-                const int P = a.n * a.h * a.w / T;
-                e = psw::bn_apply_from_partials(a.n, a.c, a.h, a.w, act(o.in0), (const float*)ws, T, P, W, W + o.cin,
-                                                o.in1 >= 0 ? act(o.in1) : nullptr, r.c, r.h, r.w,
-                                                (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, act(i + 1), save,
-                                                save + o.cin, save + 2 * o.cin, rm, rvv, st);
-                if (e == hipSuccess) break;
-                if (e != hipErrorNotSupported) return hip_check(e, "bn_apply");
-                // not supported: nothing launched, the statistics are recomputed below
-            }
-            PSW_TRY(psw::bn_fwd(a.n, a.c, a.h, a.w, act(o.in0), W, W + o.cin, o.in1 >= 0 ? act(o.in1) : nullptr, r.c,
-                                r.h, r.w, (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, act(i + 1), save, save + o.cin, rm,
-                                rvv, ws, wsb, st, save + 2 * o.cin),
-                    "bn_fwd");
-            break;
-        }
-        case PSW_OP_MAXPOOL:
-            kind = PSW_PROF_POOL;
-            PSW_TRY(psw::maxpool_fwd(a.n, a.c, a.h, a.w, o.k, o.stride, act(o.in0), act(i + 1),
-                                     (int32_t*)(A + net->save_off[i]), st),
-                    "maxpool_fwd");
-            break;
-        case PSW_OP_GAVG:
-            kind = PSW_PROF_POOL;
-            PSW_TRY(psw::gavgpool_fwd(a.n, a.c, a.h, a.w, act(o.in0), act(i + 1), st), "gavgpool_fwd");
-            break;
-        case PSW_OP_FC: {
-            const float* b = (o.flags & PSW_F_BIAS) ? W + (int64_t)o.cout * o.cin : nullptr;
-            kind = PSW_PROF_FC;
-            PSW_TRY(psw::fc_fwd(a.n, o.cin, o.cout, act(o.in0), W, b, (o.flags & PSW_F_RELU) != 0, act(i + 1), bf16, st),
-                    "fc_fwd");
-            break;
-        }
-        }
-    }
-    // ---- loss ----
-    const Tensor lg = net->t[L];
-    kind = PSW_PROF_LOSS;
-    PSW_TRY(psw::softmax_xent(lg.n, lg.c, act(L), labels, loss_out, grd(L), st), "softmax_xent");
-    // ---- backward: weight grads from saved activations, data grads with version t ----
-    for (int i = L - 1; i >= 0; --i) {
-        const psw_layer& o = net->ops[i];
-        const Tensor a = net->t[o.in0];
-        const Tensor y = net->t[i + 1];
-        float* g = grd(i + 1);
-        float* din = o.in0 > 0 ? grd(o.in0) : nullptr;
-        const int acc0 = net->grad_accum[2 * i];
-        switch (o.kind) {
-        case PSW_OP_CONV: {
-            psw::ConvShape cs;
-            check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, net->prec, &cs);
-            kind = PSW_PROF_OTHER;
-            if (o.flags & PSW_F_RELU) PSW_TRY(psw::relu_mask(y.numel(), act(i + 1), g, st), "relu_mask");
-            float* dw = gptr(i);
-            float* db = (o.flags & PSW_F_BIAS) ? dw + (int64_t)o.cout * o.cin * o.k * o.k : nullptr;
-            kind = PSW_PROF_CONV_BWD_WEIGHT;
-            // fork: the weight gradient runs beside the data-gradient chain
-            PSW_TRY(hipEventRecord(net->fork_ev[i], st), "fork");
-            PSW_TRY(hipStreamWaitEvent(net->side, net->fork_ev[i], 0), "fork");
-            forked = true;
-            PSW_TRY(psw::conv_bwd_weight(cs, act(o.in0), g, dw, db, bf16, wsw, wswb, net->side), "conv_bwd_weight");
-            kind = PSW_PROF_CONV_BWD_DATA;
-            net->fused_bwd_now[i] = 0;
-            if (din && net->fuse_bwd[i]) {  // BN op i-1's backward sums out of this dgrad
-                const psw_layer& bo = net->ops[i - 1];
-                const float* bsave = (const float*)(A + net->save_off[i - 1]);
-                psw::BnBwdFuse bnb{(float*)ws, act(i), act(bo.in0), bsave, bsave + bo.cin,
-                                   (bo.flags & PSW_F_RELU) != 0};
-                if (bo.in1 < 0) {  // no residual: the ReLU mask comes from y and the forward's scale / shift
-                    bnb.scale = bsave + 2 * bo.cin;
-                    bnb.shift = bsave + 3 * bo.cin;
-                }
-                e = psw::conv_bwd_data_bnsums(cs, wcur(i), g, din, acc0, bnb, st);
-                if (e == hipSuccess) {
-                    net->fused_bwd_now[i] = 1;
-                    break;
-                }
-                if (e != hipErrorNotSupported) return hip_check(e, "conv_bwd_data_bnsums");
-                // not supported: nothing launched, unfused path below
-            }
-            if (din) PSW_TRY(psw::conv_bwd_data(cs, wcur(i), g, din, acc0, bf16, st), "conv_bwd_data");
-            break;
-        }
-        case PSW_OP_BN: {
-            const float* save = (const float*)(A + net->save_off[i]);
-            const Tensor r = o.in1 >= 0 ? net->t[o.in1] : Tensor{0, 0, 0, 0};
-            float* dres = o.in1 > 0 ? grd(o.in1) : nullptr;
-            float* dg = gptr(i);
-            if (!din) return fail(PSW_ERR_UNSUPPORTED, "op %d: BN directly on the input batch", i);
-            kind = PSW_PROF_BN_BWD;
-            if (i + 1 < L && net->fused_bwd_now[i + 1]) {  // sums written by the next conv's dgrad into ws
-                const psw_layer& cv = net->ops[i + 1];
-                psw::ConvShape ccs;
-                check_conv(y.n, y.c, y.h, y.w, cv.cout, cv.k, cv.k, cv.stride, cv.pad, net->prec, &ccs);
-                const int T = psw::conv_bwd_data_bnsums_tiles(ccs);
-                // without a residual the ReLU mask comes from y and the forward's scale / shift
-                const float* scale = o.in1 < 0 ? save + 2 * o.cin : nullptr;
-                e = psw::bn_bwd_from_partials(a.n, a.c, a.h, a.w, g, act(i + 1), act(o.in0), wcur(i), save,
-                                              save + o.cin, scale, (const float*)ws, T, (o.flags & PSW_F_RELU) != 0,
-                                              din, dg, dg + o.cin, dres, r.c, r.h, r.w, net->grad_accum[2 * i + 1], st);
-                if (e == hipSuccess) break;
-                if (e != hipErrorNotSupported) return hip_check(e, "bn_bwd_from_partials");
-                // not supported: nothing launched, the sums are recomputed below
-            }
-            PSW_TRY(psw::bn_bwd(a.n, a.c, a.h, a.w, g, act(i + 1), act(o.in0), wcur(i), save, save + o.cin,
-                                (o.flags & PSW_F_RELU) != 0, din, dg, dg + o.cin, dres, r.c, r.h, r.w,
-                                net->grad_accum[2 * i + 1], ws, wsb, st),
-                    "bn_bwd");
-            break;
-        }
-        case PSW_OP_MAXPOOL:
-            kind = PSW_PROF_POOL;
-            if (din)
-                PSW_TRY(psw::maxpool_bwd(a.n, a.c, a.h, a.w, o.k, o.stride, g, (const int32_t*)(A + net->save_off[i]),
-                                         din, acc0, st),
-                        "maxpool_bwd");
-            break;
-        case PSW_OP_GAVG:
-            kind = PSW_PROF_POOL;
-            if (din) PSW_TRY(psw::gavgpool_bwd(a.n, a.c, a.h, a.w, g, din, acc0, st), "gavgpool_bwd");
-            break;
-        case PSW_OP_FC: {
-            kind = PSW_PROF_OTHER;
-            if (o.flags & PSW_F_RELU) PSW_TRY(psw::relu_mask(y.numel(), act(i + 1), g, st), "relu_mask");
-            float* dw = gptr(i);
-            float* db = (o.flags & PSW_F_BIAS) ? dw + (int64_t)o.cout * o.cin : nullptr;
-            kind = PSW_PROF_FC;
-            PSW_TRY(psw::fc_bwd(a.n, o.cin, o.cout, act(o.in0), wcur(i), g, din, acc0, dw, db, bf16, ws, wsb, st),
-                    "fc_bwd");
-            break;
-        }
-        }
-    }
-    // ---- join: every weight gradient is complete before the update ----
-    PSW_TRY(joiner.join(), "join");
-    // ---- update: version t+1 of every stage ----
-    for (int s = 0; s < net->S; ++s) {
-        const float* win = slot_ptr(net, s, t);
-        float* wout = slot_ptr(net, s, t + 1);
-        kind = PSW_PROF_SGD;
-        PSW_TRY(psw::sgd_momentum(net->stage_np[s], win, wout, net->momentum + net->flat_off[s],
-                                  net->grad + net->flat_off[s], lr[s], mom, wd, nesterov, st),
-                "sgd");
-    }
-#undef PSW_TRY
+    StepIO io{t, std::vector<int64_t>(net->S), net->arena, x, labels, loss_out, lr, mom, wd, nesterov};
+    for (int s = 0; s < net->S; ++s) io.rv[s] = fwd_version(t, staleness[s]);
+    Issue is{net, io};
+    net->rec.kind = PSW_PROF_OTHER;
+    RecorderScope rec_scope(net->profiling ? &net->rec : nullptr);
+    // forward and the data-gradient chain on the caller's stream; weight
+    // gradients and updates on the side stream, joined back at the end (also
+    // when a launcher fails part way)
+    hipError_t e = issue_forward(is, st, [](int) { return hipSuccess; });
+    if (e == hipSuccess) e = issue_backward(is, st, net->side, [](int) { return hipSuccess; });
+    hipError_t ej = hipEventRecord(net->join_ev, net->side);
+    if (ej == hipSuccess) ej = hipStreamWaitEvent(st, net->join_ev, 0);
+    if (e != hipSuccess) return hip_check(e, is.what);
+    if (ej != hipSuccess) return hip_check(ej, "join");
     if (versions_out)
-        for (int s = 0; s < net->S; ++s) versions_out[s] = (int32_t)rv[s];
+        for (int s = 0; s < net->S; ++s) versions_out[s] = (int32_t)io.rv[s];
     net->next_t = t + 1;
+    return PSW_OK;
+}
+
+int psw_net_pipeline_bytes(const psw_net* net, int64_t* bytes)
+{
+    if (!net || !bytes) return fail(PSW_ERR_NULL, "net_pipeline_bytes: required pointer is NULL");
+    *bytes = (int64_t)net->step_bytes;
+    return PSW_OK;
+}
+
+int psw_net_bind_pipeline(psw_net* net, void* step_set, size_t bytes)
+{
+    if (!net || !step_set) return fail(PSW_ERR_NULL, "net_bind_pipeline: required pointer is NULL");
+    if (!net->bound) return fail(PSW_ERR_STATE, "net_bind_pipeline: bind the net first");
+    if (bytes < net->step_bytes)
+        return fail(PSW_ERR_WORKSPACE, "net_bind_pipeline: %zu < %zu bytes", bytes, net->step_bytes);
+    if (((uintptr_t)step_set) % 256 != 0) return fail(PSW_ERR_SHAPE, "net_bind_pipeline: must be 256-byte aligned");
+    if (!net->fwd) {
+        hipError_t e = hipStreamCreateWithFlags(&net->fwd, hipStreamNonBlocking);
+        if (e != hipSuccess) {
+            net->fwd = nullptr;
+            return hip_check(e, "net_bind_pipeline: forward stream");
+        }
+        int D = 1;
+        for (int d : net->ring_depth) D = std::max(D, d);
+        net->upd_q = D + 1;
+        net->upd_ev.assign((size_t)net->S * net->upd_q, nullptr);
+        std::vector<hipEvent_t*> evs;
+        for (auto& ev : net->upd_ev) evs.push_back(&ev);
+        for (auto& ev : net->par_ev) evs.push_back(&ev);
+        evs.push_back(&net->fdone_ev);
+        evs.push_back(&net->start_ev);
+        for (hipEvent_t* ev : evs) {
+            e = hipEventCreateWithFlags(ev, hipEventDisableTiming);
+            if (e != hipSuccess) return hip_check(e, "net_bind_pipeline: events");
+        }
+    }
+    net->step2 = (char*)step_set;
+    return PSW_OK;
+}
+
+int psw_pipeline_run(psw_net* net, int64_t t0, int n_steps, const int32_t* staleness, const float* lr, float mom,
+                     float wd, int nesterov, const float* x, const int32_t* labels, int n_batches, float* losses,
+                     int32_t* versions_out, void* stream)
+{
+    if (!net) return fail(PSW_ERR_NULL, "pipeline_run: net is NULL");
+    if (!net->bound || !net->step2) return fail(PSW_ERR_STATE, "pipeline_run: bind the net and its pipeline set first");
+    if (!staleness || !lr || !x || !labels || !losses) return fail(PSW_ERR_NULL, "pipeline_run: required pointer is NULL");
+    if (n_steps < 0 || n_batches < 1) return fail(PSW_ERR_SHAPE, "pipeline_run: n_steps >= 0 and n_batches >= 1");
+    if (t0 != net->next_t)
+        return fail(PSW_ERR_STEP_ORDER, "pipeline_run: expected t0 = %lld, got %lld", (long long)net->next_t,
+                    (long long)t0);
+    for (int i = 0; i < n_steps; ++i) {
+        int rc = check_staleness(net, t0 + i, staleness + (size_t)i * net->S);
+        if (rc) return rc;
+    }
+    if (n_steps == 0) return PSW_OK;
+    hipStream_t sb = S(stream), sf = net->fwd, sw = net->side;
+    const Tensor in = net->t[0];
+    const size_t xs = (size_t)in.numel();
+    const int S_ = net->S, Q = net->upd_q;
+    net->rec.kind = PSW_PROF_OTHER;
+    RecorderScope rec_scope(net->profiling ? &net->rec : nullptr);
+    // everything the caller enqueued before (inputs, earlier versions) comes first
+    hipError_t e = hipEventRecord(net->start_ev, sb);
+    if (e == hipSuccess) e = hipStreamWaitEvent(sf, net->start_ev, 0);
+    if (e == hipSuccess) e = hipStreamWaitEvent(sw, net->start_ev, 0);
+    if (e != hipSuccess) return hip_check(e, "pipeline_run: start");
+    const char* what = "";
+    int64_t issued = 0;
+    for (int i = 0; i < n_steps && e == hipSuccess; ++i) {
+        const int64_t t = t0 + i;
+        const int p = (int)(t & 1);
+        hipEvent_t bdone = net->par_ev[2 * p], wdone = net->par_ev[2 * p + 1];
+        StepIO io{t, std::vector<int64_t>(S_), p ? net->step2 : net->arena, x + (size_t)(i % n_batches) * xs,
+                  labels + (size_t)(i % n_batches) * in.n, losses + i, lr + (size_t)i * S_, mom, wd, nesterov};
+        for (int s = 0; s < S_; ++s) io.rv[s] = fwd_version(t, staleness[(size_t)i * S_ + s]);
+        Issue is{net, io};
+        // forward of t: its step set is free once step t-2 is done with it
+        if (i >= 2) {
+            e = hipStreamWaitEvent(sf, bdone, 0);
+            if (e == hipSuccess) e = hipStreamWaitEvent(sf, wdone, 0);
+            if (e != hipSuccess) {
+                what = "pipeline_run: step set";
+                break;
+            }
+        }
+        // stage s reads version r = rv[s]; wait for the update that wrote it
+        // when it was written inside this run
+        e = issue_forward(is, sf, [&](int s) -> hipError_t {
+            const int64_t r = io.rv[s];
+            if (r - 1 < t0) return hipSuccess;
+            return hipStreamWaitEvent(sf, net->upd_ev[(size_t)s * Q + (size_t)(r % Q)], 0);
+        });
+        if (e != hipSuccess) {
+            what = is.what;
+            break;
+        }
+        // backward of t after its forward, and after step t-1's updates have
+        // read the shared parameter gradients
+        e = hipEventRecord(net->fdone_ev, sf);
+        if (e == hipSuccess) e = hipStreamWaitEvent(sb, net->fdone_ev, 0);
+        if (e == hipSuccess && i >= 1) e = hipStreamWaitEvent(sb, net->par_ev[2 * (1 - p) + 1], 0);
+        if (e != hipSuccess) {
+            what = "pipeline_run: backward order";
+            break;
+        }
+        e = issue_backward(is, sb, sw, [&](int s) -> hipError_t {
+            return hipEventRecord(net->upd_ev[(size_t)s * Q + (size_t)((t + 1) % Q)], sw);
+        });
+        if (e != hipSuccess) {
+            what = is.what;
+            break;
+        }
+        e = hipEventRecord(bdone, sb);
+        if (e == hipSuccess) e = hipEventRecord(wdone, sw);
+        if (e != hipSuccess) {
+            what = "pipeline_run: step done";
+            break;
+        }
+        if (versions_out)
+            for (int s = 0; s < S_; ++s) versions_out[(size_t)i * S_ + s] = (int32_t)io.rv[s];
+        ++issued;
+    }
+    // join: the caller's stream waits for the forward and weight streams
+    hipError_t ej = hipEventRecord(net->join_ev, sw);
+    if (ej == hipSuccess) ej = hipStreamWaitEvent(sb, net->join_ev, 0);
+    if (ej == hipSuccess) ej = hipEventRecord(net->fdone_ev, sf);
+    if (ej == hipSuccess) ej = hipStreamWaitEvent(sb, net->fdone_ev, 0);
+    if (e != hipSuccess) return hip_check(e, what);
+    if (ej != hipSuccess) return hip_check(ej, "pipeline_run: join");
+    net->next_t = t0 + issued;
     return PSW_OK;
 }
 

@@ -83,6 +83,9 @@ SIGNATURES = {
     "psw_net_profile_read": (_I, [_P, _I, _P, _P]),
     "psw_net_profile_kernels": (_I, [_P, _I, _P, _P]),
     "psw_net_profile_only": (_I, [_P, _I, ctypes.c_char_p]),
+    "psw_net_pipeline_bytes": (_I, [_P, _P]),
+    "psw_net_bind_pipeline": (_I, [_P, _P, _SZ]),
+    "psw_pipeline_run": (_I, [_P, _I64, _I, _P, _P, _F, _F, _I, _P, _P, _I, _P, _P, _P]),
 }
 
 PROF_KINDS = ["conv_fwd", "conv_bwd_data", "conv_bwd_weight", "bn_fwd", "bn_bwd", "pool", "fc", "loss", "sgd",
@@ -330,6 +333,25 @@ class Net:
         ver = np.zeros(self.S, dtype=np.int32)
         _check(lib().psw_stage_step(self.handle, int(t), st.ctypes.data, lrs.ctypes.data, mom, wd, int(nesterov),
                                     _ptr(x), _ptr(labels), _ptr(self.loss), ver.ctypes.data, _stream(stream)))
+        return ver
+
+    def pipeline_run(self, t0, staleness, lr, xs, labels, losses, mom=0.9, wd=0.0, nesterov=False, stream=None):
+        """Steps t0 .. t0+n-1 as a pipeline (psw_pipeline_run): staleness [n, S] and lr ([n, S] or [S] or scalar)
+        host arrays; xs [n_batches, batch, ...] and labels [n_batches, batch] device tensors (step t0+i uses batch
+        i mod n_batches); losses: device float32 tensor of n entries.  Returns the versions [n, S]."""
+        if getattr(self, "step2", None) is None:
+            nb = ctypes.c_int64()
+            _check(lib().psw_net_pipeline_bytes(self.handle, ctypes.byref(nb)))
+            self.step2 = torch.empty(max(nb.value, 256), dtype=torch.uint8, device=self.device)
+            _check(lib().psw_net_bind_pipeline(self.handle, _ptr(self.step2), self.step2.numel()))
+        st = np.ascontiguousarray(staleness, dtype=np.int32).reshape(-1, self.S)
+        n = st.shape[0]
+        lrs = np.ascontiguousarray(np.broadcast_to(np.asarray(lr, dtype=np.float32), (n, self.S)))
+        assert losses.numel() >= n and xs.shape[0] == labels.shape[0]
+        ver = np.zeros((n, self.S), dtype=np.int32)
+        _check(lib().psw_pipeline_run(self.handle, int(t0), n, st.ctypes.data, lrs.ctypes.data, mom, wd,
+                                      int(nesterov), _ptr(xs), _ptr(labels), int(xs.shape[0]), _ptr(losses),
+                                      ver.ctypes.data, _stream(stream)))
         return ver
 
     def profile(self, enable=True, only=None):

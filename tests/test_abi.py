@@ -77,14 +77,21 @@ def test_plan_versions_follow_schedule(psw):
             assert stage == stage_of[op]
             assert ver == max(0, t - d[stage])                  # forward reads version t - d_s
         assert all(ver == t for _, _, _, ver in bwd)            # backward reads the current version
-        assert [(s, v) for _, _, s, v in sgd] == [(s, t) for s in range(S)]
-    # order: every forward before the loss, every backward after it, updates last
+        assert [(s, v) for _, _, s, v in sgd] == [(s, t) for s in reversed(range(S))]
+    # order: every forward before the loss, every backward after it; stage s
+    # is updated right after the backward pass is done with it (its last
+    # backward operation), before any backward operation of stage s-1
     plan = _plan(psw, wl, 5, [3, 2, 1, 0])
     kinds = [p[1] for p in plan]
     li = kinds.index(5)
     assert all(k in (1, 2, 3, 4) for k in kinds[:li])
     assert all(k not in (1, 2, 3, 4) for k in kinds[li + 1:])
-    assert kinds[-S:] == [12] * S
+    back = plan[li + 1:]
+    for s in range(S):
+        u = next(j for j, p in enumerate(back) if p[1] == 12 and p[2] == s)
+        assert all(p[2] != s for p in back[u + 1:] if p[1] != 12)
+        assert all(p[2] == s or p[1] == 12 for p in back[u - 1:u]) and all(p[2] != s - 1 for p in back[:u])
+    assert kinds[-1] == 12
     # 19 conv forwards, 19 wgrads, 18 dgrads (none for the stem) in ResNet-20
     assert kinds.count(1) == 19 and kinds.count(7) == 19 and kinds.count(8) == 18
 

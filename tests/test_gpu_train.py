@@ -219,3 +219,92 @@ def test_step_order_enforced(P):
     with pytest.raises(P.PswError) as e:
         net.step(0, [4, 0, 0, 0], wl.lr, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda())
     assert e.value.code == -4
+
+
+# ---- pipelined execution (psw_pipeline_run) -------------------------------
+def _sequential(P, wl, N, st, lr):
+    net = P.Net(wl.ops, N, wl.in_shape, wl.stage_end, [int(st[:, s].max()) + 1 for s in range(st.shape[1])],
+                bf16=wl.bf16)
+    net.load_params(synth.init_params(wl))
+    losses, versions = [], []
+    for t in range(st.shape[0]):
+        x, y = synth.batch(wl, t, N)
+        versions.append(net.step(t, st[t], lr, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), wl.momentum,
+                                 wl.weight_decay, wl.nesterov))
+        losses.append(float(net.loss.item()))
+    torch.cuda.synchronize()
+    return net, np.array(losses, dtype=np.float32), np.array(versions)
+
+
+def _pipelined(P, wl, N, st, lr, chunks):
+    T = st.shape[0]
+    net = P.Net(wl.ops, N, wl.in_shape, wl.stage_end, [int(st[:, s].max()) + 1 for s in range(st.shape[1])],
+                bf16=wl.bf16)
+    net.load_params(synth.init_params(wl))
+    xs, ys = synth.batches(wl, T, N)
+    xs, ys = torch.from_numpy(xs).cuda(), torch.from_numpy(ys).cuda()
+    losses = torch.zeros(T, dtype=torch.float32, device="cuda")
+    versions = []
+    t0 = 0
+    for n in chunks:  # consecutive runs continue the same schedule
+        versions.append(net.pipeline_run(t0, st[t0:t0 + n], lr, xs[t0:t0 + n], ys[t0:t0 + n], losses[t0:t0 + n],
+                                         wl.momentum, wl.weight_decay, wl.nesterov))
+        t0 += n
+    assert t0 == T
+    torch.cuda.synchronize()
+    return net, losses.cpu().numpy(), np.concatenate(versions)
+
+
+def _table(rows, T, S):
+    return np.array([rows(t) for t in range(T)], dtype=np.int32).reshape(T, S)
+
+
+PIPE_CASES = [
+    # name, workload, batch, staleness table (t -> per-stage d), steps, chunks
+    ("resnet20_stale", lambda: synth.resnet20_workload(batch=8), 8, lambda t: [3, 2, 1, 0], 8, [8]),
+    ("resnet20_paper_d", lambda: synth.resnet20_workload(batch=8), 8, lambda t: [6, 4, 2, 0], 9, [4, 5]),
+    ("resnet20_hybrid", lambda: synth.resnet20_workload(batch=8), 8,
+     lambda t: [3, 2, 1, 0] if t < 4 else [0, 0, 0, 0], 7, [7]),
+    ("resnet20_sgd", lambda: synth.resnet20_workload(batch=8), 8, lambda t: [0, 0, 0, 0], 4, [4]),
+    ("resnet20_bf16", lambda: synth.resnet20_workload(batch=8, bf16=True), 8, lambda t: [3, 2, 1, 0], 5, [2, 3]),
+    ("alexnet", lambda: synth.alexnet_workload(batch=4), 4, lambda t: [2, 0], 5, [5]),
+    ("vgg16_hybrid", lambda: synth.vgg16_workload(batch=8, n_pipelined=3), 8, None, 5, [5]),
+]
+
+
+@pytest.mark.parametrize("name,factory,N,rows,T,chunks", PIPE_CASES, ids=[c[0] for c in PIPE_CASES])
+def test_pipeline_run_equals_stage_steps(P, name, factory, N, rows, T, chunks):
+    """The pipelined run reorders work across streams only where the
+    schedule's dependencies allow it, so it must reproduce the per-step calls
+    bit for bit: parameters of the final version, momentum, running
+    statistics, every loss and the versions table."""
+    wl = factory()
+    st = wl.staleness(T) if rows is None else _table(rows, T, len(wl.stage_end))
+    a, la, va = _sequential(P, wl, N, st, wl.lr)
+    b, lb, vb = _pipelined(P, wl, N, st, wl.lr, chunks)
+    np.testing.assert_array_equal(va, vb)
+    np.testing.assert_array_equal(la, lb)
+    assert torch.equal(a.params(T), b.params(T))
+    assert torch.equal(a.momentum, b.momentum)
+    assert torch.equal(a.run_mean, b.run_mean) and torch.equal(a.run_var, b.run_var)
+    print(f"{name}: {T} steps bit-identical, last loss {lb[-1]:.5f}")
+
+
+def test_pipeline_after_stage_steps(P):
+    """Per-step calls, then a pipelined run from the next step: same as
+    per-step calls throughout."""
+    wl = synth.resnet20_workload(batch=8)
+    st = _table(lambda t: [3, 2, 1, 0], 6, 4)
+    a, la, _ = _sequential(P, wl, 8, st, wl.lr)
+    net = P.Net(wl.ops, 8, wl.in_shape, wl.stage_end, [4, 3, 2, 1], bf16=False)
+    net.load_params(synth.init_params(wl))
+    for t in range(2):
+        x, y = synth.batch(wl, t, 8)
+        net.step(t, st[t], wl.lr, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), wl.momentum)
+    xs, ys = synth.batches(wl, 6, 8)
+    losses = torch.zeros(4, device="cuda")
+    net.pipeline_run(2, st[2:], wl.lr, torch.from_numpy(xs[2:]).cuda(), torch.from_numpy(ys[2:]).cuda(), losses,
+                     wl.momentum)
+    torch.cuda.synchronize()
+    assert torch.equal(a.params(6), net.params(6))
+    np.testing.assert_array_equal(la[2:], losses.cpu().numpy())
