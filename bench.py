@@ -5,19 +5,24 @@ One step = one mini-batch through all 4 stages: forward (PPV (7,13,19),
 weights of version t - d_s with d = [3,2,1,0]), softmax cross-entropy,
 backward (weight gradients + data gradients with the current weights), and
 the SGD-momentum update into each stage's weight-version ring.  The steps
-run as the paper's pipeline on one GPU (psw_pipeline_run: the forward pass
-of mini-batch t+1 overlaps the backward pass of mini-batch t where the
-stale weights allow it; results identical to one psw_stage_step call per
-step, which --sequential times instead).  Inputs are synthetic N(0,1)
-[128,3,32,32] batches with uniform labels, all resident in HBM before timing
-starts.
+run as the paper's pipeline on one GPU: the forward pass of mini-batch t+1
+overlaps the backward pass of mini-batch t where the stale weights allow it
+(psw_pipeline_run; results identical to one psw_stage_step call per step).
+By default the timed steps are one eager psw_pipeline_run call; --mode
+graph replays a HIP graph that captured one period (lcm of the ring depths
+and 2 = 12 steps) of the pipeline, --mode sequential makes one
+psw_stage_step call per step; the modes not selected are timed over K more
+steps for context (on ROCm 7.2 the graph replays of this three-stream
+pipeline run slower than issuing it eagerly).  Inputs
+are synthetic N(0,1) [128,3,32,32] batches with uniform labels, all resident
+in HBM before timing starts.
 
-Prints one JSON line.  `value` is images/s over the K timed steps; the other
-execution mode is timed over K more steps for context.
+Prints one JSON line.  `value` is images/s over the K timed steps.
 
-Measurement, in order: W warm-up steps; the K timed steps (wall clock, no
-events); then a profiling pass of min(K, 100) steps of the same workload in
-which every kernel is launched with a start / stop HIP event pair that the
+Measurement, in order: W warm-up steps (eager, including the pipeline
+fill), the graph capture and one untimed replay; the K timed steps (wall
+clock, no events); the other modes; then a profiling pass of min(K, 100)
+eager pipelined steps of the same workload in which every kernel is launched with a start / stop HIP event pair that the
 runtime stamps from the kernel's own dispatch (so the durations agree with a
 rocprofv3 kernel trace).  That pass gives the per-kernel table, the conv
 matrix-core figure the metric names, and the dominant kernel (largest summed
@@ -130,8 +135,9 @@ def main():
     ap.add_argument("--warmup", type=int, default=20)
     ap.add_argument("--bf16", action="store_true", help="bf16-in / fp32-accumulate conv and FC products")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--sequential", action="store_true",
-                    help="time one psw_stage_step call per step instead of the pipelined run")
+    ap.add_argument("--mode", choices=("pipelined", "graph", "sequential"), default="pipelined",
+                    help="pipelined: psw_pipeline_run issued eagerly (default); graph: the same steps replayed "
+                         "from a captured HIP graph; sequential: one psw_stage_step call per step")
     ap.add_argument("--no-profile", action="store_true",
                     help="no events at all: skip the profiling pass and the dominant-kernel timing")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -155,7 +161,10 @@ def main():
     wl = synth.resnet20_workload(bf16=args.bf16)
     K, W = args.steps, args.warmup
     KP = 0 if args.no_profile else min(K, PROFILE_STEPS)
-    T = W + KP + 2 * K
+    period = 2
+    for d in wl.ring_depth():
+        period = period * d // __import__("math").gcd(period, d)
+    T = W + period + KP + 3 * K
     net = psw.Net(wl.ops, wl.batch, wl.in_shape, wl.stage_end, wl.ring_depth(T), bf16=wl.bf16)
     net.load_params(synth.init_params(wl))
     stal = wl.staleness(T)
@@ -184,25 +193,49 @@ def main():
         net.pipeline_run(t, stal[t:t + n], wl.lr, xs, ys, losses[:n], wl.momentum, wl.weight_decay, wl.nesterov)
         t += n
 
-    run = run_sequential if args.sequential else run_pipelined
+    graph = None
+    glosses = torch.zeros(period, dtype=torch.float32, device="cuda")
 
-    run(W)
+    def run_graph(n):
+        # replays of one captured period (the next `period` steps each), the
+        # remainder issued eagerly
+        nonlocal t
+        for _ in range(n // period):
+            graph.launch()
+            t += period
+        if n % period:
+            run_pipelined(n % period)
+
+    modes = {"graph": run_graph, "pipelined": run_pipelined, "sequential": run_sequential}
+    run = modes[args.mode]
+
+    run_pipelined(W)  # includes the pipeline fill (versions clamped at 0)
+    graph = net.capture(stal[t:t + period], wl.lr, xs, ys, glosses, wl.momentum, wl.weight_decay, wl.nesterov)
+    run_graph(period)  # first replay uploads the graph
     torch.cuda.synchronize()
     # timed region: no events
     t0 = time.perf_counter()
     run(K)
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
-    loss = float(net.loss.item() if args.sequential else losses[K - 1].item())
+    if args.mode == "sequential":
+        loss = float(net.loss.item())
+    elif args.mode == "graph" and K % period == 0:
+        loss = float(glosses[-1].item())
+    else:  # the last call was an eager pipelined run of K (or K mod period) steps
+        loss = float(losses[(K if args.mode == "pipelined" else K % period) - 1].item())
     assert np.isfinite(loss), loss
     ms_per_step = 1000.0 * elapsed / K
     img_s = wl.batch * K / elapsed
-    # the other execution mode, for context (same workload, continuing the run)
-    other = run_pipelined if args.sequential else run_sequential
-    t1 = time.perf_counter()
-    other(K)
-    torch.cuda.synchronize()
-    other_img_s = wl.batch * K / (time.perf_counter() - t1)
+    # the other execution modes, for context (same workload, continuing the run)
+    others = {}
+    for name, fn in modes.items():
+        if name == args.mode:
+            continue
+        t1 = time.perf_counter()
+        fn(K)
+        torch.cuda.synchronize()
+        others[name] = round(wl.batch * K / (time.perf_counter() - t1), 2)
 
     # profiling pass over the same workload: every kernel launched with
     # start / stop events stamped from its own dispatch
@@ -210,7 +243,7 @@ def main():
     kernels, breakdown, conv, roof = [], None, None, None
     if KP:
         net.profile(True)
-        run(KP)
+        (run_sequential if args.mode == "sequential" else run_pipelined)(KP)  # graphs carry no events
         torch.cuda.synchronize()
         prof = net.profile_read()
         kernels = net.profile_kernels()
@@ -255,9 +288,11 @@ def main():
         "config": {"workload": "ResNet-20 (CIFAR shape), batch 128, 4 stages at PPV (7,13,19), staleness [3,2,1,0], "
                                "SGD momentum 0.9, lr 0.01",
                    "global_batch": wl.batch, "input": "3x32x32 N(0,1)", "parallelism": "single GPU, all stages",
-                   "execution": "per-step psw_stage_step calls" if args.sequential else
-                                "pipelined psw_pipeline_run (forward of t+1 overlaps backward of t)"},
-        ("pipelined_value" if args.sequential else "sequential_value"): round(other_img_s, 2),
+                   "execution": {"graph": f"pipelined (forward of t+1 overlaps backward of t), replayed from a "
+                                          f"HIP graph of {period} captured steps",
+                                 "pipelined": "pipelined psw_pipeline_run issued eagerly",
+                                 "sequential": "one psw_stage_step call per step"}[args.mode]},
+        "other_modes_images_per_s": others,
         "roofline": roof,
         "conv_mfma": conv,
         "kernel_ms_per_step": breakdown,

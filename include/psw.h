@@ -272,6 +272,25 @@ int psw_pipeline_run(psw_net *net, int64_t t0, int n_steps, const int32_t *stale
                      float mom, float wd, int nesterov, const float *x, const int32_t *labels,
                      int n_batches, float *losses, int32_t *versions_out, void *stream);
 
+/* The same pipelined steps captured once into a HIP graph and replayed:
+ * psw_pipeline_capture records (does not run) n_steps steps from the net's
+ * next step t0 with psw_pipeline_run's arguments; every psw_graph_launch
+ * then runs the next n_steps steps on `stream` (net at step t0 + k*n_steps
+ * or any step congruent to t0 modulo the period; else PSW_ERR_STEP_ORDER),
+ * with the captured staleness, lr, batches (relative to the launch) and
+ * losses buffer.  n_steps must be a multiple of the period
+ * lcm(ring_depth[s], 2) after which ring slots and step sets repeat, and no
+ * captured step may clamp its version at 0 (run the pipeline fill eagerly).
+ * The captured pointers must stay valid until psw_graph_destroy.  Graph
+ * launches skip the host-side cost of issuing ~10^2 kernels and events per
+ * step, which otherwise bounds small networks. */
+typedef struct psw_graph psw_graph;
+int psw_pipeline_capture(psw_net *net, int n_steps, const int32_t *staleness, const float *lr, float mom,
+                         float wd, int nesterov, const float *x, const int32_t *labels, int n_batches,
+                         float *losses, psw_graph **out);
+int psw_graph_launch(psw_graph *g, void *stream);
+int psw_graph_destroy(psw_graph *g);
+
 /* Set the next expected step (resume from a checkpoint whose ring holds
  * versions t-ring_depth+1 .. t in their slots v mod ring_depth). */
 int psw_net_set_step(psw_net *net, int64_t t);
@@ -345,6 +364,18 @@ int psw_net_profile(psw_net *net, int enable);
 int psw_net_profile_only(psw_net *net, int enable, const char *kernel);
 int psw_net_profile_read(psw_net *net, int n_kinds, double *ms, int64_t *launches);
 int psw_net_profile_kernels(psw_net *net, int cap, psw_kernel_stat *out, int *n_out);
+/* psw_net_profile_timeline: one psw_kernel_span per recorded launch, in
+ * issue order (at most cap; *n_out = the record count): start and end in
+ * microseconds after the first record's start, and the stream it ran on
+ * (0 the caller's, 1 the library's weight-gradient / update stream, 2 the
+ * library's forward stream of psw_pipeline_run). */
+typedef struct psw_kernel_span {
+    char name[96];
+    int32_t kind;
+    int32_t stream;
+    double start_us, end_us;
+} psw_kernel_span;
+int psw_net_profile_timeline(psw_net *net, int cap, psw_kernel_span *out, int *n_out);
 
 #ifdef __cplusplus
 }

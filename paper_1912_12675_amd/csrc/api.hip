@@ -284,7 +284,8 @@ struct psw_net {
     std::vector<char> fused_bwd_now;        // per conv op: the fused dgrad ran in the current step
 
     std::vector<char> grad_accum;           // per op input slot: 0 overwrite, 1 accumulate (in0, in1)
-    size_t step_bytes = 0;                  // one step set (activations, saves, logits' gradient, forward ws)
+    size_t step_bytes = 0;                  // one step set (activations, saves, gradients, forward ws)
+    size_t pgrad_off = 0;                   // parameter gradients in the step set (pipelined runs)
     size_t wsf_off = 0;                     // forward workspace, in the step set
     size_t ws_off = 0, ws_bytes = 0, arena_bytes = 0;  // backward workspace, in the shared set
     size_t wsw_off = 0, wsw_bytes = 0;      // workspace of the backward-weight kernels (shared set)
@@ -292,17 +293,16 @@ struct psw_net {
     // from the caller's stream when a conv's output gradient is final and
     // joined before the update (created at bind, default priority)
     hipStream_t side = nullptr;
-    std::vector<hipEvent_t> fork_ev;        // per op
     std::vector<hipEvent_t> stage_ev;       // per stage: the chain is done with the stage
     hipEvent_t join_ev = nullptr;
     // pipelined runs (psw_pipeline_run): forward stream, second step set,
     // per-stage update events indexed by version mod upd_q, per step-set
-    // parity "backward done" / "weight stream done" events
+    // parity "weight stream done with the step" events
     hipStream_t fwd = nullptr;
     char* step2 = nullptr;
     int upd_q = 0;
     std::vector<hipEvent_t> upd_ev;
-    hipEvent_t par_ev[4] = {nullptr, nullptr, nullptr, nullptr};
+    hipEvent_t wdone_ev[2] = {nullptr, nullptr};
     hipEvent_t fdone_ev = nullptr, start_ev = nullptr;
     // bound memory
     float *ring = nullptr, *momentum = nullptr, *grad = nullptr, *run_mean = nullptr, *run_var = nullptr;
@@ -317,6 +317,7 @@ struct psw_net {
         std::string name;
         psw::Work work;
         hipEvent_t a, b;
+        int stream;  // 0 the caller's, 1 the weight stream, 2 the forward stream
     };
     struct Recorder final : psw::KernelRecorder {
         psw_net* net = nullptr;
@@ -329,9 +330,10 @@ struct psw_net {
             *stop = *start ? net->next_event() : nullptr;
             return *start && *stop;
         }
-        void end(std::string&& name, const psw::Work& w, hipEvent_t start, hipEvent_t stop) override
+        void end(std::string&& name, const psw::Work& w, hipEvent_t start, hipEvent_t stop, hipStream_t st) override
         {
-            net->krecs.push_back(KRec{kind, std::move(name), w, start, stop});
+            const int sid = st == net->side ? 1 : (st == net->fwd && st ? 2 : 0);
+            net->krecs.push_back(KRec{kind, std::move(name), w, start, stop, sid});
         }
     };
     bool profiling = false;
@@ -347,13 +349,11 @@ struct psw_net {
         for (hipEvent_t e : ev_pool) (void)hipEventDestroy(e);
         if (side) (void)hipStreamSynchronize(side);
         if (fwd) (void)hipStreamSynchronize(fwd);
-        for (hipEvent_t e : fork_ev)
-            if (e) (void)hipEventDestroy(e);
         for (hipEvent_t e : stage_ev)
             if (e) (void)hipEventDestroy(e);
         for (hipEvent_t e : upd_ev)
             if (e) (void)hipEventDestroy(e);
-        for (hipEvent_t e : par_ev)
+        for (hipEvent_t e : wdone_ev)
             if (e) (void)hipEventDestroy(e);
         for (hipEvent_t e : {join_ev, fdone_ev, start_ev})
             if (e) (void)hipEventDestroy(e);
@@ -502,13 +502,14 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
         fo += net->stage_np[s];
         ro += net->stage_np[s] * net->ring_depth[s];
     }
-    // arena = [step set][shared set].  The step set holds what a step's
-    // forward pass writes and its backward pass reads: activations, saved BN
-    // statistics / max-pool argmax, the logits' gradient (written by the
-    // loss), and the forward workspace; a pipelined run alternates between
-    // two step sets (psw_net_bind_pipeline).  The shared set holds the other
-    // gradients, the backward workspace and the backward-weight workspace.
-    // Offsets of both sets are relative to the start of their set.
+    // arena = [step set][shared set].  The step set holds everything one
+    // step writes and a later stream of the same step reads: activations,
+    // saved BN statistics / max-pool argmax, every tensor's gradient, the
+    // parameter gradients of a pipelined run, and the forward workspace; a
+    // pipelined run alternates between two step sets (psw_net_bind_pipeline)
+    // so that step t+1 never writes what step t's weight stream still reads.
+    // The shared set holds the backward and backward-weight workspaces, each
+    // used by one stream only.  Offsets are relative to their set.
     size_t off = 0;
     net->act_off.assign(n_layers + 1, 0);
     net->grad_off.assign(n_layers + 1, 0);
@@ -554,17 +555,19 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
             ws = std::max(ws, psw::fc_bwd_ws_bytes(a.n, o.cin, o.cout));
         }
     }
-    net->grad_off[n_layers] = off;  // the logits' gradient: step set
-    off = align256(off + (size_t)net->t[n_layers].numel() * sizeof(float));
+    for (int i = 1; i <= n_layers; ++i) {  // gradients of every tensor
+        net->grad_off[i] = off;
+        off = align256(off + (size_t)net->t[i].numel() * sizeof(float));
+    }
+    int64_t np_all = 0;
+    for (int s = 0; s < n_stages; ++s) np_all += net->stage_np[s];
+    net->pgrad_off = off;  // parameter gradients, stage-major (pipelined runs)
+    off = align256(off + (size_t)np_all * sizeof(float));
     net->ws_bytes = align256(ws);
     net->wsf_off = off;
     off += net->ws_bytes;
     net->step_bytes = off;
     off = 0;  // shared set
-    for (int i = 1; i < n_layers; ++i) {
-        net->grad_off[i] = off;
-        off = align256(off + (size_t)net->t[i].numel() * sizeof(float));
-    }
     net->ws_off = off;
     off += net->ws_bytes;
     net->wsw_off = off;
@@ -653,11 +656,6 @@ int psw_net_bind(psw_net* net, float* ring, float* momentum, float* grad, float*
             net->side = nullptr;
             return hip_check(e, "net_bind: side stream");
         }
-        net->fork_ev.assign(net->ops.size(), nullptr);
-        for (auto& ev : net->fork_ev) {
-            e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
-            if (e != hipSuccess) return hip_check(e, "net_bind: events");
-        }
         net->stage_ev.assign(net->S, nullptr);
         for (auto& ev : net->stage_ev) {
             e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
@@ -731,7 +729,6 @@ int psw_net_plan(const psw_net* net, int64_t t, const int32_t* staleness, psw_la
         switch (o.kind) {
         case PSW_OP_CONV:
             if (o.flags & PSW_F_RELU) rec(i, PSW_PLAN_RELU_MASK, s, -1);
-            rec(i, PSW_PLAN_CONV_BWD_WEIGHT, s, -1);
             if (o.in0 > 0) rec(i, PSW_PLAN_CONV_BWD_DATA, s, t);
             break;
         case PSW_OP_BN: rec(i, PSW_PLAN_BN_BWD, s, t); break;
@@ -744,8 +741,13 @@ int psw_net_plan(const psw_net* net, int64_t t, const int32_t* staleness, psw_la
             rec(i, PSW_PLAN_FC_BWD, s, t);
             break;
         }
-        // a stage is updated (version t -> t+1) as soon as the backward pass is done with it
-        if (i == net->stage_begin[s]) rec(-1, PSW_PLAN_SGD, s, t);
+        // when the data-gradient chain is done with a stage: the stage's
+        // weight gradients, then its update (version t -> t+1)
+        if (i == net->stage_begin[s]) {
+            for (int j = net->stage_end[s] - 1; j >= net->stage_begin[s]; --j)
+                if (net->ops[j].kind == PSW_OP_CONV) rec(j, PSW_PLAN_CONV_BWD_WEIGHT, s, -1);
+            rec(-1, PSW_PLAN_SGD, s, t);
+        }
     }
     *n_out = n;
     return PSW_OK;
@@ -766,6 +768,7 @@ struct StepIO {
     const float* lr;          // per stage
     float mom, wd;
     int nesterov;
+    float* gbase;             // packed parameter gradients (stage-major)
 };
 
 struct Issue {
@@ -775,11 +778,7 @@ struct Issue {
     const char* what = "";
     char* A() const { return io.P; }
     float* act(int id) const { return id == 0 ? (float*)io.x : (float*)(io.P + net->act_off[id]); }
-    float* grd(int id) const
-    {
-        const int L = (int)net->ops.size();
-        return id == L ? (float*)(io.P + net->grad_off[id]) : (float*)(net->arena + net->step_bytes + net->grad_off[id]);
-    }
+    float* grd(int id) const { return (float*)(io.P + net->grad_off[id]); }
     float* save(int i) const { return (float*)(io.P + net->save_off[i]); }
     void* wsf() const { return io.P + net->wsf_off; }
     void* wsb() const { return net->arena + net->step_bytes + net->ws_off; }
@@ -790,7 +789,7 @@ struct Issue {
         return slot_ptr(net, s, io.rv[s]) + net->poff[i];
     }
     const float* wcur(int i) const { return slot_ptr(net, net->stage_of[i], io.t) + net->poff[i]; }
-    float* gptr(int i) const { return net->grad + net->flat_off[net->stage_of[i]] + net->poff[i]; }
+    float* gptr(int i) const { return io.gbase + net->flat_off[net->stage_of[i]] + net->poff[i]; }
 };
 
 #define PSW_TRY(expr, w)          \
@@ -925,13 +924,6 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, AfterUpdate
             check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, net->prec, &cs);
             kind = PSW_PROF_OTHER;
             if (o.flags & PSW_F_RELU) PSW_TRY(psw::relu_mask(y.numel(), is.act(i + 1), g, sb), "relu_mask");
-            float* dw = is.gptr(i);
-            float* db = (o.flags & PSW_F_BIAS) ? dw + (int64_t)o.cout * o.cin * o.k * o.k : nullptr;
-            kind = PSW_PROF_CONV_BWD_WEIGHT;
-            // fork: the weight gradient runs beside the data-gradient chain
-            PSW_TRY(hipEventRecord(net->fork_ev[i], sb), "fork");
-            PSW_TRY(hipStreamWaitEvent(sw, net->fork_ev[i], 0), "fork");
-            PSW_TRY(psw::conv_bwd_weight(cs, is.act(o.in0), g, dw, db, bf16, wsw, wswb, sw), "conv_bwd_weight");
             kind = PSW_PROF_CONV_BWD_DATA;
             net->fused_bwd_now[i] = 0;
             if (din && net->fuse_bwd[i]) {  // BN op i-1's backward sums out of this dgrad
@@ -1010,12 +1002,27 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, AfterUpdate
         }
         }
         const int s = net->stage_of[i];
-        if (i == net->stage_begin[s]) {  // the chain is done with stage s: update it on sw
+        if (i == net->stage_begin[s]) {
+            // the chain is done with stage s: its weight gradients (from the
+            // step's activations and the now final output gradients) and its
+            // update run on sw, beside the chain's next stage
             PSW_TRY(hipEventRecord(net->stage_ev[s], sb), "stage join");
             PSW_TRY(hipStreamWaitEvent(sw, net->stage_ev[s], 0), "stage join");
+            for (int j = net->stage_end[s] - 1; j >= net->stage_begin[s]; --j) {
+                const psw_layer& c = net->ops[j];
+                if (c.kind != PSW_OP_CONV) continue;
+                const Tensor ca = net->t[c.in0];
+                psw::ConvShape ccs;
+                check_conv(ca.n, ca.c, ca.h, ca.w, c.cout, c.k, c.k, c.stride, c.pad, net->prec, &ccs);
+                float* dw = is.gptr(j);
+                float* db = (c.flags & PSW_F_BIAS) ? dw + (int64_t)c.cout * c.cin * c.k * c.k : nullptr;
+                kind = PSW_PROF_CONV_BWD_WEIGHT;
+                PSW_TRY(psw::conv_bwd_weight(ccs, is.act(c.in0), is.grd(j + 1), dw, db, bf16, wsw, wswb, sw),
+                        "conv_bwd_weight");
+            }
             kind = PSW_PROF_SGD;
             PSW_TRY(psw::sgd_momentum(net->stage_np[s], slot_ptr(net, s, io.t), slot_ptr(net, s, io.t + 1),
-                                      net->momentum + net->flat_off[s], net->grad + net->flat_off[s], io.lr[s], io.mom,
+                                      net->momentum + net->flat_off[s], io.gbase + net->flat_off[s], io.lr[s], io.mom,
                                       io.wd, io.nesterov, sw),
                     "sgd");
             PSW_TRY(after_update(s), "update event");
@@ -1047,7 +1054,7 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
     if (t != net->next_t)
         return fail(PSW_ERR_STEP_ORDER, "stage_step: expected t = %lld, got %lld", (long long)net->next_t, (long long)t);
     hipStream_t st = S(stream);
-    StepIO io{t, std::vector<int64_t>(net->S), net->arena, x, labels, loss_out, lr, mom, wd, nesterov};
+    StepIO io{t, std::vector<int64_t>(net->S), net->arena, x, labels, loss_out, lr, mom, wd, nesterov, net->grad};
     for (int s = 0; s < net->S; ++s) io.rv[s] = fwd_version(t, staleness[s]);
     Issue is{net, io};
     net->rec.kind = PSW_PROF_OTHER;
@@ -1093,7 +1100,7 @@ int psw_net_bind_pipeline(psw_net* net, void* step_set, size_t bytes)
         net->upd_ev.assign((size_t)net->S * net->upd_q, nullptr);
         std::vector<hipEvent_t*> evs;
         for (auto& ev : net->upd_ev) evs.push_back(&ev);
-        for (auto& ev : net->par_ev) evs.push_back(&ev);
+        for (auto& ev : net->wdone_ev) evs.push_back(&ev);
         evs.push_back(&net->fdone_ev);
         evs.push_back(&net->start_ev);
         for (hipEvent_t* ev : evs) {
@@ -1105,49 +1112,43 @@ int psw_net_bind_pipeline(psw_net* net, void* step_set, size_t bytes)
     return PSW_OK;
 }
 
-int psw_pipeline_run(psw_net* net, int64_t t0, int n_steps, const int32_t* staleness, const float* lr, float mom,
-                     float wd, int nesterov, const float* x, const int32_t* labels, int n_batches, float* losses,
-                     int32_t* versions_out, void* stream)
+}  // extern "C"
+
+namespace {
+
+// Issues steps t0 .. t0+n_steps-1 as a pipeline joined into sb (validated
+// by the caller).  Returns a PSW status; *issued = steps fully issued.
+int issue_pipeline(psw_net* net, int64_t t0, int n_steps, const int32_t* staleness, const float* lr, float mom,
+                   float wd, int nesterov, const float* x, const int32_t* labels, int n_batches, float* losses,
+                   int32_t* versions_out, hipStream_t sb, int64_t* issued)
 {
-    if (!net) return fail(PSW_ERR_NULL, "pipeline_run: net is NULL");
-    if (!net->bound || !net->step2) return fail(PSW_ERR_STATE, "pipeline_run: bind the net and its pipeline set first");
-    if (!staleness || !lr || !x || !labels || !losses) return fail(PSW_ERR_NULL, "pipeline_run: required pointer is NULL");
-    if (n_steps < 0 || n_batches < 1) return fail(PSW_ERR_SHAPE, "pipeline_run: n_steps >= 0 and n_batches >= 1");
-    if (t0 != net->next_t)
-        return fail(PSW_ERR_STEP_ORDER, "pipeline_run: expected t0 = %lld, got %lld", (long long)net->next_t,
-                    (long long)t0);
-    for (int i = 0; i < n_steps; ++i) {
-        int rc = check_staleness(net, t0 + i, staleness + (size_t)i * net->S);
-        if (rc) return rc;
-    }
-    if (n_steps == 0) return PSW_OK;
-    hipStream_t sb = S(stream), sf = net->fwd, sw = net->side;
+    hipStream_t sf = net->fwd, sw = net->side;
     const Tensor in = net->t[0];
     const size_t xs = (size_t)in.numel();
     const int S_ = net->S, Q = net->upd_q;
-    net->rec.kind = PSW_PROF_OTHER;
-    RecorderScope rec_scope(net->profiling ? &net->rec : nullptr);
+    *issued = 0;
     // everything the caller enqueued before (inputs, earlier versions) comes first
     hipError_t e = hipEventRecord(net->start_ev, sb);
     if (e == hipSuccess) e = hipStreamWaitEvent(sf, net->start_ev, 0);
     if (e == hipSuccess) e = hipStreamWaitEvent(sw, net->start_ev, 0);
-    if (e != hipSuccess) return hip_check(e, "pipeline_run: start");
+    if (e != hipSuccess) return hip_check(e, "pipeline: start");
     const char* what = "";
-    int64_t issued = 0;
     for (int i = 0; i < n_steps && e == hipSuccess; ++i) {
         const int64_t t = t0 + i;
         const int p = (int)(t & 1);
-        hipEvent_t bdone = net->par_ev[2 * p], wdone = net->par_ev[2 * p + 1];
-        StepIO io{t, std::vector<int64_t>(S_), p ? net->step2 : net->arena, x + (size_t)(i % n_batches) * xs,
-                  labels + (size_t)(i % n_batches) * in.n, losses + i, lr + (size_t)i * S_, mom, wd, nesterov};
+        hipEvent_t wdone = net->wdone_ev[p];
+        char* P = p ? net->step2 : net->arena;
+        StepIO io{t, std::vector<int64_t>(S_), P, x + (size_t)(i % n_batches) * xs,
+                  labels + (size_t)(i % n_batches) * in.n, losses + i, lr + (size_t)i * S_, mom, wd, nesterov,
+                  (float*)(P + net->pgrad_off)};
         for (int s = 0; s < S_; ++s) io.rv[s] = fwd_version(t, staleness[(size_t)i * S_ + s]);
         Issue is{net, io};
         // forward of t: its step set is free once step t-2 is done with it
+        // (the weight stream's last update of a step follows the chain's end)
         if (i >= 2) {
-            e = hipStreamWaitEvent(sf, bdone, 0);
-            if (e == hipSuccess) e = hipStreamWaitEvent(sf, wdone, 0);
+            e = hipStreamWaitEvent(sf, wdone, 0);
             if (e != hipSuccess) {
-                what = "pipeline_run: step set";
+                what = "pipeline: step set";
                 break;
             }
         }
@@ -1162,13 +1163,11 @@ int psw_pipeline_run(psw_net* net, int64_t t0, int n_steps, const int32_t* stale
             what = is.what;
             break;
         }
-        // backward of t after its forward, and after step t-1's updates have
-        // read the shared parameter gradients
+        // backward of t after its forward
         e = hipEventRecord(net->fdone_ev, sf);
         if (e == hipSuccess) e = hipStreamWaitEvent(sb, net->fdone_ev, 0);
-        if (e == hipSuccess && i >= 1) e = hipStreamWaitEvent(sb, net->par_ev[2 * (1 - p) + 1], 0);
         if (e != hipSuccess) {
-            what = "pipeline_run: backward order";
+            what = "pipeline: backward order";
             break;
         }
         e = issue_backward(is, sb, sw, [&](int s) -> hipError_t {
@@ -1178,24 +1177,154 @@ int psw_pipeline_run(psw_net* net, int64_t t0, int n_steps, const int32_t* stale
             what = is.what;
             break;
         }
-        e = hipEventRecord(bdone, sb);
-        if (e == hipSuccess) e = hipEventRecord(wdone, sw);
+        e = hipEventRecord(wdone, sw);
         if (e != hipSuccess) {
-            what = "pipeline_run: step done";
+            what = "pipeline: step done";
             break;
         }
         if (versions_out)
             for (int s = 0; s < S_; ++s) versions_out[(size_t)i * S_ + s] = (int32_t)io.rv[s];
-        ++issued;
+        ++*issued;
     }
-    // join: the caller's stream waits for the forward and weight streams
+    // join: sb waits for the forward and weight streams
     hipError_t ej = hipEventRecord(net->join_ev, sw);
     if (ej == hipSuccess) ej = hipStreamWaitEvent(sb, net->join_ev, 0);
     if (ej == hipSuccess) ej = hipEventRecord(net->fdone_ev, sf);
     if (ej == hipSuccess) ej = hipStreamWaitEvent(sb, net->fdone_ev, 0);
     if (e != hipSuccess) return hip_check(e, what);
-    if (ej != hipSuccess) return hip_check(ej, "pipeline_run: join");
+    if (ej != hipSuccess) return hip_check(ej, "pipeline: join");
+    return PSW_OK;
+}
+
+int check_pipeline_args(const psw_net* net, int64_t t0, int n_steps, const int32_t* staleness, const float* lr,
+                        const float* x, const int32_t* labels, int n_batches, const float* losses, const char* who)
+{
+    if (!net) return fail(PSW_ERR_NULL, "%s: net is NULL", who);
+    if (!net->bound || !net->step2) return fail(PSW_ERR_STATE, "%s: bind the net and its pipeline set first", who);
+    if (!staleness || !lr || !x || !labels || !losses) return fail(PSW_ERR_NULL, "%s: required pointer is NULL", who);
+    if (n_steps < 0 || n_batches < 1) return fail(PSW_ERR_SHAPE, "%s: n_steps >= 0 and n_batches >= 1", who);
+    for (int i = 0; i < n_steps; ++i) {
+        int rc = check_staleness(net, t0 + i, staleness + (size_t)i * net->S);
+        if (rc) return rc;
+    }
+    return PSW_OK;
+}
+
+int64_t gcd64(int64_t a, int64_t b) { return b ? gcd64(b, a % b) : a; }
+
+// period of the per-step buffers: ring slots (t mod D_s) and step sets (t mod 2)
+int64_t replay_period(const psw_net* net)
+{
+    int64_t p = 2;
+    for (int d : net->ring_depth) p = p / gcd64(p, d) * d;
+    return p;
+}
+
+}  // namespace
+
+struct psw_graph {
+    psw_net* net = nullptr;
+    hipGraph_t graph = nullptr;
+    hipGraphExec_t exec = nullptr;
+    int64_t t0 = 0, period = 1;
+    int n_steps = 0;
+    ~psw_graph()
+    {
+        if (exec) (void)hipGraphExecDestroy(exec);
+        if (graph) (void)hipGraphDestroy(graph);
+    }
+};
+
+extern "C" {
+
+int psw_pipeline_run(psw_net* net, int64_t t0, int n_steps, const int32_t* staleness, const float* lr, float mom,
+                     float wd, int nesterov, const float* x, const int32_t* labels, int n_batches, float* losses,
+                     int32_t* versions_out, void* stream)
+{
+    int rc = check_pipeline_args(net, t0, n_steps, staleness, lr, x, labels, n_batches, losses, "pipeline_run");
+    if (rc) return rc;
+    if (t0 != net->next_t)
+        return fail(PSW_ERR_STEP_ORDER, "pipeline_run: expected t0 = %lld, got %lld", (long long)net->next_t,
+                    (long long)t0);
+    if (n_steps == 0) return PSW_OK;
+    net->rec.kind = PSW_PROF_OTHER;
+    RecorderScope rec_scope(net->profiling ? &net->rec : nullptr);
+    int64_t issued = 0;
+    rc = issue_pipeline(net, t0, n_steps, staleness, lr, mom, wd, nesterov, x, labels, n_batches, losses,
+                        versions_out, S(stream), &issued);
     net->next_t = t0 + issued;
+    return rc;
+}
+
+int psw_pipeline_capture(psw_net* net, int n_steps, const int32_t* staleness, const float* lr, float mom, float wd,
+                         int nesterov, const float* x, const int32_t* labels, int n_batches, float* losses,
+                         psw_graph** out)
+{
+    if (!out) return fail(PSW_ERR_NULL, "pipeline_capture: out is NULL");
+    *out = nullptr;
+    const int64_t t0 = net ? net->next_t : 0;
+    int rc = check_pipeline_args(net, t0, n_steps, staleness, lr, x, labels, n_batches, losses, "pipeline_capture");
+    if (rc) return rc;
+    const int64_t period = replay_period(net);
+    if (n_steps <= 0 || n_steps % period != 0)
+        return fail(PSW_ERR_SHAPE, "pipeline_capture: n_steps must be a positive multiple of %lld", (long long)period);
+    for (int i = 0; i < n_steps; ++i)
+        for (int s = 0; s < net->S; ++s)
+            if (t0 + i - staleness[(size_t)i * net->S + s] < 0)
+                return fail(PSW_ERR_STALENESS, "pipeline_capture: step %lld clamps its version at 0 (pipeline fill); "
+                            "run the fill with psw_pipeline_run first", (long long)(t0 + i));
+    psw_graph* g = new psw_graph;
+    g->net = net;
+    g->t0 = t0;
+    g->period = period;
+    g->n_steps = n_steps;
+    hipStream_t cap = nullptr;
+    hipError_t e = hipStreamCreateWithFlags(&cap, hipStreamNonBlocking);
+    if (e != hipSuccess) {
+        delete g;
+        return hip_check(e, "pipeline_capture: stream");
+    }
+    RecorderScope rec_scope(nullptr);  // no per-kernel events inside a graph
+    e = hipStreamBeginCapture(cap, hipStreamCaptureModeThreadLocal);
+    int64_t issued = 0;
+    if (e == hipSuccess)
+        rc = issue_pipeline(net, t0, n_steps, staleness, lr, mom, wd, nesterov, x, labels, n_batches, losses, nullptr,
+                            cap, &issued);
+    hipGraph_t graph = nullptr;
+    hipError_t ee = e == hipSuccess ? hipStreamEndCapture(cap, &graph) : e;
+    (void)hipStreamDestroy(cap);
+    g->graph = graph;
+    if (e != hipSuccess || ee != hipSuccess || rc != PSW_OK) {
+        delete g;
+        if (rc != PSW_OK) return rc;
+        return hip_check(e != hipSuccess ? e : ee, "pipeline_capture");
+    }
+    e = hipGraphInstantiate(&g->exec, graph, nullptr, nullptr, 0);
+    if (e != hipSuccess) {
+        g->exec = nullptr;
+        delete g;
+        return hip_check(e, "pipeline_capture: instantiate");
+    }
+    *out = g;
+    return PSW_OK;
+}
+
+int psw_graph_launch(psw_graph* g, void* stream)
+{
+    if (!g || !g->exec) return fail(PSW_ERR_NULL, "graph_launch: graph is NULL");
+    psw_net* net = g->net;
+    if ((net->next_t - g->t0) % g->period != 0 || net->next_t < g->t0)
+        return fail(PSW_ERR_STEP_ORDER, "graph_launch: the net is at step %lld; this graph replays from steps "
+                    "%lld + k*%lld", (long long)net->next_t, (long long)g->t0, (long long)g->period);
+    hipError_t e = hipGraphLaunch(g->exec, S(stream));
+    if (e != hipSuccess) return hip_check(e, "graph_launch");
+    net->next_t += g->n_steps;
+    return PSW_OK;
+}
+
+int psw_graph_destroy(psw_graph* g)
+{
+    delete g;
     return PSW_OK;
 }
 
@@ -1241,6 +1370,32 @@ int psw_net_profile_read(psw_net* net, int n_kinds, double* ms, int64_t* launche
             ms[r.kind] += t;
             launches[r.kind] += 1;
         }
+    }
+    return PSW_OK;
+}
+
+int psw_net_profile_timeline(psw_net* net, int cap, psw_kernel_span* out, int* n_out)
+{
+    if (!net || !n_out || (cap > 0 && !out)) return fail(PSW_ERR_NULL, "net_profile_timeline: required pointer is NULL");
+    *n_out = (int)net->krecs.size();
+    if (net->krecs.empty()) return PSW_OK;
+    const psw_net::KRec& first = net->krecs.front();
+    hipError_t e = hipEventSynchronize(net->krecs.back().b);
+    if (e != hipSuccess) return hip_check(e, "net_profile_timeline");
+    for (int i = 0; i < cap && i < (int)net->krecs.size(); ++i) {
+        const psw_net::KRec& r = net->krecs[i];
+        float t0 = 0.f, t1 = 0.f;
+        e = hipEventSynchronize(r.b);
+        if (e == hipSuccess) e = hipEventElapsedTime(&t0, first.a, r.a);
+        if (e == hipSuccess) e = hipEventElapsedTime(&t1, first.a, r.b);
+        if (e != hipSuccess) return hip_check(e, "net_profile_timeline");
+        psw_kernel_span sp{};
+        snprintf(sp.name, sizeof(sp.name), "%s", r.name.c_str());
+        sp.kind = r.kind;
+        sp.stream = r.stream;
+        sp.start_us = 1e3 * t0;
+        sp.end_us = 1e3 * t1;
+        out[i] = sp;
     }
     return PSW_OK;
 }

@@ -28,7 +28,7 @@ class KernelRecorder {
 public:
     // false: do not time this launch; else *start / *stop are the events
     virtual bool begin(const std::string& name, hipEvent_t* start, hipEvent_t* stop) = 0;
-    virtual void end(std::string&& name, const Work& w, hipEvent_t start, hipEvent_t stop) = 0;
+    virtual void end(std::string&& name, const Work& w, hipEvent_t start, hipEvent_t stop, hipStream_t st) = 0;
 
 protected:
     ~KernelRecorder() = default;
@@ -64,7 +64,7 @@ std::string kname(const char* base, T... v)
             hipExtLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, psw_e0_, psw_e1_, 0, __VA_ARGS__); \
         else                                                                                      \
             hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, __VA_ARGS__);                  \
-        if (psw_rec_) psw_rec_->end(std::move(psw_name_), WORK, psw_e0_, psw_e1_);                \
+        if (psw_rec_) psw_rec_->end(std::move(psw_name_), WORK, psw_e0_, psw_e1_, STREAM);        \
     } while (0)
 
 constexpr double kF = 4.0;  // bytes per float

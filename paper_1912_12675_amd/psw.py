@@ -44,6 +44,11 @@ class psw_launch(ctypes.Structure):
                 ("version", ctypes.c_int64)]
 
 
+class psw_kernel_span(ctypes.Structure):
+    _fields_ = [("name", ctypes.c_char * 96), ("kind", ctypes.c_int32), ("stream", ctypes.c_int32),
+                ("start_us", ctypes.c_double), ("end_us", ctypes.c_double)]
+
+
 class psw_kernel_stat(ctypes.Structure):
     _fields_ = [("name", ctypes.c_char * 192), ("kind", ctypes.c_int32), ("launches", ctypes.c_int64),
                 ("ms", ctypes.c_double), ("flops", ctypes.c_double), ("bytes", ctypes.c_double)]
@@ -83,9 +88,13 @@ SIGNATURES = {
     "psw_net_profile_read": (_I, [_P, _I, _P, _P]),
     "psw_net_profile_kernels": (_I, [_P, _I, _P, _P]),
     "psw_net_profile_only": (_I, [_P, _I, ctypes.c_char_p]),
+    "psw_net_profile_timeline": (_I, [_P, _I, _P, _P]),
     "psw_net_pipeline_bytes": (_I, [_P, _P]),
     "psw_net_bind_pipeline": (_I, [_P, _P, _SZ]),
     "psw_pipeline_run": (_I, [_P, _I64, _I, _P, _P, _F, _F, _I, _P, _P, _I, _P, _P, _P]),
+    "psw_pipeline_capture": (_I, [_P, _I, _P, _P, _F, _F, _I, _P, _P, _I, _P, _P]),
+    "psw_graph_launch": (_I, [_P, _P]),
+    "psw_graph_destroy": (_I, [_P]),
 }
 
 PROF_KINDS = ["conv_fwd", "conv_bwd_data", "conv_bwd_weight", "bn_fwd", "bn_bwd", "pool", "fc", "loss", "sgd",
@@ -255,6 +264,22 @@ def _layers(ops):
     return arr
 
 
+class Graph:
+    """A captured pipelined run (psw_pipeline_capture); keeps the captured tensors alive."""
+
+    def __init__(self, handle, keep):
+        self.handle, self._keep = handle, keep
+
+    def launch(self, stream=None):
+        _check(lib().psw_graph_launch(self.handle, _stream(stream)))
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h and _lib is not None:
+            _lib.psw_graph_destroy(h)
+            self.handle = None
+
+
 class Net:
     """A network bound to torch-allocated device buffers.
 
@@ -339,11 +364,7 @@ class Net:
         """Steps t0 .. t0+n-1 as a pipeline (psw_pipeline_run): staleness [n, S] and lr ([n, S] or [S] or scalar)
         host arrays; xs [n_batches, batch, ...] and labels [n_batches, batch] device tensors (step t0+i uses batch
         i mod n_batches); losses: device float32 tensor of n entries.  Returns the versions [n, S]."""
-        if getattr(self, "step2", None) is None:
-            nb = ctypes.c_int64()
-            _check(lib().psw_net_pipeline_bytes(self.handle, ctypes.byref(nb)))
-            self.step2 = torch.empty(max(nb.value, 256), dtype=torch.uint8, device=self.device)
-            _check(lib().psw_net_bind_pipeline(self.handle, _ptr(self.step2), self.step2.numel()))
+        self._ensure_pipeline_set()
         st = np.ascontiguousarray(staleness, dtype=np.int32).reshape(-1, self.S)
         n = st.shape[0]
         lrs = np.ascontiguousarray(np.broadcast_to(np.asarray(lr, dtype=np.float32), (n, self.S)))
@@ -353,6 +374,25 @@ class Net:
                                       int(nesterov), _ptr(xs), _ptr(labels), int(xs.shape[0]), _ptr(losses),
                                       ver.ctypes.data, _stream(stream)))
         return ver
+
+    def _ensure_pipeline_set(self):
+        if getattr(self, "step2", None) is None:
+            nb = ctypes.c_int64()
+            _check(lib().psw_net_pipeline_bytes(self.handle, ctypes.byref(nb)))
+            self.step2 = torch.empty(max(nb.value, 256), dtype=torch.uint8, device=self.device)
+            _check(lib().psw_net_bind_pipeline(self.handle, _ptr(self.step2), self.step2.numel()))
+
+    def capture(self, staleness, lr, xs, labels, losses, mom=0.9, wd=0.0, nesterov=False):
+        """Capture the next n pipelined steps into a graph (psw_pipeline_capture); returns a Graph whose
+        launch() runs the next n steps each time.  The tensors passed must outlive the graph."""
+        self._ensure_pipeline_set()
+        st = np.ascontiguousarray(staleness, dtype=np.int32).reshape(-1, self.S)
+        n = st.shape[0]
+        lrs = np.ascontiguousarray(np.broadcast_to(np.asarray(lr, dtype=np.float32), (n, self.S)))
+        g = ctypes.c_void_p()
+        _check(lib().psw_pipeline_capture(self.handle, n, st.ctypes.data, lrs.ctypes.data, mom, wd, int(nesterov),
+                                          _ptr(xs), _ptr(labels), int(xs.shape[0]), _ptr(losses), ctypes.byref(g)))
+        return Graph(g.value, (self, xs, labels, losses))
 
     def profile(self, enable=True, only=None):
         """Enable / disable HIP-event timing of the kernels launched by step() (all of them, or only the
@@ -368,6 +408,15 @@ class Net:
         cnt = np.zeros(len(PROF_KINDS), dtype=np.int64)
         _check(lib().psw_net_profile_read(self.handle, len(PROF_KINDS), ms.ctypes.data, cnt.ctypes.data))
         return {k: (float(ms[i]), int(cnt[i])) for i, k in enumerate(PROF_KINDS)}
+
+    def profile_timeline(self, cap=1 << 20):
+        """[(name, kind, stream, start_us, end_us)] per recorded launch, in issue order."""
+        n = ctypes.c_int()
+        _check(lib().psw_net_profile_timeline(self.handle, 0, None, ctypes.byref(n)))
+        buf = (psw_kernel_span * max(1, min(n.value, cap)))()
+        _check(lib().psw_net_profile_timeline(self.handle, min(n.value, cap), buf, ctypes.byref(n)))
+        return [(buf[i].name.decode(), PROF_KINDS[buf[i].kind] if 0 <= buf[i].kind < len(PROF_KINDS) else "other",
+                 int(buf[i].stream), float(buf[i].start_us), float(buf[i].end_us)) for i in range(min(n.value, cap))]
 
     def profile_kernels(self, cap=256):
         """[{name, kind, launches, ms, flops, bytes}] per distinct kernel, in decreasing total time."""

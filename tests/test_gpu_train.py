@@ -308,3 +308,59 @@ def test_pipeline_after_stage_steps(P):
     torch.cuda.synchronize()
     assert torch.equal(a.params(6), net.params(6))
     np.testing.assert_array_equal(la[2:], losses.cpu().numpy())
+
+
+def test_graph_replays_equal_stage_steps(P):
+    """A pipelined run captured into a HIP graph (12 steps = the period of
+    the ring slots [4,3,2,1] and of the two step sets) and replayed three
+    times, with eager work and synchronisations between the replays: after
+    every replay the parameters, losses, momentum and running statistics
+    equal those of one psw_stage_step call per step."""
+    wl = synth.resnet20_workload(batch=8)
+    N, fill, per, reps = 8, 3, 12, 3
+    T = fill + per * reps
+    bidx = [t if t < fill else fill + (t - fill) % per for t in range(T)]
+    st = _table(lambda t: [3, 2, 1, 0], T, 4)
+    # reference: per-step calls
+    ref = P.Net(wl.ops, N, wl.in_shape, wl.stage_end, [4, 3, 2, 1])
+    ref.load_params(synth.init_params(wl))
+    ref_losses, ref_params = [], {}
+    for t in range(T):
+        x, y = synth.batch(wl, bidx[t], N)
+        ref.step(t, st[t], wl.lr, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), wl.momentum)
+        ref_losses.append(float(ref.loss.item()))
+        if t + 1 >= fill and (t + 1 - fill) % per == 0:
+            ref_params[t + 1] = ref.params(t + 1).clone()
+    # pipeline fill eagerly, then the graph
+    net = P.Net(wl.ops, N, wl.in_shape, wl.stage_end, [4, 3, 2, 1])
+    net.load_params(synth.init_params(wl))
+    xs, ys = synth.batches(wl, fill + per, N)
+    xs, ys = torch.from_numpy(xs).cuda(), torch.from_numpy(ys).cuda()
+    fill_losses = torch.zeros(fill, device="cuda")
+    net.pipeline_run(0, st[:fill], wl.lr, xs[:fill], ys[:fill], fill_losses, wl.momentum)
+    losses = torch.zeros(per, device="cuda")
+    graph = net.capture(st[fill:fill + per], wl.lr, xs[fill:], ys[fill:], losses, wl.momentum)
+    torch.cuda.synchronize()
+    assert torch.equal(net.params(fill), ref_params[fill])
+    for k in range(reps):
+        graph.launch()
+        torch.cuda.synchronize()
+        t1 = fill + per * (k + 1)
+        assert torch.equal(net.params(t1), ref_params[t1]), f"replay {k}"
+        np.testing.assert_array_equal(losses.cpu().numpy(), np.array(ref_losses[t1 - per:t1], dtype=np.float32))
+        _ = (net.ring.sum() + losses.sum()).item()  # eager work between replays
+    assert torch.equal(net.momentum, ref.momentum)
+    assert torch.equal(net.run_mean, ref.run_mean) and torch.equal(net.run_var, ref.run_var)
+
+
+def test_graph_capture_rejects_fill_and_bad_length(P):
+    wl = synth.resnet20_workload(batch=8)
+    net = P.Net(wl.ops, 8, wl.in_shape, wl.stage_end, [4, 3, 2, 1])
+    xs, ys = synth.batches(wl, 12, 8)
+    xs, ys = torch.from_numpy(xs).cuda(), torch.from_numpy(ys).cuda()
+    losses = torch.zeros(12, device="cuda")
+    st = _table(lambda t: [3, 2, 1, 0], 12, 4)
+    with pytest.raises(P.PswError):   # steps 0..2 clamp their versions
+        net.capture(st, wl.lr, xs, ys, losses)
+    with pytest.raises(P.PswError):   # not a multiple of the period 12
+        net.capture(st[:5], wl.lr, xs, ys, losses)
