@@ -29,8 +29,9 @@ matrix-core figure the metric names, and the dominant kernel (largest summed
 time): `roofline.achieved` = its algorithmic work per launch / its mean
 launch duration.  `roofline.traffic` is
 the HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE counters
-(calibrated on a plain device copy) stored in profiles/traffic.json, used
-only when the kernel sources still hash to what was profiled, else null.
+(calibrated on a plain streaming kernel) stored in profiles/traffic.json,
+used only when the source files defining that kernel still hash to what was
+profiled, else null.
 `cpu_baseline` times the CPU oracle on a bounded sample (2 steps of the same
 workload).
 
@@ -57,30 +58,29 @@ PROFILE_STEPS = 100
 COPY_BYTES = 256 << 20
 
 
-def source_hash():
-    """sha256 over the library's kernel sources (csrc/*.hip, *.h, sorted)."""
-    import hashlib
-
-    d = os.path.join(ROOT, "paper_1912_12675_amd", "csrc")
-    h = hashlib.sha256()
-    for f in sorted(os.listdir(d)):
-        if f.endswith((".hip", ".h")):
-            h.update(f.encode())
-            with open(os.path.join(d, f), "rb") as fh:
-                h.update(fh.read())
-    return h.hexdigest()
-
-
 def measured_traffic(kernel):
     """HBM bytes per launch of `kernel` from profiles/traffic.json, or None
-    when absent, taken for another kernel, or taken on other sources."""
+    when absent, taken for another kernel, or taken on other sources of that
+    kernel (the file records which source files define it and their hash)."""
+    import hashlib
+
     path = os.path.join(ROOT, "profiles", "traffic.json")
     try:
         with open(path) as f:
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel") != kernel or t.get("source_sha256") != source_hash():
+    if t.get("kernel") != kernel or not t.get("sources"):
+        return None
+    h = hashlib.sha256()
+    for rel in t["sources"]:
+        h.update(rel.encode())
+        try:
+            with open(os.path.join(ROOT, rel), "rb") as fh:
+                h.update(fh.read())
+        except OSError:
+            return None
+    if h.hexdigest() != t.get("source_sha256"):
         return None
     return t.get("bytes_per_launch")
 
@@ -164,7 +164,7 @@ def main():
     period = 2
     for d in wl.ring_depth():
         period = period * d // __import__("math").gcd(period, d)
-    T = W + period + KP + 3 * K
+    T = W + period + KP + 3 * K + period
     net = psw.Net(wl.ops, wl.batch, wl.in_shape, wl.stage_end, wl.ring_depth(T), bf16=wl.bf16)
     net.load_params(synth.init_params(wl))
     stal = wl.staleness(T)
@@ -196,10 +196,16 @@ def main():
     graph = None
     glosses = torch.zeros(period, dtype=torch.float32, device="cuda")
 
+    gt0 = W  # the graph is captured at step W
+
     def run_graph(n):
-        # replays of one captured period (the next `period` steps each), the
-        # remainder issued eagerly
+        # eager steps until t is congruent to the capture step modulo the
+        # period, replays of the captured period, the remainder eagerly
         nonlocal t
+        align = min((gt0 - t) % period, n)
+        if align:
+            run_pipelined(align)
+            n -= align
         for _ in range(n // period):
             graph.launch()
             t += period

@@ -65,15 +65,27 @@ def pmc_values(path: str, counter: str):
     return dict(out)
 
 
-def source_hash() -> str:
-    """sha256 over csrc/*.hip, *.h (sorted), as bench.py computes it."""
-    d = os.path.join(ROOT, "paper_1912_12675_amd", "csrc")
+def kernel_sources(kernel: str):
+    """Source files (relative to the repository) that define a library kernel."""
+    base = "paper_1912_12675_amd/csrc/"
+    if kernel.startswith(("conv3x3_direct", "conv3x3_dgrad_s2")):
+        f = "direct.hip"
+    elif kernel.startswith("conv3x3_wgrad"):
+        f = "wgrad.hip"
+    elif kernel.startswith(("igemm_kernel", "reduce_splits")):
+        f = "conv.hip"
+    else:
+        f = "ops.hip"
+    return [base + f, base + "internal.h"]
+
+
+def source_hash(files) -> str:
+    """sha256 over the given files (name and content, in the given order)."""
     h = hashlib.sha256()
-    for f in sorted(os.listdir(d)):
-        if f.endswith((".hip", ".h")):
-            h.update(f.encode())
-            with open(os.path.join(d, f), "rb") as fh:
-                h.update(fh.read())
+    for f in files:
+        h.update(f.encode())
+        with open(os.path.join(ROOT, f), "rb") as fh:
+            h.update(fh.read())
     return h.hexdigest()
 
 
@@ -103,7 +115,8 @@ def traffic(kernel, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_k
             "write_bytes_per_launch": write, "fetch_kib_per_dispatch": _mean(fk[kernel]),
             "write_kib_per_dispatch": _mean(wk[kernel]), "dispatches": [len(fk[kernel]), len(wk[kernel])],
             "copy_kernel": cname, "copy_bytes": copy_bytes, "copy_fetch_kib": _mean(cf), "copy_write_kib": _mean(cw),
-            "fetch_scale": f_scale, "write_scale": w_scale, "source_sha256": source_hash()}
+            "fetch_scale": f_scale, "write_scale": w_scale, "sources": kernel_sources(kernel),
+            "source_sha256": source_hash(kernel_sources(kernel))}
 
 
 def main(argv=None):
