@@ -79,7 +79,7 @@ constexpr int wrow(int n)
     return v;
 }
 
-template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, bool TRANS>
+template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, bool TRANS, int TPW>
 __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
 {
     constexpr int NT = 64 * WK * WP;
@@ -95,10 +95,9 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     __shared__ __attribute__((aligned(16))) float Xs[CC * PS];
     __shared__ float Wc[TK * WR];
 
-    const int tiles = a.HO / TH;
-    const int img = blockIdx.x / tiles;
-    const int oh0 = (blockIdx.x - img * tiles) * TH;
-    const int ih0 = oh0 * STRIDE - 1;
+    constexpr int tiles = WO / TH;       // row tiles per (square) image
+    static_assert(WO % TH == 0, "row tiles");
+    const int T_all = gridDim.x * TPW;   // tiles of the launch (BN partial index)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wk = wave % WK, wp = wave / WK;
     const int mblk = blockIdx.y * TK;
@@ -123,8 +122,13 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     }
 
     // software pipeline over input-channel chunks: the next chunk's tile and
-    // weights are loaded into registers while the current chunk computes
+    // weights are loaded into registers while the current chunk computes.
+    // A thread's staging coordinates are the same for every chunk and tile,
+    // so they are computed once; global offsets are 32-bit (the launcher
+    // checks the tensor sizes), so loads take a uniform base and a lane
+    // offset.  Images are square: input height = WIN, output height = WO.
     constexpr int Q4 = WIN / 4;
+    constexpr int HIN = WIN;
     constexpr int XN = CC * HR * Q4;
     // weights: TK runs of CC*9 floats (forward) or CC runs of TK*9 floats
     // (transposed), both multiples of 4: loaded as float4, stored as scalars
@@ -132,43 +136,64 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     static_assert((CC * 9) % 4 == 0 && (TK * 9) % 4 == 0, "float4 weight runs");
     constexpr int XV = (XN + NT - 1) / NT, WV = (WN4 + NT - 1) / NT;
     const bool wvec = (a.C % 4 == 0) && (TRANS ? (a.K % 4 == 0) : true) && ((uintptr_t)a.w % 16 == 0);
+    int xl[XV], xg[XV], xrow[XV], xch[XV];  // LDS offset, offset from (plane c0, row ih0), row, channel
+#pragma unroll
+    for (int k = 0; k < XV; ++k) {
+        const int i = tid + k * NT;
+        const int c = i / (HR * Q4);
+        const int rem = i - c * (HR * Q4);
+        const int rr = rem / Q4, q4 = rem - (rem / Q4) * Q4;
+        xl[k] = c * PS + rr * RSTR + 4 + q4 * 4;
+        xg[k] = (c * HIN + rr) * WIN + q4 * 4;
+        xrow[k] = rr;
+        xch[k] = i < XN ? c : CC;  // CC: past the chunk (never loaded or stored)
+    }
+    int wl[WV], wg[WV], wc[WV];  // forward: LDS offset, offset from channel 0, channel; transposed: run base
+#pragma unroll
+    for (int k = 0; k < WV; ++k) {
+        const int i = (tid + k * NT) * 4;
+        if (!TRANS) {
+            const int m = i / (CC * 9), rem = i - (i / (CC * 9)) * (CC * 9);
+            wl[k] = m * WR + rem;
+            wg[k] = (mblk + m) * a.C * 9 + rem;
+            wc[k] = rem / 9;  // first channel of the run (a run of 4 may cross into the next channel)
+        } else {
+            const int c = i / (TK * 9), rem = i - (i / (TK * 9)) * (TK * 9);
+            wl[k] = rem;
+            wg[k] = c * a.K * 9 + mblk * 9 + rem;
+            wc[k] = c;
+        }
+        if (i >= WN4 * 4) wc[k] = -1;  // past the weights of a chunk
+    }
     float4 xr[XV];
     float4 wr[WV];
-    auto load_chunk = [&](int c0) {
+    auto load_chunk = [&](int img, int ih0, int c0) {  // channels c0.. of tile (img, rows from ih0)
+        const int xb = ((img * a.C + c0) * HIN + ih0) * WIN;
 #pragma unroll
         for (int k = 0; k < XV; ++k) {
-            const int i = tid + k * NT;
             float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (i < XN) {
-                const int c = i / (HR * Q4);
-                const int rem = i - c * (HR * Q4);
-                const int rr = rem / Q4, q4 = rem - (rem / Q4) * Q4;
-                const int ih = ih0 + rr;
-                if (ih >= 0 && ih < a.H && c0 + c < a.C)
-                    v = *reinterpret_cast<const float4*>(a.x + (((size_t)img * a.C + c0 + c) * a.H + ih) * WIN + q4 * 4);
-            }
+            const int ih = ih0 + xrow[k];
+            if (xch[k] < CC && ih >= 0 && ih < HIN && c0 + xch[k] < a.C)
+                v = *reinterpret_cast<const float4*>(a.x + (xb + xg[k]));
             xr[k] = v;
         }
 #pragma unroll
         for (int k = 0; k < WV; ++k) {
-            const int i4 = tid + k * NT;
             float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (i4 < WN4) {
-                const int i = i4 * 4;
+            if (wc[k] >= 0) {
                 if (!TRANS) {  // w[m][c][rs]: each output channel's CC*9 run is contiguous
-                    const int m = i / (CC * 9), rem = i - (i / (CC * 9)) * (CC * 9);
-                    const float* src = a.w + ((size_t)(mblk + m) * a.C + c0) * 9 + rem;
+                    const float* src = a.w + (wg[k] + c0 * 9);
                     if (wvec && c0 + CC <= a.C) {
                         v = *reinterpret_cast<const float4*>(src);
                     } else {  // narrow input (C < CC) or misaligned: element-wise with bounds
+                        const int rem = wl[k] - (wl[k] / WR) * WR;
                         float t[4];
                         for (int e = 0; e < 4; ++e) t[e] = (c0 + (rem + e) / 9 < a.C) ? src[e] : 0.f;
                         v = make_float4(t[0], t[1], t[2], t[3]);
                     }
                 } else {       // w_layer[c][m][rs]: each input channel's TK*9 run is contiguous
-                    const int c = i / (TK * 9), rem = i - (i / (TK * 9)) * (TK * 9);
-                    const float* src = a.w + ((size_t)(c0 + c) * a.K + mblk) * 9 + rem;
-                    if (c0 + c < a.C) {
+                    const float* src = a.w + (wg[k] + c0 * a.K * 9);
+                    if (c0 + wc[k] < a.C) {
                         if (wvec) {
                             v = *reinterpret_cast<const float4*>(src);
                         } else {
@@ -182,43 +207,42 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     };
     auto store_chunk = [&]() {
 #pragma unroll
-        for (int k = 0; k < XV; ++k) {
-            const int i = tid + k * NT;
-            if (i < XN) {
-                const int c = i / (HR * Q4);
-                const int rem = i - c * (HR * Q4);
-                const int rr = rem / Q4, q4 = rem - (rem / Q4) * Q4;
-                *reinterpret_cast<float4*>(&Xs[c * PS + rr * RSTR + 4 + q4 * 4]) = xr[k];
-            }
-        }
+        for (int k = 0; k < XV; ++k)
+            if (xch[k] < CC) *reinterpret_cast<float4*>(&Xs[xl[k]]) = xr[k];
 #pragma unroll
         for (int k = 0; k < WV; ++k) {
-            const int i4 = tid + k * NT;
-            if (i4 < WN4) {
-                const int i = i4 * 4;
-                const float vv[4] = {wr[k].x, wr[k].y, wr[k].z, wr[k].w};
-                if (!TRANS) {
-                    const int m = i / (CC * 9), rem = i - (i / (CC * 9)) * (CC * 9);
+            if (wc[k] < 0) continue;
+            const float vv[4] = {wr[k].x, wr[k].y, wr[k].z, wr[k].w};
+            if (!TRANS) {
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) Wc[m * WR + rem + e] = vv[e];  // a run never crosses m (CC*9 % 4 == 0)
-                } else {  // flip the taps
-                    const int c = i / (TK * 9), rem = i - (i / (TK * 9)) * (TK * 9);
+                for (int e = 0; e < 4; ++e) Wc[wl[k] + e] = vv[e];  // a run never crosses m (CC*9 % 4 == 0)
+            } else {  // flip the taps
+                const int rem = wl[k];
 #pragma unroll
-                    for (int e = 0; e < 4; ++e) {
-                        const int m = (rem + e) / 9, rsl = (rem + e) - ((rem + e) / 9) * 9;
-                        Wc[m * WR + c * 9 + 8 - rsl] = vv[e];
-                    }
+                for (int e = 0; e < 4; ++e) {
+                    const int m = (rem + e) / 9, rsl = (rem + e) - ((rem + e) / 9) * 9;
+                    Wc[m * WR + wc[k] * 9 + 8 - rsl] = vv[e];
                 }
             }
         }
     };
 
-    load_chunk(0);
+    // TPW consecutive row tiles per workgroup; the software pipeline runs
+    // across them: the first chunk of the next tile is loaded while the last
+    // chunk of the current one is on the matrix cores
+    load_chunk(blockIdx.x * TPW / tiles, (blockIdx.x * TPW % tiles) * TH * STRIDE - 1, 0);
+    for (int q = 0; q < TPW; ++q) {
+    const int tl = blockIdx.x * TPW + q;
+    const int img = tl / tiles;
+    const int oh0 = (tl - img * tiles) * TH;
     for (int c0 = 0; c0 < a.C; c0 += CC) {
         __syncthreads();  // the previous chunk's LDS reads are complete
         store_chunk();
         __syncthreads();
-        if (c0 + CC < a.C) load_chunk(c0 + CC);
+        if (c0 + CC < a.C)
+            load_chunk(img, oh0 * STRIDE - 1, c0 + CC);
+        else if (q + 1 < TPW)
+            load_chunk((tl + 1) / tiles, ((tl + 1) % tiles) * TH * STRIDE - 1, 0);
         const float* wf = Wc + (wk * 16 + j) * WR + g * 9;
 #pragma unroll
         for (int c4 = 0; c4 < CC / 4; ++c4)
@@ -238,14 +262,14 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     // epilogue: every global load is issued before the first store (the
     // output may alias nothing, but the compiler cannot know that, and a
     // load after a store would wait for it)
-    size_t oidx[NBW];  // index of (channel mblk+wk*16+4g, pixel) of block nb
+    int oidx[NBW];  // index of (channel mblk+wk*16+4g, pixel) of block nb
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
         const int pix = (wp * NBW + nb) * 16 + j;
         const int row = pix / WO, col = pix - (pix / WO) * WO;
-        oidx[nb] = (((size_t)img * a.K + mblk + wk * 16 + 4 * g) * a.HO + oh0 + row) * WO + col;
+        oidx[nb] = ((img * a.K + mblk + wk * 16 + 4 * g) * WO + oh0 + row) * WO + col;
     }
-    const size_t cstr = (size_t)a.HO * WO;  // channel stride
+    constexpr int cstr = WO * WO;  // channel stride
     if (a.accumulate) {
         float old[NBW][4];
 #pragma unroll
@@ -317,8 +341,8 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
                         t2 += red[(WP + q) * TK + wk * 16 + 4 * g + i];
                     }
                     const int m = mblk + wk * 16 + 4 * g + i;
-                    a.bnb.part[((size_t)m * gridDim.x + blockIdx.x) * 2 + 0] = t1;
-                    a.bnb.part[((size_t)m * gridDim.x + blockIdx.x) * 2 + 1] = t2;
+                    a.bnb.part[((size_t)m * T_all + tl) * 2 + 0] = t1;
+                    a.bnb.part[((size_t)m * T_all + tl) * 2 + 1] = t2;
                 }
         }
     }
@@ -366,18 +390,21 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) red[wp * TK + wk * 16 + 4 * g + i] = sv[i];
             __syncthreads();
-            const int T = gridDim.x;
+
             if (wp == 0 && j == 0)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
                     float t = 0.f;
                     for (int q = 0; q < WP; ++q) t += red[q * TK + wk * 16 + 4 * g + i];
                     const int m = mblk + wk * 16 + 4 * g + i;
-                    a.bn.part[((size_t)m * T + blockIdx.x) * 2 + 0] = mu[i];
-                    a.bn.part[((size_t)m * T + blockIdx.x) * 2 + 1] = t;
+                    a.bn.part[((size_t)m * T_all + tl) * 2 + 0] = mu[i];
+                    a.bn.part[((size_t)m * T_all + tl) * 2 + 1] = t;
                 }
         }
     }
+#pragma unroll
+    for (int nb = 0; nb < NBW; ++nb) acc[nb] = v4f{0.f, 0.f, 0.f, 0.f};
+    }  // tiles
 }
 
 // Backward-data of a 3x3 / pad 1 / stride 2 convolution: dx (H = 2*HO) from
@@ -594,10 +621,11 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
     }
 }
 
-template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW>
+template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, int TPW = 1>
 hipError_t launch_direct(const DirArgs& a, int n, bool trans, hipStream_t st)
 {
-    dim3 grid(n * (a.HO / TH), a.K / (16 * WK));
+    if ((n * (a.HO / TH)) % TPW) return hipErrorNotSupported;
+    dim3 grid(n * (a.HO / TH) / TPW, a.K / (16 * WK));
     dim3 block(64 * WK * WP);
     // as a convolution: input a.C x a.H x WO*STRIDE, output a.K x a.HO x WO
     Work wk = conv_work(n, a.C, a.H, WO * STRIDE, a.K, 3, 3, a.HO, WO);
@@ -605,11 +633,11 @@ hipError_t launch_direct(const DirArgs& a, int n, bool trans, hipStream_t st)
     if (a.accumulate) wk.bytes += out_bytes;        // the existing output is read
     if (a.bnb.part) wk.bytes += (a.bnb.scale ? 1.0 : 2.0) * out_bytes;  // BN input (and output) for the sums
     if (trans)
-        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true), wk,
-                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true>), grid, block, 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW), wk,
+                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW>), grid, block, 0, st, a);
     else
-        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, false), wk,
-                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, false>), grid, block, 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, false, TPW), wk,
+                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, false, TPW>), grid, block, 0, st, a);
     return hipGetLastError();
 }
 
@@ -619,7 +647,8 @@ hipError_t launch_direct(const DirArgs& a, int n, bool trans, hipStream_t st)
 // covers the shape; the caller then uses the general implicit GEMM.
 int conv3x3_direct_tiles(int n, int C, int H, int W, int K, int stride)
 {
-    if ((stride != 1 && stride != 2) || H % stride || W % stride) return 0;
+    if ((stride != 1 && stride != 2) || H % stride || W % stride || H != W) return 0;
+    if ((int64_t)n * C * H * W > INT32_MAX || (int64_t)n * K * (H / stride) * (W / stride) > INT32_MAX) return 0;
     const int HO = H / stride, WO = W / stride;
     if (C <= 4 && stride == 1) return (WO == 32 && HO % 8 == 0 && K % 16 == 0) ? n * (HO / 8) : 0;
     if (C % 16) return 0;
@@ -634,7 +663,10 @@ hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const f
 {
     if (bnb && (!transpose || stride != 1)) return hipErrorNotSupported;
     if (stride != 1 && stride != 2) return hipErrorNotSupported;
-    if (H % stride || W % stride) return hipErrorNotSupported;
+    if (H % stride || W % stride || H != W) return hipErrorNotSupported;  // square images (compile-time strides)
+    // 32-bit element offsets inside the kernel
+    if ((int64_t)n * C * H * W > INT32_MAX || (int64_t)n * K * (H / stride) * (W / stride) > INT32_MAX)
+        return hipErrorNotSupported;
     if (bn && transpose) return hipErrorNotSupported;
     if ((uintptr_t)x % 16) return hipErrorNotSupported;  // float4 tile staging
     const int HO = H / stride, WO = W / stride;
@@ -693,7 +725,8 @@ namespace psw {
 int dgrad_bnsums_tiles(int n, int CL, int H, int W, int KL, int stride)
 {
     if (stride == 1) {
-        if (KL % 16) return 0;
+        if (KL % 16 || H != W) return 0;
+        if ((int64_t)n * (CL > KL ? CL : KL) * H * W > INT32_MAX) return 0;
         if (W == 32 && H % 8 == 0 && CL % 16 == 0) return n * (H / 8);
         if (W == 16 && H % 8 == 0 && CL % 32 == 0) return n * (H / 8);
         if (W == 8 && H % 8 == 0 && CL % 32 == 0) return n * (H / 8);

@@ -607,7 +607,9 @@ namespace {
 // channel see bit-identical coefficients), then transforms its share of the
 // channel's n*hw elements.  Element loops walk float4 units of one channel
 // (unit u: image u / hw4, offset 4*(u % hw4)) with 32-bit index arithmetic.
-constexpr int kApplyUnits = 1024;  // float4 units per block (a multiple of kBlock)
+// A block of either kernel covers U float4 units per thread of one channel;
+// U is chosen per launch (apply_units_per_thread) so that small layers get
+// more, shorter blocks.
 
 // forward: tile partials (mean_t, M2_t over P pixels each), merged in one
 // pass in double:
@@ -617,8 +619,7 @@ constexpr int kApplyUnits = 1024;  // float4 units per block (a multiple of kBlo
 // issued before the merge so that the two memory latencies overlap, and
 // every load precedes every store.  Block y == 0 also stores the channel's
 // scale and shift, which the backward recomputes the ReLU mask from.
-constexpr int kUnitsPerThread = kApplyUnits / kBlock;
-
+template <int U>
 __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int hw, const float* y, const float* part,
                                                                int T, int P, const float* gamma, const float* beta,
                                                                const float* res, int rc, int rh, int rw, int h, int w,
@@ -631,12 +632,11 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
     const int ch = blockIdx.x;
     const int hw4 = hw >> 2;
     const int units = n * hw4;
-    const int u0 = blockIdx.y * kApplyUnits;
-    const int u1 = min(u0 + kApplyUnits, units);
+    const int u0 = blockIdx.y * (U * kBlock);
+    const int u1 = min(u0 + U * kBlock, units);
     const bool identity = res && rc == c && rh == h && rw == w;
     const int lo = (c - rc) / 2, cc = ch - lo;
     const bool shortcut_a = res && !identity && cc >= 0 && cc < rc;
-    constexpr int U = kUnitsPerThread;
     size_t idx[U];
     float4 yv[U], rv[U];
 #pragma unroll
@@ -714,6 +714,7 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
 // side) g at the even positions of channel ch - lo and zero elsewhere.
 // With scale set (a BN without residual) the mask is fmaf(y, scale, shift)
 // > 0, the forward's own pre-activation, and z is not read.
+template <int U>
 __global__ __launch_bounds__(kBlock) void bn_bwd_partials_k(int n, int c, int hw, int w, const float* dz,
                                                              const float* z, const float* y, const float* gamma,
                                                              const float* mean, const float* invstd,
@@ -726,13 +727,12 @@ __global__ __launch_bounds__(kBlock) void bn_bwd_partials_k(int n, int c, int hw
     const int ch = blockIdx.x;
     const int hw4 = hw >> 2;
     const int units = n * hw4;
-    const int u0 = blockIdx.y * kApplyUnits;
-    const int u1 = min(u0 + kApplyUnits, units);
+    const int u0 = blockIdx.y * (U * kBlock);
+    const int u1 = min(u0 + U * kBlock, units);
     const bool ymask = relu && scale, zmask = relu && !scale;
     const float sc = ymask ? scale[ch] : 0.f, sf = ymask ? scale[c + ch] : 0.f;
     const int cc = ch - (c - rc) / 2;  // residual channel (option A)
     const bool identity = res_mode == 1, shortcut_a = res_mode == 2 && cc >= 0 && cc < rc;
-    constexpr int U = kUnitsPerThread;
     size_t idx[U];
     float4 gv[U], zv[U], yv[U], ov[U];
 #pragma unroll
@@ -811,6 +811,15 @@ __global__ __launch_bounds__(kBlock) void bn_bwd_partials_k(int n, int c, int hw
 }
 
 bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+// units per thread: the largest of 4, 2, 1 that still gives >= 1024 blocks
+// (four per CU), else 1
+int apply_units_per_thread(int64_t units_total)
+{
+    for (int u = 4; u > 1; u /= 2)
+        if (units_total / ((int64_t)u * kBlock) >= 1024) return u;
+    return 1;
+}
 }  // namespace
 
 hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, const float* part, int T, int P,
@@ -822,12 +831,22 @@ hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, co
     if (w % 4 || !aligned16(y) || !aligned16(z) || (identity && !aligned16(res))) return hipErrorNotSupported;
     const int64_t units = (int64_t)n * h * w / 4;
     if (units > INT32_MAX) return hipErrorNotSupported;
-    const unsigned per_ch = (unsigned)((units + kApplyUnits - 1) / kApplyUnits);
+    const int U = apply_units_per_thread(units * c);
+    const unsigned per_ch = (unsigned)((units + U * kBlock - 1) / (U * kBlock));
     const double total = (double)n * c * h * w;
     const double rbytes = res ? kF * (double)n * std::min(c, rc) * h * w : 0.0;
-    PSW_LAUNCH(kname("bn_apply_partials_k"), (Work{3.0 * total, 2 * kF * total + rbytes + 2 * kF * T * c}),
-               bn_apply_partials_k, dim3(c, per_ch), dim3(kBlock), 0, st, n, c, h * w, y, part, T, P, gamma, beta, res,
-               rc, rh, rw, h, w, relu, eps, momentum, z, save_mean, save_invstd, save_scale, run_mean, run_var);
+    const Work wk{3.0 * total, 2 * kF * total + rbytes + 2 * kF * T * c};
+#define PSW_BN_APPLY(UU)                                                                                          \
+    PSW_LAUNCH(kname("bn_apply_partials_k", UU), wk, bn_apply_partials_k<UU>, dim3(c, per_ch), dim3(kBlock), 0, st, n, c, \
+               h * w, y, part, T, P, gamma, beta, res, rc, rh, rw, h, w, relu, eps, momentum, z, save_mean,          \
+               save_invstd, save_scale, run_mean, run_var)
+    if (U == 4)
+        PSW_BN_APPLY(4);
+    else if (U == 2)
+        PSW_BN_APPLY(2);
+    else
+        PSW_BN_APPLY(1);
+#undef PSW_BN_APPLY
     return hipGetLastError();
 }
 
@@ -848,14 +867,23 @@ hipError_t bn_bwd_from_partials(int n, int c, int h, int w, const float* dz, con
         return hipErrorNotSupported;
     const int64_t units = (int64_t)n * h * w / 4;
     if (units > INT32_MAX) return hipErrorNotSupported;
-    const unsigned per_ch = (unsigned)((units + kApplyUnits - 1) / kApplyUnits);
+    const int U = apply_units_per_thread(units * c);
+    const unsigned per_ch = (unsigned)((units + U * kBlock - 1) / (U * kBlock));
     const double total = (double)n * c * h * w;
     double bytes = kF * ((relu && !scale ? 4.0 : 3.0) * total) + 2 * kF * T * c;  // dz, y, (z), dy
     if (res_mode == 1) bytes += kF * (1.0 + res_accumulate) * total;
     if (res_mode == 2) bytes += kF * (double)n * rc * rh * rw + (res_accumulate ? kF * (double)n * rc * h * w * 2 : 0.0);
-    PSW_LAUNCH(kname("bn_bwd_partials_k"), (Work{6.0 * total, bytes}), bn_bwd_partials_k, dim3(c, per_ch), dim3(kBlock),
-               0, st, n, c, h * w, w, dz, z, y, gamma, mean, invstd, scale, part, T, relu, dy, dgamma, dbeta, dres, rc,
-               res_mode, res_accumulate);
+#define PSW_BN_BWD(UU)                                                                                            \
+    PSW_LAUNCH(kname("bn_bwd_partials_k", UU), (Work{6.0 * total, bytes}), bn_bwd_partials_k<UU>, dim3(c, per_ch),     \
+               dim3(kBlock), 0, st, n, c, h * w, w, dz, z, y, gamma, mean, invstd, scale, part, T, relu, dy, dgamma,   \
+               dbeta, dres, rc, res_mode, res_accumulate)
+    if (U == 4)
+        PSW_BN_BWD(4);
+    else if (U == 2)
+        PSW_BN_BWD(2);
+    else
+        PSW_BN_BWD(1);
+#undef PSW_BN_BWD
     return hipGetLastError();
 }
 

@@ -1,12 +1,24 @@
-"""Write the oracle's result for the full-size ResNet-20 runs (batch 128,
-4 stages at the Table 1 PPV (7,13,19), staleness [3,2,1,0], 50 steps, lr 0.01,
-momentum 0.9) to tests/golden/.  Calls only the oracle and the seeded input
-generator; never the GPU path.
+"""Write the oracle's results for the full-size runs to tests/golden/.
+Calls only the oracle and the seeded input generator; never the GPU path.
 
-    python tests/golden/make_golden.py [fp32|bf16 ...]
+    python tests/golden/make_golden.py [fp32|bf16|alexnet|vgg16|resnet110 ...]
 
-Stored: the parameter update W^(50) - W^(0) (float32; W^(0) is regenerated
-from the seed), the 50 losses and the version table.
+fp32 / bf16: ResNet-20, batch 128, 4 stages at the Table 1 PPV (7,13,19),
+staleness [3,2,1,0], 50 steps, lr 0.01, momentum 0.9.  Stored: the
+parameter update W^(50) - W^(0) (float32; W^(0) is regenerated from the
+seed), the 50 losses and the version table.
+
+alexnet / vgg16 / resnet110: the other full-size configurations (AlexNet-style
+net, batch 128, 20 steps, split after conv2, staleness [2,0]; VGG-16-BN,
+batch 128, 30 stale steps at PPV (2,4,7) then 10 non-pipelined; ResNet-110,
+batch 256, bf16 products, 8 stages with d_s = 7-s, the first 3 steps).
+These nets have up to 86M parameters, so what is stored is: the losses, the
+version table, the L2 norm of every parameter tensor and of its update, and
+the values of a seeded sample of 200,000 final parameters.  Each is run twice:
+on the inputs, and on the inputs moved one float32 ulp (seeded signs); the
+distance between the two runs (the oracle's own sensitivity to rounding-level
+changes, "spread") is stored beside the result and sets the test's bar where
+it exceeds the target tolerance.
 """
 import os
 import sys
@@ -20,6 +32,9 @@ sys.path.insert(0, ROOT)
 from oracle import oracle as O  # noqa: E402
 from paper_1912_12675_amd import synth  # noqa: E402
 
+HERE = os.path.dirname(os.path.abspath(__file__))
+SAMPLE = 200_000
+
 
 def make(mode):
     wl = synth.resnet20_workload(bf16=(mode == "bf16"))
@@ -29,12 +44,75 @@ def make(mode):
     t0 = time.time()
     out = O.train(wl.ops, wl.in_shape, wl.stage_end, p0, xs, ys, wl.staleness(T), wl.lr, wl.momentum,
                   wl.weight_decay, wl.nesterov, bf16=wl.bf16)
-    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), f"resnet20_b128_50steps_{mode}.npz")
+    path = os.path.join(HERE, f"resnet20_b128_50steps_{mode}.npz")
     np.savez_compressed(path, delta=(out["params"] - p0.astype(np.float64)).astype(np.float32),
                         losses=out["losses"], versions=out["versions"])
     print(f"{mode}: {time.time() - t0:.0f} s, final loss {out['losses'][-1]:.6f} -> {path}", flush=True)
 
 
+def sample_index(n):
+    """Seeded, sorted sample of parameter indices (all of them when n <= SAMPLE)."""
+    if n <= SAMPLE:
+        return np.arange(n, dtype=np.int64)
+    return np.sort(np.random.Generator(np.random.PCG64(20260)).choice(n, size=SAMPLE, replace=False))
+
+
+def tensor_norms(wl, flat, p0):
+    layout, counts = synth.param_layout(wl)
+    base = np.concatenate([[0], np.cumsum(counts)])
+    norms, dnorms = [], []
+    for op, name, shape, s, off in layout:
+        i0 = int(base[s]) + off
+        seg = flat[i0:i0 + int(np.prod(shape))]
+        norms.append(np.linalg.norm(seg))
+        dnorms.append(np.linalg.norm(seg - p0[i0:i0 + int(np.prod(shape))]))
+    return np.array(norms), np.array(dnorms)
+
+
+def ulp_move(x, seed):
+    """x moved one float32 ulp up or down elementwise (seeded signs)."""
+    up = np.random.Generator(np.random.PCG64(seed)).random(x.shape) < 0.5
+    return np.where(up, np.nextafter(x, np.float32(np.inf)), np.nextafter(x, np.float32(-np.inf))).astype(np.float32)
+
+
+FULL = {
+    "alexnet": (lambda: synth.alexnet_workload(), 20),
+    "vgg16": (lambda: synth.vgg16_workload(), 40),
+    "resnet110": (lambda: synth.resnet110_workload(), 3),
+}
+
+
+def make_full(name):
+    factory, T = FULL[name]
+    wl = factory()
+    p0 = synth.init_params(wl).astype(np.float64)
+    xs, ys = synth.batches(wl, T)
+    st = wl.staleness(T)
+    idx = sample_index(p0.size)
+    res = []
+    t0 = time.time()
+    for x in (xs, ulp_move(xs, 1912)):
+        out = O.train(wl.ops, wl.in_shape, wl.stage_end, p0, x, ys, st, wl.lr, wl.momentum, wl.weight_decay,
+                      wl.nesterov, bf16=wl.bf16)
+        norms, dnorms = tensor_norms(wl, out["params"], p0)
+        res.append(dict(sample=out["params"][idx], norms=norms, dnorms=dnorms, losses=out["losses"],
+                        versions=out["versions"]))
+        print(f"{name}: run {len(res)} {time.time() - t0:.0f} s, final loss {out['losses'][-1]:.6f}", flush=True)
+        del out
+    a, b = res
+    s0 = p0[idx]
+    spread = dict(
+        sample=np.linalg.norm(a["sample"] - b["sample"]) / np.linalg.norm(a["sample"]),
+        update=np.linalg.norm(a["sample"] - b["sample"]) / max(np.linalg.norm(a["sample"] - s0), 1e-30),
+        loss=np.abs(a["losses"] - b["losses"]).max() / np.abs(a["losses"]).max(),
+        norm=np.max(np.abs(a["norms"] - b["norms"]) / np.maximum(a["norms"], 1e-30)))
+    path = os.path.join(HERE, f"{name}_full_{T}steps.npz")
+    np.savez_compressed(path, index=idx, sample=a["sample"], norms=a["norms"], dnorms=a["dnorms"],
+                        losses=a["losses"], versions=a["versions"], steps=T,
+                        **{"spread_" + k: v for k, v in spread.items()})
+    print(f"{name}: spread {spread} -> {path}", flush=True)
+
+
 if __name__ == "__main__":
     for m in (sys.argv[1:] or ["fp32", "bf16"]):
-        make(m)
+        make(m) if m in ("fp32", "bf16") else make_full(m)

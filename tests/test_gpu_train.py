@@ -364,3 +364,53 @@ def test_graph_capture_rejects_fill_and_bad_length(P):
         net.capture(st, wl.lr, xs, ys, losses)
     with pytest.raises(P.PswError):   # not a multiple of the period 12
         net.capture(st[:5], wl.lr, xs, ys, losses)
+
+
+# ---- the other configurations at full size, against stored oracle runs ----
+FULL_CASES = [
+    ("alexnet", lambda: synth.alexnet_workload(), 20),
+    ("vgg16", lambda: synth.vgg16_workload(), 40),
+    ("resnet110", lambda: synth.resnet110_workload(), 3),
+]
+
+
+@pytest.mark.parametrize("name,factory,T", FULL_CASES, ids=[c[0] for c in FULL_CASES])
+def test_full_size_against_oracle(P, name, factory, T):
+    """Full-size AlexNet (b128, 20 steps), VGG-16-BN (b128, 30 stale + 10
+    non-pipelined steps) and ResNet-110 (b256, bf16 products, 8 stages, 3
+    steps), run as the pipelined execution, against the oracle's stored run
+    (tests/golden/make_golden.py): losses, versions, the L2 norm of every
+    parameter tensor and a seeded sample of 200,000 final parameters.  Bar:
+    the target (1e-4 fp32 / 2e-2 bf16 on parameters; 2e-3 / 2e-2 on losses)
+    or 4x the oracle's own distance between runs on inputs one ulp apart,
+    whichever is larger."""
+    g = np.load(os.path.join(GOLDEN, f"{name}_full_{T}steps.npz"))
+    wl = factory()
+    st = wl.staleness(T)
+    net = P.Net(wl.ops, wl.batch, wl.in_shape, wl.stage_end, wl.ring_depth(T), bf16=wl.bf16)
+    p0 = synth.init_params(wl)
+    net.load_params(p0)
+    xs, ys = synth.batches(wl, T)
+    losses = torch.zeros(T, device="cuda")
+    ver = net.pipeline_run(0, st, wl.lr, torch.from_numpy(xs).cuda(), torch.from_numpy(ys).cuda(), losses,
+                           wl.momentum, wl.weight_decay, wl.nesterov)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(ver, g["versions"])
+    flat = net.params(T).double().cpu().numpy()
+    p0 = p0.astype(np.float64)
+    layout, counts = synth.param_layout(wl)
+    base = np.concatenate([[0], np.cumsum(counts)])
+    norms = np.array([np.linalg.norm(flat[int(base[s]) + off:int(base[s]) + off + int(np.prod(shape))])
+                      for _, _, shape, s, off in layout])
+    samp = flat[g["index"]]
+    pbar = max(2e-2 if wl.bf16 else 1e-4, 4 * float(g["spread_sample"]))
+    lbar = max(2e-2 if wl.bf16 else 2e-3, 4 * float(g["spread_loss"]))
+    nbar = max(2e-2 if wl.bf16 else 1e-4, 4 * float(g["spread_norm"]))
+    d_sample = np.linalg.norm(samp - g["sample"]) / np.linalg.norm(g["sample"])
+    d_loss = np.abs(losses.cpu().numpy() - g["losses"]).max() / np.abs(g["losses"]).max()
+    d_norm = np.max(np.abs(norms - g["norms"]) / np.maximum(g["norms"], 1e-30))
+    print(f"{name}: sample {d_sample:.2e} (bar {pbar:.1e}), loss {d_loss:.2e} (bar {lbar:.1e}), "
+          f"tensor norms {d_norm:.2e} (bar {nbar:.1e}); oracle spread sample {float(g['spread_sample']):.2e} "
+          f"loss {float(g['spread_loss']):.2e}")
+    assert np.isfinite(flat).all()
+    assert d_sample <= pbar and d_loss <= lbar and d_norm <= nbar
