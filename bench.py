@@ -10,7 +10,7 @@ overlaps the backward pass of mini-batch t where the stale weights allow it
 (psw_pipeline_run; results identical to one psw_stage_step call per step).
 By default the timed steps are one eager psw_pipeline_run call; --mode
 graph replays a HIP graph that captured one period (lcm of the ring depths
-and 2 = 12 steps) of the pipeline, --mode sequential makes one
+and of the 3 step sets = 12 steps) of the pipeline, --mode sequential makes one
 psw_stage_step call per step; the modes not selected are timed over K more
 steps for context (on ROCm 7.2 the graph replays of this three-stream
 pipeline run slower than issuing it eagerly).  Inputs
@@ -161,7 +161,7 @@ def main():
     wl = synth.resnet20_workload(bf16=args.bf16)
     K, W = args.steps, args.warmup
     KP = 0 if args.no_profile else min(K, PROFILE_STEPS)
-    period = 2
+    period = 3  # step sets of the pipelined run
     for d in wl.ring_depth():
         period = period * d // __import__("math").gcd(period, d)
     T = W + period + KP + 3 * K + period

@@ -258,8 +258,11 @@ int psw_stage_step(psw_net *net, int64_t t, const int32_t *staleness, const floa
  * waits for the update that wrote its version t - d_s, so with d_s >= 1 it
  * overlaps the backward pass of step t-1 (with every d_s = 0 nothing
  * overlaps, as in plain SGD).  The step sets (activations, saved
- * statistics) alternate between the net's arena and a second set bound with
- * psw_net_bind_pipeline (psw_net_pipeline_bytes gives its size).
+ * statistics, gradients) rotate between the net's arena and one or two more
+ * sets bound with psw_net_bind_pipeline: psw_net_pipeline_bytes gives the
+ * size of one set; `bytes` covering two sets gives three step sets, so the
+ * forward pass of step t waits for the weight stream to finish step t-3
+ * instead of t-2.
  * staleness and lr: host arrays [n_steps][n_stages].  x: device array of
  * n_batches mini-batches [n_batches][batch,c0,h0,w0]; step t0+i uses batch
  * i mod n_batches (labels likewise [n_batches][batch]); every batch must

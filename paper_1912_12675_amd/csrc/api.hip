@@ -295,14 +295,16 @@ struct psw_net {
     hipStream_t side = nullptr;
     std::vector<hipEvent_t> stage_ev;       // per stage: the chain is done with the stage
     hipEvent_t join_ev = nullptr;
-    // pipelined runs (psw_pipeline_run): forward stream, second step set,
-    // per-stage update events indexed by version mod upd_q, per step-set
-    // parity "weight stream done with the step" events
+    // pipelined runs (psw_pipeline_run): forward stream, further step sets,
+    // per-stage update events indexed by version mod upd_q, per step set
+    // "weight stream done with the step" events
     hipStream_t fwd = nullptr;
-    char* step2 = nullptr;
+    static constexpr int kMaxSets = 3;
+    char* sets[kMaxSets] = {nullptr, nullptr, nullptr};  // step sets: [0] in the arena, more bound for pipelining
+    int nsets = 1;
     int upd_q = 0;
     std::vector<hipEvent_t> upd_ev;
-    hipEvent_t wdone_ev[2] = {nullptr, nullptr};
+    hipEvent_t wdone_ev[kMaxSets] = {nullptr, nullptr, nullptr};
     hipEvent_t fdone_ev = nullptr, start_ev = nullptr;
     // bound memory
     float *ring = nullptr, *momentum = nullptr, *grad = nullptr, *run_mean = nullptr, *run_var = nullptr;
@@ -1087,6 +1089,7 @@ int psw_net_bind_pipeline(psw_net* net, void* step_set, size_t bytes)
     if (!net->bound) return fail(PSW_ERR_STATE, "net_bind_pipeline: bind the net first");
     if (bytes < net->step_bytes)
         return fail(PSW_ERR_WORKSPACE, "net_bind_pipeline: %zu < %zu bytes", bytes, net->step_bytes);
+    const int extra = (int)std::min<size_t>(bytes / net->step_bytes, psw_net::kMaxSets - 1);
     if (((uintptr_t)step_set) % 256 != 0) return fail(PSW_ERR_SHAPE, "net_bind_pipeline: must be 256-byte aligned");
     if (!net->fwd) {
         hipError_t e = hipStreamCreateWithFlags(&net->fwd, hipStreamNonBlocking);
@@ -1108,7 +1111,9 @@ int psw_net_bind_pipeline(psw_net* net, void* step_set, size_t bytes)
             if (e != hipSuccess) return hip_check(e, "net_bind_pipeline: events");
         }
     }
-    net->step2 = (char*)step_set;
+    net->sets[0] = net->arena;
+    for (int k = 0; k < extra; ++k) net->sets[1 + k] = (char*)step_set + (size_t)k * net->step_bytes;
+    net->nsets = 1 + extra;
     return PSW_OK;
 }
 
@@ -1135,17 +1140,18 @@ int issue_pipeline(psw_net* net, int64_t t0, int n_steps, const int32_t* stalene
     const char* what = "";
     for (int i = 0; i < n_steps && e == hipSuccess; ++i) {
         const int64_t t = t0 + i;
-        const int p = (int)(t & 1);
+        const int NS = net->nsets;
+        const int p = (int)(t % NS);
         hipEvent_t wdone = net->wdone_ev[p];
-        char* P = p ? net->step2 : net->arena;
+        char* P = net->sets[p];
         StepIO io{t, std::vector<int64_t>(S_), P, x + (size_t)(i % n_batches) * xs,
                   labels + (size_t)(i % n_batches) * in.n, losses + i, lr + (size_t)i * S_, mom, wd, nesterov,
                   (float*)(P + net->pgrad_off)};
         for (int s = 0; s < S_; ++s) io.rv[s] = fwd_version(t, staleness[(size_t)i * S_ + s]);
         Issue is{net, io};
-        // forward of t: its step set is free once step t-2 is done with it
+        // forward of t: its step set is free once step t-NS is done with it
         // (the weight stream's last update of a step follows the chain's end)
-        if (i >= 2) {
+        if (i >= NS) {
             e = hipStreamWaitEvent(sf, wdone, 0);
             if (e != hipSuccess) {
                 what = "pipeline: step set";
@@ -1200,7 +1206,7 @@ int check_pipeline_args(const psw_net* net, int64_t t0, int n_steps, const int32
                         const float* x, const int32_t* labels, int n_batches, const float* losses, const char* who)
 {
     if (!net) return fail(PSW_ERR_NULL, "%s: net is NULL", who);
-    if (!net->bound || !net->step2) return fail(PSW_ERR_STATE, "%s: bind the net and its pipeline set first", who);
+    if (!net->bound || net->nsets < 2) return fail(PSW_ERR_STATE, "%s: bind the net and its pipeline sets first", who);
     if (!staleness || !lr || !x || !labels || !losses) return fail(PSW_ERR_NULL, "%s: required pointer is NULL", who);
     if (n_steps < 0 || n_batches < 1) return fail(PSW_ERR_SHAPE, "%s: n_steps >= 0 and n_batches >= 1", who);
     for (int i = 0; i < n_steps; ++i) {
@@ -1212,10 +1218,10 @@ int check_pipeline_args(const psw_net* net, int64_t t0, int n_steps, const int32
 
 int64_t gcd64(int64_t a, int64_t b) { return b ? gcd64(b, a % b) : a; }
 
-// period of the per-step buffers: ring slots (t mod D_s) and step sets (t mod 2)
+// period of the per-step buffers: ring slots (t mod D_s) and step sets (t mod nsets)
 int64_t replay_period(const psw_net* net)
 {
-    int64_t p = 2;
+    int64_t p = net->nsets;
     for (int d : net->ring_depth) p = p / gcd64(p, d) * d;
     return p;
 }

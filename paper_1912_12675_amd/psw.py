@@ -379,7 +379,7 @@ class Net:
         if getattr(self, "step2", None) is None:
             nb = ctypes.c_int64()
             _check(lib().psw_net_pipeline_bytes(self.handle, ctypes.byref(nb)))
-            self.step2 = torch.empty(max(nb.value, 256), dtype=torch.uint8, device=self.device)
+            self.step2 = torch.empty(max(2 * nb.value, 256), dtype=torch.uint8, device=self.device)  # two more sets
             _check(lib().psw_net_bind_pipeline(self.handle, _ptr(self.step2), self.step2.numel()))
 
     def capture(self, staleness, lr, xs, labels, losses, mom=0.9, wd=0.0, nesterov=False):

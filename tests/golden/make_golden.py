@@ -58,15 +58,21 @@ def sample_index(n):
 
 
 def tensor_norms(wl, flat, p0):
+    """Per parameter tensor: L2 norm of the final values, of the update, and
+    whether the initial value is non-zero (zero-initialised tensors -- BN
+    beta, biases -- hold only their update, so their norm is compared through
+    the parameter sample instead)."""
     layout, counts = synth.param_layout(wl)
     base = np.concatenate([[0], np.cumsum(counts)])
-    norms, dnorms = [], []
+    norms, dnorms, nz = [], [], []
     for op, name, shape, s, off in layout:
         i0 = int(base[s]) + off
+        seg0 = p0[i0:i0 + int(np.prod(shape))]
         seg = flat[i0:i0 + int(np.prod(shape))]
         norms.append(np.linalg.norm(seg))
-        dnorms.append(np.linalg.norm(seg - p0[i0:i0 + int(np.prod(shape))]))
-    return np.array(norms), np.array(dnorms)
+        dnorms.append(np.linalg.norm(seg - seg0))
+        nz.append(np.linalg.norm(seg0) > 0.0)
+    return np.array(norms), np.array(dnorms), np.array(nz)
 
 
 def ulp_move(x, seed):
@@ -94,8 +100,8 @@ def make_full(name):
     for x in (xs, ulp_move(xs, 1912)):
         out = O.train(wl.ops, wl.in_shape, wl.stage_end, p0, x, ys, st, wl.lr, wl.momentum, wl.weight_decay,
                       wl.nesterov, bf16=wl.bf16)
-        norms, dnorms = tensor_norms(wl, out["params"], p0)
-        res.append(dict(sample=out["params"][idx], norms=norms, dnorms=dnorms, losses=out["losses"],
+        norms, dnorms, nz = tensor_norms(wl, out["params"], p0)
+        res.append(dict(sample=out["params"][idx], norms=norms, dnorms=dnorms, nz=nz, losses=out["losses"],
                         versions=out["versions"]))
         print(f"{name}: run {len(res)} {time.time() - t0:.0f} s, final loss {out['losses'][-1]:.6f}", flush=True)
         del out
@@ -105,9 +111,9 @@ def make_full(name):
         sample=np.linalg.norm(a["sample"] - b["sample"]) / np.linalg.norm(a["sample"]),
         update=np.linalg.norm(a["sample"] - b["sample"]) / max(np.linalg.norm(a["sample"] - s0), 1e-30),
         loss=np.abs(a["losses"] - b["losses"]).max() / np.abs(a["losses"]).max(),
-        norm=np.max(np.abs(a["norms"] - b["norms"]) / np.maximum(a["norms"], 1e-30)))
+        norm=np.max((np.abs(a["norms"] - b["norms"]) / np.maximum(a["norms"], 1e-30))[a["nz"]]))
     path = os.path.join(HERE, f"{name}_full_{T}steps.npz")
-    np.savez_compressed(path, index=idx, sample=a["sample"], norms=a["norms"], dnorms=a["dnorms"],
+    np.savez_compressed(path, index=idx, sample=a["sample"], norms=a["norms"], dnorms=a["dnorms"], nonzero_init=a["nz"],
                         losses=a["losses"], versions=a["versions"], steps=T,
                         **{"spread_" + k: v for k, v in spread.items()})
     print(f"{name}: spread {spread} -> {path}", flush=True)
