@@ -816,6 +816,7 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
     void* ws = is.wsf();
     const size_t wsb = net->ws_bytes;
     hipError_t e = hipSuccess;
+    bool head = false;
     for (int i = 0; i < L; ++i) {
         if (i == 0 || net->stage_of[i] != net->stage_of[i - 1]) PSW_TRY(before_stage(net->stage_of[i]), "stage wait");
         const psw_layer& o = net->ops[i];
@@ -881,6 +882,15 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
         case PSW_OP_FC: {
             const float* b = (o.flags & PSW_F_BIAS) ? W + (int64_t)o.cout * o.cin : nullptr;
             kind = PSW_PROF_FC;
+            if (i == L - 1 && !(o.flags & PSW_F_RELU)) {  // the classifier: with the loss in one launch if small
+                e = psw::fc_softmax_xent(a.n, o.cin, o.cout, is.act(o.in0), W, b, is.act(i + 1), bf16,
+                                         is.io.labels, is.io.loss_out, is.grd(L), sf);
+                if (e == hipSuccess) {
+                    head = true;
+                    break;
+                }
+                if (e != hipErrorNotSupported) PSW_TRY(e, "fc_softmax_xent");
+            }
             PSW_TRY(psw::fc_fwd(a.n, o.cin, o.cout, is.act(o.in0), W, b, (o.flags & PSW_F_RELU) != 0, is.act(i + 1),
                                 bf16, sf),
                     "fc_fwd");
@@ -888,6 +898,7 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
         }
         }
     }
+    if (head) return hipSuccess;  // the loss came with the classifier
     const Tensor lg = net->t[L];
     kind = PSW_PROF_LOSS;
     PSW_TRY(psw::softmax_xent(lg.n, lg.c, is.act(L), is.io.labels, is.io.loss_out, is.grd(L), sf), "softmax_xent");

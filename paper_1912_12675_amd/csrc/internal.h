@@ -189,6 +189,11 @@ hipError_t gavgpool_bwd(int n, int c, int h, int w, const float* dy, float* dx, 
                         hipStream_t st);
 
 // ---- fully connected (GEMM on MFMA) ----
+// Small FC as the last layer: logits, mean softmax cross-entropy and its
+// gradient in one launch; hipErrorNotSupported (nothing launched) when the
+// layer is not small.
+hipError_t fc_softmax_xent(int n, int in, int out, const float* x, const float* w, const float* b, float* logits,
+                           int bf16, const int32_t* labels, float* loss, float* dlogits, hipStream_t st);
 hipError_t fc_fwd(int n, int in, int out, const float* x, const float* w, const float* b, int relu, float* y,
                   int bf16, hipStream_t st);
 size_t fc_bwd_ws_bytes(int n, int in, int out);

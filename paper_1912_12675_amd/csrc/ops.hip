@@ -519,6 +519,141 @@ hipError_t gemm(GemmArgs a, int bf16, void* ws, size_t ws_bytes, hipStream_t st)
 
 inline unsigned blocks_for(int64_t n, int b = kBlock) { return (unsigned)((n + b - 1) / b); }
 
+// ------------------------------------------ small fully-connected layers --
+// The classifier of the CIFAR nets (e.g. 128 x 64 -> 10) is far too small for
+// the tiled GEMM: one launch per direction does it on the vector units, every
+// sum in a fixed order (k, o or i ascending).  bf16 mode rounds both operands
+// of every product, as the GEMM does.
+constexpr int kHeadBlock = 1024;
+constexpr int kSmallFcLogits = 4096;  // n*out (logits held in LDS)
+constexpr int kFcMaxN = 256, kFcMaxOut = 64, kFcKC = 32, kFcKW = 16;
+
+bool small_fc(int n, int in, int out)
+{
+    return n <= kFcMaxN && out <= kFcMaxOut && (int64_t)n * out <= kSmallFcLogits && in <= 4096;
+}
+
+// y[i][o] = sum_k x[i][k] w[o][k] (+ b[o]) (relu), k ascending, from LDS
+// chunks of kFcKC columns; with labels: also the mean softmax cross-entropy
+// and its gradient (as softmax_xent_k).  One workgroup.
+__global__ __launch_bounds__(kHeadBlock) void fc_small_fwd_k(int n, int in, int out, const float* x, const float* w,
+                                                             const float* b, int relu, int bf16, float* y,
+                                                             const int32_t* labels, float* loss, float* dlogits)
+{
+    constexpr int KP = kFcKC + 1;
+    __shared__ float xs[kFcMaxN * KP];
+    __shared__ float ws[kFcMaxOut * KP];
+    __shared__ float z[kSmallFcLogits];
+    __shared__ double sh[kHeadBlock / 64];
+    constexpr int Q = kSmallFcLogits / kHeadBlock;
+    float acc[Q];
+#pragma unroll
+    for (int q = 0; q < Q; ++q) acc[q] = 0.f;
+    for (int k0 = 0; k0 < in; k0 += kFcKC) {
+        __syncthreads();
+        for (int idx = threadIdx.x; idx < n * kFcKC; idx += kHeadBlock) {
+            const int i = idx / kFcKC, kk = idx - (idx / kFcKC) * kFcKC, k = k0 + kk;
+            const float v = k < in ? x[(size_t)i * in + k] : 0.f;
+            xs[i * KP + kk] = bf16 ? round_bf16(v) : v;
+        }
+        for (int idx = threadIdx.x; idx < out * kFcKC; idx += kHeadBlock) {
+            const int o = idx / kFcKC, kk = idx - (idx / kFcKC) * kFcKC, k = k0 + kk;
+            const float v = k < in ? w[(size_t)o * in + k] : 0.f;
+            ws[o * KP + kk] = bf16 ? round_bf16(v) : v;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int q = 0; q < Q; ++q) {
+            const int e = threadIdx.x + q * kHeadBlock;
+            if (e < n * out) {
+                const int i = e / out, o = e - (e / out) * out;
+                const float* xr = xs + i * KP;
+                const float* wr = ws + o * KP;
+#pragma unroll 8
+                for (int kk = 0; kk < kFcKC; ++kk) acc[q] = fmaf(xr[kk], wr[kk], acc[q]);
+            }
+        }
+    }
+#pragma unroll
+    for (int q = 0; q < Q; ++q) {
+        const int e = threadIdx.x + q * kHeadBlock;
+        if (e < n * out) {
+            float v = acc[q];
+            if (b) v += b[e - (e / out) * out];
+            if (relu) v = fmaxf(v, 0.f);
+            y[e] = v;
+            z[e] = v;
+        }
+    }
+    if (!labels) return;
+    __syncthreads();
+    double part = 0.0;
+    for (int row = threadIdx.x; row < n; row += kHeadBlock) {
+        const float* zr = z + row * out;
+        float mx = zr[0];
+        for (int j = 1; j < out; ++j) mx = fmaxf(mx, zr[j]);
+        float se = 0.f;
+        for (int j = 0; j < out; ++j) se += expf(zr[j] - mx);
+        const float lse = mx + logf(se);
+        const int lab = labels[row];
+        part += (double)(lse - zr[lab]);
+        for (int j = 0; j < out; ++j)
+            dlogits[(size_t)row * out + j] = (expf(zr[j] - lse) - (j == lab ? 1.f : 0.f)) / (float)n;
+    }
+    const double t = block_sum(part, sh);
+    if (threadIdx.x == 0) loss[0] = (float)(t / n);
+}
+
+// Blocks [0, nbx): dx[i][k] (+)= sum_o dy[i][o] w[o][k], o ascending, one
+// output per thread.  Blocks [nbx, nbx + nbw): dw[o][k] = sum_i dy[i][o]
+// x[i][k], i ascending, for kFcKW columns k from LDS copies of dy and of those
+// columns of x.  Last block: db[o] = sum_i dy[i][o].
+__global__ __launch_bounds__(kBlock) void fc_small_bwd_k(int n, int in, int out, const float* x, const float* w,
+                                                         const float* dy, float* dx, int dx_accumulate, float* dw,
+                                                         float* db, int bf16, int nbx, int nbw)
+{
+    __shared__ float dys[kSmallFcLogits];
+    __shared__ float xs[kFcMaxN * (kFcKW + 1)];
+    const int bid = blockIdx.x, tid = threadIdx.x;
+    if (bid < nbx) {
+        const int64_t e = (int64_t)bid * kBlock + tid;
+        if (e >= (int64_t)n * in) return;
+        const int i = (int)(e / in), k = (int)(e - (e / in) * in);
+        float acc = 0.f;
+        for (int o = 0; o < out; ++o) {
+            const float g = dy[(size_t)i * out + o], wv = w[(size_t)o * in + k];
+            acc = fmaf(bf16 ? round_bf16(g) : g, bf16 ? round_bf16(wv) : wv, acc);
+        }
+        dx[e] = dx_accumulate ? dx[e] + acc : acc;
+        return;
+    }
+    if (bid < nbx + nbw) {
+        const int k0 = (bid - nbx) * kFcKW;
+        for (int idx = tid; idx < n * out; idx += kBlock) dys[idx] = bf16 ? round_bf16(dy[idx]) : dy[idx];
+        for (int idx = tid; idx < n * kFcKW; idx += kBlock) {
+            const int i = idx / kFcKW, kk = idx - (idx / kFcKW) * kFcKW, k = k0 + kk;
+            const float v = k < in ? x[(size_t)i * in + k] : 0.f;
+            xs[i * (kFcKW + 1) + kk] = bf16 ? round_bf16(v) : v;
+        }
+        __syncthreads();
+        for (int t = tid; t < out * kFcKW; t += kBlock) {
+            const int o = t / kFcKW, kk = t - (t / kFcKW) * kFcKW, k = k0 + kk;
+            if (k >= in) continue;
+            float acc = 0.f;
+            for (int i = 0; i < n; ++i) acc = fmaf(dys[i * out + o], xs[i * (kFcKW + 1) + kk], acc);
+            dw[(size_t)o * in + k] = acc;
+        }
+        return;
+    }
+    if (db && tid < out) {
+        float acc = 0.f;
+        for (int i = 0; i < n; ++i) acc += dy[(size_t)i * out + tid];
+        db[tid] = acc;
+    }
+}
+
+
+
 }  // namespace
 
 // ------------------------------------------------------------ launchers -----
@@ -951,12 +1086,30 @@ hipError_t sgd_momentum(int64_t count, const float* w_in, float* w_out, float* v
 hipError_t fc_fwd(int n, int in, int out, const float* x, const float* w, const float* b, int relu, float* y, int bf16,
                   hipStream_t st)
 {
+    if (small_fc(n, in, out)) {
+        const double fl = 2.0 * n * out * (double)in;
+        PSW_LAUNCH(kname("fc_small_fwd_k"), (Work{fl, kF * ((double)n * in + (double)out * in + (double)n * out)}),
+                   fc_small_fwd_k, dim3(1), dim3(kHeadBlock), 0, st, n, in, out, x, w, b, relu, bf16, y,
+                   (const int32_t*)nullptr, (float*)nullptr, (float*)nullptr);
+        return hipGetLastError();
+    }
     GemmArgs a{};
     a.A = x; a.B = w; a.C = y; a.bias = b; a.relu = relu;
     a.M = n; a.N = out; a.K = in;
     a.sam = in; a.sak = 1;    // x[n][i]
     a.sbk = 1; a.sbn = in;    // w[o][i]
     return gemm<true, true>(a, bf16, nullptr, 0, st);
+}
+
+hipError_t fc_softmax_xent(int n, int in, int out, const float* x, const float* w, const float* b, float* logits,
+                           int bf16, const int32_t* labels, float* loss, float* dlogits, hipStream_t st)
+{
+    if (!small_fc(n, in, out)) return hipErrorNotSupported;
+    const double fl = 2.0 * n * out * (double)in + 5.0 * n * out;
+    PSW_LAUNCH(kname("fc_small_fwd_k"),
+               (Work{fl, kF * ((double)n * in + (double)out * in + 3.0 * n * out + n + 1.0)}), fc_small_fwd_k, dim3(1),
+               dim3(kHeadBlock), 0, st, n, in, out, x, w, b, 0, bf16, logits, labels, loss, dlogits);
+    return hipGetLastError();
 }
 
 size_t fc_bwd_ws_bytes(int n, int in, int out)
@@ -975,6 +1128,15 @@ hipError_t fc_bwd(int n, int in, int out, const float* x, const float* w, const 
                   float* dw, float* db, int bf16, void* ws, size_t ws_bytes, hipStream_t st)
 {
     if (ws_bytes < fc_bwd_ws_bytes(n, in, out)) return hipErrorInvalidValue;
+    if (small_fc(n, in, out)) {
+        const int nbx = dx ? (int)blocks_for((int64_t)n * in) : 0, nbw = (in + kFcKW - 1) / kFcKW;
+        const double fl = 2.0 * (dx ? 2.0 : 1.0) * n * out * (double)in + (double)n * out;
+        const double bytes = kF * ((double)n * out + (double)out * in + (double)n * in * (dx ? 2.0 + dx_accumulate : 1.0) +
+                                   (double)out * in + out);
+        PSW_LAUNCH(kname("fc_small_bwd_k"), (Work{fl, bytes}), fc_small_bwd_k, dim3(nbx + nbw + 1), dim3(kBlock), 0,
+                   st, n, in, out, x, w, dy, dx, dx_accumulate, dw, db, bf16, nbx, nbw);
+        return hipGetLastError();
+    }
     const size_t head = (((size_t)out * 2 * sizeof(double)) + 255) / 256 * 256;
     hipError_t e = hipSuccess;
     if (dx) {

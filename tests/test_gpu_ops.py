@@ -198,7 +198,8 @@ def test_gavgpool_parity(P, oracle, shape):
 
 
 @pytest.mark.parametrize("n,fin,fout,relu", [(5, 37, 13, False), (128, 64, 10, False), (3, 400, 120, True),
-                                             (70, 300, 130, True), (4, 2048, 96, False)])
+                                             (70, 300, 130, True), (4, 2048, 96, False),
+                                             (256, 100, 16, True), (64, 4096, 64, False)])
 @pytest.mark.parametrize("bf16", [False, True], ids=["fp32", "bf16"])
 def test_fc_parity(P, oracle, n, fin, fout, relu, bf16):
     rng = np.random.default_rng(n * 1000 + fin + fout)
