@@ -60,8 +60,9 @@ COPY_BYTES = 256 << 20
 
 def measured_traffic(kernel):
     """HBM bytes per launch of `kernel` from profiles/traffic.json, or None
-    when absent, taken for another kernel, or taken on other sources of that
-    kernel (the file records which source files define it and their hash)."""
+    when the file has no entry for it or the entry was taken on other sources
+    of that kernel (each entry records which source files define the kernel
+    and their hash)."""
     import hashlib
 
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -70,7 +71,8 @@ def measured_traffic(kernel):
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    if t.get("kernel") != kernel or not t.get("sources"):
+    t = t.get("kernels", {}).get(kernel)
+    if not t or not t.get("sources"):
         return None
     h = hashlib.sha256()
     for rel in t["sources"]:
@@ -276,7 +278,8 @@ def main():
         r = roofline_of(k, peak)
         top.append({"kernel": k["name"], "kind": k["kind"], "launches_per_step": k["launches"] / KP,
                     "us_per_step": round(1e3 * k["ms"] / KP, 2), "avg_launch_us": round(1e3 * k["ms"] / k["launches"], 3),
-                    "bound": r["bound"], "achieved": r["achieved"], "unit": r["unit"], "frac": r["frac"]})
+                    "bound": r["bound"], "achieved": r["achieved"], "unit": r["unit"], "frac": r["frac"],
+                    "bytes_per_launch": k["bytes"] / k["launches"], "traffic": measured_traffic(k["name"])})
 
     out = {
         "metric": METRIC,

@@ -549,19 +549,36 @@ __global__ __launch_bounds__(kHeadBlock) void fc_small_fwd_k(int n, int in, int 
     float acc[Q];
 #pragma unroll
     for (int q = 0; q < Q; ++q) acc[q] = 0.f;
+    // The next chunk's loads are issued before the current chunk's products.
+    constexpr int RX = kFcMaxN * kFcKC / kHeadBlock, RW = kFcMaxOut * kFcKC / kHeadBlock;
+    float vx[RX], vw[RW];
+    auto load_chunk = [&](int k0) {
+#pragma unroll
+        for (int r = 0; r < RX; ++r) {
+            const int idx = threadIdx.x + r * kHeadBlock, i = idx / kFcKC, k = k0 + idx % kFcKC;
+            vx[r] = (i < n && k < in) ? x[(size_t)i * in + k] : 0.f;
+        }
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+            const int idx = threadIdx.x + r * kHeadBlock, o = idx / kFcKC, k = k0 + idx % kFcKC;
+            vw[r] = (o < out && k < in) ? w[(size_t)o * in + k] : 0.f;
+        }
+    };
+    load_chunk(0);
     for (int k0 = 0; k0 < in; k0 += kFcKC) {
         __syncthreads();
-        for (int idx = threadIdx.x; idx < n * kFcKC; idx += kHeadBlock) {
-            const int i = idx / kFcKC, kk = idx - (idx / kFcKC) * kFcKC, k = k0 + kk;
-            const float v = k < in ? x[(size_t)i * in + k] : 0.f;
-            xs[i * KP + kk] = bf16 ? round_bf16(v) : v;
+#pragma unroll
+        for (int r = 0; r < RX; ++r) {
+            const int idx = threadIdx.x + r * kHeadBlock;
+            xs[(idx / kFcKC) * KP + idx % kFcKC] = bf16 ? round_bf16(vx[r]) : vx[r];
         }
-        for (int idx = threadIdx.x; idx < out * kFcKC; idx += kHeadBlock) {
-            const int o = idx / kFcKC, kk = idx - (idx / kFcKC) * kFcKC, k = k0 + kk;
-            const float v = k < in ? w[(size_t)o * in + k] : 0.f;
-            ws[o * KP + kk] = bf16 ? round_bf16(v) : v;
+#pragma unroll
+        for (int r = 0; r < RW; ++r) {
+            const int idx = threadIdx.x + r * kHeadBlock;
+            ws[(idx / kFcKC) * KP + idx % kFcKC] = bf16 ? round_bf16(vw[r]) : vw[r];
         }
         __syncthreads();
+        if (k0 + kFcKC < in) load_chunk(k0 + kFcKC);
 #pragma unroll
         for (int q = 0; q < Q; ++q) {
             const int e = threadIdx.x + q * kHeadBlock;
@@ -607,10 +624,11 @@ __global__ __launch_bounds__(kHeadBlock) void fc_small_fwd_k(int n, int in, int 
 // Blocks [0, nbx): dx[i][k] (+)= sum_o dy[i][o] w[o][k], o ascending, one
 // output per thread.  Blocks [nbx, nbx + nbw): dw[o][k] = sum_i dy[i][o]
 // x[i][k], i ascending, for kFcKW columns k from LDS copies of dy and of those
-// columns of x.  Last block: db[o] = sum_i dy[i][o].
+// columns of x; the first of them also db[o] = sum_i dy[i][o].  Global loads
+// are issued in batches before their values are used.
 __global__ __launch_bounds__(kBlock) void fc_small_bwd_k(int n, int in, int out, const float* x, const float* w,
                                                          const float* dy, float* dx, int dx_accumulate, float* dw,
-                                                         float* db, int bf16, int nbx, int nbw)
+                                                         float* db, int bf16, int nbx)
 {
     __shared__ float dys[kSmallFcLogits];
     __shared__ float xs[kFcMaxN * (kFcKW + 1)];
@@ -619,36 +637,59 @@ __global__ __launch_bounds__(kBlock) void fc_small_bwd_k(int n, int in, int out,
         const int64_t e = (int64_t)bid * kBlock + tid;
         if (e >= (int64_t)n * in) return;
         const int i = (int)(e / in), k = (int)(e - (e / in) * in);
+        const float old = dx_accumulate ? dx[e] : 0.f;
         float acc = 0.f;
-        for (int o = 0; o < out; ++o) {
-            const float g = dy[(size_t)i * out + o], wv = w[(size_t)o * in + k];
-            acc = fmaf(bf16 ? round_bf16(g) : g, bf16 ? round_bf16(wv) : wv, acc);
+        constexpr int U = 8;
+        for (int o0 = 0; o0 < out; o0 += U) {
+            float g[U], wv[U];
+#pragma unroll
+            for (int j = 0; j < U; ++j) {
+                const int o = o0 + j;
+                g[j] = o < out ? dy[(size_t)i * out + o] : 0.f;
+                wv[j] = o < out ? w[(size_t)o * in + k] : 0.f;
+            }
+#pragma unroll
+            for (int j = 0; j < U; ++j)
+                if (o0 + j < out) acc = fmaf(bf16 ? round_bf16(g[j]) : g[j], bf16 ? round_bf16(wv[j]) : wv[j], acc);
         }
-        dx[e] = dx_accumulate ? dx[e] + acc : acc;
+        dx[e] = dx_accumulate ? old + acc : acc;
         return;
     }
-    if (bid < nbx + nbw) {
-        const int k0 = (bid - nbx) * kFcKW;
-        for (int idx = tid; idx < n * out; idx += kBlock) dys[idx] = bf16 ? round_bf16(dy[idx]) : dy[idx];
-        for (int idx = tid; idx < n * kFcKW; idx += kBlock) {
-            const int i = idx / kFcKW, kk = idx - (idx / kFcKW) * kFcKW, k = k0 + kk;
-            const float v = k < in ? x[(size_t)i * in + k] : 0.f;
-            xs[i * (kFcKW + 1) + kk] = bf16 ? round_bf16(v) : v;
-        }
-        __syncthreads();
-        for (int t = tid; t < out * kFcKW; t += kBlock) {
-            const int o = t / kFcKW, kk = t - (t / kFcKW) * kFcKW, k = k0 + kk;
-            if (k >= in) continue;
-            float acc = 0.f;
-            for (int i = 0; i < n; ++i) acc = fmaf(dys[i * out + o], xs[i * (kFcKW + 1) + kk], acc);
-            dw[(size_t)o * in + k] = acc;
-        }
-        return;
+    const int k0 = (bid - nbx) * kFcKW;
+    constexpr int RD = kSmallFcLogits / kBlock, RX = kFcMaxN * kFcKW / kBlock;
+    float vd[RD], vx[RX];
+#pragma unroll
+    for (int r = 0; r < RD; ++r) {
+        const int idx = tid + r * kBlock;
+        vd[r] = idx < n * out ? dy[idx] : 0.f;
     }
-    if (db && tid < out) {
+#pragma unroll
+    for (int r = 0; r < RX; ++r) {
+        const int idx = tid + r * kBlock, i = idx / kFcKW, k = k0 + idx % kFcKW;
+        vx[r] = (i < n && k < in) ? x[(size_t)i * in + k] : 0.f;
+    }
+#pragma unroll
+    for (int r = 0; r < RD; ++r) dys[tid + r * kBlock] = vd[r];
+#pragma unroll
+    for (int r = 0; r < RX; ++r) {
+        const int idx = tid + r * kBlock;
+        xs[(idx / kFcKW) * (kFcKW + 1) + idx % kFcKW] = bf16 ? round_bf16(vx[r]) : vx[r];
+    }
+    __syncthreads();
+    if (db && bid == nbx && tid < out) {
         float acc = 0.f;
-        for (int i = 0; i < n; ++i) acc += dy[(size_t)i * out + tid];
+        for (int i = 0; i < n; ++i) acc += dys[i * out + tid];
         db[tid] = acc;
+    }
+    for (int t = tid; t < out * kFcKW; t += kBlock) {
+        const int o = t / kFcKW, kk = t % kFcKW, k = k0 + kk;
+        if (k >= in) continue;
+        float acc = 0.f;
+        for (int i = 0; i < n; ++i) {
+            const float g = dys[i * out + o];
+            acc = fmaf(bf16 ? round_bf16(g) : g, xs[i * (kFcKW + 1) + kk], acc);
+        }
+        dw[(size_t)o * in + k] = acc;
     }
 }
 
@@ -1133,8 +1174,8 @@ hipError_t fc_bwd(int n, int in, int out, const float* x, const float* w, const 
         const double fl = 2.0 * (dx ? 2.0 : 1.0) * n * out * (double)in + (double)n * out;
         const double bytes = kF * ((double)n * out + (double)out * in + (double)n * in * (dx ? 2.0 + dx_accumulate : 1.0) +
                                    (double)out * in + out);
-        PSW_LAUNCH(kname("fc_small_bwd_k"), (Work{fl, bytes}), fc_small_bwd_k, dim3(nbx + nbw + 1), dim3(kBlock), 0,
-                   st, n, in, out, x, w, dy, dx, dx_accumulate, dw, db, bf16, nbx, nbw);
+        PSW_LAUNCH(kname("fc_small_bwd_k"), (Work{fl, bytes}), fc_small_bwd_k, dim3(nbx + nbw), dim3(kBlock), 0,
+                   st, n, in, out, x, w, dy, dx, dx_accumulate, dw, db, bf16, nbx);
         return hipGetLastError();
     }
     const size_t head = (((size_t)out * 2 * sizeof(double)) + 255) / 256 * 256;

@@ -4,12 +4,12 @@
         per-kernel table (calls per step, mean / total time) of a
         `rocprofv3 --kernel-trace --stats --output-format csv` run
 
-    python -m paper_1912_12675_amd.rocprof_summary traffic --kernel NAME \
+    python -m paper_1912_12675_amd.rocprof_summary traffic --kernel NAME [--kernel NAME ...] \
             --fetch PMC_CSV --write PMC_CSV --copy-fetch PMC_CSV --copy-write PMC_CSV \
             --copy-kernel SUBSTRING --copy-bytes B [--out profiles/traffic.json]
-        HBM bytes per launch of kernel NAME from two `--pmc FETCH_SIZE` and
-        `--pmc WRITE_SIZE` runs, each counter scaled by what it reads for a
-        plain streaming kernel that reads and writes B bytes
+        HBM bytes per launch of each kernel NAME from two `--pmc FETCH_SIZE`
+        and `--pmc WRITE_SIZE` runs, each counter scaled by what it reads for
+        a plain streaming kernel that reads and writes B bytes
 
 Kernel names are compared in the short form the library's profiler reports
 (`conv3x3_direct<32, 1, 8, 16, 1, 4, 4, true>`): namespaces, a leading
@@ -93,7 +93,7 @@ def _mean(v):
     return sum(v) / len(v)
 
 
-def traffic(kernel, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_kernel, copy_bytes):
+def traffic(kernels, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_kernel, copy_bytes):
     def pick(vals, sub):
         keys = [k for k in vals if sub in k]
         if len(keys) != 1:
@@ -102,21 +102,24 @@ def traffic(kernel, fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_k
 
     fk = pmc_values(fetch_csv, "FETCH_SIZE")
     wk = pmc_values(write_csv, "WRITE_SIZE")
-    if kernel not in fk or kernel not in wk:
-        raise SystemExit(f"{kernel!r} not in the counter runs")
     cname, cf = pick(pmc_values(copy_fetch_csv, "FETCH_SIZE"), copy_kernel)
     _, cw = pick(pmc_values(copy_write_csv, "WRITE_SIZE"), copy_kernel)
     # counters are in KiB per dispatch; scale each so the copy reads/writes copy_bytes
     f_scale = copy_bytes / (1024.0 * _mean(cf))
     w_scale = copy_bytes / (1024.0 * _mean(cw))
-    fetch = 1024.0 * _mean(fk[kernel]) * f_scale
-    write = 1024.0 * _mean(wk[kernel]) * w_scale
-    return {"kernel": kernel, "bytes_per_launch": fetch + write, "fetch_bytes_per_launch": fetch,
-            "write_bytes_per_launch": write, "fetch_kib_per_dispatch": _mean(fk[kernel]),
-            "write_kib_per_dispatch": _mean(wk[kernel]), "dispatches": [len(fk[kernel]), len(wk[kernel])],
-            "copy_kernel": cname, "copy_bytes": copy_bytes, "copy_fetch_kib": _mean(cf), "copy_write_kib": _mean(cw),
-            "fetch_scale": f_scale, "write_scale": w_scale, "sources": kernel_sources(kernel),
+    out = {"copy_kernel": cname, "copy_bytes": copy_bytes, "copy_fetch_kib": _mean(cf), "copy_write_kib": _mean(cw),
+           "fetch_scale": f_scale, "write_scale": w_scale, "kernels": {}}
+    for kernel in kernels:
+        if kernel not in fk or kernel not in wk:
+            raise SystemExit(f"{kernel!r} not in the counter runs")
+        fetch = 1024.0 * _mean(fk[kernel]) * f_scale
+        write = 1024.0 * _mean(wk[kernel]) * w_scale
+        out["kernels"][kernel] = {
+            "bytes_per_launch": fetch + write, "fetch_bytes_per_launch": fetch, "write_bytes_per_launch": write,
+            "fetch_kib_per_dispatch": _mean(fk[kernel]), "write_kib_per_dispatch": _mean(wk[kernel]),
+            "dispatches": [len(fk[kernel]), len(wk[kernel])], "sources": kernel_sources(kernel),
             "source_sha256": source_hash(kernel_sources(kernel))}
+    return out
 
 
 def main(argv=None):
@@ -127,7 +130,8 @@ def main(argv=None):
     a.add_argument("--steps", type=int, required=True)
     a.add_argument("--top", type=int, default=25)
     b = sub.add_parser("traffic")
-    for k in ("kernel", "fetch", "write", "copy_fetch", "copy_write", "copy_kernel"):
+    b.add_argument("--kernel", action="append", required=True)
+    for k in ("fetch", "write", "copy_fetch", "copy_write", "copy_kernel"):
         b.add_argument("--" + k.replace("_", "-"), required=True)
     b.add_argument("--copy-bytes", type=int, required=True)
     b.add_argument("--out")
