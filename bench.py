@@ -264,8 +264,14 @@ def main():
         conv = {"achieved": round(ach, 3), "peak": peak, "unit": "TFLOP/s", "frac": round(ach / peak, 4),
                 "flop_per_step": conv_flop, "conv_kernel_ms_per_step": round(conv_ms, 4),
                 "conv_kernel_launches_per_step": sum(k["launches"] for k in ck) / KP,
-                "what": "all convolution kernels (forward, backward-data with fused BN sums, backward-weight and "
-                        "its split reduction): algorithmic conv FLOPs / summed kernel time"}
+                "what": "all convolution kernels (forward, backward-data with fused BN sums, backward-weight): "
+                        "algorithmic conv FLOPs / summed kernel time; the backward-weight split partial sums are "
+                        "reduced inside the stage update kernel (sgd_stage_k), whose time is in kernel_ms_per_step.sgd "
+                        "and in frac_with_update"}
+        uk = [k for k in kernels if k["name"] == "sgd_stage_k"]
+        if uk:
+            ums = conv_ms + sum(k["ms"] for k in uk) / KP
+            conv["frac_with_update"] = round(conv_flop / (ums * 1e-3) / 1e12 / peak, 4)
         d = kernels[0]  # the dominant kernel: largest summed time
         roof = roofline_of(d, peak)
         roof["traffic"] = measured_traffic(d["name"])

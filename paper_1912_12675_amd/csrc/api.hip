@@ -289,6 +289,18 @@ struct psw_net {
     size_t wsf_off = 0;                     // forward workspace, in the step set
     size_t ws_off = 0, ws_bytes = 0, arena_bytes = 0;  // backward workspace, in the shared set
     size_t wsw_off = 0, wsw_bytes = 0;      // workspace of the backward-weight kernels (shared set)
+    // conv weight gradients left as split partial sums for the stage update
+    // (psw::sgd_stage), one region per conv in the shared set; the regions of
+    // one stage are disjoint, stages reuse them (the weight stream runs the
+    // stages one after another)
+    std::vector<int32_t> wpart_splits;      // per op: splits, 0 = gradient reduced by conv_bwd_weight
+    std::vector<size_t> wpart_off;          // per op: offset of its region from wpart_base
+    size_t wpart_base = 0;
+    struct SegProto {
+        int64_t off, count;
+        int op;  // conv op whose partial sums give the gradient, -1: read the gradient array
+    };
+    std::vector<std::vector<SegProto>> sgd_segs;  // per stage
     // backward-weight kernels run on a second stream of the library, forked
     // from the caller's stream when a conv's output gradient is final and
     // joined before the update (created at bind, default priority)
@@ -557,6 +569,37 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
             ws = std::max(ws, psw::fc_bwd_ws_bytes(a.n, o.cin, o.cout));
         }
     }
+    // split partial sums of the conv weight gradients, reduced by the stage update
+    net->wpart_splits.assign(n_layers, 0);
+    net->wpart_off.assign(n_layers, 0);
+    net->sgd_segs.assign(n_stages, {});
+    size_t wpart = 0;
+    for (int s = 0; s < n_stages; ++s) {
+        size_t cur = 0;
+        auto& segs = net->sgd_segs[s];
+        for (int i = net->stage_begin[s]; i < net->stage_end[s]; ++i) {
+            const psw_layer& o = net->ops[i];
+            if (net->pcount[i] <= 0) continue;
+            int splits = 0;
+            if (o.kind == PSW_OP_CONV && !(o.flags & PSW_F_BIAS)) {
+                const Tensor a = net->t[o.in0];
+                psw::ConvShape cs;
+                check_conv(a.n, a.c, a.h, a.w, o.cout, o.k, o.k, o.stride, o.pad, prec, &cs);
+                splits = psw::conv_bwd_weight_part_splits(cs, prec == PSW_BF16);
+            }
+            if (splits > 0) {
+                net->wpart_splits[i] = splits;
+                net->wpart_off[i] = cur;
+                cur = align256(cur + (size_t)splits * net->pcount[i] * sizeof(float));
+                segs.push_back({net->poff[i], net->pcount[i], i});
+            } else if (!segs.empty() && segs.back().op < 0 && segs.back().off + segs.back().count == net->poff[i]) {
+                segs.back().count += net->pcount[i];
+            } else {
+                segs.push_back({net->poff[i], net->pcount[i], -1});
+            }
+        }
+        wpart = std::max(wpart, cur);
+    }
     for (int i = 1; i <= n_layers; ++i) {  // gradients of every tensor
         net->grad_off[i] = off;
         off = align256(off + (size_t)net->t[i].numel() * sizeof(float));
@@ -575,6 +618,8 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
     net->wsw_off = off;
     net->wsw_bytes = align256(wsw);
     off += net->wsw_bytes;
+    net->wpart_base = off;
+    off += wpart;
     net->arena_bytes = net->step_bytes + off;
     g_err.clear();
     return PSW_OK;
@@ -785,6 +830,7 @@ struct Issue {
     void* wsf() const { return io.P + net->wsf_off; }
     void* wsb() const { return net->arena + net->step_bytes + net->ws_off; }
     void* wsw() const { return net->arena + net->step_bytes + net->wsw_off; }
+    float* wpart(int i) const { return (float*)(net->arena + net->step_bytes + net->wpart_base + net->wpart_off[i]); }
     const float* wfwd(int i) const
     {
         const int s = net->stage_of[i];
@@ -1030,14 +1076,28 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, AfterUpdate
                 float* dw = is.gptr(j);
                 float* db = (c.flags & PSW_F_BIAS) ? dw + (int64_t)c.cout * c.cin * c.k * c.k : nullptr;
                 kind = PSW_PROF_CONV_BWD_WEIGHT;
-                PSW_TRY(psw::conv_bwd_weight(ccs, is.act(c.in0), is.grd(j + 1), dw, db, bf16, wsw, wswb, sw),
-                        "conv_bwd_weight");
+                if (net->wpart_splits[j] > 0)  // reduced by the stage update below
+                    PSW_TRY(psw::conv_bwd_weight_partials(ccs, is.act(c.in0), is.grd(j + 1), is.wpart(j), bf16, sw),
+                            "conv_bwd_weight");
+                else
+                    PSW_TRY(psw::conv_bwd_weight(ccs, is.act(c.in0), is.grd(j + 1), dw, db, bf16, wsw, wswb, sw),
+                            "conv_bwd_weight");
             }
             kind = PSW_PROF_SGD;
-            PSW_TRY(psw::sgd_momentum(net->stage_np[s], slot_ptr(net, s, io.t), slot_ptr(net, s, io.t + 1),
-                                      net->momentum + net->flat_off[s], io.gbase + net->flat_off[s], io.lr[s], io.mom,
-                                      io.wd, io.nesterov, sw),
-                    "sgd");
+            psw::SgdSeg segs[64];
+            const auto& proto = net->sgd_segs[s];
+            for (size_t q0 = 0; q0 < proto.size(); q0 += 64) {
+                const int m = (int)std::min<size_t>(64, proto.size() - q0);
+                for (int q = 0; q < m; ++q) {
+                    const auto& pr = proto[q0 + q];
+                    segs[q] = {pr.off, pr.count, pr.op >= 0 ? is.wpart(pr.op) : nullptr,
+                               pr.op >= 0 ? net->wpart_splits[pr.op] : 0};
+                }
+                PSW_TRY(psw::sgd_stage(segs, m, slot_ptr(net, s, io.t), slot_ptr(net, s, io.t + 1),
+                                       net->momentum + net->flat_off[s], io.gbase + net->flat_off[s], io.lr[s], io.mom,
+                                       io.wd, io.nesterov, sw),
+                        "sgd");
+            }
             PSW_TRY(after_update(s), "update event");
         }
     }

@@ -382,6 +382,18 @@ size_t conv_bwd_weight_ws_bytes(const ConvShape& cs, int bf16)
     return bytes;
 }
 
+int conv_bwd_weight_part_splits(const ConvShape& cs, int bf16)
+{
+    return use_direct_wgrad(cs, bf16) ? conv3x3_wgrad_splits(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride) : 0;
+}
+
+hipError_t conv_bwd_weight_partials(const ConvShape& cs, const float* x, const float* dy, float* part, int bf16,
+                                    hipStream_t st)
+{
+    if (!use_direct_wgrad(cs, bf16)) return hipErrorNotSupported;
+    return conv3x3_wgrad(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, part, st);
+}
+
 hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy, float* dw, float* db, int bf16,
                            void* ws, size_t ws_bytes, hipStream_t st)
 {

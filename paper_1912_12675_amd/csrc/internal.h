@@ -167,6 +167,13 @@ hipError_t conv_bwd_data(const ConvShape& cs, const float* w, const float* dy, f
 size_t conv_bwd_weight_ws_bytes(const ConvShape& cs, int bf16);
 hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy, float* dw, float* db,
                            int bf16, void* ws, size_t ws_bytes, hipStream_t st);
+// Weight gradient left as split partial sums part[z][k*c*r*s], z < splits,
+// for a consumer that reduces them (sgd_stage): splits = 0 when the shape has
+// no split form, and then conv_bwd_weight_partials returns
+// hipErrorNotSupported without launching.
+int conv_bwd_weight_part_splits(const ConvShape& cs, int bf16);
+hipError_t conv_bwd_weight_partials(const ConvShape& cs, const float* x, const float* dy, float* part, int bf16,
+                                    hipStream_t st);
 
 // ---- batch norm (+ residual) (+ ReLU) ----
 size_t bn_ws_bytes(int n, int c, int h, int w);
@@ -207,6 +214,20 @@ hipError_t softmax_xent(int n, int classes, const float* logits, const int32_t* 
                         float* dlogits, hipStream_t st);
 hipError_t sgd_momentum(int64_t count, const float* w_in, float* w_out, float* v, const float* g, float lr,
                         float mom, float wd, int nesterov, hipStream_t st);
+// One SGD-momentum update over a stage's packed parameters, described as
+// segments [off, off + count) (offsets relative to w_in / w_out / v / g).  A
+// segment with part != nullptr takes its gradient as the sum of `splits`
+// partial sums part[z][i] (z ascending within each of 16 residue classes
+// z mod 16, then the 16 class sums in order, as the split reduction of
+// conv_bwd_weight adds them) and also writes that sum to g; other segments
+// read g.
+struct SgdSeg {
+    int64_t off, count;
+    const float* part;
+    int32_t splits;
+};
+hipError_t sgd_stage(const SgdSeg* segs, int nseg, const float* w_in, float* w_out, float* v, float* g, float lr,
+                     float mom, float wd, int nesterov, hipStream_t st);
 hipError_t channel_sum(int n, int c, int hw, const float* x, float* out, void* ws, size_t ws_bytes,
                        hipStream_t st);
 size_t channel_sum_ws_bytes(int n, int c, int hw);

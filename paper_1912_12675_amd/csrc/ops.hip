@@ -322,16 +322,85 @@ __global__ __launch_bounds__(kBlock) void softmax_xent_k(int n, int classes, con
     if (threadIdx.x == 0) loss[0] = (float)(t / n);
 }
 
+__device__ __forceinline__ void sgd_one(int64_t i, float gv, const float* w_in, float* w_out, float* v, float lr,
+                                        float mom, float wd, int nesterov)
+{
+    const float w = w_in[i];
+    const float d = gv + wd * w;
+    const float vv = mom * v[i] + d;
+    v[i] = vv;
+    w_out[i] = w - lr * (nesterov ? d + mom * vv : vv);
+}
+
 __global__ void sgd_k(int64_t count, const float* w_in, float* w_out, float* v, const float* g, float lr, float mom,
                       float wd, int nesterov)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (i >= count) return;
-    const float w = w_in[i];
-    const float d = g[i] + wd * w;
-    const float vv = mom * v[i] + d;
-    v[i] = vv;
-    w_out[i] = w - lr * (nesterov ? d + mom * vv : vv);
+    sgd_one(i, g[i], w_in, w_out, v, lr, mom, wd, nesterov);
+}
+
+// Stage update with the split reduction of its conv weight gradients folded
+// in.  A workgroup owns one segment's range: kSgdOut consecutive parameters
+// (one 128-byte line) of a split segment, its kSgdGroups lane groups summing
+// residue classes of the splits, or kSgdBlock parameters of a plain segment.
+constexpr int kSgdBlock = 512, kSgdOut = 32, kSgdGroups = kSgdBlock / kSgdOut, kSgdMaxSegs = 48;
+static_assert(kSgdGroups == 16, "split order: 16 residue classes");
+struct SgdSegDev {
+    int64_t off, count;
+    const float* part;
+    int32_t splits, first_block;
+};
+struct SgdSegs {
+    SgdSegDev s[kSgdMaxSegs];
+    int32_t n;
+};
+
+__global__ __launch_bounds__(kSgdBlock) void sgd_stage_k(SgdSegs segs, const float* w_in, float* w_out, float* v,
+                                                         float* g, float lr, float mom, float wd, int nesterov)
+{
+    __shared__ float sh[kSgdGroups][kSgdOut + 1];
+    // the block's segment: static indices only (kernel-argument loads)
+    int64_t off = segs.s[0].off, count = segs.s[0].count;
+    const float* part = segs.s[0].part;
+    int splits = segs.s[0].splits, first = 0;
+#pragma unroll
+    for (int k = 1; k < kSgdMaxSegs; ++k)
+        if (k < segs.n && (int)blockIdx.x >= segs.s[k].first_block) {
+            off = segs.s[k].off;
+            count = segs.s[k].count;
+            part = segs.s[k].part;
+            splits = segs.s[k].splits;
+            first = segs.s[k].first_block;
+        }
+    const int b = blockIdx.x - first, tid = threadIdx.x;
+    if (!part) {
+        const int64_t i = (int64_t)b * kSgdBlock + tid;
+        if (i < count) sgd_one(off + i, g[off + i], w_in, w_out, v, lr, mom, wd, nesterov);
+        return;
+    }
+    const int o = tid % kSgdOut, zl = tid / kSgdOut;
+    const int64_t i = (int64_t)b * kSgdOut + o;
+    float acc = 0.f;
+    if (i < count) {
+        int z = zl;
+        for (; z + 7 * kSgdGroups < splits; z += 8 * kSgdGroups) {
+            float pv[8];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) pv[u] = part[(int64_t)(z + u * kSgdGroups) * count + i];
+#pragma unroll
+            for (int u = 0; u < 8; ++u) acc += pv[u];
+        }
+        for (; z < splits; z += kSgdGroups) acc += part[(int64_t)z * count + i];
+    }
+    sh[zl][o] = acc;
+    __syncthreads();
+    if (zl == 0 && i < count) {
+        float t = 0.f;
+        for (int q = 0; q < kSgdGroups; ++q) t += sh[q][o];
+        g[off + i] = t;
+        sgd_one(off + i, t, w_in, w_out, v, lr, mom, wd, nesterov);
+    }
 }
 
 // ------------------------------------------------------ FC GEMM (MFMA) -----
@@ -1122,6 +1191,37 @@ hipError_t sgd_momentum(int64_t count, const float* w_in, float* w_out, float* v
     PSW_LAUNCH(kname("sgd_k"), (Work{5.0 * count, 5 * kF * count}), sgd_k, dim3(blocks_for(count)), dim3(kBlock), 0, st,
                count, w_in, w_out, v, g, lr, mom, wd, nesterov);
     return hipGetLastError();
+}
+
+hipError_t sgd_stage(const SgdSeg* segs, int nseg, const float* w_in, float* w_out, float* v, float* g, float lr,
+                     float mom, float wd, int nesterov, hipStream_t st)
+{
+    for (int a0 = 0; a0 < nseg; a0 += kSgdMaxSegs) {
+        SgdSegs ss{};
+        int64_t nb = 0;
+        double fl = 0.0, bytes = 0.0;
+        ss.n = 0;
+        for (int k = a0; k < nseg && k < a0 + kSgdMaxSegs; ++k) {
+            const SgdSeg& q = segs[k];
+            if (q.count <= 0) continue;
+            SgdSegDev& d = ss.s[ss.n++];
+            d.off = q.off;
+            d.count = q.count;
+            d.part = q.splits > 0 ? q.part : nullptr;
+            d.splits = q.splits > 0 ? q.splits : 0;
+            d.first_block = (int32_t)nb;
+            nb += d.part ? (q.count + kSgdOut - 1) / kSgdOut : (q.count + kSgdBlock - 1) / kSgdBlock;
+            fl += 5.0 * q.count + (d.part ? (double)d.splits * q.count : 0.0);
+            bytes += kF * (5.0 * q.count + (d.part ? (double)d.splits * q.count : 0.0));
+        }
+        if (!ss.n) continue;
+        if (nb > INT32_MAX) return hipErrorInvalidValue;
+        PSW_LAUNCH(kname("sgd_stage_k"), (Work{fl, bytes}), sgd_stage_k, dim3((unsigned)nb), dim3(kSgdBlock), 0, st, ss,
+                   w_in, w_out, v, g, lr, mom, wd, nesterov);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
 }
 
 hipError_t fc_fwd(int n, int in, int out, const float* x, const float* w, const float* b, int relu, float* y, int bf16,
