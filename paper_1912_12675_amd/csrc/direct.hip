@@ -461,25 +461,71 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
         const int c = i / HR, rr = i - (i / HR) * HR;
         Xs[c * PS + rr * RSTR + WO] = 0.f;
     }
-    for (int c0 = 0; c0 < a.KL; c0 += CC) {
-        __syncthreads();
-        constexpr int Q4 = WO / 4;
-        for (int i = tid; i < CC * HR * Q4; i += NT) {
-            const int c = i / (HR * Q4);
-            const int rem = i - c * (HR * Q4);
-            const int rr = rem / Q4, q4 = rem - (rem / Q4) * Q4;
-            const int ih = i0 + rr;
+    // Software pipeline over chunks of CC dy channels: the next chunk's dy
+    // tile and weights are loaded into registers while the current one is
+    // on the matrix cores.  Per-thread staging coordinates are fixed.
+    constexpr int Q4 = WO / 4;
+    constexpr int XN = CC * HR * Q4, XV = (XN + NT - 1) / NT;
+    // weights w_layer[c][m][rs]: for each dy channel c of the chunk a run of
+    // TK*9 floats (output channels mblk.. of dx), loaded as float4
+    constexpr int WN4 = CC * TK * 9 / 4, WV = (WN4 + NT - 1) / NT;
+    static_assert((TK * 9) % 4 == 0, "float4 weight runs");
+    int xl[XV], xg[XV], xrow[XV];
+    bool xon[XV];
+#pragma unroll
+    for (int k = 0; k < XV; ++k) {
+        const int i = tid + k * NT;
+        const int c = i / (HR * Q4), rem = i - (i / (HR * Q4)) * (HR * Q4);
+        const int rr = rem / Q4, q4 = rem - (rem / Q4) * Q4;
+        xon[k] = i < XN;
+        xl[k] = c * PS + rr * RSTR + q4 * 4;
+        xg[k] = (c * a.HO + rr) * WO + q4 * 4;  // from (plane c0, row i0)
+        xrow[k] = rr;
+    }
+    int wg[WV], wl[WV][4];
+    bool won[WV];
+#pragma unroll
+    for (int k = 0; k < WV; ++k) {
+        const int i = (tid + k * NT) * 4;
+        won[k] = i < WN4 * 4;
+        const int c = i / (TK * 9), rem = i - (i / (TK * 9)) * (TK * 9);
+        wg[k] = c * a.CL * 9 + mblk * 9 + rem;  // from dy channel c0
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {  // a run of 4 never crosses c (TK*9 % 4 == 0)
+            const int m = (rem + e) / 9, rs = (rem + e) - ((rem + e) / 9) * 9;
+            wl[k][e] = m * WR + c * 9 + rs;
+        }
+    }
+    float4 xr[XV], wr[WV];
+    auto load_chunk = [&](int c0) {
+        const int xb = ((img * a.KL + c0) * a.HO + i0) * WO;
+#pragma unroll
+        for (int k = 0; k < XV; ++k) {
             float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-            if (ih < a.HO)
-                v = *reinterpret_cast<const float4*>(a.dy + (((size_t)img * a.KL + c0 + c) * a.HO + ih) * WO + q4 * 4);
-            *reinterpret_cast<float4*>(&Xs[c * PS + rr * RSTR + q4 * 4]) = v;
+            if (xon[k] && i0 + xrow[k] < a.HO) v = *reinterpret_cast<const float4*>(a.dy + (xb + xg[k]));
+            xr[k] = v;
         }
-        for (int i = tid; i < TK * CC * 9; i += NT) {  // w_layer[c][m][rs] -> Wc[m][c*9 + rs]
-            const int c = i / (TK * 9), rem = i - (i / (TK * 9)) * (TK * 9);
-            const int m = rem / 9, rs = rem - (rem / 9) * 9;
-            Wc[m * WR + c * 9 + rs] = a.w[((size_t)(c0 + c) * a.CL + mblk) * 9 + rem];
-        }
+        const float* wb = a.w + (size_t)c0 * a.CL * 9;
+#pragma unroll
+        for (int k = 0; k < WV; ++k)
+            wr[k] = won[k] ? *reinterpret_cast<const float4*>(wb + wg[k]) : make_float4(0.f, 0.f, 0.f, 0.f);
+    };
+    load_chunk(0);
+    for (int c0 = 0; c0 < a.KL; c0 += CC) {
+        __syncthreads();  // the previous chunk's LDS reads are complete
+#pragma unroll
+        for (int k = 0; k < XV; ++k)
+            if (xon[k]) *reinterpret_cast<float4*>(&Xs[xl[k]]) = xr[k];
+#pragma unroll
+        for (int k = 0; k < WV; ++k)
+            if (won[k]) {
+                Wc[wl[k][0]] = wr[k].x;
+                Wc[wl[k][1]] = wr[k].y;
+                Wc[wl[k][2]] = wr[k].z;
+                Wc[wl[k][3]] = wr[k].w;
+            }
         __syncthreads();
+        if (c0 + CC < a.KL) load_chunk(c0 + CC);
         const float* wf = Wc + (wk * 16 + j) * WR + g * 9;
 #pragma unroll
         for (int c4 = 0; c4 < CC / 4; ++c4) {
@@ -696,7 +742,10 @@ hipError_t conv3x3_dgrad_s2(int n, int CL, int H, int W, int KL, const float* w,
                             int accumulate, hipStream_t st, const BnBwdFuse* bnb)
 {
     if (H % 2 || W % 2 || KL % 16) return hipErrorNotSupported;
-    if ((uintptr_t)dy % 16 || (uintptr_t)dx % 8) return hipErrorNotSupported;  // float4 staging, float2 stores
+    // float4 staging of dy and of the weights, float2 stores
+    if ((uintptr_t)dy % 16 || (uintptr_t)w % 16 || (uintptr_t)dx % 8) return hipErrorNotSupported;
+    // 32-bit element offsets of the staging
+    if ((int64_t)n * KL * (H / 2) * (W / 2) > INT32_MAX || (int64_t)KL * CL * 9 > INT32_MAX) return hipErrorNotSupported;
     const int HO = H / 2, WO = W / 2;
     DgArgs a{dy, w, dx, KL, CL, HO, accumulate, BnBwdFuse{}};
     if (bnb) a.bnb = *bnb;

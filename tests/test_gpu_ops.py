@@ -65,6 +65,7 @@ CONV = [
     (2, 128, 16, 16, 128, 3, 1, 1),
     (2, 256, 8, 8, 256, 3, 1, 1),
     (3, 16, 16, 16, 64, 3, 2, 1),
+    (2, 48, 16, 16, 32, 3, 2, 1),
 ]
 
 
