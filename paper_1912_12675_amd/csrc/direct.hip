@@ -727,7 +727,7 @@ hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const f
     if (stride == 1) {
         if (WO == 32 && HO % 8 == 0 && K % 16 == 0) return launch_direct<32, 1, 8, 16, 1, 4, 4>(a, n, transpose, st);
         if (WO == 16 && HO % 8 == 0 && K % 32 == 0) return launch_direct<16, 1, 8, 16, 2, 4, 2>(a, n, transpose, st);
-        if (WO == 8 && HO % 8 == 0 && K % 32 == 0) return launch_direct<8, 1, 8, 16, 2, 2, 2>(a, n, transpose, st);
+        if (WO == 8 && HO % 8 == 0 && K % 32 == 0) return launch_direct<8, 1, 8, 16, 2, 4, 1>(a, n, transpose, st);
     } else if (!transpose) {
         if (WO == 16 && HO % 8 == 0 && K % 32 == 0) return launch_direct<16, 2, 8, 16, 2, 4, 2>(a, n, false, st);
         if (WO == 8 && HO % 8 == 0 && K % 32 == 0) return launch_direct<8, 2, 8, 16, 2, 2, 2>(a, n, false, st);
