@@ -308,6 +308,18 @@ int psw_net_slot(const psw_net *net, int stage, int64_t version, float **params)
  * count of operation `op`'s parameters (host outputs). */
 int psw_net_param_offset(const psw_net *net, int op, int *stage, int64_t *offset, int64_t *count);
 
+/* Comparison scheme (Sec. 6.7, Sec. 7): with on != 0, every later step's
+ * backward pass takes its data gradients (conv and FC transposes, BN's
+ * gamma) with the version its forward pass read, r_s = max(0, t - d_s), as
+ * weight stashing does, instead of the current version t (the paper's
+ * scheme, the default).  Weight gradients and the update are unchanged.
+ * The ring already holds version r_s (d_s < ring_depth[s]), so this needs no
+ * memory; a multi-device pipeline that stashes keeps d_s extra copies of
+ * stage s's weights.  Takes effect from the next psw_stage_step /
+ * psw_pipeline_run / psw_pipeline_capture call; PSW_ERR_NULL for a NULL
+ * net. */
+int psw_net_set_weight_stashing(psw_net *net, int on);
+
 /* Dry run of psw_stage_step (host only, no device work): the kernel-level
  * plan of step t.  Each record is (op, what, stage, version) where `what`
  * is a PSW_PLAN_* code, `version` the weight version it reads (-1 if

@@ -79,7 +79,7 @@ def _declare(L):
                                     _d, _d, _d]
     L.orc_loss_and_grad.restype = _I
     L.orc_train.argtypes = [_I, _i32, _I, _I, _I, _I, _I, _i32, _d, _I, _f, _i32, _i32, _d,
-                            _D, _D, _I, _D, _D, _I, _d, _d, _d, _d, _d, _i32]
+                            _D, _D, _I, _D, _D, _I, _I, _d, _d, _d, _d, _d, _i32]
     L.orc_train.restype = _I
 
 
@@ -294,10 +294,12 @@ def loss_and_grad(ops, in_shape, stage_end, params, x, labels, bn_eps=1e-5, bf16
 
 
 def train(ops, in_shape, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=0.0,
-          nesterov=False, bn_eps=1e-5, bn_mom=0.1, bf16=False):
+          nesterov=False, bn_eps=1e-5, bn_mom=0.1, bf16=False, stash=False):
     """Run T steps of the stale-weight schedule.  xs: [T, N, C, H, W] float32;
-    labels [T, N]; staleness [T, S].  Returns a dict with params, momentum,
-    run_mean, run_var, losses and versions."""
+    labels [T, N]; staleness [T, S].  stash=True: the backward pass takes its
+    data gradients with the forward's weight version (weight stashing, the
+    scheme Sec. 6.7 contrasts with) instead of the current one.  Returns a dict
+    with params, momentum, run_mean, run_var, losses and versions."""
     ops = _desc(ops)
     se = np.ascontiguousarray(stage_end, dtype=np.int32)
     S = len(se)
@@ -315,7 +317,7 @@ def train(ops, in_shape, stage_end, params0, xs, labels, staleness, lr, mom=0.9,
     versions = np.zeros((T, S), dtype=np.int32)
     rc = lib().orc_train(len(ops), _p(ops, _i32), N, *in_shape, S, _p(se, _i32), _p(params0, _d), T,
                          _p(xs, _f), _p(labels, _i32), _p(stal, _i32), _p(lr, _d), mom, wd,
-                         int(nesterov), bn_eps, bn_mom, int(bf16), _p(out, _d), _p(momb, _d),
+                         int(nesterov), bn_eps, bn_mom, int(bf16), int(stash), _p(out, _d), _p(momb, _d),
                          _p(rm, _d), _p(rv, _d), _p(losses, _d), _p(versions, _i32))
     if rc != 0:
         raise ValueError(f"oracle rejected the run (code {rc})")

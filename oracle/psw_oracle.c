@@ -847,6 +847,8 @@ int orc_loss_and_grad(int n_ops, const int32_t *desc, int N, int C0, int H0, int
 /*   loss and its gradient;                                                  */
 /*   backward: data gradients with W_s^(t), weight gradients from the saved  */
 /*   activations;                                                           */
+/*   (stash != 0: data gradients with W_s^(r_s) instead, the weight-stashing */
+/*   scheme that the paper contrasts its own with, Sec. 6.7 and Sec. 7)     */
 /*   update:  W_s^(t+1) = SGD(W_s^(t), grad_s)  for every stage s.           */
 /* The full history W_s^(0..T) is kept (no ring): version v of stage s is    */
 /* history[s][v].  The hybrid schedule of Sec. 4 is expressed by giving      */
@@ -866,7 +868,7 @@ int orc_loss_and_grad(int n_ops, const int32_t *desc, int N, int C0, int H0, int
 int orc_train(int n_ops, const int32_t *desc, int N, int C0, int H0, int W0, int n_stages,
               const int32_t *stage_end, const double *params0, int T, const float *xs,
               const int32_t *labels, const int32_t *staleness, const double *lr, double mom,
-              double wd, int nesterov, double bn_eps, double bn_mom, int bf16, double *params_out,
+              double wd, int nesterov, double bn_eps, double bn_mom, int bf16, int stash, double *params_out,
               double *mom_out, double *run_mean, double *run_var, double *losses, int32_t *versions)
 {
     orc_net net;
@@ -913,7 +915,7 @@ int orc_train(int n_ops, const int32_t *desc, int N, int C0, int H0, int W0, int
             const int r = t - d > 0 ? t - d : 0;
             versions[(int64_t)t * S + s] = r;
             wfor[s] = hist[s][r];
-            wcur[s] = hist[s][t];
+            wcur[s] = stash ? hist[s][r] : hist[s][t];
         }
         orc_fwd_state st;
         state_alloc(&st, n_ops);

@@ -301,6 +301,9 @@ struct psw_net {
         int op;  // conv op whose partial sums give the gradient, -1: read the gradient array
     };
     std::vector<std::vector<SegProto>> sgd_segs;  // per stage
+    // per stage: it has conv layers, whose weight gradients run on the weight
+    // stream; a stage without them is updated on the data-gradient stream
+    std::vector<char> stage_has_conv;
     // backward-weight kernels run on a second stream of the library, forked
     // from the caller's stream when a conv's output gradient is final and
     // joined before the update (created at bind, default priority)
@@ -323,6 +326,9 @@ struct psw_net {
     char* arena = nullptr;
     bool bound = false;
     int64_t next_t = 0;
+    // 1: the backward pass takes its data gradients with the forward's
+    // version r_s (weight stashing, the comparison scheme), 0: with version t
+    int stash = 0;
     // optional per-kernel timing with HIP events (psw_net_profile): while
     // psw_stage_step runs with profiling on, rec is this thread's kernel
     // recorder and every library kernel launch adds one KRec
@@ -573,6 +579,9 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
     net->wpart_splits.assign(n_layers, 0);
     net->wpart_off.assign(n_layers, 0);
     net->sgd_segs.assign(n_stages, {});
+    net->stage_has_conv.assign(n_stages, 0);
+    for (int i = 0; i < n_layers; ++i)
+        if (net->ops[i].kind == PSW_OP_CONV) net->stage_has_conv[net->stage_of[i]] = 1;
     size_t wpart = 0;
     for (int s = 0; s < n_stages; ++s) {
         size_t cur = 0;
@@ -746,6 +755,14 @@ int psw_net_param_offset(const psw_net* net, int op, int* stage, int64_t* offset
     return PSW_OK;
 }
 
+int psw_net_set_weight_stashing(psw_net* net, int on)
+{
+    if (!net) return fail(PSW_ERR_NULL, "net_set_weight_stashing: net is NULL");
+    net->stash = on ? 1 : 0;
+    g_err.clear();
+    return PSW_OK;
+}
+
 int psw_net_plan(const psw_net* net, int64_t t, const int32_t* staleness, psw_launch* out, int cap, int* n_out)
 {
     if (!net || !n_out) return fail(PSW_ERR_NULL, "net_plan: required pointer is NULL");
@@ -773,19 +790,20 @@ int psw_net_plan(const psw_net* net, int64_t t, const int32_t* staleness, psw_la
     for (int i = L - 1; i >= 0; --i) {
         const psw_layer& o = net->ops[i];
         const int s = net->stage_of[i];
+        const int64_t vb = net->stash ? fwd_version(t, staleness[s]) : t;  // backward's version
         switch (o.kind) {
         case PSW_OP_CONV:
             if (o.flags & PSW_F_RELU) rec(i, PSW_PLAN_RELU_MASK, s, -1);
-            if (o.in0 > 0) rec(i, PSW_PLAN_CONV_BWD_DATA, s, t);
+            if (o.in0 > 0) rec(i, PSW_PLAN_CONV_BWD_DATA, s, vb);
             break;
-        case PSW_OP_BN: rec(i, PSW_PLAN_BN_BWD, s, t); break;
+        case PSW_OP_BN: rec(i, PSW_PLAN_BN_BWD, s, vb); break;
         case PSW_OP_MAXPOOL:
         case PSW_OP_GAVG:
             if (o.in0 > 0) rec(i, PSW_PLAN_POOL_BWD, s, -1);
             break;
         case PSW_OP_FC:
             if (o.flags & PSW_F_RELU) rec(i, PSW_PLAN_RELU_MASK, s, -1);
-            rec(i, PSW_PLAN_FC_BWD, s, t);
+            rec(i, PSW_PLAN_FC_BWD, s, vb);
             break;
         }
         // when the data-gradient chain is done with a stage: the stage's
@@ -837,6 +855,8 @@ struct Issue {
         return slot_ptr(net, s, io.rv[s]) + net->poff[i];
     }
     const float* wcur(int i) const { return slot_ptr(net, net->stage_of[i], io.t) + net->poff[i]; }
+    // weights of the backward pass's data gradients
+    const float* wbwd(int i) const { return net->stash ? wfwd(i) : wcur(i); }
     float* gptr(int i) const { return io.gbase + net->flat_off[net->stage_of[i]] + net->poff[i]; }
 };
 
@@ -951,14 +971,17 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
     return hipSuccess;
 }
 
-// Backward pass and updates of one step: the data-gradient chain on sb; the
-// weight gradient of every conv forked to sw (it shares only the step's
-// activations with the chain); when the chain has finished stage s, sw waits
-// for it and writes version t+1 of stage s (all of the stage's parameter
-// gradients are then complete, and nothing later in the step reads the
-// stage's version t), then after_update(s) runs with sw current.
-template <typename AfterUpdate>
-hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, AfterUpdate after_update)
+// Backward pass and updates of one step: the data-gradient chain on sb;
+// before_stage(s) runs before the chain's first operation of stage s.  When
+// the chain has finished stage s, sw waits for it, computes the stage's conv
+// weight gradients (they share only the step's activations with the chain)
+// and writes version t+1 of stage s (all of the stage's parameter gradients
+// are then complete, and nothing later in the step reads the stage's version
+// t); a stage without convs is updated on sb.  after_update(s, stream) then
+// runs with the stream that issued the update.
+template <typename BeforeStage, typename AfterUpdate>
+hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage before_stage,
+                          AfterUpdate after_update)
 {
     psw_net* net = is.net;
     const StepIO& io = is.io;
@@ -974,6 +997,8 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, AfterUpdate
         const psw_layer& o = net->ops[i];
         const Tensor a = net->t[o.in0];
         const Tensor y = net->t[i + 1];
+        if (i == net->stage_end[net->stage_of[i]] - 1)
+            PSW_TRY(before_stage(net->stage_of[i]), "backward order");
         float* g = is.grd(i + 1);
         float* din = o.in0 > 0 ? is.grd(o.in0) : nullptr;
         const int acc0 = net->grad_accum[2 * i];
@@ -994,14 +1019,14 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, AfterUpdate
                     bnb.scale = bsave + 2 * bo.cin;
                     bnb.shift = bsave + 3 * bo.cin;
                 }
-                e = psw::conv_bwd_data_bnsums(cs, is.wcur(i), g, din, acc0, bnb, sb);
+                e = psw::conv_bwd_data_bnsums(cs, is.wbwd(i), g, din, acc0, bnb, sb);
                 if (e == hipSuccess)
                     net->fused_bwd_now[i] = 1;
                 else if (e != hipErrorNotSupported)  // not supported: nothing launched, unfused path below
                     PSW_TRY(e, "conv_bwd_data_bnsums");
             }
             if (din && !net->fused_bwd_now[i])
-                PSW_TRY(psw::conv_bwd_data(cs, is.wcur(i), g, din, acc0, bf16, sb), "conv_bwd_data");
+                PSW_TRY(psw::conv_bwd_data(cs, is.wbwd(i), g, din, acc0, bf16, sb), "conv_bwd_data");
             break;
         }
         case PSW_OP_BN: {
@@ -1022,7 +1047,7 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, AfterUpdate
                 const int T = psw::conv_bwd_data_bnsums_tiles(ccs);
                 // without a residual the ReLU mask comes from y and the forward's scale / shift
                 const float* scale = o.in1 < 0 ? save + 2 * o.cin : nullptr;
-                e = psw::bn_bwd_from_partials(a.n, a.c, a.h, a.w, g, is.act(i + 1), is.act(o.in0), is.wcur(i), save,
+                e = psw::bn_bwd_from_partials(a.n, a.c, a.h, a.w, g, is.act(i + 1), is.act(o.in0), is.wbwd(i), save,
                                               save + o.cin, scale, (const float*)ws, T, (o.flags & PSW_F_RELU) != 0,
                                               din, dg, dg + o.cin, dres, r.c, r.h, r.w, net->grad_accum[2 * i + 1], sb);
                 if (e == hipSuccess)
@@ -1031,7 +1056,7 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, AfterUpdate
                     PSW_TRY(e, "bn_bwd_from_partials");
             }
             if (!done)
-                PSW_TRY(psw::bn_bwd(a.n, a.c, a.h, a.w, g, is.act(i + 1), is.act(o.in0), is.wcur(i), save,
+                PSW_TRY(psw::bn_bwd(a.n, a.c, a.h, a.w, g, is.act(i + 1), is.act(o.in0), is.wbwd(i), save,
                                     save + o.cin, (o.flags & PSW_F_RELU) != 0, din, dg, dg + o.cin, dres, r.c, r.h,
                                     r.w, net->grad_accum[2 * i + 1], ws, wsb, sb),
                         "bn_bwd");
@@ -1054,7 +1079,7 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, AfterUpdate
             float* dw = is.gptr(i);
             float* db = (o.flags & PSW_F_BIAS) ? dw + (int64_t)o.cout * o.cin : nullptr;
             kind = PSW_PROF_FC;
-            PSW_TRY(psw::fc_bwd(a.n, o.cin, o.cout, is.act(o.in0), is.wcur(i), g, din, acc0, dw, db, bf16, ws, wsb,
+            PSW_TRY(psw::fc_bwd(a.n, o.cin, o.cout, is.act(o.in0), is.wbwd(i), g, din, acc0, dw, db, bf16, ws, wsb,
                                 sb),
                     "fc_bwd");
             break;
@@ -1064,9 +1089,13 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, AfterUpdate
         if (i == net->stage_begin[s]) {
             // the chain is done with stage s: its weight gradients (from the
             // step's activations and the now final output gradients) and its
-            // update run on sw, beside the chain's next stage
-            PSW_TRY(hipEventRecord(net->stage_ev[s], sb), "stage join");
-            PSW_TRY(hipStreamWaitEvent(sw, net->stage_ev[s], 0), "stage join");
+            // update run on sw, beside the chain's next stage; a stage
+            // without convs is updated on the chain's stream itself
+            const hipStream_t su = net->stage_has_conv[s] ? sw : sb;
+            if (su != sb) {
+                PSW_TRY(hipEventRecord(net->stage_ev[s], sb), "stage join");
+                PSW_TRY(hipStreamWaitEvent(sw, net->stage_ev[s], 0), "stage join");
+            }
             for (int j = net->stage_end[s] - 1; j >= net->stage_begin[s]; --j) {
                 const psw_layer& c = net->ops[j];
                 if (c.kind != PSW_OP_CONV) continue;
@@ -1095,10 +1124,10 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, AfterUpdate
                 }
                 PSW_TRY(psw::sgd_stage(segs, m, slot_ptr(net, s, io.t), slot_ptr(net, s, io.t + 1),
                                        net->momentum + net->flat_off[s], io.gbase + net->flat_off[s], io.lr[s], io.mom,
-                                       io.wd, io.nesterov, sw),
+                                       io.wd, io.nesterov, su),
                         "sgd");
             }
-            PSW_TRY(after_update(s), "update event");
+            PSW_TRY(after_update(s, su), "update event");
         }
     }
     return hipSuccess;
@@ -1136,7 +1165,9 @@ int psw_stage_step(psw_net* net, int64_t t, const int32_t* staleness, const floa
     // gradients and updates on the side stream, joined back at the end (also
     // when a launcher fails part way)
     hipError_t e = issue_forward(is, st, [](int) { return hipSuccess; });
-    if (e == hipSuccess) e = issue_backward(is, st, net->side, [](int) { return hipSuccess; });
+    if (e == hipSuccess)
+        e = issue_backward(is, st, net->side, [](int) { return hipSuccess; },
+                           [](int, hipStream_t) { return hipSuccess; });
     hipError_t ej = hipEventRecord(net->join_ev, net->side);
     if (ej == hipSuccess) ej = hipStreamWaitEvent(st, net->join_ev, 0);
     if (e != hipSuccess) return hip_check(e, is.what);
@@ -1231,9 +1262,11 @@ int issue_pipeline(psw_net* net, int64_t t0, int n_steps, const int32_t* stalene
         }
         // stage s reads version r = rv[s]; wait for the update that wrote it
         // when it was written inside this run
+        // (the weight stream runs in order, so the wait for step t-NS above
+        // already covers every update of steps <= t-NS)
         e = issue_forward(is, sf, [&](int s) -> hipError_t {
             const int64_t r = io.rv[s];
-            if (r - 1 < t0) return hipSuccess;
+            if (r - 1 < t0 || (i >= NS && r - 1 <= t - NS && net->stage_has_conv[s])) return hipSuccess;
             return hipStreamWaitEvent(sf, net->upd_ev[(size_t)s * Q + (size_t)(r % Q)], 0);
         });
         if (e != hipSuccess) {
@@ -1247,9 +1280,18 @@ int issue_pipeline(psw_net* net, int64_t t0, int n_steps, const int32_t* stalene
             what = "pipeline: backward order";
             break;
         }
-        e = issue_backward(is, sb, sw, [&](int s) -> hipError_t {
-            return hipEventRecord(net->upd_ev[(size_t)s * Q + (size_t)((t + 1) % Q)], sw);
-        });
+        // stage s of backward t reads version t (written by the update of step
+        // t-1 on the weight stream) unless it stashes; the forward's waits
+        // already cover d_s = 0 and stashing (both read the version r_s)
+        e = issue_backward(
+            is, sb, sw,
+            [&](int s) -> hipError_t {
+                if (net->stash || t - 1 < t0 || io.rv[s] == t || !net->stage_has_conv[s]) return hipSuccess;
+                return hipStreamWaitEvent(sb, net->upd_ev[(size_t)s * Q + (size_t)(t % Q)], 0);
+            },
+            [&](int s, hipStream_t su) -> hipError_t {
+                return hipEventRecord(net->upd_ev[(size_t)s * Q + (size_t)((t + 1) % Q)], su);
+            });
         if (e != hipSuccess) {
             what = is.what;
             break;

@@ -80,6 +80,7 @@ SIGNATURES = {
     "psw_net_bind": (_I, [_P, _P, _P, _P, _P, _P, _P, _SZ]),
     "psw_stage_step": (_I, [_P, _I64, _P, _P, _F, _F, _I, _P, _P, _P, _P, _P]),
     "psw_net_set_step": (_I, [_P, _I64]),
+    "psw_net_set_weight_stashing": (_I, [_P, _I]),
     "psw_net_slot": (_I, [_P, _I, _I64, ctypes.POINTER(ctypes.c_void_p)]),
     "psw_net_param_offset": (_I, [_P, _I, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int64),
                                   ctypes.POINTER(ctypes.c_int64)]),
@@ -352,6 +353,10 @@ class Net:
     def set_step(self, t):
         _check(lib().psw_net_set_step(self.handle, int(t)))
 
+    def set_weight_stashing(self, on=True):
+        """Backward data gradients with the forward's version (comparison scheme)."""
+        _check(lib().psw_net_set_weight_stashing(self.handle, int(bool(on))))
+
     def step(self, t, staleness, lr, x, labels, mom=0.9, wd=0.0, nesterov=False, stream=None):
         st = np.ascontiguousarray(staleness, dtype=np.int32)
         lrs = np.ascontiguousarray(np.broadcast_to(np.asarray(lr, dtype=np.float32), (self.S,)))
@@ -435,7 +440,7 @@ class Net:
         return [(buf[i].op, buf[i].what, buf[i].stage, buf[i].version) for i in range(min(n.value, cap))]
 
 
-def net_plan_only(ops, batch, in_shape, stage_end, ring_depth, t, staleness, bf16=False, cap=4096):
+def net_plan_only(ops, batch, in_shape, stage_end, ring_depth, t, staleness, bf16=False, cap=4096, stash=False):
     """psw_net_create + psw_net_plan without binding any memory (host only)."""
     L = lib()
     layers = _layers(ops)
@@ -448,6 +453,7 @@ def net_plan_only(ops, batch, in_shape, stage_end, ring_depth, t, staleness, bf1
         st = np.ascontiguousarray(staleness, dtype=np.int32)
         buf = (psw_launch * cap)()
         n = ctypes.c_int()
+        _check(L.psw_net_set_weight_stashing(h.value, int(bool(stash))))
         _check(L.psw_net_plan(h.value, int(t), st.ctypes.data, buf, cap, ctypes.byref(n)))
         return [(buf[i].op, buf[i].what, buf[i].stage, buf[i].version) for i in range(min(n.value, cap))]
     finally:

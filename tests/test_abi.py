@@ -96,6 +96,26 @@ def test_plan_versions_follow_schedule(psw):
     assert kinds.count(1) == 19 and kinds.count(7) == 19 and kinds.count(8) == 18
 
 
+def test_plan_weight_stashing(psw):
+    """With weight stashing on, the backward records read the forward's
+    version r_s; forward records and updates are unchanged."""
+    wl = synth.resnet20_workload(batch=4)
+    d = [3, 2, 1, 0]
+    for t in (0, 2, 7):
+        base = _plan(psw, wl, t, d)
+        st = psw.net_plan_only(wl.ops, 4, wl.in_shape, wl.stage_end, wl.ring_depth(20), t, d, stash=True)
+        assert len(st) == len(base)
+        for (o1, w1, s1, v1), (o2, w2, s2, v2) in zip(base, st):
+            assert (o1, w1, s1) == (o2, w2, s2)
+            if w1 in (8, 9, 11):
+                assert v1 == t and v2 == max(0, t - d[s1])
+            else:
+                assert v1 == v2
+    with pytest.raises(psw.PswError) as e:
+        psw._check(psw.lib().psw_net_set_weight_stashing(None, 1))
+    assert e.value.code == -1
+
+
 def test_plan_rejects_bad_staleness(psw):
     wl = synth.resnet20_workload(batch=4)
     with pytest.raises(psw.PswError) as e:

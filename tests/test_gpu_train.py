@@ -32,12 +32,14 @@ def P():
     return psw
 
 
-def gpu_train(P, wl, T, batch=None, net=None, t0=0):
+def gpu_train(P, wl, T, batch=None, net=None, t0=0, stash=False):
     N = wl.batch if batch is None else batch
     st = wl.staleness(T)
     if net is None:
         net = P.Net(wl.ops, N, wl.in_shape, wl.stage_end, wl.ring_depth(T), bf16=wl.bf16)
         net.load_params(synth.init_params(wl))
+        if stash:
+            net.set_weight_stashing(True)
     losses, versions = [], []
     for t in range(t0, T):
         x, y = synth.batch(wl, t, N)
@@ -49,11 +51,11 @@ def gpu_train(P, wl, T, batch=None, net=None, t0=0):
     return net, np.array(losses), np.array(versions)
 
 
-def oracle_train(oracle, wl, T, batch=None):
+def oracle_train(oracle, wl, T, batch=None, stash=False):
     N = wl.batch if batch is None else batch
     xs, ys = synth.batches(wl, T, N)
     return oracle.train(wl.ops, wl.in_shape, wl.stage_end, synth.init_params(wl), xs, ys, wl.staleness(T), wl.lr,
-                        wl.momentum, wl.weight_decay, wl.nesterov, bf16=wl.bf16)
+                        wl.momentum, wl.weight_decay, wl.nesterov, bf16=wl.bf16, stash=stash)
 
 
 def deviations(wl, flat, losses, ref_flat, ref_losses, p0):
@@ -74,7 +76,7 @@ def deviations(wl, flat, losses, ref_flat, ref_losses, p0):
     return glob, per, lrel, upd
 
 
-def reference_spread(oracle, wl, T, batch, xs, ys):
+def reference_spread(oracle, wl, T, batch, xs, ys, stash=False):
     """Independent computations at the GPU's precision, to measure how far
     such a computation lands from the oracle on this run: fp32 -> the stale
     schedule written with torch autograd in float32 (CPU) on the inputs and
@@ -88,12 +90,12 @@ def reference_spread(oracle, wl, T, batch, xs, ys):
     if not wl.bf16:
         for inp in (xs, up, down):
             p, l, _ = torch_ref.train_stale(wl.ops, wl.stage_end, p0, inp, ys, wl.staleness(T), wl.lr, wl.momentum,
-                                            wl.weight_decay, dtype=torch.float32)
+                                            wl.weight_decay, dtype=torch.float32, stash=stash)
             out.append((p, l))
         return out
     for inp in (up, down):
         o = oracle.train(wl.ops, wl.in_shape, wl.stage_end, p0, inp, ys, wl.staleness(T), wl.lr, wl.momentum,
-                         wl.weight_decay, wl.nesterov, bf16=True)
+                         wl.weight_decay, wl.nesterov, bf16=True, stash=stash)
         out.append((o["params"], o["losses"]))
     return out
 
@@ -109,8 +111,15 @@ CASES = [
 ]
 
 
-@pytest.mark.parametrize("name,factory,batch,T", CASES, ids=[c[0] for c in CASES])
-def test_train_parity(P, oracle, name, factory, batch, T):
+STASH_CASES = [
+    ("resnet20_b8_stash", lambda: synth.resnet20_workload(batch=8), 8, 10),
+    ("alexnet_b4_stash", lambda: synth.alexnet_workload(batch=4), 4, 4),
+]
+
+
+@pytest.mark.parametrize("name,factory,batch,T,stash", [c + (False,) for c in CASES] + [c + (True,) for c in STASH_CASES],
+                         ids=[c[0] for c in CASES] + [c[0] for c in STASH_CASES])
+def test_train_parity(P, oracle, name, factory, batch, T, stash):
     """Bar: max(spec bar, 4 x reference spread) for the whole parameter
     vector, for every tensor with a non-zero initial value, and for the
     losses; the spec bar is 1e-4 (fp32) / 2e-2 (bf16).  The spread
@@ -120,18 +129,21 @@ def test_train_parity(P, oracle, name, factory, batch, T):
     zero, and in bf16 mode operand roundings, flip between any two
     implementations that do not share every intermediate bit.  In VGG-16 one
     such flip (a max-pool near-tie) already moves every gradient below it by
-    1e-3..2e-3 in a single step, for torch float32 as for the GPU."""
+    1e-3..2e-3 in a single step, for torch float32 as for the GPU.
+
+    The *_stash cases run the comparison scheme (weight stashing: data
+    gradients with the forward's version) against the oracle's stash mode."""
     print(f"train parity {name}: batch {batch}, {T} steps", flush=True)
     wl = factory()
-    net, losses, versions = gpu_train(P, wl, T, batch)
-    ref = oracle_train(oracle, wl, T, batch)
+    net, losses, versions = gpu_train(P, wl, T, batch, stash=stash)
+    ref = oracle_train(oracle, wl, T, batch, stash=stash)
     xs, ys = synth.batches(wl, T, batch)
     p0 = synth.init_params(wl).astype(np.float64)
     got = net.params(T).double().numpy()
     g_glob, g_per, g_loss, g_upd = deviations(wl, got, losses, ref["params"], ref["losses"], p0)
     s_glob = s_loss = s_upd = 0.0
     s_per = {}
-    for sp_p, sp_l in reference_spread(oracle, wl, T, batch, xs, ys):
+    for sp_p, sp_l in reference_spread(oracle, wl, T, batch, xs, ys, stash=stash):
         a, b, c, d = deviations(wl, sp_p, sp_l, ref["params"], ref["losses"], p0)
         s_glob, s_loss, s_upd = max(s_glob, a), max(s_loss, c), max(s_upd, d)
         s_per = {k: max(s_per.get(k, 0.0), v) for k, v in b.items()}
@@ -222,10 +234,11 @@ def test_step_order_enforced(P):
 
 
 # ---- pipelined execution (psw_pipeline_run) -------------------------------
-def _sequential(P, wl, N, st, lr):
+def _sequential(P, wl, N, st, lr, stash=False):
     net = P.Net(wl.ops, N, wl.in_shape, wl.stage_end, [int(st[:, s].max()) + 1 for s in range(st.shape[1])],
                 bf16=wl.bf16)
     net.load_params(synth.init_params(wl))
+    net.set_weight_stashing(stash)
     losses, versions = [], []
     for t in range(st.shape[0]):
         x, y = synth.batch(wl, t, N)
@@ -236,11 +249,12 @@ def _sequential(P, wl, N, st, lr):
     return net, np.array(losses, dtype=np.float32), np.array(versions)
 
 
-def _pipelined(P, wl, N, st, lr, chunks):
+def _pipelined(P, wl, N, st, lr, chunks, stash=False):
     T = st.shape[0]
     net = P.Net(wl.ops, N, wl.in_shape, wl.stage_end, [int(st[:, s].max()) + 1 for s in range(st.shape[1])],
                 bf16=wl.bf16)
     net.load_params(synth.init_params(wl))
+    net.set_weight_stashing(stash)
     xs, ys = synth.batches(wl, T, N)
     xs, ys = torch.from_numpy(xs).cuda(), torch.from_numpy(ys).cuda()
     losses = torch.zeros(T, dtype=torch.float32, device="cuda")
@@ -269,6 +283,7 @@ PIPE_CASES = [
     ("resnet20_bf16", lambda: synth.resnet20_workload(batch=8, bf16=True), 8, lambda t: [3, 2, 1, 0], 5, [2, 3]),
     ("alexnet", lambda: synth.alexnet_workload(batch=4), 4, lambda t: [2, 0], 5, [5]),
     ("vgg16_hybrid", lambda: synth.vgg16_workload(batch=8, n_pipelined=3), 8, None, 5, [5]),
+    ("resnet20_stash", lambda: synth.resnet20_workload(batch=8), 8, lambda t: [3, 2, 1, 0], 8, [3, 5]),
 ]
 
 
@@ -280,8 +295,9 @@ def test_pipeline_run_equals_stage_steps(P, name, factory, N, rows, T, chunks):
     statistics, every loss and the versions table."""
     wl = factory()
     st = wl.staleness(T) if rows is None else _table(rows, T, len(wl.stage_end))
-    a, la, va = _sequential(P, wl, N, st, wl.lr)
-    b, lb, vb = _pipelined(P, wl, N, st, wl.lr, chunks)
+    stash = name.endswith("_stash")
+    a, la, va = _sequential(P, wl, N, st, wl.lr, stash)
+    b, lb, vb = _pipelined(P, wl, N, st, wl.lr, chunks, stash)
     np.testing.assert_array_equal(va, vb)
     np.testing.assert_array_equal(la, lb)
     assert torch.equal(a.params(T), b.params(T))

@@ -189,6 +189,31 @@ def test_oracle_matches_register_simulator(oracle, S, variant):
     assert np.abs(plain["params"] - out["params"]).max() > 1e-6
 
 
+@pytest.mark.parametrize("S,variant", [(2, "paper"), (4, "paper"), (4, "same_cycle")])
+def test_oracle_stash_matches_register_simulator(oracle, S, variant):
+    """Weight stashing (the scheme Sec. 6.7 contrasts with): the oracle's
+    stash mode, which takes data gradients with the forward's version r_s,
+    against the register simulator whose forward passes run on private weight
+    copies kept until their backward pass."""
+    ops, ins, se = _sched_net(S)
+    K = S - 1
+    T = 9
+    d = [2 * (K - i + 1) for i in range(1, K + 2)] if variant == "paper" else [K - i + 1 for i in range(1, K + 2)]
+    wl = synth.Workload("s", ops, ins, 10, 3, [], se, lambda t: d, T, [0.02] * S, seed=11)
+    p0 = synth.init_params(wl)
+    xs, ys = synth.batches(wl, T)
+    lr = [0.02 + 0.01 * s for s in range(S)]
+    sim_p, sim_loss, sim_ver, _ = torch_ref.simulate_register_pipeline(ops, se, p0, xs, ys, lr, variant=variant,
+                                                                        stash=True)
+    out = oracle.train(ops, ins, se, p0, xs, ys, wl.staleness(T), lr, 0.9, stash=True)
+    np.testing.assert_array_equal(out["versions"], sim_ver)
+    np.testing.assert_allclose(out["losses"], sim_loss, rtol=1e-10)
+    np.testing.assert_allclose(out["params"], sim_p, rtol=1e-9, atol=1e-11)
+    # and it is not the paper's scheme
+    paper = oracle.train(ops, ins, se, p0, xs, ys, wl.staleness(T), lr, 0.9)
+    assert np.abs(paper["params"] - out["params"]).max() > 1e-6
+
+
 def test_versions_closed_form_and_hybrid(oracle):
     ops, ins, se = _sched_net(4)
     T, n_p = 8, 5

@@ -238,15 +238,17 @@ def simulate_register_pipeline(ops, stage_end, params0, xs, labels, lr, mom=0.9,
     return torch.cat([w.detach() for w in W]).double().numpy(), losses, versions, last_cycle
 
 
-def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=0.0, dtype=torch.float64):
+def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=0.0, dtype=torch.float64,
+                stash=False):
     """The stale-weight schedule written with autograd, for any staleness
     table (hybrid included): keep every stage's version history; for step t
     load version max(0, t - d_s) into the stage's weight tensor and run the
     forward pass; then overwrite that tensor IN PLACE with version t and run
     backward (autograd holds the tensor by reference, so data gradients see
     version t while weight gradients use the saved activations); append
-    version t+1 = SGD(version t).  Returns (final flat params, losses,
-    versions)."""
+    version t+1 = SGD(version t).  stash=True leaves the forward's version
+    in place for the backward pass (weight stashing).  Returns (final flat
+    params, losses, versions)."""
     slices, counts = op_param_slices(ops, stage_end)
     S = len(counts)
     hist = [[torch.tensor(p, dtype=dtype)] for p in split_flat(np.asarray(params0, np.float64), counts)]
@@ -268,9 +270,10 @@ def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=
         outs = run_ops(ops, 0, n, {0: torch.tensor(xs[t], dtype=dtype)}, Wp, slices)
         loss = F.cross_entropy(outs[n].reshape(outs[n].shape[0], -1), torch.tensor(labels[t], dtype=torch.long))
         losses[t] = float(loss.detach())
-        with torch.no_grad():
-            for s in range(S):
-                Wp[s].data.copy_(hist[s][t])
+        if not stash:
+            with torch.no_grad():
+                for s in range(S):
+                    Wp[s].data.copy_(hist[s][t])
         loss.backward()
         with torch.no_grad():
             for s in range(S):
