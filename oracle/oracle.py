@@ -296,7 +296,8 @@ def loss_and_grad(ops, in_shape, stage_end, params, x, labels, bn_eps=1e-5, bf16
 def train(ops, in_shape, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=0.0,
           nesterov=False, bn_eps=1e-5, bn_mom=0.1, bf16=False, stash=False):
     """Run T steps of the stale-weight schedule.  xs: [T, N, C, H, W] float32;
-    labels [T, N]; staleness [T, S].  stash=True: the backward pass takes its
+    labels [T, N]; staleness [T, S]; lr: scalar, [S] or [T, S] (per step and
+    stage).  stash=True: the backward pass takes its
     data gradients with the forward's weight version (weight stashing, the
     scheme Sec. 6.7 contrasts with) instead of the current one.  Returns a dict
     with params, momentum, run_mean, run_var, losses and versions."""
@@ -307,7 +308,8 @@ def train(ops, in_shape, stage_end, params0, xs, labels, staleness, lr, mom=0.9,
     labels = np.ascontiguousarray(labels, dtype=np.int32)
     T, N = xs.shape[0], xs.shape[1]
     stal = np.ascontiguousarray(staleness, dtype=np.int32).reshape(T, S)
-    lr = np.ascontiguousarray(np.broadcast_to(np.asarray(lr, dtype=np.float64), (S,)))
+    lr = np.asarray(lr, dtype=np.float64)
+    lr = np.ascontiguousarray(np.broadcast_to(lr if lr.ndim == 2 else np.broadcast_to(lr, (S,)), (T, S)))
     params0 = _f64(params0)
     out = np.zeros_like(params0)
     momb = np.zeros_like(params0)

@@ -858,8 +858,8 @@ int orc_loss_and_grad(int n_ops, const int32_t *desc, int N, int C0, int H0, int
 /* xs        : T mini-batches, float32, NCHW                                */
 /* labels    : T x N int32                                                  */
 /* staleness : T x S int32 (>= 0)                                           */
-/* lr        : S learning rates (one per stage, cf. the per-stage rate of    */
-/*             Table 7)                                                     */
+/* lr        : T x S learning rates (per step, for the schedules of App. A  */
+/*             and B, and per stage, cf. the per-stage rate of Table 7)     */
 /* outputs   : params_out (W_s^(T)), mom_out (momentum buffers),             */
 /*             run_mean/run_var (BN running stats, concatenated over BN     */
 /*             ops; may be NULL), losses (T), versions (T x S: r_s)          */
@@ -926,7 +926,7 @@ int orc_train(int n_ops, const int32_t *desc, int N, int C0, int H0, int W0, int
         for (int s = 0; s < S; ++s) {
             const int64_t np = net.stage_np[s];
             hist[s][t + 1] = (double *)malloc(sizeof(double) * (size_t)(np > 0 ? np : 1));
-            orc_sgd(np, hist[s][t], hist[s][t + 1], vel[s], grad[s], lr[s], mom, wd, nesterov);
+            orc_sgd(np, hist[s][t], hist[s][t + 1], vel[s], grad[s], lr[(int64_t)t * S + s], mom, wd, nesterov);
         }
     }
     off = 0;

@@ -50,10 +50,19 @@ class Workload:
     bf16: bool = False
     seed: int = 0
     input_dist: str = "normal"      # "normal" N(0,1) or "uniform" U[0,1)
+    lr_fn: Callable[[int], List[float]] | None = None  # per-step, per-stage rates (default: lr every step)
 
     @property
     def n_stages(self) -> int:
         return len(self.stage_end)
+
+    def lr_at(self, t: int) -> List[float]:
+        return list(self.lr_fn(t)) if self.lr_fn is not None else list(self.lr)
+
+    def lr_table(self, steps: int | None = None, t0: int = 0) -> np.ndarray:
+        """[T, S] learning rates of steps t0 .. t0+T-1."""
+        T = self.steps if steps is None else steps
+        return np.array([self.lr_at(t0 + t) for t in range(T)], dtype=np.float64).reshape(T, self.n_stages)
 
     def staleness(self, steps: int | None = None) -> np.ndarray:
         T = self.steps if steps is None else steps
@@ -175,6 +184,35 @@ def resnet_cifar(depth: int):
     return b.desc(), b.layer_end, (3, 32, 32)
 
 
+# ------------------------------------------------- learning-rate policies ---
+# The schedules of App. A and B, as functions of the step t (one mini-batch).
+def lr_step(base: float, milestones: Sequence[int], gamma: float = 0.1) -> Callable[[int], float]:
+    """base, multiplied by gamma at every milestone step reached ("decreased by
+    10x twice": ResNet and AlexNet)."""
+    ms = sorted(int(m) for m in milestones)
+    return lambda t: base * gamma ** sum(1 for m in ms if t >= m)
+
+
+def lr_halving(base: float, period: int) -> Callable[[int], float]:
+    """base, halved every `period` steps (VGG-16: every 50 epochs)."""
+    return lambda t: base * 0.5 ** (t // period)
+
+
+def lr_inverse(base: float, gamma: float = 1e-4, power: float = 0.75) -> Callable[[int], float]:
+    """The inverse policy named for LeNet-5: base * (1 + gamma t)^(-power)."""
+    return lambda t: base * (1.0 + gamma * t) ** (-power)
+
+
+# Two-partition pipelines of the actual pipelined training (Table 5): the
+# register pair after layer p, and the learning rate of BKS_2, the backward
+# stage of the first partition (Table 7); the other hyperparameters are those
+# of the non-pipelined baseline (App. B: 0.1, x0.1 at epochs 100 and 150,
+# momentum 0.9, weight decay 1e-4, batch 128).
+TABLE5_PPV = {20: 7, 56: 19, 110: 37, 224: 75, 362: 121}
+TABLE7_BKS2_LR = {20: 0.1, 56: 0.01, 110: 0.001, 224: 0.001, 362: 0.001}
+CIFAR_STEPS_PER_EPOCH = 391  # 50,000 images in batches of 128, the last one partial
+
+
 # ------------------------------------------------------------- workloads ----
 def _const(d):
     return lambda t: list(d)
@@ -216,6 +254,29 @@ def resnet110_workload(batch=256, steps=50, seed=1916, bf16=True):
     se = _stage_end_from_ppv(le, ppv, len(ops))
     return Workload("resnet110" + ("_bf16" if bf16 else ""), ops, ins, 10, batch, le, se,
                     _const([7 - s for s in range(8)]), steps, [0.01] * 8, seed=seed, bf16=bf16)
+
+
+def resnet_two_partition_workload(depth=20, batch=128, steps=50, n_pipelined=None,
+                                  steps_per_epoch=CIFAR_STEPS_PER_EPOCH, seed=1917):
+    """ResNet-depth split by one register pair at its Table 5 PPV (two
+    partitions, the paper's 4-stage pipeline on 2 devices).  Staleness under
+    the cycle schedule with K = 1: d = 2(K - i + 1) = [2, 0].  Hybrid (Sec. 4)
+    when n_pipelined is given: d = [0, 0] from that step on (100 of 200 epochs
+    in Table 5).  Rates: the baseline's step policy, with the first partition's
+    backward stage (BKS_2) starting at its Table 7 rate and decayed alike."""
+    ops, le, ins = resnet_cifar(depth)
+    se = _stage_end_from_ppv(le, (TABLE5_PPV[depth],), len(ops))
+
+    def stal(t):
+        return [2, 0] if n_pipelined is None or t < n_pipelined else [0, 0]
+
+    decay = lr_step(1.0, (100 * steps_per_epoch, 150 * steps_per_epoch))
+
+    def lr_fn(t):
+        return [TABLE7_BKS2_LR[depth] * decay(t), 0.1 * decay(t)]
+
+    return Workload(f"resnet{depth}_2part", ops, ins, 10, batch, le, se, stal, steps,
+                    [TABLE7_BKS2_LR[depth], 0.1], weight_decay=1e-4, seed=seed, lr_fn=lr_fn)
 
 
 WORKLOADS = {

@@ -43,7 +43,7 @@ def gpu_train(P, wl, T, batch=None, net=None, t0=0, stash=False):
     losses, versions = [], []
     for t in range(t0, T):
         x, y = synth.batch(wl, t, N)
-        ver = net.step(t, st[t], wl.lr, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), wl.momentum,
+        ver = net.step(t, st[t], wl.lr_at(t), torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), wl.momentum,
                        wl.weight_decay, wl.nesterov)
         losses.append(float(net.loss.item()))
         versions.append(ver)
@@ -54,7 +54,7 @@ def gpu_train(P, wl, T, batch=None, net=None, t0=0, stash=False):
 def oracle_train(oracle, wl, T, batch=None, stash=False):
     N = wl.batch if batch is None else batch
     xs, ys = synth.batches(wl, T, N)
-    return oracle.train(wl.ops, wl.in_shape, wl.stage_end, synth.init_params(wl), xs, ys, wl.staleness(T), wl.lr,
+    return oracle.train(wl.ops, wl.in_shape, wl.stage_end, synth.init_params(wl), xs, ys, wl.staleness(T), wl.lr_table(T),
                         wl.momentum, wl.weight_decay, wl.nesterov, bf16=wl.bf16, stash=stash)
 
 
@@ -89,12 +89,12 @@ def reference_spread(oracle, wl, T, batch, xs, ys, stash=False):
     out = []
     if not wl.bf16:
         for inp in (xs, up, down):
-            p, l, _ = torch_ref.train_stale(wl.ops, wl.stage_end, p0, inp, ys, wl.staleness(T), wl.lr, wl.momentum,
+            p, l, _ = torch_ref.train_stale(wl.ops, wl.stage_end, p0, inp, ys, wl.staleness(T), wl.lr_table(T), wl.momentum,
                                             wl.weight_decay, dtype=torch.float32, stash=stash)
             out.append((p, l))
         return out
     for inp in (up, down):
-        o = oracle.train(wl.ops, wl.in_shape, wl.stage_end, p0, inp, ys, wl.staleness(T), wl.lr, wl.momentum,
+        o = oracle.train(wl.ops, wl.in_shape, wl.stage_end, p0, inp, ys, wl.staleness(T), wl.lr_table(T), wl.momentum,
                          wl.weight_decay, wl.nesterov, bf16=True, stash=stash)
         out.append((o["params"], o["losses"]))
     return out
@@ -108,6 +108,11 @@ CASES = [
     ("alexnet_b4", lambda: synth.alexnet_workload(batch=4), 4, 4),
     ("vgg16_hybrid_b16", lambda: synth.vgg16_workload(batch=16, n_pipelined=3), 16, 5),
     ("resnet110_bf16_b8", lambda: synth.resnet110_workload(batch=8), 8, 3),
+    # Table 5's two-partition ResNet-56 (PPV (19), d = [2, 0], BKS_2 rate of
+    # Table 7, weight decay 1e-4) with its step policy compressed so that both
+    # decays fall inside the run, then the hybrid switch
+    ("resnet56_2part_b8", lambda: synth.resnet_two_partition_workload(56, batch=8, n_pipelined=4,
+                                                                       steps_per_epoch=0.02), 8, 6),
 ]
 
 

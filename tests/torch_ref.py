@@ -254,7 +254,8 @@ def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=
     hist = [[torch.tensor(p, dtype=dtype)] for p in split_flat(np.asarray(params0, np.float64), counts)]
     Wp = [torch.zeros(c, dtype=dtype, requires_grad=True) for c in counts]
     V = [torch.zeros(c, dtype=dtype) for c in counts]
-    lrs = np.broadcast_to(np.asarray(lr, dtype=np.float64), (S,))
+    lr_arr = np.asarray(lr, dtype=np.float64)
+    lrs_t = np.broadcast_to(lr_arr if lr_arr.ndim == 2 else np.broadcast_to(lr_arr, (S,)), (len(xs), S))
     T = len(xs)
     st = np.asarray(staleness).reshape(T, S)
     n = len(ops)
@@ -279,5 +280,5 @@ def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=
             for s in range(S):
                 g = Wp[s].grad if Wp[s].grad is not None else torch.zeros_like(V[s])
                 V[s].mul_(mom).add_(g + wd * hist[s][t])
-                hist[s].append(hist[s][t] - float(lrs[s]) * V[s])
+                hist[s].append(hist[s][t] - float(lrs_t[t, s]) * V[s])
     return torch.cat([h[-1] for h in hist]).double().numpy(), losses, versions
