@@ -174,6 +174,19 @@ int psw_softmax_xent(int n, int classes, const float *logits, const int32_t *lab
 int psw_sgd_momentum_step(int64_t count, const float *w_in, float *w_out, float *v, const float *g,
                           float lr, float mom, float wd, int nesterov, void *stream);
 
+/* Dropout (App. A: VGG-16 trains with dropout), inverted:
+ *   out[j] (+)= keep(j) ? in[j] * 2^24 / (2^24 - p24) : 0
+ * over count floats (accumulate != 0 adds to out).  The mask is a function of
+ * (seed, op, t, j) only: element j is kept iff the top 24 bits of word j % 4
+ * of Philox4x32-10 (Salmon et al., SC 2011) with counter (j / 4, op,
+ * t mod 2^32, t / 2^32) and key (seed mod 2^32, seed / 2^32) are >= p24, so
+ * drop probability = p24 / 2^24 (0 < p24 < 2^24) and the backward pass of a
+ * mini-batch is the same call on the gradients with the same (seed, op, t).
+ * count / 4 must fit in 32 bits; t >= 0.  in and out may be the same array
+ * when accumulate == 0. */
+int psw_dropout(int64_t count, const float *in, float *out, int accumulate, int p24, uint64_t seed,
+                int32_t op, int64_t t, void *stream);
+
 /* ------------------------------------------------------------------------ */
 /* Networks and the stale-weight stage scheduler (Sec. 3, Sec. 4).          */
 /* ------------------------------------------------------------------------ */
@@ -181,14 +194,16 @@ int psw_sgd_momentum_step(int64_t count, const float *w_in, float *w_out, float 
 /* One operation of a network; tensor 0 is the mini-batch, operation i
  * writes tensor i+1.  kind: PSW_OP_*.  in0: input tensor id; in1: residual
  * tensor id of a batch norm (-1 none).  cin/cout: channels (features for
- * FC); k, stride, pad: conv / max-pool geometry.  flags: PSW_F_BIAS,
- * PSW_F_RELU.  Parameters of a stage are packed, in operation order, as
+ * FC); k, stride, pad: conv / max-pool geometry; for PSW_OP_DROPOUT k is the
+ * drop threshold p24 of psw_dropout, and the mask of step t is that of
+ * psw_dropout with op = the operation's index and the net's dropout seed
+ * (psw_net_set_dropout_seed).  flags: PSW_F_BIAS, PSW_F_RELU.  Parameters of a stage are packed, in operation order, as
  * conv (weight, bias), bn (gamma, beta), fc (weight, bias). */
 typedef struct {
     int32_t kind, in0, in1, cin, cout, k, stride, pad, flags;
 } psw_layer;
 
-enum { PSW_OP_CONV = 1, PSW_OP_BN = 2, PSW_OP_MAXPOOL = 3, PSW_OP_GAVG = 4, PSW_OP_FC = 5 };
+enum { PSW_OP_CONV = 1, PSW_OP_BN = 2, PSW_OP_MAXPOOL = 3, PSW_OP_GAVG = 4, PSW_OP_FC = 5, PSW_OP_DROPOUT = 6 };
 enum { PSW_F_BIAS = 1, PSW_F_RELU = 2 };
 
 typedef struct psw_net psw_net;
@@ -320,6 +335,10 @@ int psw_net_param_offset(const psw_net *net, int op, int *stage, int64_t *offset
  * net. */
 int psw_net_set_weight_stashing(psw_net *net, int on);
 
+/* Key of the net's dropout masks (default 0); takes effect from the next
+ * step.  PSW_ERR_NULL for a NULL net. */
+int psw_net_set_dropout_seed(psw_net *net, uint64_t seed);
+
 /* Dry run of psw_stage_step (host only, no device work): the kernel-level
  * plan of step t.  Each record is (op, what, stage, version) where `what`
  * is a PSW_PLAN_* code, `version` the weight version it reads (-1 if
@@ -333,7 +352,7 @@ typedef struct {
 enum {
     PSW_PLAN_CONV_FWD = 1, PSW_PLAN_BN_FWD, PSW_PLAN_POOL_FWD, PSW_PLAN_FC_FWD, PSW_PLAN_LOSS,
     PSW_PLAN_RELU_MASK, PSW_PLAN_CONV_BWD_WEIGHT, PSW_PLAN_CONV_BWD_DATA, PSW_PLAN_BN_BWD,
-    PSW_PLAN_POOL_BWD, PSW_PLAN_FC_BWD, PSW_PLAN_SGD
+    PSW_PLAN_POOL_BWD, PSW_PLAN_FC_BWD, PSW_PLAN_SGD, PSW_PLAN_DROPOUT_FWD, PSW_PLAN_DROPOUT_BWD
 };
 
 int psw_net_plan(const psw_net *net, int64_t t, const int32_t *staleness, psw_launch *out, int cap,

@@ -51,6 +51,7 @@ _f = ctypes.POINTER(ctypes.c_float)
 _i32 = ctypes.POINTER(ctypes.c_int32)
 _i64 = ctypes.POINTER(ctypes.c_int64)
 _I = ctypes.c_int
+_i64v = ctypes.c_int64
 _D = ctypes.c_double
 
 
@@ -76,10 +77,17 @@ def _declare(L):
     L.orc_shapes.argtypes = [_I, _i32, _I, _I, _I, _I, _I, _i32, _i32]
     L.orc_shapes.restype = _I
     L.orc_loss_and_grad.argtypes = [_I, _i32, _I, _I, _I, _I, _I, _i32, _d, _f, _i32, _D, _I,
-                                    _d, _d, _d]
+                                    _d, _d, _d, ctypes.c_uint64, _i64v]
     L.orc_loss_and_grad.restype = _I
     L.orc_train.argtypes = [_I, _i32, _I, _I, _I, _I, _I, _i32, _d, _I, _f, _i32, _i32, _d,
-                            _D, _D, _I, _D, _D, _I, _I, _d, _d, _d, _d, _d, _i32]
+                            _D, _D, _I, _D, _D, _I, _I, _d, _d, _d, _d, _d, _i32, ctypes.c_uint64]
+    _u32 = ctypes.POINTER(ctypes.c_uint32)
+    L.orc_philox4x32_10.argtypes = [_u32, _u32, _u32]
+    L.orc_philox4x32_10.restype = None
+    L.orc_dropout_fwd.argtypes = [_i64v, _d, _d, _I, ctypes.c_uint64, _I, _i64v]
+    L.orc_dropout_fwd.restype = None
+    L.orc_dropout_bwd.argtypes = [_i64v, _d, _d, _I, ctypes.c_uint64, _I, _i64v]
+    L.orc_dropout_bwd.restype = None
     L.orc_train.restype = _I
 
 
@@ -269,8 +277,32 @@ def shapes(ops, in_shape, batch, stage_end):
     return out
 
 
+def philox4x32_10(counter, key):
+    """Philox4x32-10 of a 4-word counter under a 2-word key (uint32 words)."""
+    c = np.ascontiguousarray(counter, dtype=np.uint32)
+    k = np.ascontiguousarray(key, dtype=np.uint32)
+    out = np.zeros(4, dtype=np.uint32)
+    u32 = ctypes.POINTER(ctypes.c_uint32)
+    lib().orc_philox4x32_10(c.ctypes.data_as(u32), k.ctypes.data_as(u32), out.ctypes.data_as(u32))
+    return out
+
+
+def dropout_fwd(x, p24, seed, op, step):
+    x = _f64(x)
+    y = np.zeros_like(x)
+    lib().orc_dropout_fwd(x.size, _p(x, _d), _p(y, _d), int(p24), int(seed), int(op), int(step))
+    return y
+
+
+def dropout_bwd(dy, p24, seed, op, step):
+    dy = _f64(dy)
+    dx = np.zeros_like(dy)
+    lib().orc_dropout_bwd(dy.size, _p(dy, _d), _p(dx, _d), int(p24), int(seed), int(op), int(step))
+    return dx
+
+
 def loss_and_grad(ops, in_shape, stage_end, params, x, labels, bn_eps=1e-5, bf16=False,
-                  want_acts=False):
+                  want_acts=False, dropout_seed=0, step=0):
     ops = _desc(ops)
     se = np.ascontiguousarray(stage_end, dtype=np.int32)
     params = _f64(params)
@@ -285,7 +317,7 @@ def loss_and_grad(ops, in_shape, stage_end, params, x, labels, bn_eps=1e-5, bf16
     loss = ctypes.c_double(0.0)
     rc = lib().orc_loss_and_grad(len(ops), _p(ops, _i32), N, *in_shape, len(se), _p(se, _i32),
                                  _p(params, _d), _p(x, _f), _p(labels, _i32), bn_eps, int(bf16),
-                                 ctypes.byref(loss), _p(grads, _d), _p(acts, _d))
+                                 ctypes.byref(loss), _p(grads, _d), _p(acts, _d), int(dropout_seed), int(step))
     if rc != 0:
         raise ValueError(f"oracle rejected the network description (code {rc})")
     if want_acts:
@@ -294,7 +326,7 @@ def loss_and_grad(ops, in_shape, stage_end, params, x, labels, bn_eps=1e-5, bf16
 
 
 def train(ops, in_shape, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=0.0,
-          nesterov=False, bn_eps=1e-5, bn_mom=0.1, bf16=False, stash=False):
+          nesterov=False, bn_eps=1e-5, bn_mom=0.1, bf16=False, stash=False, dropout_seed=0):
     """Run T steps of the stale-weight schedule.  xs: [T, N, C, H, W] float32;
     labels [T, N]; staleness [T, S]; lr: scalar, [S] or [T, S] (per step and
     stage).  stash=True: the backward pass takes its
@@ -320,7 +352,7 @@ def train(ops, in_shape, stage_end, params0, xs, labels, staleness, lr, mom=0.9,
     rc = lib().orc_train(len(ops), _p(ops, _i32), N, *in_shape, S, _p(se, _i32), _p(params0, _d), T,
                          _p(xs, _f), _p(labels, _i32), _p(stal, _i32), _p(lr, _d), mom, wd,
                          int(nesterov), bn_eps, bn_mom, int(bf16), int(stash), _p(out, _d), _p(momb, _d),
-                         _p(rm, _d), _p(rv, _d), _p(losses, _d), _p(versions, _i32))
+                         _p(rm, _d), _p(rv, _d), _p(losses, _d), _p(versions, _i32), int(dropout_seed))
     if rc != 0:
         raise ValueError(f"oracle rejected the run (code {rc})")
     return dict(params=out, momentum=momb, run_mean=rm[:n_bn], run_var=rv[:n_bn], losses=losses,

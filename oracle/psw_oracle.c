@@ -22,6 +22,9 @@
  *   - per-layer forward and backward of conv / BN(+residual)+ReLU / max-pool /
  *     global average pool / fully connected / softmax cross-entropy, and the
  *     SGD-momentum update  [Sec. 2, backpropagation; App. A/B hyperparameters]
+ *   - dropout (App. A: VGG-16 trains with dropout), its masks drawn from a
+ *     counter-based generator (Philox4x32-10) so that the backward pass of a
+ *     mini-batch recomputes the mask its forward pass used
  *   - the stale-weight schedule  [Sec. 3, pipelined backpropagation]:
  *     every stage s keeps its FULL weight history W_s^(0), W_s^(1), ...;
  *     the forward pass of mini-batch t reads W_s^(max(0, t - d_s)), the
@@ -44,6 +47,72 @@
 #ifdef _OPENMP
 #include <omp.h>
 #endif
+
+/* ------------------------------------------------------------------------ */
+/* Philox4x32-10 (Salmon, Moraes, Dror and Shaw, "Parallel random numbers:   */
+/* as easy as 1, 2, 3", SC 2011): a 4 x 32-bit counter is transformed by ten */
+/* rounds under a 2 x 32-bit key.  A round multiplies counter words 0 and 2  */
+/* by the two round constants (full 64-bit products), and forms the new     */
+/* counter from the high halves xor-ed with the other two words and the key, */
+/* and the low halves; the key grows by the two Weyl constants between      */
+/* rounds.                                                                  */
+/* ------------------------------------------------------------------------ */
+void orc_philox4x32_10(const uint32_t ctr[4], const uint32_t key[2], uint32_t out[4])
+{
+    uint32_t c0 = ctr[0], c1 = ctr[1], c2 = ctr[2], c3 = ctr[3];
+    uint32_t k0 = key[0], k1 = key[1];
+    for (int round = 0; round < 10; ++round) {
+        if (round > 0) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        const uint64_t a = (uint64_t)0xD2511F53u * c0;
+        const uint64_t b = (uint64_t)0xCD9E8D57u * c2;
+        const uint32_t n0 = (uint32_t)(b >> 32) ^ c1 ^ k0;
+        const uint32_t n1 = (uint32_t)b;
+        const uint32_t n2 = (uint32_t)(a >> 32) ^ c3 ^ k1;
+        const uint32_t n3 = (uint32_t)a;
+        c0 = n0;
+        c1 = n1;
+        c2 = n2;
+        c3 = n3;
+    }
+    out[0] = c0;
+    out[1] = c1;
+    out[2] = c2;
+    out[3] = c3;
+}
+
+/* Dropout mask of the tensor written by operation `op` in mini-batch t: an
+ * element with flat NCHW index j is kept iff the top 24 bits of word j % 4 of
+ * Philox4x32-10(counter (j / 4, op, t mod 2^32, t / 2^32), key (seed mod
+ * 2^32, seed / 2^32)) are >= p24, i.e. it is dropped with probability
+ * p24 / 2^24.  Kept elements are scaled by 2^24 / (2^24 - p24) (inverted
+ * dropout: the expectation of the output is the input). */
+static int dropout_keep(int64_t j, int op, int64_t t, uint64_t seed, int p24)
+{
+    const uint32_t ctr[4] = {(uint32_t)(j / 4), (uint32_t)op, (uint32_t)t, (uint32_t)((uint64_t)t >> 32)};
+    const uint32_t key[2] = {(uint32_t)seed, (uint32_t)(seed >> 32)};
+    uint32_t r[4];
+    orc_philox4x32_10(ctr, key, r);
+    return (int)(r[j % 4] >> 8) >= p24;
+}
+
+void orc_dropout_fwd(int64_t n, const double *x, double *y, int p24, uint64_t seed, int op, int64_t t)
+{
+    const double scale = 16777216.0 / (16777216.0 - p24);
+#pragma omp parallel for schedule(static)
+    for (int64_t j = 0; j < n; ++j) y[j] = dropout_keep(j, op, t, seed, p24) ? x[j] * scale : 0.0;
+}
+
+/* dx += mask * scale * dy (accumulates, as every data gradient here) */
+void orc_dropout_bwd(int64_t n, const double *dy, double *dx, int p24, uint64_t seed, int op, int64_t t)
+{
+    const double scale = 16777216.0 / (16777216.0 - p24);
+#pragma omp parallel for schedule(static)
+    for (int64_t j = 0; j < n; ++j)
+        if (dropout_keep(j, op, t, seed, p24)) dx[j] += dy[j] * scale;
+}
 
 /* ------------------------------------------------------------------------ */
 /* bf16 operand rounding (emulation of the GPU's bf16-in / fp32-acc mode).   */
@@ -481,14 +550,15 @@ void orc_sgd(int64_t n, const double *w_in, double *w_out, double *v, const doub
 /* mini-batch input and operation i writes tensor i+1.  Each operation is   */
 /* nine int32 values:                                                       */
 /*   kind, in0, in1, cin, cout, k, stride, pad, flags                       */
-/* kind: 1 conv, 2 batch-norm, 3 max-pool, 4 global avg-pool, 5 fc          */
+/* kind: 1 conv, 2 batch-norm, 3 max-pool, 4 global avg-pool, 5 fc,        */
+/*       6 dropout (k: drop probability in units of 2^-24)                  */
 /* in1 : residual tensor of a batch-norm (-1: none)                         */
 /* flags: bit0 bias (conv, fc), bit1 ReLU (conv, bn, fc)                    */
 /* A stage split is given as stage_end[s] = one past the last operation of  */
 /* stage s; the parameters of a stage are the concatenation, in operation   */
 /* order, of conv (weight, bias), bn (gamma, beta), fc (weight, bias).      */
 /* ======================================================================== */
-enum { OP_CONV = 1, OP_BN = 2, OP_MAXPOOL = 3, OP_GAVG = 4, OP_FC = 5 };
+enum { OP_CONV = 1, OP_BN = 2, OP_MAXPOOL = 3, OP_GAVG = 4, OP_FC = 5, OP_DROPOUT = 6 };
 enum { F_BIAS = 1, F_RELU = 2 };
 
 typedef struct {
@@ -527,6 +597,8 @@ static void net_free(orc_net *net)
     free(net->bn_index);
     free(net->bn_off);
 }
+
+static int64_t shape_numel_(orc_shape s) { return (int64_t)s.n * s.c * s.h * s.w; }
 
 /* returns 0 on success, a negative number naming the first bad op otherwise */
 static int net_build(orc_net *net, int n_ops, const int32_t *desc, int N, int C0, int H0, int W0,
@@ -593,6 +665,10 @@ static int net_build(orc_net *net, int n_ops, const int32_t *desc, int N, int C0
             out.h = out.w = 1;
             np = (int64_t)o.cout * o.cin + ((o.flags & F_BIAS) ? o.cout : 0);
             break;
+        case OP_DROPOUT: /* k = drop probability in units of 2^-24 */
+            if (a.c != o.cin || o.cout != o.cin || o.k <= 0 || o.k >= (1 << 24)) return -(i + 1);
+            if (shape_numel_(a) / 4 > (int64_t)UINT32_MAX) return -(i + 1);
+            break;
         default:
             return -(i + 1);
         }
@@ -650,7 +726,7 @@ typedef struct {
  * (gradient of the loss w.r.t. the last tensor) into *dlogits_out. */
 static double forward(const orc_net *net, double *const *wfor, const float *x, const int32_t *labels,
                       orc_fwd_state *st, double *run_mean, double *run_var, double bn_eps,
-                      double bn_mom, int bf16, double *dlogits)
+                      double bn_mom, int bf16, double *dlogits, uint64_t seed, int64_t t)
 {
     const int n_ops = net->n_ops;
     const int64_t n0 = shape_numel(net->shape[0]);
@@ -696,6 +772,9 @@ static double forward(const orc_net *net, double *const *wfor, const float *x, c
                        (o.flags & F_BIAS) ? p + (int64_t)o.cout * o.cin : NULL, y, bf16);
             if (o.flags & F_RELU) orc_relu_inplace(shape_numel(out), y);
             break;
+        case OP_DROPOUT:
+            orc_dropout_fwd(shape_numel(out), st->act[o.in0], y, o.k, seed, i, t);
+            break;
         }
     }
     const orc_shape last = net->shape[n_ops];
@@ -706,7 +785,7 @@ static double forward(const orc_net *net, double *const *wfor, const float *x, c
  * (the schedule passes the current version W_s^(t)); weight gradients use
  * the saved forward activations.  grads[s] receives stage s's gradient. */
 static void backward(const orc_net *net, double *const *wcur, const orc_fwd_state *st,
-                     const double *dlogits, double *const *grads, int bf16)
+                     const double *dlogits, double *const *grads, int bf16, uint64_t seed, int64_t t)
 {
     const int n_ops = net->n_ops;
     double **d = (double **)calloc((size_t)n_ops + 1, sizeof(double *));
@@ -765,6 +844,9 @@ static void backward(const orc_net *net, double *const *wcur, const orc_fwd_stat
                        (o.flags & F_BIAS) ? g + nw : NULL, bf16);
             break;
         }
+        case OP_DROPOUT: /* the mask of this mini-batch's forward pass, recomputed */
+            if (din) orc_dropout_bwd(shape_numel(out), dout, din, o.k, seed, i, t);
+            break;
         }
     }
     for (int t = 1; t <= n_ops; ++t) free(d[t]);
@@ -800,7 +882,7 @@ static void state_free(orc_fwd_state *st, int n_ops)
 int orc_loss_and_grad(int n_ops, const int32_t *desc, int N, int C0, int H0, int W0, int n_stages,
                       const int32_t *stage_end, const double *params, const float *x,
                       const int32_t *labels, double bn_eps, int bf16, double *loss, double *grads_out,
-                      double *acts_out)
+                      double *acts_out, uint64_t dropout_seed, int64_t step)
 {
     orc_net net;
     int rc = net_build(&net, n_ops, desc, N, C0, H0, W0, n_stages, stage_end);
@@ -820,8 +902,8 @@ int orc_loss_and_grad(int n_ops, const int32_t *desc, int N, int C0, int H0, int
     state_alloc(&st, n_ops);
     const orc_shape last = net.shape[n_ops];
     double *dlog = (double *)malloc(sizeof(double) * (size_t)shape_numel(last));
-    *loss = forward(&net, wv, x, labels, &st, NULL, NULL, bn_eps, 0.1, bf16, dlog);
-    backward(&net, wv, &st, dlog, gv, bf16);
+    *loss = forward(&net, wv, x, labels, &st, NULL, NULL, bn_eps, 0.1, bf16, dlog, dropout_seed, step);
+    backward(&net, wv, &st, dlog, gv, bf16, dropout_seed, step);
     if (acts_out) {
         int64_t o2 = 0;
         for (int t = 0; t <= n_ops; ++t) {
@@ -869,7 +951,8 @@ int orc_train(int n_ops, const int32_t *desc, int N, int C0, int H0, int W0, int
               const int32_t *stage_end, const double *params0, int T, const float *xs,
               const int32_t *labels, const int32_t *staleness, const double *lr, double mom,
               double wd, int nesterov, double bn_eps, double bn_mom, int bf16, int stash, double *params_out,
-              double *mom_out, double *run_mean, double *run_var, double *losses, int32_t *versions)
+              double *mom_out, double *run_mean, double *run_var, double *losses, int32_t *versions,
+              uint64_t dropout_seed)
 {
     orc_net net;
     int rc = net_build(&net, n_ops, desc, N, C0, H0, W0, n_stages, stage_end);
@@ -920,8 +1003,8 @@ int orc_train(int n_ops, const int32_t *desc, int N, int C0, int H0, int W0, int
         orc_fwd_state st;
         state_alloc(&st, n_ops);
         losses[t] = forward(&net, wfor, xs + (int64_t)t * in_numel, labels + (int64_t)t * N, &st,
-                            run_mean, run_var, bn_eps, bn_mom, bf16, dlog);
-        backward(&net, wcur, &st, dlog, grad, bf16);
+                            run_mean, run_var, bn_eps, bn_mom, bf16, dlog, dropout_seed, t);
+        backward(&net, wcur, &st, dlog, grad, bf16, dropout_seed, t);
         state_free(&st, n_ops);
         for (int s = 0; s < S; ++s) {
             const int64_t np = net.stage_np[s];

@@ -243,6 +243,17 @@ int psw_softmax_xent(int n, int classes, const float* logits, const int32_t* lab
     return hip_check(psw::softmax_xent(n, classes, logits, labels, loss, dlogits, S(stream)), "softmax_xent");
 }
 
+int psw_dropout(int64_t count, const float* in, float* out, int accumulate, int p24, uint64_t seed, int32_t op,
+                int64_t t, void* stream)
+{
+    if (count < 0 || t < 0) return fail(PSW_ERR_SHAPE, "dropout: count and t must be >= 0");
+    if ((count + 3) / 4 > (int64_t)UINT32_MAX + 1) return fail(PSW_ERR_SHAPE, "dropout: count / 4 exceeds 32 bits");
+    if (p24 <= 0 || p24 >= (1 << 24)) return fail(PSW_ERR_SHAPE, "dropout: p24 must be in (0, 2^24)");
+    if (count > 0 && (!in || !out)) return fail(PSW_ERR_NULL, "dropout: in and out are required");
+    return hip_check(psw::dropout_apply(count, in, out, accumulate, p24, seed, (uint32_t)op, t, S(stream)),
+                     "dropout");
+}
+
 int psw_sgd_momentum_step(int64_t count, const float* w_in, float* w_out, float* v, const float* g, float lr,
                           float mom, float wd, int nesterov, void* stream)
 {
@@ -329,6 +340,7 @@ struct psw_net {
     // 1: the backward pass takes its data gradients with the forward's
     // version r_s (weight stashing, the comparison scheme), 0: with version t
     int stash = 0;
+    uint64_t dropout_seed = 0;  // key of the dropout masks
     // optional per-kernel timing with HIP events (psw_net_profile): while
     // psw_stage_step runs with profiling on, rec is this thread's kernel
     // recorder and every library kernel launch adds one KRec
@@ -474,6 +486,12 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
             break;
         case PSW_OP_GAVG:
             out.h = out.w = 1;
+            break;
+        case PSW_OP_DROPOUT:
+            if (a.c != o.cin || o.cout != o.cin) return fail(PSW_ERR_SHAPE, "op %d: dropout channels", i);
+            if (o.k <= 0 || o.k >= (1 << 24)) return fail(PSW_ERR_SHAPE, "op %d: dropout threshold outside (0, 2^24)", i);
+            if (((int64_t)a.numel() + 3) / 4 > (int64_t)UINT32_MAX + 1)
+                return fail(PSW_ERR_SHAPE, "op %d: dropout tensor too large", i);
             break;
         case PSW_OP_FC:
             if ((int64_t)a.c * a.h * a.w != o.cin || o.cout <= 0)
@@ -763,6 +781,14 @@ int psw_net_set_weight_stashing(psw_net* net, int on)
     return PSW_OK;
 }
 
+int psw_net_set_dropout_seed(psw_net* net, uint64_t seed)
+{
+    if (!net) return fail(PSW_ERR_NULL, "net_set_dropout_seed: net is NULL");
+    net->dropout_seed = seed;
+    g_err.clear();
+    return PSW_OK;
+}
+
 int psw_net_plan(const psw_net* net, int64_t t, const int32_t* staleness, psw_launch* out, int cap, int* n_out)
 {
     if (!net || !n_out) return fail(PSW_ERR_NULL, "net_plan: required pointer is NULL");
@@ -784,6 +810,7 @@ int psw_net_plan(const psw_net* net, int64_t t, const int32_t* staleness, psw_la
         case PSW_OP_MAXPOOL:
         case PSW_OP_GAVG: rec(i, PSW_PLAN_POOL_FWD, s, -1); break;
         case PSW_OP_FC: rec(i, PSW_PLAN_FC_FWD, s, r); break;
+        case PSW_OP_DROPOUT: rec(i, PSW_PLAN_DROPOUT_FWD, s, -1); break;
         }
     }
     rec(L - 1, PSW_PLAN_LOSS, net->stage_of[L - 1], -1);
@@ -804,6 +831,9 @@ int psw_net_plan(const psw_net* net, int64_t t, const int32_t* staleness, psw_la
         case PSW_OP_FC:
             if (o.flags & PSW_F_RELU) rec(i, PSW_PLAN_RELU_MASK, s, -1);
             rec(i, PSW_PLAN_FC_BWD, s, vb);
+            break;
+        case PSW_OP_DROPOUT:
+            if (o.in0 > 0) rec(i, PSW_PLAN_DROPOUT_BWD, s, -1);
             break;
         }
         // when the data-gradient chain is done with a stage: the stage's
@@ -945,6 +975,12 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
             kind = PSW_PROF_POOL;
             PSW_TRY(psw::gavgpool_fwd(a.n, a.c, a.h, a.w, is.act(o.in0), is.act(i + 1), sf), "gavgpool_fwd");
             break;
+        case PSW_OP_DROPOUT:
+            kind = PSW_PROF_OTHER;
+            PSW_TRY(psw::dropout_apply(a.numel(), is.act(o.in0), is.act(i + 1), 0, o.k, net->dropout_seed, (uint32_t)i,
+                                       is.io.t, sf),
+                    "dropout");
+            break;
         case PSW_OP_FC: {
             const float* b = (o.flags & PSW_F_BIAS) ? W + (int64_t)o.cout * o.cin : nullptr;
             kind = PSW_PROF_FC;
@@ -1072,6 +1108,12 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
         case PSW_OP_GAVG:
             kind = PSW_PROF_POOL;
             if (din) PSW_TRY(psw::gavgpool_bwd(a.n, a.c, a.h, a.w, g, din, acc0, sb), "gavgpool_bwd");
+            break;
+        case PSW_OP_DROPOUT:  // the mask of this step's forward pass, recomputed
+            kind = PSW_PROF_OTHER;
+            if (din)
+                PSW_TRY(psw::dropout_apply(y.numel(), g, din, acc0, o.k, net->dropout_seed, (uint32_t)i, io.t, sb),
+                        "dropout");
             break;
         case PSW_OP_FC: {
             kind = PSW_PROF_OTHER;

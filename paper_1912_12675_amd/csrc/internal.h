@@ -230,6 +230,12 @@ hipError_t sgd_stage(const SgdSeg* segs, int nseg, const float* w_in, float* w_o
                      float mom, float wd, int nesterov, hipStream_t st);
 hipError_t channel_sum(int n, int c, int hw, const float* x, float* out, void* ws, size_t ws_bytes,
                        hipStream_t st);
+// Dropout with counter-based masks (Philox4x32-10): out (+)= keep * in * scale
+// over n floats, the mask of operation `op` at step t under `seed`, drop
+// probability p24 / 2^24 (0 < p24 < 2^24); the same call with the gradients
+// is the backward pass.
+hipError_t dropout_apply(int64_t n, const float* in, float* out, int accumulate, int p24, uint64_t seed, uint32_t op,
+                         int64_t t, hipStream_t st);
 size_t channel_sum_ws_bytes(int n, int c, int hw);
 
 }  // namespace psw

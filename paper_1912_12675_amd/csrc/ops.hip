@@ -1224,6 +1224,89 @@ hipError_t sgd_stage(const SgdSeg* segs, int nseg, const float* w_in, float* w_o
     return hipSuccess;
 }
 
+// ------------------------------------------------------------- dropout -----
+// Masks from Philox4x32-10 (Salmon, Moraes, Dror, Shaw, SC 2011): ten rounds
+// on a 4-word counter; each round takes the two 32x32 -> 64-bit products of
+// counter words 0 and 2 with the round multipliers, and the new counter is
+// (hi(word 2 product) ^ word 1 ^ key 0, lo(word 2 product), hi(word 0
+// product) ^ word 3 ^ key 1, lo(word 0 product)); the key grows by the two
+// Weyl increments between rounds.  Thread q draws the words of elements
+// 4q .. 4q+3 from counter (q, op, t mod 2^32, t / 2^32) under key
+// (seed mod 2^32, seed / 2^32); element j is kept iff the top 24 bits of its
+// word are >= p24, and kept values are scaled by 2^24 / (2^24 - p24).
+__device__ __forceinline__ uint4 philox4x32_10(uint4 c, uint32_t k0, uint32_t k1)
+{
+#pragma unroll
+    for (int round = 0; round < 10; ++round) {
+        if (round) {
+            k0 += 0x9E3779B9u;
+            k1 += 0xBB67AE85u;
+        }
+        const uint32_t hi0 = __umulhi(0xD2511F53u, c.x), lo0 = 0xD2511F53u * c.x;
+        const uint32_t hi1 = __umulhi(0xCD9E8D57u, c.z), lo1 = 0xCD9E8D57u * c.z;
+        c = make_uint4(hi1 ^ c.y ^ k0, lo1, hi0 ^ c.w ^ k1, lo0);
+    }
+    return c;
+}
+
+struct DropKey {
+    uint32_t k0, k1, op, t_lo, t_hi;
+    int p24;
+    float scale;
+};
+
+// out[j] (+)= keep(j) ? in[j] * scale : 0, four elements per thread
+__global__ void dropout_k(int64_t n, const float* in, float* out, int accumulate, DropKey dk)
+{
+    const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t j0 = q * 4;
+    if (j0 >= n) return;
+    const uint4 r = philox4x32_10(make_uint4((uint32_t)q, dk.op, dk.t_lo, dk.t_hi), dk.k0, dk.k1);
+    const uint32_t w[4] = {r.x, r.y, r.z, r.w};
+    float v[4], o[4] = {0.f, 0.f, 0.f, 0.f};
+    const bool full = j0 + 4 <= n && (uintptr_t)(in + j0) % 16 == 0 && (uintptr_t)(out + j0) % 16 == 0;
+    if (full) {
+        const float4 a = *reinterpret_cast<const float4*>(in + j0);
+        v[0] = a.x, v[1] = a.y, v[2] = a.z, v[3] = a.w;
+        if (accumulate) {
+            const float4 b = *reinterpret_cast<const float4*>(out + j0);
+            o[0] = b.x, o[1] = b.y, o[2] = b.z, o[3] = b.w;
+        }
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            v[e] = j0 + e < n ? in[j0 + e] : 0.f;
+            if (accumulate && j0 + e < n) o[e] = out[j0 + e];
+        }
+    }
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const float d = (int)(w[e] >> 8) >= dk.p24 ? v[e] * dk.scale : 0.f;
+        o[e] = accumulate ? o[e] + d : d;
+    }
+    if (full) {
+        *reinterpret_cast<float4*>(out + j0) = make_float4(o[0], o[1], o[2], o[3]);
+    } else {
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            if (j0 + e < n) out[j0 + e] = o[e];
+    }
+}
+
+hipError_t dropout_apply(int64_t n, const float* in, float* out, int accumulate, int p24, uint64_t seed, uint32_t op,
+                         int64_t t, hipStream_t st)
+{
+    if (n < 0 || p24 <= 0 || p24 >= (1 << 24) || t < 0) return hipErrorInvalidValue;
+    if ((n + 3) / 4 > (int64_t)UINT32_MAX + 1) return hipErrorInvalidValue;  // counter word 0 is j / 4
+    if (n == 0) return hipSuccess;
+    DropKey dk{(uint32_t)seed, (uint32_t)(seed >> 32), op, (uint32_t)t, (uint32_t)((uint64_t)t >> 32), p24,
+               (float)(16777216.0 / (16777216.0 - p24))};
+    const int64_t quads = (n + 3) / 4;
+    PSW_LAUNCH(kname("dropout_k"), (Work{(double)n, kF * (2.0 + accumulate) * n}),
+               dropout_k, dim3(blocks_for(quads)), dim3(kBlock), 0, st, n, in, out, accumulate, dk);
+    return hipGetLastError();
+}
+
 hipError_t fc_fwd(int n, int in, int out, const float* x, const float* w, const float* b, int relu, float* y, int bf16,
                   hipStream_t st)
 {

@@ -73,6 +73,8 @@ SIGNATURES = {
     "psw_relu_mask": (_I, [_I64, _P, _P, _P]),
     "psw_softmax_xent": (_I, [_I, _I, _P, _P, _P, _P, _P]),
     "psw_sgd_momentum_step": (_I, [_I64, _P, _P, _P, _P, _F, _F, _F, _I, _P]),
+    "psw_dropout": (_I, [_I64, _P, _P, _I, _I, ctypes.c_uint64, ctypes.c_int32, _I64, _P]),
+    "psw_net_set_dropout_seed": (_I, [_P, ctypes.c_uint64]),
     "psw_net_create": (_I, [ctypes.POINTER(psw_layer), _I, _I, _I, _I, _I, _P, _I, _P, _I,
                             ctypes.POINTER(ctypes.c_void_p)]),
     "psw_net_destroy": (None, [_P]),
@@ -256,6 +258,12 @@ def psw_sgd_momentum_step(w_in, w_out, v, g, lr, mom=0.9, wd=0.0, nesterov=False
                                        int(nesterov), _stream(stream)))
 
 
+def psw_dropout(x, y, p24, seed, op, t, accumulate=False, stream=None):
+    """y (+)= keep * x * 2^24 / (2^24 - p24), the Philox mask of (seed, op, t)."""
+    _check(lib().psw_dropout(x.numel(), _ptr(x), _ptr(y), int(accumulate), int(p24), int(seed), int(op), int(t),
+                             _stream(stream)))
+
+
 # ------------------------------------------------------------- networks ----
 def _layers(ops):
     ops = np.ascontiguousarray(ops, dtype=np.int32).reshape(-1, 9)
@@ -352,6 +360,9 @@ class Net:
 
     def set_step(self, t):
         _check(lib().psw_net_set_step(self.handle, int(t)))
+
+    def set_dropout_seed(self, seed):
+        _check(lib().psw_net_set_dropout_seed(self.handle, int(seed)))
 
     def set_weight_stashing(self, on=True):
         """Backward data gradients with the forward's version (comparison scheme)."""

@@ -12,7 +12,10 @@ mini-batch, operation i writes tensor i+1):
 
 kind: 1 conv, 2 batch-norm (+ optional residual in1, + optional ReLU),
 3 max-pool (k x k, stride, no padding), 4 global average pool, 5 fully
-connected.  flags: bit0 bias, bit1 ReLU.  A batch-norm whose residual has
+connected, 6 dropout (k = drop probability in units of 2^-24; its mask is a
+function of the seed, the operation, the step and the element, so the
+backward pass of a mini-batch recomputes the forward's mask).  flags: bit0
+bias, bit1 ReLU.  A batch-norm whose residual has
 fewer channels or a larger spatial size than its output uses the CIFAR-ResNet
 "option A" shortcut (subsample + zero channel padding).
 
@@ -28,8 +31,15 @@ from typing import Callable, List, Sequence
 
 import numpy as np
 
-CONV, BN, MAXPOOL, GAVG, FC = 1, 2, 3, 4, 5
+CONV, BN, MAXPOOL, GAVG, FC, DROPOUT = 1, 2, 3, 4, 5, 6
 F_BIAS, F_RELU = 1, 2
+
+
+def dropout_threshold(p: float) -> int:
+    """The dropout op's k field: drop probability p in units of 2^-24."""
+    k = int(round(p * (1 << 24)))
+    assert 0 < k < (1 << 24), p
+    return k
 
 
 @dataclasses.dataclass
@@ -51,6 +61,7 @@ class Workload:
     seed: int = 0
     input_dist: str = "normal"      # "normal" N(0,1) or "uniform" U[0,1)
     lr_fn: Callable[[int], List[float]] | None = None  # per-step, per-stage rates (default: lr every step)
+    dropout_seed: int = 0            # key of the dropout masks (64-bit)
 
     @property
     def n_stages(self) -> int:
@@ -136,9 +147,11 @@ def alexnet_cifar():
     return b.desc(), b.layer_end, (3, 32, 32)
 
 
-def vgg16_bn():
+def vgg16_bn(dropout: float | None = None):
     """VGG-16 with BN, CIFAR shape: 13 conv 3x3 (no bias) -> BN -> ReLU,
-    max-pool 2x2/2 after convs 2, 4, 7, 10, 13, fc 512-10."""
+    max-pool 2x2/2 after convs 2, 4, 7, 10, 13, fc 512-10.  With dropout = p:
+    dropout(p) after every BN+ReLU that no max-pool follows, and before the
+    classifier (App. A names dropout for VGG-16 without placing it)."""
     b = _Builder()
     chans = [64, 64, 128, 128, 256, 256, 256, 512, 512, 512, 512, 512, 512]
     pools = {2, 4, 7, 10, 13}
@@ -148,8 +161,12 @@ def vgg16_bn():
         t = b.add(BN, t, c, c, flags=F_RELU)
         if i in pools:
             t = b.add(MAXPOOL, t, c, c, 2, 2)
+        elif dropout is not None:
+            t = b.add(DROPOUT, t, c, c, dropout_threshold(dropout))
         b.end_layer()
         cin = c
+    if dropout is not None:
+        t = b.add(DROPOUT, t, 512, 512, dropout_threshold(dropout))
     b.add(FC, t, 512, 10, flags=F_BIAS)
     b.end_layer()
     return b.desc(), b.layer_end, (3, 32, 32)
@@ -238,13 +255,14 @@ def resnet20_workload(batch=128, steps=50, seed=1914, bf16=False):
                     _const([3, 2, 1, 0]), steps, [0.01] * 4, seed=seed, bf16=bf16)
 
 
-def vgg16_workload(batch=128, steps=40, n_pipelined=30, seed=1915):
-    ops, le, ins = vgg16_bn()
+def vgg16_workload(batch=128, steps=40, n_pipelined=30, seed=1915, dropout=None):
+    ops, le, ins = vgg16_bn(dropout)
     se = _stage_end_from_ppv(le, (2, 4, 7), len(ops))    # Table 1, VGG-16 (2,4,7)
 
     def hybrid(t, n_p=n_pipelined):
         return [3, 2, 1, 0] if t < n_p else [0, 0, 0, 0]
-    return Workload("vgg16_bn", ops, ins, 10, batch, le, se, hybrid, steps, [0.01] * 4, seed=seed)
+    return Workload("vgg16_bn" + ("_dropout" if dropout is not None else ""), ops, ins, 10, batch, le, se, hybrid,
+                    steps, [0.01] * 4, seed=seed, dropout_seed=(seed << 32) | 0x5EED if dropout is not None else 0)
 
 
 def resnet110_workload(batch=256, steps=50, seed=1916, bf16=True):

@@ -225,6 +225,43 @@ def test_fc_parity(P, oracle, n, fin, fout, relu, bf16):
     assert_close(dx2, rdx + base, what="fc dx acc")
 
 
+@pytest.mark.parametrize("n,p,offset", [(5, 0.5, 0), (1 << 20, 0.3, 0), (1000003, 0.5, 1), (4097, 0.9, 3)])
+def test_dropout_parity(P, oracle, n, p, offset):
+    """Keep decisions bit-exact against the oracle's (integer comparisons of
+    the same Philox words); kept values within fp32 rounding; forward and
+    accumulating backward; ragged counts and misaligned (scalar) views."""
+    from paper_1912_12675_amd import synth
+    k = synth.dropout_threshold(p)
+    rng = np.random.default_rng(n + offset)
+    x = f32(rng, (n,))
+    seed, op, t = 0x0123_4567_89AB_CDEF, 11, (1 << 32) + 17
+    xb = torch.zeros(n + offset, device="cuda")
+    xb[offset:] = dev(x)
+    yb = torch.full((n + offset,), 7.0, device="cuda")
+    P.psw_dropout(xb[offset:], yb[offset:], k, seed, op, t)
+    ref = oracle.dropout_fwd(x, k, seed, op, t)
+    y = yb[offset:].cpu().numpy()
+    np.testing.assert_array_equal(y == 0, ref == 0)
+    np.testing.assert_allclose(y, ref, rtol=2e-7, atol=0)
+    assert yb[:offset].eq(7.0).all()
+    base = f32(rng, (n,))
+    gb = torch.zeros(n + offset, device="cuda")
+    gb[offset:] = dev(base)
+    P.psw_dropout(xb[offset:], gb[offset:], k, seed, op, t, accumulate=True)
+    np.testing.assert_allclose(gb[offset:].cpu().numpy(), base + oracle.dropout_bwd(x, k, seed, op, t), rtol=1e-6,
+                               atol=1e-6)
+
+
+def test_dropout_rejects_bad_arguments(P):
+    x = torch.zeros(8, device="cuda")
+    for kw in (dict(p24=0), dict(p24=1 << 24)):
+        with pytest.raises(P.PswError):
+            P.psw_dropout(x, x, kw["p24"], 1, 0, 0)
+    with pytest.raises(P.PswError):
+        P.psw_dropout(x, x, 100, 1, 0, -1)
+    P.psw_dropout(x[:0], x[:0], 100, 1, 0, 0)  # empty: nothing to do
+
+
 def test_relu_mask(P):
     rng = np.random.default_rng(1)
     z = np.maximum(f32(rng, (1000,)), 0)

@@ -11,7 +11,7 @@ import numpy as np
 import torch
 import torch.nn.functional as F
 
-from paper_1912_12675_amd.synth import BN, CONV, F_BIAS, F_RELU, FC, GAVG, MAXPOOL
+from paper_1912_12675_amd.synth import BN, CONV, DROPOUT, F_BIAS, F_RELU, FC, GAVG, MAXPOOL
 
 
 def op_param_slices(ops, stage_end):
@@ -54,11 +54,41 @@ def _shortcut(res, c_out, h_out):
     return F.pad(res[:, :, ::step, ::step], (0, 0, 0, 0, lo, c_out - c_in - lo))
 
 
-def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5, bn_mom=0.1):
+def philox4x32_10(ctr, key):
+    """Philox4x32-10 (Salmon et al., SC 2011) over arrays: ctr [n, 4] and key
+    [n, 2] (or [2]) as uint32; returns [n, 4] uint32.  Written independently
+    of the oracle's C version (numpy, vectorised over counters)."""
+    c = [np.asarray(ctr, dtype=np.uint64)[:, i] for i in range(4)]
+    k = np.broadcast_to(np.asarray(key, dtype=np.uint64), (c[0].shape[0], 2))
+    k0, k1 = k[:, 0].copy(), k[:, 1].copy()
+    mask = np.uint64(0xFFFFFFFF)
+    for r in range(10):
+        if r:
+            k0 = (k0 + np.uint64(0x9E3779B9)) & mask
+            k1 = (k1 + np.uint64(0xBB67AE85)) & mask
+        p0 = np.uint64(0xD2511F53) * c[0]
+        p1 = np.uint64(0xCD9E8D57) * c[2]
+        c = [((p1 >> np.uint64(32)) ^ c[1] ^ k0) & mask, p1 & mask, ((p0 >> np.uint64(32)) ^ c[3] ^ k1) & mask,
+             p0 & mask]
+    return np.stack(c, axis=1).astype(np.uint32)
+
+
+def dropout_mask(numel, p24, seed, op, step):
+    """Keep mask (bool, flat NCHW order) of the dropout op `op` at step `step`:
+    element j is kept iff the top 24 bits of word j % 4 of Philox4x32-10 with
+    counter (j // 4, op, step low, step high) and key (seed low, seed high)
+    are >= p24."""
+    q = np.arange((numel + 3) // 4, dtype=np.uint64)
+    ctr = np.stack([q, np.full_like(q, op), np.full_like(q, step & 0xFFFFFFFF), np.full_like(q, step >> 32)], axis=1)
+    r = philox4x32_10(ctr, [seed & 0xFFFFFFFF, seed >> 32]).reshape(-1)[:numel]
+    return (r >> 8) >= p24
+
+
+def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5, bn_mom=0.1, dropout_key=None):
     """Apply ops[lo:hi].  inputs: dict tensor_id -> tensor (must hold every
     tensor that ops[lo:hi] read from outside the range).  stage_params: list
-    of flat per-stage torch tensors.  Returns the dict extended with the
-    tensors written."""
+    of flat per-stage torch tensors.  dropout_key: (seed, step) of the
+    dropout masks.  Returns the dict extended with the tensors written."""
     t = dict(inputs)
     for i in range(lo, hi):
         kind, in0, in1, cin, cout, k, stride, pad, flags = (int(v) for v in ops[i])
@@ -87,6 +117,10 @@ def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5
             if flags & F_RELU:
                 y = F.relu(y)
             y = y.reshape(y.shape[0], -1, 1, 1)
+        elif kind == DROPOUT:
+            seed, step = dropout_key if dropout_key is not None else (0, 0)
+            keep = torch.from_numpy(dropout_mask(a.numel(), k, seed, i, step)).reshape(a.shape)
+            y = a * keep.to(a.dtype) * (16777216.0 / (16777216.0 - k))
         else:
             raise ValueError(kind)
         t[i + 1] = y
@@ -239,7 +273,7 @@ def simulate_register_pipeline(ops, stage_end, params0, xs, labels, lr, mom=0.9,
 
 
 def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=0.0, dtype=torch.float64,
-                stash=False):
+                stash=False, dropout_seed=0):
     """The stale-weight schedule written with autograd, for any staleness
     table (hybrid included): keep every stage's version history; for step t
     load version max(0, t - d_s) into the stage's weight tensor and run the
@@ -268,7 +302,7 @@ def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=
             with torch.no_grad():
                 Wp[s].copy_(hist[s][r])
             Wp[s].grad = None
-        outs = run_ops(ops, 0, n, {0: torch.tensor(xs[t], dtype=dtype)}, Wp, slices)
+        outs = run_ops(ops, 0, n, {0: torch.tensor(xs[t], dtype=dtype)}, Wp, slices, dropout_key=(dropout_seed, t))
         loss = F.cross_entropy(outs[n].reshape(outs[n].shape[0], -1), torch.tensor(labels[t], dtype=torch.long))
         losses[t] = float(loss.detach())
         if not stash:
