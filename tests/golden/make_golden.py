@@ -42,8 +42,8 @@ def make(mode):
     p0 = synth.init_params(wl)
     xs, ys = synth.batches(wl, T)
     t0 = time.time()
-    out = O.train(wl.ops, wl.in_shape, wl.stage_end, p0, xs, ys, wl.staleness(T), wl.lr, wl.momentum,
-                  wl.weight_decay, wl.nesterov, bf16=wl.bf16)
+    out = O.train(wl.ops, wl.in_shape, wl.stage_end, p0, xs, ys, wl.staleness(T), wl.lr_table(T), wl.momentum,
+                  wl.weight_decay, wl.nesterov, bf16=wl.bf16, dropout_seed=wl.dropout_seed)
     path = os.path.join(HERE, f"resnet20_b128_50steps_{mode}.npz")
     np.savez_compressed(path, delta=(out["params"] - p0.astype(np.float64)).astype(np.float32),
                         losses=out["losses"], versions=out["versions"])
@@ -98,8 +98,8 @@ def make_full(name):
     res = []
     t0 = time.time()
     for x in (xs, ulp_move(xs, 1912)):
-        out = O.train(wl.ops, wl.in_shape, wl.stage_end, p0, x, ys, st, wl.lr, wl.momentum, wl.weight_decay,
-                      wl.nesterov, bf16=wl.bf16)
+        out = O.train(wl.ops, wl.in_shape, wl.stage_end, p0, x, ys, st, wl.lr_table(T), wl.momentum,
+                      wl.weight_decay, wl.nesterov, bf16=wl.bf16, dropout_seed=wl.dropout_seed)
         norms, dnorms, nz = tensor_norms(wl, out["params"], p0)
         res.append(dict(sample=out["params"][idx], norms=norms, dnorms=dnorms, nz=nz, losses=out["losses"],
                         versions=out["versions"]))

@@ -429,7 +429,8 @@ def test_full_size_against_oracle(P, name, factory, T):
     net.load_params(p0)
     xs, ys = synth.batches(wl, T)
     losses = torch.zeros(T, device="cuda")
-    ver = net.pipeline_run(0, st, wl.lr, torch.from_numpy(xs).cuda(), torch.from_numpy(ys).cuda(), losses,
+    net.set_dropout_seed(wl.dropout_seed)
+    ver = net.pipeline_run(0, st, wl.lr_table(T), torch.from_numpy(xs).cuda(), torch.from_numpy(ys).cuda(), losses,
                            wl.momentum, wl.weight_decay, wl.nesterov)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(ver, g["versions"])
