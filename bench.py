@@ -32,8 +32,9 @@ the HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE counters
 (calibrated on a plain streaming kernel) stored in profiles/traffic.json,
 used only when the source files defining that kernel still hash to what was
 profiled, else null.
-`cpu_baseline` times the CPU oracle on a bounded sample (2 steps of the same
-workload).
+`cpu_baseline` times the CPU oracle on a bounded sample: 2-step runs of the
+same workload, repeated until 10 s of host time have passed (about 12 steps
+on 16 host threads).
 
 `python bench.py --copy-calibration` instead runs a plain streaming kernel
 five times: y = -x over 256 MiB (reads and writes 256 MiB each; the
@@ -113,21 +114,26 @@ def copy_calibration():
     print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 5}), flush=True)
 
 
-def cpu_baseline(wl, steps=2):
+def cpu_baseline(wl, chunk=2, min_seconds=10.0, max_chunks=15):
     from oracle import oracle
     from paper_1912_12675_amd import synth
 
     oracle.build()
     p0 = synth.init_params(wl)
-    xs, ys = synth.batches(wl, steps)
-    t0 = time.perf_counter()
-    oracle.train(wl.ops, wl.in_shape, wl.stage_end, p0, xs, ys, wl.staleness(steps), wl.lr, wl.momentum,
-                 wl.weight_decay, wl.nesterov, bf16=wl.bf16)
+    xs, ys = synth.batches(wl, chunk)
+    steps, t0 = 0, time.perf_counter()
+    while steps < chunk * max_chunks:
+        oracle.train(wl.ops, wl.in_shape, wl.stage_end, p0, xs, ys, wl.staleness(chunk), wl.lr_table(chunk),
+                     wl.momentum, wl.weight_decay, wl.nesterov, bf16=wl.bf16)
+        steps += chunk
+        if time.perf_counter() - t0 >= min_seconds:
+            break
     dt = time.perf_counter() - t0
     return {"value": round(steps * wl.batch / dt, 3), "unit": "images/s", "cores": oracle.num_threads(),
             "kind": "oracle",
             "sample": f"{steps} stale-weight training steps of the same workload (ResNet-20, batch {wl.batch}, "
-                      f"float64 direct loops, OpenMP), {dt:.1f} s"}
+                      f"float64 direct loops, OpenMP; runs of {chunk} steps until {min_seconds:.0f} s), "
+                      f"{dt:.1f} s"}
 
 
 def main():
