@@ -129,11 +129,23 @@ def cpu_baseline(wl, chunk=2, min_seconds=10.0, max_chunks=15):
         if time.perf_counter() - t0 >= min_seconds:
             break
     dt = time.perf_counter() - t0
-    return {"value": round(steps * wl.batch / dt, 3), "unit": "images/s", "cores": oracle.num_threads(),
+    cores = oracle.num_threads()
+    # one step on one host thread, for the single-threaded figure
+    oracle.set_threads(1)
+    try:
+        t1 = time.perf_counter()
+        oracle.train(wl.ops, wl.in_shape, wl.stage_end, p0, xs[:1], ys[:1], wl.staleness(1), wl.lr_table(1),
+                     wl.momentum, wl.weight_decay, wl.nesterov, bf16=wl.bf16)
+        dt1 = time.perf_counter() - t1
+    finally:
+        oracle.set_threads(cores)
+    return {"value": round(steps * wl.batch / dt, 3), "unit": "images/s", "cores": cores,
             "kind": "oracle",
             "sample": f"{steps} stale-weight training steps of the same workload (ResNet-20, batch {wl.batch}, "
                       f"float64 direct loops, OpenMP; runs of {chunk} steps until {min_seconds:.0f} s), "
-                      f"{dt:.1f} s"}
+                      f"{dt:.1f} s",
+            "single_thread": {"value": round(wl.batch / dt1, 3), "unit": "images/s", "cores": 1,
+                              "sample": f"1 step of the same workload on one thread, {dt1:.1f} s"}}
 
 
 def main():
