@@ -297,8 +297,11 @@ int psw_pipeline_run(psw_net *net, int64_t t0, int n_steps, const int32_t *stale
  * or any step congruent to t0 modulo the period; else PSW_ERR_STEP_ORDER),
  * with the captured staleness, lr, batches (relative to the launch) and
  * losses buffer.  n_steps must be a multiple of the period
- * lcm(ring_depth[s], 2) after which ring slots and step sets repeat, and no
- * captured step may clamp its version at 0 (run the pipeline fill eagerly).
+ * lcm(ring_depth[s], number of step sets) after which ring slots and step
+ * sets repeat, and no captured step may clamp its version at 0 (run the
+ * pipeline fill eagerly).  Nets with dropout are rejected
+ * (PSW_ERR_UNSUPPORTED): their masks depend on the step, which a replay
+ * would not advance.
  * The captured pointers must stay valid until psw_graph_destroy.  Graph
  * launches skip the host-side cost of issuing ~10^2 kernels and events per
  * step, which otherwise bounds small networks. */

@@ -1426,6 +1426,10 @@ int psw_pipeline_capture(psw_net* net, int n_steps, const int32_t* staleness, co
     const int64_t t0 = net ? net->next_t : 0;
     int rc = check_pipeline_args(net, t0, n_steps, staleness, lr, x, labels, n_batches, losses, "pipeline_capture");
     if (rc) return rc;
+    for (const psw_layer& o : net->ops)  // a replay would repeat the captured steps' masks
+        if (o.kind == PSW_OP_DROPOUT)
+            return fail(PSW_ERR_UNSUPPORTED, "pipeline_capture: dropout masks depend on the step; run nets with "
+                        "dropout with psw_pipeline_run");
     const int64_t period = replay_period(net);
     if (n_steps <= 0 || n_steps % period != 0)
         return fail(PSW_ERR_SHAPE, "pipeline_capture: n_steps must be a positive multiple of %lld", (long long)period);

@@ -399,6 +399,21 @@ def test_graph_capture_rejects_fill_and_bad_length(P):
         net.capture(st[:5], wl.lr, xs, ys, losses)
 
 
+def test_graph_capture_rejects_dropout(P):
+    """A replay would repeat the captured steps' dropout masks."""
+    wl = synth.vgg16_workload(batch=2, dropout=0.3)
+    net = P.Net(wl.ops, 2, wl.in_shape, wl.stage_end, [4, 3, 2, 1])
+    net.load_params(synth.init_params(wl))
+    xs, ys = synth.batches(wl, 12, 2)
+    xs, ys = torch.from_numpy(xs).cuda(), torch.from_numpy(ys).cuda()
+    losses = torch.zeros(12, device="cuda")
+    st = _table(lambda t: [3, 2, 1, 0], 12, 4)
+    net.pipeline_run(0, st[:3], wl.lr, xs[:3], ys[:3], losses[:3], wl.momentum)
+    with pytest.raises(P.PswError) as e:
+        net.capture(st, wl.lr, xs, ys, losses)
+    assert e.value.code == -3
+
+
 # ---- the other configurations at full size, against stored oracle runs ----
 FULL_CASES = [
     ("alexnet", lambda: synth.alexnet_workload(), 20),
