@@ -167,15 +167,29 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     }
     float4 xr[XV];
     float4 wr[WV];
+    // Loads are issued without branches: a lane whose element lies outside
+    // the tensor (halo rows, channels past C, threads past the chunk) loads
+    // from offset 0 and keeps zero, so the compiler can count outstanding
+    // memory operations exactly instead of waiting for all of them.
+    const bool wfast = wvec && (a.C % CC == 0);  // every weight run of every chunk is in range
     auto load_chunk = [&](int img, int ih0, int c0) {  // channels c0.. of tile (img, rows from ih0)
         const int xb = ((img * a.C + c0) * HIN + ih0) * WIN;
 #pragma unroll
         for (int k = 0; k < XV; ++k) {
-            float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
             const int ih = ih0 + xrow[k];
-            if (xch[k] < CC && ih >= 0 && ih < HIN && c0 + xch[k] < a.C)
-                v = *reinterpret_cast<const float4*>(a.x + (xb + xg[k]));
-            xr[k] = v;
+            const bool ok = ((k + 1) * NT <= XN || xch[k] < CC) && ih >= 0 && ih < HIN && c0 + xch[k] < a.C;
+            const float4 v = *reinterpret_cast<const float4*>(a.x + (ok ? xb + xg[k] : 0));
+            xr[k] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+        if (wfast) {
+#pragma unroll
+            for (int k = 0; k < WV; ++k) {
+                const bool ok = (k + 1) * NT * 4 <= WN4 * 4 || wc[k] >= 0;
+                const int off = TRANS ? wg[k] + c0 * a.K * 9 : wg[k] + c0 * 9;
+                const float4 v = *reinterpret_cast<const float4*>(a.w + (ok ? off : 0));
+                wr[k] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+            return;
         }
 #pragma unroll
         for (int k = 0; k < WV; ++k) {
@@ -208,10 +222,10 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     auto store_chunk = [&]() {
 #pragma unroll
         for (int k = 0; k < XV; ++k)
-            if (xch[k] < CC) *reinterpret_cast<float4*>(&Xs[xl[k]]) = xr[k];
+            if ((k + 1) * NT <= XN || xch[k] < CC) *reinterpret_cast<float4*>(&Xs[xl[k]]) = xr[k];
 #pragma unroll
         for (int k = 0; k < WV; ++k) {
-            if (wc[k] < 0) continue;
+            if (!((k + 1) * NT * 4 <= WN4 * 4 || wc[k] >= 0)) continue;
             const float vv[4] = {wr[k].x, wr[k].y, wr[k].z, wr[k].w};
             if (!TRANS) {
 #pragma unroll
