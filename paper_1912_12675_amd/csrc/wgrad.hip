@@ -7,7 +7,8 @@
 // A workgroup reduces over TPW consecutive (image, TH-row band) tiles and
 // writes one dW-shaped partial sum; the partials are added in a fixed order
 // by the reduction kernel of conv.hip, so the result is bit-reproducible.
-// blockIdx.y selects a group of CBW 16-channel input blocks.  In the
+// blockIdx.y selects a group of CBW 16-channel input blocks and blockIdx.z a
+// group of KBW 16-channel output blocks.  In the
 // workgroup, wave (kb, cb, wpx) owns the 16x16 output blocks (output channels
 // kb*16.., input channels of block cb) of all 9 taps (9 MFMA accumulators)
 // and the pixel quads wpx, wpx+WPX, ...; waves that differ only in wpx are
@@ -75,6 +76,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
     const int g = lane >> 4, j = lane & 15;
     const int bands = a.HO / TH;         // row bands per image
     const int cbase = blockIdx.y * CCH;  // first input channel of this workgroup
+    const int kbase = blockIdx.z * KC;   // first output channel of this workgroup
 
     v4f acc[9];
 #pragma unroll
@@ -103,7 +105,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
             if (i4 < DN4) {
                 const int i = i4 * 4;
                 const int k = i / NPC, pix = i - (i / NPC) * NPC;
-                val = *reinterpret_cast<const float4*>(a.dy + (((size_t)img * a.K + k) * a.HO + oh0) * WO + pix);
+                val = *reinterpret_cast<const float4*>(a.dy + (((size_t)img * a.K + kbase + k) * a.HO + oh0) * WO + pix);
             }
             dr[v] = val;
         }
@@ -197,7 +199,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
     float* out = a.part + (size_t)blockIdx.x * a.K * a.C * 9;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        const int k = kb * 16 + 4 * g + i, c = cbase + cb * 16 + j;
+        const int k = kbase + kb * 16 + 4 * g + i, c = cbase + cb * 16 + j;
         if (c >= a.C) continue;  // zero-filled channels of a narrow input (C < 16)
         float* o = out + ((size_t)k * a.C + c) * 9;
 #pragma unroll
@@ -209,8 +211,8 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
 int wgrad_config(int n, int C, int H, int W, int K, int stride)
 {
     if (stride == 1 && H == 32 && W == 32 && C == 16 && K == 16) return 1;
-    if (stride == 1 && H == 16 && W == 16 && C == 32 && K == 32) return 2;
-    if (stride == 1 && H == 8 && W == 8 && C == 64 && K == 64 && n % 2 == 0) return 3;
+    if (stride == 1 && H == 16 && W == 16 && C == 32 && K == 32 && n % 2 == 0) return 2;
+    if (stride == 1 && H == 8 && W == 8 && C == 64 && K == 64 && n % 4 == 0) return 3;
     if (stride == 2 && H == 32 && W == 32 && C == 16 && K == 32) return 4;
     if (stride == 2 && H == 16 && W == 16 && C == 32 && K == 64) return 5;
     if (stride == 1 && H == 32 && W == 32 && C < 16 && K == 16) return 6;
@@ -224,8 +226,8 @@ int conv3x3_wgrad_splits(int n, int C, int H, int W, int K, int stride)
 {
     switch (wgrad_config(n, C, H, W, K, stride)) {
     case 1: return n * 2;       // one 16-row band (of 32) per workgroup
-    case 2: return n;           // one image per workgroup
-    case 3: return n / 2;       // two images per workgroup
+    case 2: return n / 2;       // two images per workgroup (and 16 of the 32 output channels)
+    case 3: return n / 4;       // four images per workgroup (and 32 of the 64 output channels)
     case 4: return n * 2;       // one 8-row band (of 16 output rows) per workgroup
     case 5: return n;           // one image per workgroup
     case 6: return n * 2;       // as 1, input channels zero-filled to 16
@@ -242,7 +244,9 @@ hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const fl
     WgArgs a{x, dy, part, n, C, H, W, K, H / stride};
     const int splits = conv3x3_wgrad_splits(n, C, H, W, K, stride);
     const int cgroups = (C + 15) / 16;  // one 16-channel block per workgroup (grid.y)
-    const dim3 grid(splits, cgroups);
+    // output-channel groups: configurations 2 and 3 split K over the grid
+    const int kgroups = cfg == 2 ? K / 16 : cfg == 3 ? K / 32 : 1;
+    const dim3 grid(splits, cgroups, kgroups);
     const Work wk = conv_work(n, C, H, W, K, 3, 3, H / stride, W / stride);
     switch (cfg) {
     case 6:
@@ -251,11 +255,11 @@ hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const fl
                    st, a);
         break;
     case 2:
-        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 16, 16, 2, 1, 2, 1, 4), wk, (conv3x3_wgrad<1, 16, 16, 2, 1, 2, 1, 4>), grid, dim3(256), 0,
+        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 16, 16, 1, 1, 4, 2, 8), wk, (conv3x3_wgrad<1, 16, 16, 1, 1, 4, 2, 8>), grid, dim3(256), 0,
                    st, a);
         break;
     case 3:
-        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 8, 8, 4, 1, 1, 2, 8), wk, (conv3x3_wgrad<1, 8, 8, 4, 1, 1, 2, 8>), grid, dim3(256), 0,
+        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 8, 8, 2, 1, 2, 4, 8), wk, (conv3x3_wgrad<1, 8, 8, 2, 1, 2, 4, 8>), grid, dim3(256), 0,
                    st, a);
         break;
     case 4:

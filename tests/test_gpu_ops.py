@@ -66,6 +66,10 @@ CONV = [
     (2, 256, 8, 8, 256, 3, 1, 1),
     (3, 16, 16, 16, 64, 3, 2, 1),
     (2, 48, 16, 16, 32, 3, 2, 1),
+    # the ResNet group-2 and group-3 weight-gradient tilings need 2 and 4
+    # images per workgroup
+    (4, 32, 16, 16, 32, 3, 1, 1),
+    (8, 64, 8, 8, 64, 3, 1, 1),
 ]
 
 
