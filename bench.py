@@ -164,7 +164,7 @@ def main():
                     help="run a plain 256 MiB streaming kernel 5 times (counter calibration) and exit")
     args = ap.parse_args()
     if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for {args.gpus}): this build has no multi-GPU path; "
+        print(f"bench.py runs on one GPU only (asked for {args.gpus}): the library has no multi-GPU path; "
               "the pipeline's stages all run on a single MI355X.", file=sys.stderr)
         sys.exit(2)
 

@@ -45,7 +45,7 @@ enum {
     PSW_OK = 0,
     PSW_ERR_NULL = -1,        /* a required pointer is NULL */
     PSW_ERR_SHAPE = -2,       /* inconsistent or out-of-range sizes */
-    PSW_ERR_UNSUPPORTED = -3, /* valid request this build does not implement */
+    PSW_ERR_UNSUPPORTED = -3, /* valid request the library does not implement */
     PSW_ERR_STALENESS = -4,   /* staleness < 0 or >= ring depth */
     PSW_ERR_STEP_ORDER = -5,  /* stage_step t is not the expected next step */
     PSW_ERR_WORKSPACE = -6,   /* workspace / arena too small */
