@@ -9,7 +9,8 @@ parameter update W^(50) - W^(0) (float32; W^(0) is regenerated from the
 seed), the 50 losses and the version table.
 
 alexnet / vgg16 / resnet110: the other full-size configurations (AlexNet-style
-net, batch 128, 20 steps, split after conv2, staleness [2,0]; VGG-16-BN,
+net, batch 128, 20 steps, split after conv2, staleness [2,0], App. A's rate
+0.001 with Nesterov momentum and weight decay 0.004; VGG-16-BN,
 batch 128, 30 stale steps at PPV (2,4,7) then 10 non-pipelined; ResNet-110,
 batch 256, bf16 products, 8 stages with d_s = 7-s, the first 3 steps).
 These nets have up to 86M parameters, so what is stored is: the losses, the

@@ -116,6 +116,23 @@ def test_plan_weight_stashing(psw):
     assert e.value.code == -1
 
 
+def test_plan_dropout_records(psw):
+    """Dropout ops appear in the plan as a forward record after their input's
+    producer and a backward record in reverse order, reading no weights."""
+    wl = synth.vgg16_workload(batch=2, dropout=0.3)
+    plan = psw.net_plan_only(wl.ops, 2, wl.in_shape, wl.stage_end, [4, 3, 2, 1], 5, [3, 2, 1, 0])
+    drop_ops = [i for i, o in enumerate(wl.ops) if int(o[0]) == synth.DROPOUT]
+    fwd = [(op, v) for op, what, _, v in plan if what == 13]
+    bwd = [(op, v) for op, what, _, v in plan if what == 14]
+    assert [op for op, _ in fwd] == drop_ops and all(v == -1 for _, v in fwd)
+    assert [op for op, _ in bwd] == drop_ops[::-1] and all(v == -1 for _, v in bwd)
+    # a bad threshold is rejected when the net is created
+    ops = np.array(wl.ops).copy()
+    ops[drop_ops[0], 5] = 1 << 24
+    with pytest.raises(psw.PswError):
+        psw.net_plan_only(ops, 2, wl.in_shape, wl.stage_end, [4, 3, 2, 1], 5, [3, 2, 1, 0])
+
+
 def test_plan_rejects_bad_staleness(psw):
     wl = synth.resnet20_workload(batch=4)
     with pytest.raises(psw.PswError) as e:
