@@ -257,7 +257,8 @@ def _sequential(P, wl, N, st, lr, stash=False):
     losses, versions = [], []
     for t in range(st.shape[0]):
         x, y = synth.batch(wl, t, N)
-        versions.append(net.step(t, st[t], lr, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), wl.momentum,
+        lr_t = lr[t] if np.ndim(lr) == 2 else lr
+        versions.append(net.step(t, st[t], lr_t, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), wl.momentum,
                                  wl.weight_decay, wl.nesterov))
         losses.append(float(net.loss.item()))
     torch.cuda.synchronize()
@@ -277,7 +278,8 @@ def _pipelined(P, wl, N, st, lr, chunks, stash=False):
     versions = []
     t0 = 0
     for n in chunks:  # consecutive runs continue the same schedule
-        versions.append(net.pipeline_run(t0, st[t0:t0 + n], lr, xs[t0:t0 + n], ys[t0:t0 + n], losses[t0:t0 + n],
+        lr_n = lr[t0:t0 + n] if np.ndim(lr) == 2 else lr
+        versions.append(net.pipeline_run(t0, st[t0:t0 + n], lr_n, xs[t0:t0 + n], ys[t0:t0 + n], losses[t0:t0 + n],
                                          wl.momentum, wl.weight_decay, wl.nesterov))
         t0 += n
     assert t0 == T
@@ -301,6 +303,11 @@ PIPE_CASES = [
     ("vgg16_hybrid", lambda: synth.vgg16_workload(batch=8, n_pipelined=3), 8, None, 5, [5]),
     ("resnet20_stash", lambda: synth.resnet20_workload(batch=8), 8, lambda t: [3, 2, 1, 0], 8, [3, 5]),
     ("vgg16_dropout", lambda: synth.vgg16_workload(batch=8, n_pipelined=3, dropout=0.4), 8, None, 5, [2, 3]),
+    # eight stages, ring depths 8..1, bf16 products: the deepest ring
+    ("resnet110_bf16", lambda: synth.resnet110_workload(batch=4), 4, None, 11, [9, 2]),
+    # Table 5's two-partition ResNet-56 with its hybrid switch
+    ("resnet56_2part", lambda: synth.resnet_two_partition_workload(56, batch=4, n_pipelined=5,
+                                                                    steps_per_epoch=0.03), 4, None, 8, [3, 5]),
 ]
 
 
@@ -313,8 +320,8 @@ def test_pipeline_run_equals_stage_steps(P, name, factory, N, rows, T, chunks):
     wl = factory()
     st = wl.staleness(T) if rows is None else _table(rows, T, len(wl.stage_end))
     stash = name.endswith("_stash")
-    a, la, va = _sequential(P, wl, N, st, wl.lr, stash)
-    b, lb, vb = _pipelined(P, wl, N, st, wl.lr, chunks, stash)
+    a, la, va = _sequential(P, wl, N, st, wl.lr_table(T), stash)
+    b, lb, vb = _pipelined(P, wl, N, st, wl.lr_table(T), chunks, stash)
     np.testing.assert_array_equal(va, vb)
     np.testing.assert_array_equal(la, lb)
     assert torch.equal(a.params(T), b.params(T))
