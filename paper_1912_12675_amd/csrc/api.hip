@@ -1338,7 +1338,13 @@ int issue_pipeline(psw_net* net, int64_t t0, int n_steps, const int32_t* stalene
             what = is.what;
             break;
         }
-        e = hipEventRecord(wdone, sw);
+        // the chain's end reaches the weight stream through stage 0's weight
+        // gradients; a stage 0 without convs (no work on sw) is joined here
+        if (!net->stage_has_conv[0]) {
+            e = hipEventRecord(net->stage_ev[0], sb);
+            if (e == hipSuccess) e = hipStreamWaitEvent(sw, net->stage_ev[0], 0);
+        }
+        if (e == hipSuccess) e = hipEventRecord(wdone, sw);
         if (e != hipSuccess) {
             what = "pipeline: step done";
             break;

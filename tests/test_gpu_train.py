@@ -291,6 +291,20 @@ def _table(rows, T, S):
     return np.array([rows(t) for t in range(T)], dtype=np.int32).reshape(T, S)
 
 
+def _mlp_workload(batch=8):
+    """Three FC stages and no convolution: every stage is updated on the
+    chain's own stream, and the weight stream has no work of its own."""
+    b = synth._Builder()
+    t = b.add(synth.FC, 0, 784, 64, flags=synth.F_BIAS | synth.F_RELU)
+    b.end_layer()
+    t = b.add(synth.FC, t, 64, 32, flags=synth.F_BIAS | synth.F_RELU)
+    b.end_layer()
+    b.add(synth.FC, t, 32, 10, flags=synth.F_BIAS)
+    b.end_layer()
+    return synth.Workload("mlp", b.desc(), (1, 28, 28), 10, batch, b.layer_end, [1, 2, 3],
+                          lambda t: [2, 1, 0], 6, [0.01] * 3, seed=1917)
+
+
 PIPE_CASES = [
     # name, workload, batch, staleness table (t -> per-stage d), steps, chunks
     ("resnet20_stale", lambda: synth.resnet20_workload(batch=8), 8, lambda t: [3, 2, 1, 0], 8, [8]),
@@ -308,6 +322,8 @@ PIPE_CASES = [
     # Table 5's two-partition ResNet-56 with its hybrid switch
     ("resnet56_2part", lambda: synth.resnet_two_partition_workload(56, batch=4, n_pipelined=5,
                                                                     steps_per_epoch=0.03), 4, None, 8, [3, 5]),
+    # no convolution anywhere: the step sets are freed through the chain's end
+    ("mlp_conv_free", lambda: _mlp_workload(batch=8), 8, None, 9, [9]),
 ]
 
 
