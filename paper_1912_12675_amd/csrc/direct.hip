@@ -245,6 +245,27 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     // across them: the first chunk of the next tile is loaded while the last
     // chunk of the current one is on the matrix cores
     load_chunk(blockIdx.x * TPW / tiles, (blockIdx.x * TPW % tiles) * TH * STRIDE - 1, 0);
+    // backward sums with one tile per workgroup: the BN tensors the epilogue
+    // reads are loaded now, so that their latency passes under the matrix work
+    constexpr bool PRE = TRANS && TPW == 1;
+    float pyy[PRE ? NBW : 1][4], pzz[PRE ? NBW : 1][4];
+    if constexpr (PRE) {
+        if (a.bnb.part) {
+            const int img = blockIdx.x / tiles, oh0 = (blockIdx.x - img * tiles) * TH;
+            const bool zmask = a.bnb.relu && !a.bnb.scale;
+#pragma unroll
+            for (int nb = 0; nb < NBW; ++nb) {
+                const int pix = (wp * NBW + nb) * 16 + j;
+                const int row = pix / WO, col = pix - (pix / WO) * WO;
+                const int o = ((img * a.K + mblk + wk * 16 + 4 * g) * WO + oh0 + row) * WO + col;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) pyy[nb][i] = a.bnb.y[o + i * WO * WO];
+                if (zmask)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) pzz[nb][i] = a.bnb.z[o + i * WO * WO];
+            }
+        }
+    }
     for (int q = 0; q < TPW; ++q) {
     const int tl = blockIdx.x * TPW + q;
     const int img = tl / tiles;
@@ -303,8 +324,13 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
         for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                yy[nb][i] = a.bnb.y[oidx[nb] + i * cstr];
-                zz[nb][i] = zmask ? a.bnb.z[oidx[nb] + i * cstr] : 1.f;
+                if constexpr (PRE) {
+                    yy[nb][i] = pyy[nb][i];
+                    zz[nb][i] = zmask ? pzz[nb][i] : 1.f;
+                } else {
+                    yy[nb][i] = a.bnb.y[oidx[nb] + i * cstr];
+                    zz[nb][i] = zmask ? a.bnb.z[oidx[nb] + i * cstr] : 1.f;
+                }
             }
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
