@@ -1138,6 +1138,20 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
                 PSW_TRY(hipEventRecord(net->stage_ev[s], sb), "stage join");
                 PSW_TRY(hipStreamWaitEvent(sw, net->stage_ev[s], 0), "stage join");
             }
+            // consecutive convs of one shape whose partial sums the update
+            // reduces share a launch (each keeps its own operands and sums)
+            const float* gx[psw::kWgradGroupMax];
+            const float* gdy[psw::kWgradGroupMax];
+            float* gpart[psw::kWgradGroupMax];
+            int gn = 0;
+            psw::ConvShape gcs{};
+            auto flush = [&]() -> hipError_t {
+                if (gn == 0) return hipSuccess;
+                kind = PSW_PROF_CONV_BWD_WEIGHT;
+                const int m = gn;
+                gn = 0;
+                return psw::conv_bwd_weight_partials_group(gcs, gx, gdy, gpart, m, bf16, sw);
+            };
             for (int j = net->stage_end[s] - 1; j >= net->stage_begin[s]; --j) {
                 const psw_layer& c = net->ops[j];
                 if (c.kind != PSW_OP_CONV) continue;
@@ -1146,14 +1160,22 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
                 check_conv(ca.n, ca.c, ca.h, ca.w, c.cout, c.k, c.k, c.stride, c.pad, net->prec, &ccs);
                 float* dw = is.gptr(j);
                 float* db = (c.flags & PSW_F_BIAS) ? dw + (int64_t)c.cout * c.cin * c.k * c.k : nullptr;
-                kind = PSW_PROF_CONV_BWD_WEIGHT;
-                if (net->wpart_splits[j] > 0)  // reduced by the stage update below
-                    PSW_TRY(psw::conv_bwd_weight_partials(ccs, is.act(c.in0), is.grd(j + 1), is.wpart(j), bf16, sw),
-                            "conv_bwd_weight");
-                else
+                if (net->wpart_splits[j] > 0) {  // reduced by the stage update below
+                    if (gn > 0 && (gn == psw::kWgradGroupMax || memcmp(&gcs, &ccs, sizeof ccs) != 0))
+                        PSW_TRY(flush(), "conv_bwd_weight");
+                    gcs = ccs;
+                    gx[gn] = is.act(c.in0);
+                    gdy[gn] = is.grd(j + 1);
+                    gpart[gn] = is.wpart(j);
+                    ++gn;
+                } else {
+                    PSW_TRY(flush(), "conv_bwd_weight");
+                    kind = PSW_PROF_CONV_BWD_WEIGHT;
                     PSW_TRY(psw::conv_bwd_weight(ccs, is.act(c.in0), is.grd(j + 1), dw, db, bf16, wsw, wswb, sw),
                             "conv_bwd_weight");
+                }
             }
+            PSW_TRY(flush(), "conv_bwd_weight");
             kind = PSW_PROF_SGD;
             psw::SgdSeg segs[64];
             const auto& proto = net->sgd_segs[s];

@@ -394,6 +394,13 @@ hipError_t conv_bwd_weight_partials(const ConvShape& cs, const float* x, const f
     return conv3x3_wgrad(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, part, st);
 }
 
+hipError_t conv_bwd_weight_partials_group(const ConvShape& cs, const float* const* x, const float* const* dy,
+                                          float* const* part, int count, int bf16, hipStream_t st)
+{
+    if (!use_direct_wgrad(cs, bf16)) return hipErrorNotSupported;
+    return conv3x3_wgrad_group(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, part, count, st);
+}
+
 hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy, float* dw, float* db, int bf16,
                            void* ws, size_t ws_bytes, hipStream_t st)
 {

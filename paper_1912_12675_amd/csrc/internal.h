@@ -160,6 +160,11 @@ hipError_t bn_bwd_from_partials(int n, int c, int h, int w, const float* dz, con
 int conv3x3_wgrad_splits(int n, int C, int H, int W, int K, int stride);
 hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const float* x, const float* dy, float* part,
                          hipStream_t st);
+// The same for `count` (<= kWgradGroupMax) convolutions of one shape in one
+// launch: member i reads x[i], dy[i] and writes its partial sums to part[i].
+constexpr int kWgradGroupMax = 8;
+hipError_t conv3x3_wgrad_group(int n, int C, int H, int W, int K, int stride, const float* const* x,
+                               const float* const* dy, float* const* part, int count, hipStream_t st);
 hipError_t conv_fwd(const ConvShape& cs, const float* x, const float* w, const float* bias, int relu,
                     float* y, int bf16, hipStream_t st);
 hipError_t conv_bwd_data(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate,
@@ -174,6 +179,9 @@ hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy,
 int conv_bwd_weight_part_splits(const ConvShape& cs, int bf16);
 hipError_t conv_bwd_weight_partials(const ConvShape& cs, const float* x, const float* dy, float* part, int bf16,
                                     hipStream_t st);
+// The same for `count` convolutions of shape cs in one launch.
+hipError_t conv_bwd_weight_partials_group(const ConvShape& cs, const float* const* x, const float* const* dy,
+                                          float* const* part, int count, int bf16, hipStream_t st);
 
 // ---- batch norm (+ residual) (+ ReLU) ----
 size_t bn_ws_bytes(int n, int c, int h, int w);

@@ -7,6 +7,9 @@
 // A workgroup reduces over TPW consecutive (image, TH-row band) tiles and
 // writes one dW-shaped partial sum; the partials are added in a fixed order
 // by the reduction kernel of conv.hip, so the result is bit-reproducible.
+// One launch may cover several convolutions of the same shape (the
+// same-shape layers of a pipeline stage): blockIdx.x / splits selects the
+// convolution, and each has its own operands and partial sums.
 // blockIdx.y selects a group of CBW 16-channel input blocks and blockIdx.z a
 // group of KBW 16-channel output blocks.  In the
 // workgroup, wave (kb, cb, wpx) owns the 16x16 output blocks (output channels
@@ -33,10 +36,11 @@ namespace {
 typedef float v4f __attribute__((ext_vector_type(4)));
 
 struct WgArgs {
-    const float* x;   // [n][C][H][W]
-    const float* dy;  // [n][K][HO][WO]
-    float* part;      // [gridDim.x][K][C][9]
+    const float* x[kWgradGroupMax];   // member i: [n][C][H][W]
+    const float* dy[kWgradGroupMax];  // [n][K][HO][WO]
+    float* part[kWgradGroupMax];      // [splits][K][C][9]
     int n, C, H, W, K, HO;
+    int splits;                       // workgroups (partial sums) per member
 };
 
 // smallest v >= lo with v % 32 == 2
@@ -74,6 +78,10 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int kb = wave % KBW, cb = (wave / KBW) % CBW, wpx = wave / (KBW * CBW);
     const int g = lane >> 4, j = lane & 15;
+    const int mem = blockIdx.x / a.splits;          // member of the group
+    const int bx = blockIdx.x - mem * a.splits;     // partial-sum index within it
+    const float* gx = a.x[mem];
+    const float* gdy = a.dy[mem];
     const int bands = a.HO / TH;         // row bands per image
     const int cbase = blockIdx.y * CCH;  // first input channel of this workgroup
     const int kbase = blockIdx.z * KC;   // first output channel of this workgroup
@@ -94,7 +102,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
     constexpr int DV = (DN4 + NT - 1) / NT, XV = (XN4 + NT - 1) / NT;
     float4 dr[DV], xr[XV];
     auto load_chunk = [&](int ch) {
-        const int tl = blockIdx.x * TPW + ch / (TH / RC);
+        const int tl = bx * TPW + ch / (TH / RC);
         const int img = tl / bands;
         const int oh0 = (tl - img * bands) * TH + (ch % (TH / RC)) * RC;
         const int ih0 = oh0 * STRIDE - 1;
@@ -105,7 +113,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
             if (i4 < DN4) {
                 const int i = i4 * 4;
                 const int k = i / NPC, pix = i - (i / NPC) * NPC;
-                val = *reinterpret_cast<const float4*>(a.dy + (((size_t)img * a.K + kbase + k) * a.HO + oh0) * WO + pix);
+                val = *reinterpret_cast<const float4*>(gdy + (((size_t)img * a.K + kbase + k) * a.HO + oh0) * WO + pix);
             }
             dr[v] = val;
         }
@@ -120,7 +128,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
                 const int rr = rem / WIN, iw = rem - (rem / WIN) * WIN;
                 const int ih = ih0 + rr;
                 if (ih >= 0 && ih < a.H && cbase + c < a.C)
-                    val = *reinterpret_cast<const float4*>(a.x + (((size_t)img * a.C + cbase + c) * a.H + ih) * WIN + iw);
+                    val = *reinterpret_cast<const float4*>(gx + (((size_t)img * a.C + cbase + c) * a.H + ih) * WIN + iw);
             }
             xr[v] = val;
         }
@@ -196,7 +204,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
         }
     }
     // D lane l, register i: output channel kb*16 + 4g + i, input channel cb*16 + j
-    float* out = a.part + (size_t)blockIdx.x * a.K * a.C * 9;
+    float* out = a.part[mem] + (size_t)bx * a.K * a.C * 9;
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
         const int k = kbase + kb * 16 + 4 * g + i, c = cbase + cb * 16 + j;
@@ -235,19 +243,28 @@ int conv3x3_wgrad_splits(int n, int C, int H, int W, int K, int stride)
     }
 }
 
-hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const float* x, const float* dy, float* part,
-                         hipStream_t st)
+hipError_t conv3x3_wgrad_group(int n, int C, int H, int W, int K, int stride, const float* const* x,
+                               const float* const* dy, float* const* part, int count, hipStream_t st)
 {
     const int cfg = wgrad_config(n, C, H, W, K, stride);
-    if (!cfg) return hipErrorNotSupported;
-    if ((uintptr_t)x % 16 || (uintptr_t)dy % 16) return hipErrorNotSupported;  // float4 staging
-    WgArgs a{x, dy, part, n, C, H, W, K, H / stride};
+    if (!cfg || count < 1 || count > kWgradGroupMax) return hipErrorNotSupported;
+    WgArgs a{};
+    for (int i = 0; i < count; ++i) {
+        if ((uintptr_t)x[i] % 16 || (uintptr_t)dy[i] % 16) return hipErrorNotSupported;  // float4 staging
+        a.x[i] = x[i];
+        a.dy[i] = dy[i];
+        a.part[i] = part[i];
+    }
+    a.n = n; a.C = C; a.H = H; a.W = W; a.K = K; a.HO = H / stride;
     const int splits = conv3x3_wgrad_splits(n, C, H, W, K, stride);
+    a.splits = splits;
     const int cgroups = (C + 15) / 16;  // one 16-channel block per workgroup (grid.y)
     // output-channel groups: configurations 2 and 3 split K over the grid
     const int kgroups = cfg == 2 ? K / 16 : cfg == 3 ? K / 32 : 1;
-    const dim3 grid(splits, cgroups, kgroups);
-    const Work wk = conv_work(n, C, H, W, K, 3, 3, H / stride, W / stride);
+    const dim3 grid(splits * count, cgroups, kgroups);
+    Work wk = conv_work(n, C, H, W, K, 3, 3, H / stride, W / stride);
+    wk.flops *= count;
+    wk.bytes *= count;
     switch (cfg) {
     case 6:
     case 1:
@@ -272,6 +289,12 @@ hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const fl
         break;
     }
     return hipGetLastError();
+}
+
+hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const float* x, const float* dy, float* part,
+                         hipStream_t st)
+{
+    return conv3x3_wgrad_group(n, C, H, W, K, stride, &x, &dy, &part, 1, st);
 }
 
 }  // namespace psw
