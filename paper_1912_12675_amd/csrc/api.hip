@@ -293,6 +293,13 @@ struct psw_net {
     std::vector<char> fused_now;            // per conv op: the fused kernel ran in the current step
     std::vector<char> fuse_bwd;             // per conv op: its input's BN (op-1) backward sums come from its dgrad
     std::vector<char> fused_bwd_now;        // per conv op: the fused dgrad ran in the current step
+    // per BN op without residual: its backward is folded into the convs
+    // around it (the next conv's dgrad writes its per-tile sums to the op's
+    // own region at fold_off from fold_base in the shared set, and the
+    // previous conv's dgrad merges them and forms dy while staging)
+    std::vector<char> fold_bn, folded_now;
+    std::vector<size_t> fold_off;
+    size_t fold_base = 0, fold_bytes = 0;
 
     std::vector<char> grad_accum;           // per op input slot: 0 overwrite, 1 accumulate (in0, in1)
     size_t step_bytes = 0;                  // one step set (activations, saves, gradients, forward ws)
@@ -593,6 +600,33 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
             ws = std::max(ws, psw::fc_bwd_ws_bytes(a.n, o.cin, o.cout));
         }
     }
+    // BN backward folded into the neighbouring convs' backward-data kernels:
+    // a BN without residual between two stride-1 direct-kernel convs of its
+    // own stage whose gradient it writes once (fp32)
+    net->fold_bn.assign(n_layers, 0);
+    net->folded_now.assign(n_layers, 0);
+    net->fold_off.assign(n_layers, 0);
+    size_t fold = 0;
+    for (int i = 1; i + 1 < n_layers; ++i) {
+        const psw_layer& o = net->ops[i];
+        const psw_layer& pc = net->ops[i - 1];
+        const psw_layer& nc = net->ops[i + 1];
+        if (o.kind != PSW_OP_BN || o.in1 >= 0 || o.in0 != i || prec != PSW_FP32) continue;
+        if (pc.kind != PSW_OP_CONV || pc.in0 <= 0 || (pc.flags & PSW_F_RELU)) continue;
+        if (!net->fuse_bwd[i + 1] || nc.stride != 1 || net->grad_accum[2 * i]) continue;
+        if (net->stage_of[i - 1] != net->stage_of[i] || net->stage_of[i + 1] != net->stage_of[i]) continue;
+        const Tensor a = net->t[pc.in0];
+        psw::ConvShape cs;
+        check_conv(a.n, a.c, a.h, a.w, pc.cout, pc.k, pc.k, pc.stride, pc.pad, prec, &cs);
+        if (!psw::conv_bwd_data_fold_ok(cs)) continue;
+        const Tensor z = net->t[i + 1];
+        psw::ConvShape ncs;
+        check_conv(z.n, z.c, z.h, z.w, nc.cout, nc.k, nc.k, nc.stride, nc.pad, prec, &ncs);
+        net->fold_bn[i] = 1;
+        net->fold_off[i] = fold;  // per-tile sums [c][T][2]
+        fold = align256(fold + (size_t)psw::conv_bwd_data_bnsums_tiles(ncs) * o.cin * 2 * sizeof(float));
+    }
+    net->fold_bytes = fold;
     // split partial sums of the conv weight gradients, reduced by the stage update
     net->wpart_splits.assign(n_layers, 0);
     net->wpart_off.assign(n_layers, 0);
@@ -647,6 +681,8 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
     off += net->wsw_bytes;
     net->wpart_base = off;
     off += wpart;
+    net->fold_base = off;
+    off += net->fold_bytes;
     net->arena_bytes = net->step_bytes + off;
     g_err.clear();
     return PSW_OK;
@@ -879,6 +915,7 @@ struct Issue {
     void* wsb() const { return net->arena + net->step_bytes + net->ws_off; }
     void* wsw() const { return net->arena + net->step_bytes + net->wsw_off; }
     float* wpart(int i) const { return (float*)(net->arena + net->step_bytes + net->wpart_base + net->wpart_off[i]); }
+    float* fold_part(int i) const { return (float*)(net->arena + net->step_bytes + net->fold_base + net->fold_off[i]); }
     const float* wfwd(int i) const
     {
         const int s = net->stage_of[i];
@@ -1046,6 +1083,32 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
             if (o.flags & PSW_F_RELU) PSW_TRY(psw::relu_mask(y.numel(), is.act(i + 1), g, sb), "relu_mask");
             kind = PSW_PROF_CONV_BWD_DATA;
             net->fused_bwd_now[i] = 0;
+            // BN op i+1 folded: this dgrad forms its input g (the BN's input
+            // gradient, also written out) from that BN's output gradient
+            const bool fold_in = i + 1 < L && net->folded_now[i + 1];
+            psw::BnFold fold;
+            if (fold_in) {
+                const psw_layer& fb = net->ops[i + 1];
+                const psw_layer& nc = net->ops[i + 2];
+                const Tensor z = net->t[i + 2];
+                psw::ConvShape ncs;
+                check_conv(z.n, z.c, z.h, z.w, nc.cout, nc.k, nc.k, nc.stride, nc.pad, net->prec, &ncs);
+                const float* fsave = is.save(i + 1);
+                float* dgb = is.gptr(i + 1);
+                fold.g = is.grd(i + 2);
+                fold.y = is.act(i + 1);
+                fold.part = is.fold_part(i + 1);
+                fold.T = psw::conv_bwd_data_bnsums_tiles(ncs);
+                fold.count = (double)y.n * y.h * y.w;
+                fold.gamma = is.wbwd(i + 1);
+                fold.mean = fsave;
+                fold.invstd = fsave + fb.cin;
+                fold.scale = fsave + 2 * fb.cin;
+                fold.relu = (fb.flags & PSW_F_RELU) != 0;
+                fold.dy = g;
+                fold.dgamma = dgb;
+                fold.dbeta = dgb + fb.cin;
+            }
             if (din && net->fuse_bwd[i]) {  // BN op i-1's backward sums out of this dgrad
                 const psw_layer& bo = net->ops[i - 1];
                 const float* bsave = is.save(i - 1);
@@ -1055,17 +1118,26 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
                     bnb.scale = bsave + 2 * bo.cin;
                     bnb.shift = bsave + 3 * bo.cin;
                 }
-                e = psw::conv_bwd_data_bnsums(cs, is.wbwd(i), g, din, acc0, bnb, sb);
+                if (net->fold_bn[i - 1]) bnb.part = is.fold_part(i - 1);  // merged by the dgrad of op i-2
+                e = fold_in ? psw::conv_bwd_data_fold(cs, is.wbwd(i), din, acc0, &bnb, fold, sb)
+                            : psw::conv_bwd_data_bnsums(cs, is.wbwd(i), g, din, acc0, bnb, sb);
                 if (e == hipSuccess)
                     net->fused_bwd_now[i] = 1;
                 else if (e != hipErrorNotSupported)  // not supported: nothing launched, unfused path below
                     PSW_TRY(e, "conv_bwd_data_bnsums");
             }
-            if (din && !net->fused_bwd_now[i])
-                PSW_TRY(psw::conv_bwd_data(cs, is.wbwd(i), g, din, acc0, bf16, sb), "conv_bwd_data");
+            if (i >= 1) net->folded_now[i - 1] = net->fused_bwd_now[i] && net->fold_bn[i - 1];
+            if (din && !net->fused_bwd_now[i]) {
+                if (fold_in)  // covered by construction (the fold's conditions when the net was created)
+                    PSW_TRY(psw::conv_bwd_data_fold(cs, is.wbwd(i), din, acc0, nullptr, fold, sb),
+                            "conv_bwd_data (folded BN backward)");
+                else
+                    PSW_TRY(psw::conv_bwd_data(cs, is.wbwd(i), g, din, acc0, bf16, sb), "conv_bwd_data");
+            }
             break;
         }
         case PSW_OP_BN: {
+            if (net->folded_now[i]) break;  // done by the dgrads of ops i+1 (sums) and i-1 (dy)
             const float* save = is.save(i);
             const Tensor r = o.in1 >= 0 ? net->t[o.in1] : Tensor{0, 0, 0, 0};
             float* dres = o.in1 > 0 ? is.grd(o.in1) : nullptr;

@@ -372,6 +372,22 @@ hipError_t conv_bwd_data_bnsums(const ConvShape& cs, const float* w, const float
     return conv3x3_dgrad_s2(cs.n, cs.c, cs.h, cs.w, cs.k, w, dy, dx, accumulate, st, &bnb);
 }
 
+bool conv_bwd_data_fold_ok(const ConvShape& cs)
+{
+    return cs.r == 3 && cs.s == 3 && cs.pad == 1 && cs.stride == 1 && cs.k <= kFoldMaxChannels &&
+           (cs.k & (cs.k - 1)) == 0 && conv3x3_direct_covers(cs.n, cs.k, cs.h, cs.w, cs.c, 1, true);
+}
+
+hipError_t conv_bwd_data_fold(const ConvShape& cs, const float* w, float* dx, int accumulate, const BnBwdFuse* bnb,
+                              const BnFold& fold, hipStream_t st)
+{
+    if (!conv_bwd_data_fold_ok(cs)) return hipErrorNotSupported;
+    if (bnb && (conv_bwd_data_bnsums_tiles(cs) == 0 || (uintptr_t)bnb->z % 8 || (uintptr_t)bnb->y % 8))
+        return hipErrorNotSupported;
+    if ((uintptr_t)fold.g % 16 || (uintptr_t)fold.y % 16) return hipErrorNotSupported;
+    return conv3x3_direct(cs.n, cs.k, cs.h, cs.w, cs.c, 1, fold.dy, w, dx, accumulate, true, st, nullptr, bnb, &fold);
+}
+
 size_t conv_bwd_weight_ws_bytes(const ConvShape& cs, int bf16)
 {
     int z = wgrad_splits(cs, bf16);

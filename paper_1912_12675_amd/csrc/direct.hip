@@ -33,6 +33,7 @@ struct DirArgs {
     int accumulate;
     BnStatsFuse bn;  // bn.part == nullptr: no statistics
     BnBwdFuse bnb;   // bnb.part == nullptr: no backward sums (transposed kernel only)
+    BnFold fold;     // input formed from a folded BN backward (FOLD kernels only)
 };
 
 constexpr int round4(int v) { return (v + 3) / 4 * 4; }
@@ -79,9 +80,10 @@ constexpr int wrow(int n)
     return v;
 }
 
-template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, bool TRANS, int TPW>
+template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, bool TRANS, int TPW, bool FOLD>
 __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
 {
+    static_assert(!FOLD || (TRANS && STRIDE == 1 && TPW == 1), "folded BN backward: stride-1 backward data");
     constexpr int NT = 64 * WK * WP;
     constexpr int WIN = WO * STRIDE;                       // input width
     constexpr int HR = (TH - 1) * STRIDE + 3;              // staged input rows
@@ -94,6 +96,8 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     static_assert(CC * PS >= 2 * WP * TK, "input tile reused by the statistics epilogue");
     __shared__ __attribute__((aligned(16))) float Xs[CC * PS];
     __shared__ float Wc[TK * WR];
+    // folded BN backward: per input channel (a, b, d, mean, invstd, scale, shift)
+    __shared__ __attribute__((aligned(16))) float ftab[FOLD ? kFoldMaxChannels * 8 : 4];
 
     constexpr int tiles = WO / TH;       // row tiles per (square) image
     static_assert(WO % TH == 0, "row tiles");
@@ -167,6 +171,8 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     }
     float4 xr[XV];
     float4 wr[WV];
+    float4 fyr[FOLD ? XV : 1];  // folded BN: xr holds its output gradient, fyr its input
+    unsigned okm = 0;           // folded BN: bit k set when element k lies inside the tensor
     // Loads are issued without branches: a lane whose element lies outside
     // the tensor (halo rows, channels past C, threads past the chunk) loads
     // from offset 0 and keeps zero, so the compiler can count outstanding
@@ -174,12 +180,21 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     const bool wfast = wvec && (a.C % CC == 0);  // every weight run of every chunk is in range
     auto load_chunk = [&](int img, int ih0, int c0) {  // channels c0.. of tile (img, rows from ih0)
         const int xb = ((img * a.C + c0) * HIN + ih0) * WIN;
+        if constexpr (FOLD) okm = 0;
 #pragma unroll
         for (int k = 0; k < XV; ++k) {
             const int ih = ih0 + xrow[k];
             const bool ok = ((k + 1) * NT <= XN || xch[k] < CC) && ih >= 0 && ih < HIN && c0 + xch[k] < a.C;
-            const float4 v = *reinterpret_cast<const float4*>(a.x + (ok ? xb + xg[k] : 0));
-            xr[k] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+            if constexpr (FOLD) {
+                const float4 v = *reinterpret_cast<const float4*>(a.fold.g + (ok ? xb + xg[k] : 0));
+                const float4 u = *reinterpret_cast<const float4*>(a.fold.y + (ok ? xb + xg[k] : 0));
+                xr[k] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+                fyr[k] = ok ? u : make_float4(0.f, 0.f, 0.f, 0.f);
+                okm |= ok ? 1u << k : 0u;
+            } else {
+                const float4 v = *reinterpret_cast<const float4*>(a.x + (ok ? xb + xg[k] : 0));
+                xr[k] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
         }
         if (wfast) {
 #pragma unroll
@@ -219,10 +234,50 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
             wr[k] = v;
         }
     };
-    auto store_chunk = [&]() {
+    // folded BN: the staged tile's own rows (1..TH) of dy go to global memory
+    // after the barrier that follows the staging, so that the stores drain
+    // under the matrix loop instead of delaying the barrier
+    auto write_dy = [&](int img, int ih0, int c0) {
+        if constexpr (FOLD) {
+            if (blockIdx.y != 0) return;
+            const int xb = ((img * a.C + c0) * HIN + ih0) * WIN;
 #pragma unroll
-        for (int k = 0; k < XV; ++k)
-            if ((k + 1) * NT <= XN || xch[k] < CC) *reinterpret_cast<float4*>(&Xs[xl[k]]) = xr[k];
+            for (int k = 0; k < XV; ++k)
+                if ((okm & (1u << k)) && xrow[k] >= 1 && xrow[k] <= TH)
+                    *reinterpret_cast<float4*>(a.fold.dy + xb + xg[k]) = xr[k];
+        }
+    };
+    auto store_chunk = [&](int img, int ih0, int c0) {
+        (void)img;
+        (void)ih0;
+        if constexpr (FOLD) {  // the BN backward of each staged element, in the order of bn_bwd_partials_k
+#pragma unroll
+            for (int k = 0; k < XV; ++k) {
+                if (!((k + 1) * NT <= XN || xch[k] < CC)) continue;
+                float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+                if (okm & (1u << k)) {
+                    const float4 f0 = *reinterpret_cast<const float4*>(ftab + (c0 + xch[k]) * 8);
+                    const float4 f1 = *reinterpret_cast<const float4*>(ftab + (c0 + xch[k]) * 8 + 4);
+                    const float fa = f0.x, fb = f0.y, fd = f0.z, mu = f0.w, is = f1.x, sc = f1.y, sf = f1.z;
+                    const float gg[4] = {xr[k].x, xr[k].y, xr[k].z, xr[k].w};
+                    const float yy[4] = {fyr[k].x, fyr[k].y, fyr[k].z, fyr[k].w};
+                    float r[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float gm = (a.fold.relu && !(__fmaf_rn(yy[e], sc, sf) > 0.f)) ? 0.f : gg[e];
+                        const float xh = (yy[e] - mu) * is;
+                        r[e] = fa * (gm - fb - xh * fd);
+                    }
+                    o = make_float4(r[0], r[1], r[2], r[3]);
+                }
+                *reinterpret_cast<float4*>(&Xs[xl[k]]) = o;
+                xr[k] = o;  // written out by write_dy
+            }
+        } else {
+#pragma unroll
+            for (int k = 0; k < XV; ++k)
+                if ((k + 1) * NT <= XN || xch[k] < CC) *reinterpret_cast<float4*>(&Xs[xl[k]]) = xr[k];
+        }
 #pragma unroll
         for (int k = 0; k < WV; ++k) {
             if (!((k + 1) * NT * 4 <= WN4 * 4 || wc[k] >= 0)) continue;
@@ -245,6 +300,60 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     // across them: the first chunk of the next tile is loaded while the last
     // chunk of the current one is on the matrix cores
     load_chunk(blockIdx.x * TPW / tiles, (blockIdx.x * TPW % tiles) * TH * STRIDE - 1, 0);
+    if constexpr (FOLD) {
+        // merge the BN's per-tile sums while the first tile loads are in
+        // flight: G = NT / C consecutive threads per channel, thread q of a
+        // channel sums tiles q, q+G, ... in fp64, then the G partial sums
+        // meet in a fixed xor tree; the table is read after the first
+        // barrier below
+        const int G = NT / a.C;
+        const int ch = tid / G, q = tid - (tid / G) * G;
+        const float2* pp = reinterpret_cast<const float2*>(a.fold.part) + (size_t)ch * a.fold.T;
+        // tiles q, q+G, ... in that order: nf of them for every thread (16
+        // unconditional loads in flight at a time), then one more for the
+        // first T - nf*G threads
+        double s1 = 0.0, s2 = 0.0;
+        const int nf = a.fold.T / G;
+        int u = 0;
+        for (; u + 16 <= nf; u += 16) {
+            float2 v[16];
+#pragma unroll
+            for (int k = 0; k < 16; ++k) v[k] = pp[q + (u + k) * G];
+#pragma unroll
+            for (int k = 0; k < 16; ++k) {
+                s1 += (double)v[k].x;
+                s2 += (double)v[k].y;
+            }
+        }
+        for (; u < nf; ++u) {
+            const float2 v = pp[q + u * G];
+            s1 += (double)v.x;
+            s2 += (double)v.y;
+        }
+        if (q < a.fold.T - nf * G) {
+            const float2 v = pp[q + nf * G];
+            s1 += (double)v.x;
+            s2 += (double)v.y;
+        }
+        for (int off = G / 2; off > 0; off >>= 1) {
+            s1 += __shfl_xor(s1, off, G);
+            s2 += __shfl_xor(s2, off, G);
+        }
+        if (q == 0) {
+            const float is = a.fold.invstd[ch];
+            ftab[ch * 8 + 0] = (float)((double)a.fold.gamma[ch] * (double)is);
+            ftab[ch * 8 + 1] = (float)(s1 / a.fold.count);
+            ftab[ch * 8 + 2] = (float)(s2 / a.fold.count);
+            ftab[ch * 8 + 3] = a.fold.mean[ch];
+            ftab[ch * 8 + 4] = is;
+            ftab[ch * 8 + 5] = a.fold.relu ? a.fold.scale[ch] : 0.f;
+            ftab[ch * 8 + 6] = a.fold.relu ? a.fold.scale[a.C + ch] : 0.f;
+            if (blockIdx.x == 0 && blockIdx.y == 0) {
+                a.fold.dbeta[ch] = (float)s1;
+                a.fold.dgamma[ch] = (float)s2;
+            }
+        }
+    }
     // backward sums with one tile per workgroup: the BN tensors the epilogue
     // reads are loaded now, so that their latency passes under the matrix work
     constexpr bool PRE = TRANS && TPW == 1;
@@ -272,8 +381,9 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     const int oh0 = (tl - img * tiles) * TH;
     for (int c0 = 0; c0 < a.C; c0 += CC) {
         __syncthreads();  // the previous chunk's LDS reads are complete
-        store_chunk();
+        store_chunk(img, oh0 * STRIDE - 1, c0);
         __syncthreads();
+        write_dy(img, oh0 * STRIDE - 1, c0);
         if (c0 + CC < a.C)
             load_chunk(img, oh0 * STRIDE - 1, c0 + CC);
         else if (q + 1 < TPW)
@@ -716,14 +826,23 @@ hipError_t launch_direct(const DirArgs& a, int n, bool trans, hipStream_t st)
     // as a convolution: input a.C x a.H x WO*STRIDE, output a.K x a.HO x WO
     Work wk = conv_work(n, a.C, a.H, WO * STRIDE, a.K, 3, 3, a.HO, WO);
     const double out_bytes = kF * n * (double)a.K * a.HO * WO;
+    const double in_bytes = kF * n * (double)a.C * a.H * a.H;
     if (a.accumulate) wk.bytes += out_bytes;        // the existing output is read
     if (a.bnb.part) wk.bytes += (a.bnb.scale ? 1.0 : 2.0) * out_bytes;  // BN input (and output) for the sums
-    if (trans)
-        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW), wk,
-                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW>), grid, block, 0, st, a);
-    else
-        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, false, TPW), wk,
-                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, false, TPW>), grid, block, 0, st, a);
+    if (a.fold.g) wk.bytes += 2.0 * in_bytes;       // folded BN: g and y read instead of dy, dy written
+    if (trans && a.fold.g) {
+        if constexpr (STRIDE == 1 && TPW == 1)
+            PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, true), wk,
+                       (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, true>), grid, block, 0, st, a);
+        else
+            return hipErrorNotSupported;
+    } else if (trans) {
+        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, false), wk,
+                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, false>), grid, block, 0, st, a);
+    } else {
+        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, false, TPW, false), wk,
+                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, false, TPW, false>), grid, block, 0, st, a);
+    }
     return hipGetLastError();
 }
 
@@ -744,10 +863,29 @@ int conv3x3_direct_tiles(int n, int C, int H, int W, int K, int stride)
     return 0;
 }
 
+bool conv3x3_direct_covers(int n, int C, int H, int W, int K, int stride, bool transpose)
+{
+    if (stride != 1 && stride != 2) return false;
+    if (H % stride || W % stride || H != W) return false;
+    if ((int64_t)n * C * H * W > INT32_MAX || (int64_t)n * K * (H / stride) * (W / stride) > INT32_MAX) return false;
+    const int HO = H / stride, WO = W / stride;
+    if (C <= 4 && stride == 1 && !transpose) return WO == 32 && HO % 8 == 0 && K % 16 == 0;
+    if (C % 16) return false;
+    if (stride == 1)
+        return (WO == 32 && HO % 8 == 0 && K % 16 == 0) || (WO == 16 && HO % 8 == 0 && K % 32 == 0) ||
+               (WO == 8 && HO % 8 == 0 && K % 32 == 0);
+    if (transpose) return false;
+    return (WO == 16 && HO % 8 == 0 && K % 32 == 0) || (WO == 8 && HO % 8 == 0 && K % 32 == 0);
+}
+
 hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const float* x, const float* w, float* y,
-                          int accumulate, bool transpose, hipStream_t st, const BnStatsFuse* bn, const BnBwdFuse* bnb)
+                          int accumulate, bool transpose, hipStream_t st, const BnStatsFuse* bn, const BnBwdFuse* bnb,
+                          const BnFold* fold)
 {
     if (bnb && (!transpose || stride != 1)) return hipErrorNotSupported;
+    if (fold && (!transpose || stride != 1 || C > kFoldMaxChannels || (C & (C - 1)) || !fold->g || !fold->y ||
+                 !fold->dy || !fold->part || (uintptr_t)fold->part % 8))
+        return hipErrorNotSupported;
     if (stride != 1 && stride != 2) return hipErrorNotSupported;
     if (H % stride || W % stride || H != W) return hipErrorNotSupported;  // square images (compile-time strides)
     // 32-bit element offsets inside the kernel
@@ -756,9 +894,10 @@ hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const f
     if (bn && transpose) return hipErrorNotSupported;
     if ((uintptr_t)x % 16) return hipErrorNotSupported;  // float4 tile staging
     const int HO = H / stride, WO = W / stride;
-    DirArgs a{x, w, y, C, H, K, HO, accumulate, BnStatsFuse{nullptr}, BnBwdFuse{}};
+    DirArgs a{x, w, y, C, H, K, HO, accumulate, BnStatsFuse{nullptr}, BnBwdFuse{}, BnFold{}};
     if (bn) a.bn = *bn;
     if (bnb) a.bnb = *bnb;
+    if (fold) a.fold = *fold;
     if (C <= 4 && stride == 1 && !transpose) {  // first layer of an image net (3 input channels)
         if (WO == 32 && HO % 8 == 0 && K % 16 == 0) return launch_direct<32, 1, 8, 4, 1, 4, 4>(a, n, false, st);
         return hipErrorNotSupported;

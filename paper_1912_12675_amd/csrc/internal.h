@@ -113,6 +113,34 @@ struct BnBwdFuse {
     const float* shift = nullptr;
 };
 
+// Backward of a BN without residual folded into the staging of the
+// backward-data conv that reads its result.  Every workgroup first merges the
+// BN's per-tile sums part[c][T][2] (written by the next conv's backward-data
+// epilogue, see BnBwdFuse) in a fixed order in fp64 into, per channel,
+// a = gamma*invstd, b = mean g', d = mean g'*xhat (workgroup 0 also writes
+// dbeta = sum g' and dgamma = sum g'*xhat); then the conv's input
+// dy = a*(g' - b - xhat*d) is formed per element while staging, from the BN
+// output gradient g (g' = g masked by the ReLU, the mask recomputed as
+// fmaf(y, scale, shift) > 0) and the BN input y, xhat = (y - mean)*invstd.
+// The rows a workgroup owns are also written to dy, which the weight
+// gradient reads.  The channel count must be a power of two.
+struct BnFold {
+    const float* g = nullptr;
+    const float* y = nullptr;
+    const float* part = nullptr;
+    int T = 0;                     // tiles (partials per channel)
+    double count = 0.0;            // elements per channel, n*h*w
+    const float* gamma = nullptr;
+    const float* mean = nullptr;
+    const float* invstd = nullptr;
+    const float* scale = nullptr;  // shift at scale + c; read when relu is set
+    int relu = 0;
+    float* dy = nullptr;
+    float* dgamma = nullptr;
+    float* dbeta = nullptr;
+};
+constexpr int kFoldMaxChannels = 128;
+
 // ---- convolution (implicit GEMM on MFMA) ----
 // Forward conv + fused BN statistics (direct kernel only); returns
 // hipErrorNotSupported when the shape has no direct configuration.
@@ -132,7 +160,9 @@ hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, co
 // when transpose is set); hipErrorNotSupported when no tile config fits.
 hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const float* x, const float* w, float* y,
                           int accumulate, bool transpose, hipStream_t st, const BnStatsFuse* bn = nullptr,
-                          const BnBwdFuse* bnb = nullptr);
+                          const BnBwdFuse* bnb = nullptr, const BnFold* fold = nullptr);
+// whether conv3x3_direct takes the shape (same arguments)
+bool conv3x3_direct_covers(int n, int C, int H, int W, int K, int stride, bool transpose);
 // number of pixel tiles (workgroups along x) of the direct forward kernel, 0 if none
 int conv3x3_direct_tiles(int n, int C, int H, int W, int K, int stride);
 // Backward-data of a 3x3 / pad 1 / stride 2 conv (layer channels CL in, KL
@@ -145,6 +175,12 @@ int dgrad_bnsums_tiles(int n, int CL, int H, int W, int KL, int stride);
 int conv_bwd_data_bnsums_tiles(const ConvShape& cs);
 hipError_t conv_bwd_data_bnsums(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate,
                                 const BnBwdFuse& bnb, hipStream_t st);
+// Backward data whose input is formed from the preceding BN's folded
+// backward (fp32 stride-1 direct kernel only; conv_bwd_data_fold_ok says
+// whether the shape is covered); bnb, if set, as for conv_bwd_data_bnsums.
+bool conv_bwd_data_fold_ok(const ConvShape& cs);
+hipError_t conv_bwd_data_fold(const ConvShape& cs, const float* w, float* dx, int accumulate, const BnBwdFuse* bnb,
+                              const BnFold& fold, hipStream_t st);
 // BN backward (+ residual) from per-tile (sum g, sum g*xhat) partials:
 // merges them in a fixed order, writes dgamma, dbeta (block 0 of a channel)
 // and dy, and dres for an identity or option-A (2x subsampled, zero-padded
