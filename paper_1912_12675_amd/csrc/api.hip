@@ -601,8 +601,10 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
         }
     }
     // BN backward folded into the neighbouring convs' backward-data kernels:
-    // a BN without residual between two stride-1 direct-kernel convs of its
-    // own stage whose gradient it writes once (fp32)
+    // a BN (without residual, or with an identity residual whose gradient it
+    // writes first) after a stride-1 direct-kernel conv of its own stage,
+    // before a conv whose dgrad forms its sums, whose input gradient it
+    // writes once (fp32)
     net->fold_bn.assign(n_layers, 0);
     net->folded_now.assign(n_layers, 0);
     net->fold_off.assign(n_layers, 0);
@@ -611,10 +613,15 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
         const psw_layer& o = net->ops[i];
         const psw_layer& pc = net->ops[i - 1];
         const psw_layer& nc = net->ops[i + 1];
-        if (o.kind != PSW_OP_BN || o.in1 >= 0 || o.in0 != i || prec != PSW_FP32) continue;
+        if (o.kind != PSW_OP_BN || o.in0 != i || prec != PSW_FP32) continue;
+        if (o.in1 == 0) continue;  // the residual is the net input: no gradient to write
+        if (o.in1 > 0) {           // identity residual whose gradient this BN writes first
+            const Tensor r = net->t[o.in1], yb = net->t[i];
+            if (r.c != yb.c || r.h != yb.h || r.w != yb.w || net->grad_accum[2 * i + 1]) continue;
+        }
         if (pc.kind != PSW_OP_CONV || pc.in0 <= 0 || (pc.flags & PSW_F_RELU)) continue;
-        if (!net->fuse_bwd[i + 1] || nc.stride != 1 || net->grad_accum[2 * i]) continue;
-        if (net->stage_of[i - 1] != net->stage_of[i] || net->stage_of[i + 1] != net->stage_of[i]) continue;
+        if (!net->fuse_bwd[i + 1] || net->grad_accum[2 * i]) continue;
+        if (net->stage_of[i - 1] != net->stage_of[i]) continue;
         const Tensor a = net->t[pc.in0];
         psw::ConvShape cs;
         check_conv(a.n, a.c, a.h, a.w, pc.cout, pc.k, pc.k, pc.stride, pc.pad, prec, &cs);
@@ -1108,6 +1115,10 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
                 fold.dy = g;
                 fold.dgamma = dgb;
                 fold.dbeta = dgb + fb.cin;
+                if (fb.in1 >= 0) {  // identity residual: mask from z, g' to the residual's gradient
+                    fold.z = is.act(i + 2);
+                    fold.dres = is.grd(fb.in1);
+                }
             }
             if (din && net->fuse_bwd[i]) {  // BN op i-1's backward sums out of this dgrad
                 const psw_layer& bo = net->ops[i - 1];

@@ -80,7 +80,11 @@ constexpr int wrow(int n)
     return v;
 }
 
-template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, bool TRANS, int TPW, bool FOLD>
+// FOLD: 0 plain input; 1 input from a folded BN backward (no residual, ReLU
+// mask from the forward's scale and shift); 2 the same for a BN with an
+// identity residual (ReLU mask from the BN output z; the masked gradient
+// is also written to the residual's gradient)
+template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, bool TRANS, int TPW, int FOLD>
 __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
 {
     static_assert(!FOLD || (TRANS && STRIDE == 1 && TPW == 1), "folded BN backward: stride-1 backward data");
@@ -172,6 +176,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     float4 xr[XV];
     float4 wr[WV];
     float4 fyr[FOLD ? XV : 1];  // folded BN: xr holds its output gradient, fyr its input
+    float4 fzr[FOLD == 2 ? XV : 1];  // and fzr its output (ReLU mask) when it has a residual
     unsigned okm = 0;           // folded BN: bit k set when element k lies inside the tensor
     // Loads are issued without branches: a lane whose element lies outside
     // the tensor (halo rows, channels past C, threads past the chunk) loads
@@ -190,6 +195,10 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
                 const float4 u = *reinterpret_cast<const float4*>(a.fold.y + (ok ? xb + xg[k] : 0));
                 xr[k] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
                 fyr[k] = ok ? u : make_float4(0.f, 0.f, 0.f, 0.f);
+                if constexpr (FOLD == 2) {
+                    const float4 w = *reinterpret_cast<const float4*>(a.fold.z + (ok ? xb + xg[k] : 0));
+                    fzr[k] = ok ? w : make_float4(0.f, 0.f, 0.f, 0.f);
+                }
                 okm |= ok ? 1u << k : 0u;
             } else {
                 const float4 v = *reinterpret_cast<const float4*>(a.x + (ok ? xb + xg[k] : 0));
@@ -243,8 +252,10 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
             const int xb = ((img * a.C + c0) * HIN + ih0) * WIN;
 #pragma unroll
             for (int k = 0; k < XV; ++k)
-                if ((okm & (1u << k)) && xrow[k] >= 1 && xrow[k] <= TH)
+                if ((okm & (1u << k)) && xrow[k] >= 1 && xrow[k] <= TH) {
                     *reinterpret_cast<float4*>(a.fold.dy + xb + xg[k]) = xr[k];
+                    if constexpr (FOLD == 2) *reinterpret_cast<float4*>(a.fold.dres + xb + xg[k]) = fyr[k];
+                }
         }
     };
     auto store_chunk = [&](int img, int ih0, int c0) {
@@ -261,14 +272,21 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
                     const float fa = f0.x, fb = f0.y, fd = f0.z, mu = f0.w, is = f1.x, sc = f1.y, sf = f1.z;
                     const float gg[4] = {xr[k].x, xr[k].y, xr[k].z, xr[k].w};
                     const float yy[4] = {fyr[k].x, fyr[k].y, fyr[k].z, fyr[k].w};
-                    float r[4];
+                    float zz[4] = {1.f, 1.f, 1.f, 1.f};
+                    if constexpr (FOLD == 2) {
+                        zz[0] = fzr[k].x; zz[1] = fzr[k].y; zz[2] = fzr[k].z; zz[3] = fzr[k].w;
+                    }
+                    float r[4], gms[4];
 #pragma unroll
                     for (int e = 0; e < 4; ++e) {
-                        const float gm = (a.fold.relu && !(__fmaf_rn(yy[e], sc, sf) > 0.f)) ? 0.f : gg[e];
+                        const bool pass = FOLD == 2 ? zz[e] > 0.f : __fmaf_rn(yy[e], sc, sf) > 0.f;
+                        const float gm = (a.fold.relu && !pass) ? 0.f : gg[e];
                         const float xh = (yy[e] - mu) * is;
                         r[e] = fa * (gm - fb - xh * fd);
+                        gms[e] = gm;
                     }
                     o = make_float4(r[0], r[1], r[2], r[3]);
+                    if constexpr (FOLD == 2) fyr[k] = make_float4(gms[0], gms[1], gms[2], gms[3]);  // the residual's gradient
                 }
                 *reinterpret_cast<float4*>(&Xs[xl[k]]) = o;
                 xr[k] = o;  // written out by write_dy
@@ -829,19 +847,25 @@ hipError_t launch_direct(const DirArgs& a, int n, bool trans, hipStream_t st)
     const double in_bytes = kF * n * (double)a.C * a.H * a.H;
     if (a.accumulate) wk.bytes += out_bytes;        // the existing output is read
     if (a.bnb.part) wk.bytes += (a.bnb.scale ? 1.0 : 2.0) * out_bytes;  // BN input (and output) for the sums
-    if (a.fold.g) wk.bytes += 2.0 * in_bytes;       // folded BN: g and y read instead of dy, dy written
+    // folded BN: g and y (and z, and the residual's gradient written) instead of dy, dy written
+    if (a.fold.g) wk.bytes += (a.fold.dres ? 4.0 : 2.0) * in_bytes;
     if (trans && a.fold.g) {
-        if constexpr (STRIDE == 1 && TPW == 1)
-            PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, true), wk,
-                       (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, true>), grid, block, 0, st, a);
-        else
+        if constexpr (STRIDE == 1 && TPW == 1) {
+            if (a.fold.dres)
+                PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, 2), wk,
+                           (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, 2>), grid, block, 0, st, a);
+            else
+                PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, 1), wk,
+                           (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, 1>), grid, block, 0, st, a);
+        } else {
             return hipErrorNotSupported;
+        }
     } else if (trans) {
-        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, false), wk,
-                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, false>), grid, block, 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, 0), wk,
+                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, 0>), grid, block, 0, st, a);
     } else {
-        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, false, TPW, false), wk,
-                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, false, TPW, false>), grid, block, 0, st, a);
+        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, false, TPW, 0), wk,
+                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, false, TPW, 0>), grid, block, 0, st, a);
     }
     return hipGetLastError();
 }
@@ -884,7 +908,9 @@ hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const f
 {
     if (bnb && (!transpose || stride != 1)) return hipErrorNotSupported;
     if (fold && (!transpose || stride != 1 || C > kFoldMaxChannels || (C & (C - 1)) || !fold->g || !fold->y ||
-                 !fold->dy || !fold->part || (uintptr_t)fold->part % 8))
+                 !fold->dy || !fold->part || (uintptr_t)fold->part % 8 || (fold->dres && !fold->z) ||
+                 (uintptr_t)fold->g % 16 || (uintptr_t)fold->y % 16 || (uintptr_t)fold->z % 16 ||
+                 (uintptr_t)fold->dres % 16))
         return hipErrorNotSupported;
     if (stride != 1 && stride != 2) return hipErrorNotSupported;
     if (H % stride || W % stride || H != W) return hipErrorNotSupported;  // square images (compile-time strides)

@@ -123,7 +123,10 @@ struct BnBwdFuse {
 // output gradient g (g' = g masked by the ReLU, the mask recomputed as
 // fmaf(y, scale, shift) > 0) and the BN input y, xhat = (y - mean)*invstd.
 // The rows a workgroup owns are also written to dy, which the weight
-// gradient reads.  The channel count must be a power of two.
+// gradient reads.  For a BN with an identity residual (dres set) the ReLU
+// mask is z > 0 with z the BN output, and g' is written to dres (the
+// residual's gradient, overwritten).  The channel count must be a power of
+// two.
 struct BnFold {
     const float* g = nullptr;
     const float* y = nullptr;
@@ -138,6 +141,8 @@ struct BnFold {
     float* dy = nullptr;
     float* dgamma = nullptr;
     float* dbeta = nullptr;
+    const float* z = nullptr;      // BN output (residual BN only)
+    float* dres = nullptr;         // residual's gradient (residual BN only)
 };
 constexpr int kFoldMaxChannels = 128;
 
