@@ -22,9 +22,15 @@ Prints one JSON line.  `value` is images/s over the K timed steps.
 Measurement, in order: W warm-up steps (eager, including the pipeline
 fill), the graph capture and one untimed replay; the K timed steps (wall
 clock, no events); the other modes; then a profiling pass of min(K, 100)
-eager pipelined steps of the same workload in which every kernel is launched with a start / stop HIP event pair that the
-runtime stamps from the kernel's own dispatch (so the durations agree with a
-rocprofv3 kernel trace).  That pass gives the per-kernel table, the conv
+eager pipelined steps of the same workload in which every kernel is launched
+with a start / stop HIP event pair (hipExtLaunchKernelGGL).  The pair's time
+includes its own marker processing and dispatch, a few microseconds per
+launch that a rocprofv3 kernel trace does not count, different on each
+stream; every profiled step also launches one recorded empty kernel on each
+of its three streams, and every launch's time is the pair's time minus the
+empty kernels' mean on its stream (`event_overhead_us`; the raw pair times
+are reported beside as `avg_launch_us_events`).  That pass gives the
+per-kernel table, the conv
 matrix-core figure the metric names, and the dominant kernel (largest summed
 time): `roofline.achieved` = its algorithmic work per launch / its mean
 launch duration.  `roofline.traffic` is
@@ -56,6 +62,7 @@ PEAK_FP32_MFMA = 157.3   # TFLOP/s, MI355X dense fp32 matrix
 PEAK_BF16_MFMA = 2500.0  # TFLOP/s, MI355X dense bf16 matrix
 PEAK_HBM = 8000.0        # GB/s, MI355X HBM3E
 PROFILE_STEPS = 100
+STREAM_NAMES = {0: "chain", 1: "weight", 2: "forward"}  # stream ids of the profile timeline
 COPY_BYTES = 256 << 20
 
 
@@ -263,18 +270,41 @@ def main():
         torch.cuda.synchronize()
         others[name] = round(wl.batch * K / (time.perf_counter() - t1), 2)
 
-    # profiling pass over the same workload: every kernel launched with
-    # start / stop events stamped from its own dispatch
+    # profiling pass over the same workload (eager pipelined: graphs carry
+    # no events): every kernel launched with a start / stop event pair.  The
+    # pair's own cost (marker processing and dispatch, a few microseconds per
+    # launch, different on each stream) is measured beside the work: every
+    # step also launches one recorded empty kernel on each of its three
+    # streams, and each launch's time is its pair's time minus the mean pair
+    # time of the empty kernels on its stream.
     peak = PEAK_BF16_MFMA if wl.bf16 else PEAK_FP32_MFMA
-    kernels, breakdown, conv, roof = [], None, None, None
+    kernels, breakdown, conv, roof, ovh_us = [], None, None, None, None
     if KP:
         net.profile(True)
-        (run_sequential if args.mode == "sequential" else run_pipelined)(KP)  # graphs carry no events
+        run_pipelined(KP)
         torch.cuda.synchronize()
-        prof = net.profile_read()
-        kernels = net.profile_kernels()
+        spans = net.profile_timeline()
+        work = {k["name"]: k for k in net.profile_kernels()}
         net.profile(False)
-        breakdown = {k: round(v[0] / KP, 4) for k, v in prof.items() if v[1]}
+        probes = {}
+        for name, kind, sid, t0_, t1_ in spans:
+            if name == "empty_probe_k":
+                probes.setdefault(sid, []).append(t1_ - t0_)
+        ovh = {sid: sum(v) / len(v) for sid, v in probes.items()}
+        ovh_us = {STREAM_NAMES.get(sid, str(sid)): round(v, 3) for sid, v in sorted(ovh.items())}
+        agg, kinds = {}, {}
+        for name, kind, sid, t0_, t1_ in spans:
+            if name == "empty_probe_k":
+                continue
+            a_ = agg.setdefault(name, [0.0, 0.0, 0])
+            a_[0] += max(t1_ - t0_ - ovh[sid], 0.0) * 1e-3
+            a_[1] += (t1_ - t0_) * 1e-3
+            a_[2] += 1
+            kinds[kind] = kinds.get(kind, 0.0) + max(t1_ - t0_ - ovh[sid], 0.0) * 1e-3
+        kernels = sorted(({"name": n, "kind": work[n]["kind"], "launches": v[2], "ms": v[0], "ms_events": v[1],
+                           "flops": work[n]["flops"], "bytes": work[n]["bytes"]} for n, v in agg.items()),
+                         key=lambda k: -k["ms"])
+        breakdown = {k: round(v / KP, 4) for k, v in kinds.items()}
         ck = [k for k in kernels if k["kind"] in ("conv_fwd", "conv_bwd_data", "conv_bwd_weight")]
         conv_ms = sum(k["ms"] for k in ck) / KP
         conv_flop = sum(k["flops"] for k in ck) / KP
@@ -294,14 +324,19 @@ def main():
         roof = roofline_of(d, peak)
         roof["traffic"] = measured_traffic(d["name"])
         roof.update({"kernel": d["name"], "launches": d["launches"], "avg_launch_us": round(1e3 * d["ms"] / d["launches"], 3),
+                     "avg_launch_us_events": round(1e3 * d["ms_events"] / d["launches"], 3),
+                     "event_overhead_us": ovh_us,
                      "flop_per_launch": d["flops"] / d["launches"], "bytes_per_launch": d["bytes"] / d["launches"],
-                     "timed_over": f"{KP} steps of the same workload after the timed region, every kernel launched "
-                                   "with start/stop events stamped from its own dispatch"})
+                     "timed_over": f"{KP} pipelined steps of the same workload after the timed region, every "
+                                   "kernel launched with a start/stop event pair; avg_launch_us = the pair's time "
+                                   "minus event_overhead_us of its stream, the mean pair time of one empty kernel "
+                                   "per step and stream"})
     top = []
     for k in kernels[:10]:
         r = roofline_of(k, peak)
         top.append({"kernel": k["name"], "kind": k["kind"], "launches_per_step": k["launches"] / KP,
                     "us_per_step": round(1e3 * k["ms"] / KP, 2), "avg_launch_us": round(1e3 * k["ms"] / k["launches"], 3),
+                    "avg_launch_us_events": round(1e3 * k["ms_events"] / k["launches"], 3),
                     "bound": r["bound"], "achieved": r["achieved"], "unit": r["unit"], "frac": r["frac"],
                     "bytes_per_launch": k["bytes"] / k["launches"], "traffic": measured_traffic(k["name"])})
 

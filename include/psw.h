@@ -401,6 +401,16 @@ int psw_net_profile(psw_net *net, int enable);
 int psw_net_profile_only(psw_net *net, int enable, const char *kernel);
 int psw_net_profile_read(psw_net *net, int n_kinds, double *ms, int64_t *launches);
 int psw_net_profile_kernels(psw_net *net, int cap, psw_kernel_stat *out, int *n_out);
+/* While profiling is on, psw_pipeline_run also launches one such empty
+ * kernel on each of its three streams at the start of every step.
+ * psw_net_profile_probe: while profiling is on, launches n empty kernels
+ * (one workgroup of 64 threads, named "empty_probe_k", kind PSW_PROF_OTHER,
+ * no work) on `stream`, recorded like every other launch.  Their event
+ * time is what the event pair costs a launch that does nothing (marker
+ * processing and dispatch), the part of every recorded time that is not
+ * the kernel's execution; a caller running them beside the work it times
+ * can subtract it.  PSW_ERR_STATE when profiling is off; n in [0, 1024]. */
+int psw_net_profile_probe(psw_net *net, int n, void *stream);
 /* psw_net_profile_timeline: one psw_kernel_span per recorded launch, in
  * issue order (at most cap; *n_out = the record count): start and end in
  * microseconds after the first record's start, and the stream it ran on

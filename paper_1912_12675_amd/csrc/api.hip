@@ -1398,6 +1398,15 @@ int issue_pipeline(psw_net* net, int64_t t0, int n_steps, const int32_t* stalene
                   (float*)(P + net->pgrad_off)};
         for (int s = 0; s < S_; ++s) io.rv[s] = fwd_version(t, staleness[(size_t)i * S_ + s]);
         Issue is{net, io};
+        if (net->profiling) {  // one recorded empty kernel per stream and step (the chain's below): the event pair's own cost there
+            net->rec.kind = PSW_PROF_OTHER;
+            e = psw::empty_kernels(1, sf);
+            if (e == hipSuccess) e = psw::empty_kernels(1, sw);
+            if (e != hipSuccess) {
+                what = "pipeline: profile probe";
+                break;
+            }
+        }
         // forward of t: its step set is free once step t-NS is done with it
         // (the weight stream's last update of a step follows the chain's end)
         if (i >= NS) {
@@ -1423,6 +1432,10 @@ int issue_pipeline(psw_net* net, int64_t t0, int n_steps, const int32_t* stalene
         // backward of t after its forward
         e = hipEventRecord(net->fdone_ev, sf);
         if (e == hipSuccess) e = hipStreamWaitEvent(sb, net->fdone_ev, 0);
+        if (e == hipSuccess && net->profiling) {  // the chain's probe, where its kernels start
+            net->rec.kind = PSW_PROF_OTHER;
+            e = psw::empty_kernels(1, sb);
+        }
         if (e != hipSuccess) {
             what = "pipeline: backward order";
             break;
@@ -1607,6 +1620,17 @@ int psw_graph_destroy(psw_graph* g)
 int psw_net_profile(psw_net* net, int enable)
 {
     return psw_net_profile_only(net, enable, nullptr);
+}
+
+int psw_net_profile_probe(psw_net* net, int n, void* stream)
+{
+    if (!net) return fail(PSW_ERR_NULL, "net_profile_probe: net is NULL");
+    if (!net->profiling) return fail(PSW_ERR_STATE, "net_profile_probe: profiling is off");
+    if (n < 0 || n > 1024) return fail(PSW_ERR_SHAPE, "net_profile_probe: n = %d outside [0, 1024]", n);
+    net->rec.kind = PSW_PROF_OTHER;
+    RecorderScope rec_scope(&net->rec);
+    const hipError_t e = psw::empty_kernels(n, S(stream));
+    return e == hipSuccess ? PSW_OK : hip_check(e, "net_profile_probe");
 }
 
 int psw_net_profile_only(psw_net* net, int enable, const char* kernel)

@@ -224,6 +224,9 @@ hipError_t conv_bwd_weight_partials(const ConvShape& cs, const float* x, const f
 hipError_t conv_bwd_weight_partials_group(const ConvShape& cs, const float* const* x, const float* const* dy,
                                           float* const* part, int count, int bf16, hipStream_t st);
 
+// n launches of an empty kernel (event-overhead probe of the profiler)
+hipError_t empty_kernels(int n, hipStream_t st);
+
 // ---- batch norm (+ residual) (+ ReLU) ----
 size_t bn_ws_bytes(int n, int c, int h, int w);
 hipError_t bn_fwd(int n, int c, int h, int w, const float* y, const float* gamma, const float* beta,

@@ -224,3 +224,22 @@ def test_stage_step_requires_binding(psw):
     p = ctypes.c_void_p()
     assert L.psw_net_slot(h.value, 0, 0, ctypes.byref(p)) == -8
     L.psw_net_destroy(h.value)
+
+
+def test_profile_probe_argument_checks(psw):
+    """The event-overhead probe refuses a NULL net, a net that is not
+    profiling and a bad count before touching the GPU."""
+    wl = synth.resnet20_workload(batch=2)
+    L = psw.lib()
+    layers = psw._layers(wl.ops)
+    se = np.ascontiguousarray(wl.stage_end, dtype=np.int32)
+    rd = np.ascontiguousarray(wl.ring_depth(), dtype=np.int32)
+    h = ctypes.c_void_p()
+    assert L.psw_net_create(layers, len(layers), 2, *wl.in_shape, se.ctypes.data, 4, rd.ctypes.data, 0,
+                            ctypes.byref(h)) == 0
+    assert L.psw_net_profile_probe(None, 1, None) == -1
+    assert L.psw_net_profile_probe(h.value, 1, None) == -8  # profiling off
+    assert L.psw_net_profile(h.value, 1) == 0
+    assert L.psw_net_profile_probe(h.value, -1, None) == -2
+    assert L.psw_net_profile_probe(h.value, 1025, None) == -2
+    L.psw_net_destroy(h.value)
