@@ -509,3 +509,24 @@ def test_profile_probe_records_empty_kernels(P):
     probe = ks["empty_probe_k"]
     assert probe["launches"] == 5 and probe["flops"] == 0 and probe["bytes"] == 0 and probe["ms"] > 0
     assert any(k.startswith("conv3x3_direct") for k in ks)
+
+
+def test_bn_backward_folds_run(P):
+    """ResNet-20 folds 13 of its 19 BN backward passes into the backward-data
+    convs around them (7 without residual, 6 with an identity residual): a
+    profiled step launches those folded kernels and 6 BN backward kernels of
+    their own, and its weight gradients as 6 grouped launches."""
+    wl = synth.resnet20_workload(batch=8)
+    net = P.Net(wl.ops, 8, wl.in_shape, wl.stage_end, [4, 3, 2, 1])
+    net.load_params(synth.init_params(wl))
+    x, y = synth.batch(wl, 0, 8)
+    net.profile(True)
+    net.step(0, [3, 2, 1, 0], wl.lr, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), wl.momentum)
+    torch.cuda.synchronize()
+    ks = net.profile_kernels()
+    net.profile(False)
+    count = lambda pred: sum(k["launches"] for k in ks if pred(k["name"]))
+    assert count(lambda n: n.startswith("conv3x3_direct") and n.endswith("true, 1, 1>")) == 7
+    assert count(lambda n: n.startswith("conv3x3_direct") and n.endswith("true, 1, 2>")) == 6
+    assert count(lambda n: n.startswith(("bn_bwd_partials_k", "bn_bwd_apply"))) == 6
+    assert count(lambda n: n.startswith("conv3x3_wgrad")) == 6
