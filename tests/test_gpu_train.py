@@ -107,6 +107,10 @@ CASES = [
     # (workload factory, batch, steps)
     ("lenet5", lambda: synth.lenet5_workload(), 16, 1),
     ("resnet20_b8", lambda: synth.resnet20_workload(batch=8), 8, 10),
+    # batch 6: the folded BN merges' per-thread tile counts do not divide
+    # evenly at any layer (24, 12 and 6 tiles over 16, 16 and 8 threads), and
+    # the 8x8 weight gradients take the unsplit path (6 is not a multiple of 4)
+    ("resnet20_b6", lambda: synth.resnet20_workload(batch=6), 6, 8),
     ("resnet20_bf16_b8", lambda: synth.resnet20_workload(batch=8, bf16=True), 8, 6),
     ("alexnet_b4", lambda: synth.alexnet_workload(batch=4), 4, 4),
     ("vgg16_hybrid_b16", lambda: synth.vgg16_workload(batch=16, n_pipelined=3), 16, 5),
@@ -324,6 +328,8 @@ PIPE_CASES = [
                                                                     steps_per_epoch=0.03), 4, None, 8, [3, 5]),
     # no convolution anywhere: the step sets are freed through the chain's end
     ("mlp_conv_free", lambda: _mlp_workload(batch=8), 8, None, 9, [9]),
+    # uneven tile counts in the folded BN merges (see the batch-6 parity case)
+    ("resnet20_b6", lambda: synth.resnet20_workload(batch=6), 6, lambda t: [3, 2, 1, 0], 7, [3, 4]),
 ]
 
 
