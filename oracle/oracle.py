@@ -76,6 +76,8 @@ def _declare(L):
     L.orc_param_counts.restype = _I
     L.orc_shapes.argtypes = [_I, _i32, _I, _I, _I, _I, _I, _i32, _i32]
     L.orc_shapes.restype = _I
+    L.orc_train_from.argtypes = [_I, _i32, _I, _I, _I, _I, _I, _i32, _i64v, _I, _d, _d, _I, _I, _f, _i32, _i32, _d,
+                                 _D, _D, _I, _D, _D, _I, _I, _I, _d, _d, _d, _d, _d, _d, _i32, ctypes.c_uint64]
     L.orc_loss_and_grad.argtypes = [_I, _i32, _I, _I, _I, _I, _I, _i32, _d, _f, _i32, _D, _I,
                                     _d, _d, _d, ctypes.c_uint64, _i64v]
     L.orc_loss_and_grad.restype = _I
@@ -357,3 +359,69 @@ def train(ops, in_shape, stage_end, params0, xs, labels, staleness, lr, mom=0.9,
         raise ValueError(f"oracle rejected the run (code {rc})")
     return dict(params=out, momentum=momb, run_mean=rm[:n_bn], run_var=rv[:n_bn], losses=losses,
                 versions=versions)
+
+
+def train_from(ops, in_shape, stage_end, t0, hist0, mom0, xs, labels, staleness, lr, mom=0.9, wd=0.0,
+               nesterov=False, bn_eps=1e-5, bn_mom=0.1, bf16=False, stash=False, dropout_seed=0,
+               run_mean=None, run_var=None, out_depth=1):
+    """Resume the stale-weight schedule from a checkpoint at step t0 and run
+    len(xs) steps (t0 .. t0+T-1; batch i is step t0+i's).
+
+    hist0: [S][depth] list of per-stage packed parameter vectors, versions
+    t0-depth+1 .. t0 (entries of negative versions may be None); mom0: the
+    concatenated momentum at t0 (None: zero); run_mean / run_var: the
+    running statistics at t0 (None: mean 0, var 1).  staleness [T, S]; lr
+    scalar, [S] or [T, S].  Returns a dict with `history` ([S][out_depth]
+    vectors W_s^(t0+T-out_depth+1) .. W_s^(t0+T), None below version 0),
+    `params` (W^(t0+T) concatenated), `momentum`, `grad` (the last step's
+    gradient), `run_mean`, `run_var`, `losses` and `versions`."""
+    ops = _desc(ops)
+    se = np.ascontiguousarray(stage_end, dtype=np.int32)
+    S = len(se)
+    counts = param_counts(ops, in_shape, 1, stage_end)
+    depth = len(hist0[0])
+    assert all(len(h) == depth for h in hist0), "every stage needs the same number of versions"
+    packed = np.zeros(depth * int(sum(counts)))
+    o = 0
+    for s in range(S):
+        for k in range(depth):
+            v = hist0[s][k]
+            if v is not None:
+                packed[o + k * counts[s]:o + (k + 1) * counts[s]] = np.asarray(v, dtype=np.float64)
+        o += depth * counts[s]
+    xs = np.ascontiguousarray(xs, dtype=np.float32)
+    labels = np.ascontiguousarray(labels, dtype=np.int32)
+    T = xs.shape[0]
+    stal = np.ascontiguousarray(staleness, dtype=np.int32).reshape(T, S)
+    lr = np.asarray(lr, dtype=np.float64)
+    lr = np.ascontiguousarray(np.broadcast_to(lr if lr.ndim == 2 else np.broadcast_to(lr, (S,)), (T, S)))
+    n = int(sum(counts))
+    m0 = None if mom0 is None else _f64(mom0)
+    n_bn = int(sum(o[4] for o in ops if o[0] == 2))
+    rm, rv = np.zeros(max(n_bn, 1)), np.ones(max(n_bn, 1))
+    bn_in = run_mean is not None
+    if bn_in:
+        rm[:n_bn] = run_mean
+        rv[:n_bn] = run_var
+    hist_out = np.zeros(out_depth * n)
+    momb, grad = np.zeros(n), np.zeros(n)
+    losses = np.zeros(T)
+    versions = np.zeros((T, S), dtype=np.int32)
+    rc = lib().orc_train_from(len(ops), _p(ops, _i32), xs.shape[1], *in_shape, S, _p(se, _i32), int(t0), depth,
+                              _p(packed, _d), _p(m0, _d), int(bn_in), T, _p(xs, _f), _p(labels, _i32),
+                              _p(stal, _i32), _p(lr, _d), mom, wd, int(nesterov), bn_eps, bn_mom, int(bf16),
+                              int(stash), out_depth, _p(hist_out, _d), _p(momb, _d), _p(grad, _d), _p(rm, _d),
+                              _p(rv, _d), _p(losses, _d), _p(versions, _i32), int(dropout_seed))
+    if rc != 0:
+        raise ValueError(f"oracle rejected the run (code {rc})")
+    history, o = [], 0
+    for s in range(S):
+        row = []
+        for k in range(out_depth):
+            v = t0 + T - out_depth + 1 + k
+            row.append(hist_out[o + k * counts[s]:o + (k + 1) * counts[s]].copy() if v >= 0 else None)
+        history.append(row)
+        o += out_depth * counts[s]
+    params = np.concatenate([h[-1] for h in history])
+    return dict(history=history, params=params, momentum=momb, grad=grad, run_mean=rm[:n_bn], run_var=rv[:n_bn],
+                losses=losses, versions=versions)

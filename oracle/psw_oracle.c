@@ -923,7 +923,7 @@ int orc_loss_and_grad(int n_ops, const int32_t *desc, int N, int C0, int H0, int
 /* ======================================================================== */
 /* Training under the stale-weight schedule [Sec. 3, Sec. 4].                */
 /*                                                                          */
-/* For t = 0 .. T-1, with d_s = staleness[t*S + s]:                         */
+/* For t = t0 .. t0+T-1, with d_s = staleness[(t-t0)*S + s]:                */
 /*   r_s = max(0, t - d_s)                  (version read by the forward)   */
 /*   forward with W_s^(r_s) for every stage s, saving activations;           */
 /*   loss and its gradient;                                                  */
@@ -932,28 +932,42 @@ int orc_loss_and_grad(int n_ops, const int32_t *desc, int N, int C0, int H0, int
 /*   (stash != 0: data gradients with W_s^(r_s) instead, the weight-stashing */
 /*   scheme that the paper contrasts its own with, Sec. 6.7 and Sec. 7)     */
 /*   update:  W_s^(t+1) = SGD(W_s^(t), grad_s)  for every stage s.           */
-/* The full history W_s^(0..T) is kept (no ring): version v of stage s is    */
+/* Every version produced is kept (no ring): version v of stage s is         */
 /* history[s][v].  The hybrid schedule of Sec. 4 is expressed by giving      */
 /* d_s = 0 from step n_p on.                                                */
 /*                                                                          */
-/* params0   : concatenated W_s^(0), stage by stage                         */
-/* xs        : T mini-batches, float32, NCHW                                */
+/* The run may start from a checkpoint at step t0 >= 0:                     */
+/* depth     : versions given per stage (>= 1)                              */
+/* hist0     : stage by stage, `depth` packed parameter vectors holding      */
+/*             W_s^(t0-depth+1) .. W_s^(t0) in that order; vectors of        */
+/*             versions below 0 are present but ignored                     */
+/* mom0      : momentum buffers at t0, concatenated (NULL: zero)            */
+/* bn_in     : 0 -> running statistics start at mean 0, var 1; else         */
+/*             run_mean / run_var hold the checkpoint's values on entry     */
+/* xs        : T mini-batches, float32, NCHW  (step t0+i uses batch i)      */
 /* labels    : T x N int32                                                  */
 /* staleness : T x S int32 (>= 0)                                           */
 /* lr        : T x S learning rates (per step, for the schedules of App. A  */
 /*             and B, and per stage, cf. the per-stage rate of Table 7)     */
-/* outputs   : params_out (W_s^(T)), mom_out (momentum buffers),             */
-/*             run_mean/run_var (BN running stats, concatenated over BN     */
-/*             ops; may be NULL), losses (T), versions (T x S: r_s)          */
-/* Returns 0 or a negative error code.                                      */
+/* outputs   : hist_out: stage by stage, `out_depth` vectors                */
+/*             W_s^(t0+T-out_depth+1) .. W_s^(t0+T) (versions below 0 are   */
+/*             left untouched); mom_out (momentum buffers); grad_out (the  */
+/*             gradient of the last step, may be NULL); run_mean/run_var    */
+/*             (BN running stats, concatenated over BN ops; may be NULL);   */
+/*             losses (T); versions (T x S: r_s)                            */
+/* Returns 0, or -2000 for a negative staleness, -2001 when a forward pass   */
+/* would read a version older than the checkpoint holds, -2002 for bad      */
+/* t0 / depth / out_depth.                                                  */
 /* ======================================================================== */
-int orc_train(int n_ops, const int32_t *desc, int N, int C0, int H0, int W0, int n_stages,
-              const int32_t *stage_end, const double *params0, int T, const float *xs,
-              const int32_t *labels, const int32_t *staleness, const double *lr, double mom,
-              double wd, int nesterov, double bn_eps, double bn_mom, int bf16, int stash, double *params_out,
-              double *mom_out, double *run_mean, double *run_var, double *losses, int32_t *versions,
-              uint64_t dropout_seed)
+int orc_train_from(int n_ops, const int32_t *desc, int N, int C0, int H0, int W0, int n_stages,
+                   const int32_t *stage_end, int64_t t0, int depth, const double *hist0,
+                   const double *mom0, int bn_in, int T, const float *xs, const int32_t *labels,
+                   const int32_t *staleness, const double *lr, double mom, double wd, int nesterov,
+                   double bn_eps, double bn_mom, int bf16, int stash, int out_depth, double *hist_out,
+                   double *mom_out, double *grad_out, double *run_mean, double *run_var,
+                   double *losses, int32_t *versions, uint64_t dropout_seed)
 {
+    if (t0 < 0 || depth < 1 || out_depth < 1 || T < 0) return -2002;
     orc_net net;
     int rc = net_build(&net, n_ops, desc, N, C0, H0, W0, n_stages, stage_end);
     if (rc != 0) {
@@ -961,30 +975,46 @@ int orc_train(int n_ops, const int32_t *desc, int N, int C0, int H0, int W0, int
         return rc;
     }
     const int S = n_stages;
-    for (int t = 0; t < T; ++t)
-        for (int s = 0; s < S; ++s)
-            if (staleness[(int64_t)t * S + s] < 0) {
+    const int64_t oldest = t0 - depth + 1 > 0 ? t0 - depth + 1 : 0; /* oldest version held */
+    for (int i = 0; i < T; ++i)
+        for (int s = 0; s < S; ++s) {
+            const int d = staleness[(int64_t)i * S + s];
+            if (d < 0) {
                 net_free(&net);
                 return -2000;
             }
-    /* history[s][v], v = 0..T */
+            const int64_t t = t0 + i;
+            if ((t - d > 0 ? t - d : 0) < oldest) {
+                net_free(&net);
+                return -2001;
+            }
+        }
+    /* history[s][v], v = 0 .. t0+T; only versions >= oldest are allocated */
+    const int64_t nv = t0 + T + 1;
     double ***hist = (double ***)calloc((size_t)S, sizeof(double **));
     double **vel = (double **)calloc((size_t)S, sizeof(double *));
     double **grad = (double **)calloc((size_t)S, sizeof(double *));
     int64_t off = 0;
     for (int s = 0; s < S; ++s) {
         const int64_t np = net.stage_np[s];
-        hist[s] = (double **)calloc((size_t)T + 1, sizeof(double *));
-        hist[s][0] = (double *)malloc(sizeof(double) * (size_t)(np > 0 ? np : 1));
-        memcpy(hist[s][0], params0 + off, sizeof(double) * (size_t)np);
+        hist[s] = (double **)calloc((size_t)nv, sizeof(double *));
+        for (int k = 0; k < depth; ++k) {
+            const int64_t v = t0 - depth + 1 + k;
+            if (v < 0) continue;
+            hist[s][v] = (double *)malloc(sizeof(double) * (size_t)(np > 0 ? np : 1));
+            memcpy(hist[s][v], hist0 + (int64_t)depth * off + (int64_t)k * np, sizeof(double) * (size_t)np);
+        }
         vel[s] = (double *)calloc((size_t)(np > 0 ? np : 1), sizeof(double));
+        if (mom0) memcpy(vel[s], mom0 + off, sizeof(double) * (size_t)np);
         grad[s] = (double *)calloc((size_t)(np > 0 ? np : 1), sizeof(double));
         off += np;
     }
-    if (run_mean)
-        for (int64_t i = 0; i < net.bn_total; ++i) run_mean[i] = 0.0;
-    if (run_var)
-        for (int64_t i = 0; i < net.bn_total; ++i) run_var[i] = 1.0;
+    if (!bn_in) {
+        if (run_mean)
+            for (int64_t i = 0; i < net.bn_total; ++i) run_mean[i] = 0.0;
+        if (run_var)
+            for (int64_t i = 0; i < net.bn_total; ++i) run_var[i] = 1.0;
+    }
 
     const int64_t in_numel = shape_numel(net.shape[0]);
     const orc_shape last = net.shape[n_ops];
@@ -992,33 +1022,39 @@ int orc_train(int n_ops, const int32_t *desc, int N, int C0, int H0, int W0, int
     double **wfor = (double **)calloc((size_t)S, sizeof(double *));
     double **wcur = (double **)calloc((size_t)S, sizeof(double *));
 
-    for (int t = 0; t < T; ++t) {
+    for (int i = 0; i < T; ++i) {
+        const int64_t t = t0 + i;
         for (int s = 0; s < S; ++s) {
-            const int d = staleness[(int64_t)t * S + s];
-            const int r = t - d > 0 ? t - d : 0;
-            versions[(int64_t)t * S + s] = r;
+            const int d = staleness[(int64_t)i * S + s];
+            const int64_t r = t - d > 0 ? t - d : 0;
+            versions[(int64_t)i * S + s] = (int32_t)r;
             wfor[s] = hist[s][r];
             wcur[s] = stash ? hist[s][r] : hist[s][t];
         }
         orc_fwd_state st;
         state_alloc(&st, n_ops);
-        losses[t] = forward(&net, wfor, xs + (int64_t)t * in_numel, labels + (int64_t)t * N, &st,
+        losses[i] = forward(&net, wfor, xs + (int64_t)i * in_numel, labels + (int64_t)i * N, &st,
                             run_mean, run_var, bn_eps, bn_mom, bf16, dlog, dropout_seed, t);
         backward(&net, wcur, &st, dlog, grad, bf16, dropout_seed, t);
         state_free(&st, n_ops);
         for (int s = 0; s < S; ++s) {
             const int64_t np = net.stage_np[s];
             hist[s][t + 1] = (double *)malloc(sizeof(double) * (size_t)(np > 0 ? np : 1));
-            orc_sgd(np, hist[s][t], hist[s][t + 1], vel[s], grad[s], lr[(int64_t)t * S + s], mom, wd, nesterov);
+            orc_sgd(np, hist[s][t], hist[s][t + 1], vel[s], grad[s], lr[(int64_t)i * S + s], mom, wd, nesterov);
         }
     }
     off = 0;
     for (int s = 0; s < S; ++s) {
         const int64_t np = net.stage_np[s];
-        memcpy(params_out + off, hist[s][T], sizeof(double) * (size_t)np);
+        for (int k = 0; k < out_depth; ++k) {
+            const int64_t v = t0 + T - out_depth + 1 + k;
+            if (v >= 0 && hist[s][v])
+                memcpy(hist_out + (int64_t)out_depth * off + (int64_t)k * np, hist[s][v], sizeof(double) * (size_t)np);
+        }
         if (mom_out) memcpy(mom_out + off, vel[s], sizeof(double) * (size_t)np);
+        if (grad_out) memcpy(grad_out + off, grad[s], sizeof(double) * (size_t)np);
         off += np;
-        for (int v = 0; v <= T; ++v) free(hist[s][v]);
+        for (int64_t v = 0; v < nv; ++v) free(hist[s][v]);
         free(hist[s]);
         free(vel[s]);
         free(grad[s]);
@@ -1031,4 +1067,19 @@ int orc_train(int n_ops, const int32_t *desc, int N, int C0, int H0, int W0, int
     free(wcur);
     net_free(&net);
     return 0;
+}
+
+/* The run from step 0: W_s^(0) = params0 (concatenated, stage by stage),
+ * momentum zero, running statistics mean 0 / var 1; params_out receives
+ * W_s^(T).  Arguments otherwise as orc_train_from. */
+int orc_train(int n_ops, const int32_t *desc, int N, int C0, int H0, int W0, int n_stages,
+              const int32_t *stage_end, const double *params0, int T, const float *xs,
+              const int32_t *labels, const int32_t *staleness, const double *lr, double mom,
+              double wd, int nesterov, double bn_eps, double bn_mom, int bf16, int stash, double *params_out,
+              double *mom_out, double *run_mean, double *run_var, double *losses, int32_t *versions,
+              uint64_t dropout_seed)
+{
+    return orc_train_from(n_ops, desc, N, C0, H0, W0, n_stages, stage_end, 0, 1, params0, NULL, 0, T, xs,
+                          labels, staleness, lr, mom, wd, nesterov, bn_eps, bn_mom, bf16, stash, 1, params_out,
+                          mom_out, NULL, run_mean, run_var, losses, versions, dropout_seed);
 }

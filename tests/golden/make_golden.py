@@ -1,12 +1,19 @@
 """Write the oracle's results for the full-size runs to tests/golden/.
 Calls only the oracle and the seeded input generator; never the GPU path.
 
-    python tests/golden/make_golden.py [fp32|bf16|alexnet|vgg16|resnet110 ...]
+    python tests/golden/make_golden.py [fp32|bf16|alexnet|vgg16|resnet110|states_fp32|states_bf16 ...]
 
 fp32 / bf16: ResNet-20, batch 128, 4 stages at the Table 1 PPV (7,13,19),
 staleness [3,2,1,0], 50 steps, lr 0.01, momentum 0.9.  Stored: the
 parameter update W^(50) - W^(0) (float32; W^(0) is regenerated from the
 seed), the 50 losses and the version table.
+
+states_fp32 / states_bf16: the same ResNet-20 run's state at steps 25 and
+49 -- for every stage s the versions W_s^(t-d_s) .. W_s^(t) its ring holds
+(d = [3,2,1,0]), the momentum and the BN running statistics, all rounded to
+float32 -- so that a test can start one step from a point on the oracle's
+own trajectory (the oracle run to 25, then resumed from its exact float64
+state to 49).
 
 alexnet / vgg16 / resnet110: the other full-size configurations (AlexNet-style
 net, batch 128, 20 steps, split after conv2, staleness [2,0], App. A's rate
@@ -120,6 +127,45 @@ def make_full(name):
     print(f"{name}: spread {spread} -> {path}", flush=True)
 
 
+STATE_STEPS = (25, 49)
+
+
+def make_states(mode):
+    wl = synth.resnet20_workload(bf16=(mode == "bf16"))
+    T = STATE_STEPS[-1]
+    D = max(wl.ring_depth(T))
+    p0 = synth.init_params(wl).astype(np.float64)
+    xs, ys = synth.batches(wl, T)
+    st, lr = wl.staleness(T), wl.lr_table(T)
+    counts = O.param_counts(wl.ops, wl.in_shape, 1, wl.stage_end)
+    depth = wl.ring_depth(T)
+    out, t_prev, res = {}, 0, None
+    t0 = time.time()
+    for t in STATE_STEPS:
+        if res is None:
+            hist0, mom0, rm, rv = [[v] for v in np.split(p0, np.cumsum(counts)[:-1])], None, None, None
+        else:
+            hist0, mom0, rm, rv = [row[-D:] for row in res["history"]], res["momentum"], res["run_mean"], res["run_var"]
+        res = O.train_from(wl.ops, wl.in_shape, wl.stage_end, t_prev, hist0, mom0, xs[t_prev:t], ys[t_prev:t],
+                           st[t_prev:t], lr[t_prev:t], wl.momentum, wl.weight_decay, wl.nesterov, bf16=wl.bf16,
+                           dropout_seed=wl.dropout_seed, run_mean=rm, run_var=rv, out_depth=D)
+        for s_, row in enumerate(res["history"]):
+            out[f"t{t}_s{s_}"] = np.stack(row[D - depth[s_]:]).astype(np.float32)  # versions t-d_s .. t
+        out[f"t{t}_momentum"] = res["momentum"].astype(np.float32)
+        out[f"t{t}_run_mean"] = res["run_mean"].astype(np.float32)
+        out[f"t{t}_run_var"] = res["run_var"].astype(np.float32)
+        print(f"states {mode}: t={t} {time.time() - t0:.0f} s, loss {res['losses'][-1]:.6f}", flush=True)
+        t_prev = t
+    path = os.path.join(HERE, f"resnet20_b128_states_{mode}.npz")
+    np.savez_compressed(path, steps=np.array(STATE_STEPS), **out)
+    print(f"-> {path} ({os.path.getsize(path) / 2**20:.1f} MiB)", flush=True)
+
+
 if __name__ == "__main__":
     for m in (sys.argv[1:] or ["fp32", "bf16"]):
-        make(m) if m in ("fp32", "bf16") else make_full(m)
+        if m in ("fp32", "bf16"):
+            make(m)
+        elif m.startswith("states_"):
+            make_states(m[len("states_"):])
+        else:
+            make_full(m)

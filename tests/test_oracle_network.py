@@ -253,3 +253,91 @@ def test_oracle_matches_autograd_stale_schedule(oracle):
     np.testing.assert_array_equal(versions, out["versions"])
     np.testing.assert_allclose(losses, out["losses"], rtol=1e-12)
     np.testing.assert_allclose(p, out["params"], rtol=1e-10, atol=1e-12)
+
+
+# ------------------------------------------------------ checkpoint / resume ---
+def _window(res, depth):
+    """The last `depth` versions of every stage from a train_from result."""
+    return [row[-depth:] for row in res["history"]]
+
+
+def test_oracle_resume_25_plus_25_equals_50(oracle):
+    """Checkpoint after 25 steps (the versions the schedule can still read,
+    momentum, running statistics), resume for 25 more: bit-identical to 50
+    uninterrupted steps (ResNet-20, batch 4, staleness [3,2,1,0])."""
+    wl = synth.resnet20_workload(batch=4)
+    T, D = 50, 4
+    p0 = synth.init_params(wl)
+    xs, ys = synth.batches(wl, T, 4)
+    st, lr = wl.staleness(T), wl.lr_table(T)
+    full = oracle.train(wl.ops, wl.in_shape, wl.stage_end, p0, xs, ys, st, lr, wl.momentum)
+    counts = oracle.param_counts(wl.ops, wl.in_shape, 1, wl.stage_end)
+    first = oracle.train_from(wl.ops, wl.in_shape, wl.stage_end, 0, [[v] for v in np.split(p0.astype(np.float64),
+                              np.cumsum(counts)[:-1])], None, xs[:25], ys[:25], st[:25], lr[:25], wl.momentum,
+                              out_depth=D)
+    second = oracle.train_from(wl.ops, wl.in_shape, wl.stage_end, 25, _window(first, D), first["momentum"],
+                               xs[25:], ys[25:], st[25:], lr[25:], wl.momentum, run_mean=first["run_mean"],
+                               run_var=first["run_var"])
+    np.testing.assert_array_equal(second["params"], full["params"])
+    np.testing.assert_array_equal(second["momentum"], full["momentum"])
+    np.testing.assert_array_equal(second["run_mean"], full["run_mean"])
+    np.testing.assert_array_equal(second["run_var"], full["run_var"])
+    np.testing.assert_array_equal(np.concatenate([first["losses"], second["losses"]]), full["losses"])
+    np.testing.assert_array_equal(np.concatenate([first["versions"], second["versions"]]), full["versions"])
+    # from a checkpoint at 49, one step: the same W^(50), and the returned
+    # gradient is what moved the momentum (v50 = 0.9 v49 + g49)
+    mid = oracle.train_from(wl.ops, wl.in_shape, wl.stage_end, 25, _window(first, D), first["momentum"], xs[25:49],
+                            ys[25:49], st[25:49], lr[25:49], wl.momentum, run_mean=first["run_mean"],
+                            run_var=first["run_var"], out_depth=D)
+    one = oracle.train_from(wl.ops, wl.in_shape, wl.stage_end, 49, _window(mid, D), mid["momentum"], xs[49:],
+                            ys[49:], st[49:], lr[49:], wl.momentum)
+    np.testing.assert_array_equal(one["params"], full["params"])
+    np.testing.assert_array_equal(one["momentum"], wl.momentum * mid["momentum"] + one["grad"])
+
+
+def test_oracle_resume_rejects_missing_versions(oracle):
+    """A forward pass that would read a version older than the checkpoint
+    holds is an error, not a silent clamp."""
+    wl = synth.resnet20_workload(batch=2)
+    p0 = synth.init_params(wl).astype(np.float64)
+    counts = oracle.param_counts(wl.ops, wl.in_shape, 1, wl.stage_end)
+    one = [[v, v] for v in np.split(p0, np.cumsum(counts)[:-1])]  # versions 9, 10 only
+    xs, ys = synth.batches(wl, 1, 2)
+    with pytest.raises(ValueError):
+        oracle.train_from(wl.ops, wl.in_shape, wl.stage_end, 10, one, None, xs, ys, [[3, 2, 1, 0]], wl.lr)
+    out = oracle.train_from(wl.ops, wl.in_shape, wl.stage_end, 10, one, None, xs, ys, [[1, 1, 1, 0]], wl.lr)
+    np.testing.assert_array_equal(out["versions"], [[9, 9, 9, 10]])
+
+
+@pytest.mark.parametrize("bf16", [False, True], ids=["fp64", "bf16_operands"])
+def test_one_step_from_state_matches_autograd(oracle, bf16):
+    """One step of the stale schedule from a checkpoint whose ring slots all
+    differ (ResNet-20, batch 4, t = 5, staleness [3,2,1,0]): the oracle's
+    resume form against the step written with torch autograd in float64
+    (forward with version t - d_s, the current version swapped in before
+    the backward pass).  With bf16=True both round the operands of every
+    product to bfloat16 (the oracle via its own rounding routine, torch via
+    its bfloat16 conversion), which pins the torch reference the GPU tests
+    use for their bf16 spread."""
+    wl = synth.resnet20_workload(batch=4, bf16=bf16)
+    t, st = 5, np.array([3, 2, 1, 0])
+    counts = [int(c) for c in oracle.param_counts(wl.ops, wl.in_shape, 1, wl.stage_end)]
+    rng = np.random.Generator(np.random.PCG64(77))
+    p0 = synth.init_params(wl).astype(np.float64)
+    versions = [{v: p + 1e-2 * rng.standard_normal(p.size) for v in range(t - 3, t + 1)}
+                for p in np.split(p0, np.cumsum(counts)[:-1])]
+    mom0 = 1e-2 * rng.standard_normal(p0.size)
+    x, y = synth.batch(wl, t, 4)
+    r = oracle.train_from(wl.ops, wl.in_shape, wl.stage_end, t, [[w[v] for v in range(t - 3, t + 1)] for w in versions],
+                          mom0, x[None], y[None], st[None], wl.lr, wl.momentum, bf16=bf16)
+    ref = torch_ref.stale_step_from(wl.ops, wl.stage_end, [w[t - d] for w, d in zip(versions, st)],
+                                    [w[t] for w in versions], mom0, x, y, wl.lr, wl.momentum, bf16=bf16)
+    np.testing.assert_array_equal(r["versions"][0], t - st)
+    assert abs(r["losses"][0] - ref["loss"]) <= 1e-12 * abs(ref["loss"])
+    for k in ("grad", "momentum", "params"):
+        err = np.linalg.norm(r[k] - ref[k]) / np.linalg.norm(ref[k])
+        assert err <= 1e-11, (k, err)
+    # the stale versions matter: the same step with every stage current differs
+    fresh = torch_ref.stale_step_from(wl.ops, wl.stage_end, [w[t] for w in versions], [w[t] for w in versions], mom0,
+                                      x, y, wl.lr, wl.momentum, bf16=bf16)
+    assert np.linalg.norm(fresh["grad"] - ref["grad"]) > 1e-3 * np.linalg.norm(ref["grad"])

@@ -84,7 +84,48 @@ def dropout_mask(numel, p24, seed, op, step):
     return (r >> 8) >= p24
 
 
-def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5, bn_mom=0.1, dropout_key=None):
+def _rb(t):
+    """t with every element rounded to bfloat16 (round to nearest even), in t's dtype."""
+    return t.to(torch.bfloat16).to(t.dtype)
+
+
+class _Bf16Conv(torch.autograd.Function):
+    """conv2d whose product operands are rounded to bfloat16 in each pass:
+    forward x, w; backward-data dy, w; backward-weight x, dy.  The weight is
+    held by reference, so a backward pass sees whatever the tensor holds
+    then (the stale schedule swaps in the current version before it)."""
+
+    @staticmethod
+    def forward(ctx, x, w, b, stride, pad):
+        ctx.x, ctx.w, ctx.has_b, ctx.stride, ctx.pad = x, w, b is not None, stride, pad
+        return F.conv2d(_rb(x), _rb(w), b, stride=stride, padding=pad)
+
+    @staticmethod
+    def backward(ctx, dy):
+        x, w = ctx.x, ctx.w
+        dx = torch.nn.grad.conv2d_input(x.shape, _rb(w), _rb(dy), stride=ctx.stride, padding=ctx.pad)
+        dw = torch.nn.grad.conv2d_weight(_rb(x), w.shape, _rb(dy), stride=ctx.stride, padding=ctx.pad)
+        db = dy.sum(dim=(0, 2, 3)) if ctx.has_b else None
+        return dx, dw, db, None, None
+
+
+class _Bf16Linear(torch.autograd.Function):
+    """linear with bfloat16-rounded product operands in each pass (as _Bf16Conv)."""
+
+    @staticmethod
+    def forward(ctx, x, w, b):
+        ctx.x, ctx.w, ctx.has_b = x, w, b is not None
+        return F.linear(_rb(x), _rb(w), b)
+
+    @staticmethod
+    def backward(ctx, dy):
+        x, w = ctx.x, ctx.w
+        db = dy.sum(dim=0) if ctx.has_b else None
+        return _rb(dy) @ _rb(w), _rb(dy).t() @ _rb(x), db
+
+
+def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5, bn_mom=0.1, dropout_key=None,
+            bf16=False):
     """Apply ops[lo:hi].  inputs: dict tensor_id -> tensor (must hold every
     tensor that ops[lo:hi] read from outside the range).  stage_params: list
     of flat per-stage torch tensors.  dropout_key: (seed, step) of the
@@ -96,7 +137,10 @@ def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5
         P = {name: stage_params[s][off:off + int(np.prod(shape))].view(shape) for name, off, shape in lst}
         a = t[in0]
         if kind == CONV:
-            y = F.conv2d(a, P["weight"], P.get("bias"), stride=stride, padding=pad)
+            if bf16:
+                y = _Bf16Conv.apply(a, P["weight"], P.get("bias"), stride, pad)
+            else:
+                y = F.conv2d(a, P["weight"], P.get("bias"), stride=stride, padding=pad)
             if flags & F_RELU:
                 y = F.relu(y)
         elif kind == BN:
@@ -113,7 +157,10 @@ def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5
         elif kind == GAVG:
             y = a.mean(dim=(2, 3), keepdim=True)
         elif kind == FC:
-            y = F.linear(a.reshape(a.shape[0], -1), P["weight"], P.get("bias"))
+            if bf16:
+                y = _Bf16Linear.apply(a.reshape(a.shape[0], -1), P["weight"], P.get("bias"))
+            else:
+                y = F.linear(a.reshape(a.shape[0], -1), P["weight"], P.get("bias"))
             if flags & F_RELU:
                 y = F.relu(y)
             y = y.reshape(y.shape[0], -1, 1, 1)
@@ -316,3 +363,39 @@ def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=
                 V[s].mul_(mom).add_(g + wd * hist[s][t])
                 hist[s].append(hist[s][t] - float(lrs_t[t, s]) * V[s])
     return torch.cat([h[-1] for h in hist]).double().numpy(), losses, versions
+
+
+def stale_step_from(ops, stage_end, wfor, wcur, mom0, x, labels, lr, mom=0.9, wd=0.0, nesterov=False,
+                    dtype=torch.float64, bf16=False, dropout_key=None):
+    """One step of the stale-weight schedule from a given state, written with
+    autograd: forward with the per-stage vectors wfor (version t - d_s), then
+    the current versions wcur are swapped into the same tensors before the
+    backward pass (data gradients with version t, weight gradients from the
+    saved activations), then d = g + wd*wcur, v = mom*v0 + d,
+    w = wcur - lr*(nesterov ? d + mom*v : v).
+    lr: scalar or [S].  Returns dict(grad, momentum, params, loss), vectors
+    concatenated over stages."""
+    slices, counts = op_param_slices(ops, stage_end)
+    S = len(counts)
+    Wp = [torch.tensor(np.asarray(w, np.float64), dtype=dtype, requires_grad=True) for w in wfor]
+    cur = [torch.tensor(np.asarray(w, np.float64), dtype=dtype) for w in wcur]
+    v0 = split_flat(torch.tensor(np.asarray(mom0, np.float64), dtype=dtype), counts)
+    lrs = np.broadcast_to(np.asarray(lr, dtype=np.float64), (S,))
+    n = len(ops)
+    outs = run_ops(ops, 0, n, {0: torch.tensor(x, dtype=dtype)}, Wp, slices, dropout_key=dropout_key, bf16=bf16)
+    loss = F.cross_entropy(outs[n].reshape(outs[n].shape[0], -1), torch.tensor(labels, dtype=torch.long))
+    with torch.no_grad():
+        for s in range(S):
+            Wp[s].data.copy_(cur[s])
+    loss.backward()
+    g, v, w = [], [], []
+    with torch.no_grad():
+        for s in range(S):
+            gs = Wp[s].grad if Wp[s].grad is not None else torch.zeros_like(cur[s])
+            ds = gs + wd * cur[s]
+            vs = mom * v0[s] + ds
+            g.append(gs)
+            v.append(vs)
+            w.append(cur[s] - float(lrs[s]) * (ds + mom * vs if nesterov else vs))
+    cat = lambda L: torch.cat(L).double().numpy()
+    return dict(grad=cat(g), momentum=cat(v), params=cat(w), loss=float(loss.detach()))
