@@ -16,7 +16,7 @@
  *  - Every pointer argument is a DEVICE pointer unless its comment says
  *    "host".  The caller owns all device memory; the library never
  *    allocates device memory.
- *  - Activations are float32 NCHW (layout code PSW_NCHW); conv weights are
+ *  - Activations are float32 NCHW (the only layout); conv weights are
  *    KCRS [K_out][C_in][R][S]; FC weights are [out][in]; all contiguous.
  *  - `stream` is a hipStream_t passed as void* (NULL = default stream).
  *    Every call only enqueues work on that stream; nothing synchronises the
@@ -53,7 +53,6 @@ enum {
     PSW_ERR_STATE = -8        /* object not ready (e.g. net not bound) */
 };
 
-enum { PSW_NCHW = 0, PSW_NHWC = 1 };
 enum { PSW_FP32 = 0, PSW_BF16 = 1 };
 
 /* Thread-local message of the last failing call on this thread ("" if none). */
@@ -322,6 +321,18 @@ int psw_net_set_step(psw_net *net, int64_t t);
  * ring_depth. */
 int psw_net_slot(const psw_net *net, int stage, int64_t version, float **params);
 
+/* Read-back of the step set psw_stage_step uses (for tests and inspection):
+ * *ptr receives the device address of tensor `tensor` (1..n_layers; tensor
+ * i+1 is operation i's output) and *count (may be NULL) its element count.
+ * grad == 0: the value the last psw_stage_step's forward pass computed;
+ * grad != 0: the gradient of the loss with respect to that tensor from its
+ * backward pass (for a conv or FC with ReLU, with respect to the output
+ * after the ReLU, masked by it).  The contents are those of the last
+ * psw_stage_step until the next step of the net is issued; a pipelined run
+ * may use other step sets.  PSW_ERR_SHAPE for tensor 0 (the caller's batch)
+ * or out of range, PSW_ERR_STATE before psw_net_bind. */
+int psw_net_tensor(const psw_net *net, int tensor, int grad, float **ptr, int64_t *count);
+
 /* Offset (in floats, inside the packed parameters of the op's stage) and
  * count of operation `op`'s parameters (host outputs). */
 int psw_net_param_offset(const psw_net *net, int op, int *stage, int64_t *offset, int64_t *count);
@@ -345,8 +356,12 @@ int psw_net_set_dropout_seed(psw_net *net, uint64_t seed);
 /* Dry run of psw_stage_step (host only, no device work): the kernel-level
  * plan of step t.  Each record is (op, what, stage, version) where `what`
  * is a PSW_PLAN_* code, `version` the weight version it reads (-1 if
- * none).  Writes up to cap records; *n_out receives the total count.
- * Validates exactly as psw_stage_step does (step order excepted). */
+ * none).  A BN whose backward pass has no kernel of its own (it is folded
+ * into the backward-data kernels of the convs around it: the next conv's
+ * forms its sums, the previous conv's applies it while staging its input)
+ * is recorded as PSW_PLAN_BN_BWD_FOLDED instead of PSW_PLAN_BN_BWD.
+ * Writes up to cap records; *n_out receives the total count.  Validates
+ * exactly as psw_stage_step does (step order excepted). */
 typedef struct {
     int32_t op, what, stage;
     int64_t version;
@@ -355,7 +370,8 @@ typedef struct {
 enum {
     PSW_PLAN_CONV_FWD = 1, PSW_PLAN_BN_FWD, PSW_PLAN_POOL_FWD, PSW_PLAN_FC_FWD, PSW_PLAN_LOSS,
     PSW_PLAN_RELU_MASK, PSW_PLAN_CONV_BWD_WEIGHT, PSW_PLAN_CONV_BWD_DATA, PSW_PLAN_BN_BWD,
-    PSW_PLAN_POOL_BWD, PSW_PLAN_FC_BWD, PSW_PLAN_SGD, PSW_PLAN_DROPOUT_FWD, PSW_PLAN_DROPOUT_BWD
+    PSW_PLAN_POOL_BWD, PSW_PLAN_FC_BWD, PSW_PLAN_SGD, PSW_PLAN_DROPOUT_FWD, PSW_PLAN_DROPOUT_BWD,
+    PSW_PLAN_BN_BWD_FOLDED
 };
 
 int psw_net_plan(const psw_net *net, int64_t t, const int32_t *staleness, psw_launch *out, int cap,

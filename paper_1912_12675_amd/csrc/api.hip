@@ -620,6 +620,10 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
             if (r.c != yb.c || r.h != yb.h || r.w != yb.w || net->grad_accum[2 * i + 1]) continue;
         }
         if (pc.kind != PSW_OP_CONV || pc.in0 <= 0 || (pc.flags & PSW_F_RELU)) continue;
+        // the residual's gradient (written by the fold) must not be the
+        // folded conv's own input gradient (x -> conv -> BN(+x)): inside one
+        // launch some workgroups would write it while others still read it
+        if (o.in1 > 0 && o.in1 == pc.in0) continue;
         if (!net->fuse_bwd[i + 1] || net->grad_accum[2 * i]) continue;
         if (net->stage_of[i - 1] != net->stage_of[i]) continue;
         const Tensor a = net->t[pc.in0];
@@ -806,6 +810,17 @@ int psw_net_slot(const psw_net* net, int stage, int64_t version, float** params)
     return PSW_OK;
 }
 
+int psw_net_tensor(const psw_net* net, int tensor, int grad, float** ptr, int64_t* count)
+{
+    if (!net || !ptr) return fail(PSW_ERR_NULL, "net_tensor: required pointer is NULL");
+    if (!net->bound) return fail(PSW_ERR_STATE, "net_tensor: net is not bound");
+    const int L = (int)net->ops.size();
+    if (tensor < 1 || tensor > L) return fail(PSW_ERR_SHAPE, "net_tensor: tensor %d out of range 1..%d", tensor, L);
+    *ptr = (float*)(net->arena + (grad ? net->grad_off[tensor] : net->act_off[tensor]));
+    if (count) *count = net->t[tensor].numel();
+    return PSW_OK;
+}
+
 int psw_net_param_offset(const psw_net* net, int op, int* stage, int64_t* offset, int64_t* count)
 {
     if (!net) return fail(PSW_ERR_NULL, "net_param_offset: net is NULL");
@@ -866,7 +881,7 @@ int psw_net_plan(const psw_net* net, int64_t t, const int32_t* staleness, psw_la
             if (o.flags & PSW_F_RELU) rec(i, PSW_PLAN_RELU_MASK, s, -1);
             if (o.in0 > 0) rec(i, PSW_PLAN_CONV_BWD_DATA, s, vb);
             break;
-        case PSW_OP_BN: rec(i, PSW_PLAN_BN_BWD, s, vb); break;
+        case PSW_OP_BN: rec(i, net->fold_bn[i] ? PSW_PLAN_BN_BWD_FOLDED : PSW_PLAN_BN_BWD, s, vb); break;
         case PSW_OP_MAXPOOL:
         case PSW_OP_GAVG:
             if (o.in0 > 0) rec(i, PSW_PLAN_POOL_BWD, s, -1);

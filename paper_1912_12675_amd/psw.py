@@ -86,6 +86,7 @@ SIGNATURES = {
     "psw_net_slot": (_I, [_P, _I, _I64, ctypes.POINTER(ctypes.c_void_p)]),
     "psw_net_param_offset": (_I, [_P, _I, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int64),
                                   ctypes.POINTER(ctypes.c_int64)]),
+    "psw_net_tensor": (_I, [_P, _I, _I, ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_int64)]),
     "psw_net_plan": (_I, [_P, _I64, _P, ctypes.POINTER(psw_launch), _I, ctypes.POINTER(ctypes.c_int)]),
     "psw_net_profile": (_I, [_P, _I]),
     "psw_net_profile_read": (_I, [_P, _I, _P, _P]),
@@ -358,6 +359,14 @@ class Net:
     def params(self, version):
         """All stages' parameters at `version` (concatenated, float32 on host)."""
         return torch.cat([self.slot(s, version).detach().cpu() for s in range(self.S)])
+
+    def tensor(self, tensor, grad=False):
+        """View of tensor `tensor` (op tensor-1's output) of the last
+        psw_stage_step, or of its gradient (psw_net_tensor)."""
+        p, n = ctypes.c_void_p(), ctypes.c_int64()
+        _check(lib().psw_net_tensor(self.handle, int(tensor), int(bool(grad)), ctypes.byref(p), ctypes.byref(n)))
+        off = p.value - self.arena.data_ptr()
+        return self.arena[off:off + 4 * n.value].view(torch.float32)
 
     def set_step(self, t):
         _check(lib().psw_net_set_step(self.handle, int(t)))

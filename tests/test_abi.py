@@ -71,7 +71,7 @@ def test_plan_versions_follow_schedule(psw):
         d = [3, 2, 1, 0]
         plan = _plan(psw, wl, t, d)
         fwd = [p for p in plan if p[1] in (1, 2, 4)]           # conv / bn / fc forward
-        bwd = [p for p in plan if p[1] in (8, 9, 11)]          # bwd-data / bn bwd / fc bwd
+        bwd = [p for p in plan if p[1] in (8, 9, 11, 15)]      # bwd-data / bn bwd (folded) / fc bwd
         sgd = [p for p in plan if p[1] == 12]
         for op, what, stage, ver in fwd:
             assert stage == stage_of[op]
@@ -107,7 +107,7 @@ def test_plan_weight_stashing(psw):
         assert len(st) == len(base)
         for (o1, w1, s1, v1), (o2, w2, s2, v2) in zip(base, st):
             assert (o1, w1, s1) == (o2, w2, s2)
-            if w1 in (8, 9, 11):
+            if w1 in (8, 9, 11, 15):
                 assert v1 == t and v2 == max(0, t - d[s1])
             else:
                 assert v1 == v2
@@ -243,3 +243,52 @@ def test_profile_probe_argument_checks(psw):
     assert L.psw_net_profile_probe(h.value, -1, None) == -2
     assert L.psw_net_profile_probe(h.value, 1025, None) == -2
     L.psw_net_destroy(h.value)
+
+
+
+def conv_residual_workload(batch=4):
+    """A residual block whose BN adds the block conv's own input
+    (x -> conv -> BN(+x) -> ReLU), between two ordinary conv + BN layers,
+    then pool and classifier: 16 channels at 32x32, one stage."""
+    b = synth._Builder()
+    t = b.add(synth.CONV, 0, 3, 16, 3, 1, 1)
+    x = b.add(synth.BN, t, 16, 16, flags=synth.F_RELU)
+    b.end_layer()
+    t = b.add(synth.CONV, x, 16, 16, 3, 1, 1)
+    t = b.add(synth.BN, t, 16, 16, flags=synth.F_RELU, in1=x)
+    b.end_layer()
+    t = b.add(synth.CONV, t, 16, 16, 3, 1, 1)
+    t = b.add(synth.BN, t, 16, 16, flags=synth.F_RELU)
+    b.end_layer()
+    t = b.add(synth.GAVG, t, 16, 16)
+    b.add(synth.FC, t, 16, 10, flags=synth.F_BIAS)
+    b.end_layer()
+    return synth.Workload("conv_residual", b.desc(), (3, 32, 32), 10, batch, b.layer_end, [len(b.ops)],
+                          lambda t: [0], 4, [0.01], seed=1918)
+
+
+def test_plan_reports_folded_bn_backward(psw):
+    """ResNet-20 folds 13 of its 19 BN backward passes (7 without residual,
+    6 with an identity residual) into the backward-data kernels around
+    them; the plan records them as folded."""
+    wl = synth.resnet20_workload(batch=8)
+    plan = _plan(psw, wl, 3, [3, 2, 1, 0])
+    folded = [p[0] for p in plan if p[1] == 15]
+    plain = [p[0] for p in plan if p[1] == 9]
+    assert len(folded) == 13 and len(plain) == 6
+    assert sum(1 for i in folded if wl.ops[i][2] >= 0) == 6
+
+
+def test_plan_no_fold_when_residual_is_the_conv_input(psw):
+    """x -> conv -> BN(+x): folding this BN would make the backward-data
+    kernel write the residual's gradient (the conv's own input gradient)
+    in some workgroups while others still read it, so it is not folded.
+    """
+    wl = conv_residual_workload()
+    plan = _plan(psw, wl, 0, [0])
+    bn_bwd = {p[0]: p[1] for p in plan if p[1] in (9, 15)}
+    # every other fold condition holds for op 3 (identity residual written
+    # first, stride-1 direct conv before it in the same stage, a conv after
+    # it whose backward-data kernel forms its sums): only the aliasing
+    # keeps it from being folded
+    assert bn_bwd[3] == 9
