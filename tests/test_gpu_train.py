@@ -18,6 +18,7 @@ import torch
 
 from paper_1912_12675_amd import synth
 from tests import torch_ref
+from tests.test_abi import conv_residual_workload
 
 pytestmark = pytest.mark.gpu
 
@@ -126,6 +127,10 @@ CASES = [
     # oracle (a max-pool / ReLU near-tie decided the other way), so the case
     # runs at batch 16 like the plain VGG-16 case.
     ("vgg16_dropout_b16", lambda: synth.vgg16_workload(batch=16, n_pipelined=3, dropout=0.4), 16, 5),
+    # a residual BN that adds its block conv's own input (x -> conv ->
+    # BN(+x)): its backward is not folded into that conv's backward-data
+    # kernel, which reads the gradient the fold would write
+    ("conv_residual_b4", lambda: conv_residual_workload(batch=4), 4, 4),
 ]
 
 
