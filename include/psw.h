@@ -97,6 +97,24 @@ int psw_conv_bwd_weight(int n, int c, int h, int w, int k, int r, int s, int str
                         const float *x, const float *dy, float *dw, float *dbias, int prec, void *ws,
                         size_t ws_bytes, void *stream);
 
+/* Allocation-free psw_conv_bwd_weight, for callers that cannot allocate
+ * device memory or pass a workspace (code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc).  Same arguments and
+ * results (bit for bit) without (ws, ws_bytes): the split partial sums live
+ * in a static device array of PSW_NOALLOC_SCRATCH_BYTES that the library
+ * holds on every GPU it runs on until the process ends; its address is
+ * resolved on the first call on each device (the calling thread's current
+ * device, to which `stream` must belong).  No call allocates or frees
+ * device memory.  A shape whose workspace (psw_conv_bwd_weight_ws_bytes)
+ * exceeds the array is rejected with PSW_ERR_WORKSPACE, nothing enqueued.
+ * All calls on one GPU share the array and every call overwrites it before
+ * reading it: calls that can overlap on one GPU (on different streams, or
+ * from different threads) race and must be ordered by the caller. */
+#define PSW_NOALLOC_SCRATCH_BYTES ((size_t)32 << 20)
+int psw_conv_bwd_weight_noalloc(int n, int c, int h, int w, int k, int r, int s, int stride, int pad,
+                                const float *x, const float *dy, float *dw, float *dbias, int prec,
+                                void *stream);
+
 /* Workspace bytes of the batch-norm entry points for [n,c,h,w]. */
 size_t psw_bn_ws_bytes(int n, int c, int h, int w);
 

@@ -23,6 +23,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -74,6 +75,35 @@ int check_conv(int n, int c, int h, int w, int k, int r, int s, int stride, int 
     return PSW_OK;
 }
 
+// Scratch of psw_conv_bwd_weight_noalloc: one array per GPU, part of the
+// library's device code, so that the entry point allocates nothing.  Host
+// code must not pass `scratch` itself to a kernel (in host code the name is
+// a stand-in, not a device address): its device address is resolved once per
+// device with hipGetSymbolAddress, with that device current, and kept here.
+constexpr size_t kScratchBytes = PSW_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) static char scratch[kScratchBytes];
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];  // device address of `scratch` per device, nullptr until resolved
+
+int scratch_of_current_device(void** out, const char* what)
+{
+    int dev = -1;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_check(e, what);
+    if (dev < 0 || dev >= kMaxDevices) return fail(PSW_ERR_UNSUPPORTED, "%s: device %d out of range", what, dev);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return hip_check(e, what);
+        if (!p) return fail(PSW_ERR_HIP, "%s: hipGetSymbolAddress returned no address", what);
+        g_scratch_ptr[dev] = p;
+    }
+    *out = g_scratch_ptr[dev];
+    return PSW_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -119,6 +149,24 @@ int psw_conv_bwd_weight(int n, int c, int h, int w, int k, int r, int s, int str
     if (ws_bytes < need) return fail(PSW_ERR_WORKSPACE, "conv_bwd_weight: workspace %zu < %zu bytes", ws_bytes, need);
     return hip_check(psw::conv_bwd_weight(cs, x, dy, dw, dbias, prec == PSW_BF16, ws, ws_bytes, S(stream)),
                      "conv_bwd_weight");
+}
+
+int psw_conv_bwd_weight_noalloc(int n, int c, int h, int w, int k, int r, int s, int stride, int pad,
+                                const float* x, const float* dy, float* dw, float* dbias, int prec, void* stream)
+{
+    psw::ConvShape cs;
+    int rc = check_conv(n, c, h, w, k, r, s, stride, pad, prec, &cs);
+    if (rc) return rc;
+    if (!x || !dy || !dw) return fail(PSW_ERR_NULL, "conv_bwd_weight_noalloc: x, dy and dw are required");
+    const size_t need = psw::conv_bwd_weight_ws_bytes(cs, prec == PSW_BF16);
+    if (need > kScratchBytes)
+        return fail(PSW_ERR_WORKSPACE, "conv_bwd_weight_noalloc: shape needs %zu bytes of scratch, the limit is %zu",
+                    need, kScratchBytes);
+    void* ws = nullptr;
+    rc = scratch_of_current_device(&ws, "conv_bwd_weight_noalloc: scratch");
+    if (rc) return rc;
+    return hip_check(psw::conv_bwd_weight(cs, x, dy, dw, dbias, prec == PSW_BF16, ws, kScratchBytes, S(stream)),
+                     "conv_bwd_weight_noalloc");
 }
 
 size_t psw_bn_ws_bytes(int n, int c, int h, int w)

@@ -62,6 +62,7 @@ SIGNATURES = {
     "psw_conv_bwd_data": (_I, [_I] * 9 + [_P, _P, _P, _I, _I, _P]),
     "psw_conv_bwd_weight_ws_bytes": (_SZ, [_I] * 10),
     "psw_conv_bwd_weight": (_I, [_I] * 9 + [_P, _P, _P, _P, _I, _P, _SZ, _P]),
+    "psw_conv_bwd_weight_noalloc": (_I, [_I] * 9 + [_P, _P, _P, _P, _I, _P]),
     "psw_bn_ws_bytes": (_SZ, [_I] * 4),
     "psw_bn_relu_fwd": (_I, [_I] * 4 + [_P, _P, _P, _P, _I, _I, _I, _I, _F, _F, _P, _P, _P, _P, _P, _P, _SZ, _P]),
     "psw_bn_relu_bwd": (_I, [_I] * 4 + [_P] * 6 + [_I, _P, _P, _P, _P, _I, _I, _I, _I, _P, _SZ, _P]),
@@ -185,6 +186,14 @@ def psw_conv_bwd_weight(x, dy, dw, stride=1, pad=0, dbias=None, bf16=False, ws=N
         ws = torch.empty(max(nb, 1), dtype=torch.uint8, device=x.device)
     _check(lib().psw_conv_bwd_weight(n, c, h, wd, k, r, s, stride, pad, _ptr(x), _ptr(dy), _ptr(dw), _ptr(dbias),
                                      _prec(bf16), _ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
+
+
+def psw_conv_bwd_weight_noalloc(x, dy, dw, stride=1, pad=0, dbias=None, bf16=False, stream=None):
+    """psw_conv_bwd_weight without a workspace (the library's static scratch)."""
+    N, C, H, W = x.shape
+    K, _, R, S = dw.shape
+    _check(lib().psw_conv_bwd_weight_noalloc(N, C, H, W, K, R, S, stride, pad, _ptr(x), _ptr(dy), _ptr(dw),
+                                             _ptr(dbias), _prec(bf16), _stream(stream)))
 
 
 def psw_bn_ws_bytes(shape):
