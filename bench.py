@@ -21,23 +21,26 @@ Prints one JSON line.  `value` is images/s over the K timed steps.
 
 Measurement, in order: W warm-up steps (eager, including the pipeline
 fill), the graph capture and one untimed replay; the K timed steps (wall
-clock, no events); the other modes; then a profiling pass of min(K, 100)
-eager pipelined steps of the same workload in which every kernel is launched
-with a start / stop HIP event pair (hipExtLaunchKernelGGL).  The pair's time
-includes its own marker processing and dispatch, a few microseconds per
-launch that a rocprofv3 kernel trace does not count, different on each
-stream; every profiled step also launches one recorded empty kernel on each
-of its three streams, and every launch's time is the pair's time minus the
-empty kernels' mean on its stream (`event_overhead_us`; the raw pair times
-are reported beside as `avg_launch_us_events`).  That pass gives the
-per-kernel table, the conv
-matrix-core figure the metric names, and the dominant kernel (largest summed
-time): `roofline.achieved` = its algorithmic work per launch / its mean
-launch duration.  `roofline.traffic` is
-the HBM bytes per launch from rocprofv3 FETCH_SIZE / WRITE_SIZE counters
-(calibrated on a plain streaming kernel) stored in profiles/traffic.json,
-used only when the source files defining that kernel still hash to what was
-profiled, else null.
+clock, no events); the other modes; then a kernel-timing pass of
+REPLAY_STEPS eager pipelined steps of the same workload in which every
+kernel launch is replayed in isolation (psw_net_profile_replay): the
+library waits for the device to be idle, then issues the launch REPLAY_REPS
+times back to back on its stream between one start / stop event pair.  The
+mean per launch is the kernel's own duration plus the dispatch gap between
+consecutive launches of one stream, with no event-pair cost in it and no
+other stream's kernels beside it; a rocprofv3 kernel trace of the same
+command shows each replay as its own dispatch (paper_1912_12675_amd/
+rocprof_summary.py --replays pairs them up).  That pass gives the per-kernel
+table, the conv matrix-core figure the metric names (algorithmic conv FLOPs
+per step / summed conv kernel time per step) and the dominant kernel
+(largest summed time per step): `roofline.achieved` = its algorithmic work
+per launch / its mean launch time.  `conv_mfma.in_step` is the conv FLOPs
+per step over the whole step time instead (all kernels of the three
+streams sharing the chip).  `roofline.traffic` is the HBM bytes per launch
+from rocprofv3 FETCH_SIZE / WRITE_SIZE counters (calibrated on a plain
+streaming kernel) stored in profiles/traffic.json, used only when the
+source files defining that kernel still hash to what was profiled, else
+null.
 `cpu_baseline` times the CPU oracle on a bounded sample: 2-step runs of the
 same workload, repeated until 10 s of host time have passed (about 12 steps
 on 16 host threads).
@@ -61,8 +64,8 @@ METRIC = "training images/sec at 1 GPU (ResNet-20, batch 128) + conv MFMA % of p
 PEAK_FP32_MFMA = 157.3   # TFLOP/s, MI355X dense fp32 matrix
 PEAK_BF16_MFMA = 2500.0  # TFLOP/s, MI355X dense bf16 matrix
 PEAK_HBM = 8000.0        # GB/s, MI355X HBM3E
-PROFILE_STEPS = 100
-STREAM_NAMES = {0: "chain", 1: "weight", 2: "forward"}  # stream ids of the profile timeline
+REPLAY_STEPS = 3   # pipelined steps of the kernel-timing pass
+REPLAY_REPS = 20   # back-to-back launches per recorded launch
 COPY_BYTES = 256 << 20
 
 
@@ -121,6 +124,20 @@ def copy_calibration():
     print(json.dumps({"copy_bytes": COPY_BYTES, "launches": 5}), flush=True)
 
 
+def host_cpu():
+    """Model name of the host CPU and the number of logical CPUs this process may use."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return {"model": model, "logical_cpus_available": len(os.sched_getaffinity(0))}
+
+
 def cpu_baseline(wl, chunk=2, min_seconds=10.0, max_chunks=15):
     from oracle import oracle
     from paper_1912_12675_amd import synth
@@ -147,7 +164,7 @@ def cpu_baseline(wl, chunk=2, min_seconds=10.0, max_chunks=15):
     finally:
         oracle.set_threads(cores)
     return {"value": round(steps * wl.batch / dt, 3), "unit": "images/s", "cores": cores,
-            "kind": "oracle",
+            "kind": "oracle", "host": host_cpu(),
             "sample": f"{steps} stale-weight training steps of the same workload (ResNet-20, batch {wl.batch}, "
                       f"float64 direct loops, OpenMP; runs of {chunk} steps until {min_seconds:.0f} s), "
                       f"{dt:.1f} s",
@@ -166,7 +183,7 @@ def main():
                     help="pipelined: psw_pipeline_run issued eagerly (default); graph: the same steps replayed "
                          "from a captured HIP graph; sequential: one psw_stage_step call per step")
     ap.add_argument("--no-profile", action="store_true",
-                    help="no events at all: skip the profiling pass and the dominant-kernel timing")
+                    help="no events at all: skip the kernel-timing pass")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run a plain 256 MiB streaming kernel 5 times (counter calibration) and exit")
     args = ap.parse_args()
@@ -187,11 +204,10 @@ def main():
         return
     wl = synth.resnet20_workload(bf16=args.bf16)
     K, W = args.steps, args.warmup
-    KP = 0 if args.no_profile else min(K, PROFILE_STEPS)
     period = 3  # step sets of the pipelined run
     for d in wl.ring_depth():
         period = period * d // __import__("math").gcd(period, d)
-    T = W + period + KP + 3 * K + period
+    T = W + period + REPLAY_STEPS + 3 * K + period
     net = psw.Net(wl.ops, wl.batch, wl.in_shape, wl.stage_end, wl.ring_depth(T), bf16=wl.bf16)
     net.load_params(synth.init_params(wl))
     stal = wl.staleness(T)
@@ -205,7 +221,7 @@ def main():
         ys[i].copy_(torch.from_numpy(y))
     torch.cuda.synchronize()
     t = 0
-    losses = torch.zeros(max(K, W, KP, 1), dtype=torch.float32, device="cuda")
+    losses = torch.zeros(max(K, W, REPLAY_STEPS, 1), dtype=torch.float32, device="cuda")
 
     def run_sequential(n):
         nonlocal t
@@ -270,52 +286,37 @@ def main():
         torch.cuda.synchronize()
         others[name] = round(wl.batch * K / (time.perf_counter() - t1), 2)
 
-    # profiling pass over the same workload (eager pipelined: graphs carry
-    # no events): every kernel launched with a start / stop event pair.  The
-    # pair's own cost (marker processing and dispatch, a few microseconds per
-    # launch, different on each stream) is measured beside the work: every
-    # step also launches one recorded empty kernel on each of its three
-    # streams, and each launch's time is its pair's time minus the mean pair
-    # time of the empty kernels on its stream.
+    # kernel-timing pass over the same workload (eager pipelined: graphs carry
+    # no events): every launch replayed REPLAY_REPS times in isolation
     peak = PEAK_BF16_MFMA if wl.bf16 else PEAK_FP32_MFMA
-    kernels, breakdown, conv, roof, ovh_us = [], None, None, None, None
+    kernels, breakdown, conv, roof = [], None, None, None
+    KP = REPLAY_STEPS if not args.no_profile else 0
     if KP:
         net.profile(True)
+        net.profile_replay(REPLAY_REPS)
         run_pipelined(KP)
         torch.cuda.synchronize()
-        spans = net.profile_timeline()
-        work = {k["name"]: k for k in net.profile_kernels()}
+        kernels = sorted(net.profile_kernels(), key=lambda k: -k["ms"])
+        net.profile_replay(1)
         net.profile(False)
-        probes = {}
-        for name, kind, sid, t0_, t1_ in spans:
-            if name == "empty_probe_k":
-                probes.setdefault(sid, []).append(t1_ - t0_)
-        ovh = {sid: sum(v) / len(v) for sid, v in probes.items()}
-        ovh_us = {STREAM_NAMES.get(sid, str(sid)): round(v, 3) for sid, v in sorted(ovh.items())}
-        agg, kinds = {}, {}
-        for name, kind, sid, t0_, t1_ in spans:
-            if name == "empty_probe_k":
-                continue
-            a_ = agg.setdefault(name, [0.0, 0.0, 0])
-            a_[0] += max(t1_ - t0_ - ovh[sid], 0.0) * 1e-3
-            a_[1] += (t1_ - t0_) * 1e-3
-            a_[2] += 1
-            kinds[kind] = kinds.get(kind, 0.0) + max(t1_ - t0_ - ovh[sid], 0.0) * 1e-3
-        kernels = sorted(({"name": n, "kind": work[n]["kind"], "launches": v[2], "ms": v[0], "ms_events": v[1],
-                           "flops": work[n]["flops"], "bytes": work[n]["bytes"]} for n, v in agg.items()),
-                         key=lambda k: -k["ms"])
+        kinds = {}
+        for k in kernels:
+            kinds[k["kind"]] = kinds.get(k["kind"], 0.0) + k["ms"]
         breakdown = {k: round(v / KP, 4) for k, v in kinds.items()}
         ck = [k for k in kernels if k["kind"] in ("conv_fwd", "conv_bwd_data", "conv_bwd_weight")]
         conv_ms = sum(k["ms"] for k in ck) / KP
         conv_flop = sum(k["flops"] for k in ck) / KP
         ach = conv_flop / (conv_ms * 1e-3) / 1e12
+        in_step = conv_flop / (ms_per_step * 1e-3) / 1e12
         conv = {"achieved": round(ach, 3), "peak": peak, "unit": "TFLOP/s", "frac": round(ach / peak, 4),
                 "flop_per_step": conv_flop, "conv_kernel_ms_per_step": round(conv_ms, 4),
                 "conv_kernel_launches_per_step": sum(k["launches"] for k in ck) / KP,
-                "what": "all convolution kernels (forward, backward-data with fused BN sums, backward-weight): "
-                        "algorithmic conv FLOPs / summed kernel time; the backward-weight split partial sums are "
-                        "reduced inside the stage update kernel (sgd_stage_k), whose time is in kernel_ms_per_step.sgd "
-                        "and in frac_with_update"}
+                "in_step": {"achieved": round(in_step, 3), "frac": round(in_step / peak, 4),
+                            "what": "conv FLOPs per step / ms_per_step of the timed run"},
+                "what": "all convolution kernels (forward, backward-data with fused BN sums or folded BN backward, "
+                        "backward-weight): algorithmic conv FLOPs / summed kernel time, each kernel timed in "
+                        f"isolation as {REPLAY_REPS} back-to-back launches; the backward-weight split partial sums "
+                        "are reduced inside the stage update kernel (sgd_stage_k), counted in frac_with_update"}
         uk = [k for k in kernels if k["name"] == "sgd_stage_k"]
         if uk:
             ums = conv_ms + sum(k["ms"] for k in uk) / KP
@@ -323,23 +324,24 @@ def main():
         d = kernels[0]  # the dominant kernel: largest summed time
         roof = roofline_of(d, peak)
         roof["traffic"] = measured_traffic(d["name"])
-        roof.update({"kernel": d["name"], "launches": d["launches"], "avg_launch_us": round(1e3 * d["ms"] / d["launches"], 3),
-                     "avg_launch_us_events": round(1e3 * d["ms_events"] / d["launches"], 3),
-                     "event_overhead_us": ovh_us,
+        roof.update({"kernel": d["name"], "launches": d["launches"],
+                     "avg_launch_us": round(1e3 * d["ms"] / d["launches"], 3),
                      "flop_per_launch": d["flops"] / d["launches"], "bytes_per_launch": d["bytes"] / d["launches"],
-                     "timed_over": f"{KP} pipelined steps of the same workload after the timed region, every "
-                                   "kernel launched with a start/stop event pair; avg_launch_us = the pair's time "
-                                   "minus event_overhead_us of its stream, the mean pair time of one empty kernel "
-                                   "per step and stream"})
+                     "timed_over": f"{KP} pipelined steps of the same workload after the timed region; every launch "
+                                   f"replayed {REPLAY_REPS} times back to back on its stream with the device "
+                                   "otherwise idle, between one start/stop HIP event pair; avg_launch_us = the "
+                                   f"pair's time / {REPLAY_REPS}"})
     top = []
     for k in kernels[:10]:
         r = roofline_of(k, peak)
         top.append({"kernel": k["name"], "kind": k["kind"], "launches_per_step": k["launches"] / KP,
                     "us_per_step": round(1e3 * k["ms"] / KP, 2), "avg_launch_us": round(1e3 * k["ms"] / k["launches"], 3),
-                    "avg_launch_us_events": round(1e3 * k["ms_events"] / k["launches"], 3),
                     "bound": r["bound"], "achieved": r["achieved"], "unit": r["unit"], "frac": r["frac"],
                     "bytes_per_launch": k["bytes"] / k["launches"], "traffic": measured_traffic(k["name"])})
 
+    every = [{"kernel": k["name"], "kind": k["kind"], "launches_per_step": k["launches"] / KP,
+              "avg_launch_us": round(1e3 * k["ms"] / k["launches"], 3), "flop_per_launch": k["flops"] / k["launches"],
+              "bytes_per_launch": k["bytes"] / k["launches"]} for k in kernels]
     out = {
         "metric": METRIC,
         "value": round(img_s, 2),
@@ -365,6 +367,7 @@ def main():
         "conv_mfma": conv,
         "kernel_ms_per_step": breakdown,
         "top_kernels": top,
+        "kernels": every,
         "final_loss": round(loss, 5),
     }
     if not args.no_cpu_baseline:

@@ -427,7 +427,7 @@ typedef struct psw_kernel_stat {
     char name[192];
     int32_t kind;     /* PSW_PROF_* kind of its first launch */
     int64_t launches;
-    double ms;        /* summed event time */
+    double ms;        /* summed event time per launch */
     double flops;     /* summed algorithmic floating-point operations */
     double bytes;     /* summed algorithmic HBM bytes */
 } psw_kernel_stat;
@@ -435,16 +435,19 @@ int psw_net_profile(psw_net *net, int enable);
 int psw_net_profile_only(psw_net *net, int enable, const char *kernel);
 int psw_net_profile_read(psw_net *net, int n_kinds, double *ms, int64_t *launches);
 int psw_net_profile_kernels(psw_net *net, int cap, psw_kernel_stat *out, int *n_out);
-/* While profiling is on, psw_pipeline_run also launches one such empty
- * kernel on each of its three streams at the start of every step.
- * psw_net_profile_probe: while profiling is on, launches n empty kernels
- * (one workgroup of 64 threads, named "empty_probe_k", kind PSW_PROF_OTHER,
- * no work) on `stream`, recorded like every other launch.  Their event
- * time is what the event pair costs a launch that does nothing (marker
- * processing and dispatch), the part of every recorded time that is not
- * the kernel's execution; a caller running them beside the work it times
- * can subtract it.  PSW_ERR_STATE when profiling is off; n in [0, 1024]. */
-int psw_net_profile_probe(psw_net *net, int n, void *stream);
+/* psw_net_profile_replay: with reps > 1, every launch recorded from then on
+ * is timed in isolation instead: the library waits until the device is idle
+ * (hipDeviceSynchronize), then issues the kernel reps times back to back on
+ * its stream with the same arguments between a start and a stop event, and
+ * records the mean time per launch (ms of psw_kernel_stat and the kinds of
+ * psw_net_profile_read are per launch, launches count the recorded launch
+ * once).  This is the kernel's own duration plus the dispatch gap between
+ * consecutive launches on one stream, without the event pair's cost.  The
+ * replays repeat the launch's work on the same buffers (a kernel that
+ * accumulates or updates applies it reps times), so the numerical results of
+ * a replayed run are not those of the schedule: for timing only.  reps == 1
+ * (the default) restores one event pair per launch.  reps in [1, 1000]. */
+int psw_net_profile_replay(psw_net *net, int reps);
 /* psw_net_profile_timeline: one psw_kernel_span per recorded launch, in
  * issue order (at most cap; *n_out = the record count): start and end in
  * microseconds after the first record's start, and the stream it ran on

@@ -405,22 +405,31 @@ struct psw_net {
         psw::Work work;
         hipEvent_t a, b;
         int stream;  // 0 the caller's, 1 the weight stream, 2 the forward stream
+        int reps;    // launches between a and b
     };
     struct Recorder final : psw::KernelRecorder {
         psw_net* net = nullptr;
         int kind = PSW_PROF_OTHER;  // the launcher being issued
         std::string only;           // non-empty: time launches of this kernel only
-        bool begin(const std::string& name, hipEvent_t* start, hipEvent_t* stop) override
+        int replay = 1;             // > 1: isolated back-to-back replays (psw_net_profile_replay)
+        bool begin(const std::string& name, hipEvent_t* start, hipEvent_t* stop, int* reps) override
         {
             if (!only.empty() && name != only) return false;
             *start = net->next_event();
             *stop = *start ? net->next_event() : nullptr;
-            return *start && *stop;
+            if (!*start || !*stop) return false;
+            if (replay > 1) {
+                // the kernel runs alone: everything issued before it is done
+                if (hipDeviceSynchronize() != hipSuccess) return false;
+                *reps = replay;
+            }
+            return true;
         }
-        void end(std::string&& name, const psw::Work& w, hipEvent_t start, hipEvent_t stop, hipStream_t st) override
+        void end(std::string&& name, const psw::Work& w, hipEvent_t start, hipEvent_t stop, int reps,
+                 hipStream_t st) override
         {
             const int sid = st == net->side ? 1 : (st == net->fwd && st ? 2 : 0);
-            net->krecs.push_back(KRec{kind, std::move(name), w, start, stop, sid});
+            net->krecs.push_back(KRec{kind, std::move(name), w, start, stop, sid, reps});
         }
     };
     bool profiling = false;
@@ -1461,15 +1470,6 @@ int issue_pipeline(psw_net* net, int64_t t0, int n_steps, const int32_t* stalene
                   (float*)(P + net->pgrad_off)};
         for (int s = 0; s < S_; ++s) io.rv[s] = fwd_version(t, staleness[(size_t)i * S_ + s]);
         Issue is{net, io};
-        if (net->profiling) {  // one recorded empty kernel per stream and step (the chain's below): the event pair's own cost there
-            net->rec.kind = PSW_PROF_OTHER;
-            e = psw::empty_kernels(1, sf);
-            if (e == hipSuccess) e = psw::empty_kernels(1, sw);
-            if (e != hipSuccess) {
-                what = "pipeline: profile probe";
-                break;
-            }
-        }
         // forward of t: its step set is free once step t-NS is done with it
         // (the weight stream's last update of a step follows the chain's end)
         if (i >= NS) {
@@ -1495,10 +1495,6 @@ int issue_pipeline(psw_net* net, int64_t t0, int n_steps, const int32_t* stalene
         // backward of t after its forward
         e = hipEventRecord(net->fdone_ev, sf);
         if (e == hipSuccess) e = hipStreamWaitEvent(sb, net->fdone_ev, 0);
-        if (e == hipSuccess && net->profiling) {  // the chain's probe, where its kernels start
-            net->rec.kind = PSW_PROF_OTHER;
-            e = psw::empty_kernels(1, sb);
-        }
         if (e != hipSuccess) {
             what = "pipeline: backward order";
             break;
@@ -1685,15 +1681,12 @@ int psw_net_profile(psw_net* net, int enable)
     return psw_net_profile_only(net, enable, nullptr);
 }
 
-int psw_net_profile_probe(psw_net* net, int n, void* stream)
+int psw_net_profile_replay(psw_net* net, int reps)
 {
-    if (!net) return fail(PSW_ERR_NULL, "net_profile_probe: net is NULL");
-    if (!net->profiling) return fail(PSW_ERR_STATE, "net_profile_probe: profiling is off");
-    if (n < 0 || n > 1024) return fail(PSW_ERR_SHAPE, "net_profile_probe: n = %d outside [0, 1024]", n);
-    net->rec.kind = PSW_PROF_OTHER;
-    RecorderScope rec_scope(&net->rec);
-    const hipError_t e = psw::empty_kernels(n, S(stream));
-    return e == hipSuccess ? PSW_OK : hip_check(e, "net_profile_probe");
+    if (!net) return fail(PSW_ERR_NULL, "net_profile_replay: net is NULL");
+    if (reps < 1 || reps > 1000) return fail(PSW_ERR_SHAPE, "net_profile_replay: reps = %d outside [1, 1000]", reps);
+    net->rec.replay = reps;
+    return PSW_OK;
 }
 
 int psw_net_profile_only(psw_net* net, int enable, const char* kernel)
@@ -1713,7 +1706,7 @@ hipError_t krec_ms(const psw_net::KRec& r, double* ms)
     if (e != hipSuccess) return e;
     float t = 0.f;
     e = hipEventElapsedTime(&t, r.a, r.b);
-    *ms = t;
+    *ms = (double)t / r.reps;  // per launch
     return e;
 }
 }  // namespace

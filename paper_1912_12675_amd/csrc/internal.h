@@ -12,13 +12,16 @@ namespace psw {
 
 // ---- kernel timing hook -------------------------------------------------
 // While a recorder is installed on the calling thread (the scheduler does so
-// in its profiling mode), every kernel the library launches is launched with
-// hipExtLaunchKernelGGL and a start / stop event pair, which the runtime
-// stamps from the kernel's own dispatch (no extra packets in the stream), and
-// is reported with its name (template arguments spelled as the compiler
-// prints them) and its algorithmic work: the floating-point operations and
-// the minimal HBM bytes (each input read once, each output written once) of
-// what the kernel computes.
+// in its profiling mode), every kernel the library launches is timed with a
+// start / stop event pair and reported with its name (template arguments
+// spelled as the compiler prints them) and its algorithmic work: the
+// floating-point operations and the minimal HBM bytes (each input read once,
+// each output written once) of what the kernel computes.  begin() decides
+// how: *reps == 1 launches the kernel once with hipExtLaunchKernelGGL and the
+// pair stamped from its own dispatch; *reps > 1 replays it: the pair is
+// recorded on the stream around reps back-to-back launches of the same
+// kernel with the same arguments (the recorder has waited for the device to
+// be idle first, so the kernel runs alone).
 struct Work {
     double flops;
     double bytes;
@@ -26,9 +29,11 @@ struct Work {
 
 class KernelRecorder {
 public:
-    // false: do not time this launch; else *start / *stop are the events
-    virtual bool begin(const std::string& name, hipEvent_t* start, hipEvent_t* stop) = 0;
-    virtual void end(std::string&& name, const Work& w, hipEvent_t start, hipEvent_t stop, hipStream_t st) = 0;
+    // false: do not time this launch; else *start / *stop are the events and
+    // *reps (1 on entry) the number of back-to-back launches between them
+    virtual bool begin(const std::string& name, hipEvent_t* start, hipEvent_t* stop, int* reps) = 0;
+    virtual void end(std::string&& name, const Work& w, hipEvent_t start, hipEvent_t stop, int reps,
+                     hipStream_t st) = 0;
 
 protected:
     ~KernelRecorder() = default;
@@ -55,16 +60,23 @@ std::string kname(const char* base, T... v)
     do {                                                                                          \
         ::psw::KernelRecorder* psw_rec_ = ::psw::kernel_recorder();                               \
         hipEvent_t psw_e0_ = nullptr, psw_e1_ = nullptr;                                          \
+        int psw_reps_ = 1;                                                                        \
         std::string psw_name_;                                                                    \
         if (psw_rec_) {                                                                           \
             psw_name_ = NAME;                                                                     \
-            if (!psw_rec_->begin(psw_name_, &psw_e0_, &psw_e1_)) psw_rec_ = nullptr;              \
+            if (!psw_rec_->begin(psw_name_, &psw_e0_, &psw_e1_, &psw_reps_)) psw_rec_ = nullptr;  \
         }                                                                                         \
-        if (psw_rec_)                                                                             \
+        if (psw_rec_ && psw_reps_ > 1) {                                                          \
+            (void)hipEventRecord(psw_e0_, STREAM);                                                \
+            for (int psw_i_ = 0; psw_i_ < psw_reps_; ++psw_i_)                                    \
+                hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, __VA_ARGS__);              \
+            (void)hipEventRecord(psw_e1_, STREAM);                                                \
+        } else if (psw_rec_) {                                                                    \
             hipExtLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, psw_e0_, psw_e1_, 0, __VA_ARGS__); \
-        else                                                                                      \
+        } else {                                                                                  \
             hipLaunchKernelGGL(KERNEL, GRID, BLOCK, SHMEM, STREAM, __VA_ARGS__);                  \
-        if (psw_rec_) psw_rec_->end(std::move(psw_name_), WORK, psw_e0_, psw_e1_, STREAM);        \
+        }                                                                                         \
+        if (psw_rec_) psw_rec_->end(std::move(psw_name_), WORK, psw_e0_, psw_e1_, psw_reps_, STREAM); \
     } while (0)
 
 constexpr double kF = 4.0;  // bytes per float
@@ -223,9 +235,6 @@ hipError_t conv_bwd_weight_partials(const ConvShape& cs, const float* x, const f
 // The same for `count` convolutions of shape cs in one launch.
 hipError_t conv_bwd_weight_partials_group(const ConvShape& cs, const float* const* x, const float* const* dy,
                                           float* const* part, int count, int bf16, hipStream_t st);
-
-// n launches of an empty kernel (event-overhead probe of the profiler)
-hipError_t empty_kernels(int n, hipStream_t st);
 
 // ---- batch norm (+ residual) (+ ReLU) ----
 size_t bn_ws_bytes(int n, int c, int h, int w);

@@ -1132,17 +1132,6 @@ hipError_t bn_bwd_from_partials(int n, int c, int h, int w, const float* dz, con
     return hipGetLastError();
 }
 
-namespace {
-__global__ __launch_bounds__(64) void empty_probe_k(int) {}
-}  // namespace
-
-hipError_t empty_kernels(int n, hipStream_t st)
-{
-    for (int i = 0; i < n; ++i)
-        PSW_LAUNCH(kname("empty_probe_k"), (Work{0.0, 0.0}), empty_probe_k, dim3(1), dim3(64), 0, st, 0);
-    return hipGetLastError();
-}
-
 hipError_t maxpool_fwd(int n, int c, int h, int w, int k, int stride, const float* x, float* y, int32_t* argmax,
                        hipStream_t st)
 {

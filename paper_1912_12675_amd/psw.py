@@ -93,7 +93,7 @@ SIGNATURES = {
     "psw_net_profile_read": (_I, [_P, _I, _P, _P]),
     "psw_net_profile_kernels": (_I, [_P, _I, _P, _P]),
     "psw_net_profile_only": (_I, [_P, _I, ctypes.c_char_p]),
-    "psw_net_profile_probe": (_I, [_P, _I, _P]),
+    "psw_net_profile_replay": (_I, [_P, _I]),
     "psw_net_profile_timeline": (_I, [_P, _I, _P, _P]),
     "psw_net_pipeline_bytes": (_I, [_P, _P]),
     "psw_net_bind_pipeline": (_I, [_P, _P, _SZ]),
@@ -444,10 +444,10 @@ class Net:
         _check(lib().psw_net_profile_read(self.handle, len(PROF_KINDS), ms.ctypes.data, cnt.ctypes.data))
         return {k: (float(ms[i]), int(cnt[i])) for i, k in enumerate(PROF_KINDS)}
 
-    def profile_probe(self, n, stream=None):
-        """Launch n recorded empty kernels on `stream` (a torch stream; default the current one)."""
-        st = (stream or torch.cuda.current_stream()).cuda_stream
-        _check(lib().psw_net_profile_probe(self.handle, int(n), ctypes.c_void_p(st)))
+    def profile_replay(self, reps):
+        """Time every recorded launch in isolation as reps back-to-back launches (reps 1: one event pair
+        per launch); the replayed run's numbers are not the schedule's."""
+        _check(lib().psw_net_profile_replay(self.handle, int(reps)))
 
     def profile_timeline(self, cap=1 << 20):
         """[(name, kind, stream, start_us, end_us)] per recorded launch, in issue order."""

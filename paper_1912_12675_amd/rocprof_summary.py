@@ -4,6 +4,14 @@
         per-kernel table (calls per step, mean / total time) of a
         `rocprofv3 --kernel-trace --stats --output-format csv` run
 
+    python -m paper_1912_12675_amd.rocprof_summary replays KERNEL_TRACE_CSV --bench BENCH_JSON [--reps 20]
+        the kernel-timing pass of bench.py in a `rocprofv3 --kernel-trace`
+        run of the same command: runs of `reps` consecutive dispatches of one
+        kernel on one queue are its isolated replays; per kernel, the trace's
+        mean duration (end - start) and mean period (start to the next
+        replay's start, i.e. duration + dispatch gap) beside bench.py's event
+        time per launch for the same kernel
+
     python -m paper_1912_12675_amd.rocprof_summary traffic --kernel NAME [--kernel NAME ...] \
             --fetch PMC_CSV --write PMC_CSV --copy-fetch PMC_CSV --copy-write PMC_CSV \
             --copy-kernel SUBSTRING --copy-bytes B [--out profiles/traffic.json]
@@ -52,6 +60,34 @@ def kernel_stats(path: str):
                          "min_ns": float(r["MinNs"]), "max_ns": float(r["MaxNs"])})
     rows.sort(key=lambda r: -r["total_ns"])
     return rows
+
+
+def replay_runs(trace_csv: str, reps: int):
+    """{short kernel name: (durations_ns, periods_ns)} over the dispatches
+    that belong to runs of at least `reps` consecutive dispatches of the same
+    kernel on the same queue (the replays of bench.py's kernel-timing pass;
+    no kernel of the training step repeats itself like that)."""
+    by_queue = defaultdict(list)
+    with open(trace_csv) as f:
+        for r in csv.DictReader(f):
+            by_queue[r["Queue_Id"]].append((int(r["Start_Timestamp"]), int(r["End_Timestamp"]),
+                                            short_name(r["Kernel_Name"])))
+    out = defaultdict(lambda: ([], []))
+    for q, ds in by_queue.items():
+        ds.sort()
+        i = 0
+        while i < len(ds):
+            j = i
+            while j + 1 < len(ds) and ds[j + 1][2] == ds[i][2]:
+                j += 1
+            if j - i + 1 >= reps:
+                dur, per = out[ds[i][2]]
+                for k in range(i, j + 1):
+                    dur.append(ds[k][1] - ds[k][0])
+                    if k < j:
+                        per.append(ds[k + 1][0] - ds[k][0])
+            i = j + 1
+    return dict(out)
 
 
 def pmc_values(path: str, counter: str):
@@ -129,6 +165,10 @@ def main(argv=None):
     a.add_argument("csv")
     a.add_argument("--steps", type=int, required=True)
     a.add_argument("--top", type=int, default=25)
+    c = sub.add_parser("replays")
+    c.add_argument("trace")
+    c.add_argument("--bench", required=True, help="the JSON line bench.py printed in the same run")
+    c.add_argument("--reps", type=int, default=20)
     b = sub.add_parser("traffic")
     b.add_argument("--kernel", action="append", required=True)
     for k in ("fetch", "write", "copy_fetch", "copy_write", "copy_kernel"):
@@ -144,6 +184,42 @@ def main(argv=None):
             print(f"| `{r['name']}` | {r['calls'] / args.steps:.2f} | {r['avg_ns'] / 1e3:.2f} | "
                   f"{r['total_ns'] / args.steps / 1e3:.1f} | {100 * r['total_ns'] / tot:.1f}% |")
         print(f"\nall kernels: {tot / args.steps / 1e6:.4f} ms/step over {args.steps} steps")
+    elif args.cmd == "replays":
+        with open(args.bench) as f:
+            line = [l for l in f if l.startswith("{")][-1]
+        bench = json.loads(line)
+        every = {k["kernel"]: k for k in bench.get("kernels", [])}
+        ev = {k: v["avg_launch_us"] for k, v in every.items()}
+        roof = bench.get("roofline") or {}
+        runs = replay_runs(args.trace, args.reps)
+        print("| kernel | replays | trace mean duration us | trace mean period us | bench events us/launch | "
+              "events / period | events / duration |\n|---|---:|---:|---:|---:|---:|---:|")
+        for name in sorted(runs, key=lambda n: -_mean(runs[n][0]) * len(runs[n][0])):
+            dur, per = runs[name]
+            d, p_ = _mean(dur) / 1e3, (_mean(per) / 1e3 if per else float("nan"))
+            e = ev.get(name)
+            es = f"{e:.2f} | {e / p_:.3f} | {e / d:.3f}" if e else "- | - | -"
+            print(f"| `{name}` | {len(dur)} | {d:.2f} | {p_:.2f} | {es} |")
+        # the conv matrix-core figure and the dominant kernel's roofline, from
+        # the trace's durations and from bench's event times
+        conv = [k for k in every.values() if k["kind"] in ("conv_fwd", "conv_bwd_data", "conv_bwd_weight")]
+        if conv and all(k["kernel"] in runs for k in conv):
+            flop = sum(k["launches_per_step"] * k["flop_per_launch"] for k in conv)
+            t_tr = sum(k["launches_per_step"] * _mean(runs[k["kernel"]][0]) * 1e-9 for k in conv)
+            t_ev = sum(k["launches_per_step"] * k["avg_launch_us"] * 1e-6 for k in conv)
+            peak = (bench.get("conv_mfma") or {}).get("peak", 157.3)
+            print(f"\nconv kernels per step: {flop / 1e9:.3f} GFLOP; summed time {t_tr * 1e6:.1f} us (trace "
+                  f"durations) / {t_ev * 1e6:.1f} us (bench events): {flop / t_tr / 1e12:.2f} / "
+                  f"{flop / t_ev / 1e12:.2f} TFLOP/s = {flop / t_tr / 1e12 / peak:.4f} / "
+                  f"{flop / t_ev / 1e12 / peak:.4f} of {peak} TFLOP/s")
+        if roof.get("kernel") in runs and roof["kernel"] in every:
+            k = every[roof["kernel"]]
+            d = _mean(runs[roof["kernel"]][0]) * 1e-9
+            work = k["flop_per_launch"] if roof["bound"] == "mfma" else k["bytes_per_launch"]
+            scale = 1e12 if roof["bound"] == "mfma" else 1e9
+            print(f"dominant kernel `{roof['kernel']}` ({roof['bound']}): {work / d / scale:.1f} {roof['unit']} "
+                  f"from the trace's mean duration {d * 1e6:.2f} us = {work / d / scale / roof['peak']:.4f} of peak; "
+                  f"bench: {roof['achieved']} {roof['unit']} = {roof['frac']}")
     else:
         t = traffic(args.kernel, args.fetch, args.write, args.copy_fetch, args.copy_write, args.copy_kernel,
                     args.copy_bytes)

@@ -226,9 +226,9 @@ def test_stage_step_requires_binding(psw):
     L.psw_net_destroy(h.value)
 
 
-def test_profile_probe_argument_checks(psw):
-    """The event-overhead probe refuses a NULL net, a net that is not
-    profiling and a bad count before touching the GPU."""
+def test_profile_replay_argument_checks(psw):
+    """The replay setting refuses a NULL net and a count outside [1, 1000]
+    (host only, nothing launched)."""
     wl = synth.resnet20_workload(batch=2)
     L = psw.lib()
     layers = psw._layers(wl.ops)
@@ -237,11 +237,11 @@ def test_profile_probe_argument_checks(psw):
     h = ctypes.c_void_p()
     assert L.psw_net_create(layers, len(layers), 2, *wl.in_shape, se.ctypes.data, 4, rd.ctypes.data, 0,
                             ctypes.byref(h)) == 0
-    assert L.psw_net_profile_probe(None, 1, None) == -1
-    assert L.psw_net_profile_probe(h.value, 1, None) == -8  # profiling off
-    assert L.psw_net_profile(h.value, 1) == 0
-    assert L.psw_net_profile_probe(h.value, -1, None) == -2
-    assert L.psw_net_profile_probe(h.value, 1025, None) == -2
+    assert L.psw_net_profile_replay(None, 2) == -1
+    assert L.psw_net_profile_replay(h.value, 0) == -2
+    assert L.psw_net_profile_replay(h.value, 1001) == -2
+    assert L.psw_net_profile_replay(h.value, 20) == 0
+    assert L.psw_net_profile_replay(h.value, 1) == 0
     L.psw_net_destroy(h.value)
 
 

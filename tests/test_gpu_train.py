@@ -511,22 +511,26 @@ def test_full_size_against_oracle(P, name, factory, T):
     assert d_upd <= ubar and d_loss <= lbar
 
 
-def test_profile_probe_records_empty_kernels(P):
-    """psw_net_profile_probe launches recorded empty kernels beside the
-    profiled work: n launches, no algorithmic work, a positive event time."""
+def test_profile_replay_records_every_kernel(P):
+    """Replay profiling (psw_net_profile_replay): every kernel of a step is
+    recorded once per launch with a positive per-launch time, the same
+    launches as with one event pair per launch."""
     wl = synth.resnet20_workload(batch=4)
-    net = P.Net(wl.ops, 4, wl.in_shape, wl.stage_end, [4, 3, 2, 1])
-    net.load_params(synth.init_params(wl))
-    net.profile(True)
-    net.profile_probe(5)
-    x, y = synth.batch(wl, 0, 4)
-    net.step(0, [3, 2, 1, 0], wl.lr, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), wl.momentum)
-    torch.cuda.synchronize()
-    ks = {k["name"]: k for k in net.profile_kernels()}
-    net.profile(False)
-    probe = ks["empty_probe_k"]
-    assert probe["launches"] == 5 and probe["flops"] == 0 and probe["bytes"] == 0 and probe["ms"] > 0
-    assert any(k.startswith("conv3x3_direct") for k in ks)
+    counts = {}
+    for reps in (1, 5):
+        net = P.Net(wl.ops, 4, wl.in_shape, wl.stage_end, [4, 3, 2, 1])
+        net.load_params(synth.init_params(wl))
+        net.profile(True)
+        net.profile_replay(reps)
+        x, y = synth.batch(wl, 0, 4)
+        net.step(0, [3, 2, 1, 0], wl.lr, torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), wl.momentum)
+        torch.cuda.synchronize()
+        ks = net.profile_kernels()
+        net.profile(False)
+        assert all(k["ms"] > 0 for k in ks)
+        counts[reps] = {k["name"]: k["launches"] for k in ks}
+    assert counts[1] == counts[5]
+    assert any(k.startswith("conv3x3_direct") for k in counts[5])
 
 
 def test_bn_backward_folds_run(P):
