@@ -642,7 +642,7 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
             wsw = std::max(wsw, psw::conv_bwd_weight_ws_bytes(cs, prec == PSW_BF16));
             // BN right after this conv, on its output only: statistics in the conv epilogue
             const bool next_bn = i + 1 < n_layers && net->ops[i + 1].kind == PSW_OP_BN && net->ops[i + 1].in0 == i + 1;
-            const bool plain = !(o.flags & (PSW_F_BIAS | PSW_F_RELU)) && prec == PSW_FP32;
+            const bool plain = !(o.flags & (PSW_F_BIAS | PSW_F_RELU));
             const size_t pf = psw::conv_fwd_bnstats_part_floats(cs);
             net->fuse_stats[i] = next_bn && plain && pf > 0;
             if (net->fuse_stats[i]) ws = std::max(ws, pf * sizeof(float));
@@ -651,7 +651,7 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
             // the BN output's gradient and can also form the BN backward sums
             const bool prev_bn = i > 0 && net->ops[i - 1].kind == PSW_OP_BN && o.in0 == i && net->ops[i - 1].in0 > 0;
             const int tb = psw::conv_bwd_data_bnsums_tiles(cs);
-            net->fuse_bwd[i] = prev_bn && prec == PSW_FP32 && tb > 0;
+            net->fuse_bwd[i] = prev_bn && tb > 0;
             if (net->fuse_bwd[i]) ws = std::max(ws, (size_t)tb * cs.c * 2 * sizeof(float));
         } else if (o.kind == PSW_OP_FC) {
             ws = std::max(ws, psw::fc_bwd_ws_bytes(a.n, o.cin, o.cout));
@@ -670,7 +670,7 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
         const psw_layer& o = net->ops[i];
         const psw_layer& pc = net->ops[i - 1];
         const psw_layer& nc = net->ops[i + 1];
-        if (o.kind != PSW_OP_BN || o.in0 != i || prec != PSW_FP32) continue;
+        if (o.kind != PSW_OP_BN || o.in0 != i) continue;
         if (o.in1 == 0) continue;  // the residual is the net input: no gradient to write
         if (o.in1 > 0) {           // identity residual whose gradient this BN writes first
             const Tensor r = net->t[o.in1], yb = net->t[i];
@@ -1043,7 +1043,7 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
             net->fused_now[i] = 0;
             if (net->fuse_stats[i]) {  // the next op's BN statistics come out of this conv
                 psw::BnStatsFuse bn{(float*)ws};
-                e = psw::conv_fwd_bnstats(cs, is.act(o.in0), W, is.act(i + 1), bn, wsb / sizeof(float), sf);
+                e = psw::conv_fwd_bnstats(cs, is.act(o.in0), W, is.act(i + 1), bn, wsb / sizeof(float), bf16, sf);
                 if (e == hipSuccess)
                     net->fused_now[i] = 1;
                 else if (e != hipErrorNotSupported)  // not supported: nothing launched, unfused path below
@@ -1202,8 +1202,8 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
                     bnb.shift = bsave + 3 * bo.cin;
                 }
                 if (net->fold_bn[i - 1]) bnb.part = is.fold_part(i - 1);  // merged by the dgrad of op i-2
-                e = fold_in ? psw::conv_bwd_data_fold(cs, is.wbwd(i), din, acc0, &bnb, fold, sb)
-                            : psw::conv_bwd_data_bnsums(cs, is.wbwd(i), g, din, acc0, bnb, sb);
+                e = fold_in ? psw::conv_bwd_data_fold(cs, is.wbwd(i), din, acc0, &bnb, fold, bf16, sb)
+                            : psw::conv_bwd_data_bnsums(cs, is.wbwd(i), g, din, acc0, bnb, bf16, sb);
                 if (e == hipSuccess)
                     net->fused_bwd_now[i] = 1;
                 else if (e != hipErrorNotSupported)  // not supported: nothing launched, unfused path below
@@ -1212,7 +1212,7 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
             if (i >= 1) net->folded_now[i - 1] = net->fused_bwd_now[i] && net->fold_bn[i - 1];
             if (din && !net->fused_bwd_now[i]) {
                 if (fold_in)  // covered by construction (the fold's conditions when the net was created)
-                    PSW_TRY(psw::conv_bwd_data_fold(cs, is.wbwd(i), din, acc0, nullptr, fold, sb),
+                    PSW_TRY(psw::conv_bwd_data_fold(cs, is.wbwd(i), din, acc0, nullptr, fold, bf16, sb),
                             "conv_bwd_data (folded BN backward)");
                 else
                     PSW_TRY(psw::conv_bwd_data(cs, is.wbwd(i), g, din, acc0, bf16, sb), "conv_bwd_data");

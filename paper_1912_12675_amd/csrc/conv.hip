@@ -302,8 +302,9 @@ int wgrad_splits(const ConvShape& cs, int bf16)
 hipError_t conv_fwd(const ConvShape& cs, const float* x, const float* w, const float* bias, int relu, float* y,
                     int bf16, hipStream_t st)
 {
-    if (!bf16 && !bias && !relu && cs.r == 3 && cs.s == 3 && cs.pad == 1) {
-        hipError_t e = conv3x3_direct(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, w, y, 0, false, st);
+    if (!bias && !relu && cs.r == 3 && cs.s == 3 && cs.pad == 1) {
+        hipError_t e = conv3x3_direct(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, w, y, 0, false, st, nullptr, nullptr,
+                                      nullptr, bf16);
         if (e != hipErrorNotSupported) return e;
     }
     IgArgs a = make_args(cs);
@@ -322,24 +323,25 @@ int conv_fwd_bnstats_tiles(const ConvShape& cs)
 size_t conv_fwd_bnstats_part_floats(const ConvShape& cs) { return (size_t)conv_fwd_bnstats_tiles(cs) * cs.k * 2; }
 
 hipError_t conv_fwd_bnstats(const ConvShape& cs, const float* x, const float* w, float* y, const BnStatsFuse& bn,
-                            size_t part_capacity_floats, hipStream_t st)
+                            size_t part_capacity_floats, int bf16, hipStream_t st)
 {
     const size_t need = conv_fwd_bnstats_part_floats(cs);
     if (need == 0) return hipErrorNotSupported;
     if (part_capacity_floats < need) return hipErrorInvalidValue;
-    return conv3x3_direct(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, w, y, 0, false, st, &bn);
+    return conv3x3_direct(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, w, y, 0, false, st, &bn, nullptr, nullptr, bf16);
 }
 
 hipError_t conv_bwd_data(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate, int bf16,
                          hipStream_t st)
 {
-    if (!bf16 && cs.r == 3 && cs.s == 3 && cs.pad == 1 && cs.stride == 1) {
+    if (cs.r == 3 && cs.s == 3 && cs.pad == 1 && cs.stride == 1) {
         // stride-1 backward data = stride-1 conv of dy with transposed, flipped weights
-        hipError_t e = conv3x3_direct(cs.n, cs.k, cs.h, cs.w, cs.c, 1, dy, w, dx, accumulate, true, st);
+        hipError_t e = conv3x3_direct(cs.n, cs.k, cs.h, cs.w, cs.c, 1, dy, w, dx, accumulate, true, st, nullptr, nullptr,
+                                      nullptr, bf16);
         if (e != hipErrorNotSupported) return e;
     }
-    if (!bf16 && cs.r == 3 && cs.s == 3 && cs.pad == 1 && cs.stride == 2 && cs.h == 2 * cs.p && cs.w == 2 * cs.q) {
-        hipError_t e = conv3x3_dgrad_s2(cs.n, cs.c, cs.h, cs.w, cs.k, w, dy, dx, accumulate, st);
+    if (cs.r == 3 && cs.s == 3 && cs.pad == 1 && cs.stride == 2 && cs.h == 2 * cs.p && cs.w == 2 * cs.q) {
+        hipError_t e = conv3x3_dgrad_s2(cs.n, cs.c, cs.h, cs.w, cs.k, w, dy, dx, accumulate, st, nullptr, bf16);
         if (e != hipErrorNotSupported) return e;
     }
     IgArgs a = make_args(cs);
@@ -351,7 +353,8 @@ hipError_t conv_bwd_data(const ConvShape& cs, const float* w, const float* dy, f
 
 static bool use_direct_wgrad(const ConvShape& cs, int bf16)
 {
-    return !bf16 && cs.r == 3 && cs.s == 3 && cs.pad == 1 &&
+    (void)bf16;
+    return cs.r == 3 && cs.s == 3 && cs.pad == 1 &&
            conv3x3_wgrad_splits(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride) > 0;
 }
 
@@ -363,13 +366,15 @@ int conv_bwd_data_bnsums_tiles(const ConvShape& cs)
 }
 
 hipError_t conv_bwd_data_bnsums(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate,
-                                const BnBwdFuse& bnb, hipStream_t st)
+                                const BnBwdFuse& bnb, int bf16, hipStream_t st)
 {
     if (conv_bwd_data_bnsums_tiles(cs) == 0) return hipErrorNotSupported;
     if ((uintptr_t)bnb.z % 8 || (uintptr_t)bnb.y % 8) return hipErrorNotSupported;
     if (bnb.relu && !bnb.scale && !bnb.z) return hipErrorInvalidValue;
-    if (cs.stride == 1) return conv3x3_direct(cs.n, cs.k, cs.h, cs.w, cs.c, 1, dy, w, dx, accumulate, true, st, nullptr, &bnb);
-    return conv3x3_dgrad_s2(cs.n, cs.c, cs.h, cs.w, cs.k, w, dy, dx, accumulate, st, &bnb);
+    if (cs.stride == 1)
+        return conv3x3_direct(cs.n, cs.k, cs.h, cs.w, cs.c, 1, dy, w, dx, accumulate, true, st, nullptr, &bnb, nullptr,
+                              bf16);
+    return conv3x3_dgrad_s2(cs.n, cs.c, cs.h, cs.w, cs.k, w, dy, dx, accumulate, st, &bnb, bf16);
 }
 
 bool conv_bwd_data_fold_ok(const ConvShape& cs)
@@ -379,13 +384,14 @@ bool conv_bwd_data_fold_ok(const ConvShape& cs)
 }
 
 hipError_t conv_bwd_data_fold(const ConvShape& cs, const float* w, float* dx, int accumulate, const BnBwdFuse* bnb,
-                              const BnFold& fold, hipStream_t st)
+                              const BnFold& fold, int bf16, hipStream_t st)
 {
     if (!conv_bwd_data_fold_ok(cs)) return hipErrorNotSupported;
     if (bnb && (conv_bwd_data_bnsums_tiles(cs) == 0 || (uintptr_t)bnb->z % 8 || (uintptr_t)bnb->y % 8))
         return hipErrorNotSupported;
     if ((uintptr_t)fold.g % 16 || (uintptr_t)fold.y % 16) return hipErrorNotSupported;
-    return conv3x3_direct(cs.n, cs.k, cs.h, cs.w, cs.c, 1, fold.dy, w, dx, accumulate, true, st, nullptr, bnb, &fold);
+    return conv3x3_direct(cs.n, cs.k, cs.h, cs.w, cs.c, 1, fold.dy, w, dx, accumulate, true, st, nullptr, bnb, &fold,
+                          bf16);
 }
 
 size_t conv_bwd_weight_ws_bytes(const ConvShape& cs, int bf16)
@@ -407,14 +413,14 @@ hipError_t conv_bwd_weight_partials(const ConvShape& cs, const float* x, const f
                                     hipStream_t st)
 {
     if (!use_direct_wgrad(cs, bf16)) return hipErrorNotSupported;
-    return conv3x3_wgrad(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, part, st);
+    return conv3x3_wgrad(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, part, st, bf16);
 }
 
 hipError_t conv_bwd_weight_partials_group(const ConvShape& cs, const float* const* x, const float* const* dy,
                                           float* const* part, int count, int bf16, hipStream_t st)
 {
     if (!use_direct_wgrad(cs, bf16)) return hipErrorNotSupported;
-    return conv3x3_wgrad_group(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, part, count, st);
+    return conv3x3_wgrad_group(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, part, count, st, bf16);
 }
 
 hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy, float* dw, float* db, int bf16,
@@ -424,7 +430,7 @@ hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy,
     const size_t mn = (size_t)cs.k * cs.c * cs.r * cs.s;
     if (use_direct_wgrad(cs, bf16)) {
         const int zd = conv3x3_wgrad_splits(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride);
-        hipError_t e = conv3x3_wgrad(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, (float*)ws, st);
+        hipError_t e = conv3x3_wgrad(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, (float*)ws, st, bf16);
         if (e != hipErrorNotSupported) {  // otherwise (misaligned operands) fall through to the implicit GEMM
             if (e != hipSuccess) return e;
             PSW_LAUNCH(kname("reduce_splits"), (Work{(double)zd * mn, kF * (zd + 1.0) * mn}), reduce_splits,

@@ -24,6 +24,11 @@ namespace psw {
 namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef short v4s __attribute__((ext_vector_type(4)));
+
+// bfloat16 rounding (nearest even) of a float: its bits, and its value as a float
+__device__ __forceinline__ unsigned short bf16_bits(float f) { return __builtin_bit_cast(unsigned short, (__bf16)f); }
+__device__ __forceinline__ float bf16_round(float f) { return (float)(__bf16)f; }
 
 struct DirArgs {
     const float* x;  // input  [n][C][H][W]
@@ -70,6 +75,27 @@ constexpr int plane_stride_b(int lo, int wo, int stride, int rstr)
     }
     return best;
 }
+// bf16 quad-interleaved tile (8 bytes = 4 channels per pixel): bank-pair
+// collisions (16 pairs of 8 bytes) of the 16 lanes of one lane group reading
+// the pixels of a 16-pixel block, for a row stride rs (in 8-byte elements)
+constexpr int q_conflicts(int rs, int wo, int stride)
+{
+    int cnt[16] = {}, worst = 0;
+    for (int j = 0; j < 16; ++j) cnt[pix_off(j, wo, stride, rs) % 16]++;
+    for (int b = 0; b < 16; ++b) worst = cnt[b] > worst ? cnt[b] : worst;
+    return worst;
+}
+constexpr int row_stride_q(int lo, int wo, int stride)
+{
+    int best = lo, bestc = q_conflicts(lo, wo, stride);
+    for (int v = lo; v < lo + 16; ++v)
+        if (q_conflicts(v, wo, stride) < bestc) {
+            bestc = q_conflicts(v, wo, stride);
+            best = v;
+        }
+    return best;
+}
+
 // weight row stride (floats) of an LDS tile with `n` floats per output
 // channel: the smallest v >= n with v = 2 (mod 32), so that lanes
 // (m, g) -> m*v + 9*g hit distinct banks within each 32-lane half
@@ -84,7 +110,15 @@ constexpr int wrow(int n)
 // mask from the forward's scale and shift); 2 the same for a BN with an
 // identity residual (ReLU mask from the BN output z; the masked gradient
 // is also written to the residual's gradient)
-template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, bool TRANS, int TPW, int FOLD>
+// BF: bfloat16 operands (rounded to nearest even when staged) with fp32
+// accumulation.  With 16-channel chunks the products run on
+// v_mfma_f32_16x16x16_bf16 (k = 16 input channels of one tap): the input
+// tile is staged as bf16 with 4 channels interleaved per pixel (one 8-byte
+// read is a lane's B operand) and the weights as [m][tap][c] bf16 rows (one
+// 8-byte read is its A operand).  Narrower chunks (an image net's first
+// layer) keep the fp32 layout and matrix op on operands rounded to bf16,
+// which forms the same exact products.
+template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, bool TRANS, int TPW, int FOLD, bool BF>
 __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
 {
     static_assert(!FOLD || (TRANS && STRIDE == 1 && TPW == 1), "folded BN backward: stride-1 backward data");
@@ -97,9 +131,17 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     constexpr int WR = wrow(CC * 9);
     static_assert(TH * WO == 16 * NBW * WP, "pixel tiling");
     static_assert(CC % 4 == 0 && WIN % 4 == 0, "tiling");
-    static_assert(CC * PS >= 2 * WP * TK, "input tile reused by the statistics epilogue");
-    __shared__ __attribute__((aligned(16))) float Xs[CC * PS];
-    __shared__ float Wc[TK * WR];
+    constexpr bool BMF = BF && CC % 16 == 0;                    // bf16 matrix op
+    constexpr int RSQ = row_stride_q(RSTR, WO, STRIDE);         // (BMF) row stride, 8-byte elements
+    constexpr int QPS = HR * RSQ;                               // (BMF) plane stride of a channel quad
+    constexpr int WRQ = wrow(CC * 9 / 2);                       // (BMF) weight row stride, dwords
+    constexpr int XS_FLOATS = BMF ? (CC / 4) * QPS * 2 : CC * PS;
+    constexpr int WC_FLOATS = BMF ? TK * WRQ : TK * WR;
+    static_assert(XS_FLOATS >= 2 * WP * TK, "input tile reused by the statistics epilogue");
+    __shared__ __attribute__((aligned(16))) float Xs[XS_FLOATS];
+    __shared__ __attribute__((aligned(16))) float Wc[WC_FLOATS];
+    unsigned short* const Xh = reinterpret_cast<unsigned short*>(Xs);  // (BMF) bf16 views
+    unsigned short* const Wh = reinterpret_cast<unsigned short*>(Wc);
     // folded BN backward: per input channel (a, b, d, mean, invstd, scale, shift)
     __shared__ __attribute__((aligned(16))) float ftab[FOLD ? kFoldMaxChannels * 8 : 4];
 
@@ -111,22 +153,32 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     const int mblk = blockIdx.y * TK;
     const int g = lane >> 4, j = lane & 15;
 
-    int boff[NBW];
+    int boff[NBW];  // B operand: fp32 layout, float offset; BMF, byte offset of the 8-byte element
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
         const int pix = (wp * NBW + nb) * 16 + j;
         const int row = pix / WO, col = pix - (pix / WO) * WO;
-        boff[nb] = g * PS + row * STRIDE * RSTR + col * STRIDE + 3;
+        boff[nb] = BMF ? (g * QPS + row * STRIDE * RSQ + col * STRIDE + 3) * 8
+                       : g * PS + row * STRIDE * RSTR + col * STRIDE + 3;
     }
     v4f acc[NBW];
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) acc[nb] = v4f{0.f, 0.f, 0.f, 0.f};
 
     // halo columns: never overwritten by the staging loop below
-    for (int i = tid; i < CC * HR; i += NT) {
-        const int c = i / HR, rr = i - (i / HR) * HR;
-        Xs[c * PS + rr * RSTR + 3] = 0.f;
-        if (STRIDE == 1) Xs[c * PS + rr * RSTR + WIN + 4] = 0.f;
+    if constexpr (BMF) {
+        for (int i = tid; i < (CC / 4) * HR; i += NT) {
+            const int cq = i / HR, rr = i - (i / HR) * HR;
+            uint2* row = reinterpret_cast<uint2*>(Xs) + cq * QPS + rr * RSQ;
+            row[3] = make_uint2(0u, 0u);
+            if (STRIDE == 1) row[WIN + 4] = make_uint2(0u, 0u);
+        }
+    } else {
+        for (int i = tid; i < CC * HR; i += NT) {
+            const int c = i / HR, rr = i - (i / HR) * HR;
+            Xs[c * PS + rr * RSTR + 3] = 0.f;
+            if (STRIDE == 1) Xs[c * PS + rr * RSTR + WIN + 4] = 0.f;
+        }
     }
 
     // software pipeline over input-channel chunks: the next chunk's tile and
@@ -151,12 +203,15 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
         const int c = i / (HR * Q4);
         const int rem = i - c * (HR * Q4);
         const int rr = rem / Q4, q4 = rem - (rem / Q4) * Q4;
-        xl[k] = c * PS + rr * RSTR + 4 + q4 * 4;
+        // fp32: float offset of the 4 pixels; BMF: bf16 offset of the first
+        // pixel's slot of channel c (the next pixels are 4 bf16 apart)
+        xl[k] = BMF ? ((c / 4) * QPS + rr * RSQ + 4 + q4 * 4) * 4 + (c % 4) : c * PS + rr * RSTR + 4 + q4 * 4;
         xg[k] = (c * HIN + rr) * WIN + q4 * 4;
         xrow[k] = rr;
         xch[k] = i < XN ? c : CC;  // CC: past the chunk (never loaded or stored)
     }
     int wl[WV], wg[WV], wc[WV];  // forward: LDS offset, offset from channel 0, channel; transposed: run base
+    int wq[BMF ? WV : 1][4];     // BMF: bf16 LDS offset of each of the 4 weights, [m][tap][c] rows
 #pragma unroll
     for (int k = 0; k < WV; ++k) {
         const int i = (tid + k * NT) * 4;
@@ -172,6 +227,24 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
             wc[k] = c;
         }
         if (i >= WN4 * 4) wc[k] = -1;  // past the weights of a chunk
+        if constexpr (BMF) {
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                int m, c, tap;
+                if (!TRANS) {  // run of output channel m: (c, tap) = divmod(rem + e, 9)
+                    m = i / (CC * 9);
+                    const int r2 = i - m * (CC * 9) + e;
+                    c = r2 / 9;
+                    tap = r2 - c * 9;
+                } else {       // run of input channel c: (m, 8 - tap) = divmod(rem + e, 9), taps flipped
+                    c = i / (TK * 9);
+                    const int r2 = i - c * (TK * 9) + e;
+                    m = r2 / 9;
+                    tap = 8 - (r2 - m * 9);
+                }
+                wq[k][e] = m * 2 * WRQ + tap * CC + c;
+            }
+        }
     }
     float4 xr[XV];
     float4 wr[WV];
@@ -258,6 +331,20 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
                 }
         }
     };
+    // one staged float4 of the input tile (4 pixels of one channel)
+    auto put_x = [&](int k, float4 v) {
+        if constexpr (BMF) {
+            Xh[xl[k]] = bf16_bits(v.x);
+            Xh[xl[k] + 4] = bf16_bits(v.y);
+            Xh[xl[k] + 8] = bf16_bits(v.z);
+            Xh[xl[k] + 12] = bf16_bits(v.w);
+        } else if constexpr (BF) {
+            *reinterpret_cast<float4*>(&Xs[xl[k]]) =
+                make_float4(bf16_round(v.x), bf16_round(v.y), bf16_round(v.z), bf16_round(v.w));
+        } else {
+            *reinterpret_cast<float4*>(&Xs[xl[k]]) = v;
+        }
+    };
     auto store_chunk = [&](int img, int ih0, int c0) {
         (void)img;
         (void)ih0;
@@ -288,18 +375,26 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
                     o = make_float4(r[0], r[1], r[2], r[3]);
                     if constexpr (FOLD == 2) fyr[k] = make_float4(gms[0], gms[1], gms[2], gms[3]);  // the residual's gradient
                 }
-                *reinterpret_cast<float4*>(&Xs[xl[k]]) = o;
+                put_x(k, o);
                 xr[k] = o;  // written out by write_dy
             }
         } else {
 #pragma unroll
             for (int k = 0; k < XV; ++k)
-                if ((k + 1) * NT <= XN || xch[k] < CC) *reinterpret_cast<float4*>(&Xs[xl[k]]) = xr[k];
+                if ((k + 1) * NT <= XN || xch[k] < CC) put_x(k, xr[k]);
         }
 #pragma unroll
         for (int k = 0; k < WV; ++k) {
             if (!((k + 1) * NT * 4 <= WN4 * 4 || wc[k] >= 0)) continue;
-            const float vv[4] = {wr[k].x, wr[k].y, wr[k].z, wr[k].w};
+            float vv[4] = {wr[k].x, wr[k].y, wr[k].z, wr[k].w};
+            if constexpr (BMF) {
+#pragma unroll
+                for (int e = 0; e < 4; ++e) Wh[wq[k][e]] = bf16_bits(vv[e]);
+                continue;
+            }
+            if constexpr (BF)
+#pragma unroll
+                for (int e = 0; e < 4; ++e) vv[e] = bf16_round(vv[e]);
             if (!TRANS) {
 #pragma unroll
                 for (int e = 0; e < 4; ++e) Wc[wl[k] + e] = vv[e];  // a run never crosses m (CC*9 % 4 == 0)
@@ -406,20 +501,41 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
             load_chunk(img, oh0 * STRIDE - 1, c0 + CC);
         else if (q + 1 < TPW)
             load_chunk((tl + 1) / tiles, ((tl + 1) % tiles) * TH * STRIDE - 1, 0);
-        const float* wf = Wc + (wk * 16 + j) * WR + g * 9;
+        if constexpr (BMF) {
+            // lane (j, g): A = weights of output channel j, channels 4g..4g+3 of
+            // the 16-channel group, one tap; B = those 4 channels of pixel j
+            const char* wfb = reinterpret_cast<const char*>(Wc) + (wk * 16 + j) * WRQ * 4 + g * 8;
+            const char* xfb = reinterpret_cast<const char*>(Xs);
 #pragma unroll
-        for (int c4 = 0; c4 < CC / 4; ++c4)
+            for (int c16 = 0; c16 < CC / 16; ++c16)
 #pragma unroll
-            for (int r = 0; r < 3; ++r)
+                for (int r = 0; r < 3; ++r)
 #pragma unroll
-                for (int s = 0; s < 3; ++s) {
-                    const float av = wf[c4 * 36 + r * 3 + s];
+                    for (int s = 0; s < 3; ++s) {
+                        const v4s av = *reinterpret_cast<const v4s*>(wfb + ((r * 3 + s) * CC + c16 * 16) * 2);
 #pragma unroll
-                    for (int nb = 0; nb < NBW; ++nb) {
-                        const float bv = Xs[boff[nb] + c4 * 4 * PS + r * RSTR + s];
-                        acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[nb], 0, 0, 0);
+                        for (int nb = 0; nb < NBW; ++nb) {
+                            const v4s bv = *reinterpret_cast<const v4s*>(
+                                xfb + boff[nb] + (c16 * 4 * QPS + r * RSQ + s) * 8);
+                            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, bv, acc[nb], 0, 0, 0);
+                        }
                     }
-                }
+        } else {
+            const float* wf = Wc + (wk * 16 + j) * WR + g * 9;
+#pragma unroll
+            for (int c4 = 0; c4 < CC / 4; ++c4)
+#pragma unroll
+                for (int r = 0; r < 3; ++r)
+#pragma unroll
+                    for (int s = 0; s < 3; ++s) {
+                        const float av = wf[c4 * 36 + r * 3 + s];
+#pragma unroll
+                        for (int nb = 0; nb < NBW; ++nb) {
+                            const float bv = Xs[boff[nb] + c4 * 4 * PS + r * RSTR + s];
+                            acc[nb] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, acc[nb], 0, 0, 0);
+                        }
+                    }
+        }
     }
 
     // epilogue: every global load is issued before the first store (the
@@ -591,7 +707,10 @@ struct DgArgs {
     BnBwdFuse bnb;    // bnb.part == nullptr: no backward sums
 };
 
-template <int WO, int TH, int CC, int WK, int WP, int NBW>
+// BF: bf16 operands on v_mfma_f32_16x16x16_bf16 (16 dy channels per k-step),
+// staged as in conv3x3_direct (dy tile with 4 channels interleaved per
+// pixel, weights as [m][tap][c] bf16 rows).
+template <int WO, int TH, int CC, int WK, int WP, int NBW, bool BF>
 __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
 {
     constexpr int NT = 64 * WK * WP;
@@ -601,9 +720,17 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
     constexpr int TK = 16 * WK;
     constexpr int WR = wrow(CC * 9);
     static_assert(TH * WO == 16 * NBW * WP, "pixel tiling");
-    static_assert(CC * PS >= 2 * WP * TK, "input tile reused by the backward-sums epilogue");
-    __shared__ __attribute__((aligned(16))) float Xs[CC * PS];
-    __shared__ float Wc[TK * WR];
+    static_assert(!BF || CC % 16 == 0, "bf16: 16-channel chunks");
+    constexpr int RSQ = row_stride_q(RSTR, WO, 1);  // (BF) row stride, 8-byte elements
+    constexpr int QPS = HR * RSQ;                   // (BF) plane stride of a channel quad
+    constexpr int WRQ = wrow(CC * 9 / 2);           // (BF) weight row stride, dwords
+    constexpr int XS_FLOATS = BF ? (CC / 4) * QPS * 2 : CC * PS;
+    constexpr int WC_FLOATS = BF ? TK * WRQ : TK * WR;
+    static_assert(XS_FLOATS >= 2 * WP * TK, "input tile reused by the backward-sums epilogue");
+    __shared__ __attribute__((aligned(16))) float Xs[XS_FLOATS];
+    __shared__ __attribute__((aligned(16))) float Wc[WC_FLOATS];
+    unsigned short* const Xh = reinterpret_cast<unsigned short*>(Xs);
+    unsigned short* const Wh = reinterpret_cast<unsigned short*>(Wc);
 
     const int tiles = a.HO / TH;
     const int img = blockIdx.x / tiles;
@@ -613,11 +740,12 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
     const int mblk = blockIdx.y * TK;
     const int g = lane >> 4, j = lane & 15;
 
-    int boff[NBW];
+    int boff[NBW];  // fp32: float offset; BF: byte offset of the 8-byte element
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb) {
         const int pix = (wp * NBW + nb) * 16 + j;
-        boff[nb] = g * PS + (pix / WO) * RSTR + (pix - (pix / WO) * WO);
+        boff[nb] = BF ? (g * QPS + (pix / WO) * RSQ + (pix - (pix / WO) * WO)) * 8
+                      : g * PS + (pix / WO) * RSTR + (pix - (pix / WO) * WO);
     }
     v4f acc[NBW][4];  // [block][class ph*2+pw]
 #pragma unroll
@@ -625,9 +753,16 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
 #pragma unroll
         for (int q = 0; q < 4; ++q) acc[nb][q] = v4f{0.f, 0.f, 0.f, 0.f};
 
-    for (int i = tid; i < CC * HR; i += NT) {
-        const int c = i / HR, rr = i - (i / HR) * HR;
-        Xs[c * PS + rr * RSTR + WO] = 0.f;
+    if constexpr (BF) {
+        for (int i = tid; i < (CC / 4) * HR; i += NT) {
+            const int cq = i / HR, rr = i - (i / HR) * HR;
+            reinterpret_cast<uint2*>(Xs)[cq * QPS + rr * RSQ + WO] = make_uint2(0u, 0u);
+        }
+    } else {
+        for (int i = tid; i < CC * HR; i += NT) {
+            const int c = i / HR, rr = i - (i / HR) * HR;
+            Xs[c * PS + rr * RSTR + WO] = 0.f;
+        }
     }
     // Software pipeline over chunks of CC dy channels: the next chunk's dy
     // tile and weights are loaded into registers while the current one is
@@ -646,7 +781,8 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
         const int c = i / (HR * Q4), rem = i - (i / (HR * Q4)) * (HR * Q4);
         const int rr = rem / Q4, q4 = rem - (rem / Q4) * Q4;
         xon[k] = i < XN;
-        xl[k] = c * PS + rr * RSTR + q4 * 4;
+        // fp32: float offset of the 4 pixels; BF: bf16 offset of the first pixel's slot of channel c
+        xl[k] = BF ? ((c / 4) * QPS + rr * RSQ + q4 * 4) * 4 + (c % 4) : c * PS + rr * RSTR + q4 * 4;
         xg[k] = (c * a.HO + rr) * WO + q4 * 4;  // from (plane c0, row i0)
         xrow[k] = rr;
     }
@@ -661,7 +797,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
 #pragma unroll
         for (int e = 0; e < 4; ++e) {  // a run of 4 never crosses c (TK*9 % 4 == 0)
             const int m = (rem + e) / 9, rs = (rem + e) - ((rem + e) / 9) * 9;
-            wl[k][e] = m * WR + c * 9 + rs;
+            wl[k][e] = BF ? m * 2 * WRQ + rs * CC + c : m * WR + c * 9 + rs;
         }
     }
     float4 xr[XV], wr[WV];
@@ -683,17 +819,62 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
         __syncthreads();  // the previous chunk's LDS reads are complete
 #pragma unroll
         for (int k = 0; k < XV; ++k)
-            if (xon[k]) *reinterpret_cast<float4*>(&Xs[xl[k]]) = xr[k];
+            if (xon[k]) {
+                if constexpr (BF) {
+                    Xh[xl[k]] = bf16_bits(xr[k].x);
+                    Xh[xl[k] + 4] = bf16_bits(xr[k].y);
+                    Xh[xl[k] + 8] = bf16_bits(xr[k].z);
+                    Xh[xl[k] + 12] = bf16_bits(xr[k].w);
+                } else {
+                    *reinterpret_cast<float4*>(&Xs[xl[k]]) = xr[k];
+                }
+            }
 #pragma unroll
         for (int k = 0; k < WV; ++k)
             if (won[k]) {
-                Wc[wl[k][0]] = wr[k].x;
-                Wc[wl[k][1]] = wr[k].y;
-                Wc[wl[k][2]] = wr[k].z;
-                Wc[wl[k][3]] = wr[k].w;
+                if constexpr (BF) {
+                    Wh[wl[k][0]] = bf16_bits(wr[k].x);
+                    Wh[wl[k][1]] = bf16_bits(wr[k].y);
+                    Wh[wl[k][2]] = bf16_bits(wr[k].z);
+                    Wh[wl[k][3]] = bf16_bits(wr[k].w);
+                } else {
+                    Wc[wl[k][0]] = wr[k].x;
+                    Wc[wl[k][1]] = wr[k].y;
+                    Wc[wl[k][2]] = wr[k].z;
+                    Wc[wl[k][3]] = wr[k].w;
+                }
             }
         __syncthreads();
         if (c0 + CC < a.KL) load_chunk(c0 + CC);
+        if constexpr (BF) {
+            // lane (j, g): A = weights of dx channel j, dy channels 4g..4g+3 of
+            // the 16-channel group, one tap; B = those dy channels at one position
+            const char* wfb = reinterpret_cast<const char*>(Wc) + (wk * 16 + j) * WRQ * 4 + g * 8;
+            const char* xfb = reinterpret_cast<const char*>(Xs);
+#pragma unroll
+            for (int c16 = 0; c16 < CC / 16; ++c16) {
+                v4s w9[9];
+#pragma unroll
+                for (int t = 0; t < 9; ++t) w9[t] = *reinterpret_cast<const v4s*>(wfb + (t * CC + c16 * 16) * 2);
+#pragma unroll
+                for (int nb = 0; nb < NBW; ++nb) {
+                    const char* xb = xfb + boff[nb] + c16 * 4 * QPS * 8;
+                    const v4s b00 = *reinterpret_cast<const v4s*>(xb), b01 = *reinterpret_cast<const v4s*>(xb + 8);
+                    const v4s b10 = *reinterpret_cast<const v4s*>(xb + RSQ * 8);
+                    const v4s b11 = *reinterpret_cast<const v4s*>(xb + RSQ * 8 + 8);
+                    acc[nb][0] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(w9[4], b00, acc[nb][0], 0, 0, 0);
+                    acc[nb][1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(w9[3], b01, acc[nb][1], 0, 0, 0);
+                    acc[nb][1] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(w9[5], b00, acc[nb][1], 0, 0, 0);
+                    acc[nb][2] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(w9[1], b10, acc[nb][2], 0, 0, 0);
+                    acc[nb][2] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(w9[7], b00, acc[nb][2], 0, 0, 0);
+                    acc[nb][3] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(w9[0], b11, acc[nb][3], 0, 0, 0);
+                    acc[nb][3] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(w9[2], b10, acc[nb][3], 0, 0, 0);
+                    acc[nb][3] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(w9[6], b01, acc[nb][3], 0, 0, 0);
+                    acc[nb][3] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(w9[8], b00, acc[nb][3], 0, 0, 0);
+                }
+            }
+            continue;
+        }
         const float* wf = Wc + (wk * 16 + j) * WR + g * 9;
 #pragma unroll
         for (int c4 = 0; c4 < CC / 4; ++c4) {
@@ -835,8 +1016,24 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
     }
 }
 
+template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, int TPW, bool TRANS, int FOLD, bool BF>
+void launch_direct_k(const DirArgs& a, dim3 grid, dim3 block, const Work& wk, hipStream_t st)
+{
+    PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, TRANS, TPW, FOLD, BF), wk,
+               (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, TRANS, TPW, FOLD, BF>), grid, block, 0, st, a);
+}
+
+template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, int TPW, bool TRANS, int FOLD>
+void launch_direct_p(const DirArgs& a, dim3 grid, dim3 block, const Work& wk, bool bf, hipStream_t st)
+{
+    if (bf)
+        launch_direct_k<WO, STRIDE, TH, CC, WK, WP, NBW, TPW, TRANS, FOLD, true>(a, grid, block, wk, st);
+    else
+        launch_direct_k<WO, STRIDE, TH, CC, WK, WP, NBW, TPW, TRANS, FOLD, false>(a, grid, block, wk, st);
+}
+
 template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, int TPW = 1>
-hipError_t launch_direct(const DirArgs& a, int n, bool trans, hipStream_t st)
+hipError_t launch_direct(const DirArgs& a, int n, bool trans, bool bf, hipStream_t st)
 {
     if ((n * (a.HO / TH)) % TPW) return hipErrorNotSupported;
     dim3 grid(n * (a.HO / TH) / TPW, a.K / (16 * WK));
@@ -852,20 +1049,16 @@ hipError_t launch_direct(const DirArgs& a, int n, bool trans, hipStream_t st)
     if (trans && a.fold.g) {
         if constexpr (STRIDE == 1 && TPW == 1) {
             if (a.fold.dres)
-                PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, 2), wk,
-                           (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, 2>), grid, block, 0, st, a);
+                launch_direct_p<WO, STRIDE, TH, CC, WK, WP, NBW, TPW, true, 2>(a, grid, block, wk, bf, st);
             else
-                PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, 1), wk,
-                           (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, 1>), grid, block, 0, st, a);
+                launch_direct_p<WO, STRIDE, TH, CC, WK, WP, NBW, TPW, true, 1>(a, grid, block, wk, bf, st);
         } else {
             return hipErrorNotSupported;
         }
     } else if (trans) {
-        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, 0), wk,
-                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, true, TPW, 0>), grid, block, 0, st, a);
+        launch_direct_p<WO, STRIDE, TH, CC, WK, WP, NBW, TPW, true, 0>(a, grid, block, wk, bf, st);
     } else {
-        PSW_LAUNCH(kname("conv3x3_direct", WO, STRIDE, TH, CC, WK, WP, NBW, false, TPW, 0), wk,
-                   (conv3x3_direct<WO, STRIDE, TH, CC, WK, WP, NBW, false, TPW, 0>), grid, block, 0, st, a);
+        launch_direct_p<WO, STRIDE, TH, CC, WK, WP, NBW, TPW, false, 0>(a, grid, block, wk, bf, st);
     }
     return hipGetLastError();
 }
@@ -904,7 +1097,7 @@ bool conv3x3_direct_covers(int n, int C, int H, int W, int K, int stride, bool t
 
 hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const float* x, const float* w, float* y,
                           int accumulate, bool transpose, hipStream_t st, const BnStatsFuse* bn, const BnBwdFuse* bnb,
-                          const BnFold* fold)
+                          const BnFold* fold, bool bf16)
 {
     if (bnb && (!transpose || stride != 1)) return hipErrorNotSupported;
     if (fold && (!transpose || stride != 1 || C > kFoldMaxChannels || (C & (C - 1)) || !fold->g || !fold->y ||
@@ -925,17 +1118,17 @@ hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const f
     if (bnb) a.bnb = *bnb;
     if (fold) a.fold = *fold;
     if (C <= 4 && stride == 1 && !transpose) {  // first layer of an image net (3 input channels)
-        if (WO == 32 && HO % 8 == 0 && K % 16 == 0) return launch_direct<32, 1, 8, 4, 1, 4, 4>(a, n, false, st);
+        if (WO == 32 && HO % 8 == 0 && K % 16 == 0) return launch_direct<32, 1, 8, 4, 1, 4, 4>(a, n, false, bf16, st);
         return hipErrorNotSupported;
     }
     if (C % 16) return hipErrorNotSupported;
     if (stride == 1) {
-        if (WO == 32 && HO % 8 == 0 && K % 16 == 0) return launch_direct<32, 1, 8, 16, 1, 4, 4>(a, n, transpose, st);
-        if (WO == 16 && HO % 8 == 0 && K % 32 == 0) return launch_direct<16, 1, 8, 16, 2, 4, 2>(a, n, transpose, st);
-        if (WO == 8 && HO % 8 == 0 && K % 32 == 0) return launch_direct<8, 1, 8, 16, 2, 4, 1>(a, n, transpose, st);
+        if (WO == 32 && HO % 8 == 0 && K % 16 == 0) return launch_direct<32, 1, 8, 16, 1, 4, 4>(a, n, transpose, bf16, st);
+        if (WO == 16 && HO % 8 == 0 && K % 32 == 0) return launch_direct<16, 1, 8, 16, 2, 4, 2>(a, n, transpose, bf16, st);
+        if (WO == 8 && HO % 8 == 0 && K % 32 == 0) return launch_direct<8, 1, 8, 16, 2, 4, 1>(a, n, transpose, bf16, st);
     } else if (!transpose) {
-        if (WO == 16 && HO % 8 == 0 && K % 32 == 0) return launch_direct<16, 2, 8, 16, 2, 4, 2>(a, n, false, st);
-        if (WO == 8 && HO % 8 == 0 && K % 32 == 0) return launch_direct<8, 2, 8, 16, 2, 2, 2>(a, n, false, st);
+        if (WO == 16 && HO % 8 == 0 && K % 32 == 0) return launch_direct<16, 2, 8, 16, 2, 4, 2>(a, n, false, bf16, st);
+        if (WO == 8 && HO % 8 == 0 && K % 32 == 0) return launch_direct<8, 2, 8, 16, 2, 2, 2>(a, n, false, bf16, st);
     }
     return hipErrorNotSupported;
 }
@@ -944,7 +1137,7 @@ hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const f
 
 namespace psw {
 hipError_t conv3x3_dgrad_s2(int n, int CL, int H, int W, int KL, const float* w, const float* dy, float* dx,
-                            int accumulate, hipStream_t st, const BnBwdFuse* bnb)
+                            int accumulate, hipStream_t st, const BnBwdFuse* bnb, bool bf16)
 {
     if (H % 2 || W % 2 || KL % 16) return hipErrorNotSupported;
     // float4 staging of dy and of the weights, float2 stores
@@ -959,16 +1152,24 @@ hipError_t conv3x3_dgrad_s2(int n, int CL, int H, int W, int KL, const float* w,
     const double dx_bytes = kF * n * (double)CL * H * W;
     if (accumulate) wk.bytes += dx_bytes;
     if (bnb) wk.bytes += (bnb->scale ? 1.0 : 2.0) * dx_bytes;
+#define PSW_DGS2(WO_, TH_, BF_)                                                                            \
+    PSW_LAUNCH(kname("conv3x3_dgrad_s2", WO_, TH_, 16, 1, 4, 1, BF_), wk, (conv3x3_dgrad_s2<WO_, TH_, 16, 1, 4, 1, BF_>), \
+               dim3(n * (HO / TH_), CL / 16), dim3(256), 0, st, a)
     if (WO == 16 && HO % 4 == 0 && CL % 16 == 0) {
-        PSW_LAUNCH(kname("conv3x3_dgrad_s2", 16, 4, 16, 1, 4, 1), wk, (conv3x3_dgrad_s2<16, 4, 16, 1, 4, 1>),
-                   dim3(n * (HO / 4), CL / 16), dim3(256), 0, st, a);
+        if (bf16)
+            PSW_DGS2(16, 4, true);
+        else
+            PSW_DGS2(16, 4, false);
         return hipGetLastError();
     }
     if (WO == 8 && HO % 8 == 0 && CL % 16 == 0) {
-        PSW_LAUNCH(kname("conv3x3_dgrad_s2", 8, 8, 16, 1, 4, 1), wk, (conv3x3_dgrad_s2<8, 8, 16, 1, 4, 1>),
-                   dim3(n * (HO / 8), CL / 16), dim3(256), 0, st, a);
+        if (bf16)
+            PSW_DGS2(8, 8, true);
+        else
+            PSW_DGS2(8, 8, false);
         return hipGetLastError();
     }
+#undef PSW_DGS2
     return hipErrorNotSupported;
 }
 }  // namespace psw

@@ -162,7 +162,7 @@ constexpr int kFoldMaxChannels = 128;
 // Forward conv + fused BN statistics (direct kernel only); returns
 // hipErrorNotSupported when the shape has no direct configuration.
 hipError_t conv_fwd_bnstats(const ConvShape& cs, const float* x, const float* w, float* y, const BnStatsFuse& bn,
-                            size_t part_capacity_floats, hipStream_t st);
+                            size_t part_capacity_floats, int bf16, hipStream_t st);
 size_t conv_fwd_bnstats_part_floats(const ConvShape& cs);
 int conv_fwd_bnstats_tiles(const ConvShape& cs);  // tiles T (partials per channel), 0 if not fused
 // BN forward (+residual, +ReLU) whose statistics come as per-tile (mean, M2)
@@ -175,9 +175,10 @@ hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, co
                                   float* save_scale, float* run_mean, float* run_var, hipStream_t st);
 // Direct 3x3 / pad 1 kernel (forward, or backward-data of a stride-1 layer
 // when transpose is set); hipErrorNotSupported when no tile config fits.
+// bf16: both operands rounded to bfloat16 (nearest even), fp32 accumulation.
 hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const float* x, const float* w, float* y,
                           int accumulate, bool transpose, hipStream_t st, const BnStatsFuse* bn = nullptr,
-                          const BnBwdFuse* bnb = nullptr, const BnFold* fold = nullptr);
+                          const BnBwdFuse* bnb = nullptr, const BnFold* fold = nullptr, bool bf16 = false);
 // whether conv3x3_direct takes the shape (same arguments)
 bool conv3x3_direct_covers(int n, int C, int H, int W, int K, int stride, bool transpose);
 // number of pixel tiles (workgroups along x) of the direct forward kernel, 0 if none
@@ -185,19 +186,19 @@ int conv3x3_direct_tiles(int n, int C, int H, int W, int K, int stride);
 // Backward-data of a 3x3 / pad 1 / stride 2 conv (layer channels CL in, KL
 // out, input H x W); hipErrorNotSupported when no tile config fits.
 hipError_t conv3x3_dgrad_s2(int n, int CL, int H, int W, int KL, const float* w, const float* dy, float* dx,
-                            int accumulate, hipStream_t st, const BnBwdFuse* bnb = nullptr);
+                            int accumulate, hipStream_t st, const BnBwdFuse* bnb = nullptr, bool bf16 = false);
 int dgrad_bnsums_tiles(int n, int CL, int H, int W, int KL, int stride);
 // Backward data with the preceding BN's backward sums fused (direct kernel
 // or stride-2 kernel only); tiles = partials per channel, 0 if not fused.
 int conv_bwd_data_bnsums_tiles(const ConvShape& cs);
 hipError_t conv_bwd_data_bnsums(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate,
-                                const BnBwdFuse& bnb, hipStream_t st);
+                                const BnBwdFuse& bnb, int bf16, hipStream_t st);
 // Backward data whose input is formed from the preceding BN's folded
-// backward (fp32 stride-1 direct kernel only; conv_bwd_data_fold_ok says
+// backward (stride-1 direct kernel only; conv_bwd_data_fold_ok says
 // whether the shape is covered); bnb, if set, as for conv_bwd_data_bnsums.
 bool conv_bwd_data_fold_ok(const ConvShape& cs);
 hipError_t conv_bwd_data_fold(const ConvShape& cs, const float* w, float* dx, int accumulate, const BnBwdFuse* bnb,
-                              const BnFold& fold, hipStream_t st);
+                              const BnFold& fold, int bf16, hipStream_t st);
 // BN backward (+ residual) from per-tile (sum g, sum g*xhat) partials:
 // merges them in a fixed order, writes dgamma, dbeta (block 0 of a channel)
 // and dy, and dres for an identity or option-A (2x subsampled, zero-padded
@@ -212,12 +213,13 @@ hipError_t bn_bwd_from_partials(int n, int c, int h, int w, const float* dz, con
 // workgroup); conv3x3_wgrad_splits is 0 when no configuration covers it.
 int conv3x3_wgrad_splits(int n, int C, int H, int W, int K, int stride);
 hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const float* x, const float* dy, float* part,
-                         hipStream_t st);
+                         hipStream_t st, bool bf16 = false);
 // The same for `count` (<= kWgradGroupMax) convolutions of one shape in one
 // launch: member i reads x[i], dy[i] and writes its partial sums to part[i].
 constexpr int kWgradGroupMax = 8;
 hipError_t conv3x3_wgrad_group(int n, int C, int H, int W, int K, int stride, const float* const* x,
-                               const float* const* dy, float* const* part, int count, hipStream_t st);
+                               const float* const* dy, float* const* part, int count, hipStream_t st,
+                               bool bf16 = false);
 hipError_t conv_fwd(const ConvShape& cs, const float* x, const float* w, const float* bias, int relu,
                     float* y, int bf16, hipStream_t st);
 hipError_t conv_bwd_data(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate,

@@ -34,6 +34,14 @@ namespace psw {
 namespace {
 
 typedef float v4f __attribute__((ext_vector_type(4)));
+typedef short v4s __attribute__((ext_vector_type(4)));
+
+// 4 floats rounded to bfloat16 (nearest even), packed as a matrix operand
+__device__ __forceinline__ v4s bf16x4(float a, float b, float c, float d)
+{
+    return v4s{__builtin_bit_cast(short, (__bf16)a), __builtin_bit_cast(short, (__bf16)b),
+               __builtin_bit_cast(short, (__bf16)c), __builtin_bit_cast(short, (__bf16)d)};
+}
 
 struct WgArgs {
     const float* x[kWgradGroupMax];   // member i: [n][C][H][W]
@@ -53,7 +61,11 @@ constexpr int plane_stride(int lo)
 
 constexpr int round4(int v) { return (v + 3) / 4 * 4; }
 
-template <int STRIDE, int WO, int TH, int KBW, int CBW, int WPX, int TPW, int RC>
+// BF: bf16 operands with fp32 accumulation on v_mfma_f32_16x16x16_bf16, k =
+// 16 consecutive output pixels (4 pixel quads; lane group g supplies quad g):
+// the fp32 tiles are staged as before and each lane rounds its 4 dy values
+// and its 4 shifted input values to bf16 when it reads them.
+template <int STRIDE, int WO, int TH, int KBW, int CBW, int WPX, int TPW, int RC, bool BF>
 __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
 {
     constexpr int NT = 64 * KBW * CBW * WPX;
@@ -67,6 +79,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
     constexpr int XPS = plane_stride(HRC * XRS);              // x plane stride
     constexpr int NCH = TPW * (TH / RC);                      // chunks per workgroup
     static_assert(WO % 4 == 0 && TH % RC == 0 && QC % WPX == 0, "tiling");
+    static_assert(!BF || QC % (4 * WPX) == 0, "bf16: 16-pixel blocks");
     constexpr int DS_FLOATS = KC * DPS;
     constexpr int XS_FLOATS = CCH * XPS;
     constexpr int RED_FLOATS = (WPX > 1) ? (WPX - 1) * KBW * CBW * 9 * 4 * 64 : 0;
@@ -168,6 +181,28 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
         store_chunk();
         __syncthreads();
         if (ch + 1 < NCH) load_chunk(ch + 1);
+        if constexpr (BF) {
+            const float* dsb = Ds + (kb * 16 + j) * DPS;
+            const float* xsb = Xs + (cb * 16 + j) * XPS + 3;
+#pragma unroll
+            for (int qb = 0; qb < QC / (4 * WPX); ++qb) {
+                const int pix0 = ((qb * WPX + wpx) * 4 + g) * 4;  // this lane group's pixel quad
+                const int row = pix0 / WO, col0 = pix0 - (pix0 / WO) * WO;
+                const float2 d0 = *reinterpret_cast<const float2*>(dsb + pix0);
+                const float2 d1 = *reinterpret_cast<const float2*>(dsb + pix0 + 2);
+                const v4s av = bf16x4(d0.x, d0.y, d1.x, d1.y);
+                const float* xb = xsb + (row * STRIDE) * XRS + col0 * STRIDE;
+#pragma unroll
+                for (int r = 0; r < 3; ++r)
+#pragma unroll
+                    for (int s = 0; s < 3; ++s) {
+                        const float* p = xb + r * XRS + s;
+                        const v4s bv = bf16x4(p[0], p[STRIDE], p[2 * STRIDE], p[3 * STRIDE]);
+                        acc[r * 3 + s] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(av, bv, acc[r * 3 + s], 0, 0, 0);
+                    }
+            }
+            continue;
+        }
 #pragma unroll
         for (int qi = 0; qi < QC / WPX; ++qi) {
             const int pix0 = (qi * WPX + wpx) * 4;
@@ -244,7 +279,7 @@ int conv3x3_wgrad_splits(int n, int C, int H, int W, int K, int stride)
 }
 
 hipError_t conv3x3_wgrad_group(int n, int C, int H, int W, int K, int stride, const float* const* x,
-                               const float* const* dy, float* const* part, int count, hipStream_t st)
+                               const float* const* dy, float* const* part, int count, hipStream_t st, bool bf16)
 {
     const int cfg = wgrad_config(n, C, H, W, K, stride);
     if (!cfg || count < 1 || count > kWgradGroupMax) return hipErrorNotSupported;
@@ -265,36 +300,31 @@ hipError_t conv3x3_wgrad_group(int n, int C, int H, int W, int K, int stride, co
     Work wk = conv_work(n, C, H, W, K, 3, 3, H / stride, W / stride);
     wk.flops *= count;
     wk.bytes *= count;
+#define PSW_WG(S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_)                                                        \
+    do {                                                                                                      \
+        if (bf16)                                                                                             \
+            PSW_LAUNCH(kname("conv3x3_wgrad", S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, true), wk,           \
+                       (conv3x3_wgrad<S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, true>), grid, dim3(256), 0, st, a); \
+        else                                                                                                  \
+            PSW_LAUNCH(kname("conv3x3_wgrad", S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, false), wk,          \
+                       (conv3x3_wgrad<S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, false>), grid, dim3(256), 0, st, a); \
+    } while (0)
     switch (cfg) {
     case 6:
-    case 1:
-        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 32, 16, 1, 1, 4, 1, 4), wk, (conv3x3_wgrad<1, 32, 16, 1, 1, 4, 1, 4>), grid, dim3(256), 0,
-                   st, a);
-        break;
-    case 2:
-        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 16, 16, 1, 1, 4, 2, 8), wk, (conv3x3_wgrad<1, 16, 16, 1, 1, 4, 2, 8>), grid, dim3(256), 0,
-                   st, a);
-        break;
-    case 3:
-        PSW_LAUNCH(kname("conv3x3_wgrad", 1, 8, 8, 2, 1, 2, 4, 8), wk, (conv3x3_wgrad<1, 8, 8, 2, 1, 2, 4, 8>), grid, dim3(256), 0,
-                   st, a);
-        break;
-    case 4:
-        PSW_LAUNCH(kname("conv3x3_wgrad", 2, 16, 8, 2, 1, 2, 1, 4), wk, (conv3x3_wgrad<2, 16, 8, 2, 1, 2, 1, 4>), grid, dim3(256), 0,
-                   st, a);
-        break;
-    case 5:
-        PSW_LAUNCH(kname("conv3x3_wgrad", 2, 8, 8, 4, 1, 1, 1, 4), wk, (conv3x3_wgrad<2, 8, 8, 4, 1, 1, 1, 4>), grid, dim3(256), 0,
-                   st, a);
-        break;
+    case 1: PSW_WG(1, 32, 16, 1, 1, 4, 1, 4); break;
+    case 2: PSW_WG(1, 16, 16, 1, 1, 4, 2, 8); break;
+    case 3: PSW_WG(1, 8, 8, 2, 1, 2, 4, 8); break;
+    case 4: PSW_WG(2, 16, 8, 2, 1, 2, 1, 4); break;
+    case 5: PSW_WG(2, 8, 8, 4, 1, 1, 1, 4); break;
     }
+#undef PSW_WG
     return hipGetLastError();
 }
 
 hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const float* x, const float* dy, float* part,
-                         hipStream_t st)
+                         hipStream_t st, bool bf16)
 {
-    return conv3x3_wgrad_group(n, C, H, W, K, stride, &x, &dy, &part, 1, st);
+    return conv3x3_wgrad_group(n, C, H, W, K, stride, &x, &dy, &part, 1, st, bf16);
 }
 
 }  // namespace psw

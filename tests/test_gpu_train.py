@@ -548,7 +548,7 @@ def test_bn_backward_folds_run(P):
     ks = net.profile_kernels()
     net.profile(False)
     count = lambda pred: sum(k["launches"] for k in ks if pred(k["name"]))
-    assert count(lambda n: n.startswith("conv3x3_direct") and n.endswith("true, 1, 1>")) == 7
-    assert count(lambda n: n.startswith("conv3x3_direct") and n.endswith("true, 1, 2>")) == 6
+    assert count(lambda n: n.startswith("conv3x3_direct") and n.endswith("true, 1, 1, false>")) == 7
+    assert count(lambda n: n.startswith("conv3x3_direct") and n.endswith("true, 1, 2, false>")) == 6
     assert count(lambda n: n.startswith(("bn_bwd_partials_k", "bn_bwd_apply"))) == 6
     assert count(lambda n: n.startswith("conv3x3_wgrad")) == 6
