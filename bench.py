@@ -18,6 +18,11 @@ are synthetic N(0,1) [128,3,32,32] batches with uniform labels, all resident
 in HBM before timing starts.
 
 Prints one JSON line.  `value` is images/s over the K timed steps.
+`--bf16` runs the same ResNet-20 configuration with bf16 products (fp32
+accumulation); `--workload resnet110` runs ResNet-110 at batch 256 with bf16
+products, 8 stages of [7,7,7,7,7,7,6,6] blocks and staleness d_s = 7 - s
+(50 timed steps by default; its ring period of 840 steps is not captured
+as a graph).  Both report the conv kernels against HBM beside bf16 MFMA.
 
 Measurement, in order: W warm-up steps (eager, including the pipeline
 fill), the graph capture and one untimed replay; the K timed steps (wall
@@ -61,6 +66,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 METRIC = "training images/sec at 1 GPU (ResNet-20, batch 128) + conv MFMA % of peak"
+METRIC_R110 = "training images/sec at 1 GPU (ResNet-110, batch 256, bf16 products) + conv MFMA % of peak"
 PEAK_FP32_MFMA = 157.3   # TFLOP/s, MI355X dense fp32 matrix
 PEAK_BF16_MFMA = 2500.0  # TFLOP/s, MI355X dense bf16 matrix
 PEAK_HBM = 8000.0        # GB/s, MI355X HBM3E
@@ -165,9 +171,9 @@ def cpu_baseline(wl, chunk=2, min_seconds=10.0, max_chunks=15):
         oracle.set_threads(cores)
     return {"value": round(steps * wl.batch / dt, 3), "unit": "images/s", "cores": cores,
             "kind": "oracle", "host": host_cpu(),
-            "sample": f"{steps} stale-weight training steps of the same workload (ResNet-20, batch {wl.batch}, "
-                      f"float64 direct loops, OpenMP; runs of {chunk} steps until {min_seconds:.0f} s), "
-                      f"{dt:.1f} s",
+            "sample": f"{steps} stale-weight training steps of the same workload ({wl.name}, batch {wl.batch}, "
+                      f"float64 direct loops, OpenMP; runs of {chunk} steps until {min_seconds:.0f} s or "
+                      f"{chunk * max_chunks} steps), {dt:.1f} s",
             "single_thread": {"value": round(wl.batch / dt1, 3), "unit": "images/s", "cores": 1,
                               "sample": f"1 step of the same workload on one thread, {dt1:.1f} s"}}
 
@@ -175,8 +181,11 @@ def cpu_baseline(wl, chunk=2, min_seconds=10.0, max_chunks=15):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=None, help="timed steps (default 100; resnet110: 50)")
+    ap.add_argument("--warmup", type=int, default=None, help="warm-up steps (default 20; resnet110: 10)")
+    ap.add_argument("--workload", choices=("resnet20", "resnet110"), default="resnet20",
+                    help="resnet20: ResNet-20, batch 128, 4 stages, d = [3,2,1,0] (the metric's configuration); "
+                         "resnet110: ResNet-110, batch 256, bf16 products, 8 stages, d_s = 7 - s")
     ap.add_argument("--bf16", action="store_true", help="bf16-in / fp32-accumulate conv and FC products")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--mode", choices=("pipelined", "graph", "sequential"), default="pipelined",
@@ -202,11 +211,19 @@ def main():
     if args.copy_calibration:
         copy_calibration()
         return
-    wl = synth.resnet20_workload(bf16=args.bf16)
-    K, W = args.steps, args.warmup
+    r110 = args.workload == "resnet110"
+    wl = synth.resnet110_workload() if r110 else synth.resnet20_workload(bf16=args.bf16)
+    K = args.steps if args.steps is not None else (50 if r110 else 100)
+    W = args.warmup if args.warmup is not None else (10 if r110 else 20)
     period = 3  # step sets of the pipelined run
     for d in wl.ring_depth():
         period = period * d // __import__("math").gcd(period, d)
+    # a graph replays one period of ring slots and step sets: 12 steps for
+    # ResNet-20's rings [4,3,2,1], 840 for ResNet-110's [8..1] (not captured)
+    use_graph = period <= 64
+    if not use_graph and args.mode == "graph":
+        print(f"--mode graph: the pipeline's period is {period} steps, too long to capture", file=sys.stderr)
+        sys.exit(2)
     T = W + period + REPLAY_STEPS + 3 * K + period
     net = psw.Net(wl.ops, wl.batch, wl.in_shape, wl.stage_end, wl.ring_depth(T), bf16=wl.bf16)
     net.load_params(synth.init_params(wl))
@@ -256,11 +273,14 @@ def main():
             run_pipelined(n % period)
 
     modes = {"graph": run_graph, "pipelined": run_pipelined, "sequential": run_sequential}
+    if not use_graph:
+        del modes["graph"]
     run = modes[args.mode]
 
     run_pipelined(W)  # includes the pipeline fill (versions clamped at 0)
-    graph = net.capture(stal[t:t + period], wl.lr, xs, ys, glosses, wl.momentum, wl.weight_decay, wl.nesterov)
-    run_graph(period)  # first replay uploads the graph
+    if use_graph:
+        graph = net.capture(stal[t:t + period], wl.lr, xs, ys, glosses, wl.momentum, wl.weight_decay, wl.nesterov)
+        run_graph(period)  # first replay uploads the graph
     torch.cuda.synchronize()
     # timed region: no events
     t0 = time.perf_counter()
@@ -321,6 +341,12 @@ def main():
         if uk:
             ums = conv_ms + sum(k["ms"] for k in uk) / KP
             conv["frac_with_update"] = round(conv_flop / (ums * 1e-3) / 1e12 / peak, 4)
+        # the same kernels against HBM: their algorithmic bytes over their time
+        # (the binding roof of the bf16 mode, whose tensors stay fp32 in HBM)
+        conv_bytes = sum(k["bytes"] for k in ck) / KP
+        gbs = conv_bytes / (conv_ms * 1e-3) / 1e9
+        conv["hbm"] = {"achieved": round(gbs, 1), "peak": PEAK_HBM, "unit": "GB/s", "frac": round(gbs / PEAK_HBM, 4),
+                       "bytes_per_step": conv_bytes}
         d = kernels[0]  # the dominant kernel: largest summed time
         roof = roofline_of(d, peak)
         roof["traffic"] = measured_traffic(d["name"])
@@ -343,7 +369,7 @@ def main():
               "avg_launch_us": round(1e3 * k["ms"] / k["launches"], 3), "flop_per_launch": k["flops"] / k["launches"],
               "bytes_per_launch": k["bytes"] / k["launches"]} for k in kernels]
     out = {
-        "metric": METRIC,
+        "metric": METRIC_R110 if r110 else METRIC,
         "value": round(img_s, 2),
         "unit": "images/s",
         "n_gpus": 1,
@@ -355,8 +381,10 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16-in/f32-acc" if wl.bf16 else "f32",
         "data": "synthetic",
-        "config": {"workload": "ResNet-20 (CIFAR shape), batch 128, 4 stages at PPV (7,13,19), staleness [3,2,1,0], "
-                               "SGD momentum 0.9, lr 0.01",
+        "config": {"workload": ("ResNet-110 (CIFAR shape), batch 256, bf16 products with fp32 accumulation, 8 stages "
+                                "of [7,7,7,7,7,7,6,6] blocks, staleness d_s = 7 - s, SGD momentum 0.9, lr 0.01" if r110
+                                else "ResNet-20 (CIFAR shape), batch 128, 4 stages at PPV (7,13,19), staleness "
+                                     "[3,2,1,0], SGD momentum 0.9, lr 0.01"),
                    "global_batch": wl.batch, "input": "3x32x32 N(0,1)", "parallelism": "single GPU, all stages",
                    "execution": {"graph": f"pipelined (forward of t+1 overlaps backward of t), replayed from a "
                                           f"HIP graph of {period} captured steps",
@@ -371,7 +399,8 @@ def main():
         "final_loss": round(loss, 5),
     }
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(synth.resnet20_workload(bf16=args.bf16))
+        # the same workload; ResNet-110's steps take ~20 s of oracle time each
+        out["cpu_baseline"] = cpu_baseline(wl, chunk=1, max_chunks=1) if r110 else cpu_baseline(wl)
     print(json.dumps(out), flush=True)
 
 
