@@ -81,26 +81,20 @@ def deviations(wl, flat, losses, ref_flat, ref_losses, p0):
 
 def reference_spread(oracle, wl, T, batch, xs, ys, stash=False):
     """Independent computations at the GPU's precision, to measure how far
-    such a computation lands from the oracle on this run: fp32 -> the stale
-    schedule written with torch autograd in float32 (CPU) on the inputs and
-    on the inputs moved one float32 ulp up and down; bf16 mode -> the oracle
-    itself on the inputs moved one ulp up and down (bf16 rounding decisions
-    flip).  Returns a list of (params, losses)."""
+    such a computation lands from the oracle on this run: the stale schedule
+    written with torch autograd in float32 (CPU) -- in bf16 mode with both
+    operands of every product rounded to bfloat16 -- on the inputs and on
+    the inputs moved one float32 ulp up and down.  Returns a list of
+    (params, losses)."""
     p0 = synth.init_params(wl)
     up = np.nextafter(xs, np.inf, dtype=np.float32)
     down = np.nextafter(xs, -np.inf, dtype=np.float32)
     out = []
-    if not wl.bf16:
-        for inp in (xs, up, down):
-            p, l, _ = torch_ref.train_stale(wl.ops, wl.stage_end, p0, inp, ys, wl.staleness(T), wl.lr_table(T), wl.momentum,
-                                            wl.weight_decay, dtype=torch.float32, stash=stash,
-                                            dropout_seed=wl.dropout_seed)
-            out.append((p, l))
-        return out
-    for inp in (up, down):
-        o = oracle.train(wl.ops, wl.in_shape, wl.stage_end, p0, inp, ys, wl.staleness(T), wl.lr_table(T), wl.momentum,
-                         wl.weight_decay, wl.nesterov, bf16=True, stash=stash, dropout_seed=wl.dropout_seed)
-        out.append((o["params"], o["losses"]))
+    for inp in (xs, up, down):
+        p, l, _ = torch_ref.train_stale(wl.ops, wl.stage_end, p0, inp, ys, wl.staleness(T), wl.lr_table(T), wl.momentum,
+                                        wl.weight_decay, dtype=torch.float32, stash=stash,
+                                        dropout_seed=wl.dropout_seed, bf16=wl.bf16, nesterov=wl.nesterov)
+        out.append((p, l))
     return out
 
 
@@ -146,7 +140,8 @@ def test_train_parity(P, oracle, name, factory, batch, T, stash):
     """Bar: max(spec bar, 4 x reference spread) for the whole parameter
     vector, for every tensor with a non-zero initial value, and for the
     losses; the spec bar is 1e-4 (fp32) / 2e-2 (bf16).  The spread
-    (the largest deviation among the reference_spread samples) measures how
+    (the largest deviation among the reference_spread samples: torch float32,
+    with bf16-rounded product operands in bf16 mode) measures how
     much this particular run amplifies
     rounding-level differences: ReLU-sign and max-pool decisions taken near
     zero, and in bf16 mode operand roundings, flip between any two

@@ -236,11 +236,12 @@ def test_negative_staleness_rejected(oracle):
         oracle.train(ops, ins, se, synth.init_params(wl), xs, ys, np.array([[-1, 0]]), 0.01)
 
 
-def test_oracle_matches_autograd_stale_schedule(oracle):
+@pytest.mark.parametrize("nesterov", [False, True], ids=["momentum", "nesterov"])
+def test_oracle_matches_autograd_stale_schedule(oracle, nesterov):
     """The oracle's training loop against the schedule written with torch
     autograd (version history, forward on version max(0, t-d_s), backward on
     version t) in float64, on a hybrid schedule (Sec. 4): stale for 4 steps,
-    then plain SGD."""
+    then plain SGD; with plain and Nesterov momentum (App. A)."""
     ops, le, _ = synth.resnet_cifar(14)
     se = [le[3], le[7], le[11], len(ops)]
     T = 7
@@ -248,8 +249,9 @@ def test_oracle_matches_autograd_stale_schedule(oracle):
     wl = synth.Workload("s", ops, (3, 8, 8), 10, 3, [], se, lambda t: list(d[t]), T, [0.02] * 4, seed=4)
     p0 = synth.init_params(wl)
     xs, ys = synth.batches(wl, T)
-    out = oracle.train(ops, (3, 8, 8), se, p0, xs, ys, d, [0.02, 0.03, 0.02, 0.01], 0.9, wd=1e-4)
-    p, losses, versions = torch_ref.train_stale(ops, se, p0, xs, ys, d, [0.02, 0.03, 0.02, 0.01], 0.9, wd=1e-4)
+    out = oracle.train(ops, (3, 8, 8), se, p0, xs, ys, d, [0.02, 0.03, 0.02, 0.01], 0.9, wd=1e-4, nesterov=nesterov)
+    p, losses, versions = torch_ref.train_stale(ops, se, p0, xs, ys, d, [0.02, 0.03, 0.02, 0.01], 0.9, wd=1e-4,
+                                                nesterov=nesterov)
     np.testing.assert_array_equal(versions, out["versions"])
     np.testing.assert_allclose(losses, out["losses"], rtol=1e-12)
     np.testing.assert_allclose(p, out["params"], rtol=1e-10, atol=1e-12)

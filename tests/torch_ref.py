@@ -320,7 +320,7 @@ def simulate_register_pipeline(ops, stage_end, params0, xs, labels, lr, mom=0.9,
 
 
 def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=0.0, dtype=torch.float64,
-                stash=False, dropout_seed=0):
+                stash=False, dropout_seed=0, bf16=False, nesterov=False):
     """The stale-weight schedule written with autograd, for any staleness
     table (hybrid included): keep every stage's version history; for step t
     load version max(0, t - d_s) into the stage's weight tensor and run the
@@ -328,8 +328,10 @@ def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=
     backward (autograd holds the tensor by reference, so data gradients see
     version t while weight gradients use the saved activations); append
     version t+1 = SGD(version t).  stash=True leaves the forward's version
-    in place for the backward pass (weight stashing).  Returns (final flat
-    params, losses, versions)."""
+    in place for the backward pass (weight stashing).  bf16=True rounds both
+    operands of every conv / FC product to bfloat16 in each pass; nesterov
+    takes the step d + mom*v with d = g + wd*w (as torch.optim.SGD).  Returns
+    (final flat params, losses, versions)."""
     slices, counts = op_param_slices(ops, stage_end)
     S = len(counts)
     hist = [[torch.tensor(p, dtype=dtype)] for p in split_flat(np.asarray(params0, np.float64), counts)]
@@ -349,7 +351,8 @@ def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=
             with torch.no_grad():
                 Wp[s].copy_(hist[s][r])
             Wp[s].grad = None
-        outs = run_ops(ops, 0, n, {0: torch.tensor(xs[t], dtype=dtype)}, Wp, slices, dropout_key=(dropout_seed, t))
+        outs = run_ops(ops, 0, n, {0: torch.tensor(xs[t], dtype=dtype)}, Wp, slices, dropout_key=(dropout_seed, t),
+                       bf16=bf16)
         loss = F.cross_entropy(outs[n].reshape(outs[n].shape[0], -1), torch.tensor(labels[t], dtype=torch.long))
         losses[t] = float(loss.detach())
         if not stash:
@@ -360,8 +363,9 @@ def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=
         with torch.no_grad():
             for s in range(S):
                 g = Wp[s].grad if Wp[s].grad is not None else torch.zeros_like(V[s])
-                V[s].mul_(mom).add_(g + wd * hist[s][t])
-                hist[s].append(hist[s][t] - float(lrs_t[t, s]) * V[s])
+                d = g + wd * hist[s][t]
+                V[s].mul_(mom).add_(d)
+                hist[s].append(hist[s][t] - float(lrs_t[t, s]) * (d + mom * V[s] if nesterov else V[s]))
     return torch.cat([h[-1] for h in hist]).double().numpy(), losses, versions
 
 
