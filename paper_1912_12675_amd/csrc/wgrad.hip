@@ -4,9 +4,13 @@
 // (Sec. 2 of the paper: the weight gradient of layer l from x^(l-1) and
 // delta^(l)).
 //
-// A workgroup reduces over TPW consecutive (image, TH-row band) tiles and
-// writes one dW-shaped partial sum; the partials are added in a fixed order
-// by the reduction kernel of conv.hip, so the result is bit-reproducible.
+// A workgroup reduces over IPW * TPW consecutive (image, TH-row band) tiles
+// and writes one dW-shaped partial sum; the partials are added in a fixed
+// order by the stage update (or the reduction kernel of conv.hip), so the
+// result is bit-reproducible.  Its waves form IPW groups, each with its own
+// LDS tiles walking TPW of the tiles; the groups' sums meet in LDS in group
+// order at the end, so a workgroup covers IPW times the pixels of one group
+// and writes IPW times fewer partial sums than one group per workgroup would.
 // One launch may cover several convolutions of the same shape (the
 // same-shape layers of a pipeline stage): blockIdx.x / splits selects the
 // convolution, and each has its own operands and partial sums.
@@ -65,10 +69,10 @@ constexpr int round4(int v) { return (v + 3) / 4 * 4; }
 // 16 consecutive output pixels (4 pixel quads; lane group g supplies quad g):
 // the fp32 tiles are staged as before and each lane rounds its 4 dy values
 // and its 4 shifted input values to bf16 when it reads them.
-template <int STRIDE, int WO, int TH, int KBW, int CBW, int WPX, int TPW, int RC, bool BF>
-__global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
+template <int STRIDE, int WO, int TH, int KBW, int CBW, int WPX, int TPW, int RC, bool BF, int IPW>
+__global__ __launch_bounds__(64 * KBW * CBW * WPX * IPW) void conv3x3_wgrad(WgArgs a)
 {
-    constexpr int NT = 64 * KBW * CBW * WPX;
+    constexpr int NT = 64 * KBW * CBW * WPX;  // threads of one group
     constexpr int WIN = WO * STRIDE;
     constexpr int XRS = round4(WIN + (STRIDE == 1 ? 5 : 4));  // input row: cols -1 .. WIN(-1) at offsets 3 ..
     constexpr int HRC = (RC - 1) * STRIDE + 3;                // staged input rows per chunk
@@ -82,14 +86,21 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
     static_assert(!BF || QC % (4 * WPX) == 0, "bf16: 16-pixel blocks");
     constexpr int DS_FLOATS = KC * DPS;
     constexpr int XS_FLOATS = CCH * XPS;
-    constexpr int RED_FLOATS = (WPX > 1) ? (WPX - 1) * KBW * CBW * 9 * 4 * 64 : 0;
-    constexpr int LDS_FLOATS = (DS_FLOATS + XS_FLOATS) > RED_FLOATS ? (DS_FLOATS + XS_FLOATS) : RED_FLOATS;
+    constexpr int ACC_FLOATS = 9 * 4 * 64;  // one wave's accumulators
+    // final sums: within each group over wpx, then over the groups
+    constexpr int RED1 = (WPX > 1) ? IPW * (WPX - 1) * KBW * CBW * ACC_FLOATS : 0;
+    constexpr int RED2 = (IPW > 1) ? (IPW - 1) * KBW * CBW * ACC_FLOATS : 0;
+    constexpr int TILE_FLOATS = IPW * (DS_FLOATS + XS_FLOATS);
+    constexpr int LDS_FLOATS = TILE_FLOATS > RED1 ? (TILE_FLOATS > RED2 ? TILE_FLOATS : RED2) : (RED1 > RED2 ? RED1 : RED2);
+    static_assert(LDS_FLOATS * 4 <= 65536, "LDS");
     __shared__ __attribute__((aligned(16))) float lds[LDS_FLOATS];
-    float* Ds = lds;
-    float* Xs = lds + DS_FLOATS;
 
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wave_all = threadIdx.x >> 6;
+    const int ip = wave_all / (KBW * CBW * WPX);  // group
+    const int tid = threadIdx.x - ip * NT, lane = tid & 63, wave = tid >> 6;
     const int kb = wave % KBW, cb = (wave / KBW) % CBW, wpx = wave / (KBW * CBW);
+    float* Ds = lds + ip * (DS_FLOATS + XS_FLOATS);
+    float* Xs = Ds + DS_FLOATS;
     const int g = lane >> 4, j = lane & 15;
     const int mem = blockIdx.x / a.splits;          // member of the group
     const int bx = blockIdx.x - mem * a.splits;     // partial-sum index within it
@@ -115,7 +126,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
     constexpr int DV = (DN4 + NT - 1) / NT, XV = (XN4 + NT - 1) / NT;
     float4 dr[DV], xr[XV];
     auto load_chunk = [&](int ch) {
-        const int tl = bx * TPW + ch / (TH / RC);
+        const int tl = (bx * IPW + ip) * TPW + ch / (TH / RC);
         const int img = tl / bands;
         const int oh0 = (tl - img * bands) * TH + (ch % (TH / RC)) * RC;
         const int ih0 = oh0 * STRIDE - 1;
@@ -219,25 +230,46 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
         }
     }
 
+    // sums in a fixed order: within each group over wpx, then over the groups
     if constexpr (WPX > 1) {
         __syncthreads();  // LDS tiles are no longer read: reuse for the reduction
         if (wpx > 0) {
-            float* dst = lds + ((((wpx - 1) * KBW + kb) * CBW + cb) * 9) * 4 * 64;
+            float* dst = lds + ((((ip * (WPX - 1) + wpx - 1) * KBW + kb) * CBW + cb)) * ACC_FLOATS;
 #pragma unroll
             for (int t = 0; t < 9; ++t)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) dst[(t * 4 + i) * 64 + lane] = acc[t][i];
         }
         __syncthreads();
-        if (wpx != 0) return;
-        for (int w = 1; w < WPX; ++w) {
-            const float* src = lds + ((((w - 1) * KBW + kb) * CBW + cb) * 9) * 4 * 64;
+        if (wpx == 0)
+            for (int w = 1; w < WPX; ++w) {
+                const float* src = lds + ((((ip * (WPX - 1) + w - 1) * KBW + kb) * CBW + cb)) * ACC_FLOATS;
+#pragma unroll
+                for (int t = 0; t < 9; ++t)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[t][i] += src[(t * 4 + i) * 64 + lane];
+            }
+    }
+    if constexpr (IPW > 1) {
+        __syncthreads();
+        if (wpx == 0 && ip > 0) {
+            float* dst = lds + (((ip - 1) * KBW + kb) * CBW + cb) * ACC_FLOATS;
 #pragma unroll
             for (int t = 0; t < 9; ++t)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) acc[t][i] += src[(t * 4 + i) * 64 + lane];
+                for (int i = 0; i < 4; ++i) dst[(t * 4 + i) * 64 + lane] = acc[t][i];
         }
+        __syncthreads();
+        if (wpx == 0 && ip == 0)
+            for (int q = 1; q < IPW; ++q) {
+                const float* src = lds + (((q - 1) * KBW + kb) * CBW + cb) * ACC_FLOATS;
+#pragma unroll
+                for (int t = 0; t < 9; ++t)
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) acc[t][i] += src[(t * 4 + i) * 64 + lane];
+            }
     }
+    if (wpx != 0 || ip != 0) return;
     // D lane l, register i: output channel kb*16 + 4g + i, input channel cb*16 + j
     float* out = a.part[mem] + (size_t)bx * a.K * a.C * 9;
 #pragma unroll
@@ -254,10 +286,10 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX) void conv3x3_wgrad(WgArgs a)
 int wgrad_config(int n, int C, int H, int W, int K, int stride)
 {
     if (stride == 1 && H == 32 && W == 32 && C == 16 && K == 16) return 1;
-    if (stride == 1 && H == 16 && W == 16 && C == 32 && K == 32 && n % 2 == 0) return 2;
-    if (stride == 1 && H == 8 && W == 8 && C == 64 && K == 64 && n % 4 == 0) return 3;
+    if (stride == 1 && H == 16 && W == 16 && C == 32 && K == 32 && n % 4 == 0) return 2;
+    if (stride == 1 && H == 8 && W == 8 && C == 64 && K == 64 && n % 8 == 0) return 3;
     if (stride == 2 && H == 32 && W == 32 && C == 16 && K == 32) return 4;
-    if (stride == 2 && H == 16 && W == 16 && C == 32 && K == 64) return 5;
+    if (stride == 2 && H == 16 && W == 16 && C == 32 && K == 64 && n % 2 == 0) return 5;
     if (stride == 1 && H == 32 && W == 32 && C < 16 && K == 16) return 6;
     return 0;
 }
@@ -267,13 +299,13 @@ int wgrad_config(int n, int C, int H, int W, int K, int stride)
 // Number of partial sums (workgroups) for a shape; 0 when not covered.
 int conv3x3_wgrad_splits(int n, int C, int H, int W, int K, int stride)
 {
-    switch (wgrad_config(n, C, H, W, K, stride)) {
-    case 1: return n * 2;       // one 16-row band (of 32) per workgroup
-    case 2: return n / 2;       // two images per workgroup (and 16 of the 32 output channels)
-    case 3: return n / 4;       // four images per workgroup (and 32 of the 64 output channels)
-    case 4: return n * 2;       // one 8-row band (of 16 output rows) per workgroup
-    case 5: return n;           // one image per workgroup
-    case 6: return n * 2;       // as 1, input channels zero-filled to 16
+    switch (wgrad_config(n, C, H, W, K, stride)) {  // two groups of waves per workgroup
+    case 1: return n;           // one 16-row band (of 32) per group: one image per workgroup
+    case 2: return n / 4;       // two images per group (and 16 of the 32 output channels)
+    case 3: return n / 8;       // four images per group (and 32 of the 64 output channels)
+    case 4: return n;           // one 8-row band (of 16 output rows) per group
+    case 5: return n / 2;       // one image per group
+    case 6: return n;           // as 1, input channels zero-filled to 16
     default: return 0;
     }
 }
@@ -300,14 +332,16 @@ hipError_t conv3x3_wgrad_group(int n, int C, int H, int W, int K, int stride, co
     Work wk = conv_work(n, C, H, W, K, 3, 3, H / stride, W / stride);
     wk.flops *= count;
     wk.bytes *= count;
-#define PSW_WG(S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_)                                                        \
-    do {                                                                                                      \
-        if (bf16)                                                                                             \
-            PSW_LAUNCH(kname("conv3x3_wgrad", S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, true), wk,           \
-                       (conv3x3_wgrad<S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, true>), grid, dim3(256), 0, st, a); \
-        else                                                                                                  \
-            PSW_LAUNCH(kname("conv3x3_wgrad", S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, false), wk,          \
-                       (conv3x3_wgrad<S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, false>), grid, dim3(256), 0, st, a); \
+#define PSW_WG(S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_)                                                          \
+    do {                                                                                                        \
+        if (bf16)                                                                                               \
+            PSW_LAUNCH(kname("conv3x3_wgrad", S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, true, 2), wk,          \
+                       (conv3x3_wgrad<S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, true, 2>), grid, dim3(512), 0, st, \
+                       a);                                                                                      \
+        else                                                                                                    \
+            PSW_LAUNCH(kname("conv3x3_wgrad", S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, false, 2), wk,         \
+                       (conv3x3_wgrad<S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, false, 2>), grid, dim3(512), 0, st, \
+                       a);                                                                                      \
     } while (0)
     switch (cfg) {
     case 6:
