@@ -12,6 +12,13 @@
         replay's start, i.e. duration + dispatch gap) beside bench.py's event
         time per launch for the same kernel
 
+    python -m paper_1912_12675_amd.rocprof_summary mfma PMC_CSV --bench BENCH_JSON [--cycles 32] [--clock 2.4]
+        matrix-core busy cycles per launch of every conv kernel from a
+        `--pmc SQ_VALU_MFMA_BUSY_CYCLES ...` run, against the algorithmic
+        instruction count (flop_per_launch / 2048 per 16x16x4 fp32 MFMA, times
+        --cycles) and as a share of the SIMD-cycles of bench.py's launch time
+        (busy / (avg_launch_us * clock * 1024 SIMDs))
+
     python -m paper_1912_12675_amd.rocprof_summary traffic --kernel NAME [--kernel NAME ...] \
             --fetch PMC_CSV --write PMC_CSV --copy-fetch PMC_CSV --copy-write PMC_CSV \
             --copy-kernel SUBSTRING --copy-bytes B [--out profiles/traffic.json]
@@ -165,6 +172,11 @@ def main(argv=None):
     a.add_argument("csv")
     a.add_argument("--steps", type=int, required=True)
     a.add_argument("--top", type=int, default=25)
+    m = sub.add_parser("mfma")
+    m.add_argument("csv")
+    m.add_argument("--bench", required=True)
+    m.add_argument("--cycles", type=int, default=32)
+    m.add_argument("--clock", type=float, default=2.4, help="GHz")
     c = sub.add_parser("replays")
     c.add_argument("trace")
     c.add_argument("--bench", required=True, help="the JSON line bench.py printed in the same run")
@@ -184,6 +196,20 @@ def main(argv=None):
             print(f"| `{r['name']}` | {r['calls'] / args.steps:.2f} | {r['avg_ns'] / 1e3:.2f} | "
                   f"{r['total_ns'] / args.steps / 1e3:.1f} | {100 * r['total_ns'] / tot:.1f}% |")
         print(f"\nall kernels: {tot / args.steps / 1e6:.4f} ms/step over {args.steps} steps")
+    elif args.cmd == "mfma":
+        with open(args.bench) as f:
+            bench = json.loads([l for l in f if l.startswith("{")][-1])
+        busy = pmc_values(args.csv, "SQ_VALU_MFMA_BUSY_CYCLES")
+        print("| kernel | launches/step | MFMA busy cycles per launch | algorithmic instructions x cycles | "
+              "launch us (bench) | busy share |\n|---|---:|---:|---:|---:|---:|")
+        for k in bench["kernels"]:
+            if not k["kind"].startswith("conv") or k["kernel"] not in busy:
+                continue
+            b = _mean(busy[k["kernel"]])
+            alg = k["flop_per_launch"] / 2048.0 * args.cycles
+            share = b / (k["avg_launch_us"] * 1e-6 * args.clock * 1e9 * 1024)
+            print(f"| `{k['kernel']}` | {k['launches_per_step']:.2f} | {b:,.0f} | {alg:,.0f} | {k['avg_launch_us']:.2f} | "
+                  f"{100 * share:.1f}% |")
     elif args.cmd == "replays":
         with open(args.bench) as f:
             line = [l for l in f if l.startswith("{")][-1]
