@@ -26,6 +26,45 @@ namespace {
 typedef float v4f __attribute__((ext_vector_type(4)));
 typedef short v4s __attribute__((ext_vector_type(4)));
 
+// one DPP lane permutation of a float within each row of 16 lanes
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v)
+{
+    return __builtin_bit_cast(float, __builtin_amdgcn_mov_dpp(__builtin_bit_cast(int, v), CTRL, 0xF, 0xF, false));
+}
+constexpr int kDppXor1 = 0xB1, kDppXor2 = 0x4E;             // quad_perm [1,0,3,2], [2,3,0,1]
+constexpr int kDppHalfMirror = 0x141, kDppMirror = 0x140;   // lane i <-> 7-i in 8, 15-i in 16
+// sum over the 16 lanes of a row: the quad exchanges give every lane its
+// quad's sum, the half-row mirror pairs each quad with the other quad of its
+// half, the row mirror each half with the other; a + b and b + a are the same
+// float, so all 16 lanes hold the same total
+__device__ __forceinline__ float row16_sum(float v)
+{
+    v += dpp_f<kDppXor1>(v);
+    v += dpp_f<kDppXor2>(v);
+    v += dpp_f<kDppHalfMirror>(v);
+    v += dpp_f<kDppMirror>(v);
+    return v;
+}
+// (mean, M2) of n values per lane merged over the 16 lanes of a row by the
+// same pairing: two parts of equal count n give mean (m + m')/2 and
+// M2 q + q' + (n/2)(m - m')^2, the same on both lanes of a pair
+template <int CTRL>
+__device__ __forceinline__ void merge_step(float& m, float& q, float n)
+{
+    const float m2 = dpp_f<CTRL>(m), q2 = dpp_f<CTRL>(q);
+    const float d = m - m2;
+    m = 0.5f * (m + m2);
+    q = (q + q2) + 0.5f * n * (d * d);
+}
+__device__ __forceinline__ void row16_meanvar(float& m, float& q, float n)
+{
+    merge_step<kDppXor1>(m, q, n);
+    merge_step<kDppXor2>(m, q, 2.f * n);
+    merge_step<kDppHalfMirror>(m, q, 4.f * n);
+    merge_step<kDppMirror>(m, q, 8.f * n);
+}
+
 // bfloat16 rounding (nearest even) of a float: its bits, and its value as a float
 __device__ __forceinline__ unsigned short bf16_bits(float f) { return __builtin_bit_cast(unsigned short, (__bf16)f); }
 __device__ __forceinline__ float bf16_round(float f) { return (float)(__bf16)f; }
@@ -137,13 +176,14 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     constexpr int WRQ = wrow(CC * 9 / 2);                       // (BMF) weight row stride, dwords
     constexpr int XS_FLOATS = BMF ? (CC / 4) * QPS * 2 : CC * PS;
     constexpr int WC_FLOATS = BMF ? TK * WRQ : TK * WR;
-    static_assert(XS_FLOATS >= 2 * WP * TK, "input tile reused by the statistics epilogue");
     __shared__ __attribute__((aligned(16))) float Xs[XS_FLOATS];
     __shared__ __attribute__((aligned(16))) float Wc[WC_FLOATS];
     unsigned short* const Xh = reinterpret_cast<unsigned short*>(Xs);  // (BMF) bf16 views
     unsigned short* const Wh = reinterpret_cast<unsigned short*>(Wc);
     // folded BN backward: per input channel (a, b, d, mean, invstd, scale, shift)
     __shared__ __attribute__((aligned(16))) float ftab[FOLD ? kFoldMaxChannels * 8 : 4];
+    // per-wave parts of the epilogue's per-tile channel sums: [2][WP][TK]
+    __shared__ float wred[2 * WP * TK];
 
     constexpr int tiles = WO / TH;       // row tiles per (square) image
     static_assert(WO % TH == 0, "row tiles");
@@ -600,15 +640,12 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
         for (int i = 0; i < 4; ++i) a.y[oidx[nb] + i * cstr] = acc[nb][i];
     if constexpr (TRANS) {
         if (a.bnb.part) {  // per-tile backward sums of each channel
-            float* red = Xs;  // [2][WP][TK]
-            __syncthreads();
+            float* red = wred;
 #pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int off = 8; off > 0; off >>= 1) {
-                    gs1[i] += __shfl_xor(gs1[i], off, 16);
-                    gs2[i] += __shfl_xor(gs2[i], off, 16);
-                }
+            for (int i = 0; i < 4; ++i) {
+                gs1[i] = row16_sum(gs1[i]);
+                gs2[i] = row16_sum(gs2[i]);
+            }
             if (j == 0)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
@@ -628,62 +665,59 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
                     a.bnb.part[((size_t)m * T_all + tl) * 2 + 0] = t1;
                     a.bnb.part[((size_t)m * T_all + tl) * 2 + 1] = t2;
                 }
+            if (TPW > 1) __syncthreads();  // wred is written again by the next tile
         }
     }
     if constexpr (!TRANS) {
         if (a.bn.part) {
-            // per-tile statistics of each output channel over the TH*WO pixels
-            constexpr int P = TH * WO;
-            float* red = Xs;  // [WP][TK], the input tile is no longer read
-            __syncthreads();
-            float sv[4];
+            // per-tile statistics of each output channel over the TH*WO
+            // pixels: each wave takes the two-pass (mean, M2) of its own
+            // 16*NBW pixels in registers, and one lane per channel combines
+            // the WP equal-count parts (mean = mean of the means, M2 = sum
+            // of the M2 + n * sum of the squared mean deviations)
+            // (a lane's NBW values first, then the 16 lanes of its row)
+            constexpr float PW = 16.f * NBW;
+            float wm[4], wq[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
                 float v = 0.f;
 #pragma unroll
                 for (int nb = 0; nb < NBW; ++nb) v += acc[nb][i];
-#pragma unroll
-                for (int off = 8; off > 0; off >>= 1) v += __shfl_xor(v, off, 16);
-                sv[i] = v;
-            }
-            if (j == 0)
-#pragma unroll
-                for (int i = 0; i < 4; ++i) red[wp * TK + wk * 16 + 4 * g + i] = sv[i];
-            __syncthreads();
-            float mu[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                float t = 0.f;
-                for (int q = 0; q < WP; ++q) t += red[q * TK + wk * 16 + 4 * g + i];
-                mu[i] = t / (float)P;
-            }
-            __syncthreads();
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                float v = 0.f;
+                wm[i] = v / (float)NBW;
+                float q = 0.f;
 #pragma unroll
                 for (int nb = 0; nb < NBW; ++nb) {
-                    const float d = acc[nb][i] - mu[i];
-                    v += d * d;
+                    const float d = acc[nb][i] - wm[i];
+                    q += d * d;
                 }
-#pragma unroll
-                for (int off = 8; off > 0; off >>= 1) v += __shfl_xor(v, off, 16);
-                sv[i] = v;
+                wq[i] = q;
+                row16_meanvar(wm[i], wq[i], (float)NBW);
             }
             if (j == 0)
 #pragma unroll
-                for (int i = 0; i < 4; ++i) red[wp * TK + wk * 16 + 4 * g + i] = sv[i];
+                for (int i = 0; i < 4; ++i) {
+                    wred[wp * TK + wk * 16 + 4 * g + i] = wm[i];
+                    wred[(WP + wp) * TK + wk * 16 + 4 * g + i] = wq[i];
+                }
             __syncthreads();
-
             if (wp == 0 && j == 0)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    float t = 0.f;
-                    for (int q = 0; q < WP; ++q) t += red[q * TK + wk * 16 + 4 * g + i];
-                    const int m = mblk + wk * 16 + 4 * g + i;
-                    a.bn.part[((size_t)m * T_all + tl) * 2 + 0] = mu[i];
-                    a.bn.part[((size_t)m * T_all + tl) * 2 + 1] = t;
+                    const int c = wk * 16 + 4 * g + i;
+                    float mu = 0.f;
+                    for (int q = 0; q < WP; ++q) mu += wred[q * TK + c];
+                    mu /= (float)WP;
+                    float m2 = 0.f, dev = 0.f;
+                    for (int q = 0; q < WP; ++q) {
+                        const float d = wred[q * TK + c] - mu;
+                        m2 += wred[(WP + q) * TK + c];
+                        dev += d * d;
+                    }
+                    const int m = mblk + c;
+                    a.bn.part[((size_t)m * T_all + tl) * 2 + 0] = mu;
+                    a.bn.part[((size_t)m * T_all + tl) * 2 + 1] = m2 + PW * dev;
                 }
+            if (TPW > 1) __syncthreads();  // wred is written again by the next tile
         }
     }
 #pragma unroll
@@ -988,12 +1022,10 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
         float* red = Xs;  // [2][WP][TK]
         __syncthreads();
 #pragma unroll
-        for (int v = 0; v < 4; ++v)
-#pragma unroll
-            for (int off = 8; off > 0; off >>= 1) {
-                gs1[v] += __shfl_xor(gs1[v], off, 16);
-                gs2[v] += __shfl_xor(gs2[v], off, 16);
-            }
+        for (int v = 0; v < 4; ++v) {
+            gs1[v] = row16_sum(gs1[v]);
+            gs2[v] = row16_sum(gs2[v]);
+        }
         if (j == 0)
 #pragma unroll
             for (int v = 0; v < 4; ++v) {
