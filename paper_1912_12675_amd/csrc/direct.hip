@@ -366,8 +366,8 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
 #pragma unroll
             for (int k = 0; k < XV; ++k)
                 if ((okm & (1u << k)) && xrow[k] >= 1 && xrow[k] <= TH) {
-                    *reinterpret_cast<float4*>(a.fold.dy + xb + xg[k]) = xr[k];
-                    if constexpr (FOLD == 2) *reinterpret_cast<float4*>(a.fold.dres + xb + xg[k]) = fyr[k];
+                    store_stream4(a.fold.dy + xb + xg[k], xr[k]);
+                    if constexpr (FOLD == 2) store_stream4(a.fold.dres + xb + xg[k], fyr[k]);
                 }
         }
     };
@@ -637,7 +637,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
 #pragma unroll
     for (int nb = 0; nb < NBW; ++nb)
 #pragma unroll
-        for (int i = 0; i < 4; ++i) a.y[oidx[nb] + i * cstr] = acc[nb][i];
+        for (int i = 0; i < 4; ++i) store_stream(a.y + oidx[nb] + i * cstr, acc[nb][i]);
     if constexpr (TRANS) {
         if (a.bnb.part) {  // per-tile backward sums of each channel
             float* red = wred;
@@ -1017,7 +1017,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_dgrad_s2(DgArgs a)
         for (int v = 0; v < 4; ++v)
 #pragma unroll
             for (int ph = 0; ph < 2; ++ph)
-                *reinterpret_cast<float2*>(a.dx + oidx[nb] + v * cstr + ph * W2) = val[nb][v][ph];
+                store_stream2(a.dx + oidx[nb] + v * cstr + ph * W2, val[nb][v][ph]);
     if (a.bnb.part) {
         float* red = Xs;  // [2][WP][TK]
         __syncthreads();

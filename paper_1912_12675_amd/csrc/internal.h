@@ -10,6 +10,23 @@
 
 namespace psw {
 
+// ---- streaming stores ----------------------------------------------------
+// Large outputs that later kernels read back (activations, gradients, split
+// partial sums) are stored non-temporally: they stream to memory while the
+// kernel runs instead of staying dirty in the XCD's L2, which the end of a
+// kernel would otherwise write back before the next one starts.
+__device__ __forceinline__ void store_stream(float* p, float v) { __builtin_nontemporal_store(v, p); }
+__device__ __forceinline__ void store_stream2(float* p, float2 v)
+{
+    typedef float f2v __attribute__((ext_vector_type(2)));
+    __builtin_nontemporal_store(f2v{v.x, v.y}, reinterpret_cast<f2v*>(p));
+}
+__device__ __forceinline__ void store_stream4(float* p, float4 v)
+{
+    typedef float f4v __attribute__((ext_vector_type(4)));
+    __builtin_nontemporal_store(f4v{v.x, v.y, v.z, v.w}, reinterpret_cast<f4v*>(p));
+}
+
 // ---- kernel timing hook -------------------------------------------------
 // While a recorder is installed on the calling thread (the scheduler does so
 // in its profiling mode), every kernel the library launches is timed with a

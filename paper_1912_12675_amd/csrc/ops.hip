@@ -947,7 +947,7 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
 #pragma unroll
             for (int e = 0; e < 4; ++e) v[e] = fmaxf(v[e], 0.f);
         }
-        *reinterpret_cast<float4*>(z + idx[q]) = make_float4(v[0], v[1], v[2], v[3]);
+        store_stream4(z + idx[q], make_float4(v[0], v[1], v[2], v[3]));
     }
 }
 
@@ -1030,10 +1030,9 @@ __global__ __launch_bounds__(kBlock) void bn_bwd_partials_k(int n, int c, int hw
             const float xh = (yy[e] - mu) * is;
             o[e] = a * (g[e] - b - xh * d);
         }
-        *reinterpret_cast<float4*>(dy + idx[q]) = make_float4(o[0], o[1], o[2], o[3]);
+        store_stream4(dy + idx[q], make_float4(o[0], o[1], o[2], o[3]));
         if (identity) {
-            *reinterpret_cast<float4*>(dres + idx[q]) =
-                make_float4(g[0] + ov[q].x, g[1] + ov[q].y, g[2] + ov[q].z, g[3] + ov[q].w);
+            store_stream4(dres + idx[q], make_float4(g[0] + ov[q].x, g[1] + ov[q].y, g[2] + ov[q].z, g[3] + ov[q].w));
         } else if (shortcut_a) {  // residual rows 2hh (g at even columns) and 2hh+1 (zero)
             const int img = u / hw4, off = (u - img * hw4) * 4;
             const int hh = off / w, ww = off - hh * w;

@@ -278,7 +278,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX * IPW) void conv3x3_wgrad(WgAr
         if (c >= a.C) continue;  // zero-filled channels of a narrow input (C < 16)
         float* o = out + ((size_t)k * a.C + c) * 9;
 #pragma unroll
-        for (int t = 0; t < 9; ++t) o[t] = acc[t][i];
+        for (int t = 0; t < 9; ++t) store_stream(o + t, acc[t][i]);
     }
 }
 
