@@ -1,0 +1,67 @@
+"""Where a float32 training step parts from the fp64 oracle at batch 128:
+ReLU decisions on pre-activations within rounding of zero.
+
+ResNet-20 (batch 128, PPV (7,13,19), staleness [3,2,1,0]), one step of the
+stale-weight schedule (Sec. 3) from the oracle's own trajectory at t = 0 and
+t = 25.  The same step written in torch autograd
+
+  - in float64 equals the oracle (1e-10): its ReLU decisions are the oracle's;
+  - in float32 taking those decisions lands within the 1e-4 parity target of
+    the oracle (gradient and momentum, rel-L2);
+  - in float32 taking its own decisions differs from the float64 run in a
+    handful of the 24.1M decisions, each on a pre-activation within 1e-5 of
+    its layer's RMS of zero, and those few flips alone move the gradient and
+    the update by ~1e-3.
+
+So the distance of any float32 implementation from the oracle after one full
+step at this batch size is set by a few threshold decisions, not by its
+arithmetic; the GPU one-step tests hold the step to that spread and check the
+GPU's own decisions the same way, while the kernels themselves are held to
+2e-5 element by element given their inputs."""
+import numpy as np
+import pytest
+import torch
+
+from paper_1912_12675_amd import synth
+from tests.onestep_ref import distances, oracle_step, resnet20_state, torch_step
+
+
+def relu_flips(pre64, masks):
+    """(number of decisions where masks differ from pre64 > 0, largest
+    |pre64| / RMS(pre64 of its op) over them)."""
+    n, worst = 0, 0.0
+    for i, p in pre64.items():
+        d = (p > 0) != masks[i]
+        k = int(d.sum())
+        if k:
+            n += k
+            rms = float(torch.sqrt((p * p).mean()))
+            worst = max(worst, float(p[d].abs().max()) / rms)
+    return n, worst
+
+
+@pytest.mark.parametrize("t", [0, 25])
+def test_fp32_step_with_the_oracles_decisions_meets_the_target(oracle, t):
+    torch.set_num_threads(8)
+    wl = synth.resnet20_workload()
+    state = resnet20_state(oracle, wl, t)
+    ref = oracle_step(oracle, wl, state)
+    w_t = np.concatenate([w[state.t] for w in state.window]).astype(np.float64)
+    rec64 = {"pre": {}}
+    d64 = distances(wl, torch_step(wl, state, dtype=torch.float64, decisions=rec64), ref, w_t)
+    masks64 = {i: p > 0 for i, p in rec64["pre"].items()}
+    d_forced = distances(wl, torch_step(wl, state, decisions={"mask": masks64}), ref, w_t)
+    rec32 = {"pre": {}}
+    d_own = distances(wl, torch_step(wl, state, decisions=rec32), ref, w_t)
+    n_flip, worst = relu_flips(rec64["pre"], {i: p > 0 for i, p in rec32["pre"].items()})
+    total = sum(p.numel() for p in rec64["pre"].values())
+    print(f"t={t}: fp64 grad {d64['grad']:.2e} | fp32 with the fp64 decisions: grad {d_forced['grad']:.2e} "
+          f"momentum {d_forced['momentum']:.2e} update {d_forced['update']:.2e} | fp32 own decisions: grad "
+          f"{d_own['grad']:.2e} momentum {d_own['momentum']:.2e} update {d_own['update']:.2e}; "
+          f"{n_flip} of {total} decisions differ, largest |pre| / RMS {worst:.1e}")
+    assert d64["grad"] <= 1e-10 and d64["momentum"] <= 1e-10
+    assert len(rec64["pre"]) == 19  # every BN + ReLU of ResNet-20
+    assert d_forced["grad"] <= 1e-5 and d_forced["momentum"] <= 1e-5
+    assert d_forced["update"] <= 1e-4
+    assert 0 < n_flip <= 100 and worst <= 1e-5
+    assert d_own["grad"] >= 20 * d_forced["grad"]

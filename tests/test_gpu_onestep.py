@@ -31,18 +31,15 @@ computed here), t = 25 and 49 (stored by tests/golden/make_golden.py, which
 calls only the oracle).  AlexNet, VGG-16-BN and ResNet-110 start from a
 seeded synthetic checkpoint whose ring slots all differ, so every stage
 reads a stale version distinct from the current one."""
-import os
-
 import numpy as np
 import pytest
 import torch
 
 from paper_1912_12675_amd import synth
-from tests import torch_ref
+from tests.onestep_ref import distances, oracle_step, rel, resnet20_state, synthetic_state, torch_step, ulp_move
 
 pytestmark = pytest.mark.gpu
 
-GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
 @pytest.fixture(scope="module")
@@ -51,75 +48,6 @@ def P():
     psw.lib()
     assert torch.cuda.is_available(), "GPU tests need a GPU"
     return psw
-
-
-class State:
-    """Checkpoint at step t: window[s] maps version -> float32 vector of
-    stage s (versions max(0, t-D_s+1) .. t), momentum, running statistics."""
-
-    def __init__(self, t, window, momentum, run_mean, run_var):
-        self.t, self.window, self.momentum, self.run_mean, self.run_var = t, window, momentum, run_mean, run_var
-
-    def version(self, s, v):
-        return self.window[s][v]
-
-
-def _counts(oracle, wl):
-    return [int(c) for c in oracle.param_counts(wl.ops, wl.in_shape, 1, wl.stage_end)]
-
-
-def _split(flat, counts):
-    return np.split(np.asarray(flat), np.cumsum(counts)[:-1])
-
-
-def _n_bn(wl):
-    return int(sum(int(o[4]) for o in wl.ops if int(o[0]) == synth.BN))
-
-
-def resnet20_state(oracle, wl, t):
-    counts = _counts(oracle, wl)
-    depth = wl.ring_depth()
-    p0 = synth.init_params(wl)
-    nbn = _n_bn(wl)
-    if t == 0:
-        return State(0, [{0: v} for v in _split(p0, counts)], np.zeros(sum(counts), np.float32),
-                     np.zeros(nbn, np.float32), np.ones(nbn, np.float32))
-    if t == 1:  # the oracle's first step, rounded to float32 like a stored state
-        xs, ys = synth.batches(wl, 1)
-        r = oracle.train_from(wl.ops, wl.in_shape, wl.stage_end, 0, [[v] for v in _split(p0, counts)], None, xs, ys,
-                              wl.staleness(1), wl.lr_table(1), wl.momentum, wl.weight_decay, wl.nesterov,
-                              bf16=wl.bf16, out_depth=2)
-        win = [{0: p0s, 1: r["history"][s][1].astype(np.float32)} for s, p0s in enumerate(_split(p0, counts))]
-        return State(1, win, r["momentum"].astype(np.float32), r["run_mean"].astype(np.float32),
-                     r["run_var"].astype(np.float32))
-    mode = "bf16" if wl.bf16 else "fp32"
-    path = os.path.join(GOLDEN, f"resnet20_b128_states_{mode}.npz")
-    assert os.path.exists(path), f"missing {path} (python tests/golden/make_golden.py states_{mode})"
-    g = np.load(path)
-    win = []
-    for s in range(len(counts)):
-        vs = g[f"t{t}_s{s}"]
-        assert vs.shape == (depth[s], counts[s])
-        win.append({t - depth[s] + 1 + k: vs[k] for k in range(depth[s])})
-    return State(t, win, g[f"t{t}_momentum"], g[f"t{t}_run_mean"], g[f"t{t}_run_var"])
-
-
-def synthetic_state(oracle, wl, t, seed):
-    """Seeded checkpoint at step t: version v of stage s is W^(0) moved by
-    1e-3 * N(0,1) * (|W^(0)| + 1e-2) (a fresh draw per version), the momentum
-    1e-2 * N(0,1) * (|W^(0)| + 1e-2), running statistics mean 0 / var 1."""
-    counts = _counts(oracle, wl)
-    depth = wl.ring_depth(t + 1)
-    rng = np.random.Generator(np.random.PCG64([seed, t]))
-    p0 = synth.init_params(wl)
-    win = []
-    for s, p in enumerate(_split(p0, counts)):
-        scale = np.abs(p) + np.float32(1e-2)
-        win.append({v: (p + np.float32(1e-3) * rng.standard_normal(p.size, dtype=np.float32) * scale)
-                    for v in range(max(0, t - depth[s] + 1), t + 1)})
-    mom = (np.float32(1e-2) * rng.standard_normal(p0.size, dtype=np.float32) * (np.abs(p0) + np.float32(1e-2)))
-    nbn = _n_bn(wl)
-    return State(t, win, mom.astype(np.float32), np.zeros(nbn, np.float32), np.ones(nbn, np.float32))
 
 
 def gpu_step(P, wl, state, ring_depth):
@@ -140,62 +68,12 @@ def gpu_step(P, wl, state, ring_depth):
     ver = net.step(t, st, wl.lr_at(t), torch.from_numpy(x).cuda(), torch.from_numpy(y).cuda(), wl.momentum,
                    wl.weight_decay, wl.nesterov)
     torch.cuda.synchronize()
+    # the GPU's ReLU decisions: output of every op with a ReLU > 0
+    relu_ops = [i for i, o in enumerate(wl.ops) if int(o[0]) in (synth.CONV, synth.BN, synth.FC) and
+                int(o[8]) & synth.F_RELU]
+    masks = {i: (net.tensor(i + 1) > 0).cpu() for i in relu_ops}
     return dict(versions=ver, grad=net.grad.double().cpu().numpy(), momentum=net.momentum.double().cpu().numpy(),
-                params=net.params(t + 1).double().numpy(), loss=float(net.loss.item()))
-
-
-def oracle_step(oracle, wl, state):
-    t = state.t
-    D = max(len(w) for w in state.window)
-    hist0 = [[w.get(v) for v in range(t - D + 1, t + 1)] for w in state.window]
-    hist0 = [[None if a is None else a.astype(np.float64) for a in row] for row in hist0]
-    x, y = synth.batch(wl, t)
-    st = wl.staleness(t + 1)[t:t + 1]
-    nbn = _n_bn(wl)
-    r = oracle.train_from(wl.ops, wl.in_shape, wl.stage_end, t, hist0, state.momentum.astype(np.float64), x[None],
-                          y[None], st, wl.lr_table(1, t0=t), wl.momentum, wl.weight_decay, wl.nesterov, bf16=wl.bf16,
-                          dropout_seed=wl.dropout_seed,
-                          run_mean=state.run_mean.astype(np.float64) if nbn else None,
-                          run_var=state.run_var.astype(np.float64) if nbn else None)
-    return dict(versions=r["versions"][0], grad=r["grad"], momentum=r["momentum"], params=r["params"],
-                loss=float(r["losses"][0]))
-
-
-def ulp_move(x, seed):
-    """x moved one float32 ulp up or down element by element (seeded signs)."""
-    up = np.random.Generator(np.random.PCG64(seed)).random(x.shape) < 0.5
-    return np.where(up, np.nextafter(x, np.float32(np.inf)), np.nextafter(x, np.float32(-np.inf))).astype(np.float32)
-
-
-def torch_step(wl, state, x=None):
-    """The same step in torch float32 (CPU), bf16-rounded product operands in
-    bf16 mode; x replaces the step's mini-batch when given."""
-    t = state.t
-    st = wl.staleness(t + 1)[t]
-    wfor = [w[max(0, t - int(st[s]))] for s, w in enumerate(state.window)]
-    wcur = [w[t] for w in state.window]
-    xb, y = synth.batch(wl, t)
-    return torch_ref.stale_step_from(wl.ops, wl.stage_end, wfor, wcur, state.momentum, xb if x is None else x, y,
-                                     wl.lr_at(t), wl.momentum, wl.weight_decay, wl.nesterov, dtype=torch.float32,
-                                     bf16=wl.bf16, dropout_key=(wl.dropout_seed, t))
-
-
-def rel(a, b):
-    return float(np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-300))
-
-
-def distances(wl, got, ref, w_t):
-    """Distances of `got` from the oracle's `ref` (w_t: W^(t), float32 values)."""
-    layout, counts = synth.param_layout(wl)
-    base = np.concatenate([[0], np.cumsum(counts)])
-    per = {}
-    for op, name, shape, s, off in layout:
-        i0 = int(base[s]) + off
-        sl = slice(i0, i0 + int(np.prod(shape)))
-        per[f"op {op} {name}{tuple(shape)}"] = rel(got["grad"][sl], ref["grad"][sl])
-    return dict(grad=rel(got["grad"], ref["grad"]), per=per, momentum=rel(got["momentum"], ref["momentum"]),
-                update=rel(got["params"] - w_t, ref["params"] - w_t),
-                loss=abs(got["loss"] - ref["loss"]) / abs(ref["loss"]))
+                params=net.params(t + 1).double().numpy(), loss=float(net.loss.item()), masks=masks)
 
 
 SPREAD_SAMPLES = 8
@@ -241,7 +119,30 @@ def check_step(P, oracle, wl, state, ring_depth, label):
     for k in ("grad", "momentum", "update"):
         assert d[k] <= max(tol, 4 * sp[k]), f"{k} rel-L2 {d[k]:.3e} (spread {sp[k]:.2e})"
     assert d["loss"] <= max(2e-3 if wl.bf16 else 1e-5, 4 * sp["loss"]), f"loss rel {d['loss']:.3e}"
-    return d, sp
+    return got
+
+
+def check_decisions(wl, state, got, label):
+    """The GPU's ReLU decisions against those of the float64 computation of
+    the step (torch autograd, equal to the oracle at 1e-10): only a handful
+    may differ, each on a pre-activation within 1e-5 of its layer's RMS of
+    zero (float32 rounding); in float32 such ties are where every
+    implementation parts from the oracle (tests/test_decisions.py)."""
+    rec = {"pre": {}}
+    torch_step(wl, state, dtype=torch.float64, decisions=rec)
+    assert sorted(rec["pre"]) == sorted(got["masks"]), "ReLU sites"
+    n, worst, total = 0, 0.0, 0
+    for i, pre in rec["pre"].items():
+        g = got["masks"][i].reshape(pre.shape)
+        diff = (pre > 0) != g
+        total += pre.numel()
+        k = int(diff.sum())
+        if k:
+            n += k
+            worst = max(worst, float(pre[diff].abs().max() / torch.sqrt((pre * pre).mean())))
+    print(f"{label} t={state.t}: {n} of {total} ReLU decisions differ from the float64 step's, largest "
+          f"|pre-activation| / RMS {worst:.1e}", flush=True)
+    assert n <= 100 and worst <= 1e-5
 
 
 @pytest.mark.parametrize("t", [0, 1, 25, 49])
@@ -249,7 +150,10 @@ def check_step(P, oracle, wl, state, ring_depth, label):
 def test_resnet20_b128_one_step(P, oracle, mode, t):
     """The benchmark's configuration, one step from the oracle's trajectory."""
     wl = synth.resnet20_workload(bf16=(mode == "bf16"))
-    check_step(P, oracle, wl, resnet20_state(oracle, wl, t), wl.ring_depth(), f"resnet20 b128 {mode}")
+    state = resnet20_state(oracle, wl, t)
+    got = check_step(P, oracle, wl, state, wl.ring_depth(), f"resnet20 b128 {mode}")
+    if mode == "fp32":
+        check_decisions(wl, state, got, f"resnet20 b128 {mode}")
 
 
 FULL = [

@@ -124,12 +124,28 @@ class _Bf16Linear(torch.autograd.Function):
         return _rb(dy) @ _rb(w), _rb(dy).t() @ _rb(x), db
 
 
+def _relu(y, i, decisions):
+    """ReLU of op i's pre-activation y.  decisions: None, or a dict whose
+    "pre" entry (if present) collects each op's pre-activation (detached),
+    and whose "mask" entry (if present) supplies, per op, the boolean pass
+    decisions to take instead of y > 0 (the output is then y where the mask
+    passes and 0 elsewhere, the gradient passes where the mask does)."""
+    if decisions is None:
+        return F.relu(y)
+    if "pre" in decisions:
+        decisions["pre"][i] = y.detach().clone()
+    if "mask" in decisions:
+        return y * decisions["mask"][i].to(y.dtype)
+    return F.relu(y)
+
+
 def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5, bn_mom=0.1, dropout_key=None,
-            bf16=False):
+            bf16=False, decisions=None):
     """Apply ops[lo:hi].  inputs: dict tensor_id -> tensor (must hold every
     tensor that ops[lo:hi] read from outside the range).  stage_params: list
     of flat per-stage torch tensors.  dropout_key: (seed, step) of the
-    dropout masks.  Returns the dict extended with the tensors written."""
+    dropout masks.  decisions: see _relu.  Returns the dict extended with the
+    tensors written."""
     t = dict(inputs)
     for i in range(lo, hi):
         kind, in0, in1, cin, cout, k, stride, pad, flags = (int(v) for v in ops[i])
@@ -142,7 +158,7 @@ def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5
             else:
                 y = F.conv2d(a, P["weight"], P.get("bias"), stride=stride, padding=pad)
             if flags & F_RELU:
-                y = F.relu(y)
+                y = _relu(y, i, decisions)
         elif kind == BN:
             rm = rv = None
             if running is not None:
@@ -151,7 +167,7 @@ def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5
             if in1 >= 0:
                 y = y + _shortcut(t[in1], y.shape[1], y.shape[2])
             if flags & F_RELU:
-                y = F.relu(y)
+                y = _relu(y, i, decisions)
         elif kind == MAXPOOL:
             y = F.max_pool2d(a, k, stride)
         elif kind == GAVG:
@@ -162,7 +178,7 @@ def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5
             else:
                 y = F.linear(a.reshape(a.shape[0], -1), P["weight"], P.get("bias"))
             if flags & F_RELU:
-                y = F.relu(y)
+                y = _relu(y, i, decisions)
             y = y.reshape(y.shape[0], -1, 1, 1)
         elif kind == DROPOUT:
             seed, step = dropout_key if dropout_key is not None else (0, 0)
@@ -370,15 +386,15 @@ def train_stale(ops, stage_end, params0, xs, labels, staleness, lr, mom=0.9, wd=
 
 
 def stale_step_from(ops, stage_end, wfor, wcur, mom0, x, labels, lr, mom=0.9, wd=0.0, nesterov=False,
-                    dtype=torch.float64, bf16=False, dropout_key=None):
+                    dtype=torch.float64, bf16=False, dropout_key=None, decisions=None):
     """One step of the stale-weight schedule from a given state, written with
     autograd: forward with the per-stage vectors wfor (version t - d_s), then
     the current versions wcur are swapped into the same tensors before the
     backward pass (data gradients with version t, weight gradients from the
     saved activations), then d = g + wd*wcur, v = mom*v0 + d,
     w = wcur - lr*(nesterov ? d + mom*v : v).
-    lr: scalar or [S].  Returns dict(grad, momentum, params, loss), vectors
-    concatenated over stages."""
+    lr: scalar or [S].  decisions: see _relu.  Returns dict(grad, momentum,
+    params, loss), vectors concatenated over stages."""
     slices, counts = op_param_slices(ops, stage_end)
     S = len(counts)
     Wp = [torch.tensor(np.asarray(w, np.float64), dtype=dtype, requires_grad=True) for w in wfor]
@@ -386,7 +402,8 @@ def stale_step_from(ops, stage_end, wfor, wcur, mom0, x, labels, lr, mom=0.9, wd
     v0 = split_flat(torch.tensor(np.asarray(mom0, np.float64), dtype=dtype), counts)
     lrs = np.broadcast_to(np.asarray(lr, dtype=np.float64), (S,))
     n = len(ops)
-    outs = run_ops(ops, 0, n, {0: torch.tensor(x, dtype=dtype)}, Wp, slices, dropout_key=dropout_key, bf16=bf16)
+    outs = run_ops(ops, 0, n, {0: torch.tensor(x, dtype=dtype)}, Wp, slices, dropout_key=dropout_key, bf16=bf16,
+                   decisions=decisions)
     loss = F.cross_entropy(outs[n].reshape(outs[n].shape[0], -1), torch.tensor(labels, dtype=torch.long))
     with torch.no_grad():
         for s in range(S):
