@@ -1097,6 +1097,14 @@ hipError_t launch_direct(const DirArgs& a, int n, bool trans, bool bf, hipStream
 
 }  // namespace
 
+// The 32x32 stride-1 backward-data kernels use 16-row tiles once 8-row tiles
+// would number 1024 or more (batch 256): every workgroup of a folded BN
+// backward merges the per-tile sums of all the producer's tiles, so that
+// merge grows with the square of the tile count; 16-row tiles quarter it
+// (ResNet-110 b256: folded kernels 30.7 -> 27.0 us), while at batch 128 the
+// two sizes time the same.
+static bool dgrad_tall_tiles(int n, int ho) { return ho % 16 == 0 && (int64_t)n * (ho / 8) >= 1024; }
+
 // Returns hipErrorNotSupported (nothing launched) when no tile configuration
 // covers the shape; the caller then uses the general implicit GEMM.
 int conv3x3_direct_tiles(int n, int C, int H, int W, int K, int stride)
@@ -1155,7 +1163,11 @@ hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const f
     }
     if (C % 16) return hipErrorNotSupported;
     if (stride == 1) {
-        if (WO == 32 && HO % 8 == 0 && K % 16 == 0) return launch_direct<32, 1, 8, 16, 1, 4, 4>(a, n, transpose, bf16, st);
+        if (WO == 32 && HO % 8 == 0 && K % 16 == 0) {
+            if (transpose && dgrad_tall_tiles(n, HO))
+                return launch_direct<32, 1, 16, 16, 1, 8, 4>(a, n, true, bf16, st);
+            return launch_direct<32, 1, 8, 16, 1, 4, 4>(a, n, transpose, bf16, st);
+        }
         if (WO == 16 && HO % 8 == 0 && K % 32 == 0) return launch_direct<16, 1, 8, 16, 2, 4, 2>(a, n, transpose, bf16, st);
         if (WO == 8 && HO % 8 == 0 && K % 32 == 0) return launch_direct<8, 1, 8, 16, 2, 4, 1>(a, n, transpose, bf16, st);
     } else if (!transpose) {
@@ -1214,7 +1226,7 @@ int dgrad_bnsums_tiles(int n, int CL, int H, int W, int KL, int stride)
     if (stride == 1) {
         if (KL % 16 || H != W) return 0;
         if ((int64_t)n * (CL > KL ? CL : KL) * H * W > INT32_MAX) return 0;
-        if (W == 32 && H % 8 == 0 && CL % 16 == 0) return n * (H / 8);
+        if (W == 32 && H % 8 == 0 && CL % 16 == 0) return n * (H / (dgrad_tall_tiles(n, H) ? 16 : 8));
         if (W == 16 && H % 8 == 0 && CL % 32 == 0) return n * (H / 8);
         if (W == 8 && H % 8 == 0 && CL % 32 == 0) return n * (H / 8);
         return 0;

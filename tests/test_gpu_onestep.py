@@ -337,6 +337,16 @@ def test_resnet20_b128_every_kernel_in_situ(P, oracle, mode):
     check_in_situ(P, oracle, wl, resnet20_state(oracle, wl, 25), wl.ring_depth(), f"resnet20 b128 {mode}")
 
 
+@pytest.mark.parametrize("mode", ["fp32", "bf16"])
+def test_resnet20_b256_every_kernel_in_situ(P, oracle, mode):
+    """The same at batch 256, from a seeded checkpoint in the stale phase:
+    there the 32x32 backward-data kernels use 16-row tiles, and the folded
+    BN backward passes merge the producer's 512 per-tile sums of those
+    tiles (ResNet-110's configuration runs on these kernels)."""
+    wl = synth.resnet20_workload(batch=256, bf16=(mode == "bf16"))
+    check_in_situ(P, oracle, wl, synthetic_state(oracle, wl, 5, 2027), wl.ring_depth(6), f"resnet20 b256 {mode}")
+
+
 @pytest.mark.parametrize("name,factory,t", FULL[:2], ids=[c[0] for c in FULL[:2]])
 def test_full_size_every_kernel_in_situ(P, oracle, name, factory, t):
     """The same for AlexNet-style (b128: 5x5 convs with bias and ReLU, max
