@@ -864,6 +864,20 @@ namespace {
 // issued before the merge so that the two memory latencies overlap, and
 // every load precedes every store.  Block y == 0 also stores the channel's
 // scale and shift, which the backward recomputes the ReLU mask from.
+// Per-tile statistics of one channel held in registers by the BN kernels:
+// thread t takes tiles t, t + kBlock, ... (the order of the sums), up to
+// kMergeTilesPerThread of them; larger tables are read in the merge loop.
+constexpr int kMergeTilesPerThread = 4;
+__device__ __forceinline__ void load_tile_stats(const float* pp, int T, float2 (&pv)[kMergeTilesPerThread])
+{
+#pragma unroll
+    for (int k = 0; k < kMergeTilesPerThread; ++k) {
+        const int t = (int)threadIdx.x + k * kBlock;
+        pv[k] = (t < T && T <= kMergeTilesPerThread * kBlock) ? *reinterpret_cast<const float2*>(pp + 2 * t)
+                                                              : make_float2(0.f, 0.f);
+    }
+}
+
 template <int U>
 __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int hw, const float* y, const float* part,
                                                                int T, int P, const float* gamma, const float* beta,
@@ -882,6 +896,11 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
     const bool identity = res && rc == c && rh == h && rw == w;
     const int lo = (c - rc) / 2, cc = ch - lo;
     const bool shortcut_a = res && !identity && cc >= 0 && cc < rc;
+    // the per-tile statistics are loaded first, so that their merge below
+    // runs while the tensor loads are in flight (loads complete in order)
+    const float* pp = part + (size_t)ch * T * 2;
+    float2 pv[kMergeTilesPerThread];
+    load_tile_stats(pp, T, pv);
     size_t idx[U];
     float4 yv[U], rv[U];
 #pragma unroll
@@ -903,12 +922,21 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
             }
         }
     }
-    const float* pp = part + (size_t)ch * T * 2;
     double s1 = 0.0, s2 = 0.0;
-    for (int t = threadIdx.x; t < T; t += kBlock) {
-        const double m = (double)pp[2 * t];
-        s1 += m;
-        s2 += (double)pp[2 * t + 1] + (double)P * m * m;
+    if (T <= kMergeTilesPerThread * kBlock) {
+#pragma unroll
+        for (int k = 0; k < kMergeTilesPerThread; ++k)
+            if ((int)threadIdx.x + k * kBlock < T) {
+                const double m = (double)pv[k].x;
+                s1 += m;
+                s2 += (double)pv[k].y + (double)P * m * m;
+            }
+    } else {
+        for (int t = threadIdx.x; t < T; t += kBlock) {
+            const double m = (double)pp[2 * t];
+            s1 += m;
+            s2 += (double)pp[2 * t + 1] + (double)P * m * m;
+        }
     }
     block_sum2(s1, s2, sh);
     if (threadIdx.x == 0) {
@@ -978,6 +1006,9 @@ __global__ __launch_bounds__(kBlock) void bn_bwd_partials_k(int n, int c, int hw
     const float sc = ymask ? scale[ch] : 0.f, sf = ymask ? scale[c + ch] : 0.f;
     const int cc = ch - (c - rc) / 2;  // residual channel (option A)
     const bool identity = res_mode == 1, shortcut_a = res_mode == 2 && cc >= 0 && cc < rc;
+    const float* pp = part + (size_t)ch * T * 2;  // loaded first, as in bn_apply_partials_k
+    float2 pv[kMergeTilesPerThread];
+    load_tile_stats(pp, T, pv);
     size_t idx[U];
     float4 gv[U], zv[U], yv[U], ov[U];
 #pragma unroll
@@ -995,11 +1026,19 @@ __global__ __launch_bounds__(kBlock) void bn_bwd_partials_k(int n, int c, int hw
             if (identity && res_accumulate) ov[q] = *reinterpret_cast<const float4*>(dres + idx[q]);
         }
     }
-    const float* pp = part + (size_t)ch * T * 2;
     double s1 = 0.0, s2 = 0.0;
-    for (int t = threadIdx.x; t < T; t += kBlock) {
-        s1 += (double)pp[2 * t];
-        s2 += (double)pp[2 * t + 1];
+    if (T <= kMergeTilesPerThread * kBlock) {
+#pragma unroll
+        for (int k = 0; k < kMergeTilesPerThread; ++k)
+            if ((int)threadIdx.x + k * kBlock < T) {
+                s1 += (double)pv[k].x;
+                s2 += (double)pv[k].y;
+            }
+    } else {
+        for (int t = threadIdx.x; t < T; t += kBlock) {
+            s1 += (double)pp[2 * t];
+            s2 += (double)pp[2 * t + 1];
+        }
     }
     block_sum2(s1, s2, sh);
     const float mu = mean[ch], is = invstd[ch];
@@ -1072,7 +1111,8 @@ hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, co
                                   float* save_scale, float* run_mean, float* run_var, hipStream_t st)
 {
     const bool identity = res && rc == c && rh == h && rw == w;
-    if (w % 4 || !aligned16(y) || !aligned16(z) || (identity && !aligned16(res))) return hipErrorNotSupported;
+    if (w % 4 || !aligned16(y) || !aligned16(z) || (identity && !aligned16(res)) || (uintptr_t)part % 8)
+        return hipErrorNotSupported;
     const int64_t units = (int64_t)n * h * w / 4;
     if (units > INT32_MAX) return hipErrorNotSupported;
     const int U = apply_units_per_thread(units * c);
@@ -1106,7 +1146,7 @@ hipError_t bn_bwd_from_partials(int n, int c, int h, int w, const float* dz, con
         else return hipErrorNotSupported;
     }
     if (relu && !scale && !z) return hipErrorInvalidValue;
-    if (w % 4 || !aligned16(dz) || !aligned16(y) || !aligned16(dy) || (z && !aligned16(z)) ||
+    if (w % 4 || !aligned16(dz) || !aligned16(y) || !aligned16(dy) || (z && !aligned16(z)) || (uintptr_t)part % 8 ||
         (dres && !aligned16(dres)))
         return hipErrorNotSupported;
     const int64_t units = (int64_t)n * h * w / 4;
