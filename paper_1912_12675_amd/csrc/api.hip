@@ -348,6 +348,10 @@ struct psw_net {
     std::vector<char> fold_bn, folded_now;
     std::vector<size_t> fold_off;
     size_t fold_base = 0, fold_bytes = 0;
+    // a BN whose output only a global average pool reads: per BN op, that
+    // pool op (else -1); the two backward passes run as one kernel
+    std::vector<int> gavg_of;
+    std::vector<char> gavg_fused;           // per pool op: its backward runs in its BN's kernel
 
     std::vector<char> grad_accum;           // per op input slot: 0 overwrite, 1 accumulate (in0, in1)
     size_t step_bytes = 0;                  // one step set (activations, saves, gradients, forward ws)
@@ -695,6 +699,27 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
         fold = align256(fold + (size_t)psw::conv_bwd_data_bnsums_tiles(ncs) * o.cin * 2 * sizeof(float));
     }
     net->fold_bytes = fold;
+    // BN -> global average pool, nothing else reading the BN output: the
+    // pool's gradient is uniform per (image, channel), and one kernel per
+    // channel does the pool backward and the BN backward (bn_bwd_gavg)
+    net->gavg_of.assign(n_layers, -1);
+    net->gavg_fused.assign(n_layers, 0);
+    for (int j = 0; j < n_layers; ++j) {
+        const psw_layer& pg = net->ops[j];
+        if (pg.kind != PSW_OP_GAVG || pg.in0 < 2) continue;
+        const int b = pg.in0 - 1;  // the op producing the pool's input
+        const psw_layer& o = net->ops[b];
+        if (o.kind != PSW_OP_BN || consumers[pg.in0] != 1 || net->grad_accum[2 * j] || net->fold_bn[b]) continue;
+        if (o.in1 == 0) continue;
+        if (o.in1 > 0) {  // identity residual only
+            const Tensor r = net->t[o.in1], yb = net->t[o.in0];
+            if (r.c != yb.c || r.h != yb.h || r.w != yb.w) continue;
+        }
+        const Tensor zt = net->t[pg.in0];
+        if ((zt.h * zt.w) % 4) continue;
+        net->gavg_of[b] = j;
+        net->gavg_fused[j] = 1;
+    }
     // split partial sums of the conv weight gradients, reduced by the stage update
     net->wpart_splits.assign(n_layers, 0);
     net->wpart_off.assign(n_layers, 0);
@@ -1231,7 +1256,15 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
             }
             kind = PSW_PROF_BN_BWD;
             bool done = false;
-            if (i + 1 < L && net->fused_bwd_now[i + 1]) {  // sums written by the next conv's dgrad into ws
+            if (net->gavg_of[i] >= 0) {  // with the global average pool's backward: dh = the pool output's gradient
+                PSW_TRY(psw::bn_bwd_gavg(a.n, a.c, a.h, a.w, is.grd(net->gavg_of[i] + 1), is.act(i + 1),
+                                         is.act(o.in0), is.wbwd(i), save, save + o.cin,
+                                         (o.flags & PSW_F_RELU) != 0, g, din, dg, dg + o.cin, dres,
+                                         net->grad_accum[2 * i + 1], sb),
+                        "bn_bwd_gavg");
+                done = true;
+            }
+            if (!done && i + 1 < L && net->fused_bwd_now[i + 1]) {  // sums written by the next conv's dgrad into ws
                 const psw_layer& cv = net->ops[i + 1];
                 psw::ConvShape ccs;
                 check_conv(y.n, y.c, y.h, y.w, cv.cout, cv.k, cv.k, cv.stride, cv.pad, net->prec, &ccs);
@@ -1262,6 +1295,7 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
             break;
         case PSW_OP_GAVG:
             kind = PSW_PROF_POOL;
+            if (net->gavg_fused[i]) break;  // in its BN's backward kernel (bn_bwd_gavg)
             if (din) PSW_TRY(psw::gavgpool_bwd(a.n, a.c, a.h, a.w, g, din, acc0, sb), "gavgpool_bwd");
             break;
         case PSW_OP_DROPOUT:  // the mask of this step's forward pass, recomputed

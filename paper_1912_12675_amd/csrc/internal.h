@@ -266,6 +266,16 @@ hipError_t bn_bwd(int n, int c, int h, int w, const float* dz, const float* z, c
                   float* dgamma, float* dbeta, float* dres, int rc, int rh, int rw, int res_accumulate,
                   void* ws, size_t ws_bytes, hipStream_t st);
 
+// Backward of a BN whose output is read only by a global average pool, with
+// that pool's backward: dh [n][c] is the pooled output's gradient; writes the
+// BN output's gradient dz (dh / (h w) at every pixel), dy, dgamma, dbeta and,
+// for an identity residual, its gradient (res_accumulate: added).  One
+// workgroup per channel; hipErrorNotSupported (nothing launched) unless
+// h w % 4 == 0 and the tensors are 16-byte aligned.
+hipError_t bn_bwd_gavg(int n, int c, int h, int w, const float* dh, const float* z, const float* y,
+                       const float* gamma, const float* mean, const float* invstd, int relu, float* dz, float* dy,
+                       float* dgamma, float* dbeta, float* dres, int res_accumulate, hipStream_t st);
+
 // ---- pooling ----
 hipError_t maxpool_fwd(int n, int c, int h, int w, int k, int stride, const float* x, float* y,
                        int32_t* argmax, hipStream_t st);

@@ -294,6 +294,77 @@ __global__ void gavg_bwd_k(int64_t total, int hw, const float* dy, float* dx, in
     dx[i] = accumulate ? dx[i] + g : g;
 }
 
+// Backward of a BN whose output feeds only a global average pool (the last
+// BN of a CIFAR ResNet): the pool's gradient dh[n][c] / hw is the BN output's
+// gradient at every pixel of (n, c), so one workgroup per channel forms the
+// channel's sums  sum g', sum g' xhat  (g' = that gradient where the ReLU
+// passed, z > 0; double, each thread's elements in order, then the block in
+// a fixed order), and a second pass over the channel (now in L2) writes
+// dy = gamma invstd (g' - sum g' / M - xhat sum g' xhat / M), the pool's
+// gradient dz (so every tensor's gradient stays readable) and the identity
+// residual's gradient g' (added when res_accumulate).  One launch replaces
+// the pool backward, the sums, their finalisation and the apply.
+__global__ __launch_bounds__(kBlock) void bn_bwd_gavg_k(int n, int c, int hw, const float* dh, const float* z,
+                                                         const float* y, const float* gamma, const float* mean,
+                                                         const float* invstd, int relu, float* dz, float* dy,
+                                                         float* dgamma, float* dbeta, float* dres, int res_accumulate)
+{
+    __shared__ double sh[2 * kBlock / 64];
+    __shared__ float coef[3];
+    const int ch = blockIdx.x;
+    const int hw4 = hw >> 2, units = n * hw4;
+    const float mu = mean[ch], is = invstd[ch];
+    const double mud = (double)mu, isd = (double)is;
+    double s1 = 0.0, s2 = 0.0;
+#pragma unroll 4
+    for (int u = threadIdx.x; u < units; u += kBlock) {
+        const int img = u / hw4, off = (u - img * hw4) * 4;
+        const size_t i = ((size_t)img * c + ch) * hw + off;
+        const float g = dh[(size_t)img * c + ch] / (float)hw;
+        const float4 yv = *reinterpret_cast<const float4*>(y + i);
+        const float4 zv = *reinterpret_cast<const float4*>(z + i);
+        const float yy[4] = {yv.x, yv.y, yv.z, yv.w}, zz[4] = {zv.x, zv.y, zv.z, zv.w};
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            const double gg = (relu && !(zz[e] > 0.f)) ? 0.0 : (double)g;
+            s1 += gg;
+            s2 += gg * ((double)yy[e] - mud) * isd;
+        }
+    }
+    block_sum2(s1, s2, sh);
+    if (threadIdx.x == 0) {
+        const double cnt = (double)n * hw;
+        coef[0] = (float)((double)gamma[ch] * isd);
+        coef[1] = (float)(s1 / cnt);
+        coef[2] = (float)(s2 / cnt);
+        dbeta[ch] = (float)s1;
+        dgamma[ch] = (float)s2;
+    }
+    __syncthreads();
+    const float a = coef[0], b = coef[1], d = coef[2];
+#pragma unroll 4
+    for (int u = threadIdx.x; u < units; u += kBlock) {
+        const int img = u / hw4, off = (u - img * hw4) * 4;
+        const size_t i = ((size_t)img * c + ch) * hw + off;
+        const float g = dh[(size_t)img * c + ch] / (float)hw;
+        const float4 yv = *reinterpret_cast<const float4*>(y + i);
+        const float4 zv = *reinterpret_cast<const float4*>(z + i);
+        float4 ov = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (dres && res_accumulate) ov = *reinterpret_cast<const float4*>(dres + i);
+        const float yy[4] = {yv.x, yv.y, yv.z, yv.w}, zz[4] = {zv.x, zv.y, zv.z, zv.w};
+        float o[4], gm[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            gm[e] = (relu && !(zz[e] > 0.f)) ? 0.f : g;
+            const float xh = (yy[e] - mu) * is;
+            o[e] = a * (gm[e] - b - xh * d);
+        }
+        store_stream4(dz + i, make_float4(g, g, g, g));
+        store_stream4(dy + i, make_float4(o[0], o[1], o[2], o[3]));
+        if (dres) store_stream4(dres + i, make_float4(ov.x + gm[0], ov.y + gm[1], ov.z + gm[2], ov.w + gm[3]));
+    }
+}
+
 // -------------------------------------------------------------- misc -------
 __global__ void relu_mask_k(int64_t count, const float* z, float* g)
 {
@@ -1168,6 +1239,22 @@ hipError_t bn_bwd_from_partials(int n, int c, int h, int w, const float* dz, con
     else
         PSW_BN_BWD(1);
 #undef PSW_BN_BWD
+    return hipGetLastError();
+}
+
+hipError_t bn_bwd_gavg(int n, int c, int h, int w, const float* dh, const float* z, const float* y,
+                       const float* gamma, const float* mean, const float* invstd, int relu, float* dz, float* dy,
+                       float* dgamma, float* dbeta, float* dres, int res_accumulate, hipStream_t st)
+{
+    const int hw = h * w;
+    if (hw % 4 || !aligned16(z) || !aligned16(y) || !aligned16(dz) || !aligned16(dy) || (dres && !aligned16(dres)))
+        return hipErrorNotSupported;
+    if ((int64_t)n * hw > INT32_MAX) return hipErrorNotSupported;
+    const double total = (double)n * c * hw;
+    // y and z read (their second pass hits L2), dz, dy (and the residual's gradient) written
+    const Work wk{8.0 * total, kF * ((4.0 + (dres ? 1.0 + res_accumulate : 0.0)) * total + (double)n * c)};
+    PSW_LAUNCH(kname("bn_bwd_gavg_k"), wk, bn_bwd_gavg_k, dim3(c), dim3(kBlock), 0, st, n, c, hw, dh, z, y, gamma, mean,
+               invstd, relu, dz, dy, dgamma, dbeta, dres, res_accumulate);
     return hipGetLastError();
 }
 

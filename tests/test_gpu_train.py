@@ -532,7 +532,10 @@ def test_bn_backward_folds_run(P):
     """ResNet-20 folds 13 of its 19 BN backward passes into the backward-data
     convs around them (7 without residual, 6 with an identity residual): a
     profiled step launches those folded kernels and 6 BN backward kernels of
-    their own, and its weight gradients as 6 grouped launches."""
+    their own -- 5 that merge the sums of the dgrad after them, and one for
+    the last BN whose output only the global average pool reads, which also
+    does the pool's backward (no pool-backward, channel-sum, finalise or
+    apply launches) -- and its weight gradients as 6 grouped launches."""
     wl = synth.resnet20_workload(batch=8)
     net = P.Net(wl.ops, 8, wl.in_shape, wl.stage_end, [4, 3, 2, 1])
     net.load_params(synth.init_params(wl))
@@ -545,5 +548,7 @@ def test_bn_backward_folds_run(P):
     count = lambda pred: sum(k["launches"] for k in ks if pred(k["name"]))
     assert count(lambda n: n.startswith("conv3x3_direct") and n.endswith("true, 1, 1, false>")) == 7
     assert count(lambda n: n.startswith("conv3x3_direct") and n.endswith("true, 1, 2, false>")) == 6
-    assert count(lambda n: n.startswith(("bn_bwd_partials_k", "bn_bwd_apply"))) == 6
+    assert count(lambda n: n.startswith("bn_bwd_partials_k")) == 5
+    assert count(lambda n: n.startswith("bn_bwd_gavg_k")) == 1
+    assert count(lambda n: n.startswith(("gavg_bwd_k", "chan_partials", "bn_bwd_finalize", "bn_bwd_apply"))) == 0
     assert count(lambda n: n.startswith("conv3x3_wgrad")) == 6
