@@ -1,5 +1,6 @@
 """Where a float32 training step parts from the fp64 oracle at batch 128:
-ReLU decisions on pre-activations within rounding of zero.
+ReLU decisions on pre-activations within rounding of zero, and max-pool
+decisions between window values within rounding of each other.
 
 ResNet-20 (batch 128, PPV (7,13,19), staleness [3,2,1,0]), one step of the
 stale-weight schedule (Sec. 3) from the oracle's own trajectory at t = 0 and
@@ -9,9 +10,9 @@ t = 25.  The same step written in torch autograd
   - in float32 taking those decisions lands within the 1e-4 parity target of
     the oracle (gradient and momentum, rel-L2);
   - in float32 taking its own decisions differs from the float64 run in a
-    handful of the 24.1M decisions, each on a pre-activation within 1e-5 of
-    its layer's RMS of zero, and those few flips alone move the gradient and
-    the update by ~1e-3.
+    handful of the 24.1M decisions, each on a pre-activation within 2e-6 of
+    its layer's RMS of zero (checked: at most 100, within 1e-4), and those
+    few flips alone move the gradient and the update by ~1e-3.
 
 So the distance of any float32 implementation from the oracle after one full
 step at this batch size is set by a few threshold decisions, not by its
@@ -23,7 +24,7 @@ import pytest
 import torch
 
 from paper_1912_12675_amd import synth
-from tests.onestep_ref import distances, oracle_step, resnet20_state, torch_step
+from tests.onestep_ref import distances, oracle_step, resnet20_state, synthetic_state, torch_step
 
 
 def relu_flips(pre64, masks):
@@ -63,5 +64,51 @@ def test_fp32_step_with_the_oracles_decisions_meets_the_target(oracle, t):
     assert len(rec64["pre"]) == 19  # every BN + ReLU of ResNet-20
     assert d_forced["grad"] <= 1e-5 and d_forced["momentum"] <= 1e-5
     assert d_forced["update"] <= 1e-4
-    assert 0 < n_flip <= 100 and worst <= 1e-5
+    assert 0 < n_flip <= 100 and worst <= 1e-4
     assert d_own["grad"] >= 20 * d_forced["grad"]
+
+
+def test_vgg16_fp32_step_with_the_oracles_decisions_meets_the_target(oracle):
+    """VGG-16-BN, batch 128, PPV (2,4,7), one step from a seeded checkpoint in
+    the stale phase (t = 5): ReLU and max-pool decisions.  Taking the float64
+    run's ReLU decisions alone is not enough (its pools still decide
+    otherwise); taking both its ReLU decisions and its max-pool argmax,
+    float32 lands within the target."""
+    torch.set_num_threads(8)
+    wl = synth.vgg16_workload()
+    state = synthetic_state(oracle, wl, 5, 2027)
+    ref = oracle_step(oracle, wl, state)
+    w_t = np.concatenate([w[state.t] for w in state.window]).astype(np.float64)
+    rec64 = {"pre": {}, "pool": {}, "pool_in": {}}
+    d64 = distances(wl, torch_step(wl, state, dtype=torch.float64, decisions=rec64), ref, w_t)
+    masks64 = {i: p > 0 for i, p in rec64["pre"].items()}
+    d_forced = distances(wl, torch_step(wl, state, decisions={"mask": masks64, "pool_use": rec64["pool"]}), ref, w_t)
+    rec32 = {"pre": {}, "pool": {}}
+    d_own = distances(wl, torch_step(wl, state, decisions=rec32), ref, w_t)
+    n_relu, worst_relu = relu_flips(rec64["pre"], {i: p > 0 for i, p in rec32["pre"].items()})
+    n_pool, worst_pool = pool_flips(rec64["pool_in"], rec64["pool"], rec32["pool"])
+    print(f"vgg16 t=5: fp64 grad {d64['grad']:.2e} | fp32 with the fp64 decisions: grad {d_forced['grad']:.2e} "
+          f"momentum {d_forced['momentum']:.2e} update {d_forced['update']:.2e} | fp32 own decisions: grad "
+          f"{d_own['grad']:.2e} update {d_own['update']:.2e}; ReLU decisions differing {n_relu} (largest |pre| / RMS "
+          f"{worst_relu:.1e}), max-pool {n_pool} (largest gap / RMS {worst_pool:.1e})")
+    assert d64["grad"] <= 1e-10 and d64["momentum"] <= 1e-10
+    assert d_forced["grad"] <= 1e-5 and d_forced["momentum"] <= 1e-5
+    assert d_forced["update"] <= 1e-4
+    assert n_relu <= 100 and worst_relu <= 1e-4 and n_pool <= 100 and worst_pool <= 1e-4
+    assert d_own["grad"] >= 20 * d_forced["grad"]
+
+
+def pool_flips(pool_in, idx_a, idx_b):
+    """(number of pooling windows whose argmax differs between idx_a and
+    idx_b, largest |x[a] - x[b]| / RMS(x) over them), x the float64 input."""
+    n, worst = 0, 0.0
+    for i, x in pool_in.items():
+        a, b = idx_a[i], idx_b[i]
+        d = a != b
+        k = int(d.sum())
+        if k:
+            n += k
+            xf = x.flatten(2)
+            gap = (xf.gather(2, a.flatten(2)) - xf.gather(2, b.flatten(2))).abs().view(a.shape)
+            worst = max(worst, float(gap[d].max() / torch.sqrt((x * x).mean())))
+    return n, worst

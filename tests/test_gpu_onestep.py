@@ -72,8 +72,11 @@ def gpu_step(P, wl, state, ring_depth):
     relu_ops = [i for i, o in enumerate(wl.ops) if int(o[0]) in (synth.CONV, synth.BN, synth.FC) and
                 int(o[8]) & synth.F_RELU]
     masks = {i: (net.tensor(i + 1) > 0).cpu() for i in relu_ops}
+    # and its max-pool inputs and outputs, from which its argmax follows
+    pools = {i: (net.tensor(int(o[1])).cpu(), net.tensor(i + 1).cpu(), int(o[5]))
+             for i, o in enumerate(wl.ops) if int(o[0]) == synth.MAXPOOL}
     return dict(versions=ver, grad=net.grad.double().cpu().numpy(), momentum=net.momentum.double().cpu().numpy(),
-                params=net.params(t + 1).double().numpy(), loss=float(net.loss.item()), masks=masks)
+                params=net.params(t + 1).double().numpy(), loss=float(net.loss.item()), masks=masks, pools=pools)
 
 
 SPREAD_SAMPLES = 8
@@ -122,15 +125,36 @@ def check_step(P, oracle, wl, state, ring_depth, label):
     return got
 
 
+def pool_argmax(x, y, k):
+    """Argmax of a k x k / k max-pool from its input x [N,C,H,W] and output y:
+    the flat plane index of the first window element equal to the output (the
+    pool copies its maximum, so equality is exact)."""
+    N, C, H, W = x.shape
+    xw = x.view(N, C, H // k, k, W // k, k).permute(0, 1, 2, 4, 3, 5).reshape(N, C, H // k, W // k, k * k)
+    eq = xw == y.view(N, C, H // k, W // k).unsqueeze(-1)
+    assert bool(eq.any(-1).all()), "every pooled value comes from its window"
+    first = eq.to(torch.int8).argmax(-1)  # the first maximum of a 0/1 row is its first match
+    hh = torch.arange(H // k).view(1, 1, -1, 1) * k + first // k
+    ww = torch.arange(W // k).view(1, 1, 1, -1) * k + first % k
+    return hh * W + ww
+
+
 def check_decisions(wl, state, got, label):
-    """The GPU's ReLU decisions against those of the float64 computation of
-    the step (torch autograd, equal to the oracle at 1e-10): only a handful
-    may differ, each on a pre-activation within 1e-5 of its layer's RMS of
-    zero (float32 rounding); in float32 such ties are where every
-    implementation parts from the oracle (tests/test_decisions.py)."""
-    rec = {"pre": {}}
+    """The GPU's ReLU and max-pool decisions against those of the float64
+    computation of the step (torch autograd, equal to the oracle at 1e-10):
+    only a handful may differ (at most 100), each a ReLU on a pre-activation
+    within 1e-4 of its layer's RMS of zero, or a pool window whose two
+    candidates lie within 1e-4 of the RMS of each other: the rounding of
+    float32 sums of up to 4608 products (VGG-16's 512-channel layers: up to
+    1.0e-5 measured, ResNet-20 2.5e-6), while 1e-4 of the RMS still marks a
+    value as a near-tie (of VGG-16's 35.4M pre-activations 2,896 lie
+    that close to zero, and 16 flip); such ties are
+    where every float32 implementation parts from the oracle
+    (tests/test_decisions.py)."""
+    rec = {"pre": {}, "pool": {}, "pool_in": {}}
     torch_step(wl, state, dtype=torch.float64, decisions=rec)
     assert sorted(rec["pre"]) == sorted(got["masks"]), "ReLU sites"
+    assert sorted(rec["pool"]) == sorted(got["pools"]), "max-pool sites"
     n, worst, total = 0, 0.0, 0
     for i, pre in rec["pre"].items():
         g = got["masks"][i].reshape(pre.shape)
@@ -140,9 +164,24 @@ def check_decisions(wl, state, got, label):
         if k:
             n += k
             worst = max(worst, float(pre[diff].abs().max() / torch.sqrt((pre * pre).mean())))
+    npool, worst_pool, total_pool = 0, 0.0, 0
+    for i, idx64 in rec["pool"].items():
+        x64 = rec["pool_in"][i]
+        xg, yg, k = got["pools"][i]
+        idx = pool_argmax(xg.view(x64.shape), yg, k)
+        diff = idx != idx64
+        total_pool += idx64.numel()
+        m = int(diff.sum())
+        if m:
+            npool += m
+            xf = x64.flatten(2)
+            gap = (xf.gather(2, idx64.flatten(2)) - xf.gather(2, idx.flatten(2))).abs().view(idx64.shape)
+            worst_pool = max(worst_pool, float(gap[diff].max() / torch.sqrt((x64 * x64).mean())))
     print(f"{label} t={state.t}: {n} of {total} ReLU decisions differ from the float64 step's, largest "
-          f"|pre-activation| / RMS {worst:.1e}", flush=True)
-    assert n <= 100 and worst <= 1e-5
+          f"|pre-activation| / RMS {worst:.1e}; {npool} of {total_pool} max-pool windows, largest gap / RMS "
+          f"{worst_pool:.1e}", flush=True)
+    assert n <= 100 and worst <= 1e-4
+    assert npool <= 100 and worst_pool <= 1e-4
 
 
 @pytest.mark.parametrize("t", [0, 1, 25, 49])
@@ -170,7 +209,10 @@ def test_full_size_one_step(P, oracle, name, factory, t):
     VGG-16-BN (b128) and ResNet-110 (b256, bf16 products, 8 stages with
     d_s = 7 - s) from a seeded checkpoint in the stale phase."""
     wl = factory()
-    check_step(P, oracle, wl, synthetic_state(oracle, wl, t, 2027), wl.ring_depth(t + 1), name)
+    state = synthetic_state(oracle, wl, t, 2027)
+    got = check_step(P, oracle, wl, state, wl.ring_depth(t + 1), name)
+    if not wl.bf16:
+        check_decisions(wl, state, got, name)
 
 
 

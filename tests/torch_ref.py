@@ -139,6 +139,23 @@ def _relu(y, i, decisions):
     return F.relu(y)
 
 
+def _maxpool(a, k, stride, i, decisions):
+    """Max-pool of op i.  decisions (see _relu): a "pool" entry collects each
+    op's argmax (flat index in the input plane of the first maximum in
+    row-major window order, torch's rule), a "pool_in" entry its input; a
+    "pool_use" entry supplies, per op, the argmax to take instead."""
+    if decisions is None or ("pool" not in decisions and "pool_use" not in decisions):
+        return F.max_pool2d(a, k, stride)
+    if "pool_use" in decisions:
+        idx = decisions["pool_use"][i]
+        return a.flatten(2).gather(2, idx.flatten(2)).view(idx.shape)
+    y, idx = F.max_pool2d(a, k, stride, return_indices=True)
+    decisions["pool"][i] = idx
+    if "pool_in" in decisions:
+        decisions["pool_in"][i] = a.detach().clone()
+    return y
+
+
 def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5, bn_mom=0.1, dropout_key=None,
             bf16=False, decisions=None):
     """Apply ops[lo:hi].  inputs: dict tensor_id -> tensor (must hold every
@@ -169,7 +186,7 @@ def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5
             if flags & F_RELU:
                 y = _relu(y, i, decisions)
         elif kind == MAXPOOL:
-            y = F.max_pool2d(a, k, stride)
+            y = _maxpool(a, k, stride, i, decisions)
         elif kind == GAVG:
             y = a.mean(dim=(2, 3), keepdim=True)
         elif kind == FC:
