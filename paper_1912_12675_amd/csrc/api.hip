@@ -710,7 +710,7 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
         const int b = pg.in0 - 1;  // the op producing the pool's input
         const psw_layer& o = net->ops[b];
         if (o.kind != PSW_OP_BN || consumers[pg.in0] != 1 || net->grad_accum[2 * j] || net->fold_bn[b]) continue;
-        if (o.in1 == 0) continue;
+        if (o.in1 == 0 || (o.in1 > 0 && net->grad_accum[2 * b + 1])) continue;  // it writes the residual's gradient first
         if (o.in1 > 0) {  // identity residual only
             const Tensor r = net->t[o.in1], yb = net->t[o.in0];
             if (r.c != yb.c || r.h != yb.h || r.w != yb.w) continue;
@@ -1259,8 +1259,7 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
             if (net->gavg_of[i] >= 0) {  // with the global average pool's backward: dh = the pool output's gradient
                 PSW_TRY(psw::bn_bwd_gavg(a.n, a.c, a.h, a.w, is.grd(net->gavg_of[i] + 1), is.act(i + 1),
                                          is.act(o.in0), is.wbwd(i), save, save + o.cin,
-                                         (o.flags & PSW_F_RELU) != 0, g, din, dg, dg + o.cin, dres,
-                                         net->grad_accum[2 * i + 1], sb),
+                                         (o.flags & PSW_F_RELU) != 0, g, din, dg, dg + o.cin, dres, sb),
                         "bn_bwd_gavg");
                 done = true;
             }

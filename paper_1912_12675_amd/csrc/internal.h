@@ -269,12 +269,12 @@ hipError_t bn_bwd(int n, int c, int h, int w, const float* dz, const float* z, c
 // Backward of a BN whose output is read only by a global average pool, with
 // that pool's backward: dh [n][c] is the pooled output's gradient; writes the
 // BN output's gradient dz (dh / (h w) at every pixel), dy, dgamma, dbeta and,
-// for an identity residual, its gradient (res_accumulate: added).  One
-// workgroup per channel; hipErrorNotSupported (nothing launched) unless
-// h w % 4 == 0 and the tensors are 16-byte aligned.
+// for an identity residual, its gradient (overwritten: the BN must be its
+// first writer).  One workgroup per channel; hipErrorNotSupported (nothing
+// launched) unless h w % 4 == 0 and the tensors are 16-byte aligned.
 hipError_t bn_bwd_gavg(int n, int c, int h, int w, const float* dh, const float* z, const float* y,
                        const float* gamma, const float* mean, const float* invstd, int relu, float* dz, float* dy,
-                       float* dgamma, float* dbeta, float* dres, int res_accumulate, hipStream_t st);
+                       float* dgamma, float* dbeta, float* dres, hipStream_t st);
 
 // ---- pooling ----
 hipError_t maxpool_fwd(int n, int c, int h, int w, int k, int stride, const float* x, float* y,

@@ -302,12 +302,12 @@ __global__ void gavg_bwd_k(int64_t total, int hw, const float* dy, float* dx, in
 // a fixed order), and a second pass over the channel (now in L2) writes
 // dy = gamma invstd (g' - sum g' / M - xhat sum g' xhat / M), the pool's
 // gradient dz (so every tensor's gradient stays readable) and the identity
-// residual's gradient g' (added when res_accumulate).  One launch replaces
+// residual's gradient g' (its first writer).  One launch replaces
 // the pool backward, the sums, their finalisation and the apply.
 __global__ __launch_bounds__(kBlock) void bn_bwd_gavg_k(int n, int c, int hw, const float* dh, const float* z,
                                                          const float* y, const float* gamma, const float* mean,
                                                          const float* invstd, int relu, float* dz, float* dy,
-                                                         float* dgamma, float* dbeta, float* dres, int res_accumulate)
+                                                         float* dgamma, float* dbeta, float* dres)
 {
     __shared__ double sh[2 * kBlock / 64];
     __shared__ float coef[3];
@@ -349,8 +349,6 @@ __global__ __launch_bounds__(kBlock) void bn_bwd_gavg_k(int n, int c, int hw, co
         const float g = dh[(size_t)img * c + ch] / (float)hw;
         const float4 yv = *reinterpret_cast<const float4*>(y + i);
         const float4 zv = *reinterpret_cast<const float4*>(z + i);
-        float4 ov = make_float4(0.f, 0.f, 0.f, 0.f);
-        if (dres && res_accumulate) ov = *reinterpret_cast<const float4*>(dres + i);
         const float yy[4] = {yv.x, yv.y, yv.z, yv.w}, zz[4] = {zv.x, zv.y, zv.z, zv.w};
         float o[4], gm[4];
 #pragma unroll
@@ -361,7 +359,7 @@ __global__ __launch_bounds__(kBlock) void bn_bwd_gavg_k(int n, int c, int hw, co
         }
         store_stream4(dz + i, make_float4(g, g, g, g));
         store_stream4(dy + i, make_float4(o[0], o[1], o[2], o[3]));
-        if (dres) store_stream4(dres + i, make_float4(ov.x + gm[0], ov.y + gm[1], ov.z + gm[2], ov.w + gm[3]));
+        if (dres) store_stream4(dres + i, make_float4(gm[0], gm[1], gm[2], gm[3]));
     }
 }
 
@@ -1244,7 +1242,7 @@ hipError_t bn_bwd_from_partials(int n, int c, int h, int w, const float* dz, con
 
 hipError_t bn_bwd_gavg(int n, int c, int h, int w, const float* dh, const float* z, const float* y,
                        const float* gamma, const float* mean, const float* invstd, int relu, float* dz, float* dy,
-                       float* dgamma, float* dbeta, float* dres, int res_accumulate, hipStream_t st)
+                       float* dgamma, float* dbeta, float* dres, hipStream_t st)
 {
     const int hw = h * w;
     if (hw % 4 || !aligned16(z) || !aligned16(y) || !aligned16(dz) || !aligned16(dy) || (dres && !aligned16(dres)))
@@ -1252,9 +1250,9 @@ hipError_t bn_bwd_gavg(int n, int c, int h, int w, const float* dh, const float*
     if ((int64_t)n * hw > INT32_MAX) return hipErrorNotSupported;
     const double total = (double)n * c * hw;
     // y and z read (their second pass hits L2), dz, dy (and the residual's gradient) written
-    const Work wk{8.0 * total, kF * ((4.0 + (dres ? 1.0 + res_accumulate : 0.0)) * total + (double)n * c)};
+    const Work wk{8.0 * total, kF * ((4.0 + (dres ? 1.0 : 0.0)) * total + (double)n * c)};
     PSW_LAUNCH(kname("bn_bwd_gavg_k"), wk, bn_bwd_gavg_k, dim3(c), dim3(kBlock), 0, st, n, c, hw, dh, z, y, gamma, mean,
-               invstd, relu, dz, dy, dgamma, dbeta, dres, res_accumulate);
+               invstd, relu, dz, dy, dgamma, dbeta, dres);
     return hipGetLastError();
 }
 
