@@ -137,9 +137,9 @@ STASH_CASES = [
 @pytest.mark.parametrize("name,factory,batch,T,stash", [c + (False,) for c in CASES] + [c + (True,) for c in STASH_CASES],
                          ids=[c[0] for c in CASES] + [c[0] for c in STASH_CASES])
 def test_train_parity(P, oracle, name, factory, batch, T, stash):
-    """Bar: max(spec bar, 4 x reference spread) for the whole parameter
+    """Bar: max(target, 4 x reference spread) for the whole parameter
     vector, for every tensor with a non-zero initial value, and for the
-    losses; the spec bar is 1e-4 (fp32) / 2e-2 (bf16).  The spread
+    losses; the target is 1e-4 (fp32) / 2e-2 (bf16).  The spread
     (the largest deviation among the reference_spread samples: torch float32,
     with bf16-rounded product operands in bf16 mode) measures how
     much this particular run amplifies
