@@ -352,6 +352,11 @@ struct psw_net {
     // pool op (else -1); the two backward passes run as one kernel
     std::vector<int> gavg_of;
     std::vector<char> gavg_fused;           // per pool op: its backward runs in its BN's kernel
+    // per BN op whose 8x8 output only a global average pool reads: that pool
+    // op (else -1); the BN apply writes the pooled means too, and the pool
+    // op launches nothing when it did (pool_done_now, per step)
+    std::vector<int> gavg_fwd_of;
+    std::vector<char> pool_done_now;
 
     std::vector<char> grad_accum;           // per op input slot: 0 overwrite, 1 accumulate (in0, in1)
     size_t step_bytes = 0;                  // one step set (activations, saves, gradients, forward ws)
@@ -704,6 +709,14 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
     // channel does the pool backward and the BN backward (bn_bwd_gavg)
     net->gavg_of.assign(n_layers, -1);
     net->gavg_fused.assign(n_layers, 0);
+    net->gavg_fwd_of.assign(n_layers, -1);
+    net->pool_done_now.assign(n_layers, 0);
+    for (int j = 0; j < n_layers; ++j) {
+        const psw_layer& pg = net->ops[j];
+        if (pg.kind != PSW_OP_GAVG || pg.in0 < 2 || consumers[pg.in0] != 1) continue;
+        const Tensor zt = net->t[pg.in0];
+        if (net->ops[pg.in0 - 1].kind == PSW_OP_BN && zt.h * zt.w == 64) net->gavg_fwd_of[pg.in0 - 1] = j;
+    }
     for (int j = 0; j < n_layers; ++j) {
         const psw_layer& pg = net->ops[j];
         if (pg.kind != PSW_OP_GAVG || pg.in0 < 2) continue;
@@ -1082,6 +1095,7 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
         case PSW_OP_BN: {
             const Tensor r = o.in1 >= 0 ? net->t[o.in1] : Tensor{0, 0, 0, 0};
             float* save = is.save(i);
+            if (net->gavg_fwd_of[i] >= 0) net->pool_done_now[net->gavg_fwd_of[i]] = 0;
             float* rm = net->run_mean ? net->run_mean + net->bn_off[i] : nullptr;
             float* rvv = net->run_var ? net->run_var + net->bn_off[i] : nullptr;
             kind = PSW_PROF_BN_FWD;
@@ -1092,11 +1106,16 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
                 check_conv(ci.n, ci.c, ci.h, ci.w, cv.cout, cv.k, cv.k, cv.stride, cv.pad, net->prec, &ccs);
                 const int T = psw::conv_fwd_bnstats_tiles(ccs);
                 const int P = a.n * a.h * a.w / T;
+                const int pj = net->gavg_fwd_of[i];  // the global pool reading this output alone, if any
                 e = psw::bn_apply_from_partials(a.n, a.c, a.h, a.w, is.act(o.in0), (const float*)ws, T, P, W,
                                                 W + o.cin, o.in1 >= 0 ? is.act(o.in1) : nullptr, r.c, r.h, r.w,
                                                 (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, is.act(i + 1), save,
-                                                save + o.cin, save + 2 * o.cin, rm, rvv, sf);
-                if (e == hipSuccess) break;
+                                                save + o.cin, save + 2 * o.cin, rm, rvv, sf,
+                                                pj >= 0 ? is.act(pj + 1) : nullptr);
+                if (e == hipSuccess) {
+                    if (pj >= 0) net->pool_done_now[pj] = 1;
+                    break;
+                }
                 if (e != hipErrorNotSupported) PSW_TRY(e, "bn_apply");
                 // not supported: nothing launched, the statistics are recomputed below
             }
@@ -1114,6 +1133,7 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
             break;
         case PSW_OP_GAVG:
             kind = PSW_PROF_POOL;
+            if (net->pool_done_now[i]) break;  // written by its BN's apply kernel
             PSW_TRY(psw::gavgpool_fwd(a.n, a.c, a.h, a.w, is.act(o.in0), is.act(i + 1), sf), "gavgpool_fwd");
             break;
         case PSW_OP_DROPOUT:

@@ -186,10 +186,14 @@ int conv_fwd_bnstats_tiles(const ConvShape& cs);  // tiles T (partials per chann
 // partials over P pixels each: every block merges its channel's T partials
 // in a fixed order (double precision), block 0 of a channel stores the saved
 // statistics and running statistics, and every block normalises its part.
+// pool: when set (an 8x8 output that only a global average pool reads), the
+// per-(image, channel) means of the output are written there as well;
+// hipErrorNotSupported (nothing launched) unless h * w == 64.
 hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, const float* part, int T, int P,
                                   const float* gamma, const float* beta, const float* res, int rc, int rh, int rw,
                                   int relu, float eps, float momentum, float* z, float* save_mean, float* save_invstd,
-                                  float* save_scale, float* run_mean, float* run_var, hipStream_t st);
+                                  float* save_scale, float* run_mean, float* run_var, hipStream_t st,
+                                  float* pool = nullptr);
 // Direct 3x3 / pad 1 kernel (forward, or backward-data of a stride-1 layer
 // when transpose is set); hipErrorNotSupported when no tile config fits.
 // bf16: both operands rounded to bfloat16 (nearest even), fp32 accumulation.

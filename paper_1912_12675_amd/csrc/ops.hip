@@ -953,7 +953,7 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
                                                                const float* res, int rc, int rh, int rw, int h, int w,
                                                                int relu, float eps, float momentum, float* z,
                                                                float* save_mean, float* save_invstd, float* save_scale,
-                                                               float* run_mean, float* run_var)
+                                                               float* run_mean, float* run_var, float* pool)
 {
     __shared__ double sh[2 * kBlock / 64];
     __shared__ float coef[2];
@@ -1034,7 +1034,7 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
     const float sc = coef[0], sf = coef[1];
 #pragma unroll
     for (int q = 0; q < U; ++q) {
-        if (u0 + (int)threadIdx.x + q * kBlock >= u1) continue;
+        const bool live = u0 + (int)threadIdx.x + q * kBlock < u1;
         float v[4] = {__fmaf_rn(yv[q].x, sc, sf), __fmaf_rn(yv[q].y, sc, sf), __fmaf_rn(yv[q].z, sc, sf),
                       __fmaf_rn(yv[q].w, sc, sf)};
         if (res) {
@@ -1044,7 +1044,17 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
 #pragma unroll
             for (int e = 0; e < 4; ++e) v[e] = fmaxf(v[e], 0.f);
         }
-        store_stream4(z + idx[q], make_float4(v[0], v[1], v[2], v[3]));
+        if (live) store_stream4(z + idx[q], make_float4(v[0], v[1], v[2], v[3]));
+        if (pool) {  // a global average pool reads this BN's output alone: the 16 units of
+                     // an 8x8 plane are 16 consecutive lanes (rows of 16 live or dead together)
+            float ps = (v[0] + v[1]) + (v[2] + v[3]);
+#pragma unroll
+            for (int off = 8; off > 0; off >>= 1) ps += __shfl_xor(ps, off, 16);
+            if (live && (threadIdx.x & 15) == 0) {
+                const int u = u0 + (int)threadIdx.x + q * kBlock;
+                pool[(size_t)(u / hw4) * c + ch] = ps / (float)hw;
+            }
+        }
     }
 }
 
@@ -1177,8 +1187,9 @@ int apply_units_per_thread(int64_t units_total)
 hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, const float* part, int T, int P,
                                   const float* gamma, const float* beta, const float* res, int rc, int rh, int rw,
                                   int relu, float eps, float momentum, float* z, float* save_mean, float* save_invstd,
-                                  float* save_scale, float* run_mean, float* run_var, hipStream_t st)
+                                  float* save_scale, float* run_mean, float* run_var, hipStream_t st, float* pool)
 {
+    if (pool && h * w != 64) return hipErrorNotSupported;
     const bool identity = res && rc == c && rh == h && rw == w;
     if (w % 4 || !aligned16(y) || !aligned16(z) || (identity && !aligned16(res)) || (uintptr_t)part % 8)
         return hipErrorNotSupported;
@@ -1188,11 +1199,12 @@ hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, co
     const unsigned per_ch = (unsigned)((units + U * kBlock - 1) / (U * kBlock));
     const double total = (double)n * c * h * w;
     const double rbytes = res ? kF * (double)n * std::min(c, rc) * h * w : 0.0;
-    const Work wk{3.0 * total, 2 * kF * total + rbytes + 2 * kF * T * c};
+    Work wk{3.0 * total, 2 * kF * total + rbytes + 2 * kF * T * c};
+    if (pool) wk.bytes += kF * (double)n * c;  // the pooled means written
 #define PSW_BN_APPLY(UU)                                                                                          \
     PSW_LAUNCH(kname("bn_apply_partials_k", UU), wk, bn_apply_partials_k<UU>, dim3(c, per_ch), dim3(kBlock), 0, st, n, c, \
                h * w, y, part, T, P, gamma, beta, res, rc, rh, rw, h, w, relu, eps, momentum, z, save_mean,          \
-               save_invstd, save_scale, run_mean, run_var)
+               save_invstd, save_scale, run_mean, run_var, pool)
     if (U == 4)
         PSW_BN_APPLY(4);
     else if (U == 2)

@@ -535,7 +535,9 @@ def test_bn_backward_folds_run(P):
     their own -- 5 that merge the sums of the dgrad after them, and one for
     the last BN whose output only the global average pool reads, which also
     does the pool's backward (no pool-backward, channel-sum, finalise or
-    apply launches) -- and its weight gradients as 6 grouped launches."""
+    apply launches; in the forward pass its BN apply writes the pooled means,
+    so no pool launch either) -- and its weight gradients as 6 grouped
+    launches."""
     wl = synth.resnet20_workload(batch=8)
     net = P.Net(wl.ops, 8, wl.in_shape, wl.stage_end, [4, 3, 2, 1])
     net.load_params(synth.init_params(wl))
@@ -551,4 +553,6 @@ def test_bn_backward_folds_run(P):
     assert count(lambda n: n.startswith("bn_bwd_partials_k")) == 5
     assert count(lambda n: n.startswith("bn_bwd_gavg_k")) == 1
     assert count(lambda n: n.startswith(("gavg_bwd_k", "chan_partials", "bn_bwd_finalize", "bn_bwd_apply"))) == 0
+    # forward: that BN's apply kernel also writes the pooled means
+    assert count(lambda n: n.startswith("gavg_fwd_k")) == 0
     assert count(lambda n: n.startswith("conv3x3_wgrad")) == 6
