@@ -112,3 +112,38 @@ def pool_flips(pool_in, idx_a, idx_b):
             gap = (xf.gather(2, a.flatten(2)) - xf.gather(2, b.flatten(2))).abs().view(a.shape)
             worst = max(worst, float(gap[d].max() / torch.sqrt((x * x).mean())))
     return n, worst
+
+
+@pytest.mark.parametrize("t", [0, 25])
+def test_bf16_step_with_the_oracles_roundings_meets_the_target(oracle, t):
+    """bf16 products (both operands of every conv / FC product rounded to
+    bfloat16, fp32 accumulation), ResNet-20 b128 from the oracle's bf16
+    trajectory: here each rounding is a decision too.  Once one operand
+    lands on the other side of a bfloat16 rounding midpoint, the next
+    layers' operands move by a bfloat16 ulp and about half of all 48M
+    rounded operand values of the step differ between a float32 and a
+    float64 computation, which puts float32 3e-2 to 7e-2 away from the
+    oracle.  Taking the float64 run's rounded activation operands (input,
+    output gradient; the weights round alike on both sides) and its ReLU
+    decisions, float32 lands within 1e-5 of it (gradient and momentum): the
+    bf16 mode's distance is the roundings', not the arithmetic's."""
+    torch.set_num_threads(8)
+    wl = synth.resnet20_workload(bf16=True)
+    state = resnet20_state(oracle, wl, t)
+    ref = oracle_step(oracle, wl, state)
+    w_t = np.concatenate([w[state.t] for w in state.window]).astype(np.float64)
+    rec64 = {"pre": {}, "bf16": {}}
+    d64 = distances(wl, torch_step(wl, state, dtype=torch.float64, decisions=rec64), ref, w_t)
+    masks64 = {i: p > 0 for i, p in rec64["pre"].items()}
+    d_forced = distances(wl, torch_step(wl, state, decisions={"mask": masks64, "bf16_use": rec64["bf16"]}), ref, w_t)
+    rec32 = {"pre": {}, "bf16": {}}
+    d_own = distances(wl, torch_step(wl, state, decisions=rec32), ref, w_t)
+    differ = sum(int((rec64["bf16"][k].float() != rec32["bf16"][k].float()).sum()) for k in rec64["bf16"])
+    total = sum(v.numel() for v in rec64["bf16"].values())
+    print(f"bf16 t={t}: fp64 grad {d64['grad']:.2e} | fp32 with the fp64 roundings and ReLU decisions: grad "
+          f"{d_forced['grad']:.2e} momentum {d_forced['momentum']:.2e} update {d_forced['update']:.2e} | fp32 own: "
+          f"grad {d_own['grad']:.2e} update {d_own['update']:.2e}; rounded operands differing {differ} of {total}")
+    assert d64["grad"] <= 1e-10 and d64["momentum"] <= 1e-10
+    assert len(rec64["bf16"]) == 2 * 20  # input and output gradient of 19 convs and the FC
+    assert d_forced["grad"] <= 1e-5 and d_forced["momentum"] <= 1e-5 and d_forced["update"] <= 1e-4
+    assert d_own["update"] >= 100 * d_forced["update"]

@@ -89,6 +89,19 @@ def _rb(t):
     return t.to(torch.bfloat16).to(t.dtype)
 
 
+def _rbd(t, key, decisions):
+    """_rb(t), or with decisions (see _relu): a "bf16" entry collects the
+    rounded activation operand under key (op, which), a "bf16_use" entry
+    supplies the rounded values to take instead (bfloat16 values are exact
+    in every wider float type)."""
+    if decisions is not None and "bf16_use" in decisions:
+        return decisions["bf16_use"][key].to(t.dtype)
+    r = _rb(t)
+    if decisions is not None and "bf16" in decisions:
+        decisions["bf16"][key] = r.detach().clone()
+    return r
+
+
 class _Bf16Conv(torch.autograd.Function):
     """conv2d whose product operands are rounded to bfloat16 in each pass:
     forward x, w; backward-data dy, w; backward-weight x, dy.  The weight is
@@ -96,32 +109,37 @@ class _Bf16Conv(torch.autograd.Function):
     then (the stale schedule swaps in the current version before it)."""
 
     @staticmethod
-    def forward(ctx, x, w, b, stride, pad):
-        ctx.x, ctx.w, ctx.has_b, ctx.stride, ctx.pad = x, w, b is not None, stride, pad
-        return F.conv2d(_rb(x), _rb(w), b, stride=stride, padding=pad)
+    def forward(ctx, x, w, b, stride, pad, op=-1, decisions=None):
+        ctx.w, ctx.has_b, ctx.stride, ctx.pad, ctx.op, ctx.dec = w, b is not None, stride, pad, op, decisions
+        ctx.xshape = x.shape
+        ctx.xr = _rbd(x, (op, "x"), decisions)
+        return F.conv2d(ctx.xr, _rb(w), b, stride=stride, padding=pad)
 
     @staticmethod
     def backward(ctx, dy):
-        x, w = ctx.x, ctx.w
-        dx = torch.nn.grad.conv2d_input(x.shape, _rb(w), _rb(dy), stride=ctx.stride, padding=ctx.pad)
-        dw = torch.nn.grad.conv2d_weight(_rb(x), w.shape, _rb(dy), stride=ctx.stride, padding=ctx.pad)
+        w = ctx.w
+        dyr = _rbd(dy, (ctx.op, "dy"), ctx.dec)
+        dx = torch.nn.grad.conv2d_input(ctx.xshape, _rb(w), dyr, stride=ctx.stride, padding=ctx.pad)
+        dw = torch.nn.grad.conv2d_weight(ctx.xr, w.shape, dyr, stride=ctx.stride, padding=ctx.pad)
         db = dy.sum(dim=(0, 2, 3)) if ctx.has_b else None
-        return dx, dw, db, None, None
+        return dx, dw, db, None, None, None, None
 
 
 class _Bf16Linear(torch.autograd.Function):
     """linear with bfloat16-rounded product operands in each pass (as _Bf16Conv)."""
 
     @staticmethod
-    def forward(ctx, x, w, b):
-        ctx.x, ctx.w, ctx.has_b = x, w, b is not None
-        return F.linear(_rb(x), _rb(w), b)
+    def forward(ctx, x, w, b, op=-1, decisions=None):
+        ctx.w, ctx.has_b, ctx.op, ctx.dec = w, b is not None, op, decisions
+        ctx.xr = _rbd(x, (op, "x"), decisions)
+        return F.linear(ctx.xr, _rb(w), b)
 
     @staticmethod
     def backward(ctx, dy):
-        x, w = ctx.x, ctx.w
+        w = ctx.w
         db = dy.sum(dim=0) if ctx.has_b else None
-        return _rb(dy) @ _rb(w), _rb(dy).t() @ _rb(x), db
+        dyr = _rbd(dy, (ctx.op, "dy"), ctx.dec)
+        return dyr @ _rb(w), dyr.t() @ ctx.xr, db, None, None
 
 
 def _relu(y, i, decisions):
@@ -171,7 +189,7 @@ def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5
         a = t[in0]
         if kind == CONV:
             if bf16:
-                y = _Bf16Conv.apply(a, P["weight"], P.get("bias"), stride, pad)
+                y = _Bf16Conv.apply(a, P["weight"], P.get("bias"), stride, pad, i, decisions)
             else:
                 y = F.conv2d(a, P["weight"], P.get("bias"), stride=stride, padding=pad)
             if flags & F_RELU:
@@ -191,7 +209,7 @@ def run_ops(ops, lo, hi, inputs, stage_params, slices, running=None, bn_eps=1e-5
             y = a.mean(dim=(2, 3), keepdim=True)
         elif kind == FC:
             if bf16:
-                y = _Bf16Linear.apply(a.reshape(a.shape[0], -1), P["weight"], P.get("bias"))
+                y = _Bf16Linear.apply(a.reshape(a.shape[0], -1), P["weight"], P.get("bias"), i, decisions)
             else:
                 y = F.linear(a.reshape(a.shape[0], -1), P["weight"], P.get("bias"))
             if flags & F_RELU:
