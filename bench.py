@@ -18,6 +18,9 @@ are synthetic N(0,1) [128,3,32,32] batches with uniform labels, all resident
 in HBM before timing starts.
 
 Prints one JSON line.  `value` is images/s over the K timed steps.
+`memory` is the device memory the net holds; `--step-sets 2` runs the
+pipeline with one step set less (the forward pass of step t then waits for
+the weight stream's step t-2 instead of t-3).
 `--bf16` runs the same ResNet-20 configuration with bf16 products (fp32
 accumulation); `--workload resnet110` runs ResNet-110 at batch 256 with bf16
 products, 8 stages of [7,7,7,7,7,7,6,6] blocks and staleness d_s = 7 - s
@@ -57,7 +60,9 @@ reference kernel for the counter scale).
 from __future__ import annotations
 
 import argparse
+import ctypes
 import json
+import math
 import os
 import sys
 import time
@@ -191,6 +196,9 @@ def main():
     ap.add_argument("--mode", choices=("pipelined", "graph", "sequential"), default="pipelined",
                     help="pipelined: psw_pipeline_run issued eagerly (default); graph: the same steps replayed "
                          "from a captured HIP graph; sequential: one psw_stage_step call per step")
+    ap.add_argument("--step-sets", type=int, choices=(2, 3), default=3,
+                    help="step sets the pipelined run rotates: 3 (default) lets the forward pass of step t wait "
+                         "for the weight stream's step t-3, 2 for its step t-2, at one step set less memory")
     ap.add_argument("--no-profile", action="store_true",
                     help="no events at all: skip the kernel-timing pass")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -215,9 +223,9 @@ def main():
     wl = synth.resnet110_workload() if r110 else synth.resnet20_workload(bf16=args.bf16)
     K = args.steps if args.steps is not None else (50 if r110 else 100)
     W = args.warmup if args.warmup is not None else (10 if r110 else 20)
-    period = 3  # step sets of the pipelined run
+    period = args.step_sets  # step sets of the pipelined run
     for d in wl.ring_depth():
-        period = period * d // __import__("math").gcd(period, d)
+        period = period * d // math.gcd(period, d)
     # a graph replays one period of ring slots and step sets: 12 steps for
     # ResNet-20's rings [4,3,2,1], 840 for ResNet-110's [8..1] (not captured)
     use_graph = period <= 64
@@ -225,7 +233,8 @@ def main():
         print(f"--mode graph: the pipeline's period is {period} steps, too long to capture", file=sys.stderr)
         sys.exit(2)
     T = W + period + REPLAY_STEPS + 3 * K + period
-    net = psw.Net(wl.ops, wl.batch, wl.in_shape, wl.stage_end, wl.ring_depth(T), bf16=wl.bf16)
+    net = psw.Net(wl.ops, wl.batch, wl.in_shape, wl.stage_end, wl.ring_depth(T), bf16=wl.bf16,
+                  step_sets=args.step_sets)
     net.load_params(synth.init_params(wl))
     stal = wl.staleness(T)
     # every mini-batch resident in HBM before timing (a fresh batch per step)
@@ -239,6 +248,9 @@ def main():
     torch.cuda.synchronize()
     t = 0
     losses = torch.zeros(max(K, W, REPLAY_STEPS, 1), dtype=torch.float32, device="cuda")
+    nb = ctypes.c_int64()
+    psw._check(psw.lib().psw_net_pipeline_bytes(net.handle, ctypes.byref(nb)))
+    net_step_bytes = nb.value
 
     def run_sequential(n):
         nonlocal t
@@ -391,6 +403,11 @@ def main():
                                  "pipelined": "pipelined psw_pipeline_run issued eagerly",
                                  "sequential": "one psw_stage_step call per step"}[args.mode]},
         "other_modes_images_per_s": others,
+        "memory": {"step_sets": args.step_sets, "step_set_bytes": net_step_bytes, "arena_bytes": net.arena_bytes,
+                   "ring_bytes": 4 * net.ring_floats, "device_bytes": net.device_bytes(),
+                   "what": "device memory of the net: weight-version rings, momentum, gradients, running "
+                           "statistics, the arena (one step set: activations, saved statistics, every tensor's "
+                           "gradient; and the shared workspaces) and the pipelined run's extra step sets"},
         "roofline": roof,
         "conv_mfma": conv,
         "kernel_ms_per_step": breakdown,

@@ -308,8 +308,11 @@ class Net:
     W^(0) (the packed stage parameters, stages concatenated) into slot 0.
     """
 
-    def __init__(self, ops, batch, in_shape, stage_end, ring_depth, bf16=False, device="cuda"):
+    def __init__(self, ops, batch, in_shape, stage_end, ring_depth, bf16=False, device="cuda", step_sets=3):
         L = lib()
+        if step_sets not in (2, 3):
+            raise ValueError(f"step_sets must be 2 or 3, got {step_sets}")
+        self.step_sets = step_sets  # step sets a pipelined run rotates (psw_net_bind_pipeline)
         self.ops = np.ascontiguousarray(ops, dtype=np.int32).reshape(-1, 9)
         self.S = len(stage_end)
         self._layers = _layers(self.ops)
@@ -324,6 +327,7 @@ class Net:
         rf, npar, nbn, ab = (ctypes.c_int64() for _ in range(4))
         _check(L.psw_net_sizes(self.handle, sp.ctypes.data, ctypes.byref(rf), ctypes.byref(npar), ctypes.byref(nbn),
                                ctypes.byref(ab)))
+        self.ring_floats, self.arena_bytes = rf.value, ab.value
         self.stage_params = [int(v) for v in sp]
         self.n_params = npar.value
         dev = torch.device(device)
@@ -414,8 +418,18 @@ class Net:
         if getattr(self, "step2", None) is None:
             nb = ctypes.c_int64()
             _check(lib().psw_net_pipeline_bytes(self.handle, ctypes.byref(nb)))
-            self.step2 = torch.empty(max(2 * nb.value, 256), dtype=torch.uint8, device=self.device)  # two more sets
+            extra = self.step_sets - 1  # sets beside the arena
+            self.step2 = torch.empty(max(extra * nb.value, 256), dtype=torch.uint8, device=self.device)
             _check(lib().psw_net_bind_pipeline(self.handle, _ptr(self.step2), self.step2.numel()))
+
+    def device_bytes(self):
+        """Device memory the net holds: the ring, momentum, gradient and running
+        statistics vectors, the arena (one step set and the shared workspaces)
+        and, once a pipelined run has bound them, the extra step sets."""
+        held = [self.ring, self.momentum, self.grad, self.run_mean, self.run_var, self.arena]
+        if getattr(self, "step2", None) is not None:
+            held.append(self.step2)
+        return sum(t.numel() * t.element_size() for t in held)
 
     def capture(self, staleness, lr, xs, labels, losses, mom=0.9, wd=0.0, nesterov=False):
         """Capture the next n pipelined steps into a graph (psw_pipeline_capture); returns a Graph whose

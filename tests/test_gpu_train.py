@@ -272,10 +272,10 @@ def _sequential(P, wl, N, st, lr, stash=False):
     return net, np.array(losses, dtype=np.float32), np.array(versions)
 
 
-def _pipelined(P, wl, N, st, lr, chunks, stash=False):
+def _pipelined(P, wl, N, st, lr, chunks, stash=False, step_sets=3):
     T = st.shape[0]
     net = P.Net(wl.ops, N, wl.in_shape, wl.stage_end, [int(st[:, s].max()) + 1 for s in range(st.shape[1])],
-                bf16=wl.bf16)
+                bf16=wl.bf16, step_sets=step_sets)
     net.load_params(synth.init_params(wl))
     net.set_weight_stashing(stash)
     net.set_dropout_seed(wl.dropout_seed)
@@ -353,6 +353,23 @@ def test_pipeline_run_equals_stage_steps(P, name, factory, N, rows, T, chunks):
     assert torch.equal(a.momentum, b.momentum)
     assert torch.equal(a.run_mean, b.run_mean) and torch.equal(a.run_var, b.run_var)
     print(f"{name}: {T} steps bit-identical, last loss {lb[-1]:.5f}")
+
+
+def test_pipeline_with_two_step_sets_equals_stage_steps(P):
+    """The pipelined run with one step set less (the forward pass of step t
+    waits for the weight stream's step t-2): still the per-step result bit
+    for bit, over enough steps for the two sets to alternate many times."""
+    wl = synth.resnet20_workload(batch=8)
+    T = 14
+    st = wl.staleness(T)
+    a, la, va = _sequential(P, wl, 8, st, wl.lr)
+    b, lb, vb = _pipelined(P, wl, 8, st, wl.lr, [5, 9], step_sets=2)
+    assert b.step_sets == 2 and b.step2 is not None
+    np.testing.assert_array_equal(va, vb)
+    np.testing.assert_array_equal(la, lb)
+    assert torch.equal(a.params(T), b.params(T))
+    assert torch.equal(a.momentum, b.momentum)
+    assert torch.equal(a.run_mean, b.run_mean) and torch.equal(a.run_var, b.run_var)
 
 
 def test_pipeline_after_stage_steps(P):
