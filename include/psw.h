@@ -351,6 +351,32 @@ int psw_net_slot(const psw_net *net, int stage, int64_t version, float **params)
  * or out of range, PSW_ERR_STATE before psw_net_bind. */
 int psw_net_tensor(const psw_net *net, int tensor, int grad, float **ptr, int64_t *count);
 
+/* Whether the forward value of tensor `tensor` is stored (host output
+ * *stored = 1) or not (0): the output of a BN + ReLU without residual that
+ * only one conv reads (the batch-norm and ReLU of Sec. 6's CNNs, before the
+ * second conv of a residual block, or between two convs of VGG) is never
+ * written while psw_net_set_bn_on_load is on; that conv forms
+ * max(y * scale + shift, 0) itself, in one fused multiply-add, from the BN's
+ * input y and the step's saved scale and shift (psw_net_bn_saved), in its
+ * forward pass and in its weight gradient.  The gradient of every tensor is
+ * stored.  Host only, valid from psw_net_create on; PSW_ERR_SHAPE for tensor
+ * 0 or out of range. */
+int psw_net_tensor_stored(const psw_net *net, int tensor, int *stored);
+
+/* Device pointers of BN operation `op`'s saved statistics of the last
+ * psw_stage_step (read-back like psw_net_tensor): mean [c], 1/sqrt(var+eps)
+ * [c] and scale_shift [2c] (gamma * invstd, then beta - mean * scale: the
+ * affine map of the forward pass, both as float).  PSW_ERR_SHAPE unless op
+ * is a BN, PSW_ERR_STATE before psw_net_bind. */
+int psw_net_bn_saved(const psw_net *net, int op, float **mean, float **invstd, float **scale_shift);
+
+/* on != 0 (the default): BNs whose output only one conv reads are applied
+ * by that conv while loading (psw_net_tensor_stored); on == 0: every BN
+ * output is stored by its own apply kernel.  Both give the same results bit
+ * for bit.  Takes effect from the next psw_stage_step / psw_pipeline_run /
+ * psw_pipeline_capture call; PSW_ERR_NULL for a NULL net. */
+int psw_net_set_bn_on_load(psw_net *net, int on);
+
 /* Offset (in floats, inside the packed parameters of the op's stage) and
  * count of operation `op`'s parameters (host outputs). */
 int psw_net_param_offset(const psw_net *net, int op, int *stage, int64_t *offset, int64_t *count);

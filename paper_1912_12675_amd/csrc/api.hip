@@ -357,6 +357,13 @@ struct psw_net {
     // op launches nothing when it did (pool_done_now, per step)
     std::vector<int> gavg_fwd_of;
     std::vector<char> pool_done_now;
+    // per BN op: a BN + ReLU without residual whose output only one conv
+    // reads; that conv applies it while staging its input (forward and weight
+    // gradient) from the BN's input and saved scale and shift, so the output
+    // is never stored and a statistics-only launch replaces the apply
+    // (bn_on_load_on: psw_net_set_bn_on_load)
+    std::vector<char> bn_on_load;
+    int bn_on_load_on = 1;
 
     std::vector<char> grad_accum;           // per op input slot: 0 overwrite, 1 accumulate (in0, in1)
     size_t step_bytes = 0;                  // one step set (activations, saves, gradients, forward ws)
@@ -767,6 +774,26 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
         }
         wpart = std::max(wpart, cur);
     }
+    // BN + ReLU applied by its one consumer conv while loading: the BN's
+    // statistics come from the conv before it, the consumer's forward and
+    // weight gradient (split partials) run on the direct kernels, which take
+    // the BN's input and scale / shift, and the BN's backward never reads its
+    // output (its sums come from the consumer's dgrad, the ReLU mask from y
+    // and the scale / shift)
+    net->bn_on_load.assign(n_layers, 0);
+    for (int j = 1; j + 1 < n_layers; ++j) {
+        const psw_layer& o = net->ops[j];
+        const psw_layer& c = net->ops[j + 1];
+        if (o.kind != PSW_OP_BN || o.in0 != j || o.in1 >= 0 || !(o.flags & PSW_F_RELU)) continue;
+        if (!net->fuse_stats[j - 1] || consumers[j + 1] != 1) continue;
+        if (c.kind != PSW_OP_CONV || c.in0 != j + 1 || (c.flags & (PSW_F_BIAS | PSW_F_RELU))) continue;
+        if (!net->fuse_bwd[j + 1] || net->wpart_splits[j + 1] <= 0 || net->t[j].w % 4) continue;
+        const Tensor a = net->t[j + 1];
+        psw::ConvShape cs;
+        check_conv(a.n, a.c, a.h, a.w, c.cout, c.k, c.k, c.stride, c.pad, prec, &cs);
+        if (!psw::conv_fwd_in_bn_ok(cs)) continue;
+        net->bn_on_load[j] = 1;
+    }
     for (int i = 1; i <= n_layers; ++i) {  // gradients of every tensor
         net->grad_off[i] = off;
         off = align256(off + (size_t)net->t[i].numel() * sizeof(float));
@@ -916,6 +943,38 @@ int psw_net_tensor(const psw_net* net, int tensor, int grad, float** ptr, int64_
     return PSW_OK;
 }
 
+int psw_net_tensor_stored(const psw_net* net, int tensor, int* stored)
+{
+    if (!net || !stored) return fail(PSW_ERR_NULL, "net_tensor_stored: required pointer is NULL");
+    const int L = (int)net->ops.size();
+    if (tensor < 1 || tensor > L)
+        return fail(PSW_ERR_SHAPE, "net_tensor_stored: tensor %d out of range 1..%d", tensor, L);
+    *stored = (net->bn_on_load_on && net->bn_on_load[tensor - 1]) ? 0 : 1;
+    return PSW_OK;
+}
+
+int psw_net_bn_saved(const psw_net* net, int op, float** mean, float** invstd, float** scale_shift)
+{
+    if (!net || !mean || !invstd || !scale_shift) return fail(PSW_ERR_NULL, "net_bn_saved: required pointer is NULL");
+    if (!net->bound) return fail(PSW_ERR_STATE, "net_bn_saved: net is not bound");
+    if (op < 0 || op >= (int)net->ops.size() || net->ops[op].kind != PSW_OP_BN)
+        return fail(PSW_ERR_SHAPE, "net_bn_saved: op %d is not a BN", op);
+    float* save = (float*)(net->arena + net->save_off[op]);
+    const int c = net->ops[op].cin;
+    *mean = save;
+    *invstd = save + c;
+    *scale_shift = save + 2 * c;
+    return PSW_OK;
+}
+
+int psw_net_set_bn_on_load(psw_net* net, int on)
+{
+    if (!net) return fail(PSW_ERR_NULL, "net_set_bn_on_load: net is NULL");
+    net->bn_on_load_on = on ? 1 : 0;
+    g_err.clear();
+    return PSW_OK;
+}
+
 int psw_net_param_offset(const psw_net* net, int op, int* stage, int64_t* offset, int64_t* count)
 {
     if (!net) return fail(PSW_ERR_NULL, "net_param_offset: net is NULL");
@@ -1028,6 +1087,8 @@ struct Issue {
     float* act(int id) const { return id == 0 ? (float*)io.x : (float*)(io.P + net->act_off[id]); }
     float* grd(int id) const { return (float*)(io.P + net->grad_off[id]); }
     float* save(int i) const { return (float*)(io.P + net->save_off[i]); }
+    // BN op j is applied by its consumer while loading (its output not stored)
+    bool on_load(int j) const { return net->bn_on_load_on && net->bn_on_load[j]; }
     void* wsf() const { return io.P + net->wsf_off; }
     void* wsb() const { return net->arena + net->step_bytes + net->ws_off; }
     void* wsw() const { return net->arena + net->step_bytes + net->wsw_off; }
@@ -1079,16 +1140,22 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
             const float* b = (o.flags & PSW_F_BIAS) ? W + (int64_t)o.cout * o.cin * o.k * o.k : nullptr;
             kind = PSW_PROF_CONV_FWD;
             net->fused_now[i] = 0;
+            // input from a BN applied on load: stage the BN's input through its
+            // scale / shift and ReLU (no fallback: the BN output is not stored)
+            const int bj = o.in0 - 1;
+            const bool ibn = bj >= 1 && is.on_load(bj);
+            const float* xin = ibn ? is.act(net->ops[bj].in0) : is.act(o.in0);
+            const float* inbn = ibn ? is.save(bj) + 2 * net->ops[bj].cin : nullptr;
             if (net->fuse_stats[i]) {  // the next op's BN statistics come out of this conv
                 psw::BnStatsFuse bn{(float*)ws};
-                e = psw::conv_fwd_bnstats(cs, is.act(o.in0), W, is.act(i + 1), bn, wsb / sizeof(float), bf16, sf);
+                e = psw::conv_fwd_bnstats(cs, xin, W, is.act(i + 1), bn, wsb / sizeof(float), bf16, sf, inbn);
                 if (e == hipSuccess)
                     net->fused_now[i] = 1;
                 else if (e != hipErrorNotSupported)  // not supported: nothing launched, unfused path below
                     PSW_TRY(e, "conv_fwd_bnstats");
             }
             if (!net->fused_now[i])
-                PSW_TRY(psw::conv_fwd(cs, is.act(o.in0), W, b, (o.flags & PSW_F_RELU) != 0, is.act(i + 1), bf16, sf),
+                PSW_TRY(psw::conv_fwd(cs, xin, W, b, (o.flags & PSW_F_RELU) != 0, is.act(i + 1), bf16, sf, inbn),
                         "conv_fwd");
             break;
         }
@@ -1106,6 +1173,12 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
                 check_conv(ci.n, ci.c, ci.h, ci.w, cv.cout, cv.k, cv.k, cv.stride, cv.pad, net->prec, &ccs);
                 const int T = psw::conv_fwd_bnstats_tiles(ccs);
                 const int P = a.n * a.h * a.w / T;
+                if (is.on_load(i)) {  // the consumer conv applies it: statistics only
+                    PSW_TRY(psw::bn_stats_from_partials(o.cin, (const float*)ws, T, P, W, W + o.cin, 1e-5f, 0.1f, save,
+                                                        save + o.cin, save + 2 * o.cin, rm, rvv, sf),
+                            "bn_stats");
+                    break;
+                }
                 const int pj = net->gavg_fwd_of[i];  // the global pool reading this output alone, if any
                 e = psw::bn_apply_from_partials(a.n, a.c, a.h, a.w, is.act(o.in0), (const float*)ws, T, P, W,
                                                 W + o.cin, o.in1 >= 0 ? is.act(o.in1) : nullptr, r.c, r.h, r.w,
@@ -1118,6 +1191,10 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
                 }
                 if (e != hipErrorNotSupported) PSW_TRY(e, "bn_apply");
                 // not supported: nothing launched, the statistics are recomputed below
+            }
+            if (is.on_load(i)) {  // excluded when the net was created
+                is.what = "BN applied on load: statistics not fused into the conv before it";
+                return hipErrorNotSupported;
             }
             PSW_TRY(psw::bn_fwd(a.n, a.c, a.h, a.w, is.act(o.in0), W, W + o.cin, o.in1 >= 0 ? is.act(o.in1) : nullptr,
                                 r.c, r.h, r.w, (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, is.act(i + 1), save,
@@ -1298,6 +1375,10 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
                 else if (e != hipErrorNotSupported)  // not supported: nothing launched, sums recomputed below
                     PSW_TRY(e, "bn_bwd_from_partials");
             }
+            if (!done && is.on_load(i)) {  // excluded when the net was created: bn_bwd reads the BN output
+                is.what = "BN applied on load: backward sums not fused into its consumer's dgrad";
+                return hipErrorNotSupported;
+            }
             if (!done)
                 PSW_TRY(psw::bn_bwd(a.n, a.c, a.h, a.w, g, is.act(i + 1), is.act(o.in0), is.wbwd(i), save,
                                     save + o.cin, (o.flags & PSW_F_RELU) != 0, din, dg, dg + o.cin, dres, r.c, r.h,
@@ -1350,6 +1431,7 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
             // reduces share a launch (each keeps its own operands and sums)
             const float* gx[psw::kWgradGroupMax];
             const float* gdy[psw::kWgradGroupMax];
+            const float* gbn[psw::kWgradGroupMax];  // input BN applied on load, else null
             float* gpart[psw::kWgradGroupMax];
             int gn = 0;
             psw::ConvShape gcs{};
@@ -1358,7 +1440,7 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
                 kind = PSW_PROF_CONV_BWD_WEIGHT;
                 const int m = gn;
                 gn = 0;
-                return psw::conv_bwd_weight_partials_group(gcs, gx, gdy, gpart, m, bf16, sw);
+                return psw::conv_bwd_weight_partials_group(gcs, gx, gdy, gpart, m, bf16, sw, gbn);
             };
             for (int j = net->stage_end[s] - 1; j >= net->stage_begin[s]; --j) {
                 const psw_layer& c = net->ops[j];
@@ -1372,7 +1454,10 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
                     if (gn > 0 && (gn == psw::kWgradGroupMax || memcmp(&gcs, &ccs, sizeof ccs) != 0))
                         PSW_TRY(flush(), "conv_bwd_weight");
                     gcs = ccs;
-                    gx[gn] = is.act(c.in0);
+                    const int bj = c.in0 - 1;  // input from a BN applied on load: its input and scale / shift
+                    const bool ibn = bj >= 1 && is.on_load(bj);
+                    gx[gn] = ibn ? is.act(net->ops[bj].in0) : is.act(c.in0);
+                    gbn[gn] = ibn ? is.save(bj) + 2 * net->ops[bj].cin : nullptr;
                     gdy[gn] = is.grd(j + 1);
                     gpart[gn] = is.wpart(j);
                     ++gn;

@@ -299,13 +299,20 @@ int wgrad_splits(const ConvShape& cs, int bf16)
 
 }  // namespace
 
-hipError_t conv_fwd(const ConvShape& cs, const float* x, const float* w, const float* bias, int relu, float* y,
-                    int bf16, hipStream_t st)
+bool conv_fwd_in_bn_ok(const ConvShape& cs)
 {
+    return cs.r == 3 && cs.s == 3 && cs.pad == 1 && cs.c <= kInBnMaxChannels &&
+           conv3x3_direct_covers(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, false);
+}
+
+hipError_t conv_fwd(const ConvShape& cs, const float* x, const float* w, const float* bias, int relu, float* y,
+                    int bf16, hipStream_t st, const float* in_bn)
+{
+    if (in_bn && (bias || relu || !conv_fwd_in_bn_ok(cs))) return hipErrorNotSupported;
     if (!bias && !relu && cs.r == 3 && cs.s == 3 && cs.pad == 1) {
         hipError_t e = conv3x3_direct(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, w, y, 0, false, st, nullptr, nullptr,
-                                      nullptr, bf16);
-        if (e != hipErrorNotSupported) return e;
+                                      nullptr, bf16, in_bn);
+        if (e != hipErrorNotSupported || in_bn) return e;
     }
     IgArgs a = make_args(cs);
     a.A = w; a.B = x; a.C = y; a.bias = bias; a.relu = relu;
@@ -323,12 +330,13 @@ int conv_fwd_bnstats_tiles(const ConvShape& cs)
 size_t conv_fwd_bnstats_part_floats(const ConvShape& cs) { return (size_t)conv_fwd_bnstats_tiles(cs) * cs.k * 2; }
 
 hipError_t conv_fwd_bnstats(const ConvShape& cs, const float* x, const float* w, float* y, const BnStatsFuse& bn,
-                            size_t part_capacity_floats, int bf16, hipStream_t st)
+                            size_t part_capacity_floats, int bf16, hipStream_t st, const float* in_bn)
 {
     const size_t need = conv_fwd_bnstats_part_floats(cs);
     if (need == 0) return hipErrorNotSupported;
     if (part_capacity_floats < need) return hipErrorInvalidValue;
-    return conv3x3_direct(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, w, y, 0, false, st, &bn, nullptr, nullptr, bf16);
+    return conv3x3_direct(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, w, y, 0, false, st, &bn, nullptr, nullptr, bf16,
+                          in_bn);
 }
 
 hipError_t conv_bwd_data(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate, int bf16,
@@ -417,10 +425,11 @@ hipError_t conv_bwd_weight_partials(const ConvShape& cs, const float* x, const f
 }
 
 hipError_t conv_bwd_weight_partials_group(const ConvShape& cs, const float* const* x, const float* const* dy,
-                                          float* const* part, int count, int bf16, hipStream_t st)
+                                          float* const* part, int count, int bf16, hipStream_t st,
+                                          const float* const* in_bn)
 {
     if (!use_direct_wgrad(cs, bf16)) return hipErrorNotSupported;
-    return conv3x3_wgrad_group(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, part, count, st, bf16);
+    return conv3x3_wgrad_group(cs.n, cs.c, cs.h, cs.w, cs.k, cs.stride, x, dy, part, count, st, bf16, in_bn);
 }
 
 hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy, float* dw, float* db, int bf16,

@@ -78,6 +78,11 @@ struct DirArgs {
     BnStatsFuse bn;  // bn.part == nullptr: no statistics
     BnBwdFuse bnb;   // bnb.part == nullptr: no backward sums (transposed kernel only)
     BnFold fold;     // input formed from a folded BN backward (FOLD kernels only)
+    // forward only, may be null: the input is the raw input of a BN + ReLU
+    // whose output is never stored; in_bn[c], in_bn[C + c] are channel c's
+    // scale and shift, and the staged input is max(fma(x, scale, shift), 0)
+    // (zero outside the image, like any halo)
+    const float* in_bn;
 };
 
 constexpr int round4(int v) { return (v + 3) / 4 * 4; }
@@ -184,6 +189,9 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     __shared__ __attribute__((aligned(16))) float ftab[FOLD ? kFoldMaxChannels * 8 : 4];
     // per-wave parts of the epilogue's per-tile channel sums: [2][WP][TK]
     __shared__ float wred[2 * WP * TK];
+    // input BN (a.in_bn, forward kernels): scale [kInBnMaxChannels], shift
+    constexpr bool IBN = !TRANS && !FOLD;
+    __shared__ float ibt[IBN ? 2 * kInBnMaxChannels : 1];
 
     constexpr int tiles = WO / TH;       // row tiles per (square) image
     static_assert(WO % TH == 0, "row tiles");
@@ -290,7 +298,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     float4 wr[WV];
     float4 fyr[FOLD ? XV : 1];  // folded BN: xr holds its output gradient, fyr its input
     float4 fzr[FOLD == 2 ? XV : 1];  // and fzr its output (ReLU mask) when it has a residual
-    unsigned okm = 0;           // folded BN: bit k set when element k lies inside the tensor
+    unsigned okm = 0;           // folded BN, input BN: bit k set when element k lies inside the tensor
     // Loads are issued without branches: a lane whose element lies outside
     // the tensor (halo rows, channels past C, threads past the chunk) loads
     // from offset 0 and keeps zero, so the compiler can count outstanding
@@ -316,6 +324,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
             } else {
                 const float4 v = *reinterpret_cast<const float4*>(a.x + (ok ? xb + xg[k] : 0));
                 xr[k] = ok ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+                if constexpr (IBN) okm = (okm & ~(1u << k)) | (ok ? 1u << k : 0u);
             }
         }
         if (wfast) {
@@ -420,8 +429,22 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
             }
         } else {
 #pragma unroll
-            for (int k = 0; k < XV; ++k)
-                if ((k + 1) * NT <= XN || xch[k] < CC) put_x(k, xr[k]);
+            for (int k = 0; k < XV; ++k) {
+                if (!((k + 1) * NT <= XN || xch[k] < CC)) continue;
+                float4 v = xr[k];
+                if constexpr (IBN) {
+                    if (a.in_bn) {  // the BN + ReLU of the stored input, exactly as its apply kernel forms it
+                        const int ch = c0 + xch[k] < a.C ? c0 + xch[k] : 0;
+                        const float sc = ibt[ch], sf = ibt[kInBnMaxChannels + ch];
+                        v = (okm & (1u << k)) ? make_float4(fmaxf(__fmaf_rn(v.x, sc, sf), 0.f),
+                                                            fmaxf(__fmaf_rn(v.y, sc, sf), 0.f),
+                                                            fmaxf(__fmaf_rn(v.z, sc, sf), 0.f),
+                                                            fmaxf(__fmaf_rn(v.w, sc, sf), 0.f))
+                                              : make_float4(0.f, 0.f, 0.f, 0.f);
+                    }
+                }
+                put_x(k, v);
+            }
         }
 #pragma unroll
         for (int k = 0; k < WV; ++k) {
@@ -453,6 +476,13 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     // across them: the first chunk of the next tile is loaded while the last
     // chunk of the current one is on the matrix cores
     load_chunk(blockIdx.x * TPW / tiles, (blockIdx.x * TPW % tiles) * TH * STRIDE - 1, 0);
+    if constexpr (IBN) {  // after the first tile's loads are issued; read after the chunk loop's first barrier
+        if (a.in_bn)
+            for (int i = tid; i < a.C; i += NT) {
+                ibt[i] = a.in_bn[i];
+                ibt[kInBnMaxChannels + i] = a.in_bn[a.C + i];
+            }
+    }
     if constexpr (FOLD) {
         // merge the BN's per-tile sums while the first tile loads are in
         // flight: G = NT / C consecutive threads per channel, thread q of a
@@ -1137,8 +1167,9 @@ bool conv3x3_direct_covers(int n, int C, int H, int W, int K, int stride, bool t
 
 hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const float* x, const float* w, float* y,
                           int accumulate, bool transpose, hipStream_t st, const BnStatsFuse* bn, const BnBwdFuse* bnb,
-                          const BnFold* fold, bool bf16)
+                          const BnFold* fold, bool bf16, const float* in_bn)
 {
+    if (in_bn && (transpose || C > kInBnMaxChannels)) return hipErrorNotSupported;
     if (bnb && (!transpose || stride != 1)) return hipErrorNotSupported;
     if (fold && (!transpose || stride != 1 || C > kFoldMaxChannels || (C & (C - 1)) || !fold->g || !fold->y ||
                  !fold->dy || !fold->part || (uintptr_t)fold->part % 8 || (fold->dres && !fold->z) ||
@@ -1153,7 +1184,7 @@ hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const f
     if (bn && transpose) return hipErrorNotSupported;
     if ((uintptr_t)x % 16) return hipErrorNotSupported;  // float4 tile staging
     const int HO = H / stride, WO = W / stride;
-    DirArgs a{x, w, y, C, H, K, HO, accumulate, BnStatsFuse{nullptr}, BnBwdFuse{}, BnFold{}};
+    DirArgs a{x, w, y, C, H, K, HO, accumulate, BnStatsFuse{nullptr}, BnBwdFuse{}, BnFold{}, in_bn};
     if (bn) a.bn = *bn;
     if (bnb) a.bnb = *bnb;
     if (fold) a.fold = *fold;

@@ -174,12 +174,15 @@ struct BnFold {
     float* dres = nullptr;         // residual's gradient (residual BN only)
 };
 constexpr int kFoldMaxChannels = 128;
+// largest input of a forward conv that applies its input's BN while loading
+constexpr int kInBnMaxChannels = 128;
 
 // ---- convolution (implicit GEMM on MFMA) ----
 // Forward conv + fused BN statistics (direct kernel only); returns
 // hipErrorNotSupported when the shape has no direct configuration.
+// in_bn (may be null): see conv_fwd.
 hipError_t conv_fwd_bnstats(const ConvShape& cs, const float* x, const float* w, float* y, const BnStatsFuse& bn,
-                            size_t part_capacity_floats, int bf16, hipStream_t st);
+                            size_t part_capacity_floats, int bf16, hipStream_t st, const float* in_bn = nullptr);
 size_t conv_fwd_bnstats_part_floats(const ConvShape& cs);
 int conv_fwd_bnstats_tiles(const ConvShape& cs);  // tiles T (partials per channel), 0 if not fused
 // BN forward (+residual, +ReLU) whose statistics come as per-tile (mean, M2)
@@ -194,12 +197,21 @@ hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, co
                                   int relu, float eps, float momentum, float* z, float* save_mean, float* save_invstd,
                                   float* save_scale, float* run_mean, float* run_var, hipStream_t st,
                                   float* pool = nullptr);
+// The statistics of bn_apply_from_partials alone (saved mean, invstd, scale
+// and shift, running statistics; the same values bit for bit), for a BN
+// whose output is never stored because its one consumer applies it while
+// loading (DirArgs::in_bn, the weight gradient's in_bn).  save_scale is
+// required.
+hipError_t bn_stats_from_partials(int c, const float* part, int T, int P, const float* gamma, const float* beta,
+                                  float eps, float momentum, float* save_mean, float* save_invstd, float* save_scale,
+                                  float* run_mean, float* run_var, hipStream_t st);
 // Direct 3x3 / pad 1 kernel (forward, or backward-data of a stride-1 layer
 // when transpose is set); hipErrorNotSupported when no tile config fits.
 // bf16: both operands rounded to bfloat16 (nearest even), fp32 accumulation.
 hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const float* x, const float* w, float* y,
                           int accumulate, bool transpose, hipStream_t st, const BnStatsFuse* bn = nullptr,
-                          const BnBwdFuse* bnb = nullptr, const BnFold* fold = nullptr, bool bf16 = false);
+                          const BnBwdFuse* bnb = nullptr, const BnFold* fold = nullptr, bool bf16 = false,
+                          const float* in_bn = nullptr);
 // whether conv3x3_direct takes the shape (same arguments)
 bool conv3x3_direct_covers(int n, int C, int H, int W, int K, int stride, bool transpose);
 // number of pixel tiles (workgroups along x) of the direct forward kernel, 0 if none
@@ -238,11 +250,20 @@ hipError_t conv3x3_wgrad(int n, int C, int H, int W, int K, int stride, const fl
 // The same for `count` (<= kWgradGroupMax) convolutions of one shape in one
 // launch: member i reads x[i], dy[i] and writes its partial sums to part[i].
 constexpr int kWgradGroupMax = 8;
+// in_bn (may be null, else one pointer per member, each may be null): see
+// the in_bn of WgArgs.
 hipError_t conv3x3_wgrad_group(int n, int C, int H, int W, int K, int stride, const float* const* x,
                                const float* const* dy, float* const* part, int count, hipStream_t st,
-                               bool bf16 = false);
+                               bool bf16 = false, const float* const* in_bn = nullptr);
+// in_bn (may be null): x is the raw input of a BN + ReLU whose output is not
+// stored, in_bn its per-channel scale [c] and shift [c] (DirArgs::in_bn);
+// only the direct kernel takes it (conv_fwd_in_bn_ok), otherwise
+// hipErrorNotSupported with nothing launched.
 hipError_t conv_fwd(const ConvShape& cs, const float* x, const float* w, const float* bias, int relu,
-                    float* y, int bf16, hipStream_t st);
+                    float* y, int bf16, hipStream_t st, const float* in_bn = nullptr);
+// whether conv_fwd / conv_fwd_bnstats take an in_bn for this shape (no bias,
+// no ReLU)
+bool conv_fwd_in_bn_ok(const ConvShape& cs);
 hipError_t conv_bwd_data(const ConvShape& cs, const float* w, const float* dy, float* dx, int accumulate,
                          int bf16, hipStream_t st);
 size_t conv_bwd_weight_ws_bytes(const ConvShape& cs, int bf16);
@@ -255,9 +276,12 @@ hipError_t conv_bwd_weight(const ConvShape& cs, const float* x, const float* dy,
 int conv_bwd_weight_part_splits(const ConvShape& cs, int bf16);
 hipError_t conv_bwd_weight_partials(const ConvShape& cs, const float* x, const float* dy, float* part, int bf16,
                                     hipStream_t st);
-// The same for `count` convolutions of shape cs in one launch.
+// The same for `count` convolutions of shape cs in one launch; in_bn (may be
+// null): per member, null or the scale / shift of a BN + ReLU applied to x
+// on load (conv3x3_wgrad_group).
 hipError_t conv_bwd_weight_partials_group(const ConvShape& cs, const float* const* x, const float* const* dy,
-                                          float* const* part, int count, int bf16, hipStream_t st);
+                                          float* const* part, int count, int bf16, hipStream_t st,
+                                          const float* const* in_bn = nullptr);
 
 // ---- batch norm (+ residual) (+ ReLU) ----
 size_t bn_ws_bytes(int n, int c, int h, int w);

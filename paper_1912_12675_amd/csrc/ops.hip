@@ -947,6 +947,77 @@ __device__ __forceinline__ void load_tile_stats(const float* pp, int T, float2 (
     }
 }
 
+// the merge of one channel's T tile statistics (thread t: tiles t,
+// t + kBlock, ... in order, from pv or, for larger tables, from pp; then the
+// block in a fixed order), and thread 0's coefficients: coef = (scale,
+// shift); block y == 0 also stores the saved and running statistics
+__device__ __forceinline__ void bn_merge_finish(const float* pp, int T, int P,
+                                                const float2 (&pv)[kMergeTilesPerThread], double* sh, float* coef,
+                                                int c, int ch, const float* gamma, const float* beta, float eps,
+                                                float momentum, float* save_mean, float* save_invstd,
+                                                float* save_scale, float* run_mean, float* run_var)
+{
+    double s1 = 0.0, s2 = 0.0;
+    if (T <= kMergeTilesPerThread * kBlock) {
+#pragma unroll
+        for (int k = 0; k < kMergeTilesPerThread; ++k)
+            if ((int)threadIdx.x + k * kBlock < T) {
+                const double m = (double)pv[k].x;
+                s1 += m;
+                s2 += (double)pv[k].y + (double)P * m * m;
+            }
+    } else {
+        for (int t = threadIdx.x; t < T; t += kBlock) {
+            const double m = (double)pp[2 * t];
+            s1 += m;
+            s2 += (double)pp[2 * t + 1] + (double)P * m * m;
+        }
+    }
+    block_sum2(s1, s2, sh);
+    if (threadIdx.x == 0) {
+        const double cnt = (double)T * P;
+        const double mean = s1 / T;
+        double var = (s2 - cnt * mean * mean) / cnt;
+        if (var < 0.0) var = 0.0;
+        const double invstd = 1.0 / sqrt(var + (double)eps);
+        const double scale = (double)gamma[ch] * invstd;
+        coef[0] = (float)scale;
+        coef[1] = (float)((double)beta[ch] - mean * scale);
+        if (blockIdx.y == 0) {
+            save_mean[ch] = (float)mean;
+            save_invstd[ch] = (float)invstd;
+            if (save_scale) {
+                save_scale[ch] = coef[0];
+                save_scale[c + ch] = coef[1];
+            }
+            if (run_mean) {
+                run_mean[ch] = (float)((1.0 - momentum) * run_mean[ch] + momentum * mean);
+                run_var[ch] = (float)((1.0 - momentum) * run_var[ch] + momentum * (cnt > 1.0 ? var * cnt / (cnt - 1.0) : var));
+            }
+        }
+    }
+}
+
+// The statistics alone (one block per channel), for a BN whose output is
+// never stored: its only consumer, a convolution, stages
+// max(fma(y, scale, shift), 0) itself from y and the saved scale and shift
+// (the values this kernel's coefficients give, bit for bit, as the apply
+// kernel would).
+__global__ __launch_bounds__(kBlock) void bn_stats_partials_k(int c, const float* part, int T, int P,
+                                                               const float* gamma, const float* beta, float eps,
+                                                               float momentum, float* save_mean, float* save_invstd,
+                                                               float* save_scale, float* run_mean, float* run_var)
+{
+    __shared__ double sh[2 * kBlock / 64];
+    __shared__ float coef[2];
+    const int ch = blockIdx.x;
+    const float* pp = part + (size_t)ch * T * 2;
+    float2 pv[kMergeTilesPerThread];
+    load_tile_stats(pp, T, pv);
+    bn_merge_finish(pp, T, P, pv, sh, coef, c, ch, gamma, beta, eps, momentum, save_mean, save_invstd, save_scale,
+                    run_mean, run_var);
+}
+
 template <int U>
 __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int hw, const float* y, const float* part,
                                                                int T, int P, const float* gamma, const float* beta,
@@ -991,45 +1062,8 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
             }
         }
     }
-    double s1 = 0.0, s2 = 0.0;
-    if (T <= kMergeTilesPerThread * kBlock) {
-#pragma unroll
-        for (int k = 0; k < kMergeTilesPerThread; ++k)
-            if ((int)threadIdx.x + k * kBlock < T) {
-                const double m = (double)pv[k].x;
-                s1 += m;
-                s2 += (double)pv[k].y + (double)P * m * m;
-            }
-    } else {
-        for (int t = threadIdx.x; t < T; t += kBlock) {
-            const double m = (double)pp[2 * t];
-            s1 += m;
-            s2 += (double)pp[2 * t + 1] + (double)P * m * m;
-        }
-    }
-    block_sum2(s1, s2, sh);
-    if (threadIdx.x == 0) {
-        const double cnt = (double)T * P;
-        const double mean = s1 / T;
-        double var = (s2 - cnt * mean * mean) / cnt;
-        if (var < 0.0) var = 0.0;
-        const double invstd = 1.0 / sqrt(var + (double)eps);
-        const double scale = (double)gamma[ch] * invstd;
-        coef[0] = (float)scale;
-        coef[1] = (float)((double)beta[ch] - mean * scale);
-        if (blockIdx.y == 0) {
-            save_mean[ch] = (float)mean;
-            save_invstd[ch] = (float)invstd;
-            if (save_scale) {
-                save_scale[ch] = coef[0];
-                save_scale[c + ch] = coef[1];
-            }
-            if (run_mean) {
-                run_mean[ch] = (float)((1.0 - momentum) * run_mean[ch] + momentum * mean);
-                run_var[ch] = (float)((1.0 - momentum) * run_var[ch] + momentum * (cnt > 1.0 ? var * cnt / (cnt - 1.0) : var));
-            }
-        }
-    }
+    bn_merge_finish(pp, T, P, pv, sh, coef, c, ch, gamma, beta, eps, momentum, save_mean, save_invstd, save_scale,
+                    run_mean, run_var);
     __syncthreads();
     const float sc = coef[0], sf = coef[1];
 #pragma unroll
@@ -1212,6 +1246,17 @@ hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, co
     else
         PSW_BN_APPLY(1);
 #undef PSW_BN_APPLY
+    return hipGetLastError();
+}
+
+hipError_t bn_stats_from_partials(int c, const float* part, int T, int P, const float* gamma, const float* beta,
+                                  float eps, float momentum, float* save_mean, float* save_invstd, float* save_scale,
+                                  float* run_mean, float* run_var, hipStream_t st)
+{
+    if (!save_scale || (uintptr_t)part % 8) return hipErrorNotSupported;
+    const Work wk{8.0 * c * T, 2 * kF * (double)T * c + 4 * kF * c};  // the partials read, four floats per channel written
+    PSW_LAUNCH(kname("bn_stats_partials_k"), wk, bn_stats_partials_k, dim3(c), dim3(kBlock), 0, st, c, part, T, P,
+               gamma, beta, eps, momentum, save_mean, save_invstd, save_scale, run_mean, run_var);
     return hipGetLastError();
 }
 

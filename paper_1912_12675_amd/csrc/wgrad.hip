@@ -51,6 +51,10 @@ struct WgArgs {
     const float* x[kWgradGroupMax];   // member i: [n][C][H][W]
     const float* dy[kWgradGroupMax];  // [n][K][HO][WO]
     float* part[kWgradGroupMax];      // [splits][K][C][9]
+    // may be null: member i's x is the raw input of a BN + ReLU whose output
+    // is not stored; in_bn[i][c], in_bn[i][C + c] are channel c's scale and
+    // shift, and the input used is max(fma(x, scale, shift), 0)
+    const float* in_bn[kWgradGroupMax];
     int n, C, H, W, K, HO;
     int splits;                       // workgroups (partial sums) per member
 };
@@ -69,7 +73,9 @@ constexpr int round4(int v) { return (v + 3) / 4 * 4; }
 // 16 consecutive output pixels (4 pixel quads; lane group g supplies quad g):
 // the fp32 tiles are staged as before and each lane rounds its 4 dy values
 // and its 4 shifted input values to bf16 when it reads them.
-template <int STRIDE, int WO, int TH, int KBW, int CBW, int WPX, int TPW, int RC, bool BF, int IPW>
+// IBN: some member may have an input BN (WgArgs::in_bn); without it the
+// staging has no such path.
+template <int STRIDE, int WO, int TH, int KBW, int CBW, int WPX, int TPW, int RC, bool BF, int IPW, bool IBN>
 __global__ __launch_bounds__(64 * KBW * CBW * WPX * IPW) void conv3x3_wgrad(WgArgs a)
 {
     constexpr int NT = 64 * KBW * CBW * WPX;  // threads of one group
@@ -94,6 +100,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX * IPW) void conv3x3_wgrad(WgAr
     constexpr int LDS_FLOATS = TILE_FLOATS > RED1 ? (TILE_FLOATS > RED2 ? TILE_FLOATS : RED2) : (RED1 > RED2 ? RED1 : RED2);
     static_assert(LDS_FLOATS * 4 <= 65536, "LDS");
     __shared__ __attribute__((aligned(16))) float lds[LDS_FLOATS];
+    __shared__ float bnt[IBN ? 2 * CCH : 1];  // the member's input BN over this workgroup's channels: scale, shift
 
     const int wave_all = threadIdx.x >> 6;
     const int ip = wave_all / (KBW * CBW * WPX);  // group
@@ -106,6 +113,7 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX * IPW) void conv3x3_wgrad(WgAr
     const int bx = blockIdx.x - mem * a.splits;     // partial-sum index within it
     const float* gx = a.x[mem];
     const float* gdy = a.dy[mem];
+    const float* ibn = IBN ? a.in_bn[mem] : nullptr;
     const int bands = a.HO / TH;         // row bands per image
     const int cbase = blockIdx.y * CCH;  // first input channel of this workgroup
     const int kbase = blockIdx.z * KC;   // first output channel of this workgroup
@@ -141,10 +149,13 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX * IPW) void conv3x3_wgrad(WgAr
             }
             dr[v] = val;
         }
+        // with an input BN, elements outside the input start as NaN: the
+        // staging's max(fma(x, scale, shift), 0) then gives exactly 0 there
+        const float fill = ibn ? __builtin_nanf("") : 0.f;
 #pragma unroll
         for (int v = 0; v < XV; ++v) {
             const int i4 = tid + v * NT;
-            float4 val = make_float4(0.f, 0.f, 0.f, 0.f);
+            float4 val = make_float4(fill, fill, fill, fill);
             if (i4 < XN4) {
                 const int i = i4 * 4;
                 const int c = i / (HRC * WIN);
@@ -177,15 +188,29 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX * IPW) void conv3x3_wgrad(WgAr
                 const int c = i / (HRC * WIN);
                 const int rem = i - c * (HRC * WIN);
                 const int rr = rem / WIN, iw = rem - (rem / WIN) * WIN;
+                float4 val = xr[v];
+                if (IBN && ibn) {  // the BN + ReLU of the stored input, exactly as its apply kernel forms it
+                    const float sc = bnt[c], sf = bnt[CCH + c];
+                    val = make_float4(fmaxf(__fmaf_rn(val.x, sc, sf), 0.f), fmaxf(__fmaf_rn(val.y, sc, sf), 0.f),
+                                      fmaxf(__fmaf_rn(val.z, sc, sf), 0.f), fmaxf(__fmaf_rn(val.w, sc, sf), 0.f));
+                }
                 float2* d = reinterpret_cast<float2*>(Xs + c * XPS + rr * XRS + 4 + iw);  // even offset
-                d[0] = make_float2(xr[v].x, xr[v].y);
-                d[1] = make_float2(xr[v].z, xr[v].w);
+                d[0] = make_float2(val.x, val.y);
+                d[1] = make_float2(val.z, val.w);
             }
         }
     };
 
     const float* dsl = Ds + (kb * 16 + j) * DPS + g;
     const float* xsl = Xs + (cb * 16 + j) * XPS + g * STRIDE + 3;
+    // the input BN's coefficients (read after the chunk loop's first
+    // barrier; loaded before the first chunk: issued after it, their wait
+    // held the staging of the 32x32 layers back by 6 us)
+    if (IBN && ibn && threadIdx.x < CCH) {
+        const int c = cbase + (int)threadIdx.x < a.C ? cbase + (int)threadIdx.x : 0;
+        bnt[threadIdx.x] = ibn[c];
+        bnt[CCH + threadIdx.x] = ibn[a.C + c];
+    }
     load_chunk(0);
     for (int ch = 0; ch < NCH; ++ch) {
         __syncthreads();  // the previous chunk's LDS reads are done
@@ -312,13 +337,14 @@ int conv3x3_wgrad_splits(int n, int C, int H, int W, int K, int stride)
     case 3: return wgrad_wide(n) ? n / 16 : n / 8;  // four (eight) images per group, 32 of the 64 output channels
     case 4: return n;           // one 8-row band (of 16 output rows) per group
     case 5: return n / 2;       // one image per group
-    case 6: return n;           // as 1, input channels zero-filled to 16
+    case 6: return 2 * n;       // one 8-row band per group, input channels zero-filled to 16
     default: return 0;
     }
 }
 
 hipError_t conv3x3_wgrad_group(int n, int C, int H, int W, int K, int stride, const float* const* x,
-                               const float* const* dy, float* const* part, int count, hipStream_t st, bool bf16)
+                               const float* const* dy, float* const* part, int count, hipStream_t st, bool bf16,
+                               const float* const* in_bn)
 {
     const int cfg = wgrad_config(n, C, H, W, K, stride);
     if (!cfg || count < 1 || count > kWgradGroupMax) return hipErrorNotSupported;
@@ -328,31 +354,38 @@ hipError_t conv3x3_wgrad_group(int n, int C, int H, int W, int K, int stride, co
         a.x[i] = x[i];
         a.dy[i] = dy[i];
         a.part[i] = part[i];
+        a.in_bn[i] = in_bn ? in_bn[i] : nullptr;
     }
     a.n = n; a.C = C; a.H = H; a.W = W; a.K = K; a.HO = H / stride;
     const int splits = conv3x3_wgrad_splits(n, C, H, W, K, stride);
     a.splits = splits;
     const int cgroups = (C + 15) / 16;  // one 16-channel block per workgroup (grid.y)
-    // output-channel groups: configurations 2 and 3 split K over the grid
-    const int kgroups = cfg == 2 ? K / 16 : cfg == 3 ? K / 32 : 1;
+    // output-channel groups: configurations 2-5 split K over the grid (the
+    // stride-2 layers' small launches then fill the chip: twice the
+    // workgroups with the same partial sums)
+    const int kgroups = (cfg == 2 || cfg == 4) ? K / 16 : (cfg == 3 || cfg == 5) ? K / 32 : 1;
     const dim3 grid(splits * count, cgroups, kgroups);
     Work wk = conv_work(n, C, H, W, K, 3, 3, H / stride, W / stride);
     wk.flops *= count;
     wk.bytes *= count;
+#define PSW_WG1(S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, BF_, IBN_)                                            \
+    PSW_LAUNCH(kname("conv3x3_wgrad", S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, BF_, 2, IBN_), wk,               \
+               (conv3x3_wgrad<S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, BF_, 2, IBN_>), grid, dim3(512), 0, st, a)
 #define PSW_WG(S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_)                                                          \
     do {                                                                                                        \
-        if (bf16)                                                                                               \
-            PSW_LAUNCH(kname("conv3x3_wgrad", S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, true, 2), wk,          \
-                       (conv3x3_wgrad<S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, true, 2>), grid, dim3(512), 0, st, \
-                       a);                                                                                      \
-        else                                                                                                    \
-            PSW_LAUNCH(kname("conv3x3_wgrad", S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, false, 2), wk,         \
-                       (conv3x3_wgrad<S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, false, 2>), grid, dim3(512), 0, st, \
-                       a);                                                                                      \
+        if (bf16 && any_bn) PSW_WG1(S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, true, true);                     \
+        else if (bf16) PSW_WG1(S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, true, false);                         \
+        else if (any_bn) PSW_WG1(S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, false, true);                       \
+        else PSW_WG1(S_, WO_, TH_, KBW_, CBW_, WPX_, TPW_, RC_, false, false);                                  \
     } while (0)
+    bool any_bn = false;
+    for (int i = 0; i < count; ++i) any_bn = any_bn || a.in_bn[i];
     switch (cfg) {
-    case 6:
-    case 1: PSW_WG(1, 32, 16, 1, 1, 4, 1, 4); break;
+    case 1:  // with an input BN the 4-row chunks' staging would pass 128 VGPRs (one workgroup per CU)
+        if (any_bn) PSW_WG(1, 32, 16, 1, 1, 4, 1, 2);
+        else PSW_WG(1, 32, 16, 1, 1, 4, 1, 4);
+        break;
+    case 6: PSW_WG(1, 32, 8, 1, 1, 4, 1, 4); break;  // a narrow input: twice the workgroups
     case 2:
         if (wgrad_wide(n)) PSW_WG(1, 16, 16, 1, 1, 4, 4, 8);
         else PSW_WG(1, 16, 16, 1, 1, 4, 2, 8);
@@ -361,10 +394,11 @@ hipError_t conv3x3_wgrad_group(int n, int C, int H, int W, int K, int stride, co
         if (wgrad_wide(n)) PSW_WG(1, 8, 8, 2, 1, 2, 8, 8);
         else PSW_WG(1, 8, 8, 2, 1, 2, 4, 8);
         break;
-    case 4: PSW_WG(2, 16, 8, 2, 1, 2, 1, 4); break;
-    case 5: PSW_WG(2, 8, 8, 4, 1, 1, 1, 4); break;
+    case 4: PSW_WG(2, 16, 8, 1, 1, 4, 1, 4); break;
+    case 5: PSW_WG(2, 8, 8, 2, 1, 2, 1, 4); break;
     }
 #undef PSW_WG
+#undef PSW_WG1
     return hipGetLastError();
 }
 

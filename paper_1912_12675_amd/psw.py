@@ -88,6 +88,9 @@ SIGNATURES = {
     "psw_net_param_offset": (_I, [_P, _I, ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int64),
                                   ctypes.POINTER(ctypes.c_int64)]),
     "psw_net_tensor": (_I, [_P, _I, _I, ctypes.POINTER(ctypes.c_void_p), ctypes.POINTER(ctypes.c_int64)]),
+    "psw_net_tensor_stored": (_I, [_P, _I, ctypes.POINTER(ctypes.c_int)]),
+    "psw_net_bn_saved": (_I, [_P, _I] + [ctypes.POINTER(ctypes.c_void_p)] * 3),
+    "psw_net_set_bn_on_load": (_I, [_P, _I]),
     "psw_net_plan": (_I, [_P, _I64, _P, ctypes.POINTER(psw_launch), _I, ctypes.POINTER(ctypes.c_int)]),
     "psw_net_profile": (_I, [_P, _I]),
     "psw_net_profile_read": (_I, [_P, _I, _P, _P]),
@@ -380,6 +383,29 @@ class Net:
         _check(lib().psw_net_tensor(self.handle, int(tensor), int(bool(grad)), ctypes.byref(p), ctypes.byref(n)))
         off = p.value - self.arena.data_ptr()
         return self.arena[off:off + 4 * n.value].view(torch.float32)
+
+    def tensor_stored(self, tensor):
+        """False for the output of a BN applied by its consumer conv while
+        loading (psw_net_tensor_stored): its psw_net_tensor view holds no value."""
+        st = ctypes.c_int()
+        _check(lib().psw_net_tensor_stored(self.handle, int(tensor), ctypes.byref(st)))
+        return bool(st.value)
+
+    def bn_saved(self, op):
+        """Views of BN op `op`'s saved mean [c], invstd [c] and scale_shift [2c] of the last
+        psw_stage_step (psw_net_bn_saved)."""
+        ptrs = [ctypes.c_void_p() for _ in range(3)]
+        _check(lib().psw_net_bn_saved(self.handle, int(op), *[ctypes.byref(q) for q in ptrs]))
+        c = int(self.ops[op][3])
+        out = []
+        for q, n in zip(ptrs, (c, c, 2 * c)):
+            off = q.value - self.arena.data_ptr()
+            out.append(self.arena[off:off + 4 * n].view(torch.float32))
+        return tuple(out)
+
+    def set_bn_on_load(self, on=True):
+        """BNs applied by their one consumer conv while loading (default) or stored by their own kernel."""
+        _check(lib().psw_net_set_bn_on_load(self.handle, int(bool(on))))
 
     def set_step(self, t):
         _check(lib().psw_net_set_step(self.handle, int(t)))

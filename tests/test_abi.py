@@ -292,3 +292,46 @@ def test_plan_no_fold_when_residual_is_the_conv_input(psw):
     # it whose backward-data kernel forms its sums): only the aliasing
     # keeps it from being folded
     assert bn_bwd[3] == 9
+
+
+def _unstored(psw, wl):
+    L = psw.lib()
+    layers = psw._layers(wl.ops)
+    se = np.ascontiguousarray(wl.stage_end, dtype=np.int32)
+    rd = np.ascontiguousarray(wl.ring_depth(), dtype=np.int32)
+    h = ctypes.c_void_p()
+    psw._check(L.psw_net_create(layers, len(layers), wl.batch, *wl.in_shape, se.ctypes.data, len(se), rd.ctypes.data,
+                                psw._prec(wl.bf16), ctypes.byref(h)))
+    try:
+        out = []
+        for k in range(1, len(layers) + 1):
+            st = ctypes.c_int()
+            psw._check(L.psw_net_tensor_stored(h.value, k, ctypes.byref(st)))
+            if not st.value:
+                out.append(k)
+        for bad in (0, len(layers) + 1):
+            assert L.psw_net_tensor_stored(h.value, bad, ctypes.byref(st)) != 0
+        return out
+    finally:
+        L.psw_net_destroy(h.value)
+
+
+def test_bn_applied_on_load_only_where_nothing_else_reads_it(psw):
+    """The BN + ReLU before a residual block's second conv (one per block:
+    its output has that conv as its only reader, no residual, statistics
+    from the conv before it) is applied by the conv while loading, so its
+    output is not stored; block outputs (BN with the residual, read by the
+    next block's conv and by the shortcut) and the stem's BN are stored.
+    VGG-16's convs outside the weight-gradient kernels' shapes, AlexNet
+    (no BN) and LeNet store everything."""
+    r20 = synth.resnet20_workload()
+    got = _unstored(psw, r20)
+    assert got == [4 * b + 4 for b in range(9)]
+    for k in got:
+        bn = r20.ops[k - 1]
+        assert bn[0] == synth.BN and bn[2] < 0 and bn[8] & synth.F_RELU
+        assert [i for i, o in enumerate(r20.ops) if o[1] == k or o[2] == k] == [k]
+    assert _unstored(psw, synth.resnet20_workload(batch=8, bf16=True)) == got
+    assert _unstored(psw, synth.resnet110_workload()) == [4 * b + 4 for b in range(54)]
+    for wl in (synth.vgg16_workload(), synth.alexnet_workload(), synth.lenet5_workload()):
+        assert _unstored(psw, wl) == []

@@ -50,6 +50,34 @@ def P():
     return psw
 
 
+def bn_preact(net, wl, j):
+    """float64 y * scale + shift of BN op j from the GPU's stored input y and
+    saved scale / shift: for a BN applied by its consumer conv while loading
+    (output not stored), the consumer forms max(fma(y, scale, shift), 0)
+    itself; the float64 value (y * scale is exact in it) has the fused
+    result's sign, so its ReLU decisions are the GPU's."""
+    c = int(wl.ops[j][3])
+    y = net.tensor(int(wl.ops[j][1])).double().view(wl.batch, c, -1)
+    ss = net.bn_saved(j)[2].double()
+    return y * ss[:c].view(1, c, 1) + ss[c:].view(1, c, 1)
+
+
+def tensor_value(net, wl, k):
+    """The forward value of tensor k: read back, or for a BN output that is
+    not stored, rebuilt from its input and saved scale / shift (the one
+    rounding of the fused multiply-add taken in float64 first: at most an ulp
+    away, rarely)."""
+    if net.tensor_stored(k):
+        return net.tensor(k)
+    return bn_preact(net, wl, k - 1).clamp_min(0).float().reshape(-1)
+
+
+def relu_mask(net, wl, i):
+    if net.tensor_stored(i + 1):
+        return (net.tensor(i + 1) > 0).cpu()
+    return (bn_preact(net, wl, i) > 0).reshape(-1).cpu()
+
+
 def gpu_step(P, wl, state, ring_depth):
     t = state.t
     net = P.Net(wl.ops, wl.batch, wl.in_shape, wl.stage_end, ring_depth, bf16=wl.bf16)
@@ -71,9 +99,9 @@ def gpu_step(P, wl, state, ring_depth):
     # the GPU's ReLU decisions: output of every op with a ReLU > 0
     relu_ops = [i for i, o in enumerate(wl.ops) if int(o[0]) in (synth.CONV, synth.BN, synth.FC) and
                 int(o[8]) & synth.F_RELU]
-    masks = {i: (net.tensor(i + 1) > 0).cpu() for i in relu_ops}
+    masks = {i: relu_mask(net, wl, i) for i in relu_ops}
     # and its max-pool inputs and outputs, from which its argmax follows
-    pools = {i: (net.tensor(int(o[1])).cpu(), net.tensor(i + 1).cpu(), int(o[5]))
+    pools = {i: (tensor_value(net, wl, int(o[1])).cpu(), tensor_value(net, wl, i + 1).cpu(), int(o[5]))
              for i, o in enumerate(wl.ops) if int(o[0]) == synth.MAXPOOL}
     return dict(versions=ver, grad=net.grad.double().cpu().numpy(), momentum=net.momentum.double().cpu().numpy(),
                 params=net.params(t + 1).double().numpy(), loss=float(net.loss.item()), masks=masks, pools=pools)
@@ -246,7 +274,7 @@ def check_in_situ(P, oracle, wl, state, ring_depth, label):
     shp = oracle.shapes(wl.ops, wl.in_shape, N, wl.stage_end)
     act, grd = {0: x}, {}
     for k in range(1, L + 1):
-        act[k] = net.tensor(k).cpu().numpy().reshape(shp[k])
+        act[k] = tensor_value(net, wl, k).cpu().numpy().reshape(shp[k])
         grd[k] = net.tensor(k, grad=True).cpu().numpy().reshape(shp[k])
     gvec = net.grad.double().cpu().numpy()
     del net

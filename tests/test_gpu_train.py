@@ -372,6 +372,34 @@ def test_pipeline_with_two_step_sets_equals_stage_steps(P):
     assert torch.equal(a.run_mean, b.run_mean) and torch.equal(a.run_var, b.run_var)
 
 
+@pytest.mark.parametrize("batch,bf16,T", [(8, False, 8), (8, True, 8), (128, False, 3), (128, True, 3)])
+def test_bn_on_load_is_bit_identical(P, batch, bf16, T):
+    """The BNs that their consumer conv applies while loading (forward and
+    weight gradient, from the BN's input and saved scale / shift) against
+    the same net with every BN output stored by its own kernel: the same
+    fused multiply-add and ReLU on the same values, so the pipelined run's
+    losses, parameters, momentum and running statistics agree bit for bit
+    (batch 128: the full-size launch configurations)."""
+    wl = synth.resnet20_workload(batch=batch, bf16=bf16)
+    st = wl.staleness(T)
+    runs = []
+    for on in (False, True):
+        net = P.Net(wl.ops, batch, wl.in_shape, wl.stage_end, wl.ring_depth(T), bf16=bf16)
+        net.set_bn_on_load(on)
+        assert all(net.tensor_stored(k) for k in range(1, len(wl.ops) + 1)) != on
+        net.load_params(synth.init_params(wl))
+        xs, ys = synth.batches(wl, T, batch)
+        losses = torch.zeros(T, dtype=torch.float32, device="cuda")
+        net.pipeline_run(0, st, wl.lr, torch.from_numpy(xs).cuda(), torch.from_numpy(ys).cuda(), losses, wl.momentum)
+        torch.cuda.synchronize()
+        runs.append((net, losses.cpu().numpy()))
+    (a, la), (b, lb) = runs
+    np.testing.assert_array_equal(la, lb)
+    assert torch.equal(a.params(T), b.params(T))
+    assert torch.equal(a.momentum, b.momentum)
+    assert torch.equal(a.run_mean, b.run_mean) and torch.equal(a.run_var, b.run_var)
+
+
 def test_pipeline_after_stage_steps(P):
     """Per-step calls, then a pipelined run from the next step: same as
     per-step calls throughout."""
@@ -554,7 +582,9 @@ def test_bn_backward_folds_run(P):
     does the pool's backward (no pool-backward, channel-sum, finalise or
     apply launches; in the forward pass its BN apply writes the pooled means,
     so no pool launch either) -- and its weight gradients as 6 grouped
-    launches."""
+    launches.  In the forward pass the 9 BNs before a block's second conv are
+    applied by that conv while loading: 9 statistics-only launches and 10
+    apply kernels for the 19 BNs."""
     wl = synth.resnet20_workload(batch=8)
     net = P.Net(wl.ops, 8, wl.in_shape, wl.stage_end, [4, 3, 2, 1])
     net.load_params(synth.init_params(wl))
@@ -572,4 +602,7 @@ def test_bn_backward_folds_run(P):
     assert count(lambda n: n.startswith(("gavg_bwd_k", "chan_partials", "bn_bwd_finalize", "bn_bwd_apply"))) == 0
     # forward: that BN's apply kernel also writes the pooled means
     assert count(lambda n: n.startswith("gavg_fwd_k")) == 0
+    assert count(lambda n: n.startswith("bn_stats_partials_k")) == 9
+    assert count(lambda n: n.startswith("bn_apply_partials_k")) == 10
+    assert [k for k in range(1, len(wl.ops) + 1) if not net.tensor_stored(k)] == [4 * b + 4 for b in range(9)]
     assert count(lambda n: n.startswith("conv3x3_wgrad")) == 6
