@@ -74,6 +74,7 @@ struct DirArgs {
     const float* w;  // layer weights as stored, KCRS
     float* y;        // output [n][K][HO][WO]
     int C, H, K, HO;
+    int n;           // images
     int accumulate;
     BnStatsFuse bn;  // bn.part == nullptr: no statistics
     BnBwdFuse bnb;   // bnb.part == nullptr: no backward sums (transposed kernel only)
@@ -195,10 +196,25 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
 
     constexpr int tiles = WO / TH;       // row tiles per (square) image
     static_assert(WO % TH == 0, "row tiles");
-    const int T_all = gridDim.x * TPW;   // tiles of the launch (BN partial index)
+    static_assert(TPW == 1 || tiles % TPW == 0, "a workgroup's tiles lie in one image");
+    // one-dimensional grid: workgroup -> (image, group of TPW tiles, block of
+    // TK output channels).  Image i's workgroups run on XCD i mod 8
+    // (consecutive workgroups go to the 8 XCDs in turn), in consecutive
+    // rounds of 8, so the row tiles of an image, which share halo rows, and
+    // its output-channel blocks, which share the whole input tile, find them
+    // in that XCD's L2; indices past the last image (the grid is a multiple
+    // of 8 images) do nothing
+    constexpr int tgroups = tiles / TPW;
+    const int kblocks = a.K / TK, combos = tgroups * kblocks;
+    const int slot = (int)(blockIdx.x >> 3) % combos;
+    const int image = (int)(blockIdx.x >> 3) / combos * 8 + (int)(blockIdx.x & 7);
+    if (image >= a.n) return;
+    const int bxl = image * tgroups + slot % tgroups;  // group of TPW consecutive tiles (image-major)
+    const int byl = slot / tgroups;                    // output-channel block
+    const int T_all = a.n * tiles;       // tiles of the launch (BN partial index)
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wk = wave % WK, wp = wave / WK;
-    const int mblk = blockIdx.y * TK;
+    const int mblk = byl * TK;
     const int g = lane >> 4, j = lane & 15;
 
     int boff[NBW];  // B operand: fp32 layout, float offset; BMF, byte offset of the 8-byte element
@@ -371,7 +387,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     // under the matrix loop instead of delaying the barrier
     auto write_dy = [&](int img, int ih0, int c0) {
         if constexpr (FOLD) {
-            if (blockIdx.y != 0) return;
+            if (byl != 0) return;
             const int xb = ((img * a.C + c0) * HIN + ih0) * WIN;
 #pragma unroll
             for (int k = 0; k < XV; ++k)
@@ -476,7 +492,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     // TPW consecutive row tiles per workgroup; the software pipeline runs
     // across them: the first chunk of the next tile is loaded while the last
     // chunk of the current one is on the matrix cores
-    load_chunk(blockIdx.x * TPW / tiles, (blockIdx.x * TPW % tiles) * TH * STRIDE - 1, 0);
+    load_chunk(bxl * TPW / tiles, (bxl * TPW % tiles) * TH * STRIDE - 1, 0);
     if constexpr (IBN) {  // after the first tile's loads are issued; read after the chunk loop's first barrier
         if (a.in_bn)
             for (int i = tid; i < a.C; i += NT) {
@@ -532,7 +548,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
             ftab[ch * 8 + 4] = is;
             ftab[ch * 8 + 5] = a.fold.relu ? a.fold.scale[ch] : 0.f;
             ftab[ch * 8 + 6] = a.fold.relu ? a.fold.scale[a.C + ch] : 0.f;
-            if (blockIdx.x == 0 && blockIdx.y == 0) {
+            if (bxl == 0 && byl == 0) {
                 a.fold.dbeta[ch] = (float)s1;
                 a.fold.dgamma[ch] = (float)s2;
             }
@@ -544,7 +560,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
     float pyy[PRE ? NBW : 1][4], pzz[PRE ? NBW : 1][4];
     if constexpr (PRE) {
         if (a.bnb.part) {
-            const int img = blockIdx.x / tiles, oh0 = (blockIdx.x - img * tiles) * TH;
+            const int img = bxl / tiles, oh0 = (bxl - img * tiles) * TH;
             const bool zmask = a.bnb.relu && !a.bnb.scale;
 #pragma unroll
             for (int nb = 0; nb < NBW; ++nb) {
@@ -560,7 +576,7 @@ __global__ __launch_bounds__(64 * WK * WP) void conv3x3_direct(DirArgs a)
         }
     }
     for (int q = 0; q < TPW; ++q) {
-    const int tl = blockIdx.x * TPW + q;
+    const int tl = bxl * TPW + q;
     const int img = tl / tiles;
     const int oh0 = (tl - img * tiles) * TH;
     for (int c0 = 0; c0 < a.C; c0 += CC) {
@@ -1098,8 +1114,10 @@ void launch_direct_p(const DirArgs& a, dim3 grid, dim3 block, const Work& wk, bo
 template <int WO, int STRIDE, int TH, int CC, int WK, int WP, int NBW, int TPW = 1>
 hipError_t launch_direct(const DirArgs& a, int n, bool trans, bool bf, hipStream_t st)
 {
-    if ((n * (a.HO / TH)) % TPW) return hipErrorNotSupported;
-    dim3 grid(n * (a.HO / TH) / TPW, a.K / (16 * WK));
+    if ((a.HO / TH) % TPW) return hipErrorNotSupported;
+    // one-dimensional, a multiple of 8 images (the kernel maps workgroups to
+    // images XCD by XCD)
+    dim3 grid((unsigned)((n + 7) / 8 * 8 * (a.HO / TH / TPW) * (a.K / (16 * WK))));
     dim3 block(64 * WK * WP);
     // as a convolution: input a.C x a.H x WO*STRIDE, output a.K x a.HO x WO
     Work wk = conv_work(n, a.C, a.H, WO * STRIDE, a.K, 3, 3, a.HO, WO);
@@ -1185,7 +1203,7 @@ hipError_t conv3x3_direct(int n, int C, int H, int W, int K, int stride, const f
     if (bn && transpose) return hipErrorNotSupported;
     if ((uintptr_t)x % 16) return hipErrorNotSupported;  // float4 tile staging
     const int HO = H / stride, WO = W / stride;
-    DirArgs a{x, w, y, C, H, K, HO, accumulate, BnStatsFuse{nullptr}, BnBwdFuse{}, BnFold{}, in_bn};
+    DirArgs a{x, w, y, C, H, K, HO, n, accumulate, BnStatsFuse{nullptr}, BnBwdFuse{}, BnFold{}, in_bn};
     if (bn) a.bn = *bn;
     if (bnb) a.bnb = *bnb;
     if (fold) a.fold = *fold;

@@ -12,11 +12,14 @@
 // order at the end, so a workgroup covers IPW times the pixels of one group
 // and writes IPW times fewer partial sums than one group per workgroup would.
 // One launch may cover several convolutions of the same shape (the
-// same-shape layers of a pipeline stage): blockIdx.x / splits selects the
-// convolution, and each has its own operands and partial sums.
-// blockIdx.y selects a group of CBW 16-channel input blocks and blockIdx.z a
-// group of KBW 16-channel output blocks.  In the
-// workgroup, wave (kb, cb, wpx) owns the 16x16 output blocks (output channels
+// same-shape layers of a pipeline stage), and each has its own operands and
+// partial sums.  The grid is one-dimensional: a workgroup's unit (member,
+// partial-sum index) and its combination of CBW-block input channels and
+// KBW-block output channels follow from its index so that the combinations
+// of one unit, which read the same input or output-gradient tile, run on
+// one XCD (consecutive workgroups go to the 8 XCDs in turn) at nearly the
+// same time, and the tiles come from that XCD's L2 after the first read.  In
+// the workgroup, wave (kb, cb, wpx) owns the 16x16 output blocks (output channels
 // kb*16.., input channels of block cb) of all 9 taps (9 MFMA accumulators)
 // and the pixel quads wpx, wpx+WPX, ...; waves that differ only in wpx are
 // summed through LDS in wpx order at the end.
@@ -57,6 +60,8 @@ struct WgArgs {
     const float* in_bn[kWgradGroupMax];
     int n, C, H, W, K, HO;
     int splits;                       // workgroups (partial sums) per member
+    int units;                        // splits * members
+    int cgroups, combos;              // input-channel groups; combos = cgroups * output-channel groups
 };
 
 // smallest v >= lo with v % 32 == 2
@@ -109,14 +114,23 @@ __global__ __launch_bounds__(64 * KBW * CBW * WPX * IPW) void conv3x3_wgrad(WgAr
     float* Ds = lds + ip * (DS_FLOATS + XS_FLOATS);
     float* Xs = Ds + DS_FLOATS;
     const int g = lane >> 4, j = lane & 15;
-    const int mem = blockIdx.x / a.splits;          // member of the group
-    const int bx = blockIdx.x - mem * a.splits;     // partial-sum index within it
+    // workgroup index -> (unit, channel combination): units u = 8g + x for
+    // g >= 0 run on XCD x, each unit's combinations in consecutive rounds of
+    // 8 workgroups; indices past the last unit (the grid is a multiple of 8
+    // units) do nothing
+    const int wgi = blockIdx.x;
+    const int slot = (wgi >> 3) % a.combos;
+    const int unit = ((wgi >> 3) / a.combos) * 8 + (wgi & 7);
+    if (unit >= a.units) return;
+    const int mem = unit / a.splits;                // member of the group
+    const int bx = unit - mem * a.splits;           // partial-sum index within it
+    const int cgi = slot % a.cgroups, kgi = slot / a.cgroups;
     const float* gx = a.x[mem];
     const float* gdy = a.dy[mem];
     const float* ibn = IBN ? a.in_bn[mem] : nullptr;
     const int bands = a.HO / TH;         // row bands per image
-    const int cbase = blockIdx.y * CCH;  // first input channel of this workgroup
-    const int kbase = blockIdx.z * KC;   // first output channel of this workgroup
+    const int cbase = cgi * CCH;  // first input channel of this workgroup
+    const int kbase = kgi * KC;   // first output channel of this workgroup
 
     v4f acc[9];
 #pragma unroll
@@ -364,7 +378,10 @@ hipError_t conv3x3_wgrad_group(int n, int C, int H, int W, int K, int stride, co
     // stride-2 layers' small launches then fill the chip: twice the
     // workgroups with the same partial sums)
     const int kgroups = (cfg == 2 || cfg == 4) ? K / 16 : (cfg == 3 || cfg == 5) ? K / 32 : 1;
-    const dim3 grid(splits * count, cgroups, kgroups);
+    a.units = splits * count;
+    a.cgroups = cgroups;
+    a.combos = cgroups * kgroups;
+    const dim3 grid((unsigned)((a.units + 7) / 8 * 8 * a.combos));
     Work wk = conv_work(n, C, H, W, K, 3, 3, H / stride, W / stride);
     wk.flops *= count;
     wk.bytes *= count;
