@@ -357,6 +357,12 @@ struct psw_net {
     // op launches nothing when it did (pool_done_now, per step)
     std::vector<int> gavg_fwd_of;
     std::vector<char> pool_done_now;
+    // per BN op with both pool fusions: its apply kernel also stores, per
+    // (image, channel), the ReLU-pass count and the sum of xhat there (at
+    // pstat_off in the step set), and its backward is one elementwise pass
+    // from them (bn_bwd_gavg_from_stats)
+    std::vector<char> gavg_pstat;
+    std::vector<size_t> pstat_off;
     // per BN op: a BN + ReLU without residual whose output only one conv
     // reads; that conv applies it while staging its input (forward and weight
     // gradient) from the BN's input and saved scale and shift, so the output
@@ -740,6 +746,14 @@ int build_net(psw_net* net, const psw_layer* layers, int n_layers, int batch, in
         net->gavg_of[b] = j;
         net->gavg_fused[j] = 1;
     }
+    net->gavg_pstat.assign(n_layers, 0);
+    net->pstat_off.assign(n_layers, 0);
+    for (int b = 1; b < n_layers; ++b) {
+        if (net->gavg_of[b] < 0 || net->gavg_fwd_of[b] < 0 || !net->fuse_stats[b - 1] || net->ops[b].in0 != b) continue;
+        net->gavg_pstat[b] = 1;
+        net->pstat_off[b] = off;
+        off = align256(off + 2 * (size_t)net->t[b + 1].n * net->ops[b].cin * sizeof(float));
+    }
     // split partial sums of the conv weight gradients, reduced by the stage update
     net->wpart_splits.assign(n_layers, 0);
     net->wpart_off.assign(n_layers, 0);
@@ -1087,6 +1101,7 @@ struct Issue {
     float* act(int id) const { return id == 0 ? (float*)io.x : (float*)(io.P + net->act_off[id]); }
     float* grd(int id) const { return (float*)(io.P + net->grad_off[id]); }
     float* save(int i) const { return (float*)(io.P + net->save_off[i]); }
+    float* pstat(int i) const { return (float*)(io.P + net->pstat_off[i]); }
     // BN op j is applied by its consumer while loading (its output not stored)
     bool on_load(int j) const { return net->bn_on_load_on && net->bn_on_load[j]; }
     void* wsf() const { return io.P + net->wsf_off; }
@@ -1184,7 +1199,8 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
                                                 W + o.cin, o.in1 >= 0 ? is.act(o.in1) : nullptr, r.c, r.h, r.w,
                                                 (o.flags & PSW_F_RELU) != 0, 1e-5f, 0.1f, is.act(i + 1), save,
                                                 save + o.cin, save + 2 * o.cin, rm, rvv, sf,
-                                                pj >= 0 ? is.act(pj + 1) : nullptr);
+                                                pj >= 0 ? is.act(pj + 1) : nullptr,
+                                                (pj >= 0 && net->gavg_pstat[i]) ? is.pstat(i) : nullptr);
                 if (e == hipSuccess) {
                     if (pj >= 0) net->pool_done_now[pj] = 1;
                     break;
@@ -1192,8 +1208,8 @@ hipError_t issue_forward(Issue& is, hipStream_t sf, BeforeStage before_stage)
                 if (e != hipErrorNotSupported) PSW_TRY(e, "bn_apply");
                 // not supported: nothing launched, the statistics are recomputed below
             }
-            if (is.on_load(i)) {  // excluded when the net was created
-                is.what = "BN applied on load: statistics not fused into the conv before it";
+            if (is.on_load(i) || net->gavg_pstat[i]) {  // excluded when the net was created
+                is.what = "BN with fused statistics: the conv before it did not produce them";
                 return hipErrorNotSupported;
             }
             PSW_TRY(psw::bn_fwd(a.n, a.c, a.h, a.w, is.act(o.in0), W, W + o.cin, o.in1 >= 0 ? is.act(o.in1) : nullptr,
@@ -1353,7 +1369,13 @@ hipError_t issue_backward(Issue& is, hipStream_t sb, hipStream_t sw, BeforeStage
             }
             kind = PSW_PROF_BN_BWD;
             bool done = false;
-            if (net->gavg_of[i] >= 0) {  // with the global average pool's backward: dh = the pool output's gradient
+            if (net->gavg_of[i] >= 0 && net->gavg_pstat[i]) {  // from the forward's plane statistics
+                PSW_TRY(psw::bn_bwd_gavg_from_stats(a.n, a.c, a.h, a.w, is.grd(net->gavg_of[i] + 1), is.pstat(i),
+                                                    is.act(i + 1), is.act(o.in0), is.wbwd(i), save, save + o.cin,
+                                                    (o.flags & PSW_F_RELU) != 0, g, din, dg, dg + o.cin, dres, sb),
+                        "bn_bwd_gavg_from_stats");
+                done = true;
+            } else if (net->gavg_of[i] >= 0) {  // with the global average pool's backward: dh = the pool output's gradient
                 PSW_TRY(psw::bn_bwd_gavg(a.n, a.c, a.h, a.w, is.grd(net->gavg_of[i] + 1), is.act(i + 1),
                                          is.act(o.in0), is.wbwd(i), save, save + o.cin,
                                          (o.flags & PSW_F_RELU) != 0, g, din, dg, dg + o.cin, dres, sb),

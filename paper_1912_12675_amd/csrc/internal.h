@@ -191,12 +191,14 @@ int conv_fwd_bnstats_tiles(const ConvShape& cs);  // tiles T (partials per chann
 // statistics and running statistics, and every block normalises its part.
 // pool: when set (an 8x8 output that only a global average pool reads), the
 // per-(image, channel) means of the output are written there as well;
-// hipErrorNotSupported (nothing launched) unless h * w == 64.
+// hipErrorNotSupported (nothing launched) unless h * w == 64.  pstat (with
+// pool only): per (image, channel) the number of elements where the ReLU
+// passed and the sum of xhat = (y - mean) * invstd over them, [n][c][2].
 hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, const float* part, int T, int P,
                                   const float* gamma, const float* beta, const float* res, int rc, int rh, int rw,
                                   int relu, float eps, float momentum, float* z, float* save_mean, float* save_invstd,
                                   float* save_scale, float* run_mean, float* run_var, hipStream_t st,
-                                  float* pool = nullptr);
+                                  float* pool = nullptr, float* pstat = nullptr);
 // The statistics of bn_apply_from_partials alone (saved mean, invstd, scale
 // and shift, running statistics; the same values bit for bit), for a BN
 // whose output is never stored because its one consumer applies it while
@@ -303,6 +305,12 @@ hipError_t bn_bwd(int n, int c, int h, int w, const float* dz, const float* z, c
 hipError_t bn_bwd_gavg(int n, int c, int h, int w, const float* dh, const float* z, const float* y,
                        const float* gamma, const float* mean, const float* invstd, int relu, float* dz, float* dy,
                        float* dgamma, float* dbeta, float* dres, hipStream_t st);
+// bn_bwd_gavg from the plane statistics the forward stored (pstat of
+// bn_apply_from_partials: per (image, channel) the ReLU-pass count and the
+// sum of xhat there): one elementwise pass over many workgroups per channel.
+hipError_t bn_bwd_gavg_from_stats(int n, int c, int h, int w, const float* dh, const float* pstat, const float* z,
+                                  const float* y, const float* gamma, const float* mean, const float* invstd, int relu,
+                                  float* dz, float* dy, float* dgamma, float* dbeta, float* dres, hipStream_t st);
 
 // ---- pooling ----
 hipError_t maxpool_fwd(int n, int c, int h, int w, int k, int stride, const float* x, float* y,

@@ -363,6 +363,81 @@ __global__ __launch_bounds__(kBlock) void bn_bwd_gavg_k(int n, int c, int hw, co
     }
 }
 
+// The same backward from the plane statistics the forward's apply kernel
+// stored (per image and channel: the number of pixels where the ReLU passed
+// and the sum of xhat there): with the pool's gradient g = dh / hw uniform
+// over a plane, sum g' = sum_n g_n cnt_n and sum g' xhat = sum_n g_n sx_n,
+// so the channel's sums come from 2n numbers and one elementwise pass
+// remains, spread over many workgroups per channel (grid (c, blocks per
+// channel), U float4 per thread).
+template <int U>
+__global__ __launch_bounds__(kBlock) void bn_bwd_gavg_stats_k(int n, int c, int hw, const float* dh,
+                                                               const float* pstat, const float* z, const float* y,
+                                                               const float* gamma, const float* mean,
+                                                               const float* invstd, int relu, float* dz, float* dy,
+                                                               float* dgamma, float* dbeta, float* dres)
+{
+    __shared__ double sh[2 * kBlock / 64];
+    __shared__ float coef[3];
+    const int ch = blockIdx.x;
+    const int hw4 = hw >> 2, units = n * hw4;
+    const int u0 = blockIdx.y * (U * kBlock), u1 = min(u0 + U * kBlock, units);
+    // the elements first (their latency passes under the sums)
+    size_t idx[U];
+    float4 yv[U], zv[U];
+    float gq[U];
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+        const int u = u0 + (int)threadIdx.x + q * kBlock;
+        idx[q] = 0;
+        yv[q] = zv[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+        gq[q] = 0.f;
+        if (u < u1) {
+            const int img = u / hw4, off = (u - img * hw4) * 4;
+            idx[q] = ((size_t)img * c + ch) * hw + off;
+            yv[q] = *reinterpret_cast<const float4*>(y + idx[q]);
+            zv[q] = *reinterpret_cast<const float4*>(z + idx[q]);
+            gq[q] = dh[(size_t)img * c + ch] / (float)hw;
+        }
+    }
+    double s1 = 0.0, s2 = 0.0;
+    for (int img = threadIdx.x; img < n; img += kBlock) {
+        const double g = (double)(dh[(size_t)img * c + ch] / (float)hw);
+        s1 += g * (double)pstat[((size_t)img * c + ch) * 2 + 0];
+        s2 += g * (double)pstat[((size_t)img * c + ch) * 2 + 1];
+    }
+    block_sum2(s1, s2, sh);
+    const float mu = mean[ch], is = invstd[ch];
+    if (threadIdx.x == 0) {
+        const double cnt = (double)n * hw;
+        coef[0] = (float)((double)gamma[ch] * (double)is);
+        coef[1] = (float)(s1 / cnt);
+        coef[2] = (float)(s2 / cnt);
+        if (blockIdx.y == 0) {
+            dbeta[ch] = (float)s1;
+            dgamma[ch] = (float)s2;
+        }
+    }
+    __syncthreads();
+    const float a = coef[0], b = coef[1], d = coef[2];
+#pragma unroll
+    for (int q = 0; q < U; ++q) {
+        if (u0 + (int)threadIdx.x + q * kBlock >= u1) continue;
+        const float g = gq[q];
+        const float yy[4] = {yv[q].x, yv[q].y, yv[q].z, yv[q].w}, zz[4] = {zv[q].x, zv[q].y, zv[q].z, zv[q].w};
+        float o[4], gm[4];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            gm[e] = (relu && !(zz[e] > 0.f)) ? 0.f : g;
+            const float xh = (yy[e] - mu) * is;
+            o[e] = a * (gm[e] - b - xh * d);
+        }
+        store_stream4(dz + idx[q], make_float4(g, g, g, g));
+        store_stream4(dy + idx[q], make_float4(o[0], o[1], o[2], o[3]));
+        if (dres) store_stream4(dres + idx[q], make_float4(gm[0], gm[1], gm[2], gm[3]));
+    }
+}
+
 // -------------------------------------------------------------- misc -------
 __global__ void relu_mask_k(int64_t count, const float* z, float* g)
 {
@@ -950,7 +1025,8 @@ __device__ __forceinline__ void load_tile_stats(const float* pp, int T, float2 (
 // the merge of one channel's T tile statistics (thread t: tiles t,
 // t + kBlock, ... in order, from pv or, for larger tables, from pp; then the
 // block in a fixed order), and thread 0's coefficients: coef = (scale,
-// shift); block y == 0 also stores the saved and running statistics
+// shift, mean, invstd) as stored; block y == 0 also stores the saved and
+// running statistics
 __device__ __forceinline__ void bn_merge_finish(const float* pp, int T, int P,
                                                 const float2 (&pv)[kMergeTilesPerThread], double* sh, float* coef,
                                                 int c, int ch, const float* gamma, const float* beta, float eps,
@@ -983,6 +1059,8 @@ __device__ __forceinline__ void bn_merge_finish(const float* pp, int T, int P,
         const double scale = (double)gamma[ch] * invstd;
         coef[0] = (float)scale;
         coef[1] = (float)((double)beta[ch] - mean * scale);
+        coef[2] = (float)mean;
+        coef[3] = (float)invstd;
         if (blockIdx.y == 0) {
             save_mean[ch] = (float)mean;
             save_invstd[ch] = (float)invstd;
@@ -1009,7 +1087,7 @@ __global__ __launch_bounds__(kBlock) void bn_stats_partials_k(int c, const float
                                                                float* save_scale, float* run_mean, float* run_var)
 {
     __shared__ double sh[2 * kBlock / 64];
-    __shared__ float coef[2];
+    __shared__ float coef[4];
     const int ch = blockIdx.x;
     const float* pp = part + (size_t)ch * T * 2;
     float2 pv[kMergeTilesPerThread];
@@ -1024,10 +1102,11 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
                                                                const float* res, int rc, int rh, int rw, int h, int w,
                                                                int relu, float eps, float momentum, float* z,
                                                                float* save_mean, float* save_invstd, float* save_scale,
-                                                               float* run_mean, float* run_var, float* pool)
+                                                               float* run_mean, float* run_var, float* pool,
+                                                               float* pstat)
 {
     __shared__ double sh[2 * kBlock / 64];
-    __shared__ float coef[2];
+    __shared__ float coef[4];
     const int ch = blockIdx.x;
     const int hw4 = hw >> 2;
     const int units = n * hw4;
@@ -1084,9 +1163,32 @@ __global__ __launch_bounds__(kBlock) void bn_apply_partials_k(int n, int c, int 
             float ps = (v[0] + v[1]) + (v[2] + v[3]);
 #pragma unroll
             for (int off = 8; off > 0; off >>= 1) ps += __shfl_xor(ps, off, 16);
+            // and, for the backward, the plane's ReLU count and sum of xhat
+            // where the ReLU passes: the pool's gradient is uniform over the
+            // plane, so the BN backward's sums follow from these two numbers
+            float pc = 0.f, px = 0.f;
+            if (pstat) {
+                const float mu = coef[2], is = coef[3];
+                const float yy[4] = {yv[q].x, yv[q].y, yv[q].z, yv[q].w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    const bool pass = !relu || v[e] > 0.f;
+                    pc += pass ? 1.f : 0.f;
+                    px += pass ? (yy[e] - mu) * is : 0.f;
+                }
+#pragma unroll
+                for (int off = 8; off > 0; off >>= 1) {
+                    pc += __shfl_xor(pc, off, 16);
+                    px += __shfl_xor(px, off, 16);
+                }
+            }
             if (live && (threadIdx.x & 15) == 0) {
                 const int u = u0 + (int)threadIdx.x + q * kBlock;
                 pool[(size_t)(u / hw4) * c + ch] = ps / (float)hw;
+                if (pstat) {
+                    pstat[((size_t)(u / hw4) * c + ch) * 2 + 0] = pc;
+                    pstat[((size_t)(u / hw4) * c + ch) * 2 + 1] = px;
+                }
             }
         }
     }
@@ -1221,9 +1323,11 @@ int apply_units_per_thread(int64_t units_total)
 hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, const float* part, int T, int P,
                                   const float* gamma, const float* beta, const float* res, int rc, int rh, int rw,
                                   int relu, float eps, float momentum, float* z, float* save_mean, float* save_invstd,
-                                  float* save_scale, float* run_mean, float* run_var, hipStream_t st, float* pool)
+                                  float* save_scale, float* run_mean, float* run_var, hipStream_t st, float* pool,
+                                  float* pstat)
 {
     if (pool && h * w != 64) return hipErrorNotSupported;
+    if (pstat && (!pool || (uintptr_t)pstat % 8)) return hipErrorNotSupported;
     const bool identity = res && rc == c && rh == h && rw == w;
     if (w % 4 || !aligned16(y) || !aligned16(z) || (identity && !aligned16(res)) || (uintptr_t)part % 8)
         return hipErrorNotSupported;
@@ -1234,11 +1338,11 @@ hipError_t bn_apply_from_partials(int n, int c, int h, int w, const float* y, co
     const double total = (double)n * c * h * w;
     const double rbytes = res ? kF * (double)n * std::min(c, rc) * h * w : 0.0;
     Work wk{3.0 * total, 2 * kF * total + rbytes + 2 * kF * T * c};
-    if (pool) wk.bytes += kF * (double)n * c;  // the pooled means written
+    if (pool) wk.bytes += kF * (double)n * c * (pstat ? 3.0 : 1.0);  // the pooled means (and plane statistics) written
 #define PSW_BN_APPLY(UU)                                                                                          \
     PSW_LAUNCH(kname("bn_apply_partials_k", UU), wk, bn_apply_partials_k<UU>, dim3(c, per_ch), dim3(kBlock), 0, st, n, c, \
                h * w, y, part, T, P, gamma, beta, res, rc, rh, rw, h, w, relu, eps, momentum, z, save_mean,          \
-               save_invstd, save_scale, run_mean, run_var, pool)
+               save_invstd, save_scale, run_mean, run_var, pool, pstat)
     if (U == 4)
         PSW_BN_APPLY(4);
     else if (U == 2)
@@ -1310,6 +1414,34 @@ hipError_t bn_bwd_gavg(int n, int c, int h, int w, const float* dh, const float*
     const Work wk{8.0 * total, kF * ((4.0 + (dres ? 1.0 : 0.0)) * total + (double)n * c)};
     PSW_LAUNCH(kname("bn_bwd_gavg_k"), wk, bn_bwd_gavg_k, dim3(c), dim3(kBlock), 0, st, n, c, hw, dh, z, y, gamma, mean,
                invstd, relu, dz, dy, dgamma, dbeta, dres);
+    return hipGetLastError();
+}
+
+hipError_t bn_bwd_gavg_from_stats(int n, int c, int h, int w, const float* dh, const float* pstat, const float* z,
+                                  const float* y, const float* gamma, const float* mean, const float* invstd, int relu,
+                                  float* dz, float* dy, float* dgamma, float* dbeta, float* dres, hipStream_t st)
+{
+    const int hw = h * w;
+    if (hw % 4 || !aligned16(z) || !aligned16(y) || !aligned16(dz) || !aligned16(dy) || (dres && !aligned16(dres)) ||
+        (uintptr_t)pstat % 8)
+        return hipErrorNotSupported;
+    const int64_t units = (int64_t)n * hw / 4;
+    if (units > INT32_MAX) return hipErrorNotSupported;
+    const int U = apply_units_per_thread(units * c);
+    const unsigned per_ch = (unsigned)((units + U * kBlock - 1) / (U * kBlock));
+    const double total = (double)n * c * hw;
+    // y and z read, dz, dy (and the residual's gradient) written, the plane statistics and dh read
+    const Work wk{6.0 * total, kF * ((4.0 + (dres ? 1.0 : 0.0)) * total + 3.0 * n * c)};
+#define PSW_BN_GS(UU)                                                                                             \
+    PSW_LAUNCH(kname("bn_bwd_gavg_stats_k", UU), wk, bn_bwd_gavg_stats_k<UU>, dim3(c, per_ch), dim3(kBlock), 0, st, n, \
+               c, hw, dh, pstat, z, y, gamma, mean, invstd, relu, dz, dy, dgamma, dbeta, dres)
+    if (U == 4)
+        PSW_BN_GS(4);
+    else if (U == 2)
+        PSW_BN_GS(2);
+    else
+        PSW_BN_GS(1);
+#undef PSW_BN_GS
     return hipGetLastError();
 }
 

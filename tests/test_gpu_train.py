@@ -598,7 +598,9 @@ def test_bn_backward_folds_run(P):
     assert count(lambda n: n.startswith("conv3x3_direct") and n.endswith("true, 1, 1, false>")) == 7
     assert count(lambda n: n.startswith("conv3x3_direct") and n.endswith("true, 1, 2, false>")) == 6
     assert count(lambda n: n.startswith("bn_bwd_partials_k")) == 5
-    assert count(lambda n: n.startswith("bn_bwd_gavg_k")) == 1
+    # (from the per-plane statistics its forward apply stored: one elementwise pass)
+    assert count(lambda n: n.startswith("bn_bwd_gavg_stats_k")) == 1
+    assert count(lambda n: n.startswith("bn_bwd_gavg_k")) == 0
     assert count(lambda n: n.startswith(("gavg_bwd_k", "chan_partials", "bn_bwd_finalize", "bn_bwd_apply"))) == 0
     # forward: that BN's apply kernel also writes the pooled means
     assert count(lambda n: n.startswith("gavg_fwd_k")) == 0
