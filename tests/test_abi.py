@@ -335,3 +335,24 @@ def test_bn_applied_on_load_only_where_nothing_else_reads_it(psw):
     assert _unstored(psw, synth.resnet110_workload()) == [4 * b + 4 for b in range(54)]
     for wl in (synth.vgg16_workload(), synth.alexnet_workload(), synth.lenet5_workload()):
         assert _unstored(psw, wl) == []
+
+
+@pytest.mark.parametrize("change", ["consumer_bias", "no_relu", "consumer_5x5"])
+def test_bn_on_load_needs_a_plain_3x3_consumer_and_relu(psw, change):
+    """The first block's BN + ReLU (tensor 4) stays stored when its consumer
+    conv has a bias, when the BN has no ReLU, or when the consumer is not a
+    3x3 / pad 1 conv (5x5 / pad 2, same output shape); the other eight
+    blocks' BNs are still applied on load."""
+    import dataclasses
+
+    r20 = synth.resnet20_workload()
+    ops = r20.ops.copy()
+    assert ops[3][0] == synth.BN and ops[4][0] == synth.CONV and ops[4][1] == 4
+    if change == "consumer_bias":
+        ops[4][8] |= synth.F_BIAS
+    elif change == "no_relu":
+        ops[3][8] &= ~synth.F_RELU
+    else:
+        ops[4][5], ops[4][7] = 5, 2
+    got = _unstored(psw, dataclasses.replace(r20, ops=ops))
+    assert got == [4 * b + 4 for b in range(1, 9)]
