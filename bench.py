@@ -46,9 +46,9 @@ per launch / its mean launch time.  `conv_mfma.in_step` is the conv FLOPs
 per step over the whole step time instead (all kernels of the three
 streams sharing the chip).  `roofline.traffic` is the HBM bytes per launch
 from rocprofv3 FETCH_SIZE / WRITE_SIZE counters (calibrated on a plain
-streaming kernel) stored in profiles/traffic.json, used only when the
-source files defining that kernel still hash to what was profiled, else
-null.
+streaming kernel) stored in profiles/traffic.json under the workload's
+key (`traffic_key`), used only when the source files defining that kernel
+still hash to what was profiled, else null.
 `cpu_baseline` times the CPU oracle on a bounded sample: 2-step runs of the
 same workload, repeated until 10 s of host time have passed (about 12 steps
 on 16 host threads).
@@ -80,11 +80,18 @@ REPLAY_REPS = 20   # back-to-back launches per recorded launch
 COPY_BYTES = 256 << 20
 
 
-def measured_traffic(kernel):
-    """HBM bytes per launch of `kernel` from profiles/traffic.json, or None
-    when the file has no entry for it or the entry was taken on other sources
-    of that kernel (each entry records which source files define the kernel
-    and their hash)."""
+def traffic_key(wl):
+    """Section of profiles/traffic.json for a workload: one kernel moves other
+    bytes at another batch size (resnet20_b128, resnet20_bf16_b128,
+    resnet110_bf16_b256)."""
+    return f"{wl.name}_b{wl.batch}"
+
+
+def measured_traffic(kernel, key):
+    """HBM bytes per launch of `kernel` in workload section `key` of
+    profiles/traffic.json, or None when the file has no entry for it or the
+    entry was taken on other sources of that kernel (each entry records which
+    source files define the kernel and their hash)."""
     import hashlib
 
     path = os.path.join(ROOT, "profiles", "traffic.json")
@@ -93,7 +100,7 @@ def measured_traffic(kernel):
             t = json.load(f)
     except (OSError, ValueError):
         return None
-    t = t.get("kernels", {}).get(kernel)
+    t = t.get("workloads", {}).get(key, {}).get("kernels", {}).get(kernel)
     if not t or not t.get("sources"):
         return None
     h = hashlib.sha256()
@@ -361,7 +368,7 @@ def main():
                        "bytes_per_step": conv_bytes}
         d = kernels[0]  # the dominant kernel: largest summed time
         roof = roofline_of(d, peak)
-        roof["traffic"] = measured_traffic(d["name"])
+        roof["traffic"] = measured_traffic(d["name"], traffic_key(wl))
         roof.update({"kernel": d["name"], "launches": d["launches"],
                      "avg_launch_us": round(1e3 * d["ms"] / d["launches"], 3),
                      "flop_per_launch": d["flops"] / d["launches"], "bytes_per_launch": d["bytes"] / d["launches"],
@@ -375,7 +382,7 @@ def main():
         top.append({"kernel": k["name"], "kind": k["kind"], "launches_per_step": k["launches"] / KP,
                     "us_per_step": round(1e3 * k["ms"] / KP, 2), "avg_launch_us": round(1e3 * k["ms"] / k["launches"], 3),
                     "bound": r["bound"], "achieved": r["achieved"], "unit": r["unit"], "frac": r["frac"],
-                    "bytes_per_launch": k["bytes"] / k["launches"], "traffic": measured_traffic(k["name"])})
+                    "bytes_per_launch": k["bytes"] / k["launches"], "traffic": measured_traffic(k["name"], traffic_key(wl))})
 
     every = [{"kernel": k["name"], "kind": k["kind"], "launches_per_step": k["launches"] / KP,
               "avg_launch_us": round(1e3 * k["ms"] / k["launches"], 3), "flop_per_launch": k["flops"] / k["launches"],

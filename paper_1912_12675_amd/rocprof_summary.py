@@ -21,11 +21,13 @@
 
     python -m paper_1912_12675_amd.rocprof_summary traffic --kernel NAME [--kernel NAME ...] \
             --fetch PMC_CSV --write PMC_CSV --copy-fetch PMC_CSV --copy-write PMC_CSV \
-            --copy-kernel SUBSTRING --copy-bytes B [--out profiles/traffic.json [--merge]]
+            --copy-kernel SUBSTRING --copy-bytes B --workload KEY [--out profiles/traffic.json]
         HBM bytes per launch of each kernel NAME from two `--pmc FETCH_SIZE`
-        and `--pmc WRITE_SIZE` runs, each counter scaled by what it reads for
-        a plain streaming kernel that reads and writes B bytes; --merge adds
-        the kernels --out does not hold yet (another workload's run) to it
+        and `--pmc WRITE_SIZE` runs of one workload, each counter scaled by
+        what it reads for a plain streaming kernel that reads and writes B
+        bytes; --out keeps one section per workload KEY (bench.py's
+        `traffic_key`: the same kernel moves other bytes at another batch)
+        and replaces only this workload's
 
 Kernel names are compared in the short form the library's profiler reports
 (`conv3x3_direct<32, 1, 8, 16, 1, 4, 4, true>`): namespaces, a leading
@@ -187,10 +189,8 @@ def main(argv=None):
     for k in ("fetch", "write", "copy_fetch", "copy_write", "copy_kernel"):
         b.add_argument("--" + k.replace("_", "-"), required=True)
     b.add_argument("--copy-bytes", type=int, required=True)
+    b.add_argument("--workload", required=True, help="section key, as bench.py's traffic_key")
     b.add_argument("--out")
-    b.add_argument("--merge", action="store_true",
-                   help="add the kernels that --out does not hold yet to it (each added entry keeps the counter "
-                        "scales of its own run) instead of writing a new file")
     args = ap.parse_args(argv)
     if args.cmd == "stats":
         rows = kernel_stats(args.csv)
@@ -253,19 +253,12 @@ def main(argv=None):
     else:
         t = traffic(args.kernel, args.fetch, args.write, args.copy_fetch, args.copy_write, args.copy_kernel,
                     args.copy_bytes)
-        if args.merge:
-            if not args.out:
-                raise SystemExit("--merge needs --out")
+        base = {"workloads": {}}
+        if args.out and os.path.exists(args.out):
             with open(args.out) as f:
                 base = json.load(f)
-            for name, entry in t["kernels"].items():
-                if name in base["kernels"]:
-                    continue
-                entry.update(fetch_scale=t["fetch_scale"], write_scale=t["write_scale"],
-                             copy_fetch_kib=t["copy_fetch_kib"], copy_write_kib=t["copy_write_kib"])
-                base["kernels"][name] = entry
-            t = base
-        s = json.dumps(t, indent=1)
+        base.setdefault("workloads", {})[args.workload] = t
+        s = json.dumps(base, indent=1)
         if args.out:
             with open(args.out, "w") as f:
                 f.write(s + "\n")
